@@ -1,0 +1,167 @@
+/*
+ * CPU ORACLE for the numeric SpGEMM C = A*B on CSR inputs.
+ *
+ * Test infrastructure only: the test suite, the smoke check and the CPU
+ * baseline leg of the benchmark call this. The GPU library never links or
+ * calls it, and it shares no code with the GPU library.
+ *
+ * What it computes is the plain definition the paper starts from:
+ *   C[i,:] = sum_j A[i,j] * B[j,:]                (Section II-B, Eq. gustav)
+ * computed row by row as in Gustavson's method (Algorithm 1): every
+ * intermediate product A[i,j]*B[j,k] of row i is formed, the products are
+ * stably sorted by column, and each run of equal columns is reduced. The
+ * sorted, unique columns are the "SortAndWrite" output of Algorithm 1.
+ * The symbolic phase (Section II-B) is the run count per row; the numeric
+ * phase fills columns and values at the given row offsets.
+ *
+ * Choices where the paper is silent:
+ *   - a column appears in C[i,:] iff some product lands there, even if the
+ *     sum is exactly zero (structural entries are kept);
+ *   - each run is reduced with Neumaier's compensated summation, so the
+ *     oracle's own rounding error is far below the comparison tolerance;
+ *   - bound[e] = sum of |A[i,j]*B[j,k]| over the run, the scale of the
+ *     per-entry tolerance |c - c_ref| <= 1e-12 * bound.
+ *
+ * Rows are processed in parallel (OpenMP, dynamic schedule); each row is
+ * computed by one thread in a fixed order, so results do not depend on the
+ * thread count.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <omp.h>
+
+typedef struct {
+    int64_t n_rows, n_cols;
+    const int64_t *row_ptr;
+    const int32_t *col;
+    const double *val;
+} oracle_csr;
+
+/* Number of intermediate products of row i: sum over A[i,:] of nnz(B[j,:]). */
+static int64_t row_products(const oracle_csr *A, const oracle_csr *B, int64_t i) {
+    int64_t n = 0;
+    for (int64_t p = A->row_ptr[i]; p < A->row_ptr[i + 1]; ++p) {
+        int32_t j = A->col[p];
+        n += B->row_ptr[j + 1] - B->row_ptr[j];
+    }
+    return n;
+}
+
+void oracle_row_products(const oracle_csr *A, const oracle_csr *B, int64_t *ip) {
+#pragma omp parallel for schedule(dynamic, 1024)
+    for (int64_t i = 0; i < A->n_rows; ++i) ip[i] = row_products(A, B, i);
+}
+
+static int cmp_u64(const void *a, const void *b) {
+    uint64_t x = *(const uint64_t *)a, y = *(const uint64_t *)b;
+    return (x > y) - (x < y);
+}
+
+/* Forms the products of row i in (j, k) order and sorts them by column.
+ * keys[q] = column << 32 | q, where q is the product's position in (j,k)
+ * order, so the sort is stable; prod[q] is the product itself. Returns the
+ * product count, or -1 on allocation failure / more than 2^32 products. */
+static int64_t expand_sorted(const oracle_csr *A, const oracle_csr *B, int64_t i, uint64_t **keys_out,
+                             double **prod_out) {
+    int64_t n = row_products(A, B, i);
+    *keys_out = NULL;
+    *prod_out = NULL;
+    if (n >= ((int64_t)1 << 32)) return -1;
+    uint64_t *keys = (uint64_t *)malloc((size_t)(n > 0 ? n : 1) * sizeof(uint64_t));
+    double *prod = (double *)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
+    if (!keys || !prod) {
+        free(keys);
+        free(prod);
+        return -1;
+    }
+    int64_t q = 0;
+    for (int64_t p = A->row_ptr[i]; p < A->row_ptr[i + 1]; ++p) {
+        int32_t j = A->col[p];
+        double a = A->val[p];
+        for (int64_t r = B->row_ptr[j]; r < B->row_ptr[j + 1]; ++r) {
+            keys[q] = ((uint64_t)(uint32_t)B->col[r] << 32) | (uint64_t)q;
+            prod[q] = a * B->val[r];
+            ++q;
+        }
+    }
+    qsort(keys, (size_t)n, sizeof(uint64_t), cmp_u64);
+    *keys_out = keys;
+    *prod_out = prod;
+    return n;
+}
+
+/* Symbolic: number of distinct columns of C[rows[t], :] into counts[t].
+ * Returns 0, or -1 if some row could not be processed. */
+int oracle_count_rows(const oracle_csr *A, const oracle_csr *B, const int64_t *rows, int64_t n_list,
+                      int64_t *counts) {
+    int failed = 0;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t t = 0; t < n_list; ++t) {
+        uint64_t *keys;
+        double *prod;
+        int64_t n = expand_sorted(A, B, rows[t], &keys, &prod);
+        if (n < 0) {
+            failed = 1;
+            counts[t] = -1;
+            continue;
+        }
+        int64_t runs = 0;
+        for (int64_t q = 0; q < n; ++q)
+            if (q == 0 || (keys[q] >> 32) != (keys[q - 1] >> 32)) ++runs;
+        counts[t] = runs;
+        free(keys);
+        free(prod);
+    }
+    return failed ? -1 : 0;
+}
+
+/* Numeric: row rows[t] is written at positions offsets[t] .. of col/val/bound. */
+int oracle_fill_rows(const oracle_csr *A, const oracle_csr *B, const int64_t *rows, int64_t n_list,
+                     const int64_t *offsets, int32_t *col, double *val, double *bound) {
+    int failed = 0;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t t = 0; t < n_list; ++t) {
+        uint64_t *keys;
+        double *prod;
+        int64_t n = expand_sorted(A, B, rows[t], &keys, &prod);
+        if (n < 0) {
+            failed = 1;
+            continue;
+        }
+        int64_t out = offsets[t] - 1;
+        double s = 0.0, comp = 0.0, mag = 0.0;
+        for (int64_t q = 0; q < n; ++q) {
+            uint32_t c = (uint32_t)(keys[q] >> 32);
+            double x = prod[keys[q] & 0xFFFFFFFFULL];
+            if (q == 0 || c != (uint32_t)(keys[q - 1] >> 32)) {
+                if (q > 0) {
+                    val[out] = s + comp;
+                    bound[out] = mag;
+                }
+                ++out;
+                col[out] = (int32_t)c;
+                s = 0.0;
+                comp = 0.0;
+                mag = 0.0;
+            }
+            /* Neumaier: carry the low-order part lost by s + x. */
+            double t2 = s + x;
+            if (fabs(s) >= fabs(x))
+                comp += (s - t2) + x;
+            else
+                comp += (x - t2) + s;
+            s = t2;
+            mag += fabs(x);
+        }
+        if (n > 0) {
+            val[out] = s + comp;
+            bound[out] = mag;
+        }
+        free(keys);
+        free(prod);
+    }
+    return failed ? -1 : 0;
+}
+
+int oracle_threads(void) { return omp_get_max_threads(); }

@@ -1,0 +1,305 @@
+"""Pins of the CPU oracle against facts fixed by the paper or by mathematics.
+
+Each pin is independent of the oracle's own algorithm (gather, stable sort,
+compensated run reduction): dense products from numpy, closed forms counted
+by hand, exact integer arithmetic, identities, and brute force on tiny
+inputs. A plausible mistake in the oracle (a dropped product, a wrong index,
+a transposed operand, lost structural zeros, uncompensated sums) fails at
+least one of them.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+from oracle import reference
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def full(A, B):
+    return oracle.spgemm(A, B)
+
+
+def as_csr(r: oracle.OracleRows, n_cols):
+    return wl.CSR(len(r.rows), n_cols, r.row_ptr, r.col, r.val)
+
+
+def csr_transpose_dense_check(C, dense):
+    got = as_csr(C, dense.shape[1]).to_dense()
+    return got
+
+
+SHAPES = [(1, 1, 1), (5, 7, 3), (17, 40, 23), (64, 64, 64), (33, 9, 50), (0, 4, 4), (6, 0, 5)]
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+@pytest.mark.parametrize("density", [0.0, 0.05, 0.3, 0.8])
+def test_dense_bruteforce(shape, density):
+    m, k, n = shape
+    seed = hash((shape, density)) & 0xFFFF
+    A = wl.uniform(m, max(k, 1), density, seed) if k else wl.empty(m, 0)
+    B = wl.uniform(k, n, density, seed + 1) if k else wl.empty(0, n)
+    if k == 0:
+        A = wl.CSR(m, 0, np.zeros(m + 1, np.int64), np.zeros(0, np.int32), np.zeros(0))
+    C = full(A, B)
+    # structure: boolean product of the patterns
+    pa = A.pattern_dense().astype(np.int64) if k else np.zeros((m, 0), np.int64)
+    pb = B.pattern_dense().astype(np.int64)
+    pattern = (pa @ pb) > 0
+    got = as_csr(C, n)
+    assert np.array_equal(got.pattern_dense(), pattern)
+    # columns strictly increasing within each row
+    for t in range(m):
+        c = C.col[C.row_ptr[t]:C.row_ptr[t + 1]]
+        assert np.all(np.diff(c) > 0)
+    # values: dense fp64 product, within a tight multiple of the bound
+    dense = (A.to_dense() if k else np.zeros((m, 0))) @ B.to_dense()
+    rows = np.repeat(np.arange(m), np.diff(C.row_ptr))
+    ref = dense[rows, C.col]
+    assert np.all(np.abs(C.val - ref) <= 1e-14 * C.bound + 1e-300)
+    # bound = sum of |a*b| = |A| @ |B|
+    absd = (np.abs(A.to_dense()) if k else np.zeros((m, 0))) @ np.abs(B.to_dense())
+    assert np.allclose(C.bound, absd[rows, C.col], rtol=1e-14, atol=0)
+
+
+def test_identity_and_permutation_exact():
+    A = wl.rmat(9, 8, 0.57, 0.19, 0.19, 5)
+    n = A.n_rows
+    I = wl.identity(n)
+    for C in (full(I, A), full(A, I)):
+        assert np.array_equal(C.row_ptr, A.row_ptr)
+        assert np.array_equal(C.col, A.col)
+        assert np.array_equal(C.val, A.val)  # one product per entry: bit-exact
+    P = wl.permutation(n, 3)
+    perm = P.col.astype(np.int64)  # P[i, perm[i]] = 1
+    # (P A)[i, :] = A[perm[i], :]
+    PA = full(P, A)
+    for i in range(0, n, 7):
+        s, e = A.row_ptr[perm[i]], A.row_ptr[perm[i] + 1]
+        c, v, _ = PA.row(i)
+        assert np.array_equal(c, A.col[s:e]) and np.array_equal(v, A.val[s:e])
+    # (A P)[i, perm[j]] = A[i, j]
+    AP = full(A, P)
+    for i in range(0, n, 5):
+        s, e = A.row_ptr[i], A.row_ptr[i + 1]
+        cols = perm[A.col[s:e]]
+        order = np.argsort(cols)
+        c, v, _ = AP.row(i)
+        assert np.array_equal(c, cols[order]) and np.array_equal(v, A.val[s:e][order])
+
+
+def test_integer_values_exact():
+    # every partial sum of small integers is exact in fp64, in any order
+    A = wl.uniform(48, 60, 0.3, 11, values="int3")
+    B = wl.uniform(60, 52, 0.3, 12, values="int3")
+    C = full(A, B)
+    dense = A.to_dense().astype(np.int64) @ B.to_dense().astype(np.int64)
+    rows = np.repeat(np.arange(48), np.diff(C.row_ptr))
+    assert np.array_equal(C.val, dense[rows, C.col].astype(np.float64))
+    # integer-valued R-MAT: sampled rows against exact per-row integer sums
+    R = wl.rmat(10, 8, 0.57, 0.19, 0.19, 4, values="int3")
+    CR = oracle.spgemm(R, R, rows=np.arange(0, R.n_rows, 3))
+    for t, i in enumerate(CR.rows):
+        acc = {}
+        for p in range(R.row_ptr[i], R.row_ptr[i + 1]):
+            k = R.col[p]
+            for q in range(R.row_ptr[k], R.row_ptr[k + 1]):
+                acc[int(R.col[q])] = acc.get(int(R.col[q]), 0) + int(R.val[p]) * int(R.val[q])
+        c, v, _ = CR.row(t)
+        assert list(c) == sorted(acc)
+        assert np.array_equal(v, np.array([acc[j] for j in sorted(acc)], np.float64))
+
+
+def _golden_rows(name):
+    out = []
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                out.append([x.strip() for x in line.split("|")])
+    return out
+
+
+@pytest.mark.parametrize("n", [200, 4096])
+def test_banded_closed_forms(n):
+    row = [r for r in _golden_rows("banded_closed_forms.txt") if int(r[0]) == n][0]
+    A = wl.banded(n, 13, 1, values="ones")
+    assert A.nnz == int(row[1])
+    ip = oracle.row_products(A, A)
+    assert int(ip.sum()) == int(row[2])
+    C = full(A, A)
+    assert int(C.row_ptr[-1]) == int(row[3])
+    # value of every entry: number of k within 13 of both i and j (brute force)
+    rows = np.repeat(np.arange(n), np.diff(C.row_ptr))
+    ks = np.arange(n)
+    sample = np.arange(0, C.col.size, max(1, C.col.size // 3000))
+    for e in sample:
+        i, j = rows[e], C.col[e]
+        cnt = np.count_nonzero((np.abs(ks - i) <= 13) & (np.abs(ks - j) <= 13))
+        assert C.val[e] == cnt
+        if 26 <= i < n - 26:
+            assert C.val[e] == 27 - abs(int(i) - int(j))
+
+
+def test_banded_full_size_counts():
+    row = [r for r in _golden_rows("banded_closed_forms.txt") if int(r[0]) == 1 << 20][0]
+    A = wl.CONFIGS["banded20"].make()
+    assert A.nnz == int(row[1])
+    assert int(oracle.row_products(A, A).sum()) == int(row[2])
+
+
+def test_er_products_per_row():
+    A = wl.erdos_renyi(4096, 4096, 16, 9)
+    assert np.all(np.diff(A.row_ptr) == 16)
+    assert np.all(oracle.row_products(A, A) == 256)
+
+
+@pytest.mark.parametrize("seed", [1, 2])
+def test_product_count_invariant(seed):
+    A = wl.rmat(11, 8, 0.57, 0.19, 0.19, seed)
+    B = wl.rmat(11, 4, 0.57, 0.19, 0.19, seed + 10)
+    ip = oracle.row_products(A, B)
+    colcount = np.bincount(A.col, minlength=A.n_cols)
+    rowlen = np.diff(B.row_ptr)
+    assert int(ip.sum()) == int((colcount * rowlen).sum())
+    # symbolic counts never exceed the product counts, and equal the distinct count
+    C = full(A, B)
+    assert np.all(np.diff(C.row_ptr) <= ip)
+
+
+def test_compensated_reduction():
+    # products 1e16, 1, -1e16 on one column: plain left-to-right summation gives 0
+    A = wl.CSR(1, 3, np.array([0, 3], np.int64), np.array([0, 1, 2], np.int32), np.array([1e16, 1.0, -1e16]))
+    B = wl.CSR(3, 2, np.array([0, 1, 2, 3], np.int64), np.array([1, 1, 1], np.int32), np.ones(3))
+    C = full(A, B)
+    assert list(C.col) == [1]
+    assert C.val[0] == 1.0
+    assert C.bound[0] == 2e16 + 1.0
+
+
+def test_structural_zero_kept():
+    # products +2 and -2 cancel exactly; the entry stays with value 0
+    A = wl.CSR(1, 2, np.array([0, 2], np.int64), np.array([0, 1], np.int32), np.array([1.0, -1.0]))
+    B = wl.CSR(2, 3, np.array([0, 2, 3], np.int64), np.array([0, 2, 2], np.int32), np.array([5.0, 2.0, 2.0]))
+    C = full(A, B)
+    assert list(C.col) == [0, 2]
+    assert list(C.val) == [5.0, 0.0]
+
+
+def test_rows_subset_matches_full():
+    A = wl.rmat(10, 8, 0.57, 0.19, 0.19, 8)
+    F = full(A, A)
+    rows = np.array([0, 5, 1023, 17, 5])
+    S = oracle.spgemm(A, A, rows=rows)
+    for t, i in enumerate(rows):
+        c, v, b = S.row(t)
+        s, e = F.row_ptr[i], F.row_ptr[i + 1]
+        assert np.array_equal(c, F.col[s:e]) and np.array_equal(v, F.val[s:e])
+
+
+def test_rejects_mismatched_shapes():
+    A = wl.uniform(4, 5, 0.5, 1)
+    with pytest.raises(ValueError):
+        oracle.spgemm(A, A)
+
+
+def test_rmat_generator_against_paper_table():
+    # Table "Properties of the representative RMat matrices": scale 15,
+    # B density 8; C.nnz / C.n = 477.6 (A density 4) and 782.3 (A density 8).
+    B = wl.rmat(15, 8, 0.57, 0.19, 0.19, 101)
+    for dens, printed in ((4, 477.6), (8, 782.3)):
+        A = wl.rmat(15, dens, 0.57, 0.19, 0.19, 200 + dens)
+        C = full(A, B)
+        ratio = C.row_ptr[-1] / A.n_rows
+        assert abs(ratio - printed) <= 0.15 * printed, (dens, ratio, printed)
+
+
+def test_rmat12_workload_shape():
+    A = wl.CONFIGS["rmat12"].make()
+    assert A.n_rows == 4096 and 27000 < A.nnz < 30000
+    rl = np.diff(A.row_ptr)
+    for i in range(A.n_rows):
+        c = A.col[A.row_ptr[i]:A.row_ptr[i + 1]]
+        assert np.all(np.diff(c) > 0)
+    assert rl.sum() == A.nnz and np.all(A.val > 0)
+
+
+# ---------------------------------------------------------------- planner pins
+
+def _parse_table(s):
+    s = s.strip()
+    if s == "N/A":
+        return None
+    if ":" in s:
+        req, rest = s.split(":")
+        return int(req), [int(x) for x in rest.split(",")]
+    return int(s), [int(s)]
+
+
+def test_planner_reproduces_printed_chunk_counts():
+    from oracle.params import get_magnus_params
+
+    n_checked = 0
+    for name, cm, pvc, h200 in _golden_rows("num_chunks.txt"):
+        for s_lm, printed in ((131072, pvc), (233472, h200)):
+            exp = _parse_table(printed)
+            if exp is None:
+                continue
+            p = get_magnus_params(int(cm), s_lm)
+            assert (p.chunks_required, p.v_chunks) == exp, (name, s_lm, p)
+            assert p.table_string() == printed.strip()
+            n_checked += 1
+    assert n_checked == 51
+
+
+def test_planner_mi355x_values():
+    from oracle.params import get_magnus_params
+
+    p = get_magnus_params(1 << 22, 163840)
+    assert (p.tau, p.dense_width, p.chunks_max, p.group_rows) == (6826, 8192, 32, 2)
+    assert p.v_chunks == [32, 16]
+    assert get_magnus_params(1 << 23, 163840).v_chunks == [32, 32]
+    assert get_magnus_params(4096, 163840).v_chunks == []
+    # paper: n_groupRows = 2 in its experiments
+    assert get_magnus_params(1 << 20, 131072).group_rows == 2
+    assert get_magnus_params(1 << 20, 233472).group_rows == 2
+
+
+# ------------------------------------------------------ reorder-step references
+
+def test_reference_multisplit_figure1_example():
+    # Section III-A: two heavy rows, C.m = 8, two chunks, one level -> four
+    # C_reord rows; the upper chunks (1 and 3) move columns [4, 8) to [0, 4).
+    rows = [(np.array([0, 5, 3, 7, 5]), np.array([1.0, 2.0, 3.0, 4.0, 5.0])),
+            (np.array([6, 1, 4]), np.array([6.0, 7.0, 8.0]))]
+    chunks, order, nh = reference.multisplit(rows, 8, 2, tau=None)
+    assert nh == 0 and order == [(0, 0), (0, 1), (1, 0), (1, 1)]
+    assert list(chunks[(0, 0)][0]) == [0, 3]
+    assert list(chunks[(0, 1)][0]) == [1, 1, 3] and list(chunks[(0, 1)][1]) == [2.0, 5.0, 4.0]
+    assert list(chunks[(1, 0)][0]) == [1]
+    assert list(chunks[(1, 1)][0]) == [0, 2]
+    # conservation: every element lands in exactly one chunk
+    assert sum(c[0].size for c in chunks.values()) == 8
+    # heavy-first ordering with a threshold
+    chunks, order, nh = reference.multisplit(rows, 8, 2, tau=2)
+    assert nh == 1 and order[0] == (0, 1)
+
+
+def test_reference_expand_matches_oracle_sums():
+    A = wl.rmat(8, 8, 0.57, 0.19, 0.19, 3)
+    ip = oracle.row_products(A, A)
+    heavy, light = reference.split_rows(ip, 40)
+    assert heavy.size + light.size == A.n_rows and np.all(ip[heavy] > 40)
+    ex = reference.expand(A, A, heavy)
+    C = oracle.spgemm(A, A, rows=heavy)
+    for t, (cols, vals) in enumerate(ex):
+        assert cols.size == ip[heavy[t]]
+        c, v, b = C.row(t)
+        u, inv = np.unique(cols, return_inverse=True)
+        sums = np.zeros(u.size)
+        np.add.at(sums, inv, vals)
+        assert np.array_equal(u, c)
+        assert np.all(np.abs(sums - v) <= 1e-13 * b)
