@@ -1,0 +1,206 @@
+"""Benchmark: SpGEMM C = A*A on one MI355X through the C ABI.
+
+One step = the whole product for the workload: row-panel split by product
+counts, then per panel the setup (row products, light/heavy split), the
+symbolic phase (heavy expansion, hierarchical multisplit, final-chunk and
+light-row counts, C row pointers) and the numeric phase (C columns and
+values). Inputs are resident in HBM before timing starts; each panel of C is
+written to HBM (panels reuse one allocation when C does not fit at once).
+
+Prints one JSON line (see the repository's benchmark contract). The
+roofline object is for the kernel class with the largest device time,
+measured with HIP events on the streams the kernels run on; the oracle is
+timed on a bounded sample of rows for the CPU baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "SpGEMM GFLOP/s (2×intermediate products/s) + achieved HBM GB/s, C=A·A"
+WORKLOADS = {
+    "rmat12": "R-MAT scale 12 (4096x4096), edge factor 8, (a,b,c,d)=(0.57,0.19,0.19,0.05), fp64 U(0,1), C=A*A",
+    "banded20": "Banded 2^20 x 2^20, 27 nnz/row at offsets -13..+13, fp64 U(-1,1), C=A*A",
+    "er22": "Erdos-Renyi 2^22 x 2^22, 16 nnz/row uniform without replacement, fp64 U(-1,1), C=A*A",
+    "rmat22": "R-MAT scale 22 (2^22 x 2^22), edge factor 16, (a,b,c,d)=(0.57,0.19,0.19,0.05), fp64 U(0,1), C=A*A",
+    "rmat23": "R-MAT scale 23 (2^23 x 2^23), edge factor 8, (a,b,c,d)=(0.60,0.17,0.17,0.06), fp64 U(0,1), C=A*A",
+}
+HEAVY_KERNELS = ["expand", "histogram", "multisplit", "chunk_symbolic", "chunk_numeric"]
+
+
+def log(msg):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def run_step(g, dA, bounds, timing, acc, c_bufs):
+    """One full product; returns (products, nnz(C))."""
+    import torch
+
+    products = 0
+    nnz = 0
+    flags = g.FLAG_TIMING if timing else 0
+    for a, b in zip(bounds[:-1], bounds[1:]):
+        with g.Plan(dA, dA, row_begin=a, row_end=b, flags=flags) as p:
+            rp, n = p.symbolic()
+            if c_bufs[0] is None or c_bufs[0].numel() < n:
+                c_bufs[0] = c_bufs[1] = None
+                c_bufs[0] = torch.empty(max(n, 1), dtype=torch.int32, device="cuda")
+                c_bufs[1] = torch.empty(max(n, 1), dtype=torch.float64, device="cuda")
+            p.numeric(c_bufs[0], c_bufs[1])
+            info = p.info() if timing else None
+        nnz += n
+        if info is not None:
+            products += info.products_total
+            for i, k in enumerate(g.K_NAMES):
+                acc.setdefault(k, [0.0, 0, 0.0])
+                acc[k][0] += info.kernel_ms[i]
+                acc[k][1] += info.kernel_launches[i]
+                acc[k][2] += info.kernel_bytes[i]
+    return products, nnz
+
+
+def cpu_baseline(A, ip, budget_products, seed=0):
+    """Times the oracle on a random sample of rows (about budget_products products)."""
+    import numpy as np
+
+    import oracle
+
+    rng = np.random.default_rng(seed)
+    order = rng.permutation(A.n_rows)
+    csum = np.cumsum(ip[order])
+    k = int(np.searchsorted(csum, budget_products)) + 1
+    rows = np.sort(order[:k])
+    sample_products = int(ip[rows].sum())
+    t0 = time.perf_counter()
+    oracle.spgemm(A, A, rows=rows)
+    dt = time.perf_counter() - t0
+    return {
+        "value": 2.0 * sample_products / dt / 1e9,
+        "unit": "GFLOP/s",
+        "cores": oracle.threads(),
+        "kind": "oracle",
+        "sample": "%d rows drawn uniformly at random (seed %d), %d intermediate products, %.1f s" % (
+            rows.size, seed, sample_products, dt),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", default="rmat22", choices=sorted(WORKLOADS))
+    ap.add_argument("--panel-products", type=float, default=4e9,
+                    help="maximum intermediate products per row panel")
+    ap.add_argument("--cpu-products", type=float, default=3e8, help="oracle sample size for the CPU baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: this build measures the single-GPU hot path "
+              "(row panels are independent; a multi-GPU run would shard panels, which is not built)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import workloads
+    from paper_2607_22866_amd import gmagnus as g
+
+    g.load()
+    if not torch.cuda.is_available():
+        raise RuntimeError("no GPU visible")
+    torch.cuda.set_device(0)
+    cfg = workloads.CONFIGS[args.config]
+    t0 = time.perf_counter()
+    A = cfg.make()
+    log("generated %s: n=%d nnz=%d in %.1fs" % (args.config, A.n_rows, A.nnz, time.perf_counter() - t0))
+    dA = g.DeviceCSR.from_host(A)
+    torch.cuda.synchronize()
+
+    bounds = g.split_panels(dA, dA, int(args.panel_products))
+    log("%d row panels (max %.2g products each)" % (len(bounds) - 1, args.panel_products))
+    acc_warm = {}
+    c_bufs = [None, None]
+    for w in range(args.warmup):
+        t = time.perf_counter()
+        run_step(g, dA, bounds, False, acc_warm, c_bufs)
+        torch.cuda.synchronize()
+        log("warmup %d: %.3fs" % (w, time.perf_counter() - t))
+
+    acc = {}
+    products = nnz = 0
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for s in range(args.steps):
+        t = time.perf_counter()
+        bounds = g.split_panels(dA, dA, int(args.panel_products))
+        products, nnz = run_step(g, dA, bounds, True, acc, c_bufs)
+        torch.cuda.synchronize()
+        log("step %d: %.3fs" % (s, time.perf_counter() - t))
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    ms_per_step = 1000.0 * elapsed / args.steps
+    gflops = 2.0 * products / (elapsed / args.steps) / 1e9
+
+    kernels = {}
+    for k, (ms, launches, byts) in acc.items():
+        if launches == 0 and ms == 0:
+            continue
+        kernels[k] = {"ms_per_step": ms / args.steps, "launches_per_step": launches / args.steps,
+                      "gb_per_step": byts / args.steps / 1e9,
+                      "achieved_gbs": (byts / (ms / 1000.0) / 1e9) if ms > 0 else None}
+    compute = {k: v for k, v in kernels.items() if k in HEAVY_KERNELS + ["light_symbolic", "light_numeric"]}
+    dom = max(compute, key=lambda k: compute[k]["ms_per_step"]) if compute else None
+    roofline = None
+    if dom:
+        d = kernels[dom]
+        roofline = {"bound": "hbm", "kernel": dom, "achieved": d["achieved_gbs"], "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": d["achieved_gbs"] / HBM_PEAK_GBS,
+                    "bytes_per_launch": d["gb_per_step"] * 1e9 / max(d["launches_per_step"], 1),
+                    "avg_launch_ms": d["ms_per_step"] / max(d["launches_per_step"], 1), "traffic": None}
+    heavy_ms = sum(kernels[k]["ms_per_step"] for k in HEAVY_KERNELS if k in kernels)
+    heavy_gb = sum(kernels[k]["gb_per_step"] for k in HEAVY_KERNELS if k in kernels)
+    all_ms = sum(v["ms_per_step"] for v in kernels.values())
+    all_gb = sum(v["gb_per_step"] for v in kernels.values())
+
+    out = {
+        "metric": METRIC,
+        "value": gflops,
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": WORKLOADS[args.config], "name": args.config, "seed": cfg.seed, "n": A.n_rows,
+                   "nnz_a": A.nnz, "products": products, "nnz_c": nnz, "panels": len(bounds) - 1,
+                   "panel_products": args.panel_products},
+        "achieved_hbm_gbs": {"heavy_path_kernels": heavy_gb / (heavy_ms / 1000.0) if heavy_ms else None,
+                             "heavy_path_frac": (heavy_gb / (heavy_ms / 1000.0)) / HBM_PEAK_GBS if heavy_ms else None,
+                             "all_kernels": all_gb / (all_ms / 1000.0) if all_ms else None,
+                             "end_to_end": all_gb / (elapsed / args.steps)},
+        "roofline": roofline,
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        ip = g.row_products(dA, dA).cpu().numpy()
+        log("timing the oracle on a sample of about %.2g products" % args.cpu_products)
+        out["cpu_baseline"] = cpu_baseline(A, ip, args.cpu_products)
+        del np
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

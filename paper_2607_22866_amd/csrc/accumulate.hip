@@ -1,0 +1,594 @@
+// Accumulation (Section III-E): symbolic (distinct-column counts) and
+// numeric (sorted rows of C) for
+//   * light rows of C -- Gustavson (Section II-B, Algorithm 1) with an LDS
+//     hash map (modulo hashing, linear probing, load factor <= 1/2) or, when
+//     the row's column span is small, an LDS dense window;
+//   * final chunks of the heavy rows ("leaves" of the multisplit) -- the
+//     chunk's (column, value) pairs are accumulated with the hash map when the
+//     chunk is light and with an LDS dense accumulator plus bitmap when it is
+//     heavy (its column range is at most W wide, Section III-D).
+// Hash output is sorted with an LDS bitonic sort; dense output comes out in
+// column order from a wave64 ballot over the bitmap. Columns of chunks are
+// shifted back by the chunk's column base on the final write.
+//
+// Work is binned by size (OpSparse-style, Section III-E): one work group per
+// row or chunk, with the work-group size and LDS table chosen per bin.
+#include "host.hpp"
+
+namespace gm {
+
+namespace {
+
+// --------------------------------------------------------------- sources
+template <int BLOCK>
+struct GusLds {
+    int32_t off[BLOCK + 1];
+    int64_t bst[BLOCK];
+    double av[BLOCK];
+    int32_t scan[BLOCK / GM_WAVE];
+};
+
+// Calls f(col, product) for every intermediate product of the A entries
+// [j0, j1) (one row of A), A entries taken in batches of BLOCK.
+template <int BLOCK, bool NUM, class F>
+GM_DEV void gustavson_row(const Csr &A, const Csr &B, int64_t j0, int64_t j1, GusLds<BLOCK> &L, F &&f) {
+    const int tid = threadIdx.x;
+    for (int64_t jb = j0; jb < j1; jb += BLOCK) {
+        const int nb = (int)(j1 - jb < BLOCK ? j1 - jb : BLOCK);
+        int32_t len = 0;
+        if (tid < nb) {
+            const int32_t k = A.ci[jb + tid];
+            const int64_t bs = B.rp[k];
+            len = (int32_t)(B.rp[k + 1] - bs);
+            L.bst[tid] = bs;
+            if (NUM) L.av[tid] = A.v[jb + tid];
+        }
+        int32_t tot;
+        const int32_t ex = block_excl_scan<BLOCK>(len, L.scan, &tot);
+        if (tid < nb) L.off[tid] = ex;
+        __syncthreads();
+        for (int32_t t = tid; t < tot; t += BLOCK) {
+            const int q = (int)find_row(L.off, 0, nb, t);
+            const int64_t src = L.bst[q] + (t - L.off[q]);
+            const int32_t c = B.ci[src];
+            if (NUM)
+                f(c, L.av[q] * B.v[src]);
+            else
+                f(c, 0.0);
+        }
+        __syncthreads();
+    }
+}
+
+// ------------------------------------------------------------ hash map
+// Probing stops after TS slots, so a table that were ever full could not
+// hang the work group (the count check of the numeric phase reports it).
+template <int TS>
+GM_DEV void hash_insert_key(int32_t *keys, int32_t c, int32_t *counter) {
+    uint32_t h = (uint32_t)c & (TS - 1);
+    for (int probe = 0; probe < TS; ++probe) {
+        int32_t old = ((volatile int32_t *)keys)[h];
+        if (old == -1) {
+            old = atomicCAS(&keys[h], -1, c);
+            if (old == -1) {
+                atomicAdd(counter, 1);
+                return;
+            }
+        }
+        if (old == c) return;
+        h = (h + 1) & (TS - 1);
+    }
+}
+
+template <int TS>
+GM_DEV void hash_insert_add(int32_t *keys, double *vals, int32_t c, double v) {
+    uint32_t h = (uint32_t)c & (TS - 1);
+    for (int probe = 0; probe < TS; ++probe) {
+        int32_t old = ((volatile int32_t *)keys)[h];
+        if (old == -1) {
+            old = atomicCAS(&keys[h], -1, c);
+            if (old == -1) old = c;
+        }
+        if (old == c) {
+            __hip_atomic_fetch_add(&vals[h], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            return;
+        }
+        h = (h + 1) & (TS - 1);
+    }
+}
+
+template <int BLOCK, int TS>
+GM_DEV void hash_clear(int32_t *keys, double *vals) {
+    for (int i = threadIdx.x; i < TS; i += BLOCK) {
+        keys[i] = -1;
+        if (vals) vals[i] = 0.0;
+    }
+}
+
+// Compacts the occupied slots to the front, sorts them by column (bitonic)
+// and writes at most `nnz` entries (the symbolic count) with the column base
+// added. Returns nothing; a count mismatch is flagged in *err.
+template <int BLOCK, int TS>
+GM_DEV void hash_emit_sorted(int32_t *keys, double *vals, int64_t nnz, int32_t col_base, int32_t *out_col,
+                             double *out_val, int32_t *scan_sm, int32_t *err) {
+    constexpr int PER = TS / BLOCK;
+    static_assert(PER * BLOCK == TS, "table size must be a multiple of the block");
+    const int tid = threadIdx.x;
+    int32_t k[PER];
+    double v[PER];
+    int cnt = 0;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+        k[q] = keys[tid * PER + q];
+        v[q] = vals[tid * PER + q];
+        cnt += k[q] != -1;
+    }
+    int32_t total;
+    int pos = block_excl_scan<BLOCK>(cnt, scan_sm, &total);
+#pragma unroll
+    for (int q = 0; q < PER; ++q)
+        if (k[q] != -1) {
+            keys[pos] = k[q];
+            vals[pos] = v[q];
+            ++pos;
+        }
+    int P = 1;
+    while (P < total) P <<= 1;
+    for (int i = total + tid; i < P; i += BLOCK) keys[i] = INT32_MAX;
+    __syncthreads();
+    for (int kk = 2; kk <= P; kk <<= 1)
+        for (int j = kk >> 1; j > 0; j >>= 1) {
+            for (int i = tid; i < P; i += BLOCK) {
+                const int ixj = i ^ j;
+                if (ixj > i) {
+                    const int32_t a = keys[i], b = keys[ixj];
+                    const bool up = (i & kk) == 0;
+                    if ((a > b) == up) {
+                        keys[i] = b;
+                        keys[ixj] = a;
+                        const double t = vals[i];
+                        vals[i] = vals[ixj];
+                        vals[ixj] = t;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+    if (tid == 0 && total != nnz) atomicOr(err, 1);
+    const int n_out = (int64_t)total < nnz ? total : (int)nnz;
+    for (int i = tid; i < n_out; i += BLOCK) {
+        out_col[i] = keys[i] + col_base;
+        out_val[i] = vals[i];
+    }
+}
+
+// ------------------------------------------------------ dense accumulator
+template <int BLOCK, int WMAX>
+struct DenseLds {
+    double vals[WMAX];
+    uint32_t bits[(WMAX + 31) / 32];
+    int32_t scan[BLOCK / GM_WAVE];
+};
+
+template <int BLOCK, int WMAX>
+GM_DEV void dense_clear(DenseLds<BLOCK, WMAX> &L, int width, bool num) {
+    for (int i = threadIdx.x; i < (width + 31) / 32; i += BLOCK) L.bits[i] = 0;
+    if (num)
+        for (int i = threadIdx.x; i < width; i += BLOCK) L.vals[i] = 0.0;
+}
+
+template <int BLOCK, int WMAX>
+GM_DEV void dense_set(DenseLds<BLOCK, WMAX> &L, int c) {
+    const uint32_t bit = 1u << (c & 31);
+    if (!(((volatile uint32_t *)L.bits)[c >> 5] & bit)) atomicOr(&L.bits[c >> 5], bit);
+}
+
+template <int BLOCK, int WMAX>
+GM_DEV void dense_add(DenseLds<BLOCK, WMAX> &L, int c, double v) {
+    dense_set(L, c);
+    __hip_atomic_fetch_add(&L.vals[c], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+template <int BLOCK, int WMAX>
+GM_DEV int32_t dense_count(DenseLds<BLOCK, WMAX> &L, int width) {
+    int32_t c = 0;
+    for (int i = threadIdx.x; i < (width + 31) / 32; i += BLOCK) c += __popc(L.bits[i]);
+    return block_reduce_sum<BLOCK>(c, L.scan);
+}
+
+// Writes the present columns in increasing order: wave w owns a contiguous
+// range of columns and walks it 64 columns at a time, one per lane.
+template <int BLOCK, int WMAX>
+GM_DEV void dense_emit(DenseLds<BLOCK, WMAX> &L, int width, int64_t nnz, int32_t col_base, int32_t *out_col,
+                       double *out_val, int32_t *err) {
+    constexpr int NW = BLOCK / GM_WAVE;
+    const int lane = threadIdx.x & (GM_WAVE - 1), w = threadIdx.x / GM_WAVE;
+    const int span = ((width + NW - 1) / NW + GM_WAVE - 1) / GM_WAVE * GM_WAVE;
+    const int c0 = w * span, c1 = c0 + span < width ? c0 + span : width;
+    int32_t cnt = 0;
+    for (int c = c0 + lane; c < c1; c += GM_WAVE) cnt += (L.bits[c >> 5] >> (c & 31)) & 1;
+    cnt = wave_reduce_sum(cnt);
+    int32_t total;
+    int32_t base = block_excl_scan<BLOCK>(lane == 0 ? cnt : 0, L.scan, &total);
+    base = __shfl(base, 0, GM_WAVE);
+    if (threadIdx.x == 0 && total != nnz) atomicOr(err, 2);
+    for (int g = c0; g < c1; g += GM_WAVE) {
+        const int c = g + lane;
+        const bool p = c < c1 && ((L.bits[c >> 5] >> (c & 31)) & 1);
+        const uint64_t m = ballot(p);
+        const int pos = base + __popcll(m & lanemask_lt());
+        if (p && pos < nnz) {
+            out_col[pos] = c + col_base;
+            out_val[pos] = L.vals[c];
+        }
+        base += __popcll(m);
+    }
+}
+
+// ----------------------------------------------------------- bin tables
+// Hash bins: (max elements or nnz, table slots, block).
+constexpr int HS_CAP[4] = {128, 512, 2048, 8192};   // symbolic: elements (load <= 1/2)
+constexpr int HN_CAP[4] = {128, 512, 2048, 7168};   // numeric: distinct columns
+constexpr int WIN0 = 64, WIN1 = 2048;
+
+GM_DEV int hash_bin_sym(int64_t n) {
+    return n <= HS_CAP[0] ? 0 : n <= HS_CAP[1] ? 1 : n <= HS_CAP[2] ? 2 : 3;
+}
+GM_DEV int hash_bin_num(int64_t nnz) {
+    return nnz <= HN_CAP[0] ? 0 : nnz <= HN_CAP[1] ? 1 : nnz <= HN_CAP[2] ? 2 : 3;
+}
+
+// Window choice for a light row: span = max column - min column + 1.
+GM_DEV int window_bin(int64_t ip, int64_t span, bool window) {
+    if (!window || span <= 0) return -1;
+    if (span <= WIN0) return 0;
+    int64_t p2 = 1;
+    while (p2 < ip) p2 <<= 1;
+    if (span <= WIN1 && span <= 4 * p2) return 1;
+    return -1;
+}
+
+__global__ void k_light_classes(const int64_t *ip, const int64_t *row_nnz, const int32_t *minc, const int32_t *maxc,
+                                int64_t n, int64_t tau, int window, uint8_t *cls) {
+    for (int64_t r = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; r < n; r += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t p = ip[r];
+        uint8_t c;
+        if (p == 0)
+            c = LIGHT_EMPTY;
+        else if (p > tau)
+            c = LIGHT_HEAVY;
+        else {
+            const int wb = window_bin(p, (int64_t)maxc[r] - minc[r] + 1, window != 0);
+            if (wb >= 0)
+                c = (uint8_t)(LIGHT_W0 + wb);
+            else
+                c = (uint8_t)(LIGHT_H0 + (row_nnz ? hash_bin_num(row_nnz[r]) : hash_bin_sym(p)));
+        }
+        cls[r] = c;
+    }
+}
+
+__global__ void k_leaf_classes(LeafSet L, const int64_t *leaf_nnz, int64_t tau, uint8_t *cls) {
+    const int64_t n = L.hi - L.lo;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t j = L.lo + i;
+        const int64_t len = L.ptr[j + 1] - L.ptr[j];
+        uint8_t c;
+        if (len == 0)
+            c = LEAF_EMPTY;
+        else if (len > tau)
+            c = LEAF_DENSE;
+        else
+            c = (uint8_t)(LEAF_H0 + (leaf_nnz ? hash_bin_num(leaf_nnz[i]) : hash_bin_sym(len)));
+        cls[i] = c;
+    }
+}
+
+// ------------------------------------------------------------- light rows
+template <int BLOCK, int TS>
+__global__ __launch_bounds__(BLOCK) void k_light_hash_sym(Csr A, Csr B, int64_t r0, const int64_t *items,
+                                                          int64_t *row_nnz) {
+    __shared__ int32_t keys[TS];
+    __shared__ GusLds<BLOCK> G;
+    __shared__ int32_t counter;
+    const int64_t r = items[blockIdx.x];
+    hash_clear<BLOCK, TS>(keys, nullptr);
+    if (threadIdx.x == 0) counter = 0;
+    __syncthreads();
+    gustavson_row<BLOCK, false>(A, B, A.rp[r0 + r], A.rp[r0 + r + 1], G,
+                                [&](int32_t c, double) { hash_insert_key<TS>(keys, c, &counter); });
+    if (threadIdx.x == 0) row_nnz[r] = counter;
+}
+
+template <int BLOCK, int TS>
+__global__ __launch_bounds__(BLOCK) void k_light_hash_num(Csr A, Csr B, int64_t r0, const int64_t *items,
+                                                          const int64_t *c_row_ptr, int32_t *c_col, double *c_val,
+                                                          int32_t *err) {
+    __shared__ int32_t keys[TS];
+    __shared__ double vals[TS];
+    __shared__ GusLds<BLOCK> G;
+    const int64_t r = items[blockIdx.x];
+    hash_clear<BLOCK, TS>(keys, vals);
+    __syncthreads();
+    gustavson_row<BLOCK, true>(A, B, A.rp[r0 + r], A.rp[r0 + r + 1], G,
+                               [&](int32_t c, double v) { hash_insert_add<TS>(keys, vals, c, v); });
+    const int64_t dst = c_row_ptr[r];
+    hash_emit_sorted<BLOCK, TS>(keys, vals, c_row_ptr[r + 1] - dst, 0, c_col + dst, c_val + dst, G.scan, err);
+}
+
+template <int BLOCK, int WMAX>
+__global__ __launch_bounds__(BLOCK) void k_light_win_sym(Csr A, Csr B, int64_t r0, const int64_t *items,
+                                                         const int32_t *minc, const int32_t *maxc,
+                                                         int64_t *row_nnz) {
+    __shared__ DenseLds<BLOCK, WMAX> D;
+    __shared__ GusLds<BLOCK> G;
+    const int64_t r = items[blockIdx.x];
+    const int32_t base = minc[r];
+    const int width = maxc[r] - base + 1;
+    dense_clear(D, width, false);
+    __syncthreads();
+    gustavson_row<BLOCK, false>(A, B, A.rp[r0 + r], A.rp[r0 + r + 1], G,
+                                [&](int32_t c, double) { dense_set(D, c - base); });
+    const int32_t cnt = dense_count(D, width);
+    if (threadIdx.x == 0) row_nnz[r] = cnt;
+}
+
+template <int BLOCK, int WMAX>
+__global__ __launch_bounds__(BLOCK) void k_light_win_num(Csr A, Csr B, int64_t r0, const int64_t *items,
+                                                         const int32_t *minc, const int32_t *maxc,
+                                                         const int64_t *c_row_ptr, int32_t *c_col, double *c_val,
+                                                         int32_t *err) {
+    __shared__ DenseLds<BLOCK, WMAX> D;
+    __shared__ GusLds<BLOCK> G;
+    const int64_t r = items[blockIdx.x];
+    const int32_t base = minc[r];
+    const int width = maxc[r] - base + 1;
+    dense_clear(D, width, true);
+    __syncthreads();
+    gustavson_row<BLOCK, true>(A, B, A.rp[r0 + r], A.rp[r0 + r + 1], G,
+                               [&](int32_t c, double v) { dense_add(D, c - base, v); });
+    const int64_t dst = c_row_ptr[r];
+    dense_emit(D, width, c_row_ptr[r + 1] - dst, base, c_col + dst, c_val + dst, err);
+}
+
+// ------------------------------------------------------------------ leaves
+template <int BLOCK, int TS>
+__global__ __launch_bounds__(BLOCK) void k_leaf_hash_sym(LeafSet L, const int64_t *items, int64_t *leaf_nnz,
+                                                         int64_t *slot_cnt) {
+    __shared__ int32_t keys[TS];
+    __shared__ int32_t counter;
+    const int64_t i = items[blockIdx.x];
+    const int64_t j = L.lo + i;
+    const int64_t s = L.ptr[j], e = L.ptr[j + 1];
+    hash_clear<BLOCK, TS>(keys, nullptr);
+    if (threadIdx.x == 0) counter = 0;
+    __syncthreads();
+    for (int64_t t = s + threadIdx.x; t < e; t += BLOCK) hash_insert_key<TS>(keys, L.col[t], &counter);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        leaf_nnz[i] = counter;
+        slot_cnt[L.origin[j]] = counter;
+    }
+}
+
+struct LeafOut {
+    int64_t n_slots_log2;
+    const int64_t *heavy_rows;
+    const int64_t *c_row_ptr;
+    const int64_t *slot_off;
+    int64_t slot_width_log2;
+    int32_t *c_col;
+    double *c_val;
+    int32_t *err;
+};
+
+GM_DEV void leaf_target(const LeafOut &o, int64_t origin, int64_t &dst, int64_t &nnz_cap, int32_t &col_base) {
+    const int64_t h = origin >> o.n_slots_log2;
+    const int64_t slot = origin & ((int64_t(1) << o.n_slots_log2) - 1);
+    const int64_t row = o.heavy_rows[h];
+    dst = o.c_row_ptr[row] + o.slot_off[origin];
+    nnz_cap = o.c_row_ptr[row + 1] - dst;
+    col_base = (int32_t)(slot << o.slot_width_log2);
+}
+
+template <int BLOCK, int TS>
+__global__ __launch_bounds__(BLOCK) void k_leaf_hash_num(LeafSet L, const int64_t *items, const int64_t *leaf_nnz,
+                                                         LeafOut o) {
+    __shared__ int32_t keys[TS];
+    __shared__ double vals[TS];
+    __shared__ int32_t scan_sm[BLOCK / GM_WAVE];
+    const int64_t i = items[blockIdx.x];
+    const int64_t j = L.lo + i;
+    const int64_t s = L.ptr[j], e = L.ptr[j + 1];
+    hash_clear<BLOCK, TS>(keys, vals);
+    __syncthreads();
+    for (int64_t t = s + threadIdx.x; t < e; t += BLOCK) hash_insert_add<TS>(keys, vals, L.col[t], L.val[t]);
+    __syncthreads();
+    int64_t dst, cap;
+    int32_t base;
+    leaf_target(o, L.origin[j], dst, cap, base);
+    const int64_t nnz = leaf_nnz[i] < cap ? leaf_nnz[i] : cap;
+    hash_emit_sorted<BLOCK, TS>(keys, vals, nnz, base, o.c_col + dst, o.c_val + dst, scan_sm, o.err);
+}
+
+constexpr int DENSE_MAX = 8192;
+
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void k_leaf_dense_sym(LeafSet L, const int64_t *items, int width,
+                                                          int64_t *leaf_nnz, int64_t *slot_cnt) {
+    __shared__ DenseLds<BLOCK, DENSE_MAX> D;
+    const int64_t i = items[blockIdx.x];
+    const int64_t j = L.lo + i;
+    const int64_t s = L.ptr[j], e = L.ptr[j + 1];
+    dense_clear(D, width, false);
+    __syncthreads();
+    for (int64_t t = s + threadIdx.x; t < e; t += BLOCK) dense_set(D, L.col[t]);
+    __syncthreads();
+    const int32_t cnt = dense_count(D, width);
+    if (threadIdx.x == 0) {
+        leaf_nnz[i] = cnt;
+        slot_cnt[L.origin[j]] = cnt;
+    }
+}
+
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void k_leaf_dense_num(LeafSet L, const int64_t *items, const int64_t *leaf_nnz,
+                                                          int width, LeafOut o) {
+    __shared__ DenseLds<BLOCK, DENSE_MAX> D;
+    const int64_t i = items[blockIdx.x];
+    const int64_t j = L.lo + i;
+    const int64_t s = L.ptr[j], e = L.ptr[j + 1];
+    dense_clear(D, width, true);
+    __syncthreads();
+    for (int64_t t = s + threadIdx.x; t < e; t += BLOCK) dense_add(D, L.col[t], L.val[t]);
+    __syncthreads();
+    int64_t dst, cap;
+    int32_t base;
+    leaf_target(o, L.origin[j], dst, cap, base);
+    const int64_t nnz = leaf_nnz[i] < cap ? leaf_nnz[i] : cap;
+    dense_emit(D, width, nnz, base, o.c_col + dst, o.c_val + dst, o.err);
+}
+
+// -------------------------------------------------------------- slot scan
+constexpr int SLOT_BLOCK = 256;
+
+__global__ __launch_bounds__(SLOT_BLOCK) void k_slot_scan(int64_t *slot, int64_t n_slots, const int64_t *heavy_rows,
+                                                          int64_t *row_nnz) {
+    __shared__ int64_t sm[SLOT_BLOCK / GM_WAVE];
+    int64_t *p = slot + blockIdx.x * n_slots;
+    int64_t carry = 0;
+    for (int64_t b = 0; b < n_slots; b += SLOT_BLOCK) {
+        const int64_t i = b + threadIdx.x;
+        const int64_t x = i < n_slots ? p[i] : 0;
+        int64_t tot;
+        const int64_t ex = block_excl_scan<SLOT_BLOCK>(x, sm, &tot);
+        if (i < n_slots) p[i] = carry + ex;
+        carry += tot;
+    }
+    if (threadIdx.x == 0) row_nnz[heavy_rows[blockIdx.x]] = carry;
+}
+
+template <class K, class... Args>
+void launch_items(K kernel, int block, int64_t n, hipStream_t s, Args... args) {
+    if (n <= 0) return;
+    GM_REQUIRE(n < (int64_t)1 << 31, GMAGNUS_ERROR_UNSUPPORTED, "too many work items for one launch");
+    hipLaunchKernelGGL(kernel, dim3((unsigned)n), dim3(block), 0, s, args...);
+    GM_CHECK_LAUNCH();
+}
+
+}  // namespace
+
+void light_classes_sym(const int64_t *ip, const int32_t *minc, const int32_t *maxc, int64_t n, int64_t tau,
+                       bool window, uint8_t *cls, hipStream_t s) {
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_light_classes, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, ip, nullptr, minc, maxc, n,
+                       tau, (int)window, cls);
+    GM_CHECK_LAUNCH();
+}
+
+void light_classes_num(const int64_t *ip, const int64_t *row_nnz, const int32_t *minc, const int32_t *maxc,
+                       int64_t n, int64_t tau, bool window, uint8_t *cls, hipStream_t s) {
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_light_classes, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, ip, row_nnz, minc, maxc, n,
+                       tau, (int)window, cls);
+    GM_CHECK_LAUNCH();
+}
+
+void leaf_classes_sym(const LeafSet &L, int64_t tau, uint8_t *cls, hipStream_t s) {
+    const int64_t n = L.hi - L.lo;
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_leaf_classes, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, L, nullptr, tau, cls);
+    GM_CHECK_LAUNCH();
+}
+
+void leaf_classes_num(const LeafSet &L, const int64_t *leaf_nnz, int64_t tau, uint8_t *cls, hipStream_t s) {
+    const int64_t n = L.hi - L.lo;
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_leaf_classes, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, L, leaf_nnz, tau, cls);
+    GM_CHECK_LAUNCH();
+}
+
+void light_symbolic(const Csr &A, const Csr &B, int64_t r0, int bin, const int64_t *items, int64_t n,
+                    const int32_t *minc, const int32_t *maxc, int64_t *row_nnz, hipStream_t s) {
+    switch (bin) {
+    case LIGHT_W0: launch_items(k_light_win_sym<64, WIN0>, 64, n, s, A, B, r0, items, minc, maxc, row_nnz); break;
+    case LIGHT_W1: launch_items(k_light_win_sym<256, WIN1>, 256, n, s, A, B, r0, items, minc, maxc, row_nnz); break;
+    case LIGHT_H0: launch_items(k_light_hash_sym<64, 2 * HS_CAP[0]>, 64, n, s, A, B, r0, items, row_nnz); break;
+    case LIGHT_H1: launch_items(k_light_hash_sym<64, 2 * HS_CAP[1]>, 64, n, s, A, B, r0, items, row_nnz); break;
+    case LIGHT_H2: launch_items(k_light_hash_sym<256, 2 * HS_CAP[2]>, 256, n, s, A, B, r0, items, row_nnz); break;
+    case LIGHT_H3: launch_items(k_light_hash_sym<512, 2 * HS_CAP[3]>, 512, n, s, A, B, r0, items, row_nnz); break;
+    default: break;
+    }
+}
+
+void light_numeric(const Csr &A, const Csr &B, int64_t r0, int bin, const int64_t *items, int64_t n,
+                   const int32_t *minc, const int32_t *maxc, const int64_t *c_row_ptr, int32_t *c_col, double *c_val,
+                   int32_t *err, hipStream_t s) {
+    switch (bin) {
+    case LIGHT_W0:
+        launch_items(k_light_win_num<64, WIN0>, 64, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col, c_val, err);
+        break;
+    case LIGHT_W1:
+        launch_items(k_light_win_num<256, WIN1>, 256, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col, c_val,
+                     err);
+        break;
+    case LIGHT_H0:
+        launch_items(k_light_hash_num<64, 256>, 64, n, s, A, B, r0, items, c_row_ptr, c_col, c_val, err);
+        break;
+    case LIGHT_H1:
+        launch_items(k_light_hash_num<64, 1024>, 64, n, s, A, B, r0, items, c_row_ptr, c_col, c_val, err);
+        break;
+    case LIGHT_H2:
+        launch_items(k_light_hash_num<256, 4096>, 256, n, s, A, B, r0, items, c_row_ptr, c_col, c_val, err);
+        break;
+    case LIGHT_H3:
+        launch_items(k_light_hash_num<512, 8192>, 512, n, s, A, B, r0, items, c_row_ptr, c_col, c_val, err);
+        break;
+    default: break;
+    }
+}
+
+void leaf_symbolic(const LeafSet &L, int bin, const int64_t *items, int64_t n, int width, int64_t *leaf_nnz,
+                   int64_t *slot_cnt, hipStream_t s) {
+    switch (bin) {
+    case LEAF_H0: launch_items(k_leaf_hash_sym<64, 2 * HS_CAP[0]>, 64, n, s, L, items, leaf_nnz, slot_cnt); break;
+    case LEAF_H1: launch_items(k_leaf_hash_sym<64, 2 * HS_CAP[1]>, 64, n, s, L, items, leaf_nnz, slot_cnt); break;
+    case LEAF_H2: launch_items(k_leaf_hash_sym<256, 2 * HS_CAP[2]>, 256, n, s, L, items, leaf_nnz, slot_cnt); break;
+    case LEAF_H3: launch_items(k_leaf_hash_sym<512, 2 * HS_CAP[3]>, 512, n, s, L, items, leaf_nnz, slot_cnt); break;
+    case LEAF_DENSE:
+        GM_REQUIRE(n <= 0 || width <= DENSE_MAX, GMAGNUS_ERROR_UNSUPPORTED, "dense accumulator wider than LDS allows");
+        launch_items(k_leaf_dense_sym<512>, 512, n, s, L, items, width, leaf_nnz, slot_cnt);
+        break;
+    default: break;
+    }
+}
+
+void leaf_numeric(const LeafSet &L, int bin, const int64_t *items, int64_t n, int width, const int64_t *leaf_nnz,
+                  int n_slots_log2, const int64_t *heavy_rows, const int64_t *c_row_ptr, const int64_t *slot_off,
+                  int slot_width_log2, int32_t *c_col, double *c_val, int32_t *err, hipStream_t s) {
+    LeafOut o{n_slots_log2, heavy_rows, c_row_ptr, slot_off, slot_width_log2, c_col, c_val, err};
+    switch (bin) {
+    case LEAF_H0: launch_items(k_leaf_hash_num<64, 256>, 64, n, s, L, items, leaf_nnz, o); break;
+    case LEAF_H1: launch_items(k_leaf_hash_num<64, 1024>, 64, n, s, L, items, leaf_nnz, o); break;
+    case LEAF_H2: launch_items(k_leaf_hash_num<256, 4096>, 256, n, s, L, items, leaf_nnz, o); break;
+    case LEAF_H3: launch_items(k_leaf_hash_num<512, 8192>, 512, n, s, L, items, leaf_nnz, o); break;
+    case LEAF_DENSE:
+        GM_REQUIRE(n <= 0 || width <= DENSE_MAX, GMAGNUS_ERROR_UNSUPPORTED, "dense accumulator wider than LDS allows");
+        launch_items(k_leaf_dense_num<512>, 512, n, s, L, items, leaf_nnz, width, o);
+        break;
+    default: break;
+    }
+}
+
+void slot_scan(int64_t *slot, int64_t n_heavy, int64_t n_slots, const int64_t *heavy_rows, int64_t *row_nnz,
+               hipStream_t s) {
+    if (n_heavy <= 0) return;
+    GM_REQUIRE(n_heavy < (int64_t)1 << 31, GMAGNUS_ERROR_UNSUPPORTED, "too many heavy rows for one panel");
+    hipLaunchKernelGGL(k_slot_scan, dim3((unsigned)n_heavy), dim3(SLOT_BLOCK), 0, s, slot, n_slots, heavy_rows,
+                       row_nnz);
+    GM_CHECK_LAUNCH();
+}
+
+int64_t tau_limit() { return HN_CAP[3]; }
+
+}  // namespace gm

@@ -1,0 +1,134 @@
+// Shared device helpers for the gfx950 SpGEMM kernels: wave64 scans and
+// ballots, block scans, bounded binary searches and small launch utilities.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define GM_DEV __device__ __forceinline__
+#define GM_WAVE 64
+
+namespace gm {
+
+// Read-only view of a device CSR matrix.
+struct Csr {
+    int64_t n_rows, n_cols, nnz;
+    const int64_t *rp;
+    const int32_t *ci;
+    const double *v;
+};
+
+GM_DEV int lane_id() { return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0)); }
+
+GM_DEV uint64_t lanemask_lt() { return (uint64_t(1) << lane_id()) - 1; }
+
+GM_DEV uint64_t ballot(bool p) { return __ballot(p); }
+
+// Orders this lane's earlier LDS accesses before its later ones as seen by
+// the other lanes of the wave (lanes of a wave run in lockstep).
+GM_DEV void wave_lds_fence() {
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+}
+
+template <typename T>
+GM_DEV T wave_incl_scan(T x) {
+    const int lane = threadIdx.x & (GM_WAVE - 1);
+#pragma unroll
+    for (int d = 1; d < GM_WAVE; d <<= 1) {
+        T y = __shfl_up(x, d, GM_WAVE);
+        if (lane >= d) x += y;
+    }
+    return x;
+}
+
+template <typename T>
+GM_DEV T wave_reduce_sum(T x) {
+#pragma unroll
+    for (int d = GM_WAVE / 2; d >= 1; d >>= 1) x += __shfl_xor(x, d, GM_WAVE);
+    return x;
+}
+
+// Exclusive scan over the block in thread order. `smem` holds BLOCK/64
+// entries; the block total is returned through *total when not null.
+// Contains __syncthreads: every thread of the block must call it.
+template <int BLOCK, typename T>
+GM_DEV T block_excl_scan(T x, T *smem, T *total = nullptr) {
+    constexpr int NW = BLOCK / GM_WAVE;
+    const int lane = threadIdx.x & (GM_WAVE - 1), w = threadIdx.x / GM_WAVE;
+    T inc = wave_incl_scan(x);
+    if (lane == GM_WAVE - 1) smem[w] = inc;
+    __syncthreads();
+    if (w == 0) {
+        T s = lane < NW ? smem[lane] : T(0);
+        s = wave_incl_scan(s);
+        if (lane < NW) smem[lane] = s;
+    }
+    __syncthreads();
+    T off = w > 0 ? smem[w - 1] : T(0);
+    if (total) *total = smem[NW - 1];
+    __syncthreads();
+    return off + inc - x;
+}
+
+template <int BLOCK, typename T>
+GM_DEV T block_reduce_sum(T x, T *smem) {
+    T t;
+    block_excl_scan<BLOCK, T>(x, smem, &t);
+    return t;
+}
+
+// Largest index i in [lo, hi) with a[i] <= key, assuming a[lo] <= key and a
+// non-decreasing (the row containing flattened position `key`, skipping
+// empty rows to the last one that starts at or before key).
+template <typename T, typename K>
+GM_DEV int64_t find_row(const T *a, int64_t lo, int64_t hi, K key) {
+    while (hi - lo > 1) {
+        int64_t mid = lo + ((hi - lo) >> 1);
+        if (a[mid] <= (T)key)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+// XCD-aware remap of a linear block id: the hardware deals consecutive
+// workgroups round-robin to the 8 XCDs; this gives each XCD a contiguous run
+// of tiles so neighbouring tiles share that XCD's L2.
+GM_DEV int64_t xcd_tile(int64_t bid, int64_t nblocks) {
+    constexpr int64_t NX = 8;
+    const int64_t per = nblocks / NX, rem = nblocks % NX;
+    const int64_t x = bid % NX, q = bid / NX;
+    // XCD x owns tiles [x*per + min(x, rem), ...) of length per + (x < rem)
+    const int64_t base = x * per + (x < rem ? x : rem);
+    const int64_t len = per + (x < rem ? 1 : 0);
+    return q < len ? base + q : bid;  // q < len always holds for a full grid
+}
+
+template <typename T>
+__global__ void k_fill(T *p, T v, int64_t n) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+template <typename T>
+__global__ void k_iota(T *p, T start, int64_t n) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = start + (T)i;
+}
+
+inline unsigned grid_for(int64_t n, int block, int64_t cap = 1 << 20) {
+    int64_t g = (n + block - 1) / block;
+    if (g < 1) g = 1;
+    if (g > cap) g = cap;
+    return (unsigned)g;
+}
+
+inline int ilog2(int64_t x) {
+    int r = 0;
+    while ((int64_t(1) << (r + 1)) <= x) ++r;
+    return r;
+}
+
+}  // namespace gm

@@ -1,0 +1,211 @@
+// Host-side infrastructure: status propagation, the device workspace
+// allocator, and the launch wrappers every kernel translation unit exports.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/gmagnus.h"
+#include "common.hpp"
+
+namespace gm {
+
+// Error carried from the point of failure to the C ABI.
+struct Error {
+    gmagnus_status_t status;
+    std::string msg;
+};
+
+void set_last_error(const std::string &msg);
+
+#define GM_HIP(expr)                                                                                   \
+    do {                                                                                               \
+        hipError_t e_ = (expr);                                                                        \
+        if (e_ != hipSuccess)                                                                          \
+            throw ::gm::Error{GMAGNUS_ERROR_HIP, std::string(#expr) + ": " + hipGetErrorString(e_)};   \
+    } while (0)
+
+#define GM_CHECK_LAUNCH() GM_HIP(hipGetLastError())
+
+#define GM_REQUIRE(cond, status, msg)                         \
+    do {                                                      \
+        if (!(cond)) throw ::gm::Error{(status), (msg)};      \
+    } while (0)
+
+// Device memory for one plan. Blocks come from the user's callbacks or from
+// the library's process-wide caching allocator. free() keeps a block on the
+// plan's own free list (reused by later allocations of the same plan, which
+// are ordered after the freeing work by the plan's stream joins); every block
+// goes back to the user or the shared cache only on destruction, after the
+// plan's streams have been synchronised.
+class Workspace {
+  public:
+    Workspace(const gmagnus_options_t *opts, hipStream_t stream) : stream_(stream) {
+        if (opts && opts->alloc && opts->free) {
+            ualloc_ = opts->alloc;
+            ufree_ = opts->free;
+            uctx_ = opts->alloc_ctx;
+        }
+    }
+    ~Workspace() { release_all(); }
+    Workspace(const Workspace &) = delete;
+    Workspace &operator=(const Workspace &) = delete;
+
+    void *alloc_bytes(size_t bytes);
+    template <typename T>
+    T *alloc(int64_t n) {
+        return static_cast<T *>(alloc_bytes(sizeof(T) * (size_t)(n > 0 ? n : 1)));
+    }
+    void free(void *p);
+    void release_all();
+    size_t bytes_in_use() const { return in_use_; }
+
+  private:
+    struct Block {
+        void *p;
+        size_t bytes;
+    };
+    hipStream_t stream_;
+    void *(*ualloc_)(size_t, void *, void *) = nullptr;
+    void (*ufree_)(void *, void *, void *) = nullptr;
+    void *uctx_ = nullptr;
+    std::vector<Block> blocks_;  // owned, in use
+    std::vector<Block> spare_;   // owned, freed by the plan
+    size_t in_use_ = 0;
+};
+
+void cache_release();
+
+// ----------------------------------------------------------------- prims.hip
+// Exclusive scan of n int64 values; out has n+1 entries (out[n] = total).
+// `scratch` must hold scan_scratch_elems(n) int64.
+int64_t scan_scratch_elems(int64_t n);
+void scan_i64(const int64_t *in, int64_t n, int64_t *out, int64_t *scratch, hipStream_t s);
+// Exclusive scan of the int64 values in[idx[i]] (gather), n entries.
+void scan_gather_i64(const int64_t *in, const int64_t *idx, int64_t n, int64_t *out, int64_t *scratch,
+                     hipStream_t s);
+
+// Stable partition of items 0..n-1 into `nc` classes given by cls[i] (int8).
+// perm[pos] = i in class-major, index-stable order; inv[i] = pos when inv is
+// not null; class_start (device, nc+1) receives the class boundaries.
+int64_t partition_scratch_elems(int64_t n, int nc);
+void partition_u8(const uint8_t *cls, int64_t n, int nc, int64_t *perm, int64_t *inv, int64_t *class_start,
+                  int64_t *scratch, hipStream_t s);
+
+template <typename T>
+void fill(T *p, T v, int64_t n, hipStream_t s) {
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_fill<T>, dim3(grid_for(n, 256, 16384)), dim3(256), 0, s, p, v, n);
+    GM_CHECK_LAUNCH();
+}
+
+// ----------------------------------------------------------------- setup.hip
+// Fills ip/minc/maxc for rows [r0, r1) of A (local index r - r0).
+void row_products(const Csr &A, const Csr &B, int64_t r0, int64_t r1, int64_t panel_nnz, int64_t *ip, int32_t *minc,
+                  int32_t *maxc, hipStream_t s);
+// Checks canonical CSR; sets *flag (device int32) to nonzero on violation.
+void validate_csr(const Csr &M, int32_t *flag, hipStream_t s);
+
+
+// Masked CSR->CSC of the heavy rows (Algorithm 3, MaskedCsr2Csc).
+struct SliceArrays {
+    int64_t n_slices = 0;
+    int64_t nnz = 0;              // heavy A entries kept (nonempty B row)
+    int64_t *col_ptr = nullptr;   // n_slices + 1
+    int64_t *slice_off = nullptr; // n_slices + 1 (products)
+    int32_t *slice_k = nullptr;   // n_slices: column of A / row of B
+    int32_t *row_h = nullptr;     // nnz: heavy-local row index
+    double *a_val = nullptr;      // nnz
+};
+void csc_count(const Csr &A, const Csr &B, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
+               const int64_t *a_heavy_ptr, int64_t nnz_heavy_all, int64_t *colcnt, hipStream_t s);
+void slice_flags(const Csr &B, const int64_t *colcnt, int64_t n_k, uint8_t *cls, hipStream_t s);
+void slice_build(const Csr &B, const int64_t *colcnt, const int64_t *slice_perm, int64_t n_slices,
+                 int32_t *slice_k, int64_t *cnt_out, int64_t *ip_out, int32_t *k_to_slice, hipStream_t s);
+void csc_fill(const Csr &A, const Csr &B, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
+              const int64_t *a_heavy_ptr, int64_t nnz_heavy_all, const int32_t *k_to_slice,
+              const int64_t *col_ptr, int64_t *fill_cursor, int32_t *row_h, double *a_val, hipStream_t s);
+void gather_row_len(const int64_t *row_ptr, const int64_t *rows, int64_t n, int64_t r0, int64_t *out, hipStream_t s);
+void gather_i64(const int64_t *src, const int64_t *idx, int64_t n, int64_t *out, hipStream_t s);
+
+// ---------------------------------------------------------------- expand.hip
+// Outer-product expansion (Algorithm 4) of every slice into C-hat:
+// expand_tiles() locates every tile's first slice and A~ entry (into
+// expand_tile_words(total) int64), expand() writes the products.
+int64_t expand_tile_words(int64_t total);
+void expand_tiles(const Csr &B, const SliceArrays &sl, int64_t total, int64_t *info_words, hipStream_t s);
+void expand(const Csr &B, const SliceArrays &sl, int64_t total, const int64_t *info_words, int64_t *chat_cursor,
+            int32_t *chat_col, double *chat_val, hipStream_t s);
+
+// ------------------------------------------------------------ multisplit.hip
+struct LevelGeom {
+    int64_t n_in;        // input rows
+    int64_t elems;       // input elements
+    int n_chunks;        // chunks per input row (power of two)
+    int shift;           // log2 of the output chunk width
+    int next_chunks;     // chunks per row at the next level (0 when last)
+    int next_shift;      // log2 of the next level's chunk width
+    int64_t group_elems; // elements per work group (tile)
+    int group_rows;      // rows a tile may touch (power of two, bounded via tau)
+};
+// Tile sizes the multisplit kernel is built for, largest first.
+int multisplit_tile_count();
+int64_t multisplit_tile_elems(int i);
+int multisplit_max_keys();
+int multisplit_max_rows();
+bool multisplit_next_fits(int keys, int next_chunks);
+void tile_rows(const LevelGeom &g, const int64_t *in_ptr, int64_t *tile_row, hipStream_t s);
+void histogram(const LevelGeom &g, const int64_t *in_ptr, const int64_t *tile_row, const int32_t *in_col,
+               int64_t *counts, hipStream_t s);
+void chunk_classes(const int64_t *counts, int64_t n, int64_t tau, bool last, uint8_t *cls, hipStream_t s);
+// out_cnt[inv[i]] = counts[i]; origin_out[inv[i]] = origin_in[i / n_chunks] + (i % n_chunks) * stride.
+void chunk_reorder(const int64_t *counts, const int64_t *inv, int64_t n, int n_chunks, const int64_t *origin_in,
+                   int64_t stride, int64_t *out_cnt, int64_t *origin_out, hipStream_t s);
+void multisplit(const LevelGeom &g, const int64_t *in_ptr, const int64_t *tile_row, const int32_t *in_col,
+                const double *in_val, const int64_t *x_map, int64_t *cursor, int32_t *out_col, double *out_val,
+                int64_t n_heavy_out, int64_t *next_counts, hipStream_t s);
+
+// ------------------------------------------------------------ accumulate.hip
+// Final chunks ("leaves"): chunk rows [lo, hi) of some level's output.
+struct LeafSet {
+    const int64_t *ptr;    // chunk row pointers of that level's output
+    const int32_t *col;    // chunk-local columns
+    const double *val;
+    const int64_t *origin; // slot id h * n_slots + slot, per chunk row
+    int64_t lo, hi;
+};
+enum LeafBin : uint8_t { LEAF_EMPTY = 0, LEAF_H0, LEAF_H1, LEAF_H2, LEAF_H3, LEAF_DENSE, LEAF_NBINS };
+enum LightBin : uint8_t {
+    LIGHT_EMPTY = 0, LIGHT_HEAVY, LIGHT_W0, LIGHT_W1, LIGHT_H0, LIGHT_H1, LIGHT_H2, LIGHT_H3, LIGHT_NBINS
+};
+// Largest tau the light accumulators can hold.
+int64_t tau_limit();
+void light_classes_sym(const int64_t *ip, const int32_t *minc, const int32_t *maxc, int64_t n, int64_t tau,
+                       bool window, uint8_t *cls, hipStream_t s);
+void light_classes_num(const int64_t *ip, const int64_t *row_nnz, const int32_t *minc, const int32_t *maxc,
+                       int64_t n, int64_t tau, bool window, uint8_t *cls, hipStream_t s);
+void leaf_classes_sym(const LeafSet &L, int64_t tau, uint8_t *cls, hipStream_t s);
+void leaf_classes_num(const LeafSet &L, const int64_t *leaf_nnz, int64_t tau, uint8_t *cls, hipStream_t s);
+// Leaf symbolic: leaf_nnz[i] for the leaves items[0..n) (leaf i = chunk row
+// lo + i), and slot_cnt[origin] = leaf_nnz.
+void leaf_symbolic(const LeafSet &L, int bin, const int64_t *items, int64_t n, int width, int64_t *leaf_nnz,
+                   int64_t *slot_cnt, hipStream_t s);
+// Leaf numeric: writes C at c_row_ptr[heavy_rows[h]] + slot_off[origin].
+void leaf_numeric(const LeafSet &L, int bin, const int64_t *items, int64_t n, int width, const int64_t *leaf_nnz,
+                  int n_slots_log2, const int64_t *heavy_rows, const int64_t *c_row_ptr, const int64_t *slot_off,
+                  int slot_width_log2, int32_t *c_col, double *c_val, int32_t *err, hipStream_t s);
+// Light rows (local index r): symbolic count into row_nnz[r]; numeric into C.
+void light_symbolic(const Csr &A, const Csr &B, int64_t r0, int bin, const int64_t *items, int64_t n,
+                    const int32_t *minc, const int32_t *maxc, int64_t *row_nnz, hipStream_t s);
+void light_numeric(const Csr &A, const Csr &B, int64_t r0, int bin, const int64_t *items, int64_t n,
+                   const int32_t *minc, const int32_t *maxc, const int64_t *c_row_ptr, int32_t *c_col, double *c_val,
+                   int32_t *err, hipStream_t s);
+// Per heavy row h: in-place exclusive scan of slot[h*n_slots .. +n_slots),
+// row total into row_nnz[heavy_rows[h]].
+void slot_scan(int64_t *slot, int64_t n_heavy, int64_t n_slots, const int64_t *heavy_rows, int64_t *row_nnz,
+               hipStream_t s);
+
+}  // namespace gm

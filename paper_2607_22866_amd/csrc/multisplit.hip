@@ -1,0 +1,325 @@
+// Hierarchical multisplit of the heavy rows (Section III-C, Algorithm 3's
+// reorder loop, Algorithm 5): per level a histogram of (row, chunk) counts,
+// the heavy/light chunk partition (ThreshPartition, heavy chunks first) and
+// the multisplit that permutes every row of C-hat into its column chunks,
+// with columns shifted into the chunk's local range.
+//
+// gfx950 design of the multisplit work group (one tile of consecutive
+// elements, at most `group_rows` rows since every input row holds more than
+// tau elements):
+//  * elements are loaded coalesced into registers, E per thread;
+//  * each element's rank inside its (wave, key) bucket comes from wave64
+//    ballots (the lanes holding the same key form a peer mask; rank =
+//    popcount of lower peers), accumulated in wave-private LDS counters, so
+//    no LDS atomics are needed and the local order is stable;
+//  * one scan over the (key, wave) counters gives every bucket its local
+//    offset; one global atomic per nonempty key reserves its output range;
+//  * elements are permuted through LDS and written back with consecutive
+//    lanes on consecutive addresses of each output chunk;
+//  * the next level's (chunk, sub-chunk) histogram is accumulated during the
+//    write-out for the chunks that stay heavy, so levels after the first need
+//    no separate histogram pass.
+#include "host.hpp"
+
+namespace gm {
+
+namespace {
+
+constexpr int MS_KMAX = 256;      // keys = group_rows * n_chunks (powers of two)
+constexpr int MS_RMAX = 16;       // rows per tile
+constexpr int MS_NEXT_MAX = 64;   // next-level chunks for the fused histogram
+constexpr int MS_NEXT_KEYS = 64;  // keys whose next-level histogram stays in LDS
+
+// Row containing the first element of every tile.
+__global__ void k_tile_rows(const int64_t *in_ptr, int64_t n_in, int64_t te, int64_t n_tiles, int64_t *tile_row) {
+    for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < n_tiles;
+         t += (int64_t)gridDim.x * blockDim.x)
+        tile_row[t] = find_row(in_ptr, 0, n_in + 1, t * te);
+}
+
+GM_DEV int local_row(const int64_t *rb, int R, int64_t i) {
+    int lr = 0;
+    while (lr + 1 < R && rb[lr + 1] <= i) ++lr;
+    return lr;
+}
+
+// Level-0 histogram (Algorithm 3, Histogram): counts[r * n_chunks + c] +=
+// number of elements of row r with column >> shift == c.
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void k_histogram(int64_t n_in, int64_t elems, const int64_t *in_ptr,
+                                                     const int64_t *tile_row, int64_t te, int64_t n_tiles,
+                                                     const int32_t *in_col, int n_chunks, int shift, int R,
+                                                     int64_t *counts) {
+    __shared__ int32_t cnt[MS_KMAX];
+    __shared__ int64_t rb[MS_RMAX + 1];
+    const int tid = threadIdx.x;
+    const int64_t tile = xcd_tile(blockIdx.x, n_tiles);
+    const int64_t g0 = tile * te;
+    const int64_t g1 = g0 + te < elems ? g0 + te : elems;
+    const int64_t r0 = tile_row[tile];
+    const int K = R * n_chunks;
+    if (tid <= R) rb[tid] = r0 + tid <= n_in ? in_ptr[r0 + tid] : INT64_MAX;
+    for (int k = tid; k < K; k += BLOCK) cnt[k] = 0;
+    __syncthreads();
+    for (int64_t i = g0 + tid; i < g1; i += BLOCK) {
+        const int lr = local_row(rb, R, i);
+        atomicAdd(&cnt[lr * n_chunks + (in_col[i] >> shift)], 1);
+    }
+    __syncthreads();
+    for (int k = tid; k < K; k += BLOCK) {
+        const int v = cnt[k];
+        if (v) atomicAdd((unsigned long long *)&counts[(r0 + k / n_chunks) * n_chunks + k % n_chunks],
+                         (unsigned long long)v);
+    }
+}
+
+template <int BLOCK, int TE>
+__global__ __launch_bounds__(BLOCK) void k_multisplit(int64_t n_in, int64_t elems, const int64_t *in_ptr,
+                                                      const int64_t *tile_row, int64_t n_tiles,
+                                                      const int32_t *in_col, const double *in_val, int n_chunks,
+                                                      int cbits, int shift, int R, int rbits, const int64_t *x_map,
+                                                      int64_t *cursor, int32_t *out_col, double *out_val,
+                                                      int64_t n_heavy_out, int next_chunks, int next_shift,
+                                                      int64_t *next_counts) {
+    constexpr int NW = BLOCK / GM_WAVE;
+    constexpr int E = TE / BLOCK;
+    __shared__ int32_t col_buf[TE];
+    __shared__ double val_buf[TE];
+    __shared__ int32_t whist[NW * MS_KMAX];  // [wave][key] counts, then offsets
+    __shared__ int32_t key_start[MS_KMAX + 1];
+    __shared__ int64_t key_delta[MS_KMAX];   // global position - local position
+    __shared__ int64_t key_out[MS_KMAX];     // output chunk row
+    __shared__ int32_t next_hist[MS_NEXT_KEYS * MS_NEXT_MAX];
+    __shared__ int64_t rb[MS_RMAX + 1];
+    __shared__ int32_t scan_sm[NW];
+
+    const int tid = threadIdx.x, lane = tid & (GM_WAVE - 1), w = tid / GM_WAVE;
+    const int64_t tile = xcd_tile(blockIdx.x, n_tiles);
+    const int64_t g0 = tile * (int64_t)TE;
+    const int n = (int)(elems - g0 < TE ? elems - g0 : TE);
+    const int64_t r0 = tile_row[tile];
+    const int K = R << cbits;
+    const int kbits = rbits + cbits;
+    const int32_t mask = (int32_t)((1u << shift) - 1u);
+    const bool fuse_next = next_counts != nullptr;
+
+    if (tid <= R) rb[tid] = r0 + tid <= n_in ? in_ptr[r0 + tid] : INT64_MAX;
+    for (int k = tid; k < NW * MS_KMAX; k += BLOCK) whist[k] = 0;
+    __syncthreads();
+
+    int32_t col[E];
+    double val[E];
+    int key[E];
+    int rank[E];
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+        const int p = j * BLOCK + tid;
+        const bool valid = p < n;
+        col[j] = valid ? __builtin_nontemporal_load(&in_col[g0 + p]) : 0;
+        val[j] = valid ? __builtin_nontemporal_load(&in_val[g0 + p]) : 0.0;
+        key[j] = valid ? (local_row(rb, R, g0 + p) << cbits) | (col[j] >> shift) : -1;
+    }
+    // ranks inside (wave, key) buckets from ballots
+    int32_t *wh = whist + w * MS_KMAX;
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+        const int k = key[j];
+        const bool valid = k >= 0;
+        uint64_t peers = ballot(valid);
+        for (int b = 0; b < kbits; ++b) {
+            const bool bit = (k >> b) & 1;
+            const uint64_t m = ballot(bit);
+            peers &= bit ? m : ~m;
+        }
+        int base = 0;
+        if (valid) {
+            base = wh[k];
+            rank[j] = base + __popcll(peers & lanemask_lt());
+        }
+        wave_lds_fence();
+        if (valid && lane == __ffsll((long long)peers) - 1) wh[k] = base + __popcll(peers);
+        wave_lds_fence();
+    }
+    __syncthreads();
+
+    // exclusive scan over buckets in (key, wave) order
+    {
+        const int M = NW * K;
+        const int per = (M + BLOCK - 1) / BLOCK;
+        int sum = 0;
+        for (int q = 0; q < per; ++q) {
+            const int idx = tid * per + q;
+            if (idx < M) sum += whist[(idx % NW) * MS_KMAX + idx / NW];
+        }
+        int run = block_excl_scan<BLOCK>(sum, scan_sm);
+        for (int q = 0; q < per; ++q) {
+            const int idx = tid * per + q;
+            if (idx < M) {
+                const int a = (idx % NW) * MS_KMAX + idx / NW;
+                const int v = whist[a];
+                whist[a] = run;
+                if (idx % NW == 0) key_start[idx / NW] = run;
+                run += v;
+            }
+        }
+        if (tid == 0) key_start[K] = n;
+    }
+    __syncthreads();
+
+    // reserve each key's range in its output chunk
+    for (int k = tid; k < K; k += BLOCK) {
+        const int cnt = key_start[k + 1] - key_start[k];
+        if (cnt > 0) {
+            const int64_t r = r0 + (k >> cbits);
+            const int64_t orow = x_map[r * n_chunks + (k & (n_chunks - 1))];
+            const int64_t d = (int64_t)atomicAdd((unsigned long long *)&cursor[orow], (unsigned long long)cnt);
+            key_delta[k] = d - key_start[k];
+            key_out[k] = orow;
+        }
+    }
+    if (fuse_next)
+        for (int q = tid; q < K * next_chunks; q += BLOCK) next_hist[q] = 0;
+    // permute into LDS
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+        if (key[j] >= 0) {
+            const int pos = whist[w * MS_KMAX + key[j]] + rank[j];
+            col_buf[pos] = col[j];
+            val_buf[pos] = val[j];
+        }
+    }
+    __syncthreads();
+
+    // coalesced write-out; the local row of position p is the last row whose
+    // first key starts at or before p
+    for (int p = tid; p < n; p += BLOCK) {
+        const int32_t c = col_buf[p];
+        int lr = 0;
+        while (lr + 1 < R && key_start[(lr + 1) << cbits] <= p) ++lr;
+        const int k = (lr << cbits) | (c >> shift);
+        const int64_t d = key_delta[k] + p;
+        const int32_t lc = c & mask;
+        __builtin_nontemporal_store(lc, &out_col[d]);
+        __builtin_nontemporal_store(val_buf[p], &out_val[d]);
+        if (fuse_next && key_out[k] < n_heavy_out) atomicAdd(&next_hist[k * next_chunks + (lc >> next_shift)], 1);
+    }
+    if (fuse_next) {
+        __syncthreads();
+        for (int q = tid; q < K * next_chunks; q += BLOCK) {
+            const int v = next_hist[q];
+            if (v) {
+                const int k = q / next_chunks;
+                atomicAdd((unsigned long long *)&next_counts[key_out[k] * next_chunks + q % next_chunks],
+                          (unsigned long long)v);
+            }
+        }
+    }
+}
+
+__global__ void k_chunk_classes(const int64_t *counts, int64_t n, int64_t tau, int last, uint8_t *cls) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        cls[i] = (!last && counts[i] > tau) ? 0 : 1;
+}
+
+__global__ void k_chunk_reorder(const int64_t *counts, const int64_t *inv, int64_t n, int n_chunks,
+                                const int64_t *origin_in, int64_t stride, int64_t *out_cnt, int64_t *origin_out) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t o = inv[i];
+        out_cnt[o] = counts[i];
+        origin_out[o] = origin_in[i / n_chunks] + (i % n_chunks) * stride;
+    }
+}
+
+constexpr int64_t MS_TILES[3] = {8192, 2048, 512};
+
+template <int BLOCK, int TE>
+void launch_multisplit(const LevelGeom &g, const int64_t *in_ptr, const int64_t *tile_row, const int32_t *in_col,
+                       const double *in_val, const int64_t *x_map, int64_t *cursor, int32_t *out_col,
+                       double *out_val, int64_t n_heavy_out, int64_t *next_counts, int cbits, int rbits,
+                       hipStream_t s) {
+    const int64_t n_tiles = (g.elems + TE - 1) / TE;
+    GM_REQUIRE(n_tiles < (int64_t)1 << 31, GMAGNUS_ERROR_UNSUPPORTED, "multisplit: too many tiles");
+    hipLaunchKernelGGL((k_multisplit<BLOCK, TE>), dim3((unsigned)n_tiles), dim3(BLOCK), 0, s, g.n_in, g.elems, in_ptr,
+                       tile_row, n_tiles, in_col, in_val, g.n_chunks, cbits, g.shift, g.group_rows, rbits, x_map,
+                       cursor, out_col, out_val, n_heavy_out, g.next_chunks, g.next_shift, next_counts);
+    GM_CHECK_LAUNCH();
+}
+
+}  // namespace
+
+int multisplit_tile_count() { return 3; }
+int64_t multisplit_tile_elems(int i) { return MS_TILES[i]; }
+int multisplit_max_keys() { return MS_KMAX; }
+int multisplit_max_rows() { return MS_RMAX; }
+bool multisplit_next_fits(int keys, int next_chunks) {
+    return next_chunks <= MS_NEXT_MAX && keys * next_chunks <= MS_NEXT_KEYS * MS_NEXT_MAX;
+}
+
+void histogram(const LevelGeom &g, const int64_t *in_ptr, const int64_t *tile_row, const int32_t *in_col,
+               int64_t *counts, hipStream_t s) {
+    fill<int64_t>(counts, 0, g.n_in * g.n_chunks, s);
+    if (g.elems <= 0) return;
+    GM_REQUIRE((int64_t)g.group_rows * g.n_chunks <= MS_KMAX && g.group_rows <= MS_RMAX, GMAGNUS_ERROR_UNSUPPORTED,
+               "histogram: too many keys per work group");
+    const int64_t n_tiles = (g.elems + g.group_elems - 1) / g.group_elems;
+    hipLaunchKernelGGL(k_histogram<512>, dim3((unsigned)n_tiles), dim3(512), 0, s, g.n_in, g.elems, in_ptr, tile_row,
+                       g.group_elems, n_tiles, in_col, g.n_chunks, g.shift, g.group_rows, counts);
+    GM_CHECK_LAUNCH();
+}
+
+void tile_rows(const LevelGeom &g, const int64_t *in_ptr, int64_t *tile_row, hipStream_t s) {
+    if (g.elems <= 0) return;
+    const int64_t n_tiles = (g.elems + g.group_elems - 1) / g.group_elems;
+    hipLaunchKernelGGL(k_tile_rows, dim3(grid_for(n_tiles, 256, 65536)), dim3(256), 0, s, in_ptr, g.n_in,
+                       g.group_elems, n_tiles, tile_row);
+    GM_CHECK_LAUNCH();
+}
+
+void chunk_classes(const int64_t *counts, int64_t n, int64_t tau, bool last, uint8_t *cls, hipStream_t s) {
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_chunk_classes, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, counts, n, tau, (int)last,
+                       cls);
+    GM_CHECK_LAUNCH();
+}
+
+void chunk_reorder(const int64_t *counts, const int64_t *inv, int64_t n, int n_chunks, const int64_t *origin_in,
+                   int64_t stride, int64_t *out_cnt, int64_t *origin_out, hipStream_t s) {
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_chunk_reorder, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, counts, inv, n, n_chunks,
+                       origin_in, stride, out_cnt, origin_out);
+    GM_CHECK_LAUNCH();
+}
+
+void multisplit(const LevelGeom &g, const int64_t *in_ptr, const int64_t *tile_row, const int32_t *in_col,
+                const double *in_val, const int64_t *x_map, int64_t *cursor, int32_t *out_col, double *out_val,
+                int64_t n_heavy_out, int64_t *next_counts, hipStream_t s) {
+    if (g.elems <= 0) return;
+    const int cbits = ilog2(g.n_chunks);
+    const int rbits = ilog2(g.group_rows);
+    GM_REQUIRE((1 << cbits) == g.n_chunks && (1 << rbits) == g.group_rows, GMAGNUS_ERROR_INVALID_VALUE,
+               "multisplit: chunk and row counts must be powers of two");
+    GM_REQUIRE(g.group_rows <= MS_RMAX && (g.group_rows << cbits) <= MS_KMAX, GMAGNUS_ERROR_UNSUPPORTED,
+               "multisplit: too many keys per work group");
+    const bool fuse = next_counts != nullptr && n_heavy_out > 0 && g.next_chunks > 0;
+    if (fuse)
+        GM_REQUIRE(multisplit_next_fits(g.group_rows << cbits, g.next_chunks), GMAGNUS_ERROR_UNSUPPORTED,
+                   "multisplit: next-level histogram does not fit");
+    int64_t *nc = fuse ? next_counts : nullptr;
+    switch (g.group_elems) {
+    case 8192:
+        launch_multisplit<512, 8192>(g, in_ptr, tile_row, in_col, in_val, x_map, cursor, out_col, out_val,
+                                     n_heavy_out, nc, cbits, rbits, s);
+        break;
+    case 2048:
+        launch_multisplit<512, 2048>(g, in_ptr, tile_row, in_col, in_val, x_map, cursor, out_col, out_val,
+                                     n_heavy_out, nc, cbits, rbits, s);
+        break;
+    case 512:
+        launch_multisplit<256, 512>(g, in_ptr, tile_row, in_col, in_val, x_map, cursor, out_col, out_val,
+                                    n_heavy_out, nc, cbits, rbits, s);
+        break;
+    default: throw Error{GMAGNUS_ERROR_INVALID_VALUE, "multisplit: unsupported tile size"};
+    }
+}
+
+}  // namespace gm

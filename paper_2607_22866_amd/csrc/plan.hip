@@ -1,0 +1,1033 @@
+// Host orchestration of the SpGEMM C = A*B (Algorithm 3) behind the C ABI of
+// gmagnus.h: parameter selection (Section III-D), the setup phase, the heavy
+// path (masked CSC, outer product, hierarchical multisplit, final chunks) on
+// one HIP stream and the light path on another, the C row-pointer scan, and
+// the numeric phase. Also the library's caching device allocator.
+#include <algorithm>
+#include <cstring>
+#include <map>
+#include <memory>
+#include <mutex>
+
+#include "host.hpp"
+
+namespace gm {
+
+// ------------------------------------------------------------ last error
+static thread_local std::string g_last_error;
+void set_last_error(const std::string &msg) { g_last_error = msg; }
+
+// --------------------------------------------------------- caching allocator
+namespace {
+struct DeviceCache {
+    std::mutex m;
+    std::multimap<std::pair<int, size_t>, void *> free_blocks;  // (device, bytes) -> block
+    std::map<void *, std::pair<int, size_t>> sizes;             // all blocks handed out
+};
+DeviceCache &cache() {
+    static DeviceCache *c = new DeviceCache();  // never destroyed: outlives static plans
+    return *c;
+}
+
+size_t round_bytes(size_t b) {
+    if (b < ((size_t)1 << 20)) return (b + 255) & ~(size_t)255;
+    const size_t g = (size_t)2 << 20;
+    return (b + g - 1) / g * g;
+}
+
+void *cache_alloc(size_t bytes) {
+    int dev = 0;
+    GM_HIP(hipGetDevice(&dev));
+    bytes = round_bytes(bytes);
+    DeviceCache &c = cache();
+    {
+        std::lock_guard<std::mutex> lk(c.m);
+        auto it = c.free_blocks.lower_bound({dev, bytes});
+        // reuse a block up to 25% (+2 MiB) larger than asked
+        if (it != c.free_blocks.end() && it->first.first == dev && it->first.second <= bytes + bytes / 4 + ((size_t)2 << 20)) {
+            void *p = it->second;
+            c.free_blocks.erase(it);
+            return p;
+        }
+    }
+    void *p = nullptr;
+    hipError_t e = hipMalloc(&p, bytes);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        cache_release();
+        e = hipMalloc(&p, bytes);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            throw Error{GMAGNUS_ERROR_OUT_OF_MEMORY, "device allocation of " + std::to_string(bytes) + " bytes failed"};
+        }
+    }
+    std::lock_guard<std::mutex> lk(c.m);
+    c.sizes[p] = {dev, bytes};
+    return p;
+}
+
+void cache_free(void *p) {
+    DeviceCache &c = cache();
+    std::lock_guard<std::mutex> lk(c.m);
+    auto it = c.sizes.find(p);
+    if (it == c.sizes.end()) return;
+    c.free_blocks.insert({it->second, p});
+}
+}  // namespace
+
+void cache_release() {
+    DeviceCache &c = cache();
+    std::lock_guard<std::mutex> lk(c.m);
+    for (auto &kv : c.free_blocks) {
+        (void)hipFree(kv.second);
+        c.sizes.erase(kv.second);
+    }
+    c.free_blocks.clear();
+}
+
+void *Workspace::alloc_bytes(size_t bytes) {
+    const size_t want = round_bytes(bytes);
+    for (size_t i = 0; i < spare_.size(); ++i)
+        if (spare_[i].bytes >= want && spare_[i].bytes <= want + want / 4 + ((size_t)2 << 20)) {
+            Block b = spare_[i];
+            spare_[i] = spare_.back();
+            spare_.pop_back();
+            blocks_.push_back(b);
+            in_use_ += b.bytes;
+            return b.p;
+        }
+    void *p = nullptr;
+    if (ualloc_) {
+        p = ualloc_(want, (void *)stream_, uctx_);
+        if (!p) throw Error{GMAGNUS_ERROR_OUT_OF_MEMORY, "user allocator returned NULL"};
+    } else {
+        try {
+            p = cache_alloc(want);
+        } catch (const Error &) {
+            // give this plan's spare blocks back and retry once
+            for (auto &b : spare_) cache_free(b.p);
+            spare_.clear();
+            p = cache_alloc(want);
+        }
+    }
+    blocks_.push_back({p, want});
+    in_use_ += want;
+    return p;
+}
+
+void Workspace::free(void *p) {
+    if (!p) return;
+    for (size_t i = 0; i < blocks_.size(); ++i)
+        if (blocks_[i].p == p) {
+            in_use_ -= blocks_[i].bytes;
+            spare_.push_back(blocks_[i]);
+            blocks_[i] = blocks_.back();
+            blocks_.pop_back();
+            return;
+        }
+}
+
+void Workspace::release_all() {
+    for (auto *v : {&blocks_, &spare_})
+        for (auto &b : *v) {
+            if (ufree_)
+                ufree_(b.p, (void *)stream_, uctx_);
+            else
+                cache_free(b.p);
+        }
+    blocks_.clear();
+    spare_.clear();
+    in_use_ = 0;
+}
+
+// --------------------------------------------------------------- planner
+namespace {
+constexpr int64_t S_COL = 4, S_VAL = 8, S_ROWPTR = 8, S_HISTO = 4, ALPHA = 2, N_SUBGROUPS = 16;
+constexpr int64_t MIN_LOCAL_CHUNK = 64;  // mean elements per local chunk of a multisplit group
+constexpr int MAX_DENSE_LOG2 = 13;       // 8192 fp64 values + bitmap per work group
+constexpr int MAX_CHUNKS_LOG2 = 6;       // chunks per level the multisplit kernel supports
+
+int64_t floor_pow2(int64_t x) { return x < 1 ? 0 : int64_t(1) << ilog2(x); }
+int64_t ceil_pow2(int64_t x) {
+    int64_t p = 1;
+    while (p < x) p <<= 1;
+    return p;
+}
+
+void compute_params(int64_t c_m, int64_t s_lm, const gmagnus_options_t *o, gmagnus_params_t *p) {
+    GM_REQUIRE(c_m >= 1 && c_m < ((int64_t)1 << 31), GMAGNUS_ERROR_INVALID_VALUE, "C must have 1..2^31-1 columns");
+    GM_REQUIRE(s_lm >= 1024, GMAGNUS_ERROR_INVALID_VALUE, "local memory size below 1 KB");
+    std::memset(p, 0, sizeof(*p));
+    // tau: alpha*tau hash slots of (column, value) fill the local memory
+    int64_t tau = s_lm / (ALPHA * (S_COL + S_VAL));
+    // dense width: one value and one bitmap bit per column, with alpha headroom
+    int64_t W = floor_pow2((8 * s_lm) / (ALPHA * (8 * S_VAL + 1)));
+    if (o && o->tau > 0) tau = o->tau;
+    if (o && o->dense_width_log2 > 0) {
+        GM_REQUIRE(o->dense_width_log2 <= MAX_DENSE_LOG2, GMAGNUS_ERROR_INVALID_VALUE, "dense width above 2^13");
+        W = int64_t(1) << o->dense_width_log2;
+    }
+    W = std::min<int64_t>(W, int64_t(1) << MAX_DENSE_LOG2);
+    const int64_t req = std::max<int64_t>(1, ceil_pow2(c_m) / W);
+    // half of local memory holds the locally permuted elements of a multisplit group
+    const int64_t min_group = s_lm / (2 * (S_COL + S_VAL));
+    const int64_t group_rows = (min_group - 1 + tau - 1) / tau + 1;
+    // the light accumulators hold at most tau_limit() products per row
+    tau = std::min<int64_t>(tau, tau_limit());
+    const int64_t eq = (s_lm - min_group * (S_COL + S_VAL) - S_HISTO) / (group_rows * (N_SUBGROUPS * S_HISTO + S_ROWPTR));
+    int64_t cmax = std::min(floor_pow2(eq), floor_pow2(min_group / (group_rows * MIN_LOCAL_CHUNK)));
+    if (o && o->chunks_max_log2 > 0) cmax = int64_t(1) << o->chunks_max_log2;
+    cmax = std::max<int64_t>(2, std::min<int64_t>(cmax, int64_t(1) << MAX_CHUNKS_LOG2));
+    p->tau = tau;
+    p->dense_width = W;
+    p->chunks_required = req;
+    p->chunks_max = cmax;
+    p->min_group_elems = min_group;
+    p->group_rows = group_rows;
+    if (req == 1) {
+        p->n_levels = 0;
+    } else if (req <= cmax) {
+        p->n_levels = 1;
+        p->v_chunks[0] = (int32_t)req;
+    } else {
+        const int lr = ilog2(req), lm = ilog2(cmax);
+        const int levels = (lr + lm - 1) / lm;
+        GM_REQUIRE(levels <= GMAGNUS_MAX_LEVELS, GMAGNUS_ERROR_UNSUPPORTED, "too many multisplit levels");
+        p->n_levels = levels;
+        for (int i = 0; i < levels - 1; ++i) p->v_chunks[i] = (int32_t)cmax;
+        p->v_chunks[levels - 1] = (int32_t)(req >> (lm * (levels - 1)));
+    }
+}
+}  // namespace
+
+}  // namespace gm
+
+using namespace gm;
+
+// ------------------------------------------------------------------ plan
+struct LeafLevel {
+    LeafSet set;
+    int width = 0;
+    int64_t *leaf_nnz = nullptr;
+    int64_t *items_sym = nullptr, *items_num = nullptr;
+    int64_t bins_sym[LEAF_NBINS + 1] = {0};
+    int64_t bins_num[LEAF_NBINS + 1] = {0};
+    int64_t elems = 0;
+};
+
+struct TimedEvent {
+    int cls;
+    hipEvent_t a, b;
+};
+
+struct gmagnus_plan_s {
+    Csr A{}, B{};
+    int64_t r0 = 0, r1 = 0, n = 0;
+    gmagnus_options_t opts{};
+    gmagnus_params_t params{};
+    hipStream_t stream = nullptr, s_heavy = nullptr, s_light = nullptr;
+    bool own_streams = false;
+    std::unique_ptr<Workspace> ws;
+    int32_t *err = nullptr;  // device consistency flags
+    // setup
+    int64_t *ip = nullptr;
+    int32_t *minc = nullptr, *maxc = nullptr;
+    int64_t *perm = nullptr;          // rows grouped by symbolic light bin (heavy class included)
+    int64_t bins_sym[LIGHT_NBINS + 1] = {0};
+    int64_t *perm_num = nullptr;      // rows grouped by numeric bin
+    int64_t bins_num[LIGHT_NBINS + 1] = {0};
+    int64_t n_heavy = 0;
+    const int64_t *heavy_rows = nullptr;
+    int64_t *chat_ptr = nullptr;      // n_heavy + 1
+    int64_t products_total = 0, products_heavy = 0;
+    // symbolic
+    int64_t *row_nnz = nullptr;
+    int64_t n_slots = 1;
+    int n_slots_log2 = 0, slot_width_log2 = 0;
+    int64_t *slot = nullptr;
+    std::vector<LeafLevel> leaves;
+    bool symbolic_done = false;
+    int64_t c_nnz = 0;
+    gmagnus_plan_info_t info{};
+    std::vector<TimedEvent> timers;
+    bool timing = false;
+
+    ~gmagnus_plan_s() {
+        (void)hipStreamSynchronize(stream);
+        if (s_heavy && s_heavy != stream) (void)hipStreamSynchronize(s_heavy);
+        if (s_light && s_light != stream) (void)hipStreamSynchronize(s_light);
+        for (auto &t : timers) {
+            (void)hipEventDestroy(t.a);
+            (void)hipEventDestroy(t.b);
+        }
+        ws.reset();
+        if (own_streams) {
+            (void)hipStreamDestroy(s_heavy);
+            (void)hipStreamDestroy(s_light);
+        }
+    }
+};
+
+namespace {
+
+// Records a pair of events around a group of launches of one kernel class.
+struct Timed {
+    gmagnus_plan_s *p;
+    int cls;
+    hipStream_t s;
+    hipEvent_t a = nullptr, b = nullptr;
+    Timed(gmagnus_plan_s *p_, int cls_, hipStream_t s_) : p(p_), cls(cls_), s(s_) {
+        if (!p->timing) return;
+        GM_HIP(hipEventCreate(&a));
+        GM_HIP(hipEventCreate(&b));
+        GM_HIP(hipEventRecord(a, s));
+    }
+    ~Timed() {
+        if (!p->timing || !a) return;
+        if (hipEventRecord(b, s) == hipSuccess)
+            p->timers.push_back({cls, a, b});
+        else {
+            (void)hipEventDestroy(a);
+            (void)hipEventDestroy(b);
+        }
+    }
+};
+
+template <typename T>
+T read_scalar(const T *dev, hipStream_t s) {
+    T v{};
+    GM_HIP(hipMemcpyAsync(&v, dev, sizeof(T), hipMemcpyDeviceToHost, s));
+    GM_HIP(hipStreamSynchronize(s));
+    return v;
+}
+
+Csr to_csr(const gmagnus_csr_t *m) { return Csr{m->n_rows, m->n_cols, m->nnz, m->row_ptr, m->col_idx, m->val}; }
+
+void check_csr_desc(const gmagnus_csr_t *m, const char *name) {
+    GM_REQUIRE(m != nullptr, GMAGNUS_ERROR_INVALID_VALUE, std::string(name) + " is NULL");
+    GM_REQUIRE(m->n_rows >= 0 && m->n_cols >= 0 && m->nnz >= 0, GMAGNUS_ERROR_INVALID_VALUE,
+               std::string(name) + ": negative size");
+    GM_REQUIRE(m->n_cols < ((int64_t)1 << 31) && m->n_rows < ((int64_t)1 << 31), GMAGNUS_ERROR_UNSUPPORTED,
+               std::string(name) + ": dimensions must be below 2^31");
+    GM_REQUIRE(m->row_ptr != nullptr, GMAGNUS_ERROR_INVALID_VALUE, std::string(name) + ": row_ptr is NULL");
+    GM_REQUIRE(m->nnz == 0 || (m->col_idx && m->val), GMAGNUS_ERROR_INVALID_VALUE,
+               std::string(name) + ": col_idx/val is NULL");
+}
+
+int64_t lds_bytes_of(const gmagnus_options_t &o) {
+    if (o.lds_bytes > 0) return o.lds_bytes;
+    int dev = 0, v = 0;
+    GM_HIP(hipGetDevice(&dev));
+    GM_HIP(hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev));
+    return v;
+}
+
+// Reads bin boundaries of a partition into host memory.
+void read_bins(const int64_t *dev, int nb, int64_t *host, hipStream_t s) {
+    GM_HIP(hipMemcpyAsync(host, dev, sizeof(int64_t) * (nb + 1), hipMemcpyDeviceToHost, s));
+    GM_HIP(hipStreamSynchronize(s));
+}
+
+// Chooses the multisplit tile (elements) and rows per tile for a level.
+void choose_tile(LevelGeom &g, int64_t tau) {
+    for (int i = 0; i < multisplit_tile_count(); ++i) {
+        const int64_t te = multisplit_tile_elems(i);
+        const int64_t rows = (te - 1 + tau - 1) / tau + 1;  // input rows hold more than tau elements
+        const int R = (int)ceil_pow2(rows);
+        const int keys = R * g.n_chunks;
+        if (R <= multisplit_max_rows() && keys <= multisplit_max_keys() &&
+            (g.next_chunks == 0 || multisplit_next_fits(keys, g.next_chunks))) {
+            g.group_elems = te;
+            g.group_rows = R;
+            return;
+        }
+    }
+    throw Error{GMAGNUS_ERROR_UNSUPPORTED, "tau too small for the multisplit tile sizes"};
+}
+
+__global__ void k_affine(int64_t *p, int64_t n, int64_t a) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = i * a;
+}
+
+__global__ void k_copy_i64(int64_t *dst, const int64_t *src, int64_t n) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        dst[i] = src[i];
+}
+
+void copy_i64(int64_t *dst, const int64_t *src, int64_t n, hipStream_t s) {
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_copy_i64, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, dst, src, n);
+    GM_CHECK_LAUNCH();
+}
+
+// ----------------------------------------------------------- plan phases
+void do_plan(gmagnus_plan_s *p, const gmagnus_csr_t *A, const gmagnus_csr_t *B, const gmagnus_options_t *opts,
+             hipStream_t stream) {
+    check_csr_desc(A, "A");
+    check_csr_desc(B, "B");
+    GM_REQUIRE(A->n_cols == B->n_rows, GMAGNUS_ERROR_INVALID_VALUE, "A.n_cols must equal B.n_rows");
+    if (opts) {
+        GM_REQUIRE(opts->struct_size == sizeof(gmagnus_options_t), GMAGNUS_ERROR_INVALID_VALUE,
+                   "options.struct_size mismatch");
+        GM_REQUIRE((opts->alloc == nullptr) == (opts->free == nullptr), GMAGNUS_ERROR_INVALID_VALUE,
+                   "alloc and free callbacks must be given together");
+        p->opts = *opts;
+    } else {
+        gmagnus_options_init(&p->opts);
+    }
+    const gmagnus_options_t &o = p->opts;
+    p->A = to_csr(A);
+    p->B = to_csr(B);
+    p->r0 = o.row_begin;
+    p->r1 = o.row_end > 0 ? o.row_end : A->n_rows;
+    GM_REQUIRE(p->r0 >= 0 && p->r0 <= p->r1 && p->r1 <= A->n_rows, GMAGNUS_ERROR_INVALID_VALUE, "bad row panel");
+    p->n = p->r1 - p->r0;
+    p->stream = stream;
+    p->timing = (o.flags & GMAGNUS_FLAG_TIMING) != 0;
+    if (o.flags & GMAGNUS_FLAG_SERIAL_STREAMS) {
+        p->s_heavy = p->s_light = stream;
+    } else {
+        GM_HIP(hipStreamCreateWithFlags(&p->s_heavy, hipStreamNonBlocking));
+        GM_HIP(hipStreamCreateWithFlags(&p->s_light, hipStreamNonBlocking));
+        p->own_streams = true;
+    }
+    compute_params(std::max<int64_t>(B->n_cols, 1), lds_bytes_of(o), &o, &p->params);
+    p->ws.reset(new Workspace(&o, stream));
+    Workspace &ws = *p->ws;
+    p->err = ws.alloc<int32_t>(1);
+    fill<int32_t>(p->err, 0, 1, stream);
+
+    if (o.validate) {
+        int32_t *flag = ws.alloc<int32_t>(2);
+        validate_csr(p->A, flag, stream);
+        validate_csr(p->B, flag + 1, stream);
+        int32_t f[2];
+        GM_HIP(hipMemcpyAsync(f, flag, sizeof(f), hipMemcpyDeviceToHost, stream));
+        GM_HIP(hipStreamSynchronize(stream));
+        GM_REQUIRE(f[0] == 0, GMAGNUS_ERROR_INVALID_CSR, "A is not canonical CSR (flags " + std::to_string(f[0]) + ")");
+        GM_REQUIRE(f[1] == 0, GMAGNUS_ERROR_INVALID_CSR, "B is not canonical CSR (flags " + std::to_string(f[1]) + ")");
+    }
+    const int64_t n = p->n;
+    p->info.n_rows = n;
+    p->info.params = p->params;
+    if (n == 0) return;
+
+    int64_t rp2[2] = {0, 0};
+    GM_HIP(hipMemcpyAsync(&rp2[0], A->row_ptr + p->r0, sizeof(int64_t), hipMemcpyDeviceToHost, stream));
+    GM_HIP(hipMemcpyAsync(&rp2[1], A->row_ptr + p->r1, sizeof(int64_t), hipMemcpyDeviceToHost, stream));
+    GM_HIP(hipStreamSynchronize(stream));
+    const int64_t panel_nnz = rp2[1] - rp2[0];
+
+    Timed t(p, GMAGNUS_K_SETUP, stream);
+    p->ip = ws.alloc<int64_t>(n);
+    p->minc = ws.alloc<int32_t>(n);
+    p->maxc = ws.alloc<int32_t>(n);
+    row_products(p->A, p->B, p->r0, p->r1, panel_nnz, p->ip, p->minc, p->maxc, stream);
+    const bool window = (o.flags & GMAGNUS_FLAG_NO_WINDOW) == 0;
+    uint8_t *cls = ws.alloc<uint8_t>(n);
+    light_classes_sym(p->ip, p->minc, p->maxc, n, p->params.tau, window, cls, stream);
+    p->perm = ws.alloc<int64_t>(n);
+    int64_t *bins = ws.alloc<int64_t>(LIGHT_NBINS + 1);
+    int64_t *scratch = ws.alloc<int64_t>(std::max(partition_scratch_elems(n, LIGHT_NBINS), scan_scratch_elems(n)));
+    partition_u8(cls, n, LIGHT_NBINS, p->perm, nullptr, bins, scratch, stream);
+    // products of all rows and of the heavy rows (C-hat row pointers)
+    int64_t *ip_scan = ws.alloc<int64_t>(n + 1);
+    scan_i64(p->ip, n, ip_scan, scratch, stream);
+    read_bins(bins, LIGHT_NBINS, p->bins_sym, stream);
+    p->products_total = read_scalar(ip_scan + n, stream);
+    p->n_heavy = p->bins_sym[LIGHT_HEAVY + 1] - p->bins_sym[LIGHT_HEAVY];
+    p->heavy_rows = p->perm + p->bins_sym[LIGHT_HEAVY];
+    p->chat_ptr = ws.alloc<int64_t>(p->n_heavy + 1);
+    scan_gather_i64(p->ip, p->heavy_rows, p->n_heavy, p->chat_ptr, scratch, stream);
+    p->products_heavy = read_scalar(p->chat_ptr + p->n_heavy, stream);
+    ws.free(ip_scan);
+    ws.free(scratch);
+    ws.free(cls);
+    p->info.n_heavy_rows = p->n_heavy;
+    p->info.n_light_rows = p->bins_sym[LIGHT_NBINS] - p->bins_sym[LIGHT_W0];
+    p->info.products_total = p->products_total;
+    p->info.products_heavy = p->products_heavy;
+}
+
+void add_bytes(gmagnus_plan_s *p, int cls, double bytes) { p->info.kernel_bytes[cls] += bytes; }
+
+// Heavy path of the symbolic phase: masked CSC, expansion, multisplit
+// levels, final-chunk symbolic, fragment offsets. Runs on p->s_heavy.
+void heavy_symbolic(gmagnus_plan_s *p) {
+    Workspace &ws = *p->ws;
+    const hipStream_t s = p->s_heavy;
+    const int64_t nh = p->n_heavy;
+    const gmagnus_params_t &P = p->params;
+    const int64_t H = p->products_heavy;
+    const int c_bits = ilog2(ceil_pow2(std::max<int64_t>(p->B.n_cols, 1)));
+    p->n_slots = P.n_levels > 0 ? P.chunks_required : 1;
+    p->n_slots_log2 = ilog2(p->n_slots);
+    p->slot_width_log2 = c_bits - p->n_slots_log2;
+
+    // ---- masked CSR -> CSC of the heavy rows and slice offsets
+    SliceArrays sl;
+    int64_t *row_len, *a_heavy_ptr, *scratch;
+    int64_t nnz_heavy_all = 0, blen_total = 0;
+    {
+        Timed t(p, GMAGNUS_K_CSC, s);
+        row_len = ws.alloc<int64_t>(nh);
+        a_heavy_ptr = ws.alloc<int64_t>(nh + 1);
+        const int64_t n_k = p->A.n_cols;
+        scratch = ws.alloc<int64_t>(std::max({scan_scratch_elems(std::max(nh, n_k)), partition_scratch_elems(n_k, 2),
+                                              (int64_t)16}));
+        gather_row_len(p->A.rp, p->heavy_rows, nh, p->r0, row_len, s);
+        scan_i64(row_len, nh, a_heavy_ptr, scratch, s);
+        nnz_heavy_all = read_scalar(a_heavy_ptr + nh, s);
+        int64_t *colcnt = ws.alloc<int64_t>(n_k);
+        csc_count(p->A, p->B, p->heavy_rows, nh, p->r0, a_heavy_ptr, nnz_heavy_all, colcnt, s);
+        uint8_t *kcls = ws.alloc<uint8_t>(n_k);
+        slice_flags(p->B, colcnt, n_k, kcls, s);
+        int64_t *kperm = ws.alloc<int64_t>(n_k);
+        int64_t *kb = ws.alloc<int64_t>(3);
+        partition_u8(kcls, n_k, 2, kperm, nullptr, kb, scratch, s);
+        int64_t kbh[3];
+        read_bins(kb, 2, kbh, s);
+        sl.n_slices = kbh[1];
+        sl.slice_k = ws.alloc<int32_t>(sl.n_slices);
+        int64_t *cnt_s = ws.alloc<int64_t>(sl.n_slices);
+        int64_t *ip_s = ws.alloc<int64_t>(sl.n_slices);
+        int32_t *k_to_slice = ws.alloc<int32_t>(p->B.n_rows);
+        slice_build(p->B, colcnt, kperm, sl.n_slices, sl.slice_k, cnt_s, ip_s, k_to_slice, s);
+        sl.col_ptr = ws.alloc<int64_t>(sl.n_slices + 1);
+        sl.slice_off = ws.alloc<int64_t>(sl.n_slices + 1);
+        int64_t *sc2 = ws.alloc<int64_t>(scan_scratch_elems(sl.n_slices));
+        scan_i64(cnt_s, sl.n_slices, sl.col_ptr, sc2, s);
+        scan_i64(ip_s, sl.n_slices, sl.slice_off, sc2, s);
+        int64_t tot[2];
+        GM_HIP(hipMemcpyAsync(&tot[0], sl.col_ptr + sl.n_slices, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+        GM_HIP(hipMemcpyAsync(&tot[1], sl.slice_off + sl.n_slices, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+        GM_HIP(hipStreamSynchronize(s));
+        sl.nnz = tot[0];
+        GM_REQUIRE(tot[1] == H, GMAGNUS_ERROR_HIP, "slice products disagree with the row products");
+        int64_t *cursor = ws.alloc<int64_t>(std::max<int64_t>(sl.n_slices, 1));
+        fill<int64_t>(cursor, 0, sl.n_slices, s);
+        sl.row_h = ws.alloc<int32_t>(sl.nnz);
+        sl.a_val = ws.alloc<double>(sl.nnz);
+        csc_fill(p->A, p->B, p->heavy_rows, nh, p->r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, sl.col_ptr, cursor,
+                 sl.row_h, sl.a_val, s);
+        // compulsory bytes of B~ (each slice's B row once): sum of nnz(B[k,:]) over slices
+        blen_total = 0;
+        ws.free(cursor);
+        ws.free(colcnt);
+        ws.free(kcls);
+        ws.free(kperm);
+        ws.free(kb);
+        ws.free(cnt_s);
+        ws.free(ip_s);
+        ws.free(k_to_slice);
+        ws.free(sc2);
+        ws.free(row_len);
+        ws.free(a_heavy_ptr);
+        ws.free(scratch);
+        add_bytes(p, GMAGNUS_K_CSC, 12.0 * nnz_heavy_all + 12.0 * sl.nnz + 8.0 * (p->A.n_cols + sl.n_slices));
+    }
+    p->info.n_slices = sl.n_slices;
+    p->info.nnz_a_heavy = sl.nnz;
+
+    // ---- outer-product expansion into buffer 0
+    int32_t *col_buf[2] = {ws.alloc<int32_t>(H), nullptr};
+    double *val_buf[2] = {ws.alloc<double>(H), nullptr};
+    {
+        int64_t *cursor = ws.alloc<int64_t>(nh);
+        int64_t *tiles = ws.alloc<int64_t>(expand_tile_words(H));
+        {
+            Timed t(p, GMAGNUS_K_CSC, s);
+            copy_i64(cursor, p->chat_ptr, nh, s);
+            expand_tiles(p->B, sl, H, tiles, s);
+        }
+        {
+            Timed t(p, GMAGNUS_K_EXPAND, s);
+            expand(p->B, sl, H, tiles, cursor, col_buf[0], val_buf[0], s);
+        }
+        ws.free(cursor);
+        ws.free(tiles);
+        p->info.kernel_launches[GMAGNUS_K_EXPAND] += 1;
+        add_bytes(p, GMAGNUS_K_EXPAND, 12.0 * H + 12.0 * sl.nnz + 8.0 * nh);
+    }
+    ws.free(sl.col_ptr);
+    ws.free(sl.slice_off);
+    ws.free(sl.slice_k);
+    ws.free(sl.row_h);
+    ws.free(sl.a_val);
+    (void)blen_total;
+
+    // ---- hierarchical multisplit
+    int64_t *origin_in = ws.alloc<int64_t>(nh);
+    hipLaunchKernelGGL(k_affine, dim3(grid_for(nh, 256, 65536)), dim3(256), 0, s, origin_in, nh, p->n_slots);
+    GM_CHECK_LAUNCH();
+    const int64_t *in_ptr = p->chat_ptr;
+    int64_t n_in = nh, elems = H;
+    int cur = 0;
+    int m_in_log2 = c_bits;
+    int64_t *counts = nullptr;
+    p->leaves.clear();
+    if (P.n_levels == 0) {
+        LeafLevel lv;
+        lv.set = LeafSet{p->chat_ptr, col_buf[0], val_buf[0], origin_in, 0, nh};
+        lv.width = 1 << c_bits;
+        lv.elems = H;
+        p->leaves.push_back(lv);
+    }
+    int64_t slots_per_chunk = p->n_slots;
+    for (int lvl = 0; lvl < P.n_levels; ++lvl) {
+        const int nc = P.v_chunks[lvl];
+        const bool last = lvl == P.n_levels - 1;
+        LevelGeom g{};
+        g.n_in = n_in;
+        g.elems = elems;
+        g.n_chunks = nc;
+        g.shift = m_in_log2 - ilog2(nc);
+        g.next_chunks = last ? 0 : P.v_chunks[lvl + 1];
+        g.next_shift = last ? 0 : g.shift - ilog2(g.next_chunks);
+        choose_tile(g, P.tau);
+        p->info.level_rows_in[lvl] = n_in;
+        p->info.level_elems_in[lvl] = elems;
+        slots_per_chunk /= nc;
+
+        const int64_t n_tiles = (elems + g.group_elems - 1) / g.group_elems;
+        int64_t *tile_row = ws.alloc<int64_t>(n_tiles);
+        const int64_t n_out = n_in * nc;
+        int64_t *sc = ws.alloc<int64_t>(std::max(partition_scratch_elems(n_out, 2), scan_scratch_elems(n_out)));
+        int64_t *x_map = ws.alloc<int64_t>(n_out);
+        int64_t *perm2 = ws.alloc<int64_t>(n_out);
+        int64_t *cb = ws.alloc<int64_t>(3);
+        int64_t *out_cnt = ws.alloc<int64_t>(n_out);
+        int64_t *origin_out = ws.alloc<int64_t>(n_out);
+        int64_t *out_ptr = ws.alloc<int64_t>(n_out + 1);
+        uint8_t *ccls = ws.alloc<uint8_t>(n_out);
+        tile_rows(g, in_ptr, tile_row, s);
+        if (lvl == 0) {
+            Timed t(p, GMAGNUS_K_HISTOGRAM, s);
+            counts = ws.alloc<int64_t>(n_out);
+            histogram(g, in_ptr, tile_row, col_buf[cur], counts, s);
+            p->info.kernel_launches[GMAGNUS_K_HISTOGRAM] += 1;
+            add_bytes(p, GMAGNUS_K_HISTOGRAM, 4.0 * elems + 8.0 * (n_in + 1) + 8.0 * n_out);
+        }
+        int64_t cbh[3];
+        {
+            Timed t(p, GMAGNUS_K_SETUP, s);
+            chunk_classes(counts, n_out, P.tau, last, ccls, s);
+            partition_u8(ccls, n_out, 2, perm2, x_map, cb, sc, s);
+            chunk_reorder(counts, x_map, n_out, nc, origin_in, slots_per_chunk, out_cnt, origin_out, s);
+            scan_i64(out_cnt, n_out, out_ptr, sc, s);
+            read_bins(cb, 2, cbh, s);
+        }
+        const int64_t nh_out = cbh[1];
+        p->info.level_heavy_out[lvl] = nh_out;
+        int64_t *next_counts = nullptr;
+        if (!last && nh_out > 0) {
+            next_counts = ws.alloc<int64_t>(nh_out * g.next_chunks);
+            fill<int64_t>(next_counts, 0, nh_out * g.next_chunks, s);
+        }
+        const int nxt = 1 - cur;
+        if (!col_buf[nxt]) {
+            col_buf[nxt] = ws.alloc<int32_t>(H);
+            val_buf[nxt] = ws.alloc<double>(H);
+        }
+        {
+            int64_t *cursor = ws.alloc<int64_t>(n_out);
+            copy_i64(cursor, out_ptr, n_out, s);
+            {
+                Timed t(p, GMAGNUS_K_MULTISPLIT, s);
+                multisplit(g, in_ptr, tile_row, col_buf[cur], val_buf[cur], x_map, cursor, col_buf[nxt],
+                           val_buf[nxt], nh_out, next_counts, s);
+            }
+            ws.free(cursor);
+            p->info.kernel_launches[GMAGNUS_K_MULTISPLIT] += 1;
+            add_bytes(p, GMAGNUS_K_MULTISPLIT, 24.0 * elems + 8.0 * (n_in + 1) + 8.0 * n_out);
+        }
+        p->info.levels_run = lvl + 1;
+        LeafLevel lv;
+        lv.set = LeafSet{out_ptr, col_buf[nxt], val_buf[nxt], origin_out, last ? 0 : nh_out, n_out};
+        lv.width = 1 << g.shift;
+        p->leaves.push_back(lv);
+        ws.free(tile_row);
+        ws.free(sc);
+        ws.free(x_map);
+        ws.free(perm2);
+        ws.free(cb);
+        ws.free(out_cnt);
+        ws.free(ccls);
+        ws.free(counts);
+        counts = next_counts;
+        if (last || nh_out == 0) break;
+        in_ptr = out_ptr;
+        n_in = nh_out;
+        elems = read_scalar(out_ptr + nh_out, s);
+        origin_in = origin_out;
+        m_in_log2 = g.shift;
+        cur = nxt;
+    }
+    if (counts) ws.free(counts);
+
+    // ---- final chunks: symbolic
+    p->slot = ws.alloc<int64_t>(nh * p->n_slots);
+    fill<int64_t>(p->slot, 0, nh * p->n_slots, s);
+    for (auto &lv : p->leaves) {
+        const int64_t nl = lv.set.hi - lv.set.lo;
+        if (nl <= 0) continue;
+        lv.leaf_nnz = ws.alloc<int64_t>(nl);
+        lv.items_sym = ws.alloc<int64_t>(nl);
+        lv.items_num = ws.alloc<int64_t>(nl);
+        int64_t *sc = ws.alloc<int64_t>(partition_scratch_elems(nl, LEAF_NBINS));
+        int64_t *bins = ws.alloc<int64_t>(LEAF_NBINS + 1);
+        uint8_t *lc = ws.alloc<uint8_t>(nl);
+        {
+            Timed t(p, GMAGNUS_K_SETUP, s);
+            fill<int64_t>(lv.leaf_nnz, 0, nl, s);
+            leaf_classes_sym(lv.set, P.tau, lc, s);
+            partition_u8(lc, nl, LEAF_NBINS, lv.items_sym, nullptr, bins, sc, s);
+            read_bins(bins, LEAF_NBINS, lv.bins_sym, s);
+        }
+        int64_t e0 = 0, e1 = 0;
+        GM_HIP(hipMemcpyAsync(&e0, lv.set.ptr + lv.set.lo, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+        GM_HIP(hipMemcpyAsync(&e1, lv.set.ptr + lv.set.hi, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+        GM_HIP(hipStreamSynchronize(s));
+        lv.elems = e1 - e0;
+        {
+            Timed t(p, GMAGNUS_K_CHUNK_SYM, s);
+            for (int b = LEAF_H0; b <= LEAF_DENSE; ++b) {
+                const int64_t cnt = lv.bins_sym[b + 1] - lv.bins_sym[b];
+                leaf_symbolic(lv.set, b, lv.items_sym + lv.bins_sym[b], cnt, lv.width, lv.leaf_nnz, p->slot, s);
+                if (cnt) p->info.kernel_launches[GMAGNUS_K_CHUNK_SYM] += 1;
+                if (b == LEAF_DENSE) p->info.n_leaves_dense += cnt;
+                else p->info.n_leaves_hash += cnt;
+            }
+            add_bytes(p, GMAGNUS_K_CHUNK_SYM, 4.0 * lv.elems + 16.0 * nl);
+        }
+        // numeric bins now, so the numeric phase needs no host round trip
+        {
+            Timed t(p, GMAGNUS_K_SETUP, s);
+            leaf_classes_num(lv.set, lv.leaf_nnz, P.tau, lc, s);
+            partition_u8(lc, nl, LEAF_NBINS, lv.items_num, nullptr, bins, sc, s);
+            read_bins(bins, LEAF_NBINS, lv.bins_num, s);
+        }
+        ws.free(sc);
+        ws.free(bins);
+        ws.free(lc);
+    }
+    {
+        Timed t(p, GMAGNUS_K_ROWPTR, s);
+        slot_scan(p->slot, nh, p->n_slots, p->heavy_rows, p->row_nnz, s);
+        add_bytes(p, GMAGNUS_K_ROWPTR, 16.0 * nh * p->n_slots);
+    }
+    // the other buffer (if only level 0 wrote into it, or never used) stays until numeric
+}
+
+void light_symbolic_all(gmagnus_plan_s *p) {
+    const hipStream_t s = p->s_light;
+    Timed t(p, GMAGNUS_K_LIGHT_SYM, s);
+    double ips = 0;
+    for (int b = LIGHT_W0; b < LIGHT_NBINS; ++b) {
+        const int64_t cnt = p->bins_sym[b + 1] - p->bins_sym[b];
+        light_symbolic(p->A, p->B, p->r0, b, p->perm + p->bins_sym[b], cnt, p->minc, p->maxc, p->row_nnz, s);
+        if (cnt) p->info.kernel_launches[GMAGNUS_K_LIGHT_SYM] += 1;
+    }
+    ips = (double)(p->products_total - p->products_heavy);
+    add_bytes(p, GMAGNUS_K_LIGHT_SYM, 4.0 * ips);
+}
+
+void do_symbolic(gmagnus_plan_s *p, int64_t *c_row_ptr, int64_t *c_nnz) {
+    GM_REQUIRE(c_row_ptr != nullptr && c_nnz != nullptr, GMAGNUS_ERROR_INVALID_VALUE, "NULL output");
+    GM_REQUIRE(!p->symbolic_done, GMAGNUS_ERROR_NOT_READY, "symbolic already ran for this plan");
+    Workspace &ws = *p->ws;
+    const int64_t n = p->n;
+    if (n == 0) {
+        fill<int64_t>(c_row_ptr, 0, 1, p->stream);
+        GM_HIP(hipStreamSynchronize(p->stream));
+        *c_nnz = 0;
+        p->symbolic_done = true;
+        return;
+    }
+    p->row_nnz = ws.alloc<int64_t>(n);
+    fill<int64_t>(p->row_nnz, 0, n, p->stream);
+    hipEvent_t fork, jh, jl;
+    GM_HIP(hipEventCreateWithFlags(&fork, hipEventDisableTiming));
+    GM_HIP(hipEventCreateWithFlags(&jh, hipEventDisableTiming));
+    GM_HIP(hipEventCreateWithFlags(&jl, hipEventDisableTiming));
+    struct EvGuard {
+        hipEvent_t a, b, c;
+        ~EvGuard() {
+            (void)hipEventDestroy(a);
+            (void)hipEventDestroy(b);
+            (void)hipEventDestroy(c);
+        }
+    } guard{fork, jh, jl};
+    GM_HIP(hipEventRecord(fork, p->stream));
+    if (p->s_light != p->stream) GM_HIP(hipStreamWaitEvent(p->s_light, fork, 0));
+    if (p->s_heavy != p->stream) GM_HIP(hipStreamWaitEvent(p->s_heavy, fork, 0));
+    // light work is enqueued first so it overlaps the heavy path's host round trips
+    light_symbolic_all(p);
+    if (p->n_heavy > 0) heavy_symbolic(p);
+    GM_HIP(hipEventRecord(jl, p->s_light));
+    GM_HIP(hipEventRecord(jh, p->s_heavy));
+    GM_HIP(hipStreamWaitEvent(p->stream, jl, 0));
+    GM_HIP(hipStreamWaitEvent(p->stream, jh, 0));
+    {
+        Timed t(p, GMAGNUS_K_ROWPTR, p->stream);
+        int64_t *sc = ws.alloc<int64_t>(scan_scratch_elems(n));
+        scan_i64(p->row_nnz, n, c_row_ptr, sc, p->stream);
+        p->c_nnz = read_scalar(c_row_ptr + n, p->stream);
+        if (p->n_heavy > 0) {
+            int64_t *hs = ws.alloc<int64_t>(p->n_heavy + 1);
+            scan_gather_i64(p->row_nnz, p->heavy_rows, p->n_heavy, hs, sc, p->stream);
+            p->info.c_nnz_heavy = read_scalar(hs + p->n_heavy, p->stream);
+            ws.free(hs);
+        }
+        ws.free(sc);
+        add_bytes(p, GMAGNUS_K_ROWPTR, 16.0 * n);
+    }
+    // numeric bins of the light rows
+    {
+        Timed t(p, GMAGNUS_K_SETUP, p->stream);
+        const bool window = (p->opts.flags & GMAGNUS_FLAG_NO_WINDOW) == 0;
+        uint8_t *cls = ws.alloc<uint8_t>(n);
+        int64_t *bins = ws.alloc<int64_t>(LIGHT_NBINS + 1);
+        int64_t *sc = ws.alloc<int64_t>(partition_scratch_elems(n, LIGHT_NBINS));
+        p->perm_num = ws.alloc<int64_t>(n);
+        light_classes_num(p->ip, p->row_nnz, p->minc, p->maxc, n, p->params.tau, window, cls, p->stream);
+        partition_u8(cls, n, LIGHT_NBINS, p->perm_num, nullptr, bins, sc, p->stream);
+        read_bins(bins, LIGHT_NBINS, p->bins_num, p->stream);
+        ws.free(cls);
+        ws.free(bins);
+        ws.free(sc);
+    }
+    *c_nnz = p->c_nnz;
+    p->info.c_nnz = p->c_nnz;
+    p->symbolic_done = true;
+}
+
+void do_numeric(gmagnus_plan_s *p, const int64_t *c_row_ptr, int32_t *c_col, double *c_val) {
+    GM_REQUIRE(p->symbolic_done, GMAGNUS_ERROR_NOT_READY, "numeric called before symbolic");
+    GM_REQUIRE(c_row_ptr != nullptr, GMAGNUS_ERROR_INVALID_VALUE, "NULL c_row_ptr");
+    GM_REQUIRE(p->c_nnz == 0 || (c_col && c_val), GMAGNUS_ERROR_INVALID_VALUE, "NULL C output arrays");
+    if (p->n == 0 || p->c_nnz == 0) return;
+    hipEvent_t fork, jh, jl;
+    GM_HIP(hipEventCreateWithFlags(&fork, hipEventDisableTiming));
+    GM_HIP(hipEventCreateWithFlags(&jh, hipEventDisableTiming));
+    GM_HIP(hipEventCreateWithFlags(&jl, hipEventDisableTiming));
+    struct EvGuard {
+        hipEvent_t a, b, c;
+        ~EvGuard() {
+            (void)hipEventDestroy(a);
+            (void)hipEventDestroy(b);
+            (void)hipEventDestroy(c);
+        }
+    } guard{fork, jh, jl};
+    GM_HIP(hipEventRecord(fork, p->stream));
+    if (p->s_light != p->stream) GM_HIP(hipStreamWaitEvent(p->s_light, fork, 0));
+    if (p->s_heavy != p->stream) GM_HIP(hipStreamWaitEvent(p->s_heavy, fork, 0));
+    {
+        const hipStream_t s = p->s_heavy;
+        Timed t(p, GMAGNUS_K_CHUNK_NUM, s);
+        for (auto &lv : p->leaves) {
+            for (int b = LEAF_H0; b <= LEAF_DENSE; ++b) {
+                const int64_t cnt = lv.bins_num[b + 1] - lv.bins_num[b];
+                leaf_numeric(lv.set, b, lv.items_num + lv.bins_num[b], cnt, lv.width, lv.leaf_nnz, p->n_slots_log2,
+                             p->heavy_rows, c_row_ptr, p->slot, p->slot_width_log2, c_col, c_val, p->err, s);
+                if (cnt) p->info.kernel_launches[GMAGNUS_K_CHUNK_NUM] += 1;
+            }
+            add_bytes(p, GMAGNUS_K_CHUNK_NUM, 12.0 * lv.elems);
+        }
+    }
+    {
+        const hipStream_t s = p->s_light;
+        Timed t(p, GMAGNUS_K_LIGHT_NUM, s);
+        for (int b = LIGHT_W0; b < LIGHT_NBINS; ++b) {
+            const int64_t cnt = p->bins_num[b + 1] - p->bins_num[b];
+            light_numeric(p->A, p->B, p->r0, b, p->perm_num + p->bins_num[b], cnt, p->minc, p->maxc, c_row_ptr, c_col,
+                          c_val, p->err, s);
+            if (cnt) p->info.kernel_launches[GMAGNUS_K_LIGHT_NUM] += 1;
+        }
+        add_bytes(p, GMAGNUS_K_LIGHT_NUM, 12.0 * (double)(p->products_total - p->products_heavy));
+    }
+    GM_HIP(hipEventRecord(jl, p->s_light));
+    GM_HIP(hipEventRecord(jh, p->s_heavy));
+    GM_HIP(hipStreamWaitEvent(p->stream, jl, 0));
+    GM_HIP(hipStreamWaitEvent(p->stream, jh, 0));
+    // output bytes of C, split by the rows they belong to
+    add_bytes(p, GMAGNUS_K_CHUNK_NUM, 12.0 * (double)p->info.c_nnz_heavy);
+    add_bytes(p, GMAGNUS_K_LIGHT_NUM, 12.0 * (double)(p->c_nnz - p->info.c_nnz_heavy));
+}
+
+template <class F>
+gmagnus_status_t guarded(F &&f) {
+    try {
+        f();
+        return GMAGNUS_SUCCESS;
+    } catch (const Error &e) {
+        set_last_error(e.msg);
+        return e.status;
+    } catch (const std::bad_alloc &) {
+        set_last_error("host allocation failed");
+        return GMAGNUS_ERROR_OUT_OF_MEMORY;
+    } catch (...) {
+        set_last_error("unexpected exception");
+        return GMAGNUS_ERROR_HIP;
+    }
+}
+
+}  // namespace
+
+// =================================================================== C ABI
+extern "C" {
+
+void gmagnus_options_init(gmagnus_options_t *opts) {
+    if (!opts) return;
+    std::memset(opts, 0, sizeof(*opts));
+    opts->struct_size = sizeof(gmagnus_options_t);
+}
+
+gmagnus_status_t gmagnus_get_params(int64_t c_m, int64_t lds_bytes, const gmagnus_options_t *opts,
+                                    gmagnus_params_t *out) {
+    return guarded([&] {
+        GM_REQUIRE(out != nullptr, GMAGNUS_ERROR_INVALID_VALUE, "NULL output");
+        GM_REQUIRE(!opts || opts->struct_size == sizeof(gmagnus_options_t), GMAGNUS_ERROR_INVALID_VALUE,
+                   "options.struct_size mismatch");
+        compute_params(c_m, lds_bytes, opts, out);
+    });
+}
+
+gmagnus_status_t gmagnus_plan(gmagnus_plan_t *out, const gmagnus_csr_t *A, const gmagnus_csr_t *B,
+                              const gmagnus_options_t *opts, void *hip_stream) {
+    if (!out) {
+        set_last_error("NULL plan output");
+        return GMAGNUS_ERROR_INVALID_VALUE;
+    }
+    *out = nullptr;
+    gmagnus_plan_s *p = nullptr;
+    gmagnus_status_t st = guarded([&] {
+        p = new gmagnus_plan_s();
+        do_plan(p, A, B, opts, (hipStream_t)hip_stream);
+    });
+    if (st != GMAGNUS_SUCCESS) {
+        delete p;
+        return st;
+    }
+    *out = p;
+    return st;
+}
+
+gmagnus_status_t gmagnus_spgemm_symbolic(gmagnus_plan_t plan, int64_t *c_row_ptr, int64_t *c_nnz) {
+    if (!plan) {
+        set_last_error("NULL plan");
+        return GMAGNUS_ERROR_INVALID_VALUE;
+    }
+    return guarded([&] { do_symbolic(plan, c_row_ptr, c_nnz); });
+}
+
+gmagnus_status_t gmagnus_spgemm_numeric(gmagnus_plan_t plan, const int64_t *c_row_ptr, int32_t *c_col_idx,
+                                        double *c_val) {
+    if (!plan) {
+        set_last_error("NULL plan");
+        return GMAGNUS_ERROR_INVALID_VALUE;
+    }
+    return guarded([&] { do_numeric(plan, c_row_ptr, c_col_idx, c_val); });
+}
+
+gmagnus_status_t gmagnus_plan_info(gmagnus_plan_t plan, gmagnus_plan_info_t *out) {
+    if (!plan || !out) {
+        set_last_error("NULL plan or output");
+        return GMAGNUS_ERROR_INVALID_VALUE;
+    }
+    return guarded([&] {
+        if (plan->timing || plan->symbolic_done) {
+            GM_HIP(hipStreamSynchronize(plan->stream));
+            if (plan->s_heavy != plan->stream) GM_HIP(hipStreamSynchronize(plan->s_heavy));
+            if (plan->s_light != plan->stream) GM_HIP(hipStreamSynchronize(plan->s_light));
+        }
+        if (plan->timing) {
+            for (auto &t : plan->timers) {
+                float ms = 0;
+                GM_HIP(hipEventElapsedTime(&ms, t.a, t.b));
+                plan->info.kernel_ms[t.cls] += ms;
+                (void)hipEventDestroy(t.a);
+                (void)hipEventDestroy(t.b);
+            }
+            plan->timers.clear();
+        }
+        if (plan->err) {
+            int32_t f = 0;
+            GM_HIP(hipMemcpy(&f, plan->err, sizeof(f), hipMemcpyDeviceToHost));
+            plan->info.check_flags = f;
+        }
+        *out = plan->info;
+    });
+}
+
+void gmagnus_plan_destroy(gmagnus_plan_t plan) { delete plan; }
+
+gmagnus_status_t gmagnus_row_products(const gmagnus_csr_t *A, const gmagnus_csr_t *B, int64_t *ip, void *hip_stream) {
+    return guarded([&] {
+        check_csr_desc(A, "A");
+        check_csr_desc(B, "B");
+        GM_REQUIRE(A->n_cols == B->n_rows, GMAGNUS_ERROR_INVALID_VALUE, "A.n_cols must equal B.n_rows");
+        GM_REQUIRE(ip != nullptr || A->n_rows == 0, GMAGNUS_ERROR_INVALID_VALUE, "NULL ip");
+        if (A->n_rows == 0) return;
+        hipStream_t s = (hipStream_t)hip_stream;
+        Workspace ws(nullptr, s);
+        int32_t *mn = ws.alloc<int32_t>(A->n_rows), *mx = ws.alloc<int32_t>(A->n_rows);
+        row_products(to_csr(A), to_csr(B), 0, A->n_rows, A->nnz, ip, mn, mx, s);
+        GM_HIP(hipStreamSynchronize(s));
+    });
+}
+
+gmagnus_status_t gmagnus_split_panels(const gmagnus_csr_t *A, const gmagnus_csr_t *B, int64_t max_products,
+                                      int64_t *bounds, int64_t max_panels, int64_t *n_panels, void *hip_stream) {
+    return guarded([&] {
+        check_csr_desc(A, "A");
+        check_csr_desc(B, "B");
+        GM_REQUIRE(A->n_cols == B->n_rows, GMAGNUS_ERROR_INVALID_VALUE, "A.n_cols must equal B.n_rows");
+        GM_REQUIRE(bounds && n_panels && max_panels >= 1 && max_products >= 1, GMAGNUS_ERROR_INVALID_VALUE,
+                   "bad panel arguments");
+        const int64_t n = A->n_rows;
+        hipStream_t s = (hipStream_t)hip_stream;
+        std::vector<int64_t> pre(n + 1, 0);
+        if (n > 0) {
+            Workspace ws(nullptr, s);
+            int64_t *ip = ws.alloc<int64_t>(n), *sc = ws.alloc<int64_t>(n + 1);
+            int64_t *scratch = ws.alloc<int64_t>(scan_scratch_elems(n));
+            int32_t *mn = ws.alloc<int32_t>(n), *mx = ws.alloc<int32_t>(n);
+            row_products(to_csr(A), to_csr(B), 0, n, A->nnz, ip, mn, mx, s);
+            scan_i64(ip, n, sc, scratch, s);
+            GM_HIP(hipMemcpyAsync(pre.data(), sc, sizeof(int64_t) * (n + 1), hipMemcpyDeviceToHost, s));
+            GM_HIP(hipStreamSynchronize(s));
+        }
+        int64_t cnt = 0, r = 0;
+        bounds[0] = 0;
+        while (r < n) {
+            // furthest end e > r with pre[e] - pre[r] <= max_products (at least one row)
+            int64_t e = std::upper_bound(pre.begin() + r + 1, pre.end(), pre[r] + max_products) - pre.begin() - 1;
+            if (e <= r) e = r + 1;
+            GM_REQUIRE(cnt < max_panels, GMAGNUS_ERROR_INVALID_VALUE, "more panels needed than max_panels");
+            bounds[++cnt] = e;
+            r = e;
+        }
+        *n_panels = cnt;
+    });
+}
+
+void gmagnus_release_cache(void) { cache_release(); }
+
+const char *gmagnus_last_error(void) { return g_last_error.c_str(); }
+
+const char *gmagnus_status_string(gmagnus_status_t status) {
+    switch (status) {
+    case GMAGNUS_SUCCESS: return "GMAGNUS_SUCCESS";
+    case GMAGNUS_ERROR_INVALID_VALUE: return "GMAGNUS_ERROR_INVALID_VALUE";
+    case GMAGNUS_ERROR_INVALID_CSR: return "GMAGNUS_ERROR_INVALID_CSR";
+    case GMAGNUS_ERROR_OUT_OF_MEMORY: return "GMAGNUS_ERROR_OUT_OF_MEMORY";
+    case GMAGNUS_ERROR_NOT_READY: return "GMAGNUS_ERROR_NOT_READY";
+    case GMAGNUS_ERROR_HIP: return "GMAGNUS_ERROR_HIP";
+    case GMAGNUS_ERROR_UNSUPPORTED: return "GMAGNUS_ERROR_UNSUPPORTED";
+    }
+    return "GMAGNUS_ERROR_UNKNOWN";
+}
+
+}  // extern "C"

@@ -1,0 +1,208 @@
+// Device-wide primitives: three-pass exclusive scan of int64 values and a
+// stable multi-class partition built on it (the flagged partitions of
+// Algorithm 3: light/heavy rows, slices, heavy/light chunks, bins).
+#include "host.hpp"
+
+namespace gm {
+
+namespace {
+
+constexpr int SCAN_BLOCK = 256;
+constexpr int SCAN_ITEMS = 8;
+constexpr int64_t SCAN_TILE = SCAN_BLOCK * SCAN_ITEMS;
+
+struct PlainIn {
+    const int64_t *p;
+    GM_DEV int64_t operator()(int64_t i) const { return p[i]; }
+};
+struct GatherIn {
+    const int64_t *p;
+    const int64_t *idx;
+    GM_DEV int64_t operator()(int64_t i) const { return p[idx[i]]; }
+};
+
+template <class In>
+__global__ __launch_bounds__(SCAN_BLOCK) void k_scan_reduce(In in, int64_t n, int64_t *partial) {
+    __shared__ int64_t sm[SCAN_BLOCK / GM_WAVE];
+    const int64_t base = blockIdx.x * SCAN_TILE + threadIdx.x * SCAN_ITEMS;
+    int64_t s = 0;
+#pragma unroll
+    for (int j = 0; j < SCAN_ITEMS; ++j)
+        if (base + j < n) s += in(base + j);
+    s = block_reduce_sum<SCAN_BLOCK>(s, sm);
+    if (threadIdx.x == 0) partial[blockIdx.x] = s;
+}
+
+// One block scans the tile sums in place (exclusive) and writes the total
+// after the last tile sum.
+__global__ __launch_bounds__(1024) void k_scan_partials(int64_t *partial, int64_t n_tiles) {
+    __shared__ int64_t sm[1024 / GM_WAVE];
+    __shared__ int64_t carry;
+    if (threadIdx.x == 0) carry = 0;
+    __syncthreads();
+    for (int64_t b = 0; b < n_tiles; b += 1024) {
+        const int64_t i = b + threadIdx.x;
+        int64_t x = i < n_tiles ? partial[i] : 0;
+        int64_t tot;
+        int64_t ex = block_excl_scan<1024>(x, sm, &tot);
+        const int64_t c = carry;
+        if (i < n_tiles) partial[i] = c + ex;
+        __syncthreads();
+        if (threadIdx.x == 0) carry = c + tot;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) partial[n_tiles] = carry;
+}
+
+template <class In>
+__global__ __launch_bounds__(SCAN_BLOCK) void k_scan_apply(In in, int64_t n, const int64_t *partial, int64_t *out) {
+    __shared__ int64_t sm[SCAN_BLOCK / GM_WAVE];
+    const int64_t base = blockIdx.x * SCAN_TILE + threadIdx.x * SCAN_ITEMS;
+    int64_t v[SCAN_ITEMS];
+    int64_t s = 0;
+#pragma unroll
+    for (int j = 0; j < SCAN_ITEMS; ++j) {
+        v[j] = base + j < n ? in(base + j) : 0;
+        s += v[j];
+    }
+    int64_t run = partial[blockIdx.x] + block_excl_scan<SCAN_BLOCK>(s, sm);
+#pragma unroll
+    for (int j = 0; j < SCAN_ITEMS; ++j) {
+        if (base + j < n) out[base + j] = run;
+        run += v[j];
+    }
+    if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) out[n] = partial[gridDim.x];
+}
+
+template <class In>
+void scan_impl(In in, int64_t n, int64_t *out, int64_t *scratch, hipStream_t s) {
+    if (n <= 0) {
+        fill<int64_t>(out, 0, 1, s);
+        return;
+    }
+    const int64_t tiles = (n + SCAN_TILE - 1) / SCAN_TILE;
+    hipLaunchKernelGGL(k_scan_reduce<In>, dim3((unsigned)tiles), dim3(SCAN_BLOCK), 0, s, in, n, scratch);
+    GM_CHECK_LAUNCH();
+    hipLaunchKernelGGL(k_scan_partials, dim3(1), dim3(1024), 0, s, scratch, tiles);
+    GM_CHECK_LAUNCH();
+    hipLaunchKernelGGL(k_scan_apply<In>, dim3((unsigned)tiles), dim3(SCAN_BLOCK), 0, s, in, n, scratch, out);
+    GM_CHECK_LAUNCH();
+}
+
+// ---------------------------------------------------------------- partition
+constexpr int PART_BLOCK = 256;
+constexpr int PART_ITEMS = 16;
+constexpr int64_t PART_TILE = PART_BLOCK * PART_ITEMS;
+constexpr int PART_MAX_CLASSES = 16;
+
+__global__ __launch_bounds__(PART_BLOCK) void k_part_count(const uint8_t *cls, int64_t n, int nc, int64_t n_tiles,
+                                                           int64_t *tile_count) {
+    __shared__ int cnt[PART_MAX_CLASSES];
+    if (threadIdx.x < PART_MAX_CLASSES) cnt[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t base = blockIdx.x * PART_TILE;
+    for (int j = 0; j < PART_ITEMS; ++j) {
+        const int64_t i = base + j * PART_BLOCK + threadIdx.x;
+        if (i < n) atomicAdd(&cnt[cls[i]], 1);
+    }
+    __syncthreads();
+    if (threadIdx.x < nc) tile_count[threadIdx.x * n_tiles + blockIdx.x] = cnt[threadIdx.x];
+}
+
+// Each thread owns PART_ITEMS consecutive items; per-class counts of the
+// threads are scanned in thread order (four 16-bit class counters per int64
+// word), so positions are stable in item order.
+__global__ __launch_bounds__(PART_BLOCK) void k_part_scatter(const uint8_t *cls, int64_t n, int nc, int64_t n_tiles,
+                                                             const int64_t *tile_off, int64_t *perm, int64_t *inv) {
+    __shared__ int64_t sm[PART_BLOCK / GM_WAVE];
+    __shared__ int64_t base_off[PART_MAX_CLASSES];
+    const int64_t base = blockIdx.x * PART_TILE + (int64_t)threadIdx.x * PART_ITEMS;
+    uint8_t c[PART_ITEMS];
+#pragma unroll
+    for (int j = 0; j < PART_ITEMS; ++j) c[j] = base + j < n ? cls[base + j] : 0xFF;
+    if (threadIdx.x < nc) base_off[threadIdx.x] = tile_off[threadIdx.x * n_tiles + blockIdx.x];
+    int prefix[PART_MAX_CLASSES];
+#pragma unroll
+    for (int g = 0; g < PART_MAX_CLASSES / 4; ++g) {
+        if (4 * g >= nc) {  // nc is uniform over the block
+#pragma unroll
+            for (int q = 0; q < 4; ++q) prefix[4 * g + q] = 0;
+            continue;
+        }
+        uint64_t packed = 0;
+#pragma unroll
+        for (int j = 0; j < PART_ITEMS; ++j) {
+            const int q = (int)c[j] - 4 * g;
+            if (c[j] != 0xFF && q >= 0 && q < 4) packed += uint64_t(1) << (16 * q);
+        }
+        const uint64_t ex = (uint64_t)block_excl_scan<PART_BLOCK>((int64_t)packed, sm);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) prefix[4 * g + q] = (int)((ex >> (16 * q)) & 0xFFFF);
+    }
+    __syncthreads();
+    int run[PART_MAX_CLASSES];
+#pragma unroll
+    for (int q = 0; q < PART_MAX_CLASSES; ++q) run[q] = 0;
+#pragma unroll
+    for (int j = 0; j < PART_ITEMS; ++j) {
+        if (c[j] == 0xFF) continue;
+        int r = 0, p = 0;
+#pragma unroll
+        for (int q = 0; q < PART_MAX_CLASSES; ++q)
+            if (q == c[j]) {
+                r = run[q]++;
+                p = prefix[q];
+            }
+        const int64_t pos = base_off[c[j]] + p + r;
+        perm[pos] = base + j;
+        if (inv) inv[base + j] = pos;
+    }
+}
+
+__global__ void k_class_starts(const int64_t *tile_off, int nc, int64_t n_tiles, int64_t *class_start) {
+    const int c = threadIdx.x;
+    if (c <= nc) class_start[c] = tile_off[(int64_t)c * n_tiles];
+}
+
+}  // namespace
+
+int64_t scan_scratch_elems(int64_t n) { return (n + SCAN_TILE - 1) / SCAN_TILE + 2; }
+
+void scan_i64(const int64_t *in, int64_t n, int64_t *out, int64_t *scratch, hipStream_t s) {
+    scan_impl(PlainIn{in}, n, out, scratch, s);
+}
+
+void scan_gather_i64(const int64_t *in, const int64_t *idx, int64_t n, int64_t *out, int64_t *scratch,
+                     hipStream_t s) {
+    scan_impl(GatherIn{in, idx}, n, out, scratch, s);
+}
+
+int64_t partition_scratch_elems(int64_t n, int nc) {
+    const int64_t tiles = (n + PART_TILE - 1) / PART_TILE;
+    const int64_t m = tiles * nc;
+    return m + (m + 1) + scan_scratch_elems(m);
+}
+
+void partition_u8(const uint8_t *cls, int64_t n, int nc, int64_t *perm, int64_t *inv, int64_t *class_start,
+                  int64_t *scratch, hipStream_t s) {
+    GM_REQUIRE(nc >= 1 && nc <= PART_MAX_CLASSES, GMAGNUS_ERROR_INVALID_VALUE, "partition: too many classes");
+    const int64_t tiles = (n + PART_TILE - 1) / PART_TILE;
+    if (n <= 0) {
+        fill<int64_t>(class_start, 0, nc + 1, s);
+        return;
+    }
+    const int64_t m = tiles * nc;
+    int64_t *tile_count = scratch;
+    int64_t *tile_off = scratch + m;
+    int64_t *sc = tile_off + m + 1;
+    hipLaunchKernelGGL(k_part_count, dim3((unsigned)tiles), dim3(PART_BLOCK), 0, s, cls, n, nc, tiles, tile_count);
+    GM_CHECK_LAUNCH();
+    scan_i64(tile_count, m, tile_off, sc, s);
+    hipLaunchKernelGGL(k_part_scatter, dim3((unsigned)tiles), dim3(PART_BLOCK), 0, s, cls, n, nc, tiles, tile_off,
+                       perm, inv);
+    GM_CHECK_LAUNCH();
+    hipLaunchKernelGGL(k_class_starts, dim3(1), dim3(64), 0, s, tile_off, nc, tiles, class_start);
+    GM_CHECK_LAUNCH();
+}
+
+}  // namespace gm

@@ -1,0 +1,226 @@
+// Setup-phase kernels (Algorithm 3): per-row product counts (InterOffsets),
+// CSR validation, and the masked CSR->CSC conversion of the heavy rows with
+// its slice offsets (Section III-B).
+#include "host.hpp"
+
+namespace gm {
+
+namespace {
+
+constexpr int FLAT_BLOCK = 256;
+constexpr int FLAT_ITEMS = 8;  // consecutive entries per thread
+
+// InterOffsets for rows [r0, r1): every thread walks FLAT_ITEMS consecutive
+// nonzeros of A, adding nnz(B[k,:]) to its current row and tracking the
+// smallest first column and largest last column of the B rows it touches
+// (the row's column span, used to pick a dense window for light rows).
+// A row split across threads is merged with atomics.
+__global__ __launch_bounds__(FLAT_BLOCK) void k_row_products(Csr A, Csr B, int64_t r0, int64_t r1, int64_t *ip,
+                                                             int32_t *minc, int32_t *maxc) {
+    const int64_t e_begin = A.rp[r0], e_end = A.rp[r1];
+    const int64_t e0 = e_begin + (blockIdx.x * (int64_t)FLAT_BLOCK + threadIdx.x) * FLAT_ITEMS;
+    if (e0 >= e_end) return;
+    const int64_t e1 = e0 + FLAT_ITEMS < e_end ? e0 + FLAT_ITEMS : e_end;
+    int64_t row = find_row(A.rp, r0, r1 + 1, e0);
+    int64_t row_end = A.rp[row + 1];
+    int64_t acc = 0;
+    int32_t lo = INT32_MAX, hi = -1;
+    for (int64_t e = e0; e < e1; ++e) {
+        while (e >= row_end) {  // flush and move to the next nonempty row
+            if (acc) atomicAdd((unsigned long long *)&ip[row - r0], (unsigned long long)acc);
+            if (hi >= 0) {
+                atomicMin(&minc[row - r0], lo);
+                atomicMax(&maxc[row - r0], hi);
+            }
+            acc = 0;
+            lo = INT32_MAX;
+            hi = -1;
+            ++row;
+            row_end = A.rp[row + 1];
+        }
+        const int32_t k = A.ci[e];
+        const int64_t b0 = B.rp[k], b1 = B.rp[k + 1];
+        if (b1 > b0) {
+            acc += b1 - b0;
+            const int32_t f = B.ci[b0], l = B.ci[b1 - 1];
+            lo = f < lo ? f : lo;
+            hi = l > hi ? l : hi;
+        }
+    }
+    if (acc) atomicAdd((unsigned long long *)&ip[row - r0], (unsigned long long)acc);
+    if (hi >= 0) {
+        atomicMin(&minc[row - r0], lo);
+        atomicMax(&maxc[row - r0], hi);
+    }
+}
+
+__global__ void k_validate_rows(Csr M, int32_t *flag) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < M.n_rows;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t s = M.rp[i], e = M.rp[i + 1];
+        if (i == 0 && s != 0) atomicOr(flag, 1);
+        if (i == M.n_rows - 1 && e != M.nnz) atomicOr(flag, 2);
+        if (e < s) {
+            atomicOr(flag, 4);
+            continue;
+        }
+        int32_t prev = -1;
+        for (int64_t p = s; p < e && p < M.nnz; ++p) {
+            const int32_t c = M.ci[p];
+            if (c < 0 || c >= M.n_cols) atomicOr(flag, 8);
+            if (c <= prev) atomicOr(flag, 16);
+            prev = c;
+        }
+    }
+}
+
+// Visits the nonzeros of the heavy rows of A in the flattened order given
+// by a_heavy_ptr (exclusive scan of the heavy rows' lengths); calls
+// f(h, j) with the heavy index h and the position j in A.
+template <class F>
+GM_DEV void for_heavy_entries(const Csr &A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
+                              const int64_t *a_heavy_ptr, int64_t total, F f) {
+    const int64_t e0 = (blockIdx.x * (int64_t)FLAT_BLOCK + threadIdx.x) * FLAT_ITEMS;
+    if (e0 >= total) return;
+    const int64_t e1 = e0 + FLAT_ITEMS < total ? e0 + FLAT_ITEMS : total;
+    int64_t h = find_row(a_heavy_ptr, 0, n_heavy + 1, e0);
+    int64_t h_end = a_heavy_ptr[h + 1];
+    int64_t a_base = A.rp[r0 + heavy_rows[h]] - a_heavy_ptr[h];
+    for (int64_t e = e0; e < e1; ++e) {
+        while (e >= h_end) {
+            ++h;
+            h_end = a_heavy_ptr[h + 1];
+            a_base = A.rp[r0 + heavy_rows[h]] - a_heavy_ptr[h];
+        }
+        f(h, a_base + e);
+    }
+}
+
+__global__ __launch_bounds__(FLAT_BLOCK) void k_csc_count(Csr A, Csr B, const int64_t *heavy_rows, int64_t n_heavy,
+                                                          int64_t r0, const int64_t *a_heavy_ptr, int64_t total,
+                                                          int64_t *colcnt) {
+    for_heavy_entries(A, heavy_rows, n_heavy, r0, a_heavy_ptr, total, [&](int64_t, int64_t j) {
+        const int32_t k = A.ci[j];
+        if (B.rp[k + 1] > B.rp[k]) atomicAdd((unsigned long long *)&colcnt[k], 1ull);
+    });
+}
+
+__global__ void k_slice_flags(Csr B, const int64_t *colcnt, int64_t n_k, uint8_t *cls) {
+    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < n_k; k += (int64_t)gridDim.x * blockDim.x)
+        cls[k] = (colcnt[k] > 0 && B.rp[k + 1] > B.rp[k]) ? 0 : 1;
+}
+
+__global__ void k_slice_build(Csr B, const int64_t *colcnt, const int64_t *perm, int64_t n_slices, int32_t *slice_k,
+                              int64_t *cnt_out, int64_t *ip_out, int32_t *k_to_slice) {
+    for (int64_t s = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; s < n_slices;
+         s += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t k = perm[s];
+        slice_k[s] = (int32_t)k;
+        cnt_out[s] = colcnt[k];
+        ip_out[s] = colcnt[k] * (B.rp[k + 1] - B.rp[k]);
+        k_to_slice[k] = (int32_t)s;
+    }
+}
+
+__global__ __launch_bounds__(FLAT_BLOCK) void k_csc_fill(Csr A, const int64_t *heavy_rows, int64_t n_heavy,
+                                                         int64_t r0, const int64_t *a_heavy_ptr, int64_t total,
+                                                         const int32_t *k_to_slice, const int64_t *col_ptr,
+                                                         int64_t *fill_cursor, int32_t *row_h, double *a_val) {
+    for_heavy_entries(A, heavy_rows, n_heavy, r0, a_heavy_ptr, total, [&](int64_t h, int64_t j) {
+        const int32_t s = k_to_slice[A.ci[j]];
+        if (s < 0) return;
+        const int64_t pos =
+            col_ptr[s] + (int64_t)atomicAdd((unsigned long long *)&fill_cursor[s], 1ull);
+        row_h[pos] = (int32_t)h;
+        a_val[pos] = A.v[j];
+    });
+}
+
+__global__ void k_gather_row_len(const int64_t *row_ptr, const int64_t *rows, int64_t n, int64_t r0, int64_t *out) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t r = r0 + rows[i];
+        out[i] = row_ptr[r + 1] - row_ptr[r];
+    }
+}
+
+__global__ void k_gather_i64(const int64_t *src, const int64_t *idx, int64_t n, int64_t *out) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        out[i] = src[idx[i]];
+}
+
+unsigned flat_grid(int64_t total) {
+    const int64_t per = (int64_t)FLAT_BLOCK * FLAT_ITEMS;
+    int64_t g = (total + per - 1) / per;
+    return (unsigned)(g < 1 ? 1 : g);
+}
+
+}  // namespace
+
+void row_products(const Csr &A, const Csr &B, int64_t r0, int64_t r1, int64_t panel_nnz, int64_t *ip, int32_t *minc,
+                  int32_t *maxc, hipStream_t s) {
+    const int64_t n = r1 - r0;
+    if (n <= 0) return;
+    fill<int64_t>(ip, 0, n, s);
+    fill<int32_t>(minc, INT32_MAX, n, s);
+    fill<int32_t>(maxc, -1, n, s);
+    if (panel_nnz <= 0) return;
+    hipLaunchKernelGGL(k_row_products, dim3(flat_grid(panel_nnz)), dim3(FLAT_BLOCK), 0, s, A, B, r0, r1, ip, minc,
+                       maxc);
+    GM_CHECK_LAUNCH();
+}
+
+void validate_csr(const Csr &M, int32_t *flag, hipStream_t s) {
+    fill<int32_t>(flag, 0, 1, s);
+    if (M.n_rows <= 0) return;
+    hipLaunchKernelGGL(k_validate_rows, dim3(grid_for(M.n_rows, 256, 8192)), dim3(256), 0, s, M, flag);
+    GM_CHECK_LAUNCH();
+}
+
+void csc_count(const Csr &A, const Csr &B, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
+               const int64_t *a_heavy_ptr, int64_t nnz_heavy_all, int64_t *colcnt, hipStream_t s) {
+    fill<int64_t>(colcnt, 0, A.n_cols, s);
+    if (n_heavy <= 0 || nnz_heavy_all <= 0) return;
+    hipLaunchKernelGGL(k_csc_count, dim3(flat_grid(nnz_heavy_all)), dim3(FLAT_BLOCK), 0, s, A, B, heavy_rows, n_heavy,
+                       r0, a_heavy_ptr, nnz_heavy_all, colcnt);
+    GM_CHECK_LAUNCH();
+}
+
+void slice_flags(const Csr &B, const int64_t *colcnt, int64_t n_k, uint8_t *cls, hipStream_t s) {
+    if (n_k <= 0) return;
+    hipLaunchKernelGGL(k_slice_flags, dim3(grid_for(n_k, 256, 16384)), dim3(256), 0, s, B, colcnt, n_k, cls);
+    GM_CHECK_LAUNCH();
+}
+
+void slice_build(const Csr &B, const int64_t *colcnt, const int64_t *slice_perm, int64_t n_slices, int32_t *slice_k,
+                 int64_t *cnt_out, int64_t *ip_out, int32_t *k_to_slice, hipStream_t s) {
+    fill<int32_t>(k_to_slice, -1, B.n_rows, s);
+    if (n_slices <= 0) return;
+    hipLaunchKernelGGL(k_slice_build, dim3(grid_for(n_slices, 256, 16384)), dim3(256), 0, s, B, colcnt, slice_perm,
+                       n_slices, slice_k, cnt_out, ip_out, k_to_slice);
+    GM_CHECK_LAUNCH();
+}
+
+void csc_fill(const Csr &A, const Csr &B, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
+              const int64_t *a_heavy_ptr, int64_t nnz_heavy_all, const int32_t *k_to_slice,
+              const int64_t *col_ptr, int64_t *fill_cursor, int32_t *row_h, double *a_val, hipStream_t s) {
+    (void)B;
+    if (n_heavy <= 0 || nnz_heavy_all <= 0) return;
+    hipLaunchKernelGGL(k_csc_fill, dim3(flat_grid(nnz_heavy_all)), dim3(FLAT_BLOCK), 0, s, A, heavy_rows, n_heavy,
+                       r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, col_ptr, fill_cursor, row_h, a_val);
+    GM_CHECK_LAUNCH();
+}
+
+void gather_row_len(const int64_t *row_ptr, const int64_t *rows, int64_t n, int64_t r0, int64_t *out,
+                    hipStream_t s) {
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_gather_row_len, dim3(grid_for(n, 256, 16384)), dim3(256), 0, s, row_ptr, rows, n, r0, out);
+    GM_CHECK_LAUNCH();
+}
+
+void gather_i64(const int64_t *src, const int64_t *idx, int64_t n, int64_t *out, hipStream_t s) {
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_gather_i64, dim3(grid_for(n, 256, 16384)), dim3(256), 0, s, src, idx, n, out);
+    GM_CHECK_LAUNCH();
+}
+
+}  // namespace gm

@@ -1,0 +1,282 @@
+"""Thin ctypes binding of libgmagnus.so (include/gmagnus.h).
+
+Argument marshalling only: torch tensors provide device memory and the HIP
+stream; every step of the SpGEMM runs in the library's HIP kernels. There is
+no fallback: if the library is missing or no GPU is present, calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgmagnus.so")
+
+MAX_LEVELS = 8
+K_NAMES = ["setup", "csc", "expand", "histogram", "multisplit", "chunk_symbolic", "chunk_numeric",
+           "light_symbolic", "light_numeric", "rowptr"]
+FLAG_TIMING = 1
+FLAG_SERIAL_STREAMS = 2
+FLAG_NO_WINDOW = 4
+
+STATUS = {0: "SUCCESS", 1: "INVALID_VALUE", 2: "INVALID_CSR", 3: "OUT_OF_MEMORY", 4: "NOT_READY", 5: "HIP",
+          6: "UNSUPPORTED"}
+
+
+class GmagnusError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__("%s: %s" % (STATUS.get(status, status), msg))
+        self.status = status
+
+
+class CsrDesc(ctypes.Structure):
+    _fields_ = [("n_rows", ctypes.c_int64), ("n_cols", ctypes.c_int64), ("nnz", ctypes.c_int64),
+                ("row_ptr", ctypes.c_void_p), ("col_idx", ctypes.c_void_p), ("val", ctypes.c_void_p)]
+
+
+ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p)
+FREE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p)
+
+
+class Options(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_size_t), ("row_begin", ctypes.c_int64), ("row_end", ctypes.c_int64),
+                ("lds_bytes", ctypes.c_int64), ("tau", ctypes.c_int64), ("dense_width_log2", ctypes.c_int32),
+                ("chunks_max_log2", ctypes.c_int32), ("validate", ctypes.c_int32), ("flags", ctypes.c_int32),
+                ("alloc", ALLOC_FN), ("free", FREE_FN), ("alloc_ctx", ctypes.c_void_p)]
+
+
+class Params(ctypes.Structure):
+    _fields_ = [("tau", ctypes.c_int64), ("dense_width", ctypes.c_int64), ("chunks_required", ctypes.c_int64),
+                ("chunks_max", ctypes.c_int64), ("min_group_elems", ctypes.c_int64), ("group_rows", ctypes.c_int64),
+                ("n_levels", ctypes.c_int32), ("v_chunks", ctypes.c_int32 * MAX_LEVELS)]
+
+    @property
+    def levels(self):
+        return [int(self.v_chunks[i]) for i in range(self.n_levels)]
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [("params", Params), ("n_rows", ctypes.c_int64), ("n_heavy_rows", ctypes.c_int64),
+                ("n_light_rows", ctypes.c_int64), ("products_total", ctypes.c_int64),
+                ("products_heavy", ctypes.c_int64), ("n_slices", ctypes.c_int64), ("nnz_a_heavy", ctypes.c_int64),
+                ("level_rows_in", ctypes.c_int64 * MAX_LEVELS), ("level_elems_in", ctypes.c_int64 * MAX_LEVELS),
+                ("level_heavy_out", ctypes.c_int64 * MAX_LEVELS), ("levels_run", ctypes.c_int32),
+                ("n_leaves_dense", ctypes.c_int64), ("n_leaves_hash", ctypes.c_int64), ("c_nnz", ctypes.c_int64),
+                ("c_nnz_heavy", ctypes.c_int64), ("check_flags", ctypes.c_int32),
+                ("kernel_ms", ctypes.c_double * len(K_NAMES)), ("kernel_launches", ctypes.c_int64 * len(K_NAMES)),
+                ("kernel_bytes", ctypes.c_double * len(K_NAMES))]
+
+    def to_dict(self) -> dict:
+        d = {f: getattr(self, f) for f, _ in self._fields_ if f not in (
+            "params", "level_rows_in", "level_elems_in", "level_heavy_out", "kernel_ms", "kernel_launches",
+            "kernel_bytes")}
+        p = self.params
+        d["params"] = {"tau": p.tau, "dense_width": p.dense_width, "chunks_required": p.chunks_required,
+                       "chunks_max": p.chunks_max, "v_chunks": p.levels}
+        n = self.levels_run
+        d["level_rows_in"] = list(self.level_rows_in[:n])
+        d["level_elems_in"] = list(self.level_elems_in[:n])
+        d["level_heavy_out"] = list(self.level_heavy_out[:n])
+        d["kernels"] = {k: {"ms": self.kernel_ms[i], "launches": self.kernel_launches[i],
+                            "bytes": self.kernel_bytes[i]} for i, k in enumerate(K_NAMES)}
+        return d
+
+
+EXPORTS = ["gmagnus_options_init", "gmagnus_get_params", "gmagnus_plan", "gmagnus_spgemm_symbolic",
+           "gmagnus_spgemm_numeric", "gmagnus_plan_info", "gmagnus_plan_destroy", "gmagnus_row_products",
+           "gmagnus_split_panels", "gmagnus_release_cache", "gmagnus_last_error", "gmagnus_status_string"]
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Loads libgmagnus.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError("libgmagnus.so not built (run python -m paper_2607_22866_amd.build)")
+    lib = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    lib.gmagnus_options_init.argtypes = [ctypes.POINTER(Options)]
+    lib.gmagnus_options_init.restype = None
+    lib.gmagnus_get_params.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.POINTER(Options), ctypes.POINTER(Params)]
+    lib.gmagnus_plan.argtypes = [ctypes.POINTER(P), ctypes.POINTER(CsrDesc), ctypes.POINTER(CsrDesc),
+                                 ctypes.POINTER(Options), P]
+    lib.gmagnus_spgemm_symbolic.argtypes = [P, P, ctypes.POINTER(ctypes.c_int64)]
+    lib.gmagnus_spgemm_numeric.argtypes = [P, P, P, P]
+    lib.gmagnus_plan_info.argtypes = [P, ctypes.POINTER(PlanInfo)]
+    lib.gmagnus_plan_destroy.argtypes = [P]
+    lib.gmagnus_plan_destroy.restype = None
+    lib.gmagnus_row_products.argtypes = [ctypes.POINTER(CsrDesc), ctypes.POINTER(CsrDesc), P, P]
+    lib.gmagnus_split_panels.argtypes = [ctypes.POINTER(CsrDesc), ctypes.POINTER(CsrDesc), ctypes.c_int64, P,
+                                         ctypes.c_int64, ctypes.POINTER(ctypes.c_int64), P]
+    lib.gmagnus_release_cache.argtypes = []
+    lib.gmagnus_release_cache.restype = None
+    lib.gmagnus_last_error.restype = ctypes.c_char_p
+    lib.gmagnus_status_string.argtypes = [ctypes.c_int]
+    lib.gmagnus_status_string.restype = ctypes.c_char_p
+    for f in ("gmagnus_get_params", "gmagnus_plan", "gmagnus_spgemm_symbolic", "gmagnus_spgemm_numeric",
+              "gmagnus_plan_info", "gmagnus_row_products", "gmagnus_split_panels"):
+        getattr(lib, f).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _check(st: int):
+    if st != 0:
+        raise GmagnusError(st, load().gmagnus_last_error().decode())
+
+
+def make_options(**kw) -> Options:
+    o = Options()
+    load().gmagnus_options_init(ctypes.byref(o))
+    for k, v in kw.items():
+        if v is None:
+            continue
+        if not hasattr(o, k):
+            raise TypeError("unknown option %r" % k)
+        setattr(o, k, v)
+    return o
+
+
+def get_params(c_m: int, lds_bytes: int = 163840, **overrides) -> Params:
+    """Host-only parameter selection of the library (no GPU needed)."""
+    p = Params()
+    o = make_options(**overrides)
+    _check(load().gmagnus_get_params(c_m, lds_bytes, ctypes.byref(o), ctypes.byref(p)))
+    return p
+
+
+@dataclass
+class DeviceCSR:
+    """CSR on the GPU: int64 row_ptr, int32 col, float64 val (torch tensors)."""
+
+    n_rows: int
+    n_cols: int
+    row_ptr: torch.Tensor
+    col: torch.Tensor
+    val: torch.Tensor
+
+    @property
+    def nnz(self) -> int:
+        return int(self.col.numel())
+
+    @staticmethod
+    def from_host(m, device="cuda") -> "DeviceCSR":
+        """Copies a host CSR (numpy or torch arrays) to the device."""
+        rp = torch.as_tensor(m.row_ptr, dtype=torch.int64).to(device)
+        col = torch.as_tensor(m.col, dtype=torch.int32).to(device)
+        val = torch.as_tensor(m.val, dtype=torch.float64).to(device)
+        return DeviceCSR(int(m.n_rows), int(m.n_cols), rp, col, val)
+
+    def desc(self) -> CsrDesc:
+        for t, dt in ((self.row_ptr, torch.int64), (self.col, torch.int32), (self.val, torch.float64)):
+            if not t.is_cuda or t.dtype != dt or not t.is_contiguous():
+                raise ValueError("DeviceCSR arrays must be contiguous CUDA tensors of int64/int32/float64")
+        return CsrDesc(self.n_rows, self.n_cols, self.nnz, self.row_ptr.data_ptr(),
+                       self.col.data_ptr() if self.nnz else None, self.val.data_ptr() if self.nnz else None)
+
+    def to_host(self):
+        return self.row_ptr.cpu().numpy(), self.col.cpu().numpy(), self.val.cpu().numpy()
+
+
+def _stream(stream) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+class Plan:
+    """One row panel of C = A*B: setup on construction, then symbolic and numeric."""
+
+    def __init__(self, A: DeviceCSR, B: DeviceCSR, stream=None, **options):
+        self._lib = load()
+        self.A, self.B = A, B  # borrowed by the library until close()
+        self._da, self._db = A.desc(), B.desc()
+        self._opts = make_options(**options)
+        self._stream = stream
+        self._h = ctypes.c_void_p()
+        _check(self._lib.gmagnus_plan(ctypes.byref(self._h), ctypes.byref(self._da), ctypes.byref(self._db),
+                                      ctypes.byref(self._opts), _stream(stream)))
+        rb = self._opts.row_begin
+        re = self._opts.row_end if self._opts.row_end > 0 else A.n_rows
+        self.n_rows = re - rb
+        self.row_ptr: Optional[torch.Tensor] = None
+        self.nnz = None
+
+    def symbolic(self):
+        """Returns (row_ptr of the panel on the device, nnz)."""
+        rp = torch.empty(self.n_rows + 1, dtype=torch.int64, device=self.A.row_ptr.device)
+        nnz = ctypes.c_int64()
+        _check(self._lib.gmagnus_spgemm_symbolic(self._h, rp.data_ptr(), ctypes.byref(nnz)))
+        self.row_ptr, self.nnz = rp, int(nnz.value)
+        return rp, self.nnz
+
+    def numeric(self, col: Optional[torch.Tensor] = None, val: Optional[torch.Tensor] = None):
+        """Fills (and returns) C's column and value arrays for the panel."""
+        dev = self.A.row_ptr.device
+        if col is None:
+            col = torch.empty(self.nnz, dtype=torch.int32, device=dev)
+        if val is None:
+            val = torch.empty(self.nnz, dtype=torch.float64, device=dev)
+        if col.numel() < self.nnz or val.numel() < self.nnz:
+            raise ValueError("output arrays smaller than nnz")
+        _check(self._lib.gmagnus_spgemm_numeric(self._h, self.row_ptr.data_ptr(),
+                                                col.data_ptr() if self.nnz else None,
+                                                val.data_ptr() if self.nnz else None))
+        return col, val
+
+    def info(self) -> PlanInfo:
+        out = PlanInfo()
+        _check(self._lib.gmagnus_plan_info(self._h, ctypes.byref(out)))
+        return out
+
+    def close(self):
+        if self._h:
+            self._lib.gmagnus_plan_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *a):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def spgemm(A: DeviceCSR, B: DeviceCSR, stream=None, **options):
+    """C = A*B for the rows selected by options (default all): (row_ptr, col, val) on the device."""
+    with Plan(A, B, stream=stream, **options) as p:
+        rp, _ = p.symbolic()
+        col, val = p.numeric()
+        return rp, col, val
+
+
+def row_products(A: DeviceCSR, B: DeviceCSR, stream=None) -> torch.Tensor:
+    ip = torch.empty(A.n_rows, dtype=torch.int64, device=A.row_ptr.device)
+    da, db = A.desc(), B.desc()
+    _check(load().gmagnus_row_products(ctypes.byref(da), ctypes.byref(db), ip.data_ptr() if A.n_rows else None,
+                                       _stream(stream)))
+    return ip
+
+
+def split_panels(A: DeviceCSR, B: DeviceCSR, max_products: int, max_panels: int = 1 << 16, stream=None):
+    bounds = (ctypes.c_int64 * (max_panels + 1))()
+    n = ctypes.c_int64()
+    da, db = A.desc(), B.desc()
+    _check(load().gmagnus_split_panels(ctypes.byref(da), ctypes.byref(db), max_products, bounds, max_panels,
+                                       ctypes.byref(n), _stream(stream)))
+    return [int(bounds[i]) for i in range(n.value + 1)]
+
+
+def release_cache():
+    load().gmagnus_release_cache()

@@ -1,0 +1,143 @@
+"""CPU-side checks of the C ABI: the library loads, exports every declared
+symbol, its host-only planner matches the paper's printed chunk counts, and
+argument validation fails with status codes before touching a device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gmagnus.h")
+
+gm = pytest.importorskip("paper_2607_22866_amd.gmagnus")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(gm.LIB_PATH):
+        from paper_2607_22866_amd import build
+
+        build.build()
+    return gm.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gmagnus_\w+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(gm.EXPORTS) == names
+
+
+def test_struct_sizes_match_header(lib):
+    # the options struct carries its own size; a mismatch is rejected
+    o = gm.make_options()
+    assert o.struct_size == ctypes.sizeof(gm.Options)
+    p = gm.Params()
+    o.struct_size = 8
+    assert lib.gmagnus_get_params(4096, 163840, ctypes.byref(o), ctypes.byref(p)) == 1
+
+
+def _golden():
+    rows = []
+    with open(os.path.join(ROOT, "tests", "golden", "num_chunks.txt")) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                rows.append([x.strip() for x in line.split("|")])
+    return rows
+
+
+def _fmt(p):
+    lv = p.levels
+    if len(lv) <= 1:
+        return str(p.chunks_required)
+    return "%d: %s" % (p.chunks_required, ", ".join(map(str, lv)))
+
+
+def test_library_planner_reproduces_printed_chunk_counts(lib):
+    n = 0
+    for name, cm, pvc, h200 in _golden():
+        for s_lm, printed in ((131072, pvc), (233472, h200)):
+            if printed == "N/A":
+                continue
+            assert _fmt(gm.get_params(int(cm), s_lm)) == printed, (name, s_lm)
+            n += 1
+    assert n == 51
+
+
+def test_library_planner_matches_oracle_planner(lib):
+    from oracle.params import get_magnus_params
+
+    for s_lm in (65536, 131072, 163840, 233472):
+        for cm in (1, 100, 4096, 8192, 8193, 65536, 1 << 20, (1 << 22) + 3, 1 << 23, 1 << 26, 2_000_000_000):
+            a = gm.get_params(cm, s_lm)
+            b = get_magnus_params(cm, s_lm)
+            assert (a.dense_width, a.chunks_required, a.chunks_max) == (b.dense_width, b.chunks_required,
+                                                                        b.chunks_max), (cm, s_lm)
+            assert a.levels == b.v_chunks, (cm, s_lm)
+            assert a.tau == min(b.tau, 7168)
+
+
+def test_planner_mi355x_defaults(lib):
+    p = gm.get_params(1 << 22, 163840)
+    assert (p.tau, p.dense_width, p.chunks_max, p.levels) == (6826, 8192, 32, [32, 16])
+    assert gm.get_params(1 << 23).levels == [32, 32]
+    assert gm.get_params(4096).levels == []
+    # overrides force any depth on a small column count
+    assert gm.get_params(4096, tau=200, dense_width_log2=6, chunks_max_log2=2).levels == [4, 4, 4]
+    assert gm.get_params(4096, dense_width_log2=8, chunks_max_log2=4).levels == [16]
+    assert gm.get_params(4096, dense_width_log2=7, chunks_max_log2=3).levels == [8, 4]
+
+
+def test_planner_rejects_bad_arguments(lib):
+    for cm, lds, kw in ((0, 163840, {}), (1 << 31, 163840, {}), (4096, 100, {}), (4096, 163840,
+                                                                                  {"dense_width_log2": 14})):
+        with pytest.raises(gm.GmagnusError) as e:
+            gm.get_params(cm, lds, **kw)
+        assert e.value.status == 1
+
+
+def _desc(n_rows, n_cols, nnz=0, ptr=0x1000):
+    return gm.CsrDesc(n_rows, n_cols, nnz, ptr, ptr if nnz else None, ptr if nnz else None)
+
+
+def test_plan_argument_validation_without_device(lib):
+    h = ctypes.c_void_p()
+    a, b = _desc(4, 5), _desc(6, 3)
+    # NULL output
+    assert lib.gmagnus_plan(None, ctypes.byref(a), ctypes.byref(b), None, None) == 1
+    # NULL operand
+    assert lib.gmagnus_plan(ctypes.byref(h), None, ctypes.byref(b), None, None) == 1
+    assert not h.value
+    # inner dimensions differ
+    assert lib.gmagnus_plan(ctypes.byref(h), ctypes.byref(a), ctypes.byref(b), None, None) == 1
+    assert b"A.n_cols" in lib.gmagnus_last_error()
+    # too many columns
+    big = _desc(4, 1 << 31)
+    assert lib.gmagnus_plan(ctypes.byref(h), ctypes.byref(_desc(4, 4)), ctypes.byref(_desc(4, 1 << 31)), None,
+                            None) == 6
+    # option struct of another size
+    o = gm.make_options()
+    o.struct_size = 4
+    b2 = _desc(5, 3)
+    assert lib.gmagnus_plan(ctypes.byref(h), ctypes.byref(a), ctypes.byref(b2), ctypes.byref(o), None) == 1
+    # NULL plan handles
+    nnz = ctypes.c_int64()
+    assert lib.gmagnus_spgemm_symbolic(None, None, ctypes.byref(nnz)) == 1
+    assert lib.gmagnus_spgemm_numeric(None, None, None, None) == 1
+    assert lib.gmagnus_plan_info(None, None) == 1
+    lib.gmagnus_plan_destroy(None)
+    del big
+
+
+def test_status_strings(lib):
+    for code, name in gm.STATUS.items():
+        assert lib.gmagnus_status_string(code).decode() == "GMAGNUS_" + ("SUCCESS" if code == 0 else "ERROR_" + name)

@@ -1,0 +1,225 @@
+"""Parity of the HIP SpGEMM (through the C ABI) with the CPU oracle, on
+seeded inputs small enough for the oracle to finish in seconds while still
+spanning many tiles and ragged tails, and on the corner cases of the method
+(empty rows/columns, forced multisplit depths, panels, explicit zeros)."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+from tests.parity import compare_full, compare_rows
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def g():
+    from paper_2607_22866_amd import gmagnus
+
+    gmagnus.load()
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return gmagnus
+
+
+def run(g, A, B, **opts):
+    dA = g.DeviceCSR.from_host(A)
+    dB = dA if B is A else g.DeviceCSR.from_host(B)
+    with g.Plan(dA, dB, **opts) as p:
+        rp, nnz = p.symbolic()
+        col, val = p.numeric()
+        info = p.info()
+    torch.cuda.synchronize()
+    assert info.check_flags == 0, info.check_flags
+    return rp.cpu().numpy(), col.cpu().numpy(), val.cpu().numpy(), info
+
+
+def check(g, A, B, **opts):
+    rp, col, val, info = run(g, A, B, **opts)
+    r0 = opts.get("row_begin", 0)
+    r1 = opts.get("row_end", 0) or A.n_rows
+    ref = oracle.spgemm(A, B, rows=np.arange(r0, r1))
+    compare_full(rp, col, val, ref)
+    return info
+
+
+RMAT12 = wl.CONFIGS["rmat12"]
+
+# (tau, dense_width_log2, chunks_max_log2) -> expected multisplit levels for C.m = 4096
+DEPTHS = [
+    ({}, []),
+    (dict(tau=600, dense_width_log2=8, chunks_max_log2=4), [16]),
+    (dict(tau=300, dense_width_log2=7, chunks_max_log2=3), [8, 4]),
+    (dict(tau=200, dense_width_log2=6, chunks_max_log2=2), [4, 4, 4]),
+    (dict(tau=150, dense_width_log2=5, chunks_max_log2=5), [32, 4]),
+    (dict(tau=128, dense_width_log2=5, chunks_max_log2=1), [2, 2, 2, 2, 2, 2, 2]),
+]
+
+
+@pytest.mark.parametrize("opts,levels", DEPTHS)
+def test_rmat12_every_depth(g, opts, levels):
+    A = RMAT12.make()
+    info = check(g, A, A, **opts)
+    assert info.params.levels == levels
+    ip = oracle.row_products(A, A)
+    tau = info.params.tau
+    assert info.n_heavy_rows == int((ip > tau).sum())
+    assert info.products_total == int(ip.sum())
+    assert info.products_heavy == int(ip[ip > tau].sum())
+    if levels:
+        assert info.levels_run >= 1
+
+
+def test_rmat12_integer_values_bit_exact(g):
+    A = wl.rmat(12, 8, 0.57, 0.19, 0.19, 12, values="int3")
+    for opts in ({}, dict(tau=200, dense_width_log2=6, chunks_max_log2=2)):
+        rp, col, val, _ = run(g, A, A, **opts)
+        ref = oracle.spgemm(A, A)
+        assert np.array_equal(rp, ref.row_ptr) and np.array_equal(col, ref.col)
+        assert np.array_equal(val, ref.val)  # exact integers in any summation order
+
+
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_rmat_scales(g, seed):
+    A = wl.rmat(13 + seed % 2, 8 + 4 * seed, 0.57, 0.19, 0.19, 40 + seed)
+    check(g, A, A)
+    check(g, A, A, tau=256, dense_width_log2=7, chunks_max_log2=3)
+
+
+def test_distinct_a_b_non_square(g):
+    A = wl.rmat(11, 8, 0.57, 0.19, 0.19, 7)
+    B = wl.erdos_renyi(A.n_cols, 3000, 12, 8)  # 2048 x 3000, C.m not a power of two
+    check(g, A, B)
+    check(g, A, B, tau=300, dense_width_log2=6, chunks_max_log2=3)
+
+
+@pytest.mark.parametrize("shape,density", [((1, 1, 1), 1.0), ((37, 50, 61), 0.1), ((200, 300, 150), 0.05),
+                                           ((64, 64, 64), 0.0), ((130, 5, 700), 0.5)])
+def test_uniform_small(g, shape, density):
+    m, k, n = shape
+    A = wl.uniform(m, k, density, m + k)
+    B = wl.uniform(k, n, density, n + 7)
+    check(g, A, B)
+    check(g, A, B, tau=128, dense_width_log2=5, chunks_max_log2=2)
+
+
+def test_banded_window_and_hash(g):
+    A = wl.banded(4096, 13, 3)
+    info = check(g, A, A)
+    assert info.n_heavy_rows == 0
+    check(g, A, A, flags=4)  # hash accumulator instead of the dense window
+    W = wl.banded(3000, 300, 4)  # 601-wide rows: wider window bin
+    check(g, W, W)
+
+
+def test_erdos_renyi(g):
+    A = wl.erdos_renyi(1 << 14, 1 << 14, 16, 5)
+    info = check(g, A, A)
+    assert info.products_total == 256 << 14
+
+
+def test_identity_permutation_exact(g):
+    A = RMAT12.make()
+    I = wl.identity(A.n_rows)
+    for X, Y in ((I, A), (A, I)):
+        rp, col, val, _ = run(g, X, Y)
+        assert np.array_equal(rp, A.row_ptr) and np.array_equal(col, A.col) and np.array_equal(val, A.val)
+    P = wl.permutation(A.n_rows, 9)
+    rp, col, val, _ = run(g, P, A)
+    perm = P.col.astype(np.int64)
+    for i in range(0, A.n_rows, 11):
+        s, e = A.row_ptr[perm[i]], A.row_ptr[perm[i] + 1]
+        assert np.array_equal(col[rp[i]:rp[i + 1]], A.col[s:e])
+        assert np.array_equal(val[rp[i]:rp[i + 1]], A.val[s:e])
+
+
+def test_structural_zeros_kept(g):
+    A = wl.CSR(2, 2, np.array([0, 2, 3], np.int64), np.array([0, 1, 1], np.int32), np.array([1.0, -1.0, 2.0]))
+    B = wl.CSR(2, 3, np.array([0, 2, 3], np.int64), np.array([0, 2, 2], np.int32), np.array([5.0, 2.0, 2.0]))
+    rp, col, val, _ = run(g, A, B)
+    assert list(rp) == [0, 2, 3] and list(col) == [0, 2, 2] and list(val) == [5.0, 0.0, 4.0]
+    # the same cancellation inside a heavy row (forced with a small tau)
+    H = wl.rmat(10, 16, 0.57, 0.19, 0.19, 2, values="int3")
+    check(g, H, H, tau=128, dense_width_log2=6, chunks_max_log2=2)
+
+
+def test_empty_and_degenerate(g):
+    E = wl.empty(50, 40)
+    B = wl.uniform(40, 30, 0.2, 1)
+    rp, col, val, info = run(g, E, B)
+    assert np.all(rp == 0) and col.size == 0
+    A = wl.uniform(30, 40, 0.2, 2)
+    rp, col, val, info = run(g, A, wl.empty(40, 30))
+    assert np.all(rp == 0) and info.products_total == 0
+    one = wl.uniform(1, 1, 1.0, 3)
+    check(g, one, one)
+    # a row panel with no rows
+    R = RMAT12.make()
+    rp, col, val, _ = run(g, R, R, row_begin=100, row_end=100)
+    assert list(rp) == [0] and col.size == 0
+
+
+def test_panels_concatenate_to_full(g):
+    A = RMAT12.make()
+    dA = g.DeviceCSR.from_host(A)
+    bounds = g.split_panels(dA, dA, 200_000)
+    assert bounds[0] == 0 and bounds[-1] == A.n_rows and len(bounds) > 3
+    ip = oracle.row_products(A, A)
+    pre = np.concatenate([[0], np.cumsum(ip)])
+    for a, b in zip(bounds[:-1], bounds[1:]):
+        assert pre[b] - pre[a] <= 200_000 or b == a + 1
+    ref = oracle.spgemm(A, A)
+    for a, b in zip(bounds[:-1], bounds[1:]):
+        rp, col, val, _ = run(g, A, A, row_begin=a, row_end=b)
+        assert np.array_equal(rp + ref.row_ptr[a], ref.row_ptr[a:b + 1])
+        s, e = ref.row_ptr[a], ref.row_ptr[b]
+        assert np.array_equal(col, ref.col[s:e])
+        assert np.all(np.abs(val - ref.val[s:e]) <= 1e-12 * ref.bound[s:e])
+
+
+def test_row_products_abi(g):
+    A = wl.rmat(13, 16, 0.57, 0.19, 0.19, 77)
+    dA = g.DeviceCSR.from_host(A)
+    ip = g.row_products(dA, dA).cpu().numpy()
+    assert np.array_equal(ip, oracle.row_products(A, A))
+
+
+def test_validate_flags_bad_csr(g):
+    A = wl.uniform(20, 20, 0.3, 5)
+    bad = wl.CSR(A.n_rows, A.n_cols, A.row_ptr.copy(), A.col.copy(), A.val.copy())
+    r = int(np.argmax(np.diff(bad.row_ptr) >= 2))
+    s = bad.row_ptr[r]
+    bad.col[s], bad.col[s + 1] = bad.col[s + 1], bad.col[s]  # unsorted row
+    dA = g.DeviceCSR.from_host(bad)
+    with pytest.raises(g.GmagnusError) as e:
+        g.Plan(dA, dA, validate=1)
+    assert e.value.status == 2
+    g.Plan(g.DeviceCSR.from_host(A), g.DeviceCSR.from_host(A), validate=1).close()
+
+
+def test_numeric_before_symbolic_rejected(g):
+    A = RMAT12.make()
+    dA = g.DeviceCSR.from_host(A)
+    with g.Plan(dA, dA) as p:
+        p.nnz = 0
+        p.row_ptr = torch.zeros(A.n_rows + 1, dtype=torch.int64, device="cuda")
+        with pytest.raises(g.GmagnusError) as e:
+            p.numeric(torch.empty(1, dtype=torch.int32, device="cuda"), torch.empty(1, dtype=torch.float64,
+                                                                                    device="cuda"))
+        assert e.value.status == 4
+
+
+def test_serial_streams_and_timing_flags(g):
+    A = RMAT12.make()
+    info = check(g, A, A, flags=1 | 2, tau=300, dense_width_log2=7, chunks_max_log2=3)
+    d = info.to_dict()
+    assert d["kernels"]["expand"]["ms"] > 0 and d["kernels"]["multisplit"]["launches"] >= 1
+
+
+def test_sampled_rows_helper(g):
+    A = wl.rmat(14, 8, 0.57, 0.19, 0.19, 5)
+    rp, col, val, _ = run(g, A, A)
+    rows = np.random.default_rng(0).choice(A.n_rows, 300, replace=False)
+    compare_rows(rows, rp, col, val, oracle.spgemm(A, A, rows=rows))
