@@ -129,6 +129,7 @@ typedef struct {
     int32_t levels_run;            /* levels actually executed (early exit when no heavy chunk) */
     int64_t n_leaves_dense;        /* final chunks accumulated densely */
     int64_t n_leaves_hash;         /* final chunks accumulated with the hash map */
+    int64_t n_leaves_rank;         /* final chunks accumulated with the bitmap-rank accumulator */
     int64_t c_nnz;                 /* nonzeros of the panel of C (after symbolic) */
     int64_t c_nnz_heavy;           /* of which in heavy rows */
     int32_t check_flags;           /* nonzero: a kernel's output count disagreed with symbolic (a bug) */

@@ -61,11 +61,20 @@ GM_DEV void gustavson_row(const Csr &A, const Csr &B, int64_t j0, int64_t j1, Gu
 }
 
 // ------------------------------------------------------------ hash map
+// Multiplicative (Fibonacci) hashing into a power-of-two table. The paper's
+// plain modulo keeps the column's low bits, which R-MAT skews heavily (each
+// bit is 0 with probability a + c), so linear probing would cluster.
+template <int TS>
+GM_DEV uint32_t hash_slot(int32_t c) {
+    static_assert((TS & (TS - 1)) == 0 && TS >= 2, "table size must be a power of two");
+    return ((uint32_t)c * 0x9E3779B1u) >> (32 - __builtin_ctz(TS));
+}
+
 // Probing stops after TS slots, so a table that were ever full could not
 // hang the work group (the count check of the numeric phase reports it).
 template <int TS>
 GM_DEV void hash_insert_key(int32_t *keys, int32_t c, int32_t *counter) {
-    uint32_t h = (uint32_t)c & (TS - 1);
+    uint32_t h = hash_slot<TS>(c);
     for (int probe = 0; probe < TS; ++probe) {
         int32_t old = ((volatile int32_t *)keys)[h];
         if (old == -1) {
@@ -82,7 +91,7 @@ GM_DEV void hash_insert_key(int32_t *keys, int32_t c, int32_t *counter) {
 
 template <int TS>
 GM_DEV void hash_insert_add(int32_t *keys, double *vals, int32_t c, double v) {
-    uint32_t h = (uint32_t)c & (TS - 1);
+    uint32_t h = hash_slot<TS>(c);
     for (int probe = 0; probe < TS; ++probe) {
         int32_t old = ((volatile int32_t *)keys)[h];
         if (old == -1) {
@@ -119,8 +128,8 @@ GM_DEV void hash_emit_sorted(int32_t *keys, double *vals, int64_t nnz, int32_t c
     int cnt = 0;
 #pragma unroll
     for (int q = 0; q < PER; ++q) {
-        k[q] = keys[tid * PER + q];
-        v[q] = vals[tid * PER + q];
+        k[q] = keys[tid + q * BLOCK];  // strided: no LDS bank conflicts
+        v[q] = vals[tid + q * BLOCK];
         cnt += k[q] != -1;
     }
     int32_t total;
@@ -268,7 +277,16 @@ __global__ void k_light_classes(const int64_t *ip, const int64_t *row_nnz, const
     }
 }
 
-__global__ void k_leaf_classes(LeafSet L, const int64_t *leaf_nnz, int64_t tau, uint8_t *cls) {
+constexpr int DENSE_MAX = 8192;          // columns of the LDS dense accumulator
+constexpr int RANK_MAX_LOG2 = 18;        // columns of the bitmap-rank accumulator
+constexpr int RANK_NNZ_MAX = 7168;       // distinct columns it holds (>= tau)
+constexpr int RANK_MIN_LEN = 256;        // smaller chunks go to the hash map
+
+// Accumulator of a final chunk of `len` elements over `width` columns:
+// heavy chunks (len > tau, width <= W) and well-filled narrow chunks use the
+// dense accumulator; wide light chunks use the bitmap-rank accumulator while
+// the bitmap fits LDS; small chunks use the hash map.
+__global__ void k_leaf_classes(LeafSet L, const int64_t *leaf_nnz, int64_t tau, int width, uint8_t *cls) {
     const int64_t n = L.hi - L.lo;
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
         const int64_t j = L.lo + i;
@@ -276,8 +294,10 @@ __global__ void k_leaf_classes(LeafSet L, const int64_t *leaf_nnz, int64_t tau, 
         uint8_t c;
         if (len == 0)
             c = LEAF_EMPTY;
-        else if (len > tau)
+        else if (width <= DENSE_MAX && (len > tau || len >= width / 16))
             c = LEAF_DENSE;
+        else if (width <= (1 << RANK_MAX_LOG2) && width >= 32 && len >= RANK_MIN_LEN)
+            c = LEAF_RANK;
         else
             c = (uint8_t)(LEAF_H0 + (leaf_nnz ? hash_bin_num(leaf_nnz[i]) : hash_bin_sym(len)));
         cls[i] = c;
@@ -411,8 +431,6 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_hash_num(LeafSet L, const int64_
     hash_emit_sorted<BLOCK, TS>(keys, vals, nnz, base, o.c_col + dst, o.c_val + dst, scan_sm, o.err);
 }
 
-constexpr int DENSE_MAX = 8192;
-
 template <int BLOCK>
 __global__ __launch_bounds__(BLOCK) void k_leaf_dense_sym(LeafSet L, const int64_t *items, int width,
                                                           int64_t *leaf_nnz, int64_t *slot_cnt) {
@@ -447,6 +465,112 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_dense_num(LeafSet L, const int64
     leaf_target(o, L.origin[j], dst, cap, base);
     const int64_t nnz = leaf_nnz[i] < cap ? leaf_nnz[i] : cap;
     dense_emit(D, width, nnz, base, o.c_col + dst, o.c_val + dst, o.err);
+}
+
+// Bitmap-rank accumulator for light chunks whose column range is too wide
+// for a dense value array: a one-bit-per-column bitmap marks the present
+// columns, an exclusive scan of the bitmap words' popcounts gives every
+// present column its rank, i.e. its position in the sorted output, and the
+// values are summed straight into a rank-indexed array. No hashing and no
+// sort; the output comes out in column order.
+template <int BLOCK>
+struct RankLds {
+    uint32_t bits[(1 << RANK_MAX_LOG2) / 32];
+    uint16_t wpre[(1 << RANK_MAX_LOG2) / 32];  // rank of each word's first bit
+    int32_t scan[BLOCK / GM_WAVE];
+};
+
+template <int BLOCK>
+GM_DEV void rank_mark(RankLds<BLOCK> &R, const int32_t *col, int64_t s, int64_t e, int nwords) {
+    for (int w = threadIdx.x; w < nwords; w += BLOCK) R.bits[w] = 0;
+    __syncthreads();
+    for (int64_t t = s + threadIdx.x; t < e; t += BLOCK) {
+        const int c = col[t];
+        const uint32_t bit = 1u << (c & 31);
+        if (!(((volatile uint32_t *)R.bits)[c >> 5] & bit)) atomicOr(&R.bits[c >> 5], bit);
+    }
+    __syncthreads();
+}
+
+// Exclusive scan of word popcounts into wpre; returns the total. Thread t
+// owns the consecutive words [t*per, (t+1)*per).
+template <int BLOCK>
+GM_DEV int32_t rank_scan(RankLds<BLOCK> &R, int nwords) {
+    const int per = (nwords + BLOCK - 1) / BLOCK;
+    const int w0 = threadIdx.x * per;
+    int32_t sum = 0;
+    for (int q = 0; q < per; ++q)
+        if (w0 + q < nwords) sum += __popc(R.bits[w0 + q]);
+    int32_t total;
+    int32_t run = block_excl_scan<BLOCK>(sum, R.scan, &total);
+    for (int q = 0; q < per; ++q)
+        if (w0 + q < nwords) {
+            R.wpre[w0 + q] = (uint16_t)run;
+            run += __popc(R.bits[w0 + q]);
+        }
+    __syncthreads();
+    return total;
+}
+
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void k_leaf_rank_sym(LeafSet L, const int64_t *items, int width,
+                                                         int64_t *leaf_nnz, int64_t *slot_cnt) {
+    __shared__ RankLds<BLOCK> R;
+    const int64_t i = items[blockIdx.x];
+    const int64_t j = L.lo + i;
+    const int nwords = width >> 5;
+    rank_mark(R, L.col, L.ptr[j], L.ptr[j + 1], nwords);
+    int32_t c = 0;
+    for (int w = threadIdx.x; w < nwords; w += BLOCK) c += __popc(R.bits[w]);
+    c = block_reduce_sum<BLOCK>(c, R.scan);
+    if (threadIdx.x == 0) {
+        leaf_nnz[i] = c;
+        slot_cnt[L.origin[j]] = c;
+    }
+}
+
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const int64_t *items, const int64_t *leaf_nnz,
+                                                         int width, LeafOut o) {
+    __shared__ RankLds<BLOCK> R;
+    __shared__ double vals[RANK_NNZ_MAX];
+    __shared__ int32_t cols[RANK_NNZ_MAX];
+    const int64_t i = items[blockIdx.x];
+    const int64_t j = L.lo + i;
+    const int64_t s = L.ptr[j], e = L.ptr[j + 1];
+    const int nwords = width >> 5;
+    rank_mark(R, L.col, s, e, nwords);
+    const int32_t total = rank_scan(R, nwords);
+    const int n = total < RANK_NNZ_MAX ? total : RANK_NNZ_MAX;
+    for (int q = threadIdx.x; q < n; q += BLOCK) vals[q] = 0.0;
+    // columns in rank order
+    for (int w = threadIdx.x; w < nwords; w += BLOCK) {
+        uint32_t b = R.bits[w];
+        int r = R.wpre[w];
+        while (b) {
+            const int bit = __ffs(b) - 1;
+            if (r < n) cols[r] = (w << 5) | bit;
+            ++r;
+            b &= b - 1;
+        }
+    }
+    __syncthreads();
+    for (int64_t t = s + threadIdx.x; t < e; t += BLOCK) {
+        const int c = L.col[t];
+        const int r = R.wpre[c >> 5] + __popc(R.bits[c >> 5] & ((1u << (c & 31)) - 1u));
+        if (r < n) __hip_atomic_fetch_add(&vals[r], L.val[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+    __syncthreads();
+    int64_t dst, cap;
+    int32_t base;
+    leaf_target(o, L.origin[j], dst, cap, base);
+    const int64_t nnz = leaf_nnz[i] < cap ? leaf_nnz[i] : cap;
+    if (threadIdx.x == 0 && (total != nnz || total > RANK_NNZ_MAX)) atomicOr(o.err, 4);
+    const int m = n < nnz ? n : (int)nnz;
+    for (int q = threadIdx.x; q < m; q += BLOCK) {
+        o.c_col[dst + q] = cols[q] + base;
+        o.c_val[dst + q] = vals[q];
+    }
 }
 
 // -------------------------------------------------------------- slot scan
@@ -494,17 +618,18 @@ void light_classes_num(const int64_t *ip, const int64_t *row_nnz, const int32_t 
     GM_CHECK_LAUNCH();
 }
 
-void leaf_classes_sym(const LeafSet &L, int64_t tau, uint8_t *cls, hipStream_t s) {
+void leaf_classes_sym(const LeafSet &L, int64_t tau, int width, uint8_t *cls, hipStream_t s) {
     const int64_t n = L.hi - L.lo;
     if (n <= 0) return;
-    hipLaunchKernelGGL(k_leaf_classes, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, L, nullptr, tau, cls);
+    hipLaunchKernelGGL(k_leaf_classes, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, L, nullptr, tau, width, cls);
     GM_CHECK_LAUNCH();
 }
 
-void leaf_classes_num(const LeafSet &L, const int64_t *leaf_nnz, int64_t tau, uint8_t *cls, hipStream_t s) {
+void leaf_classes_num(const LeafSet &L, const int64_t *leaf_nnz, int64_t tau, int width, uint8_t *cls,
+                      hipStream_t s) {
     const int64_t n = L.hi - L.lo;
     if (n <= 0) return;
-    hipLaunchKernelGGL(k_leaf_classes, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, L, leaf_nnz, tau, cls);
+    hipLaunchKernelGGL(k_leaf_classes, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, L, leaf_nnz, tau, width, cls);
     GM_CHECK_LAUNCH();
 }
 
@@ -559,6 +684,10 @@ void leaf_symbolic(const LeafSet &L, int bin, const int64_t *items, int64_t n, i
         GM_REQUIRE(n <= 0 || width <= DENSE_MAX, GMAGNUS_ERROR_UNSUPPORTED, "dense accumulator wider than LDS allows");
         launch_items(k_leaf_dense_sym<512>, 512, n, s, L, items, width, leaf_nnz, slot_cnt);
         break;
+    case LEAF_RANK:
+        GM_REQUIRE(n <= 0 || width <= (1 << RANK_MAX_LOG2), GMAGNUS_ERROR_UNSUPPORTED, "rank bitmap too wide");
+        launch_items(k_leaf_rank_sym<512>, 512, n, s, L, items, width, leaf_nnz, slot_cnt);
+        break;
     default: break;
     }
 }
@@ -575,6 +704,10 @@ void leaf_numeric(const LeafSet &L, int bin, const int64_t *items, int64_t n, in
     case LEAF_DENSE:
         GM_REQUIRE(n <= 0 || width <= DENSE_MAX, GMAGNUS_ERROR_UNSUPPORTED, "dense accumulator wider than LDS allows");
         launch_items(k_leaf_dense_num<512>, 512, n, s, L, items, leaf_nnz, width, o);
+        break;
+    case LEAF_RANK:
+        GM_REQUIRE(n <= 0 || width <= (1 << RANK_MAX_LOG2), GMAGNUS_ERROR_UNSUPPORTED, "rank bitmap too wide");
+        launch_items(k_leaf_rank_num<512>, 512, n, s, L, items, leaf_nnz, width, o);
         break;
     default: break;
     }

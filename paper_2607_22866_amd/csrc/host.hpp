@@ -177,7 +177,7 @@ struct LeafSet {
     const int64_t *origin; // slot id h * n_slots + slot, per chunk row
     int64_t lo, hi;
 };
-enum LeafBin : uint8_t { LEAF_EMPTY = 0, LEAF_H0, LEAF_H1, LEAF_H2, LEAF_H3, LEAF_DENSE, LEAF_NBINS };
+enum LeafBin : uint8_t { LEAF_EMPTY = 0, LEAF_H0, LEAF_H1, LEAF_H2, LEAF_H3, LEAF_DENSE, LEAF_RANK, LEAF_NBINS };
 enum LightBin : uint8_t {
     LIGHT_EMPTY = 0, LIGHT_HEAVY, LIGHT_W0, LIGHT_W1, LIGHT_H0, LIGHT_H1, LIGHT_H2, LIGHT_H3, LIGHT_NBINS
 };
@@ -187,8 +187,9 @@ void light_classes_sym(const int64_t *ip, const int32_t *minc, const int32_t *ma
                        bool window, uint8_t *cls, hipStream_t s);
 void light_classes_num(const int64_t *ip, const int64_t *row_nnz, const int32_t *minc, const int32_t *maxc,
                        int64_t n, int64_t tau, bool window, uint8_t *cls, hipStream_t s);
-void leaf_classes_sym(const LeafSet &L, int64_t tau, uint8_t *cls, hipStream_t s);
-void leaf_classes_num(const LeafSet &L, const int64_t *leaf_nnz, int64_t tau, uint8_t *cls, hipStream_t s);
+void leaf_classes_sym(const LeafSet &L, int64_t tau, int width, uint8_t *cls, hipStream_t s);
+void leaf_classes_num(const LeafSet &L, const int64_t *leaf_nnz, int64_t tau, int width, uint8_t *cls,
+                      hipStream_t s);
 // Leaf symbolic: leaf_nnz[i] for the leaves items[0..n) (leaf i = chunk row
 // lo + i), and slot_cnt[origin] = leaf_nnz.
 void leaf_symbolic(const LeafSet &L, int bin, const int64_t *items, int64_t n, int width, int64_t *leaf_nnz,

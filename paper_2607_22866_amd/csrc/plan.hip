@@ -164,7 +164,8 @@ void compute_params(int64_t c_m, int64_t s_lm, const gmagnus_options_t *o, gmagn
     int64_t W = floor_pow2((8 * s_lm) / (ALPHA * (8 * S_VAL + 1)));
     if (o && o->tau > 0) tau = o->tau;
     if (o && o->dense_width_log2 > 0) {
-        GM_REQUIRE(o->dense_width_log2 <= MAX_DENSE_LOG2, GMAGNUS_ERROR_INVALID_VALUE, "dense width above 2^13");
+        GM_REQUIRE(o->dense_width_log2 >= 5 && o->dense_width_log2 <= MAX_DENSE_LOG2, GMAGNUS_ERROR_INVALID_VALUE,
+                   "dense width must be 2^5 .. 2^13");
         W = int64_t(1) << o->dense_width_log2;
     }
     W = std::min<int64_t>(W, int64_t(1) << MAX_DENSE_LOG2);
@@ -681,7 +682,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         {
             Timed t(p, GMAGNUS_K_SETUP, s);
             fill<int64_t>(lv.leaf_nnz, 0, nl, s);
-            leaf_classes_sym(lv.set, P.tau, lc, s);
+            leaf_classes_sym(lv.set, P.tau, lv.width, lc, s);
             partition_u8(lc, nl, LEAF_NBINS, lv.items_sym, nullptr, bins, sc, s);
             read_bins(bins, LEAF_NBINS, lv.bins_sym, s);
         }
@@ -692,11 +693,12 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         lv.elems = e1 - e0;
         {
             Timed t(p, GMAGNUS_K_CHUNK_SYM, s);
-            for (int b = LEAF_H0; b <= LEAF_DENSE; ++b) {
+            for (int b = LEAF_H0; b < LEAF_NBINS; ++b) {
                 const int64_t cnt = lv.bins_sym[b + 1] - lv.bins_sym[b];
                 leaf_symbolic(lv.set, b, lv.items_sym + lv.bins_sym[b], cnt, lv.width, lv.leaf_nnz, p->slot, s);
                 if (cnt) p->info.kernel_launches[GMAGNUS_K_CHUNK_SYM] += 1;
                 if (b == LEAF_DENSE) p->info.n_leaves_dense += cnt;
+                else if (b == LEAF_RANK) p->info.n_leaves_rank += cnt;
                 else p->info.n_leaves_hash += cnt;
             }
             add_bytes(p, GMAGNUS_K_CHUNK_SYM, 4.0 * lv.elems + 16.0 * nl);
@@ -704,7 +706,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         // numeric bins now, so the numeric phase needs no host round trip
         {
             Timed t(p, GMAGNUS_K_SETUP, s);
-            leaf_classes_num(lv.set, lv.leaf_nnz, P.tau, lc, s);
+            leaf_classes_num(lv.set, lv.leaf_nnz, P.tau, lv.width, lc, s);
             partition_u8(lc, nl, LEAF_NBINS, lv.items_num, nullptr, bins, sc, s);
             read_bins(bins, LEAF_NBINS, lv.bins_num, s);
         }
@@ -827,7 +829,7 @@ void do_numeric(gmagnus_plan_s *p, const int64_t *c_row_ptr, int32_t *c_col, dou
         const hipStream_t s = p->s_heavy;
         Timed t(p, GMAGNUS_K_CHUNK_NUM, s);
         for (auto &lv : p->leaves) {
-            for (int b = LEAF_H0; b <= LEAF_DENSE; ++b) {
+            for (int b = LEAF_H0; b < LEAF_NBINS; ++b) {
                 const int64_t cnt = lv.bins_num[b + 1] - lv.bins_num[b];
                 leaf_numeric(lv.set, b, lv.items_num + lv.bins_num[b], cnt, lv.width, lv.leaf_nnz, p->n_slots_log2,
                              p->heavy_rows, c_row_ptr, p->slot, p->slot_width_log2, c_col, c_val, p->err, s);

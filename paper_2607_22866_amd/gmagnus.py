@@ -65,7 +65,8 @@ class PlanInfo(ctypes.Structure):
                 ("products_heavy", ctypes.c_int64), ("n_slices", ctypes.c_int64), ("nnz_a_heavy", ctypes.c_int64),
                 ("level_rows_in", ctypes.c_int64 * MAX_LEVELS), ("level_elems_in", ctypes.c_int64 * MAX_LEVELS),
                 ("level_heavy_out", ctypes.c_int64 * MAX_LEVELS), ("levels_run", ctypes.c_int32),
-                ("n_leaves_dense", ctypes.c_int64), ("n_leaves_hash", ctypes.c_int64), ("c_nnz", ctypes.c_int64),
+                ("n_leaves_dense", ctypes.c_int64), ("n_leaves_hash", ctypes.c_int64),
+                ("n_leaves_rank", ctypes.c_int64), ("c_nnz", ctypes.c_int64),
                 ("c_nnz_heavy", ctypes.c_int64), ("check_flags", ctypes.c_int32),
                 ("kernel_ms", ctypes.c_double * len(K_NAMES)), ("kernel_launches", ctypes.c_int64 * len(K_NAMES)),
                 ("kernel_bytes", ctypes.c_double * len(K_NAMES))]
