@@ -83,6 +83,8 @@ typedef struct {
 #define GMAGNUS_FLAG_TIMING 1u         /* record per-phase device times (HIP events) into the plan info */
 #define GMAGNUS_FLAG_SERIAL_STREAMS 2u /* run heavy and light work on one stream (no concurrency) */
 #define GMAGNUS_FLAG_NO_WINDOW 4u      /* never use the dense-window accumulator for light rows */
+#define GMAGNUS_FLAG_PAPER_HISTOGRAM 8u /* level-0 histogram by a pass over C-hat's columns (the paper's
+                                           kernel) instead of from the structure of A and B */
 
 #define GMAGNUS_MAX_LEVELS 8
 

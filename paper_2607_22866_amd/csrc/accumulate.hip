@@ -281,6 +281,7 @@ constexpr int DENSE_MAX = 8192;          // columns of the LDS dense accumulator
 constexpr int RANK_MAX_LOG2 = 18;        // columns of the bitmap-rank accumulator
 constexpr int RANK_NNZ_MAX = 7168;       // distinct columns it holds (>= tau)
 constexpr int RANK_MIN_LEN = 256;        // smaller chunks go to the hash map
+constexpr int RANK_SMALL = 2048;         // distinct columns of the small rank variant
 
 // Accumulator of a final chunk of `len` elements over `width` columns:
 // heavy chunks (len > tau, width <= W) and well-filled narrow chunks use the
@@ -297,7 +298,7 @@ __global__ void k_leaf_classes(LeafSet L, const int64_t *leaf_nnz, int64_t tau, 
         else if (width <= DENSE_MAX && (len > tau || len >= width / 16))
             c = LEAF_DENSE;
         else if (width <= (1 << RANK_MAX_LOG2) && width >= 32 && len >= RANK_MIN_LEN)
-            c = LEAF_RANK;
+            c = (leaf_nnz && leaf_nnz[i] > RANK_SMALL) ? LEAF_RANK_L : LEAF_RANK;
         else
             c = (uint8_t)(LEAF_H0 + (leaf_nnz ? hash_bin_num(leaf_nnz[i]) : hash_bin_sym(len)));
         cls[i] = c;
@@ -431,6 +432,11 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_hash_num(LeafSet L, const int64_
     hash_emit_sorted<BLOCK, TS>(keys, vals, nnz, base, o.c_col + dst, o.c_val + dst, scan_sm, o.err);
 }
 
+// Elements of a chunk are read in batches of LEAF_EPT per thread, all loads
+// of a batch issued before any LDS update, so the global-memory latency is
+// paid once per batch rather than once per element.
+constexpr int LEAF_EPT = 8;
+
 template <int BLOCK>
 __global__ __launch_bounds__(BLOCK) void k_leaf_dense_sym(LeafSet L, const int64_t *items, int width,
                                                           int64_t *leaf_nnz, int64_t *slot_cnt) {
@@ -440,7 +446,17 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_dense_sym(LeafSet L, const int64
     const int64_t s = L.ptr[j], e = L.ptr[j + 1];
     dense_clear(D, width, false);
     __syncthreads();
-    for (int64_t t = s + threadIdx.x; t < e; t += BLOCK) dense_set(D, L.col[t]);
+    for (int64_t b = s; b < e; b += BLOCK * 2 * LEAF_EPT) {
+        int32_t c[2 * LEAF_EPT];
+#pragma unroll
+        for (int q = 0; q < 2 * LEAF_EPT; ++q) {
+            const int64_t t = b + q * BLOCK + threadIdx.x;
+            c[q] = t < e ? __builtin_nontemporal_load(&L.col[t]) : -1;
+        }
+#pragma unroll
+        for (int q = 0; q < 2 * LEAF_EPT; ++q)
+            if (c[q] >= 0) dense_set(D, c[q]);
+    }
     __syncthreads();
     const int32_t cnt = dense_count(D, width);
     if (threadIdx.x == 0) {
@@ -458,7 +474,19 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_dense_num(LeafSet L, const int64
     const int64_t s = L.ptr[j], e = L.ptr[j + 1];
     dense_clear(D, width, true);
     __syncthreads();
-    for (int64_t t = s + threadIdx.x; t < e; t += BLOCK) dense_add(D, L.col[t], L.val[t]);
+    for (int64_t b = s; b < e; b += BLOCK * LEAF_EPT) {
+        int32_t c[LEAF_EPT];
+        double v[LEAF_EPT];
+#pragma unroll
+        for (int q = 0; q < LEAF_EPT; ++q) {
+            const int64_t t = b + q * BLOCK + threadIdx.x;
+            c[q] = t < e ? __builtin_nontemporal_load(&L.col[t]) : -1;
+            v[q] = t < e ? __builtin_nontemporal_load(&L.val[t]) : 0.0;
+        }
+#pragma unroll
+        for (int q = 0; q < LEAF_EPT; ++q)
+            if (c[q] >= 0) dense_add(D, c[q], v[q]);
+    }
     __syncthreads();
     int64_t dst, cap;
     int32_t base;
@@ -472,105 +500,108 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_dense_num(LeafSet L, const int64
 // columns, an exclusive scan of the bitmap words' popcounts gives every
 // present column its rank, i.e. its position in the sorted output, and the
 // values are summed straight into a rank-indexed array. No hashing and no
-// sort; the output comes out in column order.
-template <int BLOCK>
-struct RankLds {
-    uint32_t bits[(1 << RANK_MAX_LOG2) / 32];
-    uint16_t wpre[(1 << RANK_MAX_LOG2) / 32];  // rank of each word's first bit
-    int32_t scan[BLOCK / GM_WAVE];
-};
+// sort; the output comes out in column order. A chunk is light (at most tau
+// elements), so its elements stay in registers between the two passes.
+constexpr int RANK_BLOCK = 512;
+constexpr int RANK_EPT = 16;  // RANK_BLOCK * RANK_EPT >= tau_limit()
 
-template <int BLOCK>
-GM_DEV void rank_mark(RankLds<BLOCK> &R, const int32_t *col, int64_t s, int64_t e, int nwords) {
-    for (int w = threadIdx.x; w < nwords; w += BLOCK) R.bits[w] = 0;
-    __syncthreads();
-    for (int64_t t = s + threadIdx.x; t < e; t += BLOCK) {
-        const int c = col[t];
-        const uint32_t bit = 1u << (c & 31);
-        if (!(((volatile uint32_t *)R.bits)[c >> 5] & bit)) atomicOr(&R.bits[c >> 5], bit);
+template <int BLOCK, int EPT>
+GM_DEV void rank_load(const LeafSet &L, int64_t s, int64_t e, int32_t (&c)[EPT], double (&v)[EPT], bool vals) {
+#pragma unroll
+    for (int q = 0; q < EPT; ++q) {
+        const int64_t t = s + q * BLOCK + threadIdx.x;
+        c[q] = t < e ? __builtin_nontemporal_load(&L.col[t]) : -1;
+        if (vals) v[q] = t < e ? __builtin_nontemporal_load(&L.val[t]) : 0.0;
     }
+}
+
+template <int BLOCK, int EPT>
+GM_DEV void rank_mark(uint32_t *bits, int nwords, const int32_t (&c)[EPT]) {
+    for (int w = threadIdx.x; w < nwords; w += BLOCK) bits[w] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < EPT; ++q)
+        if (c[q] >= 0) {
+            const uint32_t bit = 1u << (c[q] & 31);
+            if (!(((volatile uint32_t *)bits)[c[q] >> 5] & bit)) atomicOr(&bits[c[q] >> 5], bit);
+        }
     __syncthreads();
 }
 
-// Exclusive scan of word popcounts into wpre; returns the total. Thread t
-// owns the consecutive words [t*per, (t+1)*per).
-template <int BLOCK>
-GM_DEV int32_t rank_scan(RankLds<BLOCK> &R, int nwords) {
+template <int BLOCK, int NWORDS>
+__global__ __launch_bounds__(BLOCK) void k_leaf_rank_sym(LeafSet L, const int64_t *items, int width,
+                                                         int64_t *leaf_nnz, int64_t *slot_cnt) {
+    __shared__ uint32_t bits[NWORDS];
+    __shared__ int32_t scan_sm[BLOCK / GM_WAVE];
+    const int64_t i = items[blockIdx.x];
+    const int64_t j = L.lo + i;
+    const int nwords = width >> 5;
+    int32_t c[RANK_EPT];
+    double v[RANK_EPT];
+    rank_load<BLOCK, RANK_EPT>(L, L.ptr[j], L.ptr[j + 1], c, v, false);
+    rank_mark<BLOCK, RANK_EPT>(bits, nwords, c);
+    int32_t cnt = 0;
+    for (int w = threadIdx.x; w < nwords; w += BLOCK) cnt += __popc(bits[w]);
+    cnt = block_reduce_sum<BLOCK>(cnt, scan_sm);
+    if (threadIdx.x == 0) {
+        leaf_nnz[i] = cnt;
+        slot_cnt[L.origin[j]] = cnt;
+    }
+}
+
+template <int BLOCK, int NWORDS, int CAP>
+__global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const int64_t *items, const int64_t *leaf_nnz,
+                                                         int width, LeafOut o) {
+    __shared__ uint32_t bits[NWORDS];
+    __shared__ uint16_t wpre[NWORDS];  // rank of each word's first bit (ranks < CAP <= 65535)
+    __shared__ double vals[CAP];
+    __shared__ int32_t scan_sm[BLOCK / GM_WAVE];
+    const int64_t i = items[blockIdx.x];
+    const int64_t j = L.lo + i;
+    const int nwords = width >> 5;
+    int32_t c[RANK_EPT];
+    double v[RANK_EPT];
+    rank_load<BLOCK, RANK_EPT>(L, L.ptr[j], L.ptr[j + 1], c, v, true);
+    rank_mark<BLOCK, RANK_EPT>(bits, nwords, c);
+    // exclusive scan of the word popcounts; thread t owns words [t*per, (t+1)*per)
     const int per = (nwords + BLOCK - 1) / BLOCK;
     const int w0 = threadIdx.x * per;
     int32_t sum = 0;
     for (int q = 0; q < per; ++q)
-        if (w0 + q < nwords) sum += __popc(R.bits[w0 + q]);
+        if (w0 + q < nwords) sum += __popc(bits[w0 + q]);
     int32_t total;
-    int32_t run = block_excl_scan<BLOCK>(sum, R.scan, &total);
-    for (int q = 0; q < per; ++q)
-        if (w0 + q < nwords) {
-            R.wpre[w0 + q] = (uint16_t)run;
-            run += __popc(R.bits[w0 + q]);
-        }
-    __syncthreads();
-    return total;
-}
-
-template <int BLOCK>
-__global__ __launch_bounds__(BLOCK) void k_leaf_rank_sym(LeafSet L, const int64_t *items, int width,
-                                                         int64_t *leaf_nnz, int64_t *slot_cnt) {
-    __shared__ RankLds<BLOCK> R;
-    const int64_t i = items[blockIdx.x];
-    const int64_t j = L.lo + i;
-    const int nwords = width >> 5;
-    rank_mark(R, L.col, L.ptr[j], L.ptr[j + 1], nwords);
-    int32_t c = 0;
-    for (int w = threadIdx.x; w < nwords; w += BLOCK) c += __popc(R.bits[w]);
-    c = block_reduce_sum<BLOCK>(c, R.scan);
-    if (threadIdx.x == 0) {
-        leaf_nnz[i] = c;
-        slot_cnt[L.origin[j]] = c;
-    }
-}
-
-template <int BLOCK>
-__global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const int64_t *items, const int64_t *leaf_nnz,
-                                                         int width, LeafOut o) {
-    __shared__ RankLds<BLOCK> R;
-    __shared__ double vals[RANK_NNZ_MAX];
-    __shared__ int32_t cols[RANK_NNZ_MAX];
-    const int64_t i = items[blockIdx.x];
-    const int64_t j = L.lo + i;
-    const int64_t s = L.ptr[j], e = L.ptr[j + 1];
-    const int nwords = width >> 5;
-    rank_mark(R, L.col, s, e, nwords);
-    const int32_t total = rank_scan(R, nwords);
-    const int n = total < RANK_NNZ_MAX ? total : RANK_NNZ_MAX;
-    for (int q = threadIdx.x; q < n; q += BLOCK) vals[q] = 0.0;
-    // columns in rank order
-    for (int w = threadIdx.x; w < nwords; w += BLOCK) {
-        uint32_t b = R.bits[w];
-        int r = R.wpre[w];
-        while (b) {
-            const int bit = __ffs(b) - 1;
-            if (r < n) cols[r] = (w << 5) | bit;
-            ++r;
-            b &= b - 1;
-        }
-    }
-    __syncthreads();
-    for (int64_t t = s + threadIdx.x; t < e; t += BLOCK) {
-        const int c = L.col[t];
-        const int r = R.wpre[c >> 5] + __popc(R.bits[c >> 5] & ((1u << (c & 31)) - 1u));
-        if (r < n) __hip_atomic_fetch_add(&vals[r], L.val[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    }
-    __syncthreads();
+    const int32_t first = block_excl_scan<BLOCK>(sum, scan_sm, &total);
     int64_t dst, cap;
     int32_t base;
     leaf_target(o, L.origin[j], dst, cap, base);
     const int64_t nnz = leaf_nnz[i] < cap ? leaf_nnz[i] : cap;
-    if (threadIdx.x == 0 && (total != nnz || total > RANK_NNZ_MAX)) atomicOr(o.err, 4);
+    const int n = total < CAP ? total : CAP;
     const int m = n < nnz ? n : (int)nnz;
-    for (int q = threadIdx.x; q < m; q += BLOCK) {
-        o.c_col[dst + q] = cols[q] + base;
-        o.c_val[dst + q] = vals[q];
-    }
+    if (threadIdx.x == 0 && (total != nnz || total > CAP)) atomicOr(o.err, 4);
+    // ranks of the words; the columns go straight to C in rank order
+    int32_t r = first;
+    for (int q = 0; q < per; ++q)
+        if (w0 + q < nwords) {
+            const int w = w0 + q;
+            wpre[w] = (uint16_t)r;
+            uint32_t b = bits[w];
+            while (b) {
+                if (r < m) o.c_col[dst + r] = base + ((w << 5) | (__ffs(b) - 1));
+                ++r;
+                b &= b - 1;
+            }
+        }
+    for (int q = threadIdx.x; q < n; q += BLOCK) vals[q] = 0.0;
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < RANK_EPT; ++q)
+        if (c[q] >= 0) {
+            const int w = c[q] >> 5;
+            const int rk = wpre[w] + __popc(bits[w] & ((1u << (c[q] & 31)) - 1u));
+            if (rk < n) __hip_atomic_fetch_add(&vals[rk], v[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        }
+    __syncthreads();
+    for (int q = threadIdx.x; q < m; q += BLOCK) o.c_val[dst + q] = vals[q];
 }
 
 // -------------------------------------------------------------- slot scan
@@ -685,8 +716,10 @@ void leaf_symbolic(const LeafSet &L, int bin, const int64_t *items, int64_t n, i
         launch_items(k_leaf_dense_sym<512>, 512, n, s, L, items, width, leaf_nnz, slot_cnt);
         break;
     case LEAF_RANK:
+    case LEAF_RANK_L:
         GM_REQUIRE(n <= 0 || width <= (1 << RANK_MAX_LOG2), GMAGNUS_ERROR_UNSUPPORTED, "rank bitmap too wide");
-        launch_items(k_leaf_rank_sym<512>, 512, n, s, L, items, width, leaf_nnz, slot_cnt);
+        launch_items(k_leaf_rank_sym<RANK_BLOCK, (1 << RANK_MAX_LOG2) / 32>, RANK_BLOCK, n, s, L, items, width,
+                     leaf_nnz, slot_cnt);
         break;
     default: break;
     }
@@ -706,9 +739,22 @@ void leaf_numeric(const LeafSet &L, int bin, const int64_t *items, int64_t n, in
         launch_items(k_leaf_dense_num<512>, 512, n, s, L, items, leaf_nnz, width, o);
         break;
     case LEAF_RANK:
+    case LEAF_RANK_L: {
         GM_REQUIRE(n <= 0 || width <= (1 << RANK_MAX_LOG2), GMAGNUS_ERROR_UNSUPPORTED, "rank bitmap too wide");
-        launch_items(k_leaf_rank_num<512>, 512, n, s, L, items, leaf_nnz, width, o);
+        constexpr int W17 = (1 << 17) / 32, W18 = (1 << 18) / 32;
+        const bool narrow = width <= (1 << 17);
+        if (bin == LEAF_RANK && narrow)
+            launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_SMALL>, RANK_BLOCK, n, s, L, items, leaf_nnz, width, o);
+        else if (bin == LEAF_RANK)
+            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_SMALL>, RANK_BLOCK, n, s, L, items, leaf_nnz, width, o);
+        else if (narrow)
+            launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_NNZ_MAX>, RANK_BLOCK, n, s, L, items, leaf_nnz, width,
+                         o);
+        else
+            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_NNZ_MAX>, RANK_BLOCK, n, s, L, items, leaf_nnz, width,
+                         o);
         break;
+    }
     default: break;
     }
 }

@@ -128,6 +128,12 @@ void slice_build(const Csr &B, const int64_t *colcnt, const int64_t *slice_perm,
 void csc_fill(const Csr &A, const Csr &B, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
               const int64_t *a_heavy_ptr, int64_t nnz_heavy_all, const int32_t *k_to_slice,
               const int64_t *col_ptr, int64_t *fill_cursor, int32_t *row_h, double *a_val, hipStream_t s);
+// Level-0 histogram from the structure: per-slice chunk counts of its B row,
+// then per heavy row the sum over its A~ entries (counts: n_heavy * nc).
+void slice_chunk_hist(const Csr &B, const SliceArrays &sl, int nc, int shift, int32_t *hist, hipStream_t s);
+void struct_hist(const Csr &A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0, const int64_t *a_heavy_ptr,
+                 int64_t nnz_heavy_all, const int32_t *k_to_slice, const int32_t *hist, int nc, int64_t *counts,
+                 hipStream_t s);
 void gather_row_len(const int64_t *row_ptr, const int64_t *rows, int64_t n, int64_t r0, int64_t *out, hipStream_t s);
 void gather_i64(const int64_t *src, const int64_t *idx, int64_t n, int64_t *out, hipStream_t s);
 
@@ -177,7 +183,9 @@ struct LeafSet {
     const int64_t *origin; // slot id h * n_slots + slot, per chunk row
     int64_t lo, hi;
 };
-enum LeafBin : uint8_t { LEAF_EMPTY = 0, LEAF_H0, LEAF_H1, LEAF_H2, LEAF_H3, LEAF_DENSE, LEAF_RANK, LEAF_NBINS };
+enum LeafBin : uint8_t {
+    LEAF_EMPTY = 0, LEAF_H0, LEAF_H1, LEAF_H2, LEAF_H3, LEAF_DENSE, LEAF_RANK, LEAF_RANK_L, LEAF_NBINS
+};
 enum LightBin : uint8_t {
     LIGHT_EMPTY = 0, LIGHT_HEAVY, LIGHT_W0, LIGHT_W1, LIGHT_H0, LIGHT_H1, LIGHT_H2, LIGHT_H3, LIGHT_NBINS
 };

@@ -25,10 +25,9 @@ namespace gm {
 
 namespace {
 
-constexpr int MS_KMAX = 256;      // keys = group_rows * n_chunks (powers of two)
+constexpr int MS_KMAX = 1024;     // keys = group_rows * n_chunks (powers of two)
 constexpr int MS_RMAX = 16;       // rows per tile
 constexpr int MS_NEXT_MAX = 64;   // next-level chunks for the fused histogram
-constexpr int MS_NEXT_KEYS = 64;  // keys whose next-level histogram stays in LDS
 
 // Row containing the first element of every tile.
 __global__ void k_tile_rows(const int64_t *in_ptr, int64_t n_in, int64_t te, int64_t n_tiles, int64_t *tile_row) {
@@ -73,6 +72,29 @@ __global__ __launch_bounds__(BLOCK) void k_histogram(int64_t n_in, int64_t elems
     }
 }
 
+// Dynamic LDS layout of one multisplit work group (byte offsets); the
+// arrays whose size depends on the level (keys, next-level histogram) are
+// sized exactly, so small levels leave room for more work groups per CU.
+struct MsLayout {
+    int val, key_delta, key_out, rb, col, whist, key_start, next_hist, scan, total;
+};
+
+__host__ __device__ inline MsLayout ms_layout(int te, int nw, int K, int next, int R) {
+    MsLayout L;
+    int o = 0;
+    L.val = o;        o += 8 * te;
+    L.key_delta = o;  o += 8 * K;
+    L.key_out = o;    o += 8 * K;
+    L.rb = o;         o += 8 * (R + 1);
+    L.col = o;        o += 4 * te;
+    L.whist = o;      o += 4 * nw * K;
+    L.key_start = o;  o += 4 * (K + 1);
+    L.next_hist = o;  o += 4 * K * next;
+    L.scan = o;       o += 4 * nw;
+    L.total = o;
+    return L;
+}
+
 template <int BLOCK, int TE>
 __global__ __launch_bounds__(BLOCK) void k_multisplit(int64_t n_in, int64_t elems, const int64_t *in_ptr,
                                                       const int64_t *tile_row, int64_t n_tiles,
@@ -83,28 +105,32 @@ __global__ __launch_bounds__(BLOCK) void k_multisplit(int64_t n_in, int64_t elem
                                                       int64_t *next_counts) {
     constexpr int NW = BLOCK / GM_WAVE;
     constexpr int E = TE / BLOCK;
-    __shared__ int32_t col_buf[TE];
-    __shared__ double val_buf[TE];
-    __shared__ int32_t whist[NW * MS_KMAX];  // [wave][key] counts, then offsets
-    __shared__ int32_t key_start[MS_KMAX + 1];
-    __shared__ int64_t key_delta[MS_KMAX];   // global position - local position
-    __shared__ int64_t key_out[MS_KMAX];     // output chunk row
-    __shared__ int32_t next_hist[MS_NEXT_KEYS * MS_NEXT_MAX];
-    __shared__ int64_t rb[MS_RMAX + 1];
-    __shared__ int32_t scan_sm[NW];
+    extern __shared__ __align__(16) unsigned char ms_smem[];
+    const int K = R << cbits;
+    const bool fuse_next = next_counts != nullptr;
+    const MsLayout Lo = ms_layout(TE, NW, K, fuse_next ? next_chunks : 0, R);
+    double *val_buf = (double *)(ms_smem + Lo.val);
+    int64_t *key_delta = (int64_t *)(ms_smem + Lo.key_delta);  // global position - local position
+    int64_t *key_out = (int64_t *)(ms_smem + Lo.key_out);      // output chunk row
+    int64_t *rb = (int64_t *)(ms_smem + Lo.rb);
+    int32_t *col_buf = (int32_t *)(ms_smem + Lo.col);
+    int32_t *whist = (int32_t *)(ms_smem + Lo.whist);  // [wave][key] counts, then offsets
+    int32_t *key_start = (int32_t *)(ms_smem + Lo.key_start);
+    int32_t *next_hist = (int32_t *)(ms_smem + Lo.next_hist);
+    int32_t *scan_sm = (int32_t *)(ms_smem + Lo.scan);
 
     const int tid = threadIdx.x, lane = tid & (GM_WAVE - 1), w = tid / GM_WAVE;
     const int64_t tile = xcd_tile(blockIdx.x, n_tiles);
     const int64_t g0 = tile * (int64_t)TE;
     const int n = (int)(elems - g0 < TE ? elems - g0 : TE);
     const int64_t r0 = tile_row[tile];
-    const int K = R << cbits;
     const int kbits = rbits + cbits;
     const int32_t mask = (int32_t)((1u << shift) - 1u);
-    const bool fuse_next = next_counts != nullptr;
 
     if (tid <= R) rb[tid] = r0 + tid <= n_in ? in_ptr[r0 + tid] : INT64_MAX;
-    for (int k = tid; k < NW * MS_KMAX; k += BLOCK) whist[k] = 0;
+    for (int k = tid; k < NW * K; k += BLOCK) whist[k] = 0;
+    if (fuse_next)
+        for (int q = tid; q < K * next_chunks; q += BLOCK) next_hist[q] = 0;
     __syncthreads();
 
     int32_t col[E];
@@ -120,7 +146,7 @@ __global__ __launch_bounds__(BLOCK) void k_multisplit(int64_t n_in, int64_t elem
         key[j] = valid ? (local_row(rb, R, g0 + p) << cbits) | (col[j] >> shift) : -1;
     }
     // ranks inside (wave, key) buckets from ballots
-    int32_t *wh = whist + w * MS_KMAX;
+    int32_t *wh = whist + w * K;
 #pragma unroll
     for (int j = 0; j < E; ++j) {
         const int k = key[j];
@@ -149,13 +175,13 @@ __global__ __launch_bounds__(BLOCK) void k_multisplit(int64_t n_in, int64_t elem
         int sum = 0;
         for (int q = 0; q < per; ++q) {
             const int idx = tid * per + q;
-            if (idx < M) sum += whist[(idx % NW) * MS_KMAX + idx / NW];
+            if (idx < M) sum += whist[(idx % NW) * K + idx / NW];
         }
         int run = block_excl_scan<BLOCK>(sum, scan_sm);
         for (int q = 0; q < per; ++q) {
             const int idx = tid * per + q;
             if (idx < M) {
-                const int a = (idx % NW) * MS_KMAX + idx / NW;
+                const int a = (idx % NW) * K + idx / NW;
                 const int v = whist[a];
                 whist[a] = run;
                 if (idx % NW == 0) key_start[idx / NW] = run;
@@ -177,13 +203,11 @@ __global__ __launch_bounds__(BLOCK) void k_multisplit(int64_t n_in, int64_t elem
             key_out[k] = orow;
         }
     }
-    if (fuse_next)
-        for (int q = tid; q < K * next_chunks; q += BLOCK) next_hist[q] = 0;
     // permute into LDS
 #pragma unroll
     for (int j = 0; j < E; ++j) {
         if (key[j] >= 0) {
-            const int pos = whist[w * MS_KMAX + key[j]] + rank[j];
+            const int pos = wh[key[j]] + rank[j];
             col_buf[pos] = col[j];
             val_buf[pos] = val[j];
         }
@@ -230,7 +254,13 @@ __global__ void k_chunk_reorder(const int64_t *counts, const int64_t *inv, int64
     }
 }
 
-constexpr int64_t MS_TILES[3] = {8192, 2048, 512};
+constexpr int64_t MS_TILES[3] = {4096, 2048, 512};
+constexpr int MS_LDS_MAX = 160 * 1024;
+
+template <int BLOCK, int TE>
+int ms_lds_bytes(int K, int next, int R) {
+    return ms_layout(TE, BLOCK / GM_WAVE, K, next, R).total;
+}
 
 template <int BLOCK, int TE>
 void launch_multisplit(const LevelGeom &g, const int64_t *in_ptr, const int64_t *tile_row, const int32_t *in_col,
@@ -239,9 +269,18 @@ void launch_multisplit(const LevelGeom &g, const int64_t *in_ptr, const int64_t 
                        hipStream_t s) {
     const int64_t n_tiles = (g.elems + TE - 1) / TE;
     GM_REQUIRE(n_tiles < (int64_t)1 << 31, GMAGNUS_ERROR_UNSUPPORTED, "multisplit: too many tiles");
-    hipLaunchKernelGGL((k_multisplit<BLOCK, TE>), dim3((unsigned)n_tiles), dim3(BLOCK), 0, s, g.n_in, g.elems, in_ptr,
-                       tile_row, n_tiles, in_col, in_val, g.n_chunks, cbits, g.shift, g.group_rows, rbits, x_map,
-                       cursor, out_col, out_val, n_heavy_out, g.next_chunks, g.next_shift, next_counts);
+    const int K = g.group_rows << cbits;
+    const int lds = ms_lds_bytes<BLOCK, TE>(K, next_counts ? g.next_chunks : 0, g.group_rows);
+    GM_REQUIRE(lds <= MS_LDS_MAX, GMAGNUS_ERROR_UNSUPPORTED, "multisplit: work-group LDS above 160 KB");
+    static bool attr_set = false;
+    if (!attr_set) {
+        GM_HIP(hipFuncSetAttribute((const void *)k_multisplit<BLOCK, TE>,
+                                   hipFuncAttributeMaxDynamicSharedMemorySize, MS_LDS_MAX));
+        attr_set = true;
+    }
+    hipLaunchKernelGGL((k_multisplit<BLOCK, TE>), dim3((unsigned)n_tiles), dim3(BLOCK), lds, s, g.n_in, g.elems,
+                       in_ptr, tile_row, n_tiles, in_col, in_val, g.n_chunks, cbits, g.shift, g.group_rows, rbits,
+                       x_map, cursor, out_col, out_val, n_heavy_out, g.next_chunks, g.next_shift, next_counts);
     GM_CHECK_LAUNCH();
 }
 
@@ -252,7 +291,7 @@ int64_t multisplit_tile_elems(int i) { return MS_TILES[i]; }
 int multisplit_max_keys() { return MS_KMAX; }
 int multisplit_max_rows() { return MS_RMAX; }
 bool multisplit_next_fits(int keys, int next_chunks) {
-    return next_chunks <= MS_NEXT_MAX && keys * next_chunks <= MS_NEXT_KEYS * MS_NEXT_MAX;
+    return next_chunks <= MS_NEXT_MAX && 4 * keys * next_chunks <= 32 * 1024;
 }
 
 void histogram(const LevelGeom &g, const int64_t *in_ptr, const int64_t *tile_row, const int32_t *in_col,
@@ -306,12 +345,12 @@ void multisplit(const LevelGeom &g, const int64_t *in_ptr, const int64_t *tile_r
                    "multisplit: next-level histogram does not fit");
     int64_t *nc = fuse ? next_counts : nullptr;
     switch (g.group_elems) {
-    case 8192:
-        launch_multisplit<512, 8192>(g, in_ptr, tile_row, in_col, in_val, x_map, cursor, out_col, out_val,
+    case 4096:
+        launch_multisplit<256, 4096>(g, in_ptr, tile_row, in_col, in_val, x_map, cursor, out_col, out_val,
                                      n_heavy_out, nc, cbits, rbits, s);
         break;
     case 2048:
-        launch_multisplit<512, 2048>(g, in_ptr, tile_row, in_col, in_val, x_map, cursor, out_col, out_val,
+        launch_multisplit<256, 2048>(g, in_ptr, tile_row, in_col, in_val, x_map, cursor, out_col, out_val,
                                      n_heavy_out, nc, cbits, rbits, s);
         break;
     case 512:

@@ -466,6 +466,9 @@ void heavy_symbolic(gmagnus_plan_s *p) {
     p->n_slots_log2 = ilog2(p->n_slots);
     p->slot_width_log2 = c_bits - p->n_slots_log2;
 
+    const bool paper_hist = (p->opts.flags & GMAGNUS_FLAG_PAPER_HISTOGRAM) != 0;
+    int64_t *counts0 = nullptr;  // level-0 counts when computed from the structure
+
     // ---- masked CSR -> CSC of the heavy rows and slice offsets
     SliceArrays sl;
     int64_t *row_len, *a_heavy_ptr, *scratch;
@@ -512,6 +515,20 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         sl.a_val = ws.alloc<double>(sl.nnz);
         csc_fill(p->A, p->B, p->heavy_rows, nh, p->r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, sl.col_ptr, cursor,
                  sl.row_h, sl.a_val, s);
+        if (P.n_levels > 0 && !paper_hist) {
+            // level-0 (row, chunk) counts from the structure of A~ and B
+            Timed t2(p, GMAGNUS_K_HISTOGRAM, s);
+            const int nc0 = P.v_chunks[0];
+            const int shift0 = c_bits - ilog2(nc0);
+            int32_t *shist = ws.alloc<int32_t>(sl.n_slices * nc0);
+            counts0 = ws.alloc<int64_t>(nh * nc0);
+            slice_chunk_hist(p->B, sl, nc0, shift0, shist, s);
+            struct_hist(p->A, p->heavy_rows, nh, p->r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, shist, nc0, counts0,
+                        s);
+            ws.free(shist);
+            p->info.kernel_launches[GMAGNUS_K_HISTOGRAM] += 1;
+            add_bytes(p, GMAGNUS_K_HISTOGRAM, 12.0 * nnz_heavy_all + 4.0 * sl.n_slices * nc0 + 8.0 * nh * nc0);
+        }
         // compulsory bytes of B~ (each slice's B row once): sum of nnz(B[k,:]) over slices
         blen_total = 0;
         ws.free(cursor);
@@ -603,7 +620,10 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         int64_t *out_ptr = ws.alloc<int64_t>(n_out + 1);
         uint8_t *ccls = ws.alloc<uint8_t>(n_out);
         tile_rows(g, in_ptr, tile_row, s);
-        if (lvl == 0) {
+        if (lvl == 0 && counts0) {
+            counts = counts0;
+        } else if (lvl == 0) {
+            // the paper's histogram kernel: one pass over the columns of C-hat
             Timed t(p, GMAGNUS_K_HISTOGRAM, s);
             counts = ws.alloc<int64_t>(n_out);
             histogram(g, in_ptr, tile_row, col_buf[cur], counts, s);
@@ -698,7 +718,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                 leaf_symbolic(lv.set, b, lv.items_sym + lv.bins_sym[b], cnt, lv.width, lv.leaf_nnz, p->slot, s);
                 if (cnt) p->info.kernel_launches[GMAGNUS_K_CHUNK_SYM] += 1;
                 if (b == LEAF_DENSE) p->info.n_leaves_dense += cnt;
-                else if (b == LEAF_RANK) p->info.n_leaves_rank += cnt;
+                else if (b == LEAF_RANK || b == LEAF_RANK_L) p->info.n_leaves_rank += cnt;
                 else p->info.n_leaves_hash += cnt;
             }
             add_bytes(p, GMAGNUS_K_CHUNK_SYM, 4.0 * lv.elems + 16.0 * nl);

@@ -136,6 +136,85 @@ __global__ __launch_bounds__(FLAT_BLOCK) void k_csc_fill(Csr A, const int64_t *h
     });
 }
 
+// Level-0 chunk counts of every slice's B row: hist[s * nc + c] = number of
+// columns of B[k,:] in [c << shift, (c + 1) << shift). The row is sorted, so
+// lane c of a wave finds the row's first column >= c << shift by binary
+// search and the counts are differences of neighbouring lanes.
+__global__ __launch_bounds__(256) void k_slice_chunk_hist(Csr B, const int32_t *slice_k, int64_t n_slices, int nc,
+                                                          int shift, int32_t *hist) {
+    const int lane = threadIdx.x & (GM_WAVE - 1);
+    const int64_t nwaves = (int64_t)gridDim.x * (blockDim.x / GM_WAVE);
+    for (int64_t s = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / GM_WAVE; s < n_slices; s += nwaves) {
+        const int32_t k = slice_k[s];
+        const int64_t b0 = B.rp[k], b1 = B.rp[k + 1];
+        int64_t lo = b0, hi = b1;
+        if (lane <= nc) {
+            const int64_t bound = (int64_t)lane << shift;
+            while (lo < hi) {
+                const int64_t mid = lo + ((hi - lo) >> 1);
+                if ((int64_t)B.ci[mid] < bound)
+                    lo = mid + 1;
+                else
+                    hi = mid;
+            }
+        }
+        const int64_t next = __shfl_down(lo, 1, GM_WAVE);
+        if (lane < nc) hist[s * nc + lane] = (int32_t)(next - lo);
+    }
+}
+
+// Level-0 histogram from the structure (Algorithm 3, Histogram at the first
+// level): the C-hat row of heavy row h is the union of the B rows of its
+// A~ entries, so counts[h * nc + c] = sum over those entries of the slice
+// histograms above. Each wave walks SH_ENTRIES consecutive A~ entries in
+// row-major order, lane c accumulating chunk c, and flushes at row ends.
+constexpr int SH_ENTRIES = 256;
+
+__global__ __launch_bounds__(256) void k_struct_hist(Csr A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
+                                                     const int64_t *a_heavy_ptr, int64_t total,
+                                                     const int32_t *k_to_slice, const int32_t *hist, int nc,
+                                                     int64_t *counts) {
+    const int lane = threadIdx.x & (GM_WAVE - 1);
+    const int64_t wid = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / GM_WAVE;
+    const int64_t e0 = wid * SH_ENTRIES;
+    if (e0 >= total) return;  // uniform across the wave
+    const int64_t e1 = e0 + SH_ENTRIES < total ? e0 + SH_ENTRIES : total;
+    int64_t cur = find_row(a_heavy_ptr, 0, n_heavy + 1, e0);  // row of the wave's first entry
+    int64_t acc = 0;
+    int64_t h = cur, h_end = a_heavy_ptr[h + 1];
+    int64_t a_base = A.rp[r0 + heavy_rows[h]] - a_heavy_ptr[h];
+    for (int64_t eb = e0; eb < e1; eb += GM_WAVE) {
+        // lane l resolves entry eb + l: its heavy row and slice
+        const int64_t e = eb + lane;
+        int32_t s = -1;
+        if (e < e1) {
+            while (e >= h_end) {
+                ++h;
+                h_end = a_heavy_ptr[h + 1];
+                a_base = A.rp[r0 + heavy_rows[h]] - a_heavy_ptr[h];
+            }
+            s = k_to_slice[A.ci[a_base + e]];
+        }
+        const int cnt = (int)(e1 - eb < GM_WAVE ? e1 - eb : GM_WAVE);
+        for (int q = 0; q < cnt; ++q) {
+            const int64_t hq = __shfl(h, q, GM_WAVE);
+            const int32_t sq = __shfl(s, q, GM_WAVE);
+            if (hq != cur) {
+                if (lane < nc && acc)
+                    atomicAdd((unsigned long long *)&counts[cur * nc + lane], (unsigned long long)acc);
+                acc = 0;
+                cur = hq;
+            }
+            if (sq >= 0 && lane < nc) acc += hist[(int64_t)sq * nc + lane];
+        }
+        // lanes past the last entry may have stopped walking; realign for the next group
+        h = __shfl(h, cnt - 1, GM_WAVE);
+        h_end = a_heavy_ptr[h + 1];
+        a_base = A.rp[r0 + heavy_rows[h]] - a_heavy_ptr[h];
+    }
+    if (lane < nc && acc) atomicAdd((unsigned long long *)&counts[cur * nc + lane], (unsigned long long)acc);
+}
+
 __global__ void k_gather_row_len(const int64_t *row_ptr, const int64_t *rows, int64_t n, int64_t r0, int64_t *out) {
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
         const int64_t r = r0 + rows[i];
@@ -207,6 +286,25 @@ void csc_fill(const Csr &A, const Csr &B, const int64_t *heavy_rows, int64_t n_h
     if (n_heavy <= 0 || nnz_heavy_all <= 0) return;
     hipLaunchKernelGGL(k_csc_fill, dim3(flat_grid(nnz_heavy_all)), dim3(FLAT_BLOCK), 0, s, A, heavy_rows, n_heavy,
                        r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, col_ptr, fill_cursor, row_h, a_val);
+    GM_CHECK_LAUNCH();
+}
+
+void slice_chunk_hist(const Csr &B, const SliceArrays &sl, int nc, int shift, int32_t *hist, hipStream_t s) {
+    if (sl.n_slices <= 0) return;
+    GM_REQUIRE(nc >= 1 && nc < GM_WAVE, GMAGNUS_ERROR_UNSUPPORTED, "level-0 chunk count must be below 64");
+    hipLaunchKernelGGL(k_slice_chunk_hist, dim3(grid_for(sl.n_slices, 4, 65536)), dim3(256), 0, s, B, sl.slice_k,
+                       sl.n_slices, nc, shift, hist);
+    GM_CHECK_LAUNCH();
+}
+
+void struct_hist(const Csr &A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0, const int64_t *a_heavy_ptr,
+                 int64_t nnz_heavy_all, const int32_t *k_to_slice, const int32_t *hist, int nc, int64_t *counts,
+                 hipStream_t s) {
+    fill<int64_t>(counts, 0, n_heavy * nc, s);
+    if (n_heavy <= 0 || nnz_heavy_all <= 0) return;
+    const int64_t waves = (nnz_heavy_all + SH_ENTRIES - 1) / SH_ENTRIES;
+    hipLaunchKernelGGL(k_struct_hist, dim3(grid_for(waves, 4, (int64_t)1 << 30)), dim3(256), 0, s, A, heavy_rows,
+                       n_heavy, r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, hist, nc, counts);
     GM_CHECK_LAUNCH();
 }
 

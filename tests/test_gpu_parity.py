@@ -72,6 +72,14 @@ def test_rmat12_every_depth(g, opts, levels):
         assert info.levels_run >= 1
 
 
+@pytest.mark.parametrize("opts,levels", DEPTHS[1:])
+def test_rmat12_paper_histogram(g, opts, levels):
+    # the level-0 histogram as a pass over C-hat's columns gives the same C
+    A = RMAT12.make()
+    info = check(g, A, A, flags=8, **opts)
+    assert info.params.levels == levels
+
+
 def test_rmat12_integer_values_bit_exact(g):
     A = wl.rmat(12, 8, 0.57, 0.19, 0.19, 12, values="int3")
     for opts in ({}, dict(tau=200, dense_width_log2=6, chunks_max_log2=2)):
