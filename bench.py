@@ -66,6 +66,25 @@ def run_step(g, dA, bounds, timing, acc, c_bufs):
     return products, nnz
 
 
+def copy_peak(torch, nbytes=4 << 30, reps=5):
+    """Device-to-device copy bandwidth (read + write bytes / time): the measured
+    peak the paper divides by in its speed-of-light comparison."""
+    src = torch.ones(nbytes // 8, dtype=torch.float64, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    gbs = 2.0 * nbytes * reps / (a.elapsed_time(b) / 1000.0) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    return gbs
+
+
 def cpu_baseline(A, ip, budget_products, seed=0):
     """Times the oracle on a random sample of rows (about budget_products products)."""
     import numpy as np
@@ -99,7 +118,7 @@ def main():
     ap.add_argument("--config", default="rmat22", choices=sorted(WORKLOADS))
     ap.add_argument("--panel-products", type=float, default=4e9,
                     help="maximum intermediate products per row panel")
-    ap.add_argument("--cpu-products", type=float, default=3e8, help="oracle sample size for the CPU baseline")
+    ap.add_argument("--cpu-products", type=float, default=4e8, help="oracle sample size for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -124,6 +143,8 @@ def main():
     log("generated %s: n=%d nnz=%d in %.1fs" % (args.config, A.n_rows, A.nnz, time.perf_counter() - t0))
     dA = g.DeviceCSR.from_host(A)
     torch.cuda.synchronize()
+    copy_gbs = copy_peak(torch)
+    log("device copy bandwidth %.0f GB/s" % copy_gbs)
 
     bounds = g.split_panels(dA, dA, int(args.panel_products))
     log("%d row panels (max %.2g products each)" % (len(bounds) - 1, args.panel_products))
@@ -189,6 +210,9 @@ def main():
                    "panel_products": args.panel_products},
         "achieved_hbm_gbs": {"heavy_path_kernels": heavy_gb / (heavy_ms / 1000.0) if heavy_ms else None,
                              "heavy_path_frac": (heavy_gb / (heavy_ms / 1000.0)) / HBM_PEAK_GBS if heavy_ms else None,
+                             "heavy_path_frac_of_copy": (heavy_gb / (heavy_ms / 1000.0)) / copy_gbs
+                             if heavy_ms else None,
+                             "copy_peak": copy_gbs,
                              "all_kernels": all_gb / (all_ms / 1000.0) if all_ms else None,
                              "end_to_end": all_gb / (elapsed / args.steps)},
         "roofline": roofline,
