@@ -24,6 +24,8 @@ GM_DEV uint64_t lanemask_lt() { return (uint64_t(1) << lane_id()) - 1; }
 
 GM_DEV uint64_t ballot(bool p) { return __ballot(p); }
 
+GM_DEV int ilog2_dev(int x) { return 31 - __clz(x); }
+
 // Orders this lane's earlier LDS accesses before its later ones as seen by
 // the other lanes of the wave (lanes of a wave run in lockstep).
 GM_DEV void wave_lds_fence() {

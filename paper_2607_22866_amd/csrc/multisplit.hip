@@ -124,8 +124,8 @@ __global__ __launch_bounds__(BLOCK) void k_multisplit(int64_t n_in, int64_t elem
     const int64_t g0 = tile * (int64_t)TE;
     const int n = (int)(elems - g0 < TE ? elems - g0 : TE);
     const int64_t r0 = tile_row[tile];
-    const int kbits = rbits + cbits;
     const int32_t mask = (int32_t)((1u << shift) - 1u);
+    (void)rbits;
 
     if (tid <= R) rb[tid] = r0 + tid <= n_in ? in_ptr[r0 + tid] : INT64_MAX;
     for (int k = tid; k < NW * K; k += BLOCK) whist[k] = 0;
@@ -145,26 +145,35 @@ __global__ __launch_bounds__(BLOCK) void k_multisplit(int64_t n_in, int64_t elem
         val[j] = valid ? __builtin_nontemporal_load(&in_val[g0 + p]) : 0.0;
         key[j] = valid ? (local_row(rb, R, g0 + p) << cbits) | (col[j] >> shift) : -1;
     }
-    // ranks inside (wave, key) buckets from ballots
+    // Ranks inside (wave, key) buckets. Rows of C-hat are made of sorted B-row
+    // segments, so equal keys come in runs over consecutive lanes: each run's
+    // first lane reserves the run's length in the wave-private counter with
+    // one LDS atomic and the run's lanes take consecutive ranks. The next
+    // level's (key, sub-chunk) counts are taken the same way, per run.
     int32_t *wh = whist + w * K;
+    const uint64_t le_mask = lanemask_lt() | (uint64_t(1) << lane);
 #pragma unroll
     for (int j = 0; j < E; ++j) {
         const int k = key[j];
-        const bool valid = k >= 0;
-        uint64_t peers = ballot(valid);
-        for (int b = 0; b < kbits; ++b) {
-            const bool bit = (k >> b) & 1;
-            const uint64_t m = ballot(bit);
-            peers &= bit ? m : ~m;
-        }
+        const int kprev = __shfl_up(k, 1, GM_WAVE);
+        const uint64_t starts = ballot(lane == 0 || k != kprev);
+        const int first = 63 - __clzll((long long)(starts & le_mask));
+        const uint64_t above = starts & ~le_mask;
+        const int len = (above ? __ffsll((long long)above) - 1 : GM_WAVE) - first;
         int base = 0;
-        if (valid) {
-            base = wh[k];
-            rank[j] = base + __popcll(peers & lanemask_lt());
+        if (k >= 0 && lane == first) base = atomicAdd(&wh[k], len);
+        base = __shfl(base, first, GM_WAVE);
+        rank[j] = base + (lane - first);
+        if (fuse_next) {
+            const int k2 = k >= 0 ? k * next_chunks + ((col[j] & mask) >> next_shift) : -1;
+            const int k2prev = __shfl_up(k2, 1, GM_WAVE);
+            const uint64_t s2 = ballot(lane == 0 || k2 != k2prev);
+            const uint64_t a2 = s2 & ~le_mask;
+            if (k2 >= 0 && ((s2 >> lane) & 1)) {
+                const int len2 = (a2 ? __ffsll((long long)a2) - 1 : GM_WAVE) - lane;
+                atomicAdd(&next_hist[k2], len2);
+            }
         }
-        wave_lds_fence();
-        if (valid && lane == __ffsll((long long)peers) - 1) wh[k] = base + __popcll(peers);
-        wave_lds_fence();
     }
     __syncthreads();
 
@@ -225,14 +234,13 @@ __global__ __launch_bounds__(BLOCK) void k_multisplit(int64_t n_in, int64_t elem
         const int32_t lc = c & mask;
         __builtin_nontemporal_store(lc, &out_col[d]);
         __builtin_nontemporal_store(val_buf[p], &out_val[d]);
-        if (fuse_next && key_out[k] < n_heavy_out) atomicAdd(&next_hist[k * next_chunks + (lc >> next_shift)], 1);
     }
     if (fuse_next) {
-        __syncthreads();
+        // counts of the chunks that stay heavy go to the next level
         for (int q = tid; q < K * next_chunks; q += BLOCK) {
             const int v = next_hist[q];
-            if (v) {
-                const int k = q / next_chunks;
+            const int k = q / next_chunks;
+            if (v && key_out[k] < n_heavy_out) {
                 atomicAdd((unsigned long long *)&next_counts[key_out[k] * next_chunks + q % next_chunks],
                           (unsigned long long)v);
             }
@@ -254,7 +262,8 @@ __global__ void k_chunk_reorder(const int64_t *counts, const int64_t *inv, int64
     }
 }
 
-constexpr int64_t MS_TILES[3] = {4096, 2048, 512};
+constexpr int MS_NTILES = 4;
+constexpr int64_t MS_TILES[MS_NTILES] = {2048, 4096, 1024, 512};
 constexpr int MS_LDS_MAX = 160 * 1024;
 
 template <int BLOCK, int TE>
@@ -286,7 +295,7 @@ void launch_multisplit(const LevelGeom &g, const int64_t *in_ptr, const int64_t 
 
 }  // namespace
 
-int multisplit_tile_count() { return 3; }
+int multisplit_tile_count() { return MS_NTILES; }
 int64_t multisplit_tile_elems(int i) { return MS_TILES[i]; }
 int multisplit_max_keys() { return MS_KMAX; }
 int multisplit_max_rows() { return MS_RMAX; }
@@ -345,6 +354,10 @@ void multisplit(const LevelGeom &g, const int64_t *in_ptr, const int64_t *tile_r
                    "multisplit: next-level histogram does not fit");
     int64_t *nc = fuse ? next_counts : nullptr;
     switch (g.group_elems) {
+    case 1024:
+        launch_multisplit<128, 1024>(g, in_ptr, tile_row, in_col, in_val, x_map, cursor, out_col, out_val,
+                                     n_heavy_out, nc, cbits, rbits, s);
+        break;
     case 4096:
         launch_multisplit<256, 4096>(g, in_ptr, tile_row, in_col, in_val, x_map, cursor, out_col, out_val,
                                      n_heavy_out, nc, cbits, rbits, s);
