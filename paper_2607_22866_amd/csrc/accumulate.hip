@@ -515,16 +515,32 @@ GM_DEV void rank_load(const LeafSet &L, int64_t s, int64_t e, int32_t (&c)[EPT],
     }
 }
 
+// Marks the chunk's columns in the bitmap and, one bit per bitmap word, in a
+// summary bitmap of the non-empty words; returns through *count the number
+// of distinct columns (a column is new when atomicOr finds its bit clear).
 template <int BLOCK, int EPT>
-GM_DEV void rank_mark(uint32_t *bits, int nwords, const int32_t (&c)[EPT]) {
+GM_DEV void rank_mark(uint32_t *bits, uint32_t *summ, int nwords, const int32_t (&c)[EPT], int32_t *count) {
+    const int nsumm = (nwords + 31) >> 5;
     for (int w = threadIdx.x; w < nwords; w += BLOCK) bits[w] = 0;
+    for (int w = threadIdx.x; w < nsumm; w += BLOCK) summ[w] = 0;
+    if (threadIdx.x == 0) *count = 0;
     __syncthreads();
+    int fresh = 0;
 #pragma unroll
     for (int q = 0; q < EPT; ++q)
         if (c[q] >= 0) {
+            const int w = c[q] >> 5;
             const uint32_t bit = 1u << (c[q] & 31);
-            if (!(((volatile uint32_t *)bits)[c[q] >> 5] & bit)) atomicOr(&bits[c[q] >> 5], bit);
+            if (!(((volatile uint32_t *)bits)[w] & bit)) {
+                const uint32_t old = atomicOr(&bits[w], bit);
+                if (!(old & bit)) {
+                    ++fresh;
+                    if (old == 0) atomicOr(&summ[w >> 5], 1u << (w & 31));
+                }
+            }
         }
+    fresh = wave_reduce_sum(fresh);
+    if ((threadIdx.x & (GM_WAVE - 1)) == 0 && fresh) atomicAdd(count, fresh);
     __syncthreads();
 }
 
@@ -532,45 +548,40 @@ template <int BLOCK, int NWORDS>
 __global__ __launch_bounds__(BLOCK) void k_leaf_rank_sym(LeafSet L, const int64_t *items, int width,
                                                          int64_t *leaf_nnz, int64_t *slot_cnt) {
     __shared__ uint32_t bits[NWORDS];
-    __shared__ int32_t scan_sm[BLOCK / GM_WAVE];
+    __shared__ uint32_t summ[NWORDS / 32];
+    __shared__ int32_t count;
     const int64_t i = items[blockIdx.x];
     const int64_t j = L.lo + i;
-    const int nwords = width >> 5;
     int32_t c[RANK_EPT];
     double v[RANK_EPT];
     rank_load<BLOCK, RANK_EPT>(L, L.ptr[j], L.ptr[j + 1], c, v, false);
-    rank_mark<BLOCK, RANK_EPT>(bits, nwords, c);
-    int32_t cnt = 0;
-    for (int w = threadIdx.x; w < nwords; w += BLOCK) cnt += __popc(bits[w]);
-    cnt = block_reduce_sum<BLOCK>(cnt, scan_sm);
+    rank_mark<BLOCK, RANK_EPT>(bits, summ, width >> 5, c, &count);
     if (threadIdx.x == 0) {
-        leaf_nnz[i] = cnt;
-        slot_cnt[L.origin[j]] = cnt;
+        leaf_nnz[i] = count;
+        slot_cnt[L.origin[j]] = count;
     }
 }
 
 template <int BLOCK, int NWORDS, int CAP>
 __global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const int64_t *items, const int64_t *leaf_nnz,
                                                          int width, LeafOut o) {
+    static_assert(NWORDS / 32 <= BLOCK, "one summary word per thread");
     __shared__ uint32_t bits[NWORDS];
-    __shared__ uint16_t wpre[NWORDS];  // rank of each word's first bit (ranks < CAP <= 65535)
+    __shared__ uint32_t summ[NWORDS / 32];
+    __shared__ uint16_t wpre[NWORDS];  // rank of each non-empty word's first bit (ranks < CAP <= 65535)
+    __shared__ uint16_t wlist[CAP];    // the non-empty words, in column order
     __shared__ double vals[CAP];
     __shared__ int32_t scan_sm[BLOCK / GM_WAVE];
+    __shared__ int32_t count;
     const int64_t i = items[blockIdx.x];
     const int64_t j = L.lo + i;
     const int nwords = width >> 5;
+    const int nsumm = (nwords + 31) >> 5;
     int32_t c[RANK_EPT];
     double v[RANK_EPT];
     rank_load<BLOCK, RANK_EPT>(L, L.ptr[j], L.ptr[j + 1], c, v, true);
-    rank_mark<BLOCK, RANK_EPT>(bits, nwords, c);
-    // exclusive scan of the word popcounts; thread t owns words [t*per, (t+1)*per)
-    const int per = (nwords + BLOCK - 1) / BLOCK;
-    const int w0 = threadIdx.x * per;
-    int32_t sum = 0;
-    for (int q = 0; q < per; ++q)
-        if (w0 + q < nwords) sum += __popc(bits[w0 + q]);
-    int32_t total;
-    const int32_t first = block_excl_scan<BLOCK>(sum, scan_sm, &total);
+    rank_mark<BLOCK, RANK_EPT>(bits, summ, nwords, c, &count);
+    const int32_t total = count;
     int64_t dst, cap;
     int32_t base;
     leaf_target(o, L.origin[j], dst, cap, base);
@@ -578,19 +589,36 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const int64_
     const int n = total < CAP ? total : CAP;
     const int m = n < nnz ? n : (int)nnz;
     if (threadIdx.x == 0 && (total != nnz || total > CAP)) atomicOr(o.err, 4);
-    // ranks of the words; the columns go straight to C in rank order
-    int32_t r = first;
-    for (int q = 0; q < per; ++q)
-        if (w0 + q < nwords) {
-            const int w = w0 + q;
-            wpre[w] = (uint16_t)r;
-            uint32_t b = bits[w];
-            while (b) {
-                if (r < m) o.c_col[dst + r] = base + ((w << 5) | (__ffs(b) - 1));
+    // list the non-empty words in order: summary word t belongs to thread t
+    {
+        const uint32_t sw = (int)threadIdx.x < nsumm ? summ[threadIdx.x] : 0u;
+        int32_t n_words;
+        int32_t pos = block_excl_scan<BLOCK>((int32_t)__popc(sw), scan_sm, &n_words);
+        uint32_t b = sw;
+        while (b) {
+            if (pos < CAP) wlist[pos] = (uint16_t)((threadIdx.x << 5) | (__ffs(b) - 1));
+            ++pos;
+            b &= b - 1;
+        }
+        __syncthreads();
+        // ranks of the listed words; the columns go straight to C in rank order
+        const int nw = n_words < CAP ? n_words : CAP;
+        const int per = (nw + BLOCK - 1) / BLOCK;
+        const int q0 = threadIdx.x * per;
+        int32_t sum = 0;
+        for (int q = q0; q < q0 + per && q < nw; ++q) sum += __popc(bits[wlist[q]]);
+        int32_t r = block_excl_scan<BLOCK>(sum, scan_sm);
+        for (int q = q0; q < q0 + per && q < nw; ++q) {
+            const int w = wlist[q];
+            wpre[w] = (uint16_t)(r < 65535 ? r : 65535);
+            uint32_t bb = bits[w];
+            while (bb) {
+                if (r < m) o.c_col[dst + r] = base + ((w << 5) | (__ffs(bb) - 1));
                 ++r;
-                b &= b - 1;
+                bb &= bb - 1;
             }
         }
+    }
     for (int q = threadIdx.x; q < n; q += BLOCK) vals[q] = 0.0;
     __syncthreads();
 #pragma unroll

@@ -25,6 +25,7 @@ namespace {
 
 constexpr int EXP_BLOCK = 256;
 constexpr int64_t EXP_TILE = 8192;
+constexpr int EXP_ILP = 4;
 
 struct TileInfo {
     int64_t s0;    // slice containing the tile's first product
@@ -95,14 +96,34 @@ __global__ __launch_bounds__(EXP_BLOCK) void k_expand(Csr B, const int64_t *col_
         }
         __syncthreads();
         const int t0 = seg_lo[0], t1 = seg_lo[nb];
-        for (int t = t0 + tid; t < t1; t += EXP_BLOCK) {
-            const int q = (int)find_row(seg_lo, 0, nb, t);
-            const int64_t src = seg_src[q] + t;
-            const int32_t c = B.ci[src];
-            const double v = seg_a[q] * B.v[src];
-            const int64_t d = seg_dst[q] + t;
-            __builtin_nontemporal_store(c, &chat_col[d]);
-            __builtin_nontemporal_store(v, &chat_val[d]);
+        // EXP_ILP products per thread per pass, all loads issued before any
+        // store; the segment of a product is the last one starting at or
+        // before it (searched from the previous product's segment)
+        int q_prev = 0;
+        for (int tb = t0 + tid; tb < t1; tb += EXP_BLOCK * EXP_ILP) {
+            int32_t c[EXP_ILP];
+            double bv[EXP_ILP], av[EXP_ILP];
+            int64_t d[EXP_ILP];
+#pragma unroll
+            for (int u = 0; u < EXP_ILP; ++u) {
+                const int t = tb + u * EXP_BLOCK;
+                if (t < t1) {
+                    const int q = (int)find_row(seg_lo, q_prev, nb, t);
+                    q_prev = q;
+                    const int64_t src = seg_src[q] + t;
+                    c[u] = B.ci[src];
+                    bv[u] = B.v[src];
+                    av[u] = seg_a[q];
+                    d[u] = seg_dst[q] + t;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < EXP_ILP; ++u) {
+                if (tb + u * EXP_BLOCK < t1) {
+                    chat_col[d[u]] = c[u];
+                    chat_val[d[u]] = av[u] * bv[u];
+                }
+            }
         }
         sbase = next_base;
         __syncthreads();

@@ -232,8 +232,8 @@ __global__ __launch_bounds__(BLOCK) void k_multisplit(int64_t n_in, int64_t elem
         const int k = (lr << cbits) | (c >> shift);
         const int64_t d = key_delta[k] + p;
         const int32_t lc = c & mask;
-        __builtin_nontemporal_store(lc, &out_col[d]);
-        __builtin_nontemporal_store(val_buf[p], &out_val[d]);
+        out_col[d] = lc;  // cached stores: the L2 merges the partial lines at chunk-run edges
+        out_val[d] = val_buf[p];
     }
     if (fuse_next) {
         // counts of the chunks that stay heavy go to the next level
