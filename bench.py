@@ -39,13 +39,13 @@ def log(msg):
     print("[bench] " + msg, file=sys.stderr, flush=True)
 
 
-def run_step(g, dA, bounds, timing, acc, c_bufs):
+def run_step(g, dA, bounds, timing, acc, c_bufs, extra_flags=0):
     """One full product; returns (products, nnz(C))."""
     import torch
 
     products = 0
     nnz = 0
-    flags = g.FLAG_TIMING if timing else 0
+    flags = (g.FLAG_TIMING if timing else 0) | extra_flags
     for a, b in zip(bounds[:-1], bounds[1:]):
         with g.Plan(dA, dA, row_begin=a, row_end=b, flags=flags) as p:
             rp, n = p.symbolic()
@@ -120,6 +120,7 @@ def main():
                     help="maximum intermediate products per row panel")
     ap.add_argument("--cpu-products", type=float, default=4e8, help="oracle sample size for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--serial", action="store_true", help="run heavy and light work on one stream")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build measures the single-GPU hot path "
@@ -150,9 +151,10 @@ def main():
     log("%d row panels (max %.2g products each)" % (len(bounds) - 1, args.panel_products))
     acc_warm = {}
     c_bufs = [None, None]
+    extra = g.FLAG_SERIAL_STREAMS if args.serial else 0
     for w in range(args.warmup):
         t = time.perf_counter()
-        run_step(g, dA, bounds, False, acc_warm, c_bufs)
+        run_step(g, dA, bounds, False, acc_warm, c_bufs, extra)
         torch.cuda.synchronize()
         log("warmup %d: %.3fs" % (w, time.perf_counter() - t))
 
@@ -163,7 +165,7 @@ def main():
     for s in range(args.steps):
         t = time.perf_counter()
         bounds = g.split_panels(dA, dA, int(args.panel_products))
-        products, nnz = run_step(g, dA, bounds, True, acc, c_bufs)
+        products, nnz = run_step(g, dA, bounds, True, acc, c_bufs, extra)
         torch.cuda.synchronize()
         log("step %d: %.3fs" % (s, time.perf_counter() - t))
     torch.cuda.synchronize()

@@ -84,7 +84,10 @@ typedef struct {
 #define GMAGNUS_FLAG_SERIAL_STREAMS 2u /* run heavy and light work on one stream (no concurrency) */
 #define GMAGNUS_FLAG_NO_WINDOW 4u      /* never use the dense-window accumulator for light rows */
 #define GMAGNUS_FLAG_PAPER_HISTOGRAM 8u /* level-0 histogram by a pass over C-hat's columns (the paper's
-                                           kernel) instead of from the structure of A and B */
+                                           kernel) instead of from the structure of A and B;
+                                           implies GMAGNUS_FLAG_PAPER_EXPANSION */
+#define GMAGNUS_FLAG_PAPER_EXPANSION 16u /* write C-hat row by row, then split it at the first level (the
+                                            paper's order), instead of splitting during the expansion */
 
 #define GMAGNUS_MAX_LEVELS 8
 

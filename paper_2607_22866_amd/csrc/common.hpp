@@ -132,5 +132,11 @@ inline int ilog2(int64_t x) {
     while ((int64_t(1) << (r + 1)) <= x) ++r;
     return r;
 }
+inline int64_t floor_pow2(int64_t x) { return x < 1 ? 0 : int64_t(1) << ilog2(x); }
+inline int64_t ceil_pow2(int64_t x) {
+    int64_t p = 1;
+    while (p < x) p <<= 1;
+    return p;
+}
 
 }  // namespace gm

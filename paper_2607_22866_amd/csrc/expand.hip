@@ -130,6 +130,135 @@ __global__ __launch_bounds__(EXP_BLOCK) void k_expand(Csr B, const int64_t *col_
     }
 }
 
+// Expansion fused with the first level's split. The tiles and segments are
+// those of k_expand; each segment (one A~ entry times a clipped run of its B
+// row) is cut further at the first-level chunk boundaries of that B row
+// (bnd: per slice, offsets of the first column of every chunk), giving
+// "runs" that all go to one (heavy row, chunk) output row. Runs stay in
+// product order (the B row is sorted), so a batch of runs again covers a
+// contiguous range of tile-local products. Each nonempty run reserves its
+// range with one atomic add on cursor[h * nc + c] (the output row's next
+// free position); the products are written with the chunk-local column.
+__global__ __launch_bounds__(EXP_BLOCK) void k_expand_split(
+    Csr B, const int64_t *col_ptr, const int64_t *slice_off, const int32_t *slice_k, const int32_t *row_h,
+    const double *a_val, int64_t n_slices, int64_t total, int64_t n_tiles, const TileInfo *info, const int32_t *bnd,
+    int nc, int shift, int64_t *cursor, int32_t *out_col, double *out_val) {
+    __shared__ int64_t cp[EXP_BLOCK + 1];
+    __shared__ int64_t sg_b[EXP_BLOCK];     // B.rp[k] of the segment's slice
+    __shared__ int64_t sg_hc[EXP_BLOCK];    // heavy row * nc
+    __shared__ double sg_a[EXP_BLOCK];
+    __shared__ int32_t sg_s[EXP_BLOCK];     // slice
+    __shared__ int32_t sg_loc[EXP_BLOCK];   // tile-local index of the segment's first product
+    __shared__ int32_t sg_off[EXP_BLOCK];   // its offset in the B row
+    __shared__ int32_t sg_end[EXP_BLOCK];   // offset one past the segment's last product
+    __shared__ int32_t sg_c[EXP_BLOCK];     // chunk of the first product
+    __shared__ int32_t run_base[EXP_BLOCK + 1];
+    __shared__ int32_t rn_lo[EXP_BLOCK + 1];  // tile-local index of each run's first product
+    __shared__ int64_t rn_dst[EXP_BLOCK];   // output position minus tile-local index
+    __shared__ int64_t rn_src[EXP_BLOCK];   // B position minus tile-local index
+    __shared__ double rn_a[EXP_BLOCK];
+    __shared__ int32_t scan_sm[EXP_BLOCK / GM_WAVE];
+    __shared__ int64_t next_base;
+
+    const int tid = threadIdx.x;
+    const int64_t tile = xcd_tile(blockIdx.x, n_tiles);
+    const int64_t g0 = tile * EXP_TILE;
+    const int64_t g1 = g0 + EXP_TILE < total ? g0 + EXP_TILE : total;
+    const TileInfo ti = info[tile];
+    const int32_t mask = (int32_t)((1u << shift) - 1u);
+    int64_t sbase = ti.s0;
+
+    for (int64_t b = 0; b < ti.nseg; b += EXP_BLOCK) {
+        const int nb = (int)(ti.nseg - b < EXP_BLOCK ? ti.nseg - b : EXP_BLOCK);
+        for (int q = tid; q <= nb; q += EXP_BLOCK) cp[q] = sbase + q <= n_slices ? col_ptr[sbase + q] : INT64_MAX;
+        __syncthreads();
+        int nr = 0;
+        if (tid < nb) {
+            const int64_t e = ti.a0 + b + tid;
+            const int64_t s = sbase + find_row(cp, 0, nb + 1, e);
+            const int32_t k = slice_k[s];
+            const int64_t bstart = B.rp[k], L = B.rp[k + 1] - bstart;
+            const int64_t seg_g = slice_off[s] + (e - cp[s - sbase]) * L;
+            const int64_t lo = seg_g > g0 ? seg_g : g0;
+            const int64_t hi = seg_g + L < g1 ? seg_g + L : g1;
+            const int32_t off0 = (int32_t)(lo - seg_g), off1 = (int32_t)(hi - seg_g);
+            const int32_t c0 = B.ci[bstart + off0] >> shift;
+            const int32_t c1 = B.ci[bstart + off1 - 1] >> shift;
+            nr = c1 - c0 + 1;
+            sg_b[tid] = bstart;
+            sg_hc[tid] = (int64_t)row_h[e] * nc;
+            sg_a[tid] = a_val[e];
+            sg_s[tid] = (int32_t)s;
+            sg_loc[tid] = (int32_t)(lo - g0);
+            sg_off[tid] = off0;
+            sg_end[tid] = off1;
+            sg_c[tid] = c0;
+            if (tid == nb - 1) next_base = s;
+        }
+        int n_runs = 0;
+        const int rbase = block_excl_scan<EXP_BLOCK, int>(nr, scan_sm, &n_runs);
+        run_base[tid] = rbase;
+        if (tid == 0) run_base[EXP_BLOCK] = n_runs;
+        __syncthreads();
+
+        for (int rb = 0; rb < n_runs; rb += EXP_BLOCK) {
+            const int nrb = n_runs - rb < EXP_BLOCK ? n_runs - rb : EXP_BLOCK;
+            if (tid < nrb) {
+                const int gr = rb + tid;
+                const int q = (int)find_row(run_base, 0, nb, gr);
+                const int c = sg_c[q] + (gr - run_base[q]);
+                const int32_t *bq = bnd + (int64_t)sg_s[q] * (nc + 1);
+                const int32_t b_lo = bq[c], b_hi = bq[c + 1];
+                // first and last runs are clipped to the segment; inner runs
+                // are whole chunks of the B row (possibly empty)
+                const int32_t lo_r = b_lo > sg_off[q] ? b_lo : sg_off[q];
+                const int32_t hi_r = b_hi < sg_end[q] ? b_hi : sg_end[q];
+                const int32_t len = hi_r - lo_r;
+                const int32_t loc = sg_loc[q] + (lo_r - sg_off[q]);
+                int64_t dst = 0;
+                if (len > 0)
+                    dst = (int64_t)atomicAdd((unsigned long long *)&cursor[sg_hc[q] + c], (unsigned long long)len);
+                rn_lo[tid] = loc;
+                rn_dst[tid] = dst - loc;
+                rn_src[tid] = sg_b[q] + lo_r - loc;
+                rn_a[tid] = sg_a[q];
+                if (tid == nrb - 1) rn_lo[nrb] = loc + len;
+            }
+            __syncthreads();
+            const int t0 = rn_lo[0], t1 = rn_lo[nrb];
+            int q_prev = 0;
+            for (int tb = t0 + tid; tb < t1; tb += EXP_BLOCK * EXP_ILP) {
+                int32_t c[EXP_ILP];
+                double bv[EXP_ILP], av[EXP_ILP];
+                int64_t d[EXP_ILP];
+#pragma unroll
+                for (int u = 0; u < EXP_ILP; ++u) {
+                    const int t = tb + u * EXP_BLOCK;
+                    if (t < t1) {
+                        const int q = (int)find_row(rn_lo, q_prev, nrb, t);
+                        q_prev = q;
+                        const int64_t src = rn_src[q] + t;
+                        c[u] = B.ci[src];
+                        bv[u] = B.v[src];
+                        av[u] = rn_a[q];
+                        d[u] = rn_dst[q] + t;
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < EXP_ILP; ++u) {
+                    if (tb + u * EXP_BLOCK < t1) {
+                        out_col[d[u]] = c[u] & mask;
+                        out_val[d[u]] = av[u] * bv[u];
+                    }
+                }
+            }
+            __syncthreads();
+        }
+        sbase = next_base;
+        __syncthreads();
+    }
+}
+
 }  // namespace
 
 int64_t expand_tile_words(int64_t total) {
@@ -153,6 +282,18 @@ void expand(const Csr &B, const SliceArrays &sl, int64_t total, const int64_t *i
     hipLaunchKernelGGL(k_expand, dim3((unsigned)n_tiles), dim3(EXP_BLOCK), 0, s, B, sl.col_ptr, sl.slice_off,
                        sl.slice_k, sl.row_h, sl.a_val, sl.n_slices, total, n_tiles, (const TileInfo *)info_words,
                        chat_cursor, chat_col, chat_val);
+    GM_CHECK_LAUNCH();
+}
+
+void expand_split(const Csr &B, const SliceArrays &sl, int64_t total, const int64_t *info_words, const int32_t *bnd,
+                  int nc, int shift, int64_t *cursor, int32_t *out_col, double *out_val, hipStream_t s) {
+    if (total <= 0 || sl.n_slices <= 0) return;
+    GM_REQUIRE(nc >= 1 && nc < GM_WAVE && shift >= 0 && shift < 31, GMAGNUS_ERROR_UNSUPPORTED,
+               "fused expansion: unsupported first-level chunking");
+    const int64_t n_tiles = (total + EXP_TILE - 1) / EXP_TILE;
+    hipLaunchKernelGGL(k_expand_split, dim3((unsigned)n_tiles), dim3(EXP_BLOCK), 0, s, B, sl.col_ptr, sl.slice_off,
+                       sl.slice_k, sl.row_h, sl.a_val, sl.n_slices, total, n_tiles, (const TileInfo *)info_words, bnd,
+                       nc, shift, cursor, out_col, out_val);
     GM_CHECK_LAUNCH();
 }
 

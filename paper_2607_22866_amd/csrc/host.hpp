@@ -128,11 +128,12 @@ void slice_build(const Csr &B, const int64_t *colcnt, const int64_t *slice_perm,
 void csc_fill(const Csr &A, const Csr &B, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
               const int64_t *a_heavy_ptr, int64_t nnz_heavy_all, const int32_t *k_to_slice,
               const int64_t *col_ptr, int64_t *fill_cursor, int32_t *row_h, double *a_val, hipStream_t s);
-// Level-0 histogram from the structure: per-slice chunk counts of its B row,
-// then per heavy row the sum over its A~ entries (counts: n_heavy * nc).
-void slice_chunk_hist(const Csr &B, const SliceArrays &sl, int nc, int shift, int32_t *hist, hipStream_t s);
+// Level-0 histogram from the structure: per-slice chunk boundaries in its B
+// row (n_slices * (nc + 1) offsets), then per heavy row the sum of its A~
+// entries' chunk sizes (counts: n_heavy * nc).
+void slice_chunk_bounds(const Csr &B, const SliceArrays &sl, int nc, int shift, int32_t *bnd, hipStream_t s);
 void struct_hist(const Csr &A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0, const int64_t *a_heavy_ptr,
-                 int64_t nnz_heavy_all, const int32_t *k_to_slice, const int32_t *hist, int nc, int64_t *counts,
+                 int64_t nnz_heavy_all, const int32_t *k_to_slice, const int32_t *bnd, int nc, int64_t *counts,
                  hipStream_t s);
 void gather_row_len(const int64_t *row_ptr, const int64_t *rows, int64_t n, int64_t r0, int64_t *out, hipStream_t s);
 void gather_i64(const int64_t *src, const int64_t *idx, int64_t n, int64_t *out, hipStream_t s);
@@ -145,6 +146,12 @@ int64_t expand_tile_words(int64_t total);
 void expand_tiles(const Csr &B, const SliceArrays &sl, int64_t total, int64_t *info_words, hipStream_t s);
 void expand(const Csr &B, const SliceArrays &sl, int64_t total, const int64_t *info_words, int64_t *chat_cursor,
             int32_t *chat_col, double *chat_val, hipStream_t s);
+// Expansion fused with the first level's split into nc chunks of 2^shift
+// columns: bnd are the slices' chunk boundaries (slice_chunk_bounds), cursor
+// the next free position of output row (h, c) at h * nc + c; columns are
+// written chunk-local.
+void expand_split(const Csr &B, const SliceArrays &sl, int64_t total, const int64_t *info_words, const int32_t *bnd,
+                  int nc, int shift, int64_t *cursor, int32_t *out_col, double *out_val, hipStream_t s);
 
 // ------------------------------------------------------------ multisplit.hip
 struct LevelGeom {
@@ -164,7 +171,10 @@ int multisplit_max_keys();
 int multisplit_max_rows();
 bool multisplit_next_fits(int keys, int next_chunks);
 void tile_rows(const LevelGeom &g, const int64_t *in_ptr, int64_t *tile_row, hipStream_t s);
-void histogram(const LevelGeom &g, const int64_t *in_ptr, const int64_t *tile_row, const int32_t *in_col,
+// Level histogram (n_in * n_chunks counts); tile_row is scratch of
+// histogram_tiles() entries.
+int64_t histogram_tiles(const LevelGeom &g, int64_t tau);
+void histogram(const LevelGeom &g, int64_t tau, const int64_t *in_ptr, const int32_t *in_col, int64_t *tile_row,
                int64_t *counts, hipStream_t s);
 void chunk_classes(const int64_t *counts, int64_t n, int64_t tau, bool last, uint8_t *cls, hipStream_t s);
 // out_cnt[inv[i]] = counts[i]; origin_out[inv[i]] = origin_in[i / n_chunks] + (i % n_chunks) * stride.

@@ -42,34 +42,74 @@ GM_DEV int local_row(const int64_t *rb, int R, int64_t i) {
     return lr;
 }
 
-// Level-0 histogram (Algorithm 3, Histogram): counts[r * n_chunks + c] +=
-// number of elements of row r with column >> shift == c.
-template <int BLOCK>
-__global__ __launch_bounds__(BLOCK) void k_histogram(int64_t n_in, int64_t elems, const int64_t *in_ptr,
-                                                     const int64_t *tile_row, int64_t te, int64_t n_tiles,
-                                                     const int32_t *in_col, int n_chunks, int shift, int R,
-                                                     int64_t *counts) {
+// Histogram of a level's input (Algorithm 3, Histogram): counts[r * n_chunks
+// + c] = number of elements of row r with column >> shift == c. Rows are
+// made of sorted B-row runs, so equal keys come in runs over consecutive
+// lanes: the first lane of each run adds the run's length with one LDS
+// atomic (no same-address atomics within a wave). Tiles are larger than the
+// multisplit's (the work group keeps only R * n_chunks counters).
+constexpr int HIST_BLOCK = 256;
+constexpr int HIST_ILP = 4;
+constexpr int HIST_NTILES = 6;
+constexpr int64_t HIST_TILES[HIST_NTILES] = {16384, 8192, 4096, 2048, 1024, 512};
+
+__global__ __launch_bounds__(HIST_BLOCK) void k_histogram(int64_t n_in, int64_t elems, const int64_t *in_ptr,
+                                                          const int64_t *tile_row, int64_t te, int64_t n_tiles,
+                                                          const int32_t *in_col, int n_chunks, int shift, int R,
+                                                          int64_t *counts) {
     __shared__ int32_t cnt[MS_KMAX];
     __shared__ int64_t rb[MS_RMAX + 1];
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & (GM_WAVE - 1);
     const int64_t tile = xcd_tile(blockIdx.x, n_tiles);
     const int64_t g0 = tile * te;
     const int64_t g1 = g0 + te < elems ? g0 + te : elems;
     const int64_t r0 = tile_row[tile];
     const int K = R * n_chunks;
     if (tid <= R) rb[tid] = r0 + tid <= n_in ? in_ptr[r0 + tid] : INT64_MAX;
-    for (int k = tid; k < K; k += BLOCK) cnt[k] = 0;
+    for (int k = tid; k < K; k += HIST_BLOCK) cnt[k] = 0;
     __syncthreads();
-    for (int64_t i = g0 + tid; i < g1; i += BLOCK) {
-        const int lr = local_row(rb, R, i);
-        atomicAdd(&cnt[lr * n_chunks + (in_col[i] >> shift)], 1);
+    const uint64_t le_mask = lanemask_lt() | (uint64_t(1) << lane);
+    // every lane runs the same iterations (ballots need the whole wave)
+    for (int64_t pb = g0; pb < g1; pb += HIST_BLOCK * HIST_ILP) {
+        int32_t c[HIST_ILP];
+#pragma unroll
+        for (int u = 0; u < HIST_ILP; ++u) {
+            const int64_t p = pb + u * HIST_BLOCK + tid;
+            c[u] = p < g1 ? __builtin_nontemporal_load(&in_col[p]) : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < HIST_ILP; ++u) {
+            const int64_t p = pb + u * HIST_BLOCK + tid;
+            const int k = c[u] >= 0 ? local_row(rb, R, p) * n_chunks + (c[u] >> shift) : -1;
+            const int kprev = __shfl_up(k, 1, GM_WAVE);
+            const uint64_t starts = ballot(lane == 0 || k != kprev);
+            if (k >= 0 && ((starts >> lane) & 1)) {
+                const uint64_t above = starts & ~le_mask;
+                const int len = (above ? __ffsll((long long)above) - 1 : GM_WAVE) - lane;
+                atomicAdd(&cnt[k], len);
+            }
+        }
     }
     __syncthreads();
-    for (int k = tid; k < K; k += BLOCK) {
+    for (int k = tid; k < K; k += HIST_BLOCK) {
         const int v = cnt[k];
         if (v) atomicAdd((unsigned long long *)&counts[(r0 + k / n_chunks) * n_chunks + k % n_chunks],
                          (unsigned long long)v);
     }
+}
+
+// Tile of the histogram pass: the largest whose rows fit the counters.
+struct HistTile {
+    int64_t te;
+    int R;
+};
+HistTile hist_tile(const LevelGeom &g, int64_t tau) {
+    for (int i = 0; i < HIST_NTILES; ++i) {
+        const int64_t te = HIST_TILES[i];
+        const int R = (int)ceil_pow2((te - 1 + tau - 1) / tau + 1);  // input rows hold more than tau elements
+        if (R <= MS_RMAX && R * g.n_chunks <= MS_KMAX) return HistTile{te, R};
+    }
+    throw Error{GMAGNUS_ERROR_UNSUPPORTED, "histogram: tau too small for its tile sizes"};
 }
 
 // Dynamic LDS layout of one multisplit work group (byte offsets); the
@@ -303,15 +343,23 @@ bool multisplit_next_fits(int keys, int next_chunks) {
     return next_chunks <= MS_NEXT_MAX && 4 * keys * next_chunks <= 32 * 1024;
 }
 
-void histogram(const LevelGeom &g, const int64_t *in_ptr, const int64_t *tile_row, const int32_t *in_col,
+int64_t histogram_tiles(const LevelGeom &g, int64_t tau) {
+    const HistTile ht = hist_tile(g, tau);
+    return (g.elems + ht.te - 1) / ht.te;
+}
+
+void histogram(const LevelGeom &g, int64_t tau, const int64_t *in_ptr, const int32_t *in_col, int64_t *tile_row,
                int64_t *counts, hipStream_t s) {
     fill<int64_t>(counts, 0, g.n_in * g.n_chunks, s);
     if (g.elems <= 0) return;
-    GM_REQUIRE((int64_t)g.group_rows * g.n_chunks <= MS_KMAX && g.group_rows <= MS_RMAX, GMAGNUS_ERROR_UNSUPPORTED,
-               "histogram: too many keys per work group");
-    const int64_t n_tiles = (g.elems + g.group_elems - 1) / g.group_elems;
-    hipLaunchKernelGGL(k_histogram<512>, dim3((unsigned)n_tiles), dim3(512), 0, s, g.n_in, g.elems, in_ptr, tile_row,
-                       g.group_elems, n_tiles, in_col, g.n_chunks, g.shift, g.group_rows, counts);
+    const HistTile ht = hist_tile(g, tau);
+    const int64_t n_tiles = (g.elems + ht.te - 1) / ht.te;
+    GM_REQUIRE(n_tiles < (int64_t)1 << 31, GMAGNUS_ERROR_UNSUPPORTED, "histogram: too many tiles");
+    hipLaunchKernelGGL(k_tile_rows, dim3(grid_for(n_tiles, 256, 65536)), dim3(256), 0, s, in_ptr, g.n_in, ht.te,
+                       n_tiles, tile_row);
+    GM_CHECK_LAUNCH();
+    hipLaunchKernelGGL(k_histogram, dim3((unsigned)n_tiles), dim3(HIST_BLOCK), 0, s, g.n_in, g.elems, in_ptr,
+                       tile_row, ht.te, n_tiles, in_col, g.n_chunks, g.shift, ht.R, counts);
     GM_CHECK_LAUNCH();
 }
 

@@ -147,13 +147,6 @@ constexpr int64_t MIN_LOCAL_CHUNK = 64;  // mean elements per local chunk of a m
 constexpr int MAX_DENSE_LOG2 = 13;       // 8192 fp64 values + bitmap per work group
 constexpr int MAX_CHUNKS_LOG2 = 6;       // chunks per level the multisplit kernel supports
 
-int64_t floor_pow2(int64_t x) { return x < 1 ? 0 : int64_t(1) << ilog2(x); }
-int64_t ceil_pow2(int64_t x) {
-    int64_t p = 1;
-    while (p < x) p <<= 1;
-    return p;
-}
-
 void compute_params(int64_t c_m, int64_t s_lm, const gmagnus_options_t *o, gmagnus_params_t *p) {
     GM_REQUIRE(c_m >= 1 && c_m < ((int64_t)1 << 31), GMAGNUS_ERROR_INVALID_VALUE, "C must have 1..2^31-1 columns");
     GM_REQUIRE(s_lm >= 1024, GMAGNUS_ERROR_INVALID_VALUE, "local memory size below 1 KB");
@@ -467,7 +460,10 @@ void heavy_symbolic(gmagnus_plan_s *p) {
     p->slot_width_log2 = c_bits - p->n_slots_log2;
 
     const bool paper_hist = (p->opts.flags & GMAGNUS_FLAG_PAPER_HISTOGRAM) != 0;
+    // split at the first level while expanding, unless the paper's order is asked for
+    const bool fused = P.n_levels > 0 && !paper_hist && (p->opts.flags & GMAGNUS_FLAG_PAPER_EXPANSION) == 0;
     int64_t *counts0 = nullptr;  // level-0 counts when computed from the structure
+    int32_t *sbnd = nullptr;     // per-slice level-0 chunk boundaries (kept for the fused expansion)
 
     // ---- masked CSR -> CSC of the heavy rows and slice offsets
     SliceArrays sl;
@@ -520,14 +516,17 @@ void heavy_symbolic(gmagnus_plan_s *p) {
             Timed t2(p, GMAGNUS_K_HISTOGRAM, s);
             const int nc0 = P.v_chunks[0];
             const int shift0 = c_bits - ilog2(nc0);
-            int32_t *shist = ws.alloc<int32_t>(sl.n_slices * nc0);
+            sbnd = ws.alloc<int32_t>(sl.n_slices * (nc0 + 1));
             counts0 = ws.alloc<int64_t>(nh * nc0);
-            slice_chunk_hist(p->B, sl, nc0, shift0, shist, s);
-            struct_hist(p->A, p->heavy_rows, nh, p->r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, shist, nc0, counts0,
+            slice_chunk_bounds(p->B, sl, nc0, shift0, sbnd, s);
+            struct_hist(p->A, p->heavy_rows, nh, p->r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, sbnd, nc0, counts0,
                         s);
-            ws.free(shist);
+            if (!fused) {
+                ws.free(sbnd);
+                sbnd = nullptr;
+            }
             p->info.kernel_launches[GMAGNUS_K_HISTOGRAM] += 1;
-            add_bytes(p, GMAGNUS_K_HISTOGRAM, 12.0 * nnz_heavy_all + 4.0 * sl.n_slices * nc0 + 8.0 * nh * nc0);
+            add_bytes(p, GMAGNUS_K_HISTOGRAM, 12.0 * nnz_heavy_all + 4.0 * sl.n_slices * (nc0 + 1) + 8.0 * nh * nc0);
         }
         // compulsory bytes of B~ (each slice's B row once): sum of nnz(B[k,:]) over slices
         blen_total = 0;
@@ -548,31 +547,37 @@ void heavy_symbolic(gmagnus_plan_s *p) {
     p->info.n_slices = sl.n_slices;
     p->info.nnz_a_heavy = sl.nnz;
 
-    // ---- outer-product expansion into buffer 0
+    // ---- outer-product expansion into buffer 0 (C-hat row by row, or
+    // already split into the first level's chunks when fused)
     int32_t *col_buf[2] = {ws.alloc<int32_t>(H), nullptr};
     double *val_buf[2] = {ws.alloc<double>(H), nullptr};
+    int64_t *exp_tiles = ws.alloc<int64_t>(std::max<int64_t>(expand_tile_words(H), 1));
     {
+        Timed t(p, GMAGNUS_K_CSC, s);
+        expand_tiles(p->B, sl, H, exp_tiles, s);
+    }
+    auto free_slices = [&]() {
+        ws.free(exp_tiles);
+        ws.free(sl.col_ptr);
+        ws.free(sl.slice_off);
+        ws.free(sl.slice_k);
+        ws.free(sl.row_h);
+        ws.free(sl.a_val);
+        if (sbnd) ws.free(sbnd);
+        sbnd = nullptr;
+    };
+    if (!fused) {
         int64_t *cursor = ws.alloc<int64_t>(nh);
-        int64_t *tiles = ws.alloc<int64_t>(expand_tile_words(H));
-        {
-            Timed t(p, GMAGNUS_K_CSC, s);
-            copy_i64(cursor, p->chat_ptr, nh, s);
-            expand_tiles(p->B, sl, H, tiles, s);
-        }
+        copy_i64(cursor, p->chat_ptr, nh, s);
         {
             Timed t(p, GMAGNUS_K_EXPAND, s);
-            expand(p->B, sl, H, tiles, cursor, col_buf[0], val_buf[0], s);
+            expand(p->B, sl, H, exp_tiles, cursor, col_buf[0], val_buf[0], s);
         }
         ws.free(cursor);
-        ws.free(tiles);
         p->info.kernel_launches[GMAGNUS_K_EXPAND] += 1;
         add_bytes(p, GMAGNUS_K_EXPAND, 12.0 * H + 12.0 * sl.nnz + 8.0 * nh);
+        free_slices();
     }
-    ws.free(sl.col_ptr);
-    ws.free(sl.slice_off);
-    ws.free(sl.slice_k);
-    ws.free(sl.row_h);
-    ws.free(sl.a_val);
     (void)blen_total;
 
     // ---- hierarchical multisplit
@@ -619,14 +624,18 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         int64_t *origin_out = ws.alloc<int64_t>(n_out);
         int64_t *out_ptr = ws.alloc<int64_t>(n_out + 1);
         uint8_t *ccls = ws.alloc<uint8_t>(n_out);
-        tile_rows(g, in_ptr, tile_row, s);
+        if (!(fused && lvl == 0)) tile_rows(g, in_ptr, tile_row, s);
         if (lvl == 0 && counts0) {
             counts = counts0;
-        } else if (lvl == 0) {
-            // the paper's histogram kernel: one pass over the columns of C-hat
+        } else if (!counts) {
+            // the paper's histogram kernel: one pass over the level's input
+            // columns (C-hat at the first level; after a fused first split,
+            // the chunks that stay heavy)
             Timed t(p, GMAGNUS_K_HISTOGRAM, s);
             counts = ws.alloc<int64_t>(n_out);
-            histogram(g, in_ptr, tile_row, col_buf[cur], counts, s);
+            int64_t *h_rows = ws.alloc<int64_t>(std::max<int64_t>(histogram_tiles(g, P.tau), 1));
+            histogram(g, P.tau, in_ptr, col_buf[cur], h_rows, counts, s);
+            ws.free(h_rows);
             p->info.kernel_launches[GMAGNUS_K_HISTOGRAM] += 1;
             add_bytes(p, GMAGNUS_K_HISTOGRAM, 4.0 * elems + 8.0 * (n_in + 1) + 8.0 * n_out);
         }
@@ -641,17 +650,32 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         }
         const int64_t nh_out = cbh[1];
         p->info.level_heavy_out[lvl] = nh_out;
+        const bool split_in_expand = fused && lvl == 0;
         int64_t *next_counts = nullptr;
-        if (!last && nh_out > 0) {
+        if (!last && nh_out > 0 && !split_in_expand &&
+            multisplit_next_fits(g.group_rows * nc, g.next_chunks)) {
+            // the multisplit takes the next level's histogram on the way
             next_counts = ws.alloc<int64_t>(nh_out * g.next_chunks);
             fill<int64_t>(next_counts, 0, nh_out * g.next_chunks, s);
         }
-        const int nxt = 1 - cur;
+        const int nxt = split_in_expand ? 0 : 1 - cur;
         if (!col_buf[nxt]) {
             col_buf[nxt] = ws.alloc<int32_t>(H);
             val_buf[nxt] = ws.alloc<double>(H);
         }
-        {
+        if (split_in_expand) {
+            // cursor of output row (h, c), indexed h * nc + c
+            int64_t *cursor = ws.alloc<int64_t>(n_out);
+            gather_i64(out_ptr, x_map, n_out, cursor, s);
+            {
+                Timed t(p, GMAGNUS_K_EXPAND, s);
+                expand_split(p->B, sl, H, exp_tiles, sbnd, nc, g.shift, cursor, col_buf[nxt], val_buf[nxt], s);
+            }
+            ws.free(cursor);
+            p->info.kernel_launches[GMAGNUS_K_EXPAND] += 1;
+            add_bytes(p, GMAGNUS_K_EXPAND, 12.0 * H + 12.0 * sl.nnz + 8.0 * n_out);
+            free_slices();
+        } else {
             int64_t *cursor = ws.alloc<int64_t>(n_out);
             copy_i64(cursor, out_ptr, n_out, s);
             {

@@ -136,12 +136,12 @@ __global__ __launch_bounds__(FLAT_BLOCK) void k_csc_fill(Csr A, const int64_t *h
     });
 }
 
-// Level-0 chunk counts of every slice's B row: hist[s * nc + c] = number of
-// columns of B[k,:] in [c << shift, (c + 1) << shift). The row is sorted, so
-// lane c of a wave finds the row's first column >= c << shift by binary
-// search and the counts are differences of neighbouring lanes.
-__global__ __launch_bounds__(256) void k_slice_chunk_hist(Csr B, const int32_t *slice_k, int64_t n_slices, int nc,
-                                                          int shift, int32_t *hist) {
+// Level-0 chunk boundaries of every slice's B row: bnd[s * (nc + 1) + c] =
+// offset in B[k,:] of the row's first column >= c << shift (c = 0..nc). The
+// row is sorted, so lane c of a wave finds it by binary search; chunk c of
+// the row is [bnd[c], bnd[c + 1]).
+__global__ __launch_bounds__(256) void k_slice_chunk_bounds(Csr B, const int32_t *slice_k, int64_t n_slices, int nc,
+                                                            int shift, int32_t *bnd) {
     const int lane = threadIdx.x & (GM_WAVE - 1);
     const int64_t nwaves = (int64_t)gridDim.x * (blockDim.x / GM_WAVE);
     for (int64_t s = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / GM_WAVE; s < n_slices; s += nwaves) {
@@ -157,22 +157,22 @@ __global__ __launch_bounds__(256) void k_slice_chunk_hist(Csr B, const int32_t *
                 else
                     hi = mid;
             }
+            bnd[s * (nc + 1) + lane] = (int32_t)(lo - b0);
         }
-        const int64_t next = __shfl_down(lo, 1, GM_WAVE);
-        if (lane < nc) hist[s * nc + lane] = (int32_t)(next - lo);
     }
 }
 
 // Level-0 histogram from the structure (Algorithm 3, Histogram at the first
 // level): the C-hat row of heavy row h is the union of the B rows of its
-// A~ entries, so counts[h * nc + c] = sum over those entries of the slice
-// histograms above. Each wave walks SH_ENTRIES consecutive A~ entries in
-// row-major order, lane c accumulating chunk c, and flushes at row ends.
+// A~ entries, so counts[h * nc + c] = sum over those entries of the slices'
+// chunk sizes (differences of the boundaries above). Each wave walks
+// SH_ENTRIES consecutive A~ entries in row-major order, lane c accumulating
+// chunk c, and flushes at row ends.
 constexpr int SH_ENTRIES = 256;
 
 __global__ __launch_bounds__(256) void k_struct_hist(Csr A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
                                                      const int64_t *a_heavy_ptr, int64_t total,
-                                                     const int32_t *k_to_slice, const int32_t *hist, int nc,
+                                                     const int32_t *k_to_slice, const int32_t *bnd, int nc,
                                                      int64_t *counts) {
     const int lane = threadIdx.x & (GM_WAVE - 1);
     const int64_t wid = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / GM_WAVE;
@@ -205,7 +205,10 @@ __global__ __launch_bounds__(256) void k_struct_hist(Csr A, const int64_t *heavy
                 acc = 0;
                 cur = hq;
             }
-            if (sq >= 0 && lane < nc) acc += hist[(int64_t)sq * nc + lane];
+            if (sq >= 0 && lane < nc) {
+                const int32_t *bq = bnd + (int64_t)sq * (nc + 1);
+                acc += bq[lane + 1] - bq[lane];
+            }
         }
         // lanes past the last entry may have stopped walking; realign for the next group
         h = __shfl(h, cnt - 1, GM_WAVE);
@@ -289,22 +292,22 @@ void csc_fill(const Csr &A, const Csr &B, const int64_t *heavy_rows, int64_t n_h
     GM_CHECK_LAUNCH();
 }
 
-void slice_chunk_hist(const Csr &B, const SliceArrays &sl, int nc, int shift, int32_t *hist, hipStream_t s) {
+void slice_chunk_bounds(const Csr &B, const SliceArrays &sl, int nc, int shift, int32_t *bnd, hipStream_t s) {
     if (sl.n_slices <= 0) return;
     GM_REQUIRE(nc >= 1 && nc < GM_WAVE, GMAGNUS_ERROR_UNSUPPORTED, "level-0 chunk count must be below 64");
-    hipLaunchKernelGGL(k_slice_chunk_hist, dim3(grid_for(sl.n_slices, 4, 65536)), dim3(256), 0, s, B, sl.slice_k,
-                       sl.n_slices, nc, shift, hist);
+    hipLaunchKernelGGL(k_slice_chunk_bounds, dim3(grid_for(sl.n_slices, 4, 65536)), dim3(256), 0, s, B, sl.slice_k,
+                       sl.n_slices, nc, shift, bnd);
     GM_CHECK_LAUNCH();
 }
 
 void struct_hist(const Csr &A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0, const int64_t *a_heavy_ptr,
-                 int64_t nnz_heavy_all, const int32_t *k_to_slice, const int32_t *hist, int nc, int64_t *counts,
+                 int64_t nnz_heavy_all, const int32_t *k_to_slice, const int32_t *bnd, int nc, int64_t *counts,
                  hipStream_t s) {
     fill<int64_t>(counts, 0, n_heavy * nc, s);
     if (n_heavy <= 0 || nnz_heavy_all <= 0) return;
     const int64_t waves = (nnz_heavy_all + SH_ENTRIES - 1) / SH_ENTRIES;
     hipLaunchKernelGGL(k_struct_hist, dim3(grid_for(waves, 4, (int64_t)1 << 30)), dim3(256), 0, s, A, heavy_rows,
-                       n_heavy, r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, hist, nc, counts);
+                       n_heavy, r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, bnd, nc, counts);
     GM_CHECK_LAUNCH();
 }
 

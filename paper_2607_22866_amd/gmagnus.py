@@ -22,6 +22,8 @@ K_NAMES = ["setup", "csc", "expand", "histogram", "multisplit", "chunk_symbolic"
 FLAG_TIMING = 1
 FLAG_SERIAL_STREAMS = 2
 FLAG_NO_WINDOW = 4
+FLAG_PAPER_HISTOGRAM = 8
+FLAG_PAPER_EXPANSION = 16
 
 STATUS = {0: "SUCCESS", 1: "INVALID_VALUE", 2: "INVALID_CSR", 3: "OUT_OF_MEMORY", 4: "NOT_READY", 5: "HIP",
           6: "UNSUPPORTED"}

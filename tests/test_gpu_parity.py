@@ -76,13 +76,23 @@ def test_rmat12_every_depth(g, opts, levels):
 def test_rmat12_paper_histogram(g, opts, levels):
     # the level-0 histogram as a pass over C-hat's columns gives the same C
     A = RMAT12.make()
-    info = check(g, A, A, flags=8, **opts)
+    info = check(g, A, A, flags=g.FLAG_PAPER_HISTOGRAM, **opts)
+    assert info.params.levels == levels
+
+
+@pytest.mark.parametrize("opts,levels", DEPTHS[1:])
+def test_rmat12_paper_expansion(g, opts, levels):
+    # C-hat written row by row and split at level 0 by the multisplit (the
+    # paper's order) gives the same C as the split fused into the expansion
+    A = RMAT12.make()
+    info = check(g, A, A, flags=g.FLAG_PAPER_EXPANSION, **opts)
     assert info.params.levels == levels
 
 
 def test_rmat12_integer_values_bit_exact(g):
     A = wl.rmat(12, 8, 0.57, 0.19, 0.19, 12, values="int3")
-    for opts in ({}, dict(tau=200, dense_width_log2=6, chunks_max_log2=2)):
+    for opts in ({}, dict(tau=200, dense_width_log2=6, chunks_max_log2=2),
+                 dict(tau=200, dense_width_log2=6, chunks_max_log2=2, flags=g.FLAG_PAPER_EXPANSION)):
         rp, col, val, _ = run(g, A, A, **opts)
         ref = oracle.spgemm(A, A)
         assert np.array_equal(rp, ref.row_ptr) and np.array_equal(col, ref.col)
