@@ -172,22 +172,28 @@ GM_DEV void hash_emit_sorted(int32_t *keys, double *vals, int64_t nnz, int32_t c
 }
 
 // ------------------------------------------------------ dense accumulator
-template <int BLOCK, int WMAX>
-struct DenseLds {
-    double vals[WMAX];
+// VALS = false keeps only the bitmap (symbolic passes), so more work groups
+// fit a CU.
+template <int BLOCK, int WMAX, bool VALS>
+struct DenseLdsT {
+    double vals[VALS ? WMAX : 1];
     uint32_t bits[(WMAX + 31) / 32];
     int32_t scan[BLOCK / GM_WAVE];
 };
-
 template <int BLOCK, int WMAX>
-GM_DEV void dense_clear(DenseLds<BLOCK, WMAX> &L, int width, bool num) {
+using DenseLds = DenseLdsT<BLOCK, WMAX, true>;
+template <int BLOCK, int WMAX>
+using DenseBits = DenseLdsT<BLOCK, WMAX, false>;
+
+template <int BLOCK, int WMAX, bool VALS>
+GM_DEV void dense_clear(DenseLdsT<BLOCK, WMAX, VALS> &L, int width, bool num) {
     for (int i = threadIdx.x; i < (width + 31) / 32; i += BLOCK) L.bits[i] = 0;
-    if (num)
+    if (VALS && num)
         for (int i = threadIdx.x; i < width; i += BLOCK) L.vals[i] = 0.0;
 }
 
-template <int BLOCK, int WMAX>
-GM_DEV void dense_set(DenseLds<BLOCK, WMAX> &L, int c) {
+template <int BLOCK, int WMAX, bool VALS>
+GM_DEV void dense_set(DenseLdsT<BLOCK, WMAX, VALS> &L, int c) {
     const uint32_t bit = 1u << (c & 31);
     if (!(((volatile uint32_t *)L.bits)[c >> 5] & bit)) atomicOr(&L.bits[c >> 5], bit);
 }
@@ -198,8 +204,8 @@ GM_DEV void dense_add(DenseLds<BLOCK, WMAX> &L, int c, double v) {
     __hip_atomic_fetch_add(&L.vals[c], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
-template <int BLOCK, int WMAX>
-GM_DEV int32_t dense_count(DenseLds<BLOCK, WMAX> &L, int width) {
+template <int BLOCK, int WMAX, bool VALS>
+GM_DEV int32_t dense_count(DenseLdsT<BLOCK, WMAX, VALS> &L, int width) {
     int32_t c = 0;
     for (int i = threadIdx.x; i < (width + 31) / 32; i += BLOCK) c += __popc(L.bits[i]);
     return block_reduce_sum<BLOCK>(c, L.scan);
@@ -341,7 +347,7 @@ template <int BLOCK, int WMAX>
 __global__ __launch_bounds__(BLOCK) void k_light_win_sym(Csr A, Csr B, int64_t r0, const int64_t *items,
                                                          const int32_t *minc, const int32_t *maxc,
                                                          int64_t *row_nnz) {
-    __shared__ DenseLds<BLOCK, WMAX> D;
+    __shared__ DenseBits<BLOCK, WMAX> D;
     __shared__ GusLds<BLOCK> G;
     const int64_t r = items[blockIdx.x];
     const int32_t base = minc[r];
@@ -374,21 +380,20 @@ __global__ __launch_bounds__(BLOCK) void k_light_win_num(Csr A, Csr B, int64_t r
 
 // ------------------------------------------------------------------ leaves
 template <int BLOCK, int TS>
-__global__ __launch_bounds__(BLOCK) void k_leaf_hash_sym(LeafSet L, const int64_t *items, int64_t *leaf_nnz,
+__global__ __launch_bounds__(BLOCK) void k_leaf_hash_sym(LeafSet L, const LeafTask *tasks, int64_t *leaf_nnz,
                                                          int64_t *slot_cnt) {
     __shared__ int32_t keys[TS];
     __shared__ int32_t counter;
-    const int64_t i = items[blockIdx.x];
-    const int64_t j = L.lo + i;
-    const int64_t s = L.ptr[j], e = L.ptr[j + 1];
+    const LeafTask tk = tasks[blockIdx.x];
+    const int64_t s = tk.s, e = tk.e;
     hash_clear<BLOCK, TS>(keys, nullptr);
     if (threadIdx.x == 0) counter = 0;
     __syncthreads();
     for (int64_t t = s + threadIdx.x; t < e; t += BLOCK) hash_insert_key<TS>(keys, L.col[t], &counter);
     __syncthreads();
     if (threadIdx.x == 0) {
-        leaf_nnz[i] = counter;
-        slot_cnt[L.origin[j]] = counter;
+        leaf_nnz[tk.a] = counter;
+        slot_cnt[tk.t] = counter;
     }
 }
 
@@ -412,23 +417,42 @@ GM_DEV void leaf_target(const LeafOut &o, int64_t origin, int64_t &dst, int64_t 
     col_base = (int32_t)(slot << o.slot_width_log2);
 }
 
+// Per-leaf launch records, in the order of a bin partition, so every leaf
+// work group starts from one load instead of a chain of dependent ones.
+__global__ void k_leaf_tasks_sym(LeafSet L, const int64_t *items, int64_t n, LeafTask *tasks) {
+    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < n; k += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i = items[k];
+        const int64_t j = L.lo + i;
+        tasks[k] = LeafTask{L.ptr[j], L.ptr[j + 1], L.origin[j], (int32_t)i, 0};
+    }
+}
+
+__global__ void k_leaf_tasks_num(LeafSet L, const int64_t *items, int64_t n, const int64_t *leaf_nnz, LeafOut o,
+                                 LeafTask *tasks) {
+    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < n; k += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i = items[k];
+        const int64_t j = L.lo + i;
+        int64_t dst, cap;
+        int32_t base;
+        leaf_target(o, L.origin[j], dst, cap, base);
+        const int64_t nnz = leaf_nnz[i] < cap ? leaf_nnz[i] : cap;
+        tasks[k] = LeafTask{L.ptr[j], L.ptr[j + 1], dst, (int32_t)nnz, base};
+    }
+}
+
 template <int BLOCK, int TS>
-__global__ __launch_bounds__(BLOCK) void k_leaf_hash_num(LeafSet L, const int64_t *items, const int64_t *leaf_nnz,
-                                                         LeafOut o) {
+__global__ __launch_bounds__(BLOCK) void k_leaf_hash_num(LeafSet L, const LeafTask *tasks, LeafOut o) {
     __shared__ int32_t keys[TS];
     __shared__ double vals[TS];
     __shared__ int32_t scan_sm[BLOCK / GM_WAVE];
-    const int64_t i = items[blockIdx.x];
-    const int64_t j = L.lo + i;
-    const int64_t s = L.ptr[j], e = L.ptr[j + 1];
+    const LeafTask tk = tasks[blockIdx.x];
+    const int64_t s = tk.s, e = tk.e;
     hash_clear<BLOCK, TS>(keys, vals);
     __syncthreads();
     for (int64_t t = s + threadIdx.x; t < e; t += BLOCK) hash_insert_add<TS>(keys, vals, L.col[t], L.val[t]);
     __syncthreads();
-    int64_t dst, cap;
-    int32_t base;
-    leaf_target(o, L.origin[j], dst, cap, base);
-    const int64_t nnz = leaf_nnz[i] < cap ? leaf_nnz[i] : cap;
+    const int64_t dst = tk.t, nnz = tk.a;
+    const int32_t base = tk.b;
     hash_emit_sorted<BLOCK, TS>(keys, vals, nnz, base, o.c_col + dst, o.c_val + dst, scan_sm, o.err);
 }
 
@@ -438,12 +462,11 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_hash_num(LeafSet L, const int64_
 constexpr int LEAF_EPT = 8;
 
 template <int BLOCK>
-__global__ __launch_bounds__(BLOCK) void k_leaf_dense_sym(LeafSet L, const int64_t *items, int width,
+__global__ __launch_bounds__(BLOCK) void k_leaf_dense_sym(LeafSet L, const LeafTask *tasks, int width,
                                                           int64_t *leaf_nnz, int64_t *slot_cnt) {
-    __shared__ DenseLds<BLOCK, DENSE_MAX> D;
-    const int64_t i = items[blockIdx.x];
-    const int64_t j = L.lo + i;
-    const int64_t s = L.ptr[j], e = L.ptr[j + 1];
+    __shared__ DenseBits<BLOCK, DENSE_MAX> D;
+    const LeafTask tk = tasks[blockIdx.x];
+    const int64_t s = tk.s, e = tk.e;
     dense_clear(D, width, false);
     __syncthreads();
     for (int64_t b = s; b < e; b += BLOCK * 2 * LEAF_EPT) {
@@ -460,38 +483,54 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_dense_sym(LeafSet L, const int64
     __syncthreads();
     const int32_t cnt = dense_count(D, width);
     if (threadIdx.x == 0) {
-        leaf_nnz[i] = cnt;
-        slot_cnt[L.origin[j]] = cnt;
+        leaf_nnz[tk.a] = cnt;
+        slot_cnt[tk.t] = cnt;
     }
 }
 
-template <int BLOCK>
-__global__ __launch_bounds__(BLOCK) void k_leaf_dense_num(LeafSet L, const int64_t *items, const int64_t *leaf_nnz,
-                                                          int width, LeafOut o) {
+// Numeric dense accumulation with 1024 threads (16 waves) per work group:
+// the next batch's loads are issued before the current batch's LDS updates
+// (and the first batch's before the LDS clear), so with only two work groups
+// per CU (64 KB of values each) a work group's loads overlap its LDS work.
+constexpr int DENSE_BLOCK = 1024, DENSE_EPT = 4;
+
+template <int BLOCK, int EPT>
+__global__ __launch_bounds__(BLOCK) void k_leaf_dense_num(LeafSet L, const LeafTask *tasks, int width, LeafOut o) {
     __shared__ DenseLds<BLOCK, DENSE_MAX> D;
-    const int64_t i = items[blockIdx.x];
-    const int64_t j = L.lo + i;
-    const int64_t s = L.ptr[j], e = L.ptr[j + 1];
+    const LeafTask tk = tasks[blockIdx.x];
+    const int64_t s = tk.s, e = tk.e;
+    constexpr int STEP = BLOCK * EPT;
+    int32_t c[EPT];
+    double v[EPT];
+#pragma unroll
+    for (int q = 0; q < EPT; ++q) {
+        const int64_t t = s + q * BLOCK + threadIdx.x;
+        c[q] = t < e ? __builtin_nontemporal_load(&L.col[t]) : -1;
+        v[q] = t < e ? __builtin_nontemporal_load(&L.val[t]) : 0.0;
+    }
     dense_clear(D, width, true);
     __syncthreads();
-    for (int64_t b = s; b < e; b += BLOCK * LEAF_EPT) {
-        int32_t c[LEAF_EPT];
-        double v[LEAF_EPT];
+    for (int64_t b = s; b < e; b += STEP) {
+        int32_t cn[EPT];
+        double vn[EPT];
 #pragma unroll
-        for (int q = 0; q < LEAF_EPT; ++q) {
-            const int64_t t = b + q * BLOCK + threadIdx.x;
-            c[q] = t < e ? __builtin_nontemporal_load(&L.col[t]) : -1;
-            v[q] = t < e ? __builtin_nontemporal_load(&L.val[t]) : 0.0;
+        for (int q = 0; q < EPT; ++q) {
+            const int64_t t = b + STEP + q * BLOCK + threadIdx.x;
+            cn[q] = t < e ? __builtin_nontemporal_load(&L.col[t]) : -1;
+            vn[q] = t < e ? __builtin_nontemporal_load(&L.val[t]) : 0.0;
         }
 #pragma unroll
-        for (int q = 0; q < LEAF_EPT; ++q)
+        for (int q = 0; q < EPT; ++q)
             if (c[q] >= 0) dense_add(D, c[q], v[q]);
+#pragma unroll
+        for (int q = 0; q < EPT; ++q) {
+            c[q] = cn[q];
+            v[q] = vn[q];
+        }
     }
     __syncthreads();
-    int64_t dst, cap;
-    int32_t base;
-    leaf_target(o, L.origin[j], dst, cap, base);
-    const int64_t nnz = leaf_nnz[i] < cap ? leaf_nnz[i] : cap;
+    const int64_t dst = tk.t, nnz = tk.a;
+    const int32_t base = tk.b;
     dense_emit(D, width, nnz, base, o.c_col + dst, o.c_val + dst, o.err);
 }
 
@@ -545,26 +584,24 @@ GM_DEV void rank_mark(uint32_t *bits, uint32_t *summ, int nwords, const int32_t 
 }
 
 template <int BLOCK, int NWORDS>
-__global__ __launch_bounds__(BLOCK) void k_leaf_rank_sym(LeafSet L, const int64_t *items, int width,
+__global__ __launch_bounds__(BLOCK) void k_leaf_rank_sym(LeafSet L, const LeafTask *tasks, int width,
                                                          int64_t *leaf_nnz, int64_t *slot_cnt) {
     __shared__ uint32_t bits[NWORDS];
     __shared__ uint32_t summ[NWORDS / 32];
     __shared__ int32_t count;
-    const int64_t i = items[blockIdx.x];
-    const int64_t j = L.lo + i;
+    const LeafTask tk = tasks[blockIdx.x];
     int32_t c[RANK_EPT];
     double v[RANK_EPT];
-    rank_load<BLOCK, RANK_EPT>(L, L.ptr[j], L.ptr[j + 1], c, v, false);
+    rank_load<BLOCK, RANK_EPT>(L, tk.s, tk.e, c, v, false);
     rank_mark<BLOCK, RANK_EPT>(bits, summ, width >> 5, c, &count);
     if (threadIdx.x == 0) {
-        leaf_nnz[i] = count;
-        slot_cnt[L.origin[j]] = count;
+        leaf_nnz[tk.a] = count;
+        slot_cnt[tk.t] = count;
     }
 }
 
 template <int BLOCK, int NWORDS, int CAP>
-__global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const int64_t *items, const int64_t *leaf_nnz,
-                                                         int width, LeafOut o) {
+__global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const LeafTask *tasks, int width, LeafOut o) {
     static_assert(NWORDS / 32 <= BLOCK, "one summary word per thread");
     __shared__ uint32_t bits[NWORDS];
     __shared__ uint32_t summ[NWORDS / 32];
@@ -573,19 +610,16 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const int64_
     __shared__ double vals[CAP];
     __shared__ int32_t scan_sm[BLOCK / GM_WAVE];
     __shared__ int32_t count;
-    const int64_t i = items[blockIdx.x];
-    const int64_t j = L.lo + i;
+    const LeafTask tk = tasks[blockIdx.x];
     const int nwords = width >> 5;
     const int nsumm = (nwords + 31) >> 5;
     int32_t c[RANK_EPT];
     double v[RANK_EPT];
-    rank_load<BLOCK, RANK_EPT>(L, L.ptr[j], L.ptr[j + 1], c, v, true);
+    rank_load<BLOCK, RANK_EPT>(L, tk.s, tk.e, c, v, true);
     rank_mark<BLOCK, RANK_EPT>(bits, summ, nwords, c, &count);
     const int32_t total = count;
-    int64_t dst, cap;
-    int32_t base;
-    leaf_target(o, L.origin[j], dst, cap, base);
-    const int64_t nnz = leaf_nnz[i] < cap ? leaf_nnz[i] : cap;
+    const int64_t dst = tk.t, nnz = tk.a;
+    const int32_t base = tk.b;
     const int n = total < CAP ? total : CAP;
     const int m = n < nnz ? n : (int)nnz;
     if (threadIdx.x == 0 && (total != nnz || total > CAP)) atomicOr(o.err, 4);
@@ -732,7 +766,23 @@ void light_numeric(const Csr &A, const Csr &B, int64_t r0, int bin, const int64_
     }
 }
 
-void leaf_symbolic(const LeafSet &L, int bin, const int64_t *items, int64_t n, int width, int64_t *leaf_nnz,
+void leaf_tasks_sym(const LeafSet &L, const int64_t *items, int64_t n, LeafTask *tasks, hipStream_t s) {
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_leaf_tasks_sym, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, L, items, n, tasks);
+    GM_CHECK_LAUNCH();
+}
+
+void leaf_tasks_num(const LeafSet &L, const int64_t *items, int64_t n, const int64_t *leaf_nnz, int n_slots_log2,
+                    const int64_t *heavy_rows, const int64_t *c_row_ptr, const int64_t *slot_off,
+                    int slot_width_log2, LeafTask *tasks, hipStream_t s) {
+    if (n <= 0) return;
+    LeafOut o{n_slots_log2, heavy_rows, c_row_ptr, slot_off, slot_width_log2, nullptr, nullptr, nullptr};
+    hipLaunchKernelGGL(k_leaf_tasks_num, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, L, items, n, leaf_nnz, o,
+                       tasks);
+    GM_CHECK_LAUNCH();
+}
+
+void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *items, int64_t n, int width, int64_t *leaf_nnz,
                    int64_t *slot_cnt, hipStream_t s) {
     switch (bin) {
     case LEAF_H0: launch_items(k_leaf_hash_sym<64, 2 * HS_CAP[0]>, 64, n, s, L, items, leaf_nnz, slot_cnt); break;
@@ -753,18 +803,17 @@ void leaf_symbolic(const LeafSet &L, int bin, const int64_t *items, int64_t n, i
     }
 }
 
-void leaf_numeric(const LeafSet &L, int bin, const int64_t *items, int64_t n, int width, const int64_t *leaf_nnz,
-                  int n_slots_log2, const int64_t *heavy_rows, const int64_t *c_row_ptr, const int64_t *slot_off,
-                  int slot_width_log2, int32_t *c_col, double *c_val, int32_t *err, hipStream_t s) {
-    LeafOut o{n_slots_log2, heavy_rows, c_row_ptr, slot_off, slot_width_log2, c_col, c_val, err};
+void leaf_numeric(const LeafSet &L, int bin, const LeafTask *items, int64_t n, int width, int32_t *c_col,
+                  double *c_val, int32_t *err, hipStream_t s) {
+    LeafOut o{0, nullptr, nullptr, nullptr, 0, c_col, c_val, err};
     switch (bin) {
-    case LEAF_H0: launch_items(k_leaf_hash_num<64, 256>, 64, n, s, L, items, leaf_nnz, o); break;
-    case LEAF_H1: launch_items(k_leaf_hash_num<64, 1024>, 64, n, s, L, items, leaf_nnz, o); break;
-    case LEAF_H2: launch_items(k_leaf_hash_num<256, 4096>, 256, n, s, L, items, leaf_nnz, o); break;
-    case LEAF_H3: launch_items(k_leaf_hash_num<512, 8192>, 512, n, s, L, items, leaf_nnz, o); break;
+    case LEAF_H0: launch_items(k_leaf_hash_num<64, 256>, 64, n, s, L, items, o); break;
+    case LEAF_H1: launch_items(k_leaf_hash_num<64, 1024>, 64, n, s, L, items, o); break;
+    case LEAF_H2: launch_items(k_leaf_hash_num<256, 4096>, 256, n, s, L, items, o); break;
+    case LEAF_H3: launch_items(k_leaf_hash_num<512, 8192>, 512, n, s, L, items, o); break;
     case LEAF_DENSE:
         GM_REQUIRE(n <= 0 || width <= DENSE_MAX, GMAGNUS_ERROR_UNSUPPORTED, "dense accumulator wider than LDS allows");
-        launch_items(k_leaf_dense_num<512>, 512, n, s, L, items, leaf_nnz, width, o);
+        launch_items(k_leaf_dense_num<DENSE_BLOCK, DENSE_EPT>, DENSE_BLOCK, n, s, L, items, width, o);
         break;
     case LEAF_RANK:
     case LEAF_RANK_L: {
@@ -772,15 +821,13 @@ void leaf_numeric(const LeafSet &L, int bin, const int64_t *items, int64_t n, in
         constexpr int W17 = (1 << 17) / 32, W18 = (1 << 18) / 32;
         const bool narrow = width <= (1 << 17);
         if (bin == LEAF_RANK && narrow)
-            launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_SMALL>, RANK_BLOCK, n, s, L, items, leaf_nnz, width, o);
+            launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_SMALL>, RANK_BLOCK, n, s, L, items, width, o);
         else if (bin == LEAF_RANK)
-            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_SMALL>, RANK_BLOCK, n, s, L, items, leaf_nnz, width, o);
+            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_SMALL>, RANK_BLOCK, n, s, L, items, width, o);
         else if (narrow)
-            launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_NNZ_MAX>, RANK_BLOCK, n, s, L, items, leaf_nnz, width,
-                         o);
+            launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_NNZ_MAX>, RANK_BLOCK, n, s, L, items, width, o);
         else
-            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_NNZ_MAX>, RANK_BLOCK, n, s, L, items, leaf_nnz, width,
-                         o);
+            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_NNZ_MAX>, RANK_BLOCK, n, s, L, items, width, o);
         break;
     }
     default: break;

@@ -135,10 +135,18 @@ __global__ __launch_bounds__(EXP_BLOCK) void k_expand(Csr B, const int64_t *col_
 // row) is cut further at the first-level chunk boundaries of that B row
 // (bnd: per slice, offsets of the first column of every chunk), giving
 // "runs" that all go to one (heavy row, chunk) output row. Runs stay in
-// product order (the B row is sorted), so a batch of runs again covers a
-// contiguous range of tile-local products. Each nonempty run reserves its
+// product order (the B row is sorted), so the nonempty runs of a batch tile
+// a contiguous range of tile-local products. Each nonempty run reserves its
 // range with one atomic add on cursor[h * nc + c] (the output row's next
 // free position); the products are written with the chunk-local column.
+//
+// A product finds its run in constant time: the nonempty runs are
+// compacted, their first products are marked in a tile-wide bitmap, and a
+// product's run is the number of marks at or before it, minus one (word
+// prefix counts plus one popcount), with no per-product search.
+constexpr int EXP_WORDS = (int)(EXP_TILE / 32);
+static_assert(EXP_WORDS == EXP_BLOCK, "one bitmap word per thread");
+
 __global__ __launch_bounds__(EXP_BLOCK) void k_expand_split(
     Csr B, const int64_t *col_ptr, const int64_t *slice_off, const int32_t *slice_k, const int32_t *row_h,
     const double *a_val, int64_t n_slices, int64_t total, int64_t n_tiles, const TileInfo *info, const int32_t *bnd,
@@ -153,11 +161,13 @@ __global__ __launch_bounds__(EXP_BLOCK) void k_expand_split(
     __shared__ int32_t sg_end[EXP_BLOCK];   // offset one past the segment's last product
     __shared__ int32_t sg_c[EXP_BLOCK];     // chunk of the first product
     __shared__ int32_t run_base[EXP_BLOCK + 1];
-    __shared__ int32_t rn_lo[EXP_BLOCK + 1];  // tile-local index of each run's first product
-    __shared__ int64_t rn_dst[EXP_BLOCK];   // output position minus tile-local index
+    __shared__ int64_t rn_dst[EXP_BLOCK];   // output position minus tile-local index (compacted runs)
     __shared__ int64_t rn_src[EXP_BLOCK];   // B position minus tile-local index
     __shared__ double rn_a[EXP_BLOCK];
+    __shared__ uint32_t start_bits[EXP_WORDS];
+    __shared__ int32_t word_pre[EXP_WORDS];
     __shared__ int32_t scan_sm[EXP_BLOCK / GM_WAVE];
+    __shared__ int32_t range[2];
     __shared__ int64_t next_base;
 
     const int tid = threadIdx.x;
@@ -203,6 +213,10 @@ __global__ __launch_bounds__(EXP_BLOCK) void k_expand_split(
 
         for (int rb = 0; rb < n_runs; rb += EXP_BLOCK) {
             const int nrb = n_runs - rb < EXP_BLOCK ? n_runs - rb : EXP_BLOCK;
+            start_bits[tid] = 0u;
+            int32_t loc = 0, len = 0;
+            int64_t dst = 0, src = 0;
+            double av = 0.0;
             if (tid < nrb) {
                 const int gr = rb + tid;
                 const int q = (int)find_row(run_base, 0, nb, gr);
@@ -213,34 +227,44 @@ __global__ __launch_bounds__(EXP_BLOCK) void k_expand_split(
                 // are whole chunks of the B row (possibly empty)
                 const int32_t lo_r = b_lo > sg_off[q] ? b_lo : sg_off[q];
                 const int32_t hi_r = b_hi < sg_end[q] ? b_hi : sg_end[q];
-                const int32_t len = hi_r - lo_r;
-                const int32_t loc = sg_loc[q] + (lo_r - sg_off[q]);
-                int64_t dst = 0;
+                len = hi_r > lo_r ? hi_r - lo_r : 0;
+                loc = sg_loc[q] + (lo_r - sg_off[q]);
                 if (len > 0)
                     dst = (int64_t)atomicAdd((unsigned long long *)&cursor[sg_hc[q] + c], (unsigned long long)len);
-                rn_lo[tid] = loc;
-                rn_dst[tid] = dst - loc;
-                rn_src[tid] = sg_b[q] + lo_r - loc;
-                rn_a[tid] = sg_a[q];
-                if (tid == nrb - 1) rn_lo[nrb] = loc + len;
+                src = sg_b[q] + lo_r;
+                av = sg_a[q];
+            }
+            // compact the nonempty runs (block_excl_scan synchronizes, so the
+            // bitmap is clear before it is marked)
+            int n_ne = 0;
+            const int slot = block_excl_scan<EXP_BLOCK, int>(len > 0 ? 1 : 0, scan_sm, &n_ne);
+            if (len > 0) {
+                rn_dst[slot] = dst - loc;
+                rn_src[slot] = src - loc;
+                rn_a[slot] = av;
+                atomicOr(&start_bits[loc >> 5], 1u << (loc & 31));
+                if (slot == 0) range[0] = loc;
+                if (slot == n_ne - 1) range[1] = loc + len;
             }
             __syncthreads();
-            const int t0 = rn_lo[0], t1 = rn_lo[nrb];
-            int q_prev = 0;
+            word_pre[tid] = block_excl_scan<EXP_BLOCK, int>(__popc(start_bits[tid]), scan_sm);
+            __syncthreads();
+            const int t0 = n_ne > 0 ? range[0] : 0, t1 = n_ne > 0 ? range[1] : 0;
             for (int tb = t0 + tid; tb < t1; tb += EXP_BLOCK * EXP_ILP) {
                 int32_t c[EXP_ILP];
-                double bv[EXP_ILP], av[EXP_ILP];
+                double bv[EXP_ILP], a[EXP_ILP];
                 int64_t d[EXP_ILP];
 #pragma unroll
                 for (int u = 0; u < EXP_ILP; ++u) {
                     const int t = tb + u * EXP_BLOCK;
                     if (t < t1) {
-                        const int q = (int)find_row(rn_lo, q_prev, nrb, t);
-                        q_prev = q;
-                        const int64_t src = rn_src[q] + t;
-                        c[u] = B.ci[src];
-                        bv[u] = B.v[src];
-                        av[u] = rn_a[q];
+                        const int w = t >> 5, bit = t & 31;
+                        const uint32_t below = bit == 31 ? ~0u : (2u << bit) - 1u;
+                        const int q = word_pre[w] + __popc(start_bits[w] & below) - 1;
+                        const int64_t sp = rn_src[q] + t;
+                        c[u] = B.ci[sp];
+                        bv[u] = B.v[sp];
+                        a[u] = rn_a[q];
                         d[u] = rn_dst[q] + t;
                     }
                 }
@@ -248,7 +272,7 @@ __global__ __launch_bounds__(EXP_BLOCK) void k_expand_split(
                 for (int u = 0; u < EXP_ILP; ++u) {
                     if (tb + u * EXP_BLOCK < t1) {
                         out_col[d[u]] = c[u] & mask;
-                        out_val[d[u]] = av[u] * bv[u];
+                        out_val[d[u]] = a[u] * bv[u];
                     }
                 }
             }

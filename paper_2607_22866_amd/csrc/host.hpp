@@ -208,14 +208,23 @@ void light_classes_num(const int64_t *ip, const int64_t *row_nnz, const int32_t 
 void leaf_classes_sym(const LeafSet &L, int64_t tau, int width, uint8_t *cls, hipStream_t s);
 void leaf_classes_num(const LeafSet &L, const int64_t *leaf_nnz, int64_t tau, int width, uint8_t *cls,
                       hipStream_t s);
-// Leaf symbolic: leaf_nnz[i] for the leaves items[0..n) (leaf i = chunk row
-// lo + i), and slot_cnt[origin] = leaf_nnz.
-void leaf_symbolic(const LeafSet &L, int bin, const int64_t *items, int64_t n, int width, int64_t *leaf_nnz,
+// Launch record of one leaf, built in bin-partition order: element range
+// [s, e); symbolic: t = slot id, a = leaf index; numeric: t = first C
+// position, a = nnz written, b = column base of the slot.
+struct LeafTask {
+    int64_t s, e, t;
+    int32_t a, b;
+};
+void leaf_tasks_sym(const LeafSet &L, const int64_t *items, int64_t n, LeafTask *tasks, hipStream_t s);
+void leaf_tasks_num(const LeafSet &L, const int64_t *items, int64_t n, const int64_t *leaf_nnz, int n_slots_log2,
+                    const int64_t *heavy_rows, const int64_t *c_row_ptr, const int64_t *slot_off,
+                    int slot_width_log2, LeafTask *tasks, hipStream_t s);
+// Leaf symbolic: leaf_nnz[leaf] and slot_cnt[slot] for the n tasks of a bin.
+void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *tasks, int64_t n, int width, int64_t *leaf_nnz,
                    int64_t *slot_cnt, hipStream_t s);
-// Leaf numeric: writes C at c_row_ptr[heavy_rows[h]] + slot_off[origin].
-void leaf_numeric(const LeafSet &L, int bin, const int64_t *items, int64_t n, int width, const int64_t *leaf_nnz,
-                  int n_slots_log2, const int64_t *heavy_rows, const int64_t *c_row_ptr, const int64_t *slot_off,
-                  int slot_width_log2, int32_t *c_col, double *c_val, int32_t *err, hipStream_t s);
+// Leaf numeric: writes C at each task's position.
+void leaf_numeric(const LeafSet &L, int bin, const LeafTask *tasks, int64_t n, int width, int32_t *c_col,
+                  double *c_val, int32_t *err, hipStream_t s);
 // Light rows (local index r): symbolic count into row_nnz[r]; numeric into C.
 void light_symbolic(const Csr &A, const Csr &B, int64_t r0, int bin, const int64_t *items, int64_t n,
                     const int32_t *minc, const int32_t *maxc, int64_t *row_nnz, hipStream_t s);

@@ -736,16 +736,19 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         GM_HIP(hipStreamSynchronize(s));
         lv.elems = e1 - e0;
         {
+            LeafTask *tasks = ws.alloc<LeafTask>(nl);
+            leaf_tasks_sym(lv.set, lv.items_sym, nl, tasks, s);
             Timed t(p, GMAGNUS_K_CHUNK_SYM, s);
             for (int b = LEAF_H0; b < LEAF_NBINS; ++b) {
                 const int64_t cnt = lv.bins_sym[b + 1] - lv.bins_sym[b];
-                leaf_symbolic(lv.set, b, lv.items_sym + lv.bins_sym[b], cnt, lv.width, lv.leaf_nnz, p->slot, s);
+                leaf_symbolic(lv.set, b, tasks + lv.bins_sym[b], cnt, lv.width, lv.leaf_nnz, p->slot, s);
                 if (cnt) p->info.kernel_launches[GMAGNUS_K_CHUNK_SYM] += 1;
                 if (b == LEAF_DENSE) p->info.n_leaves_dense += cnt;
                 else if (b == LEAF_RANK || b == LEAF_RANK_L) p->info.n_leaves_rank += cnt;
                 else p->info.n_leaves_hash += cnt;
             }
             add_bytes(p, GMAGNUS_K_CHUNK_SYM, 4.0 * lv.elems + 16.0 * nl);
+            ws.free(tasks);
         }
         // numeric bins now, so the numeric phase needs no host round trip
         {
@@ -873,12 +876,17 @@ void do_numeric(gmagnus_plan_s *p, const int64_t *c_row_ptr, int32_t *c_col, dou
         const hipStream_t s = p->s_heavy;
         Timed t(p, GMAGNUS_K_CHUNK_NUM, s);
         for (auto &lv : p->leaves) {
+            const int64_t nl = lv.set.hi - lv.set.lo;
+            if (nl <= 0) continue;
+            LeafTask *tasks = p->ws->alloc<LeafTask>(nl);
+            leaf_tasks_num(lv.set, lv.items_num, nl, lv.leaf_nnz, p->n_slots_log2, p->heavy_rows, c_row_ptr, p->slot,
+                           p->slot_width_log2, tasks, s);
             for (int b = LEAF_H0; b < LEAF_NBINS; ++b) {
                 const int64_t cnt = lv.bins_num[b + 1] - lv.bins_num[b];
-                leaf_numeric(lv.set, b, lv.items_num + lv.bins_num[b], cnt, lv.width, lv.leaf_nnz, p->n_slots_log2,
-                             p->heavy_rows, c_row_ptr, p->slot, p->slot_width_log2, c_col, c_val, p->err, s);
+                leaf_numeric(lv.set, b, tasks + lv.bins_num[b], cnt, lv.width, c_col, c_val, p->err, s);
                 if (cnt) p->info.kernel_launches[GMAGNUS_K_CHUNK_NUM] += 1;
             }
+            p->ws->free(tasks);
             add_bytes(p, GMAGNUS_K_CHUNK_NUM, 12.0 * lv.elems);
         }
     }

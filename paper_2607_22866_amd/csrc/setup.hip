@@ -92,14 +92,14 @@ GM_DEV void for_heavy_entries(const Csr &A, const int64_t *heavy_rows, int64_t n
             h_end = a_heavy_ptr[h + 1];
             a_base = A.rp[r0 + heavy_rows[h]] - a_heavy_ptr[h];
         }
-        f(h, a_base + e);
+        f(h, a_base + e, e);
     }
 }
 
 __global__ __launch_bounds__(FLAT_BLOCK) void k_csc_count(Csr A, Csr B, const int64_t *heavy_rows, int64_t n_heavy,
                                                           int64_t r0, const int64_t *a_heavy_ptr, int64_t total,
                                                           int64_t *colcnt) {
-    for_heavy_entries(A, heavy_rows, n_heavy, r0, a_heavy_ptr, total, [&](int64_t, int64_t j) {
+    for_heavy_entries(A, heavy_rows, n_heavy, r0, a_heavy_ptr, total, [&](int64_t, int64_t j, int64_t) {
         const int32_t k = A.ci[j];
         if (B.rp[k + 1] > B.rp[k]) atomicAdd((unsigned long long *)&colcnt[k], 1ull);
     });
@@ -126,7 +126,7 @@ __global__ __launch_bounds__(FLAT_BLOCK) void k_csc_fill(Csr A, const int64_t *h
                                                          int64_t r0, const int64_t *a_heavy_ptr, int64_t total,
                                                          const int32_t *k_to_slice, const int64_t *col_ptr,
                                                          int64_t *fill_cursor, int32_t *row_h, double *a_val) {
-    for_heavy_entries(A, heavy_rows, n_heavy, r0, a_heavy_ptr, total, [&](int64_t h, int64_t j) {
+    for_heavy_entries(A, heavy_rows, n_heavy, r0, a_heavy_ptr, total, [&](int64_t h, int64_t j, int64_t) {
         const int32_t s = k_to_slice[A.ci[j]];
         if (s < 0) return;
         const int64_t pos =
