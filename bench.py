@@ -8,9 +8,13 @@ values). Inputs are resident in HBM before timing starts; each panel of C is
 written to HBM (panels reuse one allocation when C does not fit at once).
 
 Prints one JSON line (see the repository's benchmark contract). The
-roofline object is for the kernel class with the largest device time,
-measured with HIP events on the streams the kernels run on; the oracle is
-timed on a bounded sample of rows for the CPU baseline.
+roofline object is for the single kernel (one launch per panel) with the
+largest device time: its algorithmic bytes per launch over its average
+launch time, measured with HIP events on the stream it runs on. Its
+"traffic" is the HBM bytes per launch from the committed rocprofv3 counter
+summary (FETCH_SIZE + WRITE_SIZE scaled by a copy kernel's reading), or null
+when there is none or the kernel's sources changed since it was taken. The
+oracle is timed on a bounded sample of rows for the CPU baseline.
 """
 from __future__ import annotations
 
@@ -33,6 +37,15 @@ WORKLOADS = {
     "rmat23": "R-MAT scale 23 (2^23 x 2^23), edge factor 8, (a,b,c,d)=(0.60,0.17,0.17,0.06), fp64 U(0,1), C=A*A",
 }
 HEAVY_KERNELS = ["expand", "histogram", "multisplit", "chunk_symbolic", "chunk_numeric"]
+# Timing classes that are exactly one kernel launch per panel: the roofline is
+# reported for the one of these with the largest device time.
+SINGLE_KERNEL_CLASSES = {"expand": "k_expand_split", "multisplit": "k_multisplit"}
+# Sources a kernel's counter summary depends on (traffic is dropped when they change).
+KERNEL_SOURCES = {"k_expand_split": ["paper_2607_22866_amd/csrc/expand.hip", "paper_2607_22866_amd/csrc/common.hpp"],
+                  "k_multisplit": ["paper_2607_22866_amd/csrc/multisplit.hip",
+                                   "paper_2607_22866_amd/csrc/common.hpp"]}
+TRAFFIC_FILES = {"k_expand_split": "profiles/expand_split_rmat22_traffic.md",
+                 "k_multisplit": "profiles/multisplit_rmat22_traffic.md"}
 
 
 def log(msg):
@@ -85,6 +98,34 @@ def copy_peak(torch, nbytes=4 << 30, reps=5):
     return gbs
 
 
+def source_hash(kernel):
+    import hashlib
+
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel, config):
+    """HBM bytes per launch from the committed counter summary of this kernel
+    (FETCH_SIZE + WRITE_SIZE, scaled by the copy-kernel calibration), or None
+    when there is none for this workload or the kernel changed since."""
+    path = os.path.join(ROOT, TRAFFIC_FILES.get(kernel, ""))
+    if not os.path.isfile(path):
+        return None
+    vals = {}
+    with open(path) as fh:
+        for line in fh:
+            if line.startswith("traffic:"):
+                k, _, v = line[len("traffic:"):].strip().partition("=")
+                vals[k.strip()] = v.strip()
+    if vals.get("source_hash") != source_hash(kernel) or vals.get("config") != config:
+        return None
+    return float(vals["bytes_per_launch"])
+
+
 def cpu_baseline(A, ip, budget_products, seed=0):
     """Times the oracle on a random sample of rows (about budget_products products)."""
     import numpy as np
@@ -118,9 +159,11 @@ def main():
     ap.add_argument("--config", default="rmat22", choices=sorted(WORKLOADS))
     ap.add_argument("--panel-products", type=float, default=4e9,
                     help="maximum intermediate products per row panel")
-    ap.add_argument("--cpu-products", type=float, default=4e8, help="oracle sample size for the CPU baseline")
+    ap.add_argument("--cpu-products", type=float, default=2.5e9, help="oracle sample size for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--serial", action="store_true", help="run heavy and light work on one stream")
+    ap.add_argument("--paper-expansion", action="store_true",
+                    help="expand C-hat row by row and split it afterwards (the paper's order)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build measures the single-GPU hot path "
@@ -151,7 +194,7 @@ def main():
     log("%d row panels (max %.2g products each)" % (len(bounds) - 1, args.panel_products))
     acc_warm = {}
     c_bufs = [None, None]
-    extra = g.FLAG_SERIAL_STREAMS if args.serial else 0
+    extra = (g.FLAG_SERIAL_STREAMS if args.serial else 0) | (g.FLAG_PAPER_EXPANSION if args.paper_expansion else 0)
     for w in range(args.warmup):
         t = time.perf_counter()
         run_step(g, dA, bounds, False, acc_warm, c_bufs, extra)
@@ -180,15 +223,21 @@ def main():
         kernels[k] = {"ms_per_step": ms / args.steps, "launches_per_step": launches / args.steps,
                       "gb_per_step": byts / args.steps / 1e9,
                       "achieved_gbs": (byts / (ms / 1000.0) / 1e9) if ms > 0 else None}
-    compute = {k: v for k, v in kernels.items() if k in HEAVY_KERNELS + ["light_symbolic", "light_numeric"]}
-    dom = max(compute, key=lambda k: compute[k]["ms_per_step"]) if compute else None
+    single = {k: v for k, v in kernels.items() if k in SINGLE_KERNEL_CLASSES and v["launches_per_step"] > 0}
+    dom = max(single, key=lambda k: single[k]["ms_per_step"]) if single else None
     roofline = None
     if dom:
         d = kernels[dom]
-        roofline = {"bound": "hbm", "kernel": dom, "achieved": d["achieved_gbs"], "peak": HBM_PEAK_GBS,
-                    "unit": "GB/s", "frac": d["achieved_gbs"] / HBM_PEAK_GBS,
-                    "bytes_per_launch": d["gb_per_step"] * 1e9 / max(d["launches_per_step"], 1),
-                    "avg_launch_ms": d["ms_per_step"] / max(d["launches_per_step"], 1), "traffic": None}
+        kname = SINGLE_KERNEL_CLASSES[dom]
+        if dom == "expand" and args.paper_expansion:
+            kname = "k_expand"
+        bpl = d["gb_per_step"] * 1e9 / d["launches_per_step"]
+        ms = d["ms_per_step"] / d["launches_per_step"]
+        achieved = bpl / (ms / 1000.0) / 1e9
+        roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(kname, args.config),
+                    "kernel": kname, "algorithmic_bytes_per_launch": bpl, "avg_launch_ms": ms,
+                    "launches_per_step": d["launches_per_step"], "frac_of_copy": achieved / copy_gbs}
     heavy_ms = sum(kernels[k]["ms_per_step"] for k in HEAVY_KERNELS if k in kernels)
     heavy_gb = sum(kernels[k]["gb_per_step"] for k in HEAVY_KERNELS if k in kernels)
     all_ms = sum(v["ms_per_step"] for v in kernels.values())

@@ -128,6 +128,8 @@ void slice_build(const Csr &B, const int64_t *colcnt, const int64_t *slice_perm,
 void csc_fill(const Csr &A, const Csr &B, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
               const int64_t *a_heavy_ptr, int64_t nnz_heavy_all, const int32_t *k_to_slice,
               const int64_t *col_ptr, int64_t *fill_cursor, int32_t *row_h, double *a_val, hipStream_t s);
+// len[s] = nnz(B[slice_k[s], :]).
+void slice_lengths(const Csr &B, const int32_t *slice_k, int64_t n, int64_t *len, hipStream_t s);
 // Level-0 histogram from the structure: per-slice chunk boundaries in its B
 // row (n_slices * (nc + 1) offsets), then per heavy row the sum of its A~
 // entries' chunk sizes (counts: n_heavy * nc).

@@ -499,11 +499,18 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         int64_t *sc2 = ws.alloc<int64_t>(scan_scratch_elems(sl.n_slices));
         scan_i64(cnt_s, sl.n_slices, sl.col_ptr, sc2, s);
         scan_i64(ip_s, sl.n_slices, sl.slice_off, sc2, s);
-        int64_t tot[2];
+        // B~: the B rows of the slices, each read once at least (compulsory bytes)
+        int64_t *blen_scan = ws.alloc<int64_t>(sl.n_slices + 1);
+        slice_lengths(p->B, sl.slice_k, sl.n_slices, cnt_s, s);
+        scan_i64(cnt_s, sl.n_slices, blen_scan, sc2, s);
+        int64_t tot[3];
         GM_HIP(hipMemcpyAsync(&tot[0], sl.col_ptr + sl.n_slices, sizeof(int64_t), hipMemcpyDeviceToHost, s));
         GM_HIP(hipMemcpyAsync(&tot[1], sl.slice_off + sl.n_slices, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+        GM_HIP(hipMemcpyAsync(&tot[2], blen_scan + sl.n_slices, sizeof(int64_t), hipMemcpyDeviceToHost, s));
         GM_HIP(hipStreamSynchronize(s));
+        ws.free(blen_scan);
         sl.nnz = tot[0];
+        blen_total = tot[2];
         GM_REQUIRE(tot[1] == H, GMAGNUS_ERROR_HIP, "slice products disagree with the row products");
         int64_t *cursor = ws.alloc<int64_t>(std::max<int64_t>(sl.n_slices, 1));
         fill<int64_t>(cursor, 0, sl.n_slices, s);
@@ -528,8 +535,6 @@ void heavy_symbolic(gmagnus_plan_s *p) {
             p->info.kernel_launches[GMAGNUS_K_HISTOGRAM] += 1;
             add_bytes(p, GMAGNUS_K_HISTOGRAM, 12.0 * nnz_heavy_all + 4.0 * sl.n_slices * (nc0 + 1) + 8.0 * nh * nc0);
         }
-        // compulsory bytes of B~ (each slice's B row once): sum of nnz(B[k,:]) over slices
-        blen_total = 0;
         ws.free(cursor);
         ws.free(colcnt);
         ws.free(kcls);
@@ -575,10 +580,9 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         }
         ws.free(cursor);
         p->info.kernel_launches[GMAGNUS_K_EXPAND] += 1;
-        add_bytes(p, GMAGNUS_K_EXPAND, 12.0 * H + 12.0 * sl.nnz + 8.0 * nh);
+        add_bytes(p, GMAGNUS_K_EXPAND, 12.0 * H + 12.0 * sl.nnz + 12.0 * blen_total + 8.0 * nh);
         free_slices();
     }
-    (void)blen_total;
 
     // ---- hierarchical multisplit
     int64_t *origin_in = ws.alloc<int64_t>(nh);
@@ -673,7 +677,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
             }
             ws.free(cursor);
             p->info.kernel_launches[GMAGNUS_K_EXPAND] += 1;
-            add_bytes(p, GMAGNUS_K_EXPAND, 12.0 * H + 12.0 * sl.nnz + 8.0 * n_out);
+            add_bytes(p, GMAGNUS_K_EXPAND, 12.0 * H + 12.0 * sl.nnz + 12.0 * blen_total + 8.0 * n_out);
             free_slices();
         } else {
             int64_t *cursor = ws.alloc<int64_t>(n_out);

@@ -136,6 +136,11 @@ __global__ __launch_bounds__(FLAT_BLOCK) void k_csc_fill(Csr A, const int64_t *h
     });
 }
 
+__global__ void k_slice_lengths(Csr B, const int32_t *slice_k, int64_t n, int64_t *len) {
+    for (int64_t s = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; s < n; s += (int64_t)gridDim.x * blockDim.x)
+        len[s] = B.rp[slice_k[s] + 1] - B.rp[slice_k[s]];
+}
+
 // Level-0 chunk boundaries of every slice's B row: bnd[s * (nc + 1) + c] =
 // offset in B[k,:] of the row's first column >= c << shift (c = 0..nc). The
 // row is sorted, so lane c of a wave finds it by binary search; chunk c of
@@ -289,6 +294,12 @@ void csc_fill(const Csr &A, const Csr &B, const int64_t *heavy_rows, int64_t n_h
     if (n_heavy <= 0 || nnz_heavy_all <= 0) return;
     hipLaunchKernelGGL(k_csc_fill, dim3(flat_grid(nnz_heavy_all)), dim3(FLAT_BLOCK), 0, s, A, heavy_rows, n_heavy,
                        r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, col_ptr, fill_cursor, row_h, a_val);
+    GM_CHECK_LAUNCH();
+}
+
+void slice_lengths(const Csr &B, const int32_t *slice_k, int64_t n, int64_t *len, hipStream_t s) {
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_slice_lengths, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, B, slice_k, n, len);
     GM_CHECK_LAUNCH();
 }
 
