@@ -99,12 +99,18 @@ def copy_peak(torch, nbytes=4 << 30, reps=5):
 
 
 def source_hash(kernel):
+    """Hash of the kernel's sources with comments and whitespace removed (so a
+    comment edit does not invalidate its counter summary)."""
     import hashlib
+    import re
 
     h = hashlib.sha256()
     for f in KERNEL_SOURCES[kernel]:
-        with open(os.path.join(ROOT, f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, f)) as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -15,8 +15,8 @@
 // fully parallel kernel (no serial binary search at work-group start);
 // segments are processed in batches of one per thread with their slice
 // pointers staged in LDS; tiles are remapped so each XCD works on a
-// contiguous range of slices (B rows reused from that XCD's L2); C-hat is
-// written with non-temporal stores (it is read back only by the next pass).
+// contiguous range of slices (B rows reused from that XCD's L2); stores are
+// cached, so the L2 merges the partial lines at the edges of short runs.
 #include "host.hpp"
 
 namespace gm {
