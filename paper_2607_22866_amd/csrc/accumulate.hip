@@ -285,7 +285,7 @@ __global__ void k_light_classes(const int64_t *ip, const int64_t *row_nnz, const
 
 constexpr int DENSE_MAX = 8192;          // columns of the LDS dense accumulator
 constexpr int RANK_MAX_LOG2 = 18;        // columns of the bitmap-rank accumulator
-constexpr int RANK_NNZ_MAX = 7168;       // distinct columns it holds (>= tau)
+constexpr int RANK_NNZ_MAX = 6912;       // distinct columns it holds (>= tau; two work groups per CU at 2^17 columns)
 constexpr int RANK_MIN_LEN = 256;        // smaller chunks go to the hash map
 constexpr int RANK_SMALL = 2048;         // distinct columns of the small rank variant
 
@@ -541,8 +541,18 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_dense_num(LeafSet L, const LeafT
 // values are summed straight into a rank-indexed array. No hashing and no
 // sort; the output comes out in column order. A chunk is light (at most tau
 // elements), so its elements stay in registers between the two passes.
+//
+// The element that first sets a column's bit writes that column to C at the
+// column's rank; chunks are made of sorted B-row runs over consecutive lanes,
+// so these stores are mostly consecutive. Two shapes: 256 threads with a
+// 256-word bitmap and 512 value slots for chunks of at most 8192 columns
+// (those hold fewer than 512 elements, so many work groups fit a CU), and
+// 512 threads with up to 2^18 columns for the wide light chunks.
 constexpr int RANK_BLOCK = 512;
 constexpr int RANK_EPT = 16;  // RANK_BLOCK * RANK_EPT >= tau_limit()
+constexpr int RANK_SBLOCK = 256, RANK_SWORDS = 256, RANK_SCAP = 512, RANK_SEPT = 2;
+static_assert(RANK_SBLOCK * RANK_SEPT >= DENSE_MAX / 16, "narrow light chunks hold fewer than width/16 elements");
+static_assert(RANK_SWORDS * 32 == DENSE_MAX, "narrow bitmap covers the dense width");
 
 template <int BLOCK, int EPT>
 GM_DEV void rank_load(const LeafSet &L, int64_t s, int64_t e, int32_t (&c)[EPT], double (&v)[EPT], bool vals) {
@@ -554,17 +564,17 @@ GM_DEV void rank_load(const LeafSet &L, int64_t s, int64_t e, int32_t (&c)[EPT],
     }
 }
 
-// Marks the chunk's columns in the bitmap and, one bit per bitmap word, in a
-// summary bitmap of the non-empty words; returns through *count the number
-// of distinct columns (a column is new when atomicOr finds its bit clear).
+// Marks the chunk's columns in the bitmap; returns, one bit per element
+// slot, the elements that found their column's bit clear (each column's
+// first element), and through *count the number of distinct columns.
 template <int BLOCK, int EPT>
-GM_DEV void rank_mark(uint32_t *bits, uint32_t *summ, int nwords, const int32_t (&c)[EPT], int32_t *count) {
-    const int nsumm = (nwords + 31) >> 5;
+GM_DEV uint32_t rank_mark(uint32_t *bits, int nwords, const int32_t (&c)[EPT], int32_t *count) {
+    static_assert(EPT <= 32, "one fresh bit per element slot");
     for (int w = threadIdx.x; w < nwords; w += BLOCK) bits[w] = 0;
-    for (int w = threadIdx.x; w < nsumm; w += BLOCK) summ[w] = 0;
     if (threadIdx.x == 0) *count = 0;
     __syncthreads();
-    int fresh = 0;
+    uint32_t fresh = 0;
+    int n_fresh = 0;
 #pragma unroll
     for (int q = 0; q < EPT; ++q)
         if (c[q] >= 0) {
@@ -573,94 +583,77 @@ GM_DEV void rank_mark(uint32_t *bits, uint32_t *summ, int nwords, const int32_t 
             if (!(((volatile uint32_t *)bits)[w] & bit)) {
                 const uint32_t old = atomicOr(&bits[w], bit);
                 if (!(old & bit)) {
-                    ++fresh;
-                    if (old == 0) atomicOr(&summ[w >> 5], 1u << (w & 31));
+                    fresh |= 1u << q;
+                    ++n_fresh;
                 }
             }
         }
-    fresh = wave_reduce_sum(fresh);
-    if ((threadIdx.x & (GM_WAVE - 1)) == 0 && fresh) atomicAdd(count, fresh);
+    n_fresh = wave_reduce_sum(n_fresh);
+    if ((threadIdx.x & (GM_WAVE - 1)) == 0 && n_fresh) atomicAdd(count, n_fresh);
     __syncthreads();
+    return fresh;
 }
 
-template <int BLOCK, int NWORDS>
+template <int BLOCK, int NWORDS, int EPT>
 __global__ __launch_bounds__(BLOCK) void k_leaf_rank_sym(LeafSet L, const LeafTask *tasks, int width,
                                                          int64_t *leaf_nnz, int64_t *slot_cnt) {
     __shared__ uint32_t bits[NWORDS];
-    __shared__ uint32_t summ[NWORDS / 32];
     __shared__ int32_t count;
     const LeafTask tk = tasks[blockIdx.x];
-    int32_t c[RANK_EPT];
-    double v[RANK_EPT];
-    rank_load<BLOCK, RANK_EPT>(L, tk.s, tk.e, c, v, false);
-    rank_mark<BLOCK, RANK_EPT>(bits, summ, width >> 5, c, &count);
+    int32_t c[EPT];
+    double v[EPT];
+    rank_load<BLOCK, EPT>(L, tk.s, tk.e, c, v, false);
+    rank_mark<BLOCK, EPT>(bits, width >> 5, c, &count);
     if (threadIdx.x == 0) {
         leaf_nnz[tk.a] = count;
         slot_cnt[tk.t] = count;
     }
 }
 
-template <int BLOCK, int NWORDS, int CAP>
+template <int BLOCK, int NWORDS, int CAP, int EPT>
 __global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const LeafTask *tasks, int width, LeafOut o) {
-    static_assert(NWORDS / 32 <= BLOCK, "one summary word per thread");
+    constexpr int WPT = (NWORDS + BLOCK - 1) / BLOCK;  // bitmap words per thread in the rank scan
     __shared__ uint32_t bits[NWORDS];
-    __shared__ uint32_t summ[NWORDS / 32];
-    __shared__ uint16_t wpre[NWORDS];  // rank of each non-empty word's first bit (ranks < CAP <= 65535)
-    __shared__ uint16_t wlist[CAP];    // the non-empty words, in column order
+    __shared__ uint16_t wpre[NWORDS];  // rank of each word's first set bit (ranks < CAP <= 65535)
     __shared__ double vals[CAP];
     __shared__ int32_t scan_sm[BLOCK / GM_WAVE];
     __shared__ int32_t count;
     const LeafTask tk = tasks[blockIdx.x];
-    const int nwords = width >> 5;
-    const int nsumm = (nwords + 31) >> 5;
-    int32_t c[RANK_EPT];
-    double v[RANK_EPT];
-    rank_load<BLOCK, RANK_EPT>(L, tk.s, tk.e, c, v, true);
-    rank_mark<BLOCK, RANK_EPT>(bits, summ, nwords, c, &count);
-    const int32_t total = count;
     const int64_t dst = tk.t, nnz = tk.a;
     const int32_t base = tk.b;
+    const int nwords = width >> 5;
+    int32_t c[EPT];
+    double v[EPT];
+    rank_load<BLOCK, EPT>(L, tk.s, tk.e, c, v, true);
+    const uint32_t fresh = rank_mark<BLOCK, EPT>(bits, nwords, c, &count);
+    const int32_t total = count;
     const int n = total < CAP ? total : CAP;
     const int m = n < nnz ? n : (int)nnz;
     if (threadIdx.x == 0 && (total != nnz || total > CAP)) atomicOr(o.err, 4);
-    // list the non-empty words in order: summary word t belongs to thread t
+    // word ranks: thread t owns words [t*WPT, t*WPT + WPT)
     {
-        const uint32_t sw = (int)threadIdx.x < nsumm ? summ[threadIdx.x] : 0u;
-        int32_t n_words;
-        int32_t pos = block_excl_scan<BLOCK>((int32_t)__popc(sw), scan_sm, &n_words);
-        uint32_t b = sw;
-        while (b) {
-            if (pos < CAP) wlist[pos] = (uint16_t)((threadIdx.x << 5) | (__ffs(b) - 1));
-            ++pos;
-            b &= b - 1;
-        }
-        __syncthreads();
-        // ranks of the listed words; the columns go straight to C in rank order
-        const int nw = n_words < CAP ? n_words : CAP;
-        const int per = (nw + BLOCK - 1) / BLOCK;
-        const int q0 = threadIdx.x * per;
+        const int w0 = threadIdx.x * WPT;
         int32_t sum = 0;
-        for (int q = q0; q < q0 + per && q < nw; ++q) sum += __popc(bits[wlist[q]]);
+#pragma unroll
+        for (int j = 0; j < WPT; ++j)
+            if (w0 + j < nwords) sum += __popc(bits[w0 + j]);
         int32_t r = block_excl_scan<BLOCK>(sum, scan_sm);
-        for (int q = q0; q < q0 + per && q < nw; ++q) {
-            const int w = wlist[q];
-            wpre[w] = (uint16_t)(r < 65535 ? r : 65535);
-            uint32_t bb = bits[w];
-            while (bb) {
-                if (r < m) o.c_col[dst + r] = base + ((w << 5) | (__ffs(bb) - 1));
-                ++r;
-                bb &= bb - 1;
+#pragma unroll
+        for (int j = 0; j < WPT; ++j)
+            if (w0 + j < nwords) {
+                wpre[w0 + j] = (uint16_t)(r < 65535 ? r : 65535);
+                r += __popc(bits[w0 + j]);
             }
-        }
     }
     for (int q = threadIdx.x; q < n; q += BLOCK) vals[q] = 0.0;
     __syncthreads();
 #pragma unroll
-    for (int q = 0; q < RANK_EPT; ++q)
+    for (int q = 0; q < EPT; ++q)
         if (c[q] >= 0) {
             const int w = c[q] >> 5;
             const int rk = wpre[w] + __popc(bits[w] & ((1u << (c[q] & 31)) - 1u));
             if (rk < n) __hip_atomic_fetch_add(&vals[rk], v[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            if (((fresh >> q) & 1u) && rk < m) o.c_col[dst + rk] = base + c[q];
         }
     __syncthreads();
     for (int q = threadIdx.x; q < m; q += BLOCK) o.c_val[dst + q] = vals[q];
@@ -794,11 +787,20 @@ void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *items, int64_t n, 
         launch_items(k_leaf_dense_sym<512>, 512, n, s, L, items, width, leaf_nnz, slot_cnt);
         break;
     case LEAF_RANK:
-    case LEAF_RANK_L:
+    case LEAF_RANK_L: {
         GM_REQUIRE(n <= 0 || width <= (1 << RANK_MAX_LOG2), GMAGNUS_ERROR_UNSUPPORTED, "rank bitmap too wide");
-        launch_items(k_leaf_rank_sym<RANK_BLOCK, (1 << RANK_MAX_LOG2) / 32>, RANK_BLOCK, n, s, L, items, width,
-                     leaf_nnz, slot_cnt);
+        constexpr int W17 = (1 << 17) / 32, W18 = (1 << 18) / 32;
+        if (width <= DENSE_MAX)
+            launch_items(k_leaf_rank_sym<RANK_SBLOCK, RANK_SWORDS, RANK_SEPT>, RANK_SBLOCK, n, s, L, items, width,
+                         leaf_nnz, slot_cnt);
+        else if (width <= (1 << 17))
+            launch_items(k_leaf_rank_sym<RANK_BLOCK, W17, RANK_EPT>, RANK_BLOCK, n, s, L, items, width, leaf_nnz,
+                         slot_cnt);
+        else
+            launch_items(k_leaf_rank_sym<RANK_BLOCK, W18, RANK_EPT>, RANK_BLOCK, n, s, L, items, width, leaf_nnz,
+                         slot_cnt);
         break;
+    }
     default: break;
     }
 }
@@ -820,14 +822,19 @@ void leaf_numeric(const LeafSet &L, int bin, const LeafTask *items, int64_t n, i
         GM_REQUIRE(n <= 0 || width <= (1 << RANK_MAX_LOG2), GMAGNUS_ERROR_UNSUPPORTED, "rank bitmap too wide");
         constexpr int W17 = (1 << 17) / 32, W18 = (1 << 18) / 32;
         const bool narrow = width <= (1 << 17);
-        if (bin == LEAF_RANK && narrow)
-            launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_SMALL>, RANK_BLOCK, n, s, L, items, width, o);
+        if (width <= DENSE_MAX)  // fewer than width/16 elements (the dense class takes the rest)
+            launch_items(k_leaf_rank_num<RANK_SBLOCK, RANK_SWORDS, RANK_SCAP, RANK_SEPT>, RANK_SBLOCK, n, s, L, items,
+                         width, o);
+        else if (bin == LEAF_RANK && narrow)
+            launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_SMALL, RANK_EPT>, RANK_BLOCK, n, s, L, items, width, o);
         else if (bin == LEAF_RANK)
-            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_SMALL>, RANK_BLOCK, n, s, L, items, width, o);
+            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_SMALL, RANK_EPT>, RANK_BLOCK, n, s, L, items, width, o);
         else if (narrow)
-            launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_NNZ_MAX>, RANK_BLOCK, n, s, L, items, width, o);
+            launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_NNZ_MAX, RANK_EPT>, RANK_BLOCK, n, s, L, items, width,
+                         o);
         else
-            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_NNZ_MAX>, RANK_BLOCK, n, s, L, items, width, o);
+            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_NNZ_MAX, RANK_EPT>, RANK_BLOCK, n, s, L, items, width,
+                         o);
         break;
     }
     default: break;
@@ -843,6 +850,6 @@ void slot_scan(int64_t *slot, int64_t n_heavy, int64_t n_slots, const int64_t *h
     GM_CHECK_LAUNCH();
 }
 
-int64_t tau_limit() { return HN_CAP[3]; }
+int64_t tau_limit() { return HN_CAP[3] < RANK_NNZ_MAX ? HN_CAP[3] : RANK_NNZ_MAX; }
 
 }  // namespace gm

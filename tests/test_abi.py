@@ -83,7 +83,7 @@ def test_library_planner_matches_oracle_planner(lib):
             assert (a.dense_width, a.chunks_required, a.chunks_max) == (b.dense_width, b.chunks_required,
                                                                         b.chunks_max), (cm, s_lm)
             assert a.levels == b.v_chunks, (cm, s_lm)
-            assert a.tau == min(b.tau, 7168)
+            assert a.tau == min(b.tau, 6912)  # the library clamps tau to its light accumulators' capacity
 
 
 def test_planner_mi355x_defaults(lib):
