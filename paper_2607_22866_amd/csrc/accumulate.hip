@@ -252,6 +252,12 @@ GM_DEV int hash_bin_sym(int64_t n) {
 GM_DEV int hash_bin_num(int64_t nnz) {
     return nnz <= HN_CAP[0] ? 0 : nnz <= HN_CAP[1] ? 1 : nnz <= HN_CAP[2] ? 2 : 3;
 }
+// Numeric light rows: the two small bins hash (by distinct columns); the two
+// large ones sort all products (by product count, SORT_CAP).
+constexpr int SORT_CAP[2] = {2048, 6912};
+GM_DEV int light_bin_num(int64_t nnz, int64_t ip) {
+    return nnz <= HN_CAP[0] ? 0 : nnz <= HN_CAP[1] ? 1 : ip <= SORT_CAP[0] ? 2 : 3;
+}
 
 // Window choice for a light row: span = max column - min column + 1.
 GM_DEV int window_bin(int64_t ip, int64_t span, bool window) {
@@ -277,7 +283,7 @@ __global__ void k_light_classes(const int64_t *ip, const int64_t *row_nnz, const
             if (wb >= 0)
                 c = (uint8_t)(LIGHT_W0 + wb);
             else
-                c = (uint8_t)(LIGHT_H0 + (row_nnz ? hash_bin_num(row_nnz[r]) : hash_bin_sym(p)));
+                c = (uint8_t)(LIGHT_H0 + (row_nnz ? light_bin_num(row_nnz[r], p) : hash_bin_sym(p)));
         }
         cls[r] = c;
     }
@@ -341,6 +347,205 @@ __global__ __launch_bounds__(BLOCK) void k_light_hash_num(Csr A, Csr B, int64_t 
                                [&](int32_t c, double v) { hash_insert_add<TS>(keys, vals, c, v); });
     const int64_t dst = c_row_ptr[r];
     hash_emit_sorted<BLOCK, TS>(keys, vals, c_row_ptr[r + 1] - dst, 0, c_col + dst, c_val + dst, G.scan, err);
+}
+
+// ------------------------------------------------ sort-based light rows
+// Light rows with many distinct columns (their products barely repeat a
+// column): every product is placed in LDS as (column - row minimum, value),
+// the columns are sorted with a stable LSD radix sort carrying the product
+// index, and runs of equal columns are summed into the row. This replaces a
+// hash table plus a bitonic sort of the whole table, whose many
+// barrier-separated stages dominated these rows.
+
+// Stable LSD radix sort of n <= CAP keys in LDS, 8-bit digits over the low
+// `bits` bits, with a 16-bit payload. Wave w ranks the contiguous range
+// [w*S, w*S + S) in 64-element batches: lanes with equal digits are found
+// with eight ballots, and per-(digit, wave) counters scanned digit-major give
+// every element its place, so equal digits keep their order. On return
+// (keys, idx) point at the sorted arrays (the two buffers are swapped).
+template <int BLOCK, int CAP>
+GM_DEV void radix_sort_lds(uint32_t *&keys, uint16_t *&idx, uint32_t *&keys_alt, uint16_t *&idx_alt, int n,
+                           int bits, int32_t *hist, int32_t *scan_sm) {
+    constexpr int NW = BLOCK / GM_WAVE;
+    constexpr int NB = (CAP + BLOCK - 1) / BLOCK;  // 64-element batches per wave
+    constexpr int S = NB * GM_WAVE;
+    constexpr int NH = NW * 256;
+    constexpr int HPT = NH / BLOCK;
+    static_assert(HPT * BLOCK == NH, "counters per thread");
+    const int tid = threadIdx.x, lane = tid & (GM_WAVE - 1), w = tid / GM_WAVE;
+    const uint64_t lt = lanemask_lt();
+    for (int shift = 0; shift < bits; shift += 8) {
+        for (int i = tid; i < NH; i += BLOCK) hist[i] = 0;
+        __syncthreads();
+        int rk[NB];
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const int i = w * S + b * GM_WAVE + lane;
+            const bool valid = i < n;
+            const uint32_t d = valid ? (keys[i] >> shift) & 255u : 0u;
+            uint64_t peers = ballot(valid);
+#pragma unroll
+            for (int bit = 0; bit < 8; ++bit) {
+                const uint64_t m = ballot((d >> bit) & 1u);
+                peers &= ((d >> bit) & 1u) ? m : ~m;
+            }
+            const int leader = peers ? __ffsll((long long)peers) - 1 : lane;
+            int base = 0;
+            if (valid && lane == leader) {
+                base = hist[d * NW + w];
+                hist[d * NW + w] = base + __popcll(peers);
+            }
+            base = __shfl(base, leader, GM_WAVE);
+            rk[b] = base + __popcll(peers & lt);
+        }
+        __syncthreads();
+        // exclusive scan of the counters in (digit, wave) order
+        {
+            int32_t v[HPT], sum = 0;
+#pragma unroll
+            for (int j = 0; j < HPT; ++j) {
+                v[j] = hist[tid * HPT + j];
+                sum += v[j];
+            }
+            int32_t run = block_excl_scan<BLOCK>(sum, scan_sm);
+#pragma unroll
+            for (int j = 0; j < HPT; ++j) {
+                hist[tid * HPT + j] = run;
+                run += v[j];
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const int i = w * S + b * GM_WAVE + lane;
+            if (i < n) {
+                const uint32_t k = keys[i];
+                const int pos = hist[((k >> shift) & 255u) * NW + w] + rk[b];
+                keys_alt[pos] = k;
+                idx_alt[pos] = idx[i];
+            }
+        }
+        __syncthreads();
+        uint32_t *tk = keys;
+        keys = keys_alt;
+        keys_alt = tk;
+        uint16_t *ti = idx;
+        idx = idx_alt;
+        idx_alt = ti;
+    }
+}
+
+template <int BLOCK, int CAP>
+struct SortLds {
+    uint32_t keys[2][CAP];
+    double vals[CAP];
+    uint16_t idx[2][CAP];
+    int32_t hist[(BLOCK / GM_WAVE) * 256];
+    int32_t off[BLOCK + 1];
+    int64_t bst[BLOCK];
+    double av[BLOCK];
+    int32_t scan[BLOCK / GM_WAVE];
+};
+
+constexpr int SORT_ILP = 4;
+
+template <int BLOCK, int CAP>
+__global__ __launch_bounds__(BLOCK) void k_light_sort_num(Csr A, Csr B, int64_t r0, const int64_t *items,
+                                                          const int32_t *minc, const int32_t *maxc,
+                                                          const int64_t *c_row_ptr, int32_t *c_col, double *c_val,
+                                                          int32_t *err) {
+    static_assert(CAP < 65536, "16-bit product indices");
+    __shared__ SortLds<BLOCK, CAP> L;
+    const int tid = threadIdx.x;
+    const int64_t r = items[blockIdx.x];
+    const int32_t base_col = minc[r];
+    const uint32_t span = (uint32_t)(maxc[r] - base_col);
+    const int64_t j0 = A.rp[r0 + r], j1 = A.rp[r0 + r + 1];
+    const int64_t dst = c_row_ptr[r], nnz = c_row_ptr[r + 1] - dst;
+    // gather every product of the row: A entries in batches of BLOCK
+    int n = 0;
+    for (int64_t jb = j0; jb < j1; jb += BLOCK) {
+        const int nb = (int)(j1 - jb < BLOCK ? j1 - jb : BLOCK);
+        int32_t len = 0;
+        if (tid < nb) {
+            const int32_t k = A.ci[jb + tid];
+            const int64_t bs = B.rp[k];
+            len = (int32_t)(B.rp[k + 1] - bs);
+            L.bst[tid] = bs;
+            L.av[tid] = A.v[jb + tid];
+        }
+        int32_t tot;
+        const int32_t ex = block_excl_scan<BLOCK>(len, L.scan, &tot);
+        if (tid < nb) L.off[tid] = ex;
+        __syncthreads();
+        if (n + tot > CAP) {  // cannot happen for a light row of this bin (ip <= CAP)
+            if (tid == 0) atomicOr(err, 8);
+            return;
+        }
+        int q_prev = 0;
+        for (int tb = tid; tb < tot; tb += BLOCK * SORT_ILP) {
+            int32_t c[SORT_ILP];
+            double v[SORT_ILP];
+#pragma unroll
+            for (int u = 0; u < SORT_ILP; ++u) {
+                const int t = tb + u * BLOCK;
+                if (t < tot) {
+                    const int q = (int)find_row(L.off, q_prev, nb, t);
+                    q_prev = q;
+                    const int64_t src = L.bst[q] + (t - L.off[q]);
+                    c[u] = B.ci[src];
+                    v[u] = L.av[q] * B.v[src];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < SORT_ILP; ++u) {
+                const int t = tb + u * BLOCK;
+                if (t < tot) {
+                    L.keys[0][n + t] = (uint32_t)(c[u] - base_col);
+                    L.vals[n + t] = v[u];
+                    L.idx[0][n + t] = (uint16_t)(n + t);
+                }
+            }
+        }
+        n += tot;
+        __syncthreads();
+    }
+    const int bits = span == 0 ? 0 : 32 - __clz((int)span);
+    uint32_t *keys = L.keys[0], *keys_alt = L.keys[1];
+    uint16_t *idx = L.idx[0], *idx_alt = L.idx[1];
+    radix_sort_lds<BLOCK, CAP>(keys, idx, keys_alt, idx_alt, n, bits, L.hist, L.scan);
+    // runs of equal columns: heads counted per thread over a contiguous
+    // range, their output positions kept in the free index buffer, then the
+    // heads are written with consecutive lanes on consecutive positions
+    constexpr int PT = (CAP + BLOCK - 1) / BLOCK;
+    const int p0 = tid * PT;
+    int32_t cnt = 0;
+#pragma unroll
+    for (int j = 0; j < PT; ++j) {
+        const int p = p0 + j;
+        if (p < n && (p == 0 || keys[p] != keys[p - 1])) ++cnt;
+    }
+    int32_t total;
+    int32_t pos = block_excl_scan<BLOCK>(cnt, L.scan, &total);
+#pragma unroll
+    for (int j = 0; j < PT; ++j) {
+        const int p = p0 + j;
+        if (p < n && (p == 0 || keys[p] != keys[p - 1])) idx_alt[p] = (uint16_t)pos++;
+    }
+    __syncthreads();
+    if (tid == 0 && total != nnz) atomicOr(err, 1);
+    for (int p = tid; p < n; p += BLOCK) {
+        const uint32_t k = keys[p];
+        if (p == 0 || k != keys[p - 1]) {
+            const int o = idx_alt[p];
+            double sum = L.vals[idx[p]];
+            for (int q = p + 1; q < n && keys[q] == k; ++q) sum += L.vals[idx[q]];
+            if (o < nnz) {
+                c_col[dst + o] = (int32_t)k + base_col;
+                c_val[dst + o] = sum;
+            }
+        }
+    }
 }
 
 template <int BLOCK, int WMAX>
@@ -750,10 +955,12 @@ void light_numeric(const Csr &A, const Csr &B, int64_t r0, int bin, const int64_
         launch_items(k_light_hash_num<64, 1024>, 64, n, s, A, B, r0, items, c_row_ptr, c_col, c_val, err);
         break;
     case LIGHT_H2:
-        launch_items(k_light_hash_num<256, 4096>, 256, n, s, A, B, r0, items, c_row_ptr, c_col, c_val, err);
+        launch_items(k_light_sort_num<256, SORT_CAP[0]>, 256, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col,
+                     c_val, err);
         break;
     case LIGHT_H3:
-        launch_items(k_light_hash_num<512, 8192>, 512, n, s, A, B, r0, items, c_row_ptr, c_col, c_val, err);
+        launch_items(k_light_sort_num<512, SORT_CAP[1]>, 512, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col,
+                     c_val, err);
         break;
     default: break;
     }
@@ -850,6 +1057,9 @@ void slot_scan(int64_t *slot, int64_t n_heavy, int64_t n_slots, const int64_t *h
     GM_CHECK_LAUNCH();
 }
 
-int64_t tau_limit() { return HN_CAP[3] < RANK_NNZ_MAX ? HN_CAP[3] : RANK_NNZ_MAX; }
+int64_t tau_limit() {
+    int64_t t = HN_CAP[3] < RANK_NNZ_MAX ? HN_CAP[3] : RANK_NNZ_MAX;
+    return t < SORT_CAP[1] ? t : SORT_CAP[1];
+}
 
 }  // namespace gm
