@@ -240,6 +240,39 @@ GM_DEV void dense_emit(DenseLds<BLOCK, WMAX> &L, int width, int64_t nnz, int32_t
     }
 }
 
+// dense_emit that also leaves the accumulator zeroed (values of the present
+// columns and this wave's bitmap words), so the next chunk needs no clear.
+template <int BLOCK, int WMAX>
+GM_DEV void dense_emit_clear(DenseLds<BLOCK, WMAX> &L, int width, int64_t nnz, int32_t col_base, int32_t *out_col,
+                             double *out_val, int32_t *err) {
+    constexpr int NW = BLOCK / GM_WAVE;
+    const int lane = threadIdx.x & (GM_WAVE - 1), w = threadIdx.x / GM_WAVE;
+    const int span = ((width + NW - 1) / NW + GM_WAVE - 1) / GM_WAVE * GM_WAVE;  // multiple of 64 columns
+    const int c0 = w * span, c1 = c0 + span < width ? c0 + span : width;
+    int32_t cnt = 0;
+    for (int c = c0 + lane; c < c1; c += GM_WAVE) cnt += (L.bits[c >> 5] >> (c & 31)) & 1;
+    cnt = wave_reduce_sum(cnt);
+    int32_t total;
+    int32_t base = block_excl_scan<BLOCK>(lane == 0 ? cnt : 0, L.scan, &total);
+    base = __shfl(base, 0, GM_WAVE);
+    if (threadIdx.x == 0 && total != nnz) atomicOr(err, 2);
+    for (int g = c0; g < c1; g += GM_WAVE) {
+        const int c = g + lane;
+        const bool p = c < c1 && ((L.bits[c >> 5] >> (c & 31)) & 1);
+        const uint64_t m = ballot(p);
+        const int pos = base + __popcll(m & lanemask_lt());
+        if (p) {
+            if (pos < nnz) {
+                out_col[pos] = c + col_base;
+                out_val[pos] = L.vals[c];
+            }
+            L.vals[c] = 0.0;
+        }
+        base += __popcll(m);
+    }
+    for (int wd = (c0 >> 5) + lane; wd < ((c1 + 31) >> 5); wd += GM_WAVE) L.bits[wd] = 0;
+}
+
 // ----------------------------------------------------------- bin tables
 // Hash bins: (max elements or nnz, table slots, block).
 constexpr int HS_CAP[4] = {128, 512, 2048, 8192};   // symbolic: elements (load <= 1/2)
@@ -308,7 +341,7 @@ __global__ void k_leaf_classes(LeafSet L, const int64_t *leaf_nnz, int64_t tau, 
         if (len == 0)
             c = LEAF_EMPTY;
         else if (width <= DENSE_MAX && (len > tau || len >= width / 16))
-            c = LEAF_DENSE;
+            c = len >= DENSE_BIG_LEN ? LEAF_DENSE_BIG : LEAF_DENSE;
         else if (width <= (1 << RANK_MAX_LOG2) && width >= 32 && len >= RANK_MIN_LEN)
             c = (leaf_nnz && leaf_nnz[i] > RANK_SMALL) ? LEAF_RANK_L : LEAF_RANK;
         else
@@ -693,50 +726,69 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_dense_sym(LeafSet L, const LeafT
     }
 }
 
-// Numeric dense accumulation with 1024 threads (16 waves) per work group:
-// the next batch's loads are issued before the current batch's LDS updates
-// (and the first batch's before the LDS clear), so with only two work groups
-// per CU (64 KB of values each) a work group's loads overlap its LDS work.
-constexpr int DENSE_BLOCK = 1024, DENSE_EPT = 4;
+// Numeric dense accumulation, 1024 threads (16 waves) per work group, two
+// work groups per CU (64 KB of values each). The work groups are persistent:
+// each takes chunks from an atomic counter, in the bin order (the big dense
+// chunks first). While a chunk is written out, the next chunk's record and
+// first batch of elements are already being loaded, and the write-out leaves
+// the accumulator zeroed, so the loads of one chunk overlap the LDS work of
+// the previous one. Within a chunk the next batch's loads are issued before
+// the current batch's LDS atomics.
+constexpr int DENSE_BLOCK = 1024, DENSE_EPT = 2, DENSE_GROUPS_PER_CU = 2;
 
 template <int BLOCK, int EPT>
-__global__ __launch_bounds__(BLOCK) void k_leaf_dense_num(LeafSet L, const LeafTask *tasks, int width, LeafOut o) {
-    __shared__ DenseLds<BLOCK, DENSE_MAX> D;
-    const LeafTask tk = tasks[blockIdx.x];
-    const int64_t s = tk.s, e = tk.e;
-    constexpr int STEP = BLOCK * EPT;
-    int32_t c[EPT];
-    double v[EPT];
+GM_DEV void dense_load(const LeafSet &L, int64_t b, int64_t e, int32_t (&c)[EPT], double (&v)[EPT]) {
 #pragma unroll
     for (int q = 0; q < EPT; ++q) {
-        const int64_t t = s + q * BLOCK + threadIdx.x;
+        const int64_t t = b + q * BLOCK + threadIdx.x;
         c[q] = t < e ? __builtin_nontemporal_load(&L.col[t]) : -1;
         v[q] = t < e ? __builtin_nontemporal_load(&L.val[t]) : 0.0;
     }
+}
+
+// (at most 64 VGPRs: two 16-wave work groups per CU need 8 waves per SIMD)
+template <int BLOCK, int EPT>
+__global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(8))) void k_leaf_dense_num(
+    LeafSet L, const LeafTask *tasks, int64_t n_tasks, int width, LeafOut o, int32_t *counter) {
+    __shared__ DenseLds<BLOCK, DENSE_MAX> D;
+    __shared__ int32_t grabbed;
+    constexpr int STEP = BLOCK * EPT;
+    if (threadIdx.x == 0) grabbed = atomicAdd(counter, 1);
     dense_clear(D, width, true);
     __syncthreads();
-    for (int64_t b = s; b < e; b += STEP) {
-        int32_t cn[EPT];
-        double vn[EPT];
+    int64_t cur = grabbed;
+    if (cur >= n_tasks) return;  // uniform across the work group
+    LeafTask tk = tasks[cur];
+    int32_t c[EPT];
+    double v[EPT];
+    dense_load<BLOCK, EPT>(L, tk.s, tk.e, c, v);
+    while (true) {
+        __syncthreads();  // the accumulator is clear and everyone has read `grabbed`
+        if (threadIdx.x == 0) grabbed = atomicAdd(counter, 1);
+        for (int64_t b = tk.s; b < tk.e; b += STEP) {
+            int32_t cn[EPT];
+            double vn[EPT];
+            dense_load<BLOCK, EPT>(L, b + STEP, tk.e, cn, vn);
 #pragma unroll
-        for (int q = 0; q < EPT; ++q) {
-            const int64_t t = b + STEP + q * BLOCK + threadIdx.x;
-            cn[q] = t < e ? __builtin_nontemporal_load(&L.col[t]) : -1;
-            vn[q] = t < e ? __builtin_nontemporal_load(&L.val[t]) : 0.0;
+            for (int q = 0; q < EPT; ++q)
+                if (c[q] >= 0) dense_add(D, c[q], v[q]);
+#pragma unroll
+            for (int q = 0; q < EPT; ++q) {
+                c[q] = cn[q];
+                v[q] = vn[q];
+            }
         }
-#pragma unroll
-        for (int q = 0; q < EPT; ++q)
-            if (c[q] >= 0) dense_add(D, c[q], v[q]);
-#pragma unroll
-        for (int q = 0; q < EPT; ++q) {
-            c[q] = cn[q];
-            v[q] = vn[q];
+        __syncthreads();
+        const int64_t nxt = grabbed;
+        LeafTask tn{};
+        if (nxt < n_tasks) {
+            tn = tasks[nxt];
+            dense_load<BLOCK, EPT>(L, tn.s, tn.e, c, v);  // in flight during the write-out
         }
+        dense_emit_clear(D, width, tk.a, tk.b, o.c_col + tk.t, o.c_val + tk.t, o.err);
+        if (nxt >= n_tasks) break;
+        tk = tn;
     }
-    __syncthreads();
-    const int64_t dst = tk.t, nnz = tk.a;
-    const int32_t base = tk.b;
-    dense_emit(D, width, nnz, base, o.c_col + dst, o.c_val + dst, o.err);
 }
 
 // Bitmap-rank accumulator for light chunks whose column range is too wide
@@ -1013,7 +1065,7 @@ void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *items, int64_t n, 
 }
 
 void leaf_numeric(const LeafSet &L, int bin, const LeafTask *items, int64_t n, int width, int32_t *c_col,
-                  double *c_val, int32_t *err, hipStream_t s) {
+                  double *c_val, int32_t *err, int32_t *counter, hipStream_t s) {
     LeafOut o{0, nullptr, nullptr, nullptr, 0, c_col, c_val, err};
     switch (bin) {
     case LEAF_H0: launch_items(k_leaf_hash_num<64, 256>, 64, n, s, L, items, o); break;
@@ -1022,7 +1074,19 @@ void leaf_numeric(const LeafSet &L, int bin, const LeafTask *items, int64_t n, i
     case LEAF_H3: launch_items(k_leaf_hash_num<512, 8192>, 512, n, s, L, items, o); break;
     case LEAF_DENSE:
         GM_REQUIRE(n <= 0 || width <= DENSE_MAX, GMAGNUS_ERROR_UNSUPPORTED, "dense accumulator wider than LDS allows");
-        launch_items(k_leaf_dense_num<DENSE_BLOCK, DENSE_EPT>, DENSE_BLOCK, n, s, L, items, width, o);
+        if (n > 0) {
+            static int n_cu = 0;
+            if (n_cu == 0) {
+                int dev = 0;
+                GM_HIP(hipGetDevice(&dev));
+                GM_HIP(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev));
+            }
+            fill<int32_t>(counter, 0, 1, s);
+            const int64_t groups = std::min<int64_t>(n, (int64_t)n_cu * DENSE_GROUPS_PER_CU);
+            hipLaunchKernelGGL((k_leaf_dense_num<DENSE_BLOCK, DENSE_EPT>), dim3((unsigned)groups), dim3(DENSE_BLOCK),
+                               0, s, L, items, n, width, o, counter);
+            GM_CHECK_LAUNCH();
+        }
         break;
     case LEAF_RANK:
     case LEAF_RANK_L: {

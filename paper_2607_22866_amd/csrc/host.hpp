@@ -196,7 +196,7 @@ struct LeafSet {
     int64_t lo, hi;
 };
 enum LeafBin : uint8_t {
-    LEAF_EMPTY = 0, LEAF_H0, LEAF_H1, LEAF_H2, LEAF_H3, LEAF_DENSE, LEAF_RANK, LEAF_RANK_L, LEAF_NBINS
+    LEAF_EMPTY = 0, LEAF_H0, LEAF_H1, LEAF_H2, LEAF_H3, LEAF_DENSE_BIG, LEAF_DENSE, LEAF_RANK, LEAF_RANK_L, LEAF_NBINS
 };
 enum LightBin : uint8_t {
     LIGHT_EMPTY = 0, LIGHT_HEAVY, LIGHT_W0, LIGHT_W1, LIGHT_H0, LIGHT_H1, LIGHT_H2, LIGHT_H3, LIGHT_NBINS
@@ -221,12 +221,17 @@ void leaf_tasks_sym(const LeafSet &L, const int64_t *items, int64_t n, LeafTask 
 void leaf_tasks_num(const LeafSet &L, const int64_t *items, int64_t n, const int64_t *leaf_nnz, int n_slots_log2,
                     const int64_t *heavy_rows, const int64_t *c_row_ptr, const int64_t *slot_off,
                     int slot_width_log2, LeafTask *tasks, hipStream_t s);
+// LEAF_DENSE_BIG holds the dense leaves of at least DENSE_BIG_LEN elements; it
+// sits just before LEAF_DENSE so one launch covers both bins with the big
+// leaves first (they start early instead of finishing last).
+constexpr int64_t DENSE_BIG_LEN = 32768;
 // Leaf symbolic: leaf_nnz[leaf] and slot_cnt[slot] for the n tasks of a bin.
 void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *tasks, int64_t n, int width, int64_t *leaf_nnz,
                    int64_t *slot_cnt, hipStream_t s);
 // Leaf numeric: writes C at each task's position.
+// counter: one device int32 the dense bin uses to hand out chunks.
 void leaf_numeric(const LeafSet &L, int bin, const LeafTask *tasks, int64_t n, int width, int32_t *c_col,
-                  double *c_val, int32_t *err, hipStream_t s);
+                  double *c_val, int32_t *err, int32_t *counter, hipStream_t s);
 // Light rows (local index r): symbolic count into row_nnz[r]; numeric into C.
 void light_symbolic(const Csr &A, const Csr &B, int64_t r0, int bin, const int64_t *items, int64_t n,
                     const int32_t *minc, const int32_t *maxc, int64_t *row_nnz, hipStream_t s);

@@ -744,8 +744,10 @@ void heavy_symbolic(gmagnus_plan_s *p) {
             leaf_tasks_sym(lv.set, lv.items_sym, nl, tasks, s);
             Timed t(p, GMAGNUS_K_CHUNK_SYM, s);
             for (int b = LEAF_H0; b < LEAF_NBINS; ++b) {
-                const int64_t cnt = lv.bins_sym[b + 1] - lv.bins_sym[b];
-                leaf_symbolic(lv.set, b, tasks + lv.bins_sym[b], cnt, lv.width, lv.leaf_nnz, p->slot, s);
+                if (b == LEAF_DENSE_BIG) continue;  // launched together with LEAF_DENSE, first
+                const int64_t b0 = b == LEAF_DENSE ? lv.bins_sym[LEAF_DENSE_BIG] : lv.bins_sym[b];
+                const int64_t cnt = lv.bins_sym[b + 1] - b0;
+                leaf_symbolic(lv.set, b, tasks + b0, cnt, lv.width, lv.leaf_nnz, p->slot, s);
                 if (cnt) p->info.kernel_launches[GMAGNUS_K_CHUNK_SYM] += 1;
                 if (b == LEAF_DENSE) p->info.n_leaves_dense += cnt;
                 else if (b == LEAF_RANK || b == LEAF_RANK_L) p->info.n_leaves_rank += cnt;
@@ -883,14 +885,18 @@ void do_numeric(gmagnus_plan_s *p, const int64_t *c_row_ptr, int32_t *c_col, dou
             const int64_t nl = lv.set.hi - lv.set.lo;
             if (nl <= 0) continue;
             LeafTask *tasks = p->ws->alloc<LeafTask>(nl);
+            int32_t *counter = p->ws->alloc<int32_t>(1);
             leaf_tasks_num(lv.set, lv.items_num, nl, lv.leaf_nnz, p->n_slots_log2, p->heavy_rows, c_row_ptr, p->slot,
                            p->slot_width_log2, tasks, s);
             for (int b = LEAF_H0; b < LEAF_NBINS; ++b) {
-                const int64_t cnt = lv.bins_num[b + 1] - lv.bins_num[b];
-                leaf_numeric(lv.set, b, tasks + lv.bins_num[b], cnt, lv.width, c_col, c_val, p->err, s);
+                if (b == LEAF_DENSE_BIG) continue;  // launched together with LEAF_DENSE, first
+                const int64_t b0 = b == LEAF_DENSE ? lv.bins_num[LEAF_DENSE_BIG] : lv.bins_num[b];
+                const int64_t cnt = lv.bins_num[b + 1] - b0;
+                leaf_numeric(lv.set, b, tasks + b0, cnt, lv.width, c_col, c_val, p->err, counter, s);
                 if (cnt) p->info.kernel_launches[GMAGNUS_K_CHUNK_NUM] += 1;
             }
             p->ws->free(tasks);
+            p->ws->free(counter);
             add_bytes(p, GMAGNUS_K_CHUNK_NUM, 12.0 * lv.elems);
         }
     }
