@@ -88,6 +88,8 @@ typedef struct {
                                            implies GMAGNUS_FLAG_PAPER_EXPANSION */
 #define GMAGNUS_FLAG_PAPER_EXPANSION 16u /* write C-hat row by row, then split it at the first level (the
                                             paper's order), instead of splitting during the expansion */
+#define GMAGNUS_FLAG_SLICE_SPLIT 32u /* split during the expansion in the paper's slice order (runs written at
+                                        atomic cursors) instead of the chunk-major row order */
 
 #define GMAGNUS_MAX_LEVELS 8
 

@@ -31,7 +31,8 @@ FLAGS = [
     "-I", os.path.join(ROOT, "include"),
 ]
 
-SOURCES = ["prims.hip", "setup.hip", "expand.hip", "multisplit.hip", "accumulate.hip", "plan.hip"]
+SOURCES = ["prims.hip", "setup.hip", "expand.hip", "rowsplit.hip", "multisplit.hip", "accumulate.hip",
+           "plan.hip"]
 
 
 def _compile(src: str) -> str:

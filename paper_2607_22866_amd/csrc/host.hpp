@@ -134,9 +134,10 @@ void slice_lengths(const Csr &B, const int32_t *slice_k, int64_t n, int64_t *len
 // row (n_slices * (nc + 1) offsets), then per heavy row the sum of its A~
 // entries' chunk sizes (counts: n_heavy * nc).
 void slice_chunk_bounds(const Csr &B, const SliceArrays &sl, int nc, int shift, int32_t *bnd, hipStream_t s);
+// (cmajor: counts[c * n_heavy + h] instead of counts[h * nc + c])
 void struct_hist(const Csr &A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0, const int64_t *a_heavy_ptr,
-                 int64_t nnz_heavy_all, const int32_t *k_to_slice, const int32_t *bnd, int nc, int64_t *counts,
-                 hipStream_t s);
+                 int64_t nnz_heavy_all, const int32_t *k_to_slice, const int32_t *bnd, int nc, bool cmajor,
+                 int64_t *counts, hipStream_t s);
 void gather_row_len(const int64_t *row_ptr, const int64_t *rows, int64_t n, int64_t r0, int64_t *out, hipStream_t s);
 void gather_i64(const int64_t *src, const int64_t *idx, int64_t n, int64_t *out, hipStream_t s);
 
@@ -154,6 +155,35 @@ void expand(const Csr &B, const SliceArrays &sl, int64_t total, const int64_t *i
 // written chunk-local.
 void expand_split(const Csr &B, const SliceArrays &sl, int64_t total, const int64_t *info_words, const int32_t *bnd,
                   int nc, int shift, int64_t *cursor, int32_t *out_col, double *out_val, hipStream_t s);
+
+// ------------------------------------------------------------- rowsplit.hip
+// The heavy rows' A entries in row order: B row, its slice (-1 for an empty
+// B row), heavy row, value.
+struct RowEntries {
+    int32_t *k = nullptr;
+    int32_t *s = nullptr;
+    int32_t *h = nullptr;
+    double *a = nullptr;
+};
+void heavy_entries(const Csr &A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0, const int64_t *a_heavy_ptr,
+                   int64_t nnz_heavy_all, const int32_t *k_to_slice, const RowEntries &ent, hipStream_t s);
+// pre[e * nc + c]: offset of entry e's chunk-c part inside region (c, row of e)
+// (segmented scan; scratch: agg and carry n_waves * nc, wfirst/wlast n_waves).
+int64_t entry_offset_waves(int64_t n_ent);
+void entry_offsets(const RowEntries &ent, int64_t n_ent, const int32_t *bnd, int nc, int64_t *agg, int32_t *wfirst,
+                   int32_t *wlast, int64_t *carry, uint32_t *pre, hipStream_t s);
+// Region r of the chunk-major level-0 output (perm: position -> c * n_heavy + h).
+void region_records(const int64_t *perm, int64_t n_out, int64_t n_heavy, const int64_t *a_heavy_ptr, int32_t *reg_c,
+                    int64_t *reg_efirst, int64_t *reg_ne, hipStream_t s);
+int64_t rows_tile_words(int64_t total);
+bool rows_next_fits(int next_nc);
+// Chunk-major row-order expansion with the level-0 split: writes the level-0
+// output (chunk-local columns) and, when next_counts is given, the next
+// level's counts of the heavy regions.
+void expand_rows(const Csr &B, const RowEntries &ent, const uint32_t *pre, const int32_t *bnd, const int64_t *out_ptr,
+                 const int64_t *seg_base, const int32_t *reg_c, const int64_t *reg_efirst, const int64_t *reg_ne,
+                 int64_t n_out, int64_t n_heavy_out, int64_t total, int nc, int shift, int next_nc, int next_shift,
+                 int64_t *next_counts, int64_t *tile_words, int32_t *out_col, double *out_val, hipStream_t s);
 
 // ------------------------------------------------------------ multisplit.hip
 struct LevelGeom {
@@ -179,9 +209,10 @@ int64_t histogram_tiles(const LevelGeom &g, int64_t tau);
 void histogram(const LevelGeom &g, int64_t tau, const int64_t *in_ptr, const int32_t *in_col, int64_t *tile_row,
                int64_t *counts, hipStream_t s);
 void chunk_classes(const int64_t *counts, int64_t n, int64_t tau, bool last, uint8_t *cls, hipStream_t s);
-// out_cnt[inv[i]] = counts[i]; origin_out[inv[i]] = origin_in[i / n_chunks] + (i % n_chunks) * stride.
+// out_cnt[inv[i]] = counts[i]; origin_out[inv[i]] = origin_in[h] + c * stride with (h, c) =
+// (i / n_chunks, i % n_chunks), or (i % cmajor_rows, i / cmajor_rows) when cmajor_rows > 0.
 void chunk_reorder(const int64_t *counts, const int64_t *inv, int64_t n, int n_chunks, const int64_t *origin_in,
-                   int64_t stride, int64_t *out_cnt, int64_t *origin_out, hipStream_t s);
+                   int64_t stride, int64_t cmajor_rows, int64_t *out_cnt, int64_t *origin_out, hipStream_t s);
 void multisplit(const LevelGeom &g, const int64_t *in_ptr, const int64_t *tile_row, const int32_t *in_col,
                 const double *in_val, const int64_t *x_map, int64_t *cursor, int32_t *out_col, double *out_val,
                 int64_t n_heavy_out, int64_t *next_counts, hipStream_t s);

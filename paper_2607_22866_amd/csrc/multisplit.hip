@@ -294,11 +294,14 @@ __global__ void k_chunk_classes(const int64_t *counts, int64_t n, int64_t tau, i
 }
 
 __global__ void k_chunk_reorder(const int64_t *counts, const int64_t *inv, int64_t n, int n_chunks,
-                                const int64_t *origin_in, int64_t stride, int64_t *out_cnt, int64_t *origin_out) {
+                                const int64_t *origin_in, int64_t stride, int64_t cmajor_rows, int64_t *out_cnt,
+                                int64_t *origin_out) {
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
         const int64_t o = inv[i];
+        const int64_t h = cmajor_rows ? i % cmajor_rows : i / n_chunks;
+        const int64_t c = cmajor_rows ? i / cmajor_rows : i % n_chunks;
         out_cnt[o] = counts[i];
-        origin_out[o] = origin_in[i / n_chunks] + (i % n_chunks) * stride;
+        origin_out[o] = origin_in[h] + c * stride;
     }
 }
 
@@ -379,10 +382,10 @@ void chunk_classes(const int64_t *counts, int64_t n, int64_t tau, bool last, uin
 }
 
 void chunk_reorder(const int64_t *counts, const int64_t *inv, int64_t n, int n_chunks, const int64_t *origin_in,
-                   int64_t stride, int64_t *out_cnt, int64_t *origin_out, hipStream_t s) {
+                   int64_t stride, int64_t cmajor_rows, int64_t *out_cnt, int64_t *origin_out, hipStream_t s) {
     if (n <= 0) return;
     hipLaunchKernelGGL(k_chunk_reorder, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, counts, inv, n, n_chunks,
-                       origin_in, stride, out_cnt, origin_out);
+                       origin_in, stride, cmajor_rows, out_cnt, origin_out);
     GM_CHECK_LAUNCH();
 }
 

@@ -462,8 +462,14 @@ void heavy_symbolic(gmagnus_plan_s *p) {
     const bool paper_hist = (p->opts.flags & GMAGNUS_FLAG_PAPER_HISTOGRAM) != 0;
     // split at the first level while expanding, unless the paper's order is asked for
     const bool fused = P.n_levels > 0 && !paper_hist && (p->opts.flags & GMAGNUS_FLAG_PAPER_EXPANSION) == 0;
+    // the fused split in chunk-major row order (32-bit offsets inside a row's chunk), else in slice order
+    const bool rows_order = fused && (p->opts.flags & GMAGNUS_FLAG_SLICE_SPLIT) == 0 &&
+                            H < ((int64_t)1 << 32) && nh < ((int64_t)1 << 31);
     int64_t *counts0 = nullptr;  // level-0 counts when computed from the structure
     int32_t *sbnd = nullptr;     // per-slice level-0 chunk boundaries (kept for the fused expansion)
+    RowEntries ent;              // chunk-major row order: entries, their chunk offsets, the row pointers of A~
+    uint32_t *pre = nullptr;
+    int64_t *a_heavy_keep = nullptr;
 
     // ---- masked CSR -> CSC of the heavy rows and slice offsets
     SliceArrays sl;
@@ -512,12 +518,21 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         sl.nnz = tot[0];
         blen_total = tot[2];
         GM_REQUIRE(tot[1] == H, GMAGNUS_ERROR_HIP, "slice products disagree with the row products");
-        int64_t *cursor = ws.alloc<int64_t>(std::max<int64_t>(sl.n_slices, 1));
-        fill<int64_t>(cursor, 0, sl.n_slices, s);
-        sl.row_h = ws.alloc<int32_t>(sl.nnz);
-        sl.a_val = ws.alloc<double>(sl.nnz);
-        csc_fill(p->A, p->B, p->heavy_rows, nh, p->r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, sl.col_ptr, cursor,
-                 sl.row_h, sl.a_val, s);
+        int64_t *cursor = nullptr;
+        if (!rows_order) {
+            cursor = ws.alloc<int64_t>(std::max<int64_t>(sl.n_slices, 1));
+            fill<int64_t>(cursor, 0, sl.n_slices, s);
+            sl.row_h = ws.alloc<int32_t>(sl.nnz);
+            sl.a_val = ws.alloc<double>(sl.nnz);
+            csc_fill(p->A, p->B, p->heavy_rows, nh, p->r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, sl.col_ptr,
+                     cursor, sl.row_h, sl.a_val, s);
+        } else {
+            ent.k = ws.alloc<int32_t>(nnz_heavy_all);
+            ent.s = ws.alloc<int32_t>(nnz_heavy_all);
+            ent.h = ws.alloc<int32_t>(nnz_heavy_all);
+            ent.a = ws.alloc<double>(nnz_heavy_all);
+            heavy_entries(p->A, p->heavy_rows, nh, p->r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, ent, s);
+        }
         if (P.n_levels > 0 && !paper_hist) {
             // level-0 (row, chunk) counts from the structure of A~ and B
             Timed t2(p, GMAGNUS_K_HISTOGRAM, s);
@@ -526,8 +541,21 @@ void heavy_symbolic(gmagnus_plan_s *p) {
             sbnd = ws.alloc<int32_t>(sl.n_slices * (nc0 + 1));
             counts0 = ws.alloc<int64_t>(nh * nc0);
             slice_chunk_bounds(p->B, sl, nc0, shift0, sbnd, s);
-            struct_hist(p->A, p->heavy_rows, nh, p->r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, sbnd, nc0, counts0,
-                        s);
+            struct_hist(p->A, p->heavy_rows, nh, p->r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, sbnd, nc0, rows_order,
+                        counts0, s);
+            if (rows_order) {
+                // every entry's offset inside its (chunk, row) region
+                const int64_t nw = entry_offset_waves(nnz_heavy_all);
+                int64_t *agg = ws.alloc<int64_t>(nw * nc0), *carry = ws.alloc<int64_t>(nw * nc0);
+                int32_t *wfirst = ws.alloc<int32_t>(nw), *wlast = ws.alloc<int32_t>(nw);
+                pre = ws.alloc<uint32_t>(nnz_heavy_all * nc0);
+                entry_offsets(ent, nnz_heavy_all, sbnd, nc0, agg, wfirst, wlast, carry, pre, s);
+                ws.free(agg);
+                ws.free(carry);
+                ws.free(wfirst);
+                ws.free(wlast);
+                add_bytes(p, GMAGNUS_K_HISTOGRAM, 8.0 * nnz_heavy_all + 4.0 * nnz_heavy_all * nc0);
+            }
             if (!fused) {
                 ws.free(sbnd);
                 sbnd = nullptr;
@@ -545,7 +573,10 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         ws.free(k_to_slice);
         ws.free(sc2);
         ws.free(row_len);
-        ws.free(a_heavy_ptr);
+        if (rows_order)
+            a_heavy_keep = a_heavy_ptr;  // region records need the row pointers of A~
+        else
+            ws.free(a_heavy_ptr);
         ws.free(scratch);
         add_bytes(p, GMAGNUS_K_CSC, 12.0 * nnz_heavy_all + 12.0 * sl.nnz + 8.0 * (p->A.n_cols + sl.n_slices));
     }
@@ -556,8 +587,9 @@ void heavy_symbolic(gmagnus_plan_s *p) {
     // already split into the first level's chunks when fused)
     int32_t *col_buf[2] = {ws.alloc<int32_t>(H), nullptr};
     double *val_buf[2] = {ws.alloc<double>(H), nullptr};
-    int64_t *exp_tiles = ws.alloc<int64_t>(std::max<int64_t>(expand_tile_words(H), 1));
-    {
+    int64_t *exp_tiles =
+        ws.alloc<int64_t>(std::max<int64_t>(rows_order ? rows_tile_words(H) : expand_tile_words(H), 1));
+    if (!rows_order) {
         Timed t(p, GMAGNUS_K_CSC, s);
         expand_tiles(p->B, sl, H, exp_tiles, s);
     }
@@ -568,6 +600,12 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         ws.free(sl.slice_k);
         ws.free(sl.row_h);
         ws.free(sl.a_val);
+        ws.free(ent.k);
+        ws.free(ent.s);
+        ws.free(ent.h);
+        ws.free(ent.a);
+        ws.free(pre);
+        ws.free(a_heavy_keep);
         if (sbnd) ws.free(sbnd);
         sbnd = nullptr;
     };
@@ -648,7 +686,8 @@ void heavy_symbolic(gmagnus_plan_s *p) {
             Timed t(p, GMAGNUS_K_SETUP, s);
             chunk_classes(counts, n_out, P.tau, last, ccls, s);
             partition_u8(ccls, n_out, 2, perm2, x_map, cb, sc, s);
-            chunk_reorder(counts, x_map, n_out, nc, origin_in, slots_per_chunk, out_cnt, origin_out, s);
+            chunk_reorder(counts, x_map, n_out, nc, origin_in, slots_per_chunk, (rows_order && lvl == 0) ? nh : 0,
+                          out_cnt, origin_out, s);
             scan_i64(out_cnt, n_out, out_ptr, sc, s);
             read_bins(cb, 2, cbh, s);
         }
@@ -656,9 +695,10 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         p->info.level_heavy_out[lvl] = nh_out;
         const bool split_in_expand = fused && lvl == 0;
         int64_t *next_counts = nullptr;
-        if (!last && nh_out > 0 && !split_in_expand &&
-            multisplit_next_fits(g.group_rows * nc, g.next_chunks)) {
-            // the multisplit takes the next level's histogram on the way
+        const bool next_fused = split_in_expand ? rows_order && rows_next_fits(g.next_chunks)
+                                                : multisplit_next_fits(g.group_rows * nc, g.next_chunks);
+        if (!last && nh_out > 0 && next_fused) {
+            // the multisplit (or the chunk-major expansion) takes the next level's histogram on the way
             next_counts = ws.alloc<int64_t>(nh_out * g.next_chunks);
             fill<int64_t>(next_counts, 0, nh_out * g.next_chunks, s);
         }
@@ -667,7 +707,31 @@ void heavy_symbolic(gmagnus_plan_s *p) {
             col_buf[nxt] = ws.alloc<int32_t>(H);
             val_buf[nxt] = ws.alloc<double>(H);
         }
-        if (split_in_expand) {
+        if (split_in_expand && rows_order) {
+            // chunk-major regions: chunk, first entry and entry count of each, segment bases
+            int32_t *reg_c = ws.alloc<int32_t>(n_out);
+            int64_t *reg_efirst = ws.alloc<int64_t>(n_out), *reg_ne = ws.alloc<int64_t>(n_out);
+            int64_t *seg_base = ws.alloc<int64_t>(n_out + 1);
+            {
+                Timed t(p, GMAGNUS_K_SETUP, s);
+                region_records(perm2, n_out, nh, a_heavy_keep, reg_c, reg_efirst, reg_ne, s);
+                scan_i64(reg_ne, n_out, seg_base, sc, s);
+            }
+            {
+                Timed t(p, GMAGNUS_K_EXPAND, s);
+                expand_rows(p->B, ent, pre, sbnd, out_ptr, seg_base, reg_c, reg_efirst, reg_ne, n_out, nh_out, H, nc,
+                            g.shift, last ? 0 : g.next_chunks, g.next_shift, next_counts, exp_tiles, col_buf[nxt],
+                            val_buf[nxt], s);
+            }
+            ws.free(reg_c);
+            ws.free(reg_efirst);
+            ws.free(reg_ne);
+            ws.free(seg_base);
+            p->info.kernel_launches[GMAGNUS_K_EXPAND] += 1;
+            add_bytes(p, GMAGNUS_K_EXPAND,
+                      12.0 * H + 20.0 * nnz_heavy_all + 4.0 * nnz_heavy_all * nc + 12.0 * blen_total + 24.0 * n_out);
+            free_slices();
+        } else if (split_in_expand) {
             // cursor of output row (h, c), indexed h * nc + c
             int64_t *cursor = ws.alloc<int64_t>(n_out);
             gather_i64(out_ptr, x_map, n_out, cursor, s);

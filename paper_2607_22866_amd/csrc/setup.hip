@@ -178,7 +178,7 @@ constexpr int SH_ENTRIES = 256;
 __global__ __launch_bounds__(256) void k_struct_hist(Csr A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
                                                      const int64_t *a_heavy_ptr, int64_t total,
                                                      const int32_t *k_to_slice, const int32_t *bnd, int nc,
-                                                     int64_t *counts) {
+                                                     int64_t cmajor_rows, int64_t *counts) {
     const int lane = threadIdx.x & (GM_WAVE - 1);
     const int64_t wid = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / GM_WAVE;
     const int64_t e0 = wid * SH_ENTRIES;
@@ -205,8 +205,10 @@ __global__ __launch_bounds__(256) void k_struct_hist(Csr A, const int64_t *heavy
             const int64_t hq = __shfl(h, q, GM_WAVE);
             const int32_t sq = __shfl(s, q, GM_WAVE);
             if (hq != cur) {
-                if (lane < nc && acc)
-                    atomicAdd((unsigned long long *)&counts[cur * nc + lane], (unsigned long long)acc);
+                if (lane < nc && acc) {
+                    const int64_t ix = cmajor_rows ? lane * cmajor_rows + cur : cur * nc + lane;
+                    atomicAdd((unsigned long long *)&counts[ix], (unsigned long long)acc);
+                }
                 acc = 0;
                 cur = hq;
             }
@@ -220,7 +222,10 @@ __global__ __launch_bounds__(256) void k_struct_hist(Csr A, const int64_t *heavy
         h_end = a_heavy_ptr[h + 1];
         a_base = A.rp[r0 + heavy_rows[h]] - a_heavy_ptr[h];
     }
-    if (lane < nc && acc) atomicAdd((unsigned long long *)&counts[cur * nc + lane], (unsigned long long)acc);
+    if (lane < nc && acc) {
+        const int64_t ix = cmajor_rows ? lane * cmajor_rows + cur : cur * nc + lane;
+        atomicAdd((unsigned long long *)&counts[ix], (unsigned long long)acc);
+    }
 }
 
 __global__ void k_gather_row_len(const int64_t *row_ptr, const int64_t *rows, int64_t n, int64_t r0, int64_t *out) {
@@ -312,13 +317,14 @@ void slice_chunk_bounds(const Csr &B, const SliceArrays &sl, int nc, int shift, 
 }
 
 void struct_hist(const Csr &A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0, const int64_t *a_heavy_ptr,
-                 int64_t nnz_heavy_all, const int32_t *k_to_slice, const int32_t *bnd, int nc, int64_t *counts,
-                 hipStream_t s) {
+                 int64_t nnz_heavy_all, const int32_t *k_to_slice, const int32_t *bnd, int nc, bool cmajor,
+                 int64_t *counts, hipStream_t s) {
     fill<int64_t>(counts, 0, n_heavy * nc, s);
     if (n_heavy <= 0 || nnz_heavy_all <= 0) return;
     const int64_t waves = (nnz_heavy_all + SH_ENTRIES - 1) / SH_ENTRIES;
     hipLaunchKernelGGL(k_struct_hist, dim3(grid_for(waves, 4, (int64_t)1 << 30)), dim3(256), 0, s, A, heavy_rows,
-                       n_heavy, r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, bnd, nc, counts);
+                       n_heavy, r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, bnd, nc, cmajor ? n_heavy : (int64_t)0,
+                       counts);
     GM_CHECK_LAUNCH();
 }
 

@@ -89,10 +89,20 @@ def test_rmat12_paper_expansion(g, opts, levels):
     assert info.params.levels == levels
 
 
+@pytest.mark.parametrize("opts,levels", DEPTHS[1:])
+def test_rmat12_slice_order_split(g, opts, levels):
+    # the first-level split done during a slice-order expansion (runs at
+    # atomic cursors) gives the same C as the chunk-major row-order one
+    A = RMAT12.make()
+    info = check(g, A, A, flags=g.FLAG_SLICE_SPLIT, **opts)
+    assert info.params.levels == levels
+
+
 def test_rmat12_integer_values_bit_exact(g):
     A = wl.rmat(12, 8, 0.57, 0.19, 0.19, 12, values="int3")
     for opts in ({}, dict(tau=200, dense_width_log2=6, chunks_max_log2=2),
-                 dict(tau=200, dense_width_log2=6, chunks_max_log2=2, flags=g.FLAG_PAPER_EXPANSION)):
+                 dict(tau=200, dense_width_log2=6, chunks_max_log2=2, flags=g.FLAG_PAPER_EXPANSION),
+                 dict(tau=200, dense_width_log2=6, chunks_max_log2=2, flags=g.FLAG_SLICE_SPLIT)):
         rp, col, val, _ = run(g, A, A, **opts)
         ref = oracle.spgemm(A, A)
         assert np.array_equal(rp, ref.row_ptr) and np.array_equal(col, ref.col)
