@@ -39,12 +39,15 @@ WORKLOADS = {
 HEAVY_KERNELS = ["expand", "histogram", "multisplit", "chunk_symbolic", "chunk_numeric"]
 # Timing classes that are exactly one kernel launch per panel: the roofline is
 # reported for the one of these with the largest device time.
-SINGLE_KERNEL_CLASSES = {"expand": "k_expand_split", "multisplit": "k_multisplit"}
+SINGLE_KERNEL_CLASSES = {"expand": "k_expand_rows", "multisplit": "k_multisplit"}
 # Sources a kernel's counter summary depends on (traffic is dropped when they change).
-KERNEL_SOURCES = {"k_expand_split": ["paper_2607_22866_amd/csrc/expand.hip", "paper_2607_22866_amd/csrc/common.hpp"],
+KERNEL_SOURCES = {"k_expand_rows": ["paper_2607_22866_amd/csrc/rowsplit.hip", "paper_2607_22866_amd/csrc/common.hpp"],
+                  "k_expand_split": ["paper_2607_22866_amd/csrc/expand.hip", "paper_2607_22866_amd/csrc/common.hpp"],
+                  "k_expand": ["paper_2607_22866_amd/csrc/expand.hip", "paper_2607_22866_amd/csrc/common.hpp"],
                   "k_multisplit": ["paper_2607_22866_amd/csrc/multisplit.hip",
                                    "paper_2607_22866_amd/csrc/common.hpp"]}
-TRAFFIC_FILES = {"k_expand_split": "profiles/expand_split_rmat22_traffic.md",
+TRAFFIC_FILES = {"k_expand_rows": "profiles/expand_rows_rmat22_traffic.md",
+                 "k_expand_split": "profiles/expand_split_rmat22_traffic.md",
                  "k_multisplit": "profiles/multisplit_rmat22_traffic.md"}
 
 
@@ -170,6 +173,8 @@ def main():
     ap.add_argument("--serial", action="store_true", help="run heavy and light work on one stream")
     ap.add_argument("--paper-expansion", action="store_true",
                     help="expand C-hat row by row and split it afterwards (the paper's order)")
+    ap.add_argument("--slice-split", action="store_true",
+                    help="split at the first level during a slice-order expansion (atomic cursors)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build measures the single-GPU hot path "
@@ -200,7 +205,8 @@ def main():
     log("%d row panels (max %.2g products each)" % (len(bounds) - 1, args.panel_products))
     acc_warm = {}
     c_bufs = [None, None]
-    extra = (g.FLAG_SERIAL_STREAMS if args.serial else 0) | (g.FLAG_PAPER_EXPANSION if args.paper_expansion else 0)
+    extra = ((g.FLAG_SERIAL_STREAMS if args.serial else 0) | (g.FLAG_PAPER_EXPANSION if args.paper_expansion else 0) |
+             (g.FLAG_SLICE_SPLIT if args.slice_split else 0))
     for w in range(args.warmup):
         t = time.perf_counter()
         run_step(g, dA, bounds, False, acc_warm, c_bufs, extra)
@@ -237,6 +243,8 @@ def main():
         kname = SINGLE_KERNEL_CLASSES[dom]
         if dom == "expand" and args.paper_expansion:
             kname = "k_expand"
+        elif dom == "expand" and args.slice_split:
+            kname = "k_expand_split"
         bpl = d["gb_per_step"] * 1e9 / d["launches_per_step"]
         ms = d["ms_per_step"] / d["launches_per_step"]
         achieved = bpl / (ms / 1000.0) / 1e9
