@@ -39,14 +39,16 @@ WORKLOADS = {
 HEAVY_KERNELS = ["expand", "histogram", "multisplit", "chunk_symbolic", "chunk_numeric"]
 # Timing classes that are exactly one kernel launch per panel: the roofline is
 # reported for the one of these with the largest device time.
-SINGLE_KERNEL_CLASSES = {"expand": "k_expand_rows", "multisplit": "k_multisplit"}
+SINGLE_KERNEL_CLASSES = {"expand": "k_expand_rows2", "multisplit": "k_multisplit"}
 # Sources a kernel's counter summary depends on (traffic is dropped when they change).
-KERNEL_SOURCES = {"k_expand_rows": ["paper_2607_22866_amd/csrc/rowsplit.hip", "paper_2607_22866_amd/csrc/common.hpp"],
+KERNEL_SOURCES = {"k_expand_rows2": ["paper_2607_22866_amd/csrc/rowsplit.hip", "paper_2607_22866_amd/csrc/common.hpp"],
+                  "k_expand_rows": ["paper_2607_22866_amd/csrc/rowsplit.hip", "paper_2607_22866_amd/csrc/common.hpp"],
                   "k_expand_split": ["paper_2607_22866_amd/csrc/expand.hip", "paper_2607_22866_amd/csrc/common.hpp"],
                   "k_expand": ["paper_2607_22866_amd/csrc/expand.hip", "paper_2607_22866_amd/csrc/common.hpp"],
                   "k_multisplit": ["paper_2607_22866_amd/csrc/multisplit.hip",
                                    "paper_2607_22866_amd/csrc/common.hpp"]}
-TRAFFIC_FILES = {"k_expand_rows": "profiles/expand_rows_rmat22_traffic.md",
+TRAFFIC_FILES = {"k_expand_rows2": "profiles/expand_rows2_rmat22_traffic.md",
+                 "k_expand_rows": "profiles/expand_rows_rmat22_traffic.md",
                  "k_expand_split": "profiles/expand_split_rmat22_traffic.md",
                  "k_multisplit": "profiles/multisplit_rmat22_traffic.md"}
 
@@ -175,6 +177,8 @@ def main():
                     help="expand C-hat row by row and split it afterwards (the paper's order)")
     ap.add_argument("--slice-split", action="store_true",
                     help="split at the first level during a slice-order expansion (atomic cursors)")
+    ap.add_argument("--level-by-level", action="store_true",
+                    help="with two levels, write the first level out and split it in a pass of its own")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build measures the single-GPU hot path "
@@ -206,7 +210,7 @@ def main():
     acc_warm = {}
     c_bufs = [None, None]
     extra = ((g.FLAG_SERIAL_STREAMS if args.serial else 0) | (g.FLAG_PAPER_EXPANSION if args.paper_expansion else 0) |
-             (g.FLAG_SLICE_SPLIT if args.slice_split else 0))
+             (g.FLAG_SLICE_SPLIT if args.slice_split else 0) | (g.FLAG_LEVEL_BY_LEVEL if args.level_by_level else 0))
     for w in range(args.warmup):
         t = time.perf_counter()
         run_step(g, dA, bounds, False, acc_warm, c_bufs, extra)
@@ -245,6 +249,8 @@ def main():
             kname = "k_expand"
         elif dom == "expand" and args.slice_split:
             kname = "k_expand_split"
+        elif dom == "expand" and args.level_by_level:
+            kname = "k_expand_rows"
         bpl = d["gb_per_step"] * 1e9 / d["launches_per_step"]
         ms = d["ms_per_step"] / d["launches_per_step"]
         achieved = bpl / (ms / 1000.0) / 1e9

@@ -90,6 +90,9 @@ typedef struct {
                                             paper's order), instead of splitting during the expansion */
 #define GMAGNUS_FLAG_SLICE_SPLIT 32u /* split during the expansion in the paper's slice order (runs written at
                                         atomic cursors) instead of the chunk-major row order */
+#define GMAGNUS_FLAG_LEVEL_BY_LEVEL 64u /* with two multisplit levels, write the first level's heavy chunks out
+                                           and split them in a pass of their own, instead of splitting them again
+                                           inside the expansion and writing the final chunks directly */
 
 #define GMAGNUS_MAX_LEVELS 8
 

@@ -185,6 +185,32 @@ void expand_rows(const Csr &B, const RowEntries &ent, const uint32_t *pre, const
                  int64_t n_out, int64_t n_heavy_out, int64_t total, int nc, int shift, int next_nc, int next_shift,
                  int64_t *next_counts, int64_t *tile_words, int32_t *out_col, double *out_val, hipStream_t s);
 
+// Two levels in one pass (the hierarchy has exactly two levels): the
+// expansion splits the products of the first level's heavy regions by the
+// second level's chunk and writes them straight into the final chunks.
+// fine_bounds: per slice, offsets of the first column >= f << fshift in its
+// B row for the nf + 1 fine boundaries (fine_bounds_words entries);
+// fine_counts: F[h * nf + f], products of heavy row h in fine chunk f;
+// level1_counts: counts of the second level's rows r * nc1 + c1 for the
+// first level's heavy regions (perm: region -> c * n_heavy + h).
+int64_t fine_bounds_words(int64_t n_slices, int nf);
+void fine_bounds(const Csr &B, const int32_t *slice_k, int64_t n_slices, int nf, int fshift, int32_t *bndf,
+                 hipStream_t s);
+void fine_counts(const RowEntries &ent, int64_t n_ent, const int32_t *bndf, int nf, int64_t n_heavy, int64_t *F,
+                 hipStream_t s);
+void level1_counts(const int64_t *perm, int64_t n_regions, int64_t n_heavy, const int64_t *F, int nf, int nc1,
+                   int64_t *counts1, hipStream_t s);
+// whether the fused second level's keys fit the work group
+bool rows2_fits(int64_t tau, int nc1, int nf);
+// cursor1: next free place of second-level row r * nc1 + c1 (starts at its
+// row pointer); light regions are written to out_*0 at their first-level place.
+void expand_rows2(const Csr &B, const RowEntries &ent, const uint32_t *pre, const int32_t *bnd,
+                  const int64_t *out_ptr, const int64_t *seg_base, const int32_t *reg_c, const int64_t *reg_efirst,
+                  const int64_t *reg_ne, int64_t n_out, int64_t n_heavy_out, int64_t total, int nc, int shift,
+                  int nc1, int shift1, int64_t tau, int64_t *cursor1, int64_t n_out1_elems, int32_t *err,
+                  int64_t *tile_words, int32_t *out_col0, double *out_val0, int32_t *out_col1, double *out_val1,
+                  hipStream_t s);
+
 // ------------------------------------------------------------ multisplit.hip
 struct LevelGeom {
     int64_t n_in;        // input rows

@@ -43,8 +43,11 @@ void *cache_alloc(size_t bytes) {
     {
         std::lock_guard<std::mutex> lk(c.m);
         auto it = c.free_blocks.lower_bound({dev, bytes});
-        // reuse a block up to 25% (+2 MiB) larger than asked
-        if (it != c.free_blocks.end() && it->first.first == dev && it->first.second <= bytes + bytes / 4 + ((size_t)2 << 20)) {
+        // reuse a block up to 25% (+2 MiB) larger than asked, or up to twice
+        // as large for blocks of 1 GiB and more (a fresh hipMalloc of that size
+        // stalls the host far longer than the memory it would save is worth)
+        const size_t slack = bytes >= ((size_t)1 << 30) ? bytes : bytes / 4 + ((size_t)2 << 20);
+        if (it != c.free_blocks.end() && it->first.first == dev && it->first.second <= bytes + slack) {
             void *p = it->second;
             c.free_blocks.erase(it);
             return p;
@@ -465,6 +468,10 @@ void heavy_symbolic(gmagnus_plan_s *p) {
     // the fused split in chunk-major row order (32-bit offsets inside a row's chunk), else in slice order
     const bool rows_order = fused && (p->opts.flags & GMAGNUS_FLAG_SLICE_SPLIT) == 0 &&
                             H < ((int64_t)1 << 32) && nh < ((int64_t)1 << 31);
+    // a hierarchy of exactly two levels in one pass: the expansion splits its
+    // heavy regions again and writes the final chunks directly
+    const bool two_level = rows_order && P.n_levels == 2 && (p->opts.flags & GMAGNUS_FLAG_LEVEL_BY_LEVEL) == 0 &&
+                           rows2_fits(P.tau, P.v_chunks[1], P.v_chunks[0] * P.v_chunks[1]);
     int64_t *counts0 = nullptr;  // level-0 counts when computed from the structure
     int32_t *sbnd = nullptr;     // per-slice level-0 chunk boundaries (kept for the fused expansion)
     RowEntries ent;              // chunk-major row order: entries, their chunk offsets, the row pointers of A~
@@ -640,6 +647,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         p->leaves.push_back(lv);
     }
     int64_t slots_per_chunk = p->n_slots;
+    LeafLevel two_done{};  // the second level's final chunks when both levels run in one pass
     for (int lvl = 0; lvl < P.n_levels; ++lvl) {
         const int nc = P.v_chunks[lvl];
         const bool last = lvl == P.n_levels - 1;
@@ -695,7 +703,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         p->info.level_heavy_out[lvl] = nh_out;
         const bool split_in_expand = fused && lvl == 0;
         int64_t *next_counts = nullptr;
-        const bool next_fused = split_in_expand ? rows_order && rows_next_fits(g.next_chunks)
+        const bool next_fused = split_in_expand ? rows_order && !two_level && rows_next_fits(g.next_chunks)
                                                 : multisplit_next_fits(g.group_rows * nc, g.next_chunks);
         if (!last && nh_out > 0 && next_fused) {
             // the multisplit (or the chunk-major expansion) takes the next level's histogram on the way
@@ -717,19 +725,87 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                 region_records(perm2, n_out, nh, a_heavy_keep, reg_c, reg_efirst, reg_ne, s);
                 scan_i64(reg_ne, n_out, seg_base, sc, s);
             }
-            {
+            if (two_level && nh_out > 0) {
+                // second level laid out from the structure, then one pass writes both
+                const int nc1 = P.v_chunks[1];
+                const int nf = nc * nc1;
+                const int shift1 = g.shift - ilog2(nc1);
+                const int64_t n_out1 = nh_out * nc1;
+                const int64_t slots1 = slots_per_chunk / nc1;
+                int64_t *counts1 = ws.alloc<int64_t>(n_out1);
+                {
+                    Timed t(p, GMAGNUS_K_HISTOGRAM, s);
+                    int32_t *bndf = ws.alloc<int32_t>(fine_bounds_words(sl.n_slices, nf));
+                    int64_t *F = ws.alloc<int64_t>(nh * nf);
+                    fine_bounds(p->B, sl.slice_k, sl.n_slices, nf, shift1, bndf, s);
+                    fine_counts(ent, nnz_heavy_all, bndf, nf, nh, F, s);
+                    level1_counts(perm2, nh_out, nh, F, nf, nc1, counts1, s);
+                    ws.free(bndf);
+                    ws.free(F);
+                    p->info.kernel_launches[GMAGNUS_K_HISTOGRAM] += 1;
+                    // B rows of the slices; fine boundaries written and read once per
+                    // entry; per-row fine counts; the heavy regions' counts
+                    add_bytes(p, GMAGNUS_K_HISTOGRAM, 4.0 * blen_total + 4.0 * (nf + 1) * sl.n_slices +
+                                                          (8.0 + 4.0 * (nf + 1)) * nnz_heavy_all + 8.0 * nh * nf +
+                                                          16.0 * n_out1);
+                }
+                uint8_t *ccls1 = ws.alloc<uint8_t>(n_out1);
+                int64_t *sc1 = ws.alloc<int64_t>(std::max(partition_scratch_elems(n_out1, 2), scan_scratch_elems(n_out1)));
+                int64_t *perm1 = ws.alloc<int64_t>(n_out1), *x_map1 = ws.alloc<int64_t>(n_out1);
+                int64_t *cb1 = ws.alloc<int64_t>(3);
+                int64_t *out_cnt1 = ws.alloc<int64_t>(n_out1);
+                int64_t *origin_out1 = ws.alloc<int64_t>(n_out1);
+                int64_t *out_ptr1 = ws.alloc<int64_t>(n_out1 + 1);
+                int64_t *cursor1 = ws.alloc<int64_t>(n_out1);
+                int64_t elems1 = 0;
+                {
+                    Timed t(p, GMAGNUS_K_SETUP, s);
+                    chunk_classes(counts1, n_out1, P.tau, true, ccls1, s);
+                    partition_u8(ccls1, n_out1, 2, perm1, x_map1, cb1, sc1, s);
+                    chunk_reorder(counts1, x_map1, n_out1, nc1, origin_out, slots1, 0, out_cnt1, origin_out1, s);
+                    scan_i64(out_cnt1, n_out1, out_ptr1, sc1, s);
+                    gather_i64(out_ptr1, x_map1, n_out1, cursor1, s);
+                    elems1 = read_scalar(out_ptr + nh_out, s);
+                }
+                // sized like the first level's buffers, so panels reuse the same blocks
+                col_buf[1] = ws.alloc<int32_t>(H);
+                val_buf[1] = ws.alloc<double>(H);
+                {
+                    Timed t(p, GMAGNUS_K_EXPAND, s);
+                    expand_rows2(p->B, ent, pre, sbnd, out_ptr, seg_base, reg_c, reg_efirst, reg_ne, n_out, nh_out, H,
+                                 nc, g.shift, nc1, shift1, P.tau, cursor1, elems1, p->err, exp_tiles, col_buf[0],
+                                 val_buf[0], col_buf[1], val_buf[1], s);
+                }
+                p->info.kernel_launches[GMAGNUS_K_EXPAND] += 1;
+                add_bytes(p, GMAGNUS_K_EXPAND, 12.0 * H + 20.0 * nnz_heavy_all + 4.0 * nnz_heavy_all * nc +
+                                                   12.0 * blen_total + 24.0 * n_out + 8.0 * n_out1);
+                p->info.level_rows_in[1] = nh_out;
+                p->info.level_elems_in[1] = elems1;
+                p->info.level_heavy_out[1] = 0;
+                two_done.set = LeafSet{out_ptr1, col_buf[1], val_buf[1], origin_out1, 0, n_out1};
+                two_done.width = 1 << shift1;
+                two_done.elems = elems1;
+                ws.free(counts1);
+                ws.free(ccls1);
+                ws.free(sc1);
+                ws.free(perm1);
+                ws.free(x_map1);
+                ws.free(cb1);
+                ws.free(out_cnt1);
+                ws.free(cursor1);
+            } else {
                 Timed t(p, GMAGNUS_K_EXPAND, s);
                 expand_rows(p->B, ent, pre, sbnd, out_ptr, seg_base, reg_c, reg_efirst, reg_ne, n_out, nh_out, H, nc,
                             g.shift, last ? 0 : g.next_chunks, g.next_shift, next_counts, exp_tiles, col_buf[nxt],
                             val_buf[nxt], s);
+                p->info.kernel_launches[GMAGNUS_K_EXPAND] += 1;
+                add_bytes(p, GMAGNUS_K_EXPAND,
+                          12.0 * H + 20.0 * nnz_heavy_all + 4.0 * nnz_heavy_all * nc + 12.0 * blen_total + 24.0 * n_out);
             }
             ws.free(reg_c);
             ws.free(reg_efirst);
             ws.free(reg_ne);
             ws.free(seg_base);
-            p->info.kernel_launches[GMAGNUS_K_EXPAND] += 1;
-            add_bytes(p, GMAGNUS_K_EXPAND,
-                      12.0 * H + 20.0 * nnz_heavy_all + 4.0 * nnz_heavy_all * nc + 12.0 * blen_total + 24.0 * n_out);
             free_slices();
         } else if (split_in_expand) {
             // cursor of output row (h, c), indexed h * nc + c
@@ -760,6 +836,10 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         lv.set = LeafSet{out_ptr, col_buf[nxt], val_buf[nxt], origin_out, last ? 0 : nh_out, n_out};
         lv.width = 1 << g.shift;
         p->leaves.push_back(lv);
+        if (two_done.set.ptr) {
+            p->leaves.push_back(two_done);
+            p->info.levels_run = lvl + 2;
+        }
         ws.free(tile_row);
         ws.free(sc);
         ws.free(x_map);
@@ -769,7 +849,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         ws.free(ccls);
         ws.free(counts);
         counts = next_counts;
-        if (last || nh_out == 0) break;
+        if (last || nh_out == 0 || two_done.set.ptr) break;
         in_ptr = out_ptr;
         n_in = nh_out;
         elems = read_scalar(out_ptr + nh_out, s);

@@ -374,6 +374,365 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows(RsArgs a) {
     }
 }
 
+
+// ---------------------------------------------------------------------------
+// Two levels in one pass. When the hierarchy has two levels, the heavy
+// regions of the first level are not written out: each tile of the
+// chunk-major expansion splits its products of heavy regions by the second
+// level's chunk in LDS (ranks over the wave's runs of equal keys, one scan,
+// one atomic per nonempty (region, chunk) reserving the tile's range in that
+// final chunk, a permutation through LDS) and writes them straight into the
+// final chunks; products of light regions (themselves final chunks) are
+// written at their first-level place. The second level's counts, needed to
+// lay out the final chunks beforehand, come from the structure: per slice
+// the boundaries of its B row at every fine chunk (first-level chunk times
+// second-level chunk), and per heavy row the sum over its entries of their
+// fine chunk sizes.
+
+// Fine boundaries: bndf[s * (nf + 1) + f] = offset in B[k,:] of the first
+// column >= f << fshift (f = 0..nf). One wave per slice; a row of at most 64
+// elements is searched in registers (lane i holds element i), a longer one
+// by binary search in memory.
+__global__ __launch_bounds__(256) void k_fine_bounds(Csr B, const int32_t *slice_k, int64_t n_slices, int nf,
+                                                     int fshift, int32_t *bndf) {
+    const int lane = threadIdx.x & (GM_WAVE - 1);
+    const int64_t nwaves = (int64_t)gridDim.x * (blockDim.x / GM_WAVE);
+    for (int64_t s = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / GM_WAVE; s < n_slices; s += nwaves) {
+        const int32_t k = slice_k[s];
+        const int64_t b0 = B.rp[k], len = B.rp[k + 1] - b0;
+        int32_t *out = bndf + s * (nf + 1);
+        if (len <= GM_WAVE) {
+            // fine chunk of element `lane`, padded past the row's end; every lane
+            // runs every shuffle (uniform trip counts, fixed-step search)
+            const int32_t fl = lane < len ? (B.ci[b0 + lane] >> fshift) : INT32_MAX;
+            for (int fb = 0; fb <= nf; fb += GM_WAVE) {
+                const int f = fb + lane;
+                // number of lanes whose chunk is below f (chunks ascend over lanes)
+                int pos = 0;
+#pragma unroll
+                for (int step = GM_WAVE / 2; step >= 1; step >>= 1)
+                    if (__shfl(fl, pos + step - 1, GM_WAVE) < f) pos += step;
+                if (__shfl(fl, pos, GM_WAVE) < f) ++pos;
+                if (f <= nf) out[f] = pos < len ? pos : (int32_t)len;
+            }
+        } else {
+            for (int f = lane; f <= nf; f += GM_WAVE) {
+                int64_t lo = b0, hi = b0 + len;
+                const int64_t bound = (int64_t)f << fshift;
+                while (lo < hi) {
+                    const int64_t mid = lo + ((hi - lo) >> 1);
+                    if ((int64_t)B.ci[mid] < bound)
+                        lo = mid + 1;
+                    else
+                        hi = mid;
+                }
+                out[f] = (int32_t)(lo - b0);
+            }
+        }
+    }
+}
+
+// F[h * nf + f] += fine chunk f's products of heavy row h: each work group
+// takes FC_ENTRIES consecutive row-ordered entries, thread t owns the fine
+// chunks t, t + FC_BLOCK, ..., and a row's partial sums are flushed with one
+// atomic per nonzero counter when the row changes.
+constexpr int FC_BLOCK = 256, FC_ENTRIES = 256, FC_MAXF = 1024;
+
+__global__ __launch_bounds__(FC_BLOCK) void k_fine_counts(RowEntries ent, int64_t n_ent, const int32_t *bndf, int nf,
+                                                          int64_t *F) {
+    constexpr int FPT = FC_MAXF / FC_BLOCK;
+    __shared__ int32_t es[FC_ENTRIES], eh[FC_ENTRIES];
+    const int64_t e0 = blockIdx.x * (int64_t)FC_ENTRIES;
+    const int ne = (int)(n_ent - e0 < FC_ENTRIES ? n_ent - e0 : FC_ENTRIES);
+    if (threadIdx.x < ne) {
+        es[threadIdx.x] = ent.s[e0 + threadIdx.x];
+        eh[threadIdx.x] = ent.h[e0 + threadIdx.x];
+    }
+    __syncthreads();
+    int64_t acc[FPT];
+#pragma unroll
+    for (int j = 0; j < FPT; ++j) acc[j] = 0;
+    int32_t cur = eh[0];
+    for (int i = 0; i < ne; ++i) {
+        const int32_t h = eh[i], sl = es[i];
+        if (h != cur) {
+#pragma unroll
+            for (int j = 0; j < FPT; ++j) {
+                const int f = threadIdx.x + j * FC_BLOCK;
+                if (f < nf && acc[j]) atomicAdd((unsigned long long *)&F[(int64_t)cur * nf + f], (unsigned long long)acc[j]);
+                acc[j] = 0;
+            }
+            cur = h;
+        }
+        if (sl < 0) continue;
+        const int32_t *bq = bndf + (int64_t)sl * (nf + 1);
+#pragma unroll
+        for (int j = 0; j < FPT; ++j) {
+            const int f = threadIdx.x + j * FC_BLOCK;
+            if (f < nf) acc[j] += bq[f + 1] - bq[f];
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < FPT; ++j) {
+        const int f = threadIdx.x + j * FC_BLOCK;
+        if (f < nf && acc[j]) atomicAdd((unsigned long long *)&F[(int64_t)cur * nf + f], (unsigned long long)acc[j]);
+    }
+}
+
+// counts1[r * nc1 + c1] = F[h * nf + c * nc1 + c1] for the heavy regions r of
+// the first level (perm: region -> c * n_heavy + h).
+__global__ void k_level1_counts(const int64_t *perm, int64_t n_regions, int64_t n_heavy, const int64_t *F, int nf,
+                                int nc1, int64_t *counts1) {
+    const int64_t n = n_regions * nc1;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t r = i / nc1, c1 = i - r * nc1;
+        const int64_t x = perm[r];
+        const int64_t c = x / n_heavy, h = x - c * n_heavy;
+        counts1[i] = F[h * nf + c * nc1 + c1];
+    }
+}
+
+constexpr int RS2_SUB = 2048;                 // products split per sub-batch
+constexpr int RS2_E = RS2_SUB / RS_BLOCK;     // per thread
+constexpr int RS2_KMAX = 1024;                // keys: heavy regions per tile times second-level chunks
+constexpr int RS2_NW = RS_BLOCK / GM_WAVE;
+
+struct Rs2Layout {
+    int whist, key_start, key_delta, col, val, key, total;
+};
+__host__ __device__ inline Rs2Layout rs2_layout(int K) {
+    Rs2Layout L;
+    int o = 0;
+    L.key_delta = o;  o += 8 * K;
+    L.val = o;        o += 8 * RS2_SUB;
+    L.whist = o;      o += 4 * RS2_NW * K;
+    L.key_start = o;  o += 4 * (K + 1);
+    L.col = o;        o += 4 * RS2_SUB;
+    L.key = o;        o += 2 * RS2_SUB;
+    L.total = (o + 15) & ~15;
+    return L;
+}
+
+struct Rs2Args {
+    Csr B;
+    RowEntries ent;
+    const uint32_t *pre;
+    const int32_t *bnd;
+    const int64_t *out_ptr;  // first level's region pointers
+    const int64_t *seg_base;
+    const int32_t *reg_c;
+    const int64_t *reg_efirst;
+    int64_t n_out;
+    int64_t n_heavy_out;     // regions [0, n_heavy_out) are split again
+    int64_t total;
+    int64_t n_tiles;
+    const RsTile *info;
+    int nc, shift;           // first level
+    int nc1, shift1, R;      // second level; heavy regions a tile can touch
+    int64_t *cursor1;        // next free place of second-level output row r * nc1 + c1
+    int64_t n_out1_elems;    // size of the second level's output
+    int32_t *err;            // set when a key or a place falls outside its range (a bug)
+    int32_t *out_col0;       // first level (light regions)
+    double *out_val0;
+    int32_t *out_col1;       // second level
+    double *out_val1;
+};
+
+__global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args a) {
+    __shared__ int64_t sb[RS_BLOCK + 2];
+    __shared__ int64_t rn_src[RS_BLOCK];
+    __shared__ double rn_a[RS_BLOCK];
+    __shared__ int32_t rn_reg[RS_BLOCK];   // region minus the tile's first region
+    __shared__ uint32_t start_bits[RS_WORDS];
+    __shared__ int32_t word_pre[RS_WORDS];
+    __shared__ int32_t scan_sm[RS_BLOCK / GM_WAVE];
+    __shared__ int32_t range[2];
+    __shared__ int64_t next_rb;
+    extern __shared__ __align__(16) unsigned char rs2_smem[];
+
+    const int K = a.R * a.nc1;
+    const Rs2Layout Lo = rs2_layout(K);
+    int64_t *key_delta = (int64_t *)(rs2_smem + Lo.key_delta);
+    double *val_buf = (double *)(rs2_smem + Lo.val);
+    int32_t *whist = (int32_t *)(rs2_smem + Lo.whist);
+    int32_t *key_start = (int32_t *)(rs2_smem + Lo.key_start);
+    int32_t *col_buf = (int32_t *)(rs2_smem + Lo.col);
+    uint16_t *key_buf = (uint16_t *)(rs2_smem + Lo.key);
+
+    const int tid = threadIdx.x, lane = tid & (GM_WAVE - 1), w = tid / GM_WAVE;
+    const int64_t tile = blockIdx.x;  // chunk-major order
+    const int64_t g0 = tile * RS_TILE;
+    const int64_t g1 = g0 + RS_TILE < a.total ? g0 + RS_TILE : a.total;
+    const RsTile ti = a.info[tile];
+    const int32_t mask = (int32_t)((1u << a.shift) - 1u);
+    const int32_t mask1 = (int32_t)((1u << a.shift1) - 1u);
+    const int64_t rt = ti.r0;  // keys are (region - rt) * nc1 + second-level chunk
+    const uint64_t le_mask = lanemask_lt() | (uint64_t(1) << lane);
+    int32_t *wh = whist + w * K;
+    for (int k = tid; k < RS2_NW * K; k += RS_BLOCK) whist[k] = 0;
+    int64_t rb = ti.r0;
+
+    for (int64_t b = 0; b < ti.nseg; b += RS_BLOCK) {
+        const int nb = (int)(ti.nseg - b < RS_BLOCK ? ti.nseg - b : RS_BLOCK);
+        const int64_t sfirst = ti.s0 + b;
+        for (int q = tid; q <= nb + 1; q += RS_BLOCK) sb[q] = rb + q <= a.n_out ? a.seg_base[rb + q] : INT64_MAX;
+        start_bits[tid] = 0u;
+        __syncthreads();
+        int32_t loc = -1, len = 0, reg = 0;
+        int64_t src = 0;
+        double av = 0.0;
+        if (tid < nb) {
+            const int64_t S = sfirst + tid;
+            const int64_t r = rb + find_row(sb, 0, nb + 2, S);
+            const int c = a.reg_c[r];
+            const int64_t e = a.reg_efirst[r] + (S - sb[r - rb]);
+            const bool last = S + 1 == sb[r - rb + 1];
+            const int64_t start = a.out_ptr[r];
+            const int64_t seg_g = start + a.pre[e * a.nc + c];
+            const int64_t seg_e = last ? a.out_ptr[r + 1] : start + a.pre[(e + 1) * a.nc + c];
+            const int64_t lo = seg_g > g0 ? seg_g : g0;
+            const int64_t hi = seg_e < g1 ? seg_e : g1;
+            if (hi > lo) {
+                const int32_t s = a.ent.s[e];
+                src = a.B.rp[a.ent.k[e]] + a.bnd[(int64_t)s * (a.nc + 1) + c] + (lo - seg_g);
+                av = a.ent.a[e];
+                loc = (int32_t)(lo - g0);
+                len = (int32_t)(hi - lo);
+                reg = (int32_t)(r - rt);
+            }
+            if (tid == nb - 1) next_rb = r;
+        }
+        int n_ne = 0;
+        const int slot = block_excl_scan<RS_BLOCK, int>(len > 0 ? 1 : 0, scan_sm, &n_ne);
+        if (len > 0) {
+            rn_src[slot] = src - loc;
+            rn_a[slot] = av;
+            rn_reg[slot] = reg;
+            atomicOr(&start_bits[loc >> 5], 1u << (loc & 31));
+            if (slot == 0) range[0] = loc;
+            if (slot == n_ne - 1) range[1] = loc + len;
+        }
+        __syncthreads();
+        word_pre[tid] = block_excl_scan<RS_BLOCK, int>(__popc(start_bits[tid]), scan_sm);
+        __syncthreads();
+        const int t0 = n_ne > 0 ? range[0] : 0, t1 = n_ne > 0 ? range[1] : 0;
+        // sub-batches of RS2_SUB products (uniform trip count: ballots and
+        // barriers need the whole work group)
+        for (int sbt = t0; sbt < t1; sbt += RS2_SUB) {
+            int32_t col[RS2_E];
+            double val[RS2_E];
+            int key[RS2_E];
+#pragma unroll
+            for (int u = 0; u < RS2_E; ++u) {
+                const int t = sbt + u * RS_BLOCK + tid;
+                key[u] = -1;
+                col[u] = 0;
+                val[u] = 0.0;
+                if (t < t1) {
+                    const int wd = t >> 5, bit = t & 31;
+                    const uint32_t below = bit == 31 ? ~0u : (2u << bit) - 1u;
+                    const int q = word_pre[wd] + __popc(start_bits[wd] & below) - 1;
+                    const int64_t sp = rn_src[q] + t;
+                    col[u] = a.B.ci[sp] & mask;
+                    val[u] = rn_a[q] * a.B.v[sp];
+                    const int rl = rn_reg[q];
+                    if (rt + rl < a.n_heavy_out) {
+                        key[u] = rl * a.nc1 + (col[u] >> a.shift1);
+                        if (key[u] >= K) {
+                            atomicOr(a.err, 8);
+                            key[u] = -1;
+                        }
+                    } else {
+                        key[u] = -2;  // light region: a final chunk of the first level
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < RS2_E; ++u) {
+                if (key[u] == -2) {
+                    const int64_t d = g0 + sbt + u * RS_BLOCK + tid;
+                    a.out_col0[d] = col[u];
+                    a.out_val0[d] = val[u];
+                    key[u] = -1;
+                }
+            }
+            // ranks inside (wave, key) buckets, one LDS atomic per run of equal keys
+            int rank[RS2_E];
+#pragma unroll
+            for (int u = 0; u < RS2_E; ++u) {
+                const int k = key[u];
+                const int kprev = __shfl_up(k, 1, GM_WAVE);
+                const uint64_t starts = ballot(lane == 0 || k != kprev);
+                const int first = 63 - __clzll((long long)(starts & le_mask));
+                const uint64_t above = starts & ~le_mask;
+                const int rl = (above ? __ffsll((long long)above) - 1 : GM_WAVE) - first;
+                int base = 0;
+                if (k >= 0 && lane == first) base = atomicAdd(&wh[k], rl);
+                base = __shfl(base, first, GM_WAVE);
+                rank[u] = base + (lane - first);
+            }
+            __syncthreads();
+            // exclusive scan over the buckets in (key, wave) order
+            {
+                const int M = RS2_NW * K;
+                const int per = (M + RS_BLOCK - 1) / RS_BLOCK;
+                int sum = 0;
+                for (int q = 0; q < per; ++q) {
+                    const int idx = tid * per + q;
+                    if (idx < M) sum += whist[(idx % RS2_NW) * K + idx / RS2_NW];
+                }
+                int tot = 0;
+                int run = block_excl_scan<RS_BLOCK>(sum, scan_sm, &tot);
+                for (int q = 0; q < per; ++q) {
+                    const int idx = tid * per + q;
+                    if (idx < M) {
+                        const int ad = (idx % RS2_NW) * K + idx / RS2_NW;
+                        const int v = whist[ad];
+                        whist[ad] = run;
+                        if (idx % RS2_NW == 0) key_start[idx / RS2_NW] = run;
+                        run += v;
+                    }
+                }
+                if (tid == 0) key_start[K] = tot;
+            }
+            __syncthreads();
+            // reserve each key's range in its final chunk
+            for (int k = tid; k < K; k += RS_BLOCK) {
+                const int cnt = key_start[k + 1] - key_start[k];
+                if (cnt > 0) {
+                    const int64_t row = (rt + k / a.nc1) * a.nc1 + (k % a.nc1);
+                    const int64_t d = (int64_t)atomicAdd((unsigned long long *)&a.cursor1[row], (unsigned long long)cnt);
+                    key_delta[k] = d - key_start[k];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < RS2_E; ++u) {
+                if (key[u] >= 0) {
+                    const int pos = wh[key[u]] + rank[u];
+                    col_buf[pos] = col[u] & mask1;
+                    val_buf[pos] = val[u];
+                    key_buf[pos] = (uint16_t)key[u];
+                }
+            }
+            __syncthreads();
+            const int nh = key_start[K];
+            for (int p = tid; p < nh; p += RS_BLOCK) {
+                const int64_t d = key_delta[key_buf[p]] + p;
+                if (d < 0 || d >= a.n_out1_elems) {
+                    atomicOr(a.err, 8);
+                    continue;
+                }
+                a.out_col1[d] = col_buf[p];
+                a.out_val1[d] = val_buf[p];
+            }
+            for (int k = tid; k < RS2_NW * K; k += RS_BLOCK) whist[k] = 0;
+            __syncthreads();
+        }
+        rb = next_rb;
+        __syncthreads();
+    }
+}
+
 }  // namespace
 
 void heavy_entries(const Csr &A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0, const int64_t *a_heavy_ptr,
@@ -433,6 +792,78 @@ void expand_rows(const Csr &B, const RowEntries &ent, const uint32_t *pre, const
     RsArgs a{B,       ent,  pre,   bnd,   out_ptr,   seg_base,   reg_c,       reg_efirst, n_out,  n_heavy_out,
              total,   n_tiles, info, nc,  shift,     next_nc,    next_shift,  next_counts, out_col, out_val};
     hipLaunchKernelGGL(k_expand_rows, dim3((unsigned)n_tiles), dim3(RS_BLOCK), 0, s, a);
+    GM_CHECK_LAUNCH();
+}
+
+// ------------------------------------------------------------ two levels
+int64_t fine_bounds_words(int64_t n_slices, int nf) { return n_slices * (nf + 1); }
+
+void fine_bounds(const Csr &B, const int32_t *slice_k, int64_t n_slices, int nf, int fshift, int32_t *bndf,
+                 hipStream_t s) {
+    if (n_slices <= 0) return;
+    hipLaunchKernelGGL(k_fine_bounds, dim3(grid_for(n_slices, 4, 65536)), dim3(256), 0, s, B, slice_k, n_slices, nf,
+                       fshift, bndf);
+    GM_CHECK_LAUNCH();
+}
+
+void fine_counts(const RowEntries &ent, int64_t n_ent, const int32_t *bndf, int nf, int64_t n_heavy, int64_t *F,
+                 hipStream_t s) {
+    fill<int64_t>(F, 0, n_heavy * nf, s);
+    if (n_ent <= 0) return;
+    GM_REQUIRE(nf >= 1 && nf <= FC_MAXF, GMAGNUS_ERROR_UNSUPPORTED, "fine counts: too many fine chunks");
+    const int64_t blocks = (n_ent + FC_ENTRIES - 1) / FC_ENTRIES;
+    GM_REQUIRE(blocks < (int64_t)1 << 31, GMAGNUS_ERROR_UNSUPPORTED, "fine counts: too many entries");
+    hipLaunchKernelGGL(k_fine_counts, dim3((unsigned)blocks), dim3(FC_BLOCK), 0, s, ent, n_ent, bndf, nf, F);
+    GM_CHECK_LAUNCH();
+}
+
+void level1_counts(const int64_t *perm, int64_t n_regions, int64_t n_heavy, const int64_t *F, int nf, int nc1,
+                   int64_t *counts1, hipStream_t s) {
+    if (n_regions <= 0) return;
+    hipLaunchKernelGGL(k_level1_counts, dim3(grid_for(n_regions * nc1, 256, 65536)), dim3(256), 0, s, perm, n_regions,
+                       n_heavy, F, nf, nc1, counts1);
+    GM_CHECK_LAUNCH();
+}
+
+int rows2_regions(int64_t tau) {
+    // heavy regions hold more than tau products: a tile meets at most this many
+    return (int)((RS_TILE - 1 + tau) / (tau + 1)) + 1;
+}
+
+bool rows2_fits(int64_t tau, int nc1, int nf) {
+    const int64_t K = (int64_t)rows2_regions(tau) * nc1;
+    return K <= RS2_KMAX && nf <= FC_MAXF && nc1 >= 1;
+}
+
+void expand_rows2(const Csr &B, const RowEntries &ent, const uint32_t *pre, const int32_t *bnd,
+                  const int64_t *out_ptr, const int64_t *seg_base, const int32_t *reg_c, const int64_t *reg_efirst,
+                  const int64_t *reg_ne, int64_t n_out, int64_t n_heavy_out, int64_t total, int nc, int shift,
+                  int nc1, int shift1, int64_t tau, int64_t *cursor1, int64_t n_out1_elems, int32_t *err,
+                  int64_t *tile_words, int32_t *out_col0, double *out_val0, int32_t *out_col1, double *out_val1,
+                  hipStream_t s) {
+    if (total <= 0) return;
+    GM_REQUIRE(nc >= 1 && nc < GM_WAVE && shift >= 0 && shift < 31 && shift1 >= 0 && shift1 <= shift,
+               GMAGNUS_ERROR_UNSUPPORTED, "two-level expansion: unsupported chunking");
+    const int R = rows2_regions(tau);
+    const int K = R * nc1;
+    GM_REQUIRE(K <= RS2_KMAX && K < 65536, GMAGNUS_ERROR_UNSUPPORTED, "two-level expansion: too many keys");
+    const int64_t n_tiles = (total + RS_TILE - 1) / RS_TILE;
+    GM_REQUIRE(n_tiles < (int64_t)1 << 31, GMAGNUS_ERROR_UNSUPPORTED, "expansion: too many tiles for one panel");
+    RsTile *info = (RsTile *)tile_words;
+    hipLaunchKernelGGL(k_rs_tiles, dim3(grid_for(n_tiles, 256, 65536)), dim3(256), 0, s, out_ptr, n_out, seg_base,
+                       reg_c, reg_efirst, reg_ne, pre, nc, total, n_tiles, info);
+    GM_CHECK_LAUNCH();
+    const int lds = rs2_layout(K).total;
+    static bool attr_set = false;
+    if (!attr_set) {
+        GM_HIP(hipFuncSetAttribute((const void *)k_expand_rows2, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                   rs2_layout(RS2_KMAX).total));
+        attr_set = true;
+    }
+    Rs2Args a{B,       ent,   pre,   bnd,  out_ptr, seg_base, reg_c,    reg_efirst, n_out,   n_heavy_out,
+              total,   n_tiles, info, nc,  shift,   nc1,      shift1,   R,          cursor1, n_out1_elems,
+              err,     out_col0, out_val0, out_col1, out_val1};
+    hipLaunchKernelGGL(k_expand_rows2, dim3((unsigned)n_tiles), dim3(RS_BLOCK), lds, s, a);
     GM_CHECK_LAUNCH();
 }
 

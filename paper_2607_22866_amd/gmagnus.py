@@ -25,6 +25,7 @@ FLAG_NO_WINDOW = 4
 FLAG_PAPER_HISTOGRAM = 8
 FLAG_PAPER_EXPANSION = 16
 FLAG_SLICE_SPLIT = 32
+FLAG_LEVEL_BY_LEVEL = 64
 
 STATUS = {0: "SUCCESS", 1: "INVALID_VALUE", 2: "INVALID_CSR", 3: "OUT_OF_MEMORY", 4: "NOT_READY", 5: "HIP",
           6: "UNSUPPORTED"}

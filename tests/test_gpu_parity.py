@@ -98,11 +98,22 @@ def test_rmat12_slice_order_split(g, opts, levels):
     assert info.params.levels == levels
 
 
+@pytest.mark.parametrize("opts,levels", [d for d in DEPTHS if len(d[1]) == 2])
+def test_rmat12_two_levels_level_by_level(g, opts, levels):
+    # with two levels the expansion writes the final chunks directly; writing
+    # the first level out and splitting it in its own pass gives the same C
+    A = RMAT12.make()
+    info = check(g, A, A, flags=g.FLAG_LEVEL_BY_LEVEL, **opts)
+    assert info.params.levels == levels and info.levels_run == 2
+
+
 def test_rmat12_integer_values_bit_exact(g):
     A = wl.rmat(12, 8, 0.57, 0.19, 0.19, 12, values="int3")
     for opts in ({}, dict(tau=200, dense_width_log2=6, chunks_max_log2=2),
                  dict(tau=200, dense_width_log2=6, chunks_max_log2=2, flags=g.FLAG_PAPER_EXPANSION),
-                 dict(tau=200, dense_width_log2=6, chunks_max_log2=2, flags=g.FLAG_SLICE_SPLIT)):
+                 dict(tau=200, dense_width_log2=6, chunks_max_log2=2, flags=g.FLAG_SLICE_SPLIT),
+                 dict(tau=300, dense_width_log2=7, chunks_max_log2=3),
+                 dict(tau=300, dense_width_log2=7, chunks_max_log2=3, flags=g.FLAG_LEVEL_BY_LEVEL)):
         rp, col, val, _ = run(g, A, A, **opts)
         ref = oracle.spgemm(A, A)
         assert np.array_equal(rp, ref.row_ptr) and np.array_equal(col, ref.col)
@@ -241,9 +252,16 @@ def test_numeric_before_symbolic_rejected(g):
 
 def test_serial_streams_and_timing_flags(g):
     A = RMAT12.make()
-    info = check(g, A, A, flags=1 | 2, tau=300, dense_width_log2=7, chunks_max_log2=3)
+    # three levels: the levels after the first run the multisplit kernel
+    info = check(g, A, A, flags=1 | 2, tau=200, dense_width_log2=6, chunks_max_log2=2)
     d = info.to_dict()
     assert d["kernels"]["expand"]["ms"] > 0 and d["kernels"]["multisplit"]["launches"] >= 1
+    # two levels: both are written by the expansion, no multisplit pass
+    info = check(g, A, A, flags=1 | 2, tau=300, dense_width_log2=7, chunks_max_log2=3)
+    d = info.to_dict()
+    assert d["kernels"]["multisplit"]["launches"] == 0 and info.levels_run == 2
+    info = check(g, A, A, flags=1 | 2 | g.FLAG_LEVEL_BY_LEVEL, tau=300, dense_width_log2=7, chunks_max_log2=3)
+    assert info.to_dict()["kernels"]["multisplit"]["launches"] == 1
 
 
 def test_sampled_rows_helper(g):
