@@ -387,7 +387,11 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows(RsArgs a) {
 // lay out the final chunks beforehand, come from the structure: per slice
 // the boundaries of its B row at every fine chunk (first-level chunk times
 // second-level chunk), and per heavy row the sum over its entries of their
-// fine chunk sizes.
+// fine chunk sizes. The outputs are written with nontemporal stores: they
+// are read again only by a later kernel, and keeping them out of the caches
+// leaves room for the B rows that the tiles gather (measured: a tile loop
+// that gathers from a 170 MB table while streaming its output out runs 15 %
+// faster with nontemporal stores).
 
 // Fine boundaries: bndf[s * (nf + 1) + f] = offset in B[k,:] of the first
 // column >= f << fshift (f = 0..nf). One wave per slice; a row of at most 64
@@ -651,8 +655,8 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args a) {
             for (int u = 0; u < RS2_E; ++u) {
                 if (key[u] == -2) {
                     const int64_t d = g0 + sbt + u * RS_BLOCK + tid;
-                    a.out_col0[d] = col[u];
-                    a.out_val0[d] = val[u];
+                    __builtin_nontemporal_store(col[u], &a.out_col0[d]);
+                    __builtin_nontemporal_store(val[u], &a.out_val0[d]);
                     key[u] = -1;
                 }
             }
@@ -722,8 +726,8 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args a) {
                     atomicOr(a.err, 8);
                     continue;
                 }
-                a.out_col1[d] = col_buf[p];
-                a.out_val1[d] = val_buf[p];
+                __builtin_nontemporal_store(col_buf[p], &a.out_col1[d]);
+                __builtin_nontemporal_store(val_buf[p], &a.out_val1[d]);
             }
             for (int k = tid; k < RS2_NW * K; k += RS_BLOCK) whist[k] = 0;
             __syncthreads();
