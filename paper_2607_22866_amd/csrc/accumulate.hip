@@ -19,6 +19,14 @@ namespace gm {
 
 namespace {
 
+// Column of element t of a leaf set: chunk-local, stored in 32 bits, or in
+// 16 bits for the final chunks the fused expansion writes (a wave-uniform
+// branch on a kernel argument).
+GM_DEV int32_t leaf_col(const LeafSet &L, int64_t t) { return L.col16 ? (int32_t)L.col16[t] : L.col[t]; }
+GM_DEV int32_t leaf_col_nt(const LeafSet &L, int64_t t) {
+    return L.col16 ? (int32_t)__builtin_nontemporal_load(&L.col16[t]) : __builtin_nontemporal_load(&L.col[t]);
+}
+
 // --------------------------------------------------------------- sources
 template <int BLOCK>
 struct GusLds {
@@ -627,7 +635,7 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_hash_sym(LeafSet L, const LeafTa
     hash_clear<BLOCK, TS>(keys, nullptr);
     if (threadIdx.x == 0) counter = 0;
     __syncthreads();
-    for (int64_t t = s + threadIdx.x; t < e; t += BLOCK) hash_insert_key<TS>(keys, L.col[t], &counter);
+    for (int64_t t = s + threadIdx.x; t < e; t += BLOCK) hash_insert_key<TS>(keys, leaf_col(L, t), &counter);
     __syncthreads();
     if (threadIdx.x == 0) {
         leaf_nnz[tk.a] = counter;
@@ -687,7 +695,7 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_hash_num(LeafSet L, const LeafTa
     const int64_t s = tk.s, e = tk.e;
     hash_clear<BLOCK, TS>(keys, vals);
     __syncthreads();
-    for (int64_t t = s + threadIdx.x; t < e; t += BLOCK) hash_insert_add<TS>(keys, vals, L.col[t], L.val[t]);
+    for (int64_t t = s + threadIdx.x; t < e; t += BLOCK) hash_insert_add<TS>(keys, vals, leaf_col(L, t), L.val[t]);
     __syncthreads();
     const int64_t dst = tk.t, nnz = tk.a;
     const int32_t base = tk.b;
@@ -712,7 +720,7 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_dense_sym(LeafSet L, const LeafT
 #pragma unroll
         for (int q = 0; q < 2 * LEAF_EPT; ++q) {
             const int64_t t = b + q * BLOCK + threadIdx.x;
-            c[q] = t < e ? __builtin_nontemporal_load(&L.col[t]) : -1;
+            c[q] = t < e ? leaf_col_nt(L, t) : -1;
         }
 #pragma unroll
         for (int q = 0; q < 2 * LEAF_EPT; ++q)
@@ -741,7 +749,7 @@ GM_DEV void dense_load(const LeafSet &L, int64_t b, int64_t e, int32_t (&c)[EPT]
 #pragma unroll
     for (int q = 0; q < EPT; ++q) {
         const int64_t t = b + q * BLOCK + threadIdx.x;
-        c[q] = t < e ? __builtin_nontemporal_load(&L.col[t]) : -1;
+        c[q] = t < e ? leaf_col_nt(L, t) : -1;
         v[q] = t < e ? __builtin_nontemporal_load(&L.val[t]) : 0.0;
     }
 }
@@ -816,7 +824,7 @@ GM_DEV void rank_load(const LeafSet &L, int64_t s, int64_t e, int32_t (&c)[EPT],
 #pragma unroll
     for (int q = 0; q < EPT; ++q) {
         const int64_t t = s + q * BLOCK + threadIdx.x;
-        c[q] = t < e ? __builtin_nontemporal_load(&L.col[t]) : -1;
+        c[q] = t < e ? leaf_col_nt(L, t) : -1;
         if (vals) v[q] = t < e ? __builtin_nontemporal_load(&L.val[t]) : 0.0;
     }
 }

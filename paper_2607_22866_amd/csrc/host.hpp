@@ -203,12 +203,13 @@ void level1_counts(const int64_t *perm, int64_t n_regions, int64_t n_heavy, cons
 // whether the fused second level's keys fit the work group
 bool rows2_fits(int64_t tau, int nc1, int nf);
 // cursor1: next free place of second-level row r * nc1 + c1 (starts at its
-// row pointer); light regions are written to out_*0 at their first-level place.
+// row pointer); light regions are written to out_*0 at their first-level place;
+// the final chunks' columns (at most 2^16 wide) are stored in 16 bits.
 void expand_rows2(const Csr &B, const RowEntries &ent, const uint32_t *pre, const int32_t *bnd,
                   const int64_t *out_ptr, const int64_t *seg_base, const int32_t *reg_c, const int64_t *reg_efirst,
                   const int64_t *reg_ne, int64_t n_out, int64_t n_heavy_out, int64_t total, int nc, int shift,
                   int nc1, int shift1, int64_t tau, int64_t *cursor1, int64_t n_out1_elems, int32_t *err,
-                  int64_t *tile_words, int32_t *out_col0, double *out_val0, int32_t *out_col1, double *out_val1,
+                  int64_t *tile_words, int32_t *out_col0, double *out_val0, uint16_t *out_col1, double *out_val1,
                   hipStream_t s);
 
 // ------------------------------------------------------------ multisplit.hip
@@ -247,10 +248,11 @@ void multisplit(const LevelGeom &g, const int64_t *in_ptr, const int64_t *tile_r
 // Final chunks ("leaves"): chunk rows [lo, hi) of some level's output.
 struct LeafSet {
     const int64_t *ptr;    // chunk row pointers of that level's output
-    const int32_t *col;    // chunk-local columns
+    const int32_t *col;    // chunk-local columns (or col16)
     const double *val;
     const int64_t *origin; // slot id h * n_slots + slot, per chunk row
     int64_t lo, hi;
+    const uint16_t *col16 = nullptr;  // chunk-local columns stored in 16 bits (final chunks of at most 2^16 columns)
 };
 enum LeafBin : uint8_t {
     LEAF_EMPTY = 0, LEAF_H0, LEAF_H1, LEAF_H2, LEAF_H3, LEAF_DENSE_BIG, LEAF_DENSE, LEAF_RANK, LEAF_RANK_L, LEAF_NBINS

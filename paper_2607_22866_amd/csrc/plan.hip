@@ -774,15 +774,17 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                     Timed t(p, GMAGNUS_K_EXPAND, s);
                     expand_rows2(p->B, ent, pre, sbnd, out_ptr, seg_base, reg_c, reg_efirst, reg_ne, n_out, nh_out, H,
                                  nc, g.shift, nc1, shift1, P.tau, cursor1, elems1, p->err, exp_tiles, col_buf[0],
-                                 val_buf[0], col_buf[1], val_buf[1], s);
+                                 val_buf[0], (uint16_t *)col_buf[1], val_buf[1], s);
                 }
                 p->info.kernel_launches[GMAGNUS_K_EXPAND] += 1;
-                add_bytes(p, GMAGNUS_K_EXPAND, 12.0 * H + 20.0 * nnz_heavy_all + 4.0 * nnz_heavy_all * nc +
-                                                   12.0 * blen_total + 24.0 * n_out + 8.0 * n_out1);
+                // products (the final chunks' columns in 16 bits), entries, offsets, B rows, row records
+                add_bytes(p, GMAGNUS_K_EXPAND, 12.0 * H - 2.0 * elems1 + 20.0 * nnz_heavy_all +
+                                                   4.0 * nnz_heavy_all * nc + 12.0 * blen_total + 24.0 * n_out +
+                                                   8.0 * n_out1);
                 p->info.level_rows_in[1] = nh_out;
                 p->info.level_elems_in[1] = elems1;
                 p->info.level_heavy_out[1] = 0;
-                two_done.set = LeafSet{out_ptr1, col_buf[1], val_buf[1], origin_out1, 0, n_out1};
+                two_done.set = LeafSet{out_ptr1, nullptr, val_buf[1], origin_out1, 0, n_out1, (const uint16_t *)col_buf[1]};
                 two_done.width = 1 << shift1;
                 two_done.elems = elems1;
                 ws.free(counts1);
@@ -897,7 +899,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                 else if (b == LEAF_RANK || b == LEAF_RANK_L) p->info.n_leaves_rank += cnt;
                 else p->info.n_leaves_hash += cnt;
             }
-            add_bytes(p, GMAGNUS_K_CHUNK_SYM, 4.0 * lv.elems + 16.0 * nl);
+            add_bytes(p, GMAGNUS_K_CHUNK_SYM, (lv.set.col16 ? 2.0 : 4.0) * lv.elems + 16.0 * nl);
             ws.free(tasks);
         }
         // numeric bins now, so the numeric phase needs no host round trip
@@ -1041,7 +1043,7 @@ void do_numeric(gmagnus_plan_s *p, const int64_t *c_row_ptr, int32_t *c_col, dou
             }
             p->ws->free(tasks);
             p->ws->free(counter);
-            add_bytes(p, GMAGNUS_K_CHUNK_NUM, 12.0 * lv.elems);
+            add_bytes(p, GMAGNUS_K_CHUNK_NUM, (lv.set.col16 ? 10.0 : 12.0) * lv.elems);
         }
     }
     {

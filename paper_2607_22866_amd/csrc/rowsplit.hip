@@ -496,7 +496,7 @@ __global__ void k_level1_counts(const int64_t *perm, int64_t n_regions, int64_t 
     }
 }
 
-constexpr int RS2_SUB = 2048;                 // products split per sub-batch
+constexpr int RS2_SUB = 1024;                 // products split per sub-batch
 constexpr int RS2_E = RS2_SUB / RS_BLOCK;     // per thread
 constexpr int RS2_KMAX = 1024;                // keys: heavy regions per tile times second-level chunks
 constexpr int RS2_NW = RS_BLOCK / GM_WAVE;
@@ -538,7 +538,7 @@ struct Rs2Args {
     int32_t *err;            // set when a key or a place falls outside its range (a bug)
     int32_t *out_col0;       // first level (light regions)
     double *out_val0;
-    int32_t *out_col1;       // second level
+    uint16_t *out_col1;      // second level (final chunks: at most 2^16 columns)
     double *out_val1;
 };
 
@@ -726,7 +726,7 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args a) {
                     atomicOr(a.err, 8);
                     continue;
                 }
-                __builtin_nontemporal_store(col_buf[p], &a.out_col1[d]);
+                __builtin_nontemporal_store((uint16_t)col_buf[p], &a.out_col1[d]);
                 __builtin_nontemporal_store(val_buf[p], &a.out_val1[d]);
             }
             for (int k = tid; k < RS2_NW * K; k += RS_BLOCK) whist[k] = 0;
@@ -843,10 +843,10 @@ void expand_rows2(const Csr &B, const RowEntries &ent, const uint32_t *pre, cons
                   const int64_t *out_ptr, const int64_t *seg_base, const int32_t *reg_c, const int64_t *reg_efirst,
                   const int64_t *reg_ne, int64_t n_out, int64_t n_heavy_out, int64_t total, int nc, int shift,
                   int nc1, int shift1, int64_t tau, int64_t *cursor1, int64_t n_out1_elems, int32_t *err,
-                  int64_t *tile_words, int32_t *out_col0, double *out_val0, int32_t *out_col1, double *out_val1,
+                  int64_t *tile_words, int32_t *out_col0, double *out_val0, uint16_t *out_col1, double *out_val1,
                   hipStream_t s) {
     if (total <= 0) return;
-    GM_REQUIRE(nc >= 1 && nc < GM_WAVE && shift >= 0 && shift < 31 && shift1 >= 0 && shift1 <= shift,
+    GM_REQUIRE(nc >= 1 && nc < GM_WAVE && shift >= 0 && shift < 31 && shift1 >= 0 && shift1 <= shift && shift1 <= 16,
                GMAGNUS_ERROR_UNSUPPORTED, "two-level expansion: unsupported chunking");
     const int R = rows2_regions(tau);
     const int K = R * nc1;
