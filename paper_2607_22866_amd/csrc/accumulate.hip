@@ -335,11 +335,19 @@ constexpr int RANK_MAX_LOG2 = 18;        // columns of the bitmap-rank accumulat
 constexpr int RANK_NNZ_MAX = 6912;       // distinct columns it holds (>= tau; two work groups per CU at 2^17 columns)
 constexpr int RANK_MIN_LEN = 256;        // smaller chunks go to the hash map
 constexpr int RANK_SMALL = 2048;         // distinct columns of the small rank variant
+constexpr int RANK_NARROW_CAP = 2048;    // chunks of at most DENSE_MAX columns and at most this many elements use
+                                         // a rank accumulator (one work group per chunk, LDS sized by the chunk)
+constexpr int RANK_NARROW_SMALL = 512;   // ... its small shape up to this many
 
-// Accumulator of a final chunk of `len` elements over `width` columns:
-// heavy chunks (len > tau, width <= W) and well-filled narrow chunks use the
-// dense accumulator; wide light chunks use the bitmap-rank accumulator while
-// the bitmap fits LDS; small chunks use the hash map.
+// Accumulator of a final chunk of `len` elements over `width` columns.
+// Chunks of at most W columns: above RANK_NARROW_CAP elements the dense
+// accumulator (a persistent kernel with the W-column value array in LDS);
+// from RANK_MIN_LEN up to RANK_NARROW_CAP the bitmap-rank accumulator, one
+// work group per chunk with LDS sized by the chunk, so many chunks run on a
+// CU at once (the dense kernel pays a chain of memory latencies per chunk,
+// and holds two work groups per CU); smaller chunks the hash map. Wider
+// chunks: the bitmap-rank accumulator while the bitmap fits LDS, else the
+// hash map.
 __global__ void k_leaf_classes(LeafSet L, const int64_t *leaf_nnz, int64_t tau, int width, uint8_t *cls) {
     const int64_t n = L.hi - L.lo;
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
@@ -348,7 +356,11 @@ __global__ void k_leaf_classes(LeafSet L, const int64_t *leaf_nnz, int64_t tau, 
         uint8_t c;
         if (len == 0)
             c = LEAF_EMPTY;
-        else if (width <= DENSE_MAX && (len > tau || len >= width / 16))
+        else if (width <= DENSE_MAX && width >= 32 && len >= RANK_MIN_LEN && len <= RANK_NARROW_CAP)
+            c = len > RANK_NARROW_SMALL ? LEAF_RANK_L : LEAF_RANK;
+        else if (width <= DENSE_MAX && width >= 32 && len > RANK_NARROW_CAP)
+            c = len >= DENSE_BIG_LEN ? LEAF_DENSE_BIG : LEAF_DENSE;
+        else if (width < 32 && (len > tau || len >= width / 16))
             c = len >= DENSE_BIG_LEN ? LEAF_DENSE_BIG : LEAF_DENSE;
         else if (width <= (1 << RANK_MAX_LOG2) && width >= 32 && len >= RANK_MIN_LEN)
             c = (leaf_nnz && leaf_nnz[i] > RANK_SMALL) ? LEAF_RANK_L : LEAF_RANK;
@@ -815,8 +827,10 @@ __global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(8))) void
 // 512 threads with up to 2^18 columns for the wide light chunks.
 constexpr int RANK_BLOCK = 512;
 constexpr int RANK_EPT = 16;  // RANK_BLOCK * RANK_EPT >= tau_limit()
-constexpr int RANK_SBLOCK = 256, RANK_SWORDS = 256, RANK_SCAP = 512, RANK_SEPT = 2;
-static_assert(RANK_SBLOCK * RANK_SEPT >= DENSE_MAX / 16, "narrow light chunks hold fewer than width/16 elements");
+constexpr int RANK_SBLOCK = 256, RANK_SWORDS = 256, RANK_SCAP = 512, RANK_SEPT = 2, RANK_LEPT = 8;
+static_assert(RANK_SBLOCK * RANK_SEPT >= RANK_NARROW_SMALL && RANK_SCAP >= RANK_NARROW_SMALL,
+              "the small narrow shape holds its chunks");
+static_assert(RANK_SBLOCK * RANK_LEPT >= RANK_NARROW_CAP, "the large narrow shape holds its chunks");
 static_assert(RANK_SWORDS * 32 == DENSE_MAX, "narrow bitmap covers the dense width");
 
 template <int BLOCK, int EPT>
@@ -1057,8 +1071,11 @@ void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *items, int64_t n, 
     case LEAF_RANK_L: {
         GM_REQUIRE(n <= 0 || width <= (1 << RANK_MAX_LOG2), GMAGNUS_ERROR_UNSUPPORTED, "rank bitmap too wide");
         constexpr int W17 = (1 << 17) / 32, W18 = (1 << 18) / 32;
-        if (width <= DENSE_MAX)
+        if (width <= DENSE_MAX && bin == LEAF_RANK)
             launch_items(k_leaf_rank_sym<RANK_SBLOCK, RANK_SWORDS, RANK_SEPT>, RANK_SBLOCK, n, s, L, items, width,
+                         leaf_nnz, slot_cnt);
+        else if (width <= DENSE_MAX)
+            launch_items(k_leaf_rank_sym<RANK_SBLOCK, RANK_SWORDS, RANK_LEPT>, RANK_SBLOCK, n, s, L, items, width,
                          leaf_nnz, slot_cnt);
         else if (width <= (1 << 17))
             launch_items(k_leaf_rank_sym<RANK_BLOCK, W17, RANK_EPT>, RANK_BLOCK, n, s, L, items, width, leaf_nnz,
@@ -1101,9 +1118,12 @@ void leaf_numeric(const LeafSet &L, int bin, const LeafTask *items, int64_t n, i
         GM_REQUIRE(n <= 0 || width <= (1 << RANK_MAX_LOG2), GMAGNUS_ERROR_UNSUPPORTED, "rank bitmap too wide");
         constexpr int W17 = (1 << 17) / 32, W18 = (1 << 18) / 32;
         const bool narrow = width <= (1 << 17);
-        if (width <= DENSE_MAX)  // fewer than width/16 elements (the dense class takes the rest)
+        if (width <= DENSE_MAX && bin == LEAF_RANK)  // at most RANK_NARROW_SMALL elements
             launch_items(k_leaf_rank_num<RANK_SBLOCK, RANK_SWORDS, RANK_SCAP, RANK_SEPT>, RANK_SBLOCK, n, s, L, items,
                          width, o);
+        else if (width <= DENSE_MAX)  // at most RANK_NARROW_CAP elements
+            launch_items(k_leaf_rank_num<RANK_SBLOCK, RANK_SWORDS, RANK_NARROW_CAP, RANK_LEPT>, RANK_SBLOCK, n, s, L,
+                         items, width, o);
         else if (bin == LEAF_RANK && narrow)
             launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_SMALL, RANK_EPT>, RANK_BLOCK, n, s, L, items, width, o);
         else if (bin == LEAF_RANK)
