@@ -335,9 +335,10 @@ constexpr int RANK_MAX_LOG2 = 18;        // columns of the bitmap-rank accumulat
 constexpr int RANK_NNZ_MAX = 6912;       // distinct columns it holds (>= tau; two work groups per CU at 2^17 columns)
 constexpr int RANK_MIN_LEN = 256;        // smaller chunks go to the hash map
 constexpr int RANK_SMALL = 2048;         // distinct columns of the small rank variant
-constexpr int RANK_NARROW_CAP = 2048;    // chunks of at most DENSE_MAX columns and at most this many elements use
+constexpr int RANK_NARROW_CAP = 4096;    // chunks of at most DENSE_MAX columns and at most this many elements use
                                          // a rank accumulator (one work group per chunk, LDS sized by the chunk)
 constexpr int RANK_NARROW_SMALL = 512;   // ... its small shape up to this many
+constexpr int RANK_NARROW_MID = 2048;    // ... its middle shape up to this many
 
 // Accumulator of a final chunk of `len` elements over `width` columns.
 // Chunks of at most W columns: above RANK_NARROW_CAP elements the dense
@@ -357,7 +358,7 @@ __global__ void k_leaf_classes(LeafSet L, const int64_t *leaf_nnz, int64_t tau, 
         if (len == 0)
             c = LEAF_EMPTY;
         else if (width <= DENSE_MAX && width >= 32 && len >= RANK_MIN_LEN && len <= RANK_NARROW_CAP)
-            c = len > RANK_NARROW_SMALL ? LEAF_RANK_L : LEAF_RANK;
+            c = len > RANK_NARROW_MID ? LEAF_RANK_XL : len > RANK_NARROW_SMALL ? LEAF_RANK_L : LEAF_RANK;
         else if (width <= DENSE_MAX && width >= 32 && len > RANK_NARROW_CAP)
             c = len >= DENSE_BIG_LEN ? LEAF_DENSE_BIG : LEAF_DENSE;
         else if (width < 32 && (len > tau || len >= width / 16))
@@ -830,7 +831,9 @@ constexpr int RANK_EPT = 16;  // RANK_BLOCK * RANK_EPT >= tau_limit()
 constexpr int RANK_SBLOCK = 256, RANK_SWORDS = 256, RANK_SCAP = 512, RANK_SEPT = 2, RANK_LEPT = 8;
 static_assert(RANK_SBLOCK * RANK_SEPT >= RANK_NARROW_SMALL && RANK_SCAP >= RANK_NARROW_SMALL,
               "the small narrow shape holds its chunks");
-static_assert(RANK_SBLOCK * RANK_LEPT >= RANK_NARROW_CAP, "the large narrow shape holds its chunks");
+static_assert(RANK_SBLOCK * RANK_LEPT >= RANK_NARROW_MID, "the middle narrow shape holds its chunks");
+constexpr int RANK_XBLOCK = 512;
+static_assert(RANK_XBLOCK * RANK_LEPT >= RANK_NARROW_CAP, "the large narrow shape holds its chunks");
 static_assert(RANK_SWORDS * 32 == DENSE_MAX, "narrow bitmap covers the dense width");
 
 template <int BLOCK, int EPT>
@@ -1068,14 +1071,18 @@ void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *items, int64_t n, 
         launch_items(k_leaf_dense_sym<512>, 512, n, s, L, items, width, leaf_nnz, slot_cnt);
         break;
     case LEAF_RANK:
-    case LEAF_RANK_L: {
+    case LEAF_RANK_L:
+    case LEAF_RANK_XL: {
         GM_REQUIRE(n <= 0 || width <= (1 << RANK_MAX_LOG2), GMAGNUS_ERROR_UNSUPPORTED, "rank bitmap too wide");
         constexpr int W17 = (1 << 17) / 32, W18 = (1 << 18) / 32;
         if (width <= DENSE_MAX && bin == LEAF_RANK)
             launch_items(k_leaf_rank_sym<RANK_SBLOCK, RANK_SWORDS, RANK_SEPT>, RANK_SBLOCK, n, s, L, items, width,
                          leaf_nnz, slot_cnt);
-        else if (width <= DENSE_MAX)
+        else if (width <= DENSE_MAX && bin == LEAF_RANK_L)
             launch_items(k_leaf_rank_sym<RANK_SBLOCK, RANK_SWORDS, RANK_LEPT>, RANK_SBLOCK, n, s, L, items, width,
+                         leaf_nnz, slot_cnt);
+        else if (width <= DENSE_MAX)
+            launch_items(k_leaf_rank_sym<RANK_XBLOCK, RANK_SWORDS, RANK_LEPT>, RANK_XBLOCK, n, s, L, items, width,
                          leaf_nnz, slot_cnt);
         else if (width <= (1 << 17))
             launch_items(k_leaf_rank_sym<RANK_BLOCK, W17, RANK_EPT>, RANK_BLOCK, n, s, L, items, width, leaf_nnz,
@@ -1114,15 +1121,19 @@ void leaf_numeric(const LeafSet &L, int bin, const LeafTask *items, int64_t n, i
         }
         break;
     case LEAF_RANK:
-    case LEAF_RANK_L: {
+    case LEAF_RANK_L:
+    case LEAF_RANK_XL: {
         GM_REQUIRE(n <= 0 || width <= (1 << RANK_MAX_LOG2), GMAGNUS_ERROR_UNSUPPORTED, "rank bitmap too wide");
         constexpr int W17 = (1 << 17) / 32, W18 = (1 << 18) / 32;
         const bool narrow = width <= (1 << 17);
         if (width <= DENSE_MAX && bin == LEAF_RANK)  // at most RANK_NARROW_SMALL elements
             launch_items(k_leaf_rank_num<RANK_SBLOCK, RANK_SWORDS, RANK_SCAP, RANK_SEPT>, RANK_SBLOCK, n, s, L, items,
                          width, o);
+        else if (width <= DENSE_MAX && bin == LEAF_RANK_L)  // at most RANK_NARROW_MID elements
+            launch_items(k_leaf_rank_num<RANK_SBLOCK, RANK_SWORDS, RANK_NARROW_MID, RANK_LEPT>, RANK_SBLOCK, n, s, L,
+                         items, width, o);
         else if (width <= DENSE_MAX)  // at most RANK_NARROW_CAP elements
-            launch_items(k_leaf_rank_num<RANK_SBLOCK, RANK_SWORDS, RANK_NARROW_CAP, RANK_LEPT>, RANK_SBLOCK, n, s, L,
+            launch_items(k_leaf_rank_num<RANK_XBLOCK, RANK_SWORDS, RANK_NARROW_CAP, RANK_LEPT>, RANK_XBLOCK, n, s, L,
                          items, width, o);
         else if (bin == LEAF_RANK && narrow)
             launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_SMALL, RANK_EPT>, RANK_BLOCK, n, s, L, items, width, o);
