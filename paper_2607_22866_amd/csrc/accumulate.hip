@@ -339,6 +339,8 @@ constexpr int RANK_NARROW_CAP = 4096;    // chunks of at most DENSE_MAX columns 
                                          // a rank accumulator (one work group per chunk, LDS sized by the chunk)
 constexpr int RANK_NARROW_SMALL = 512;   // ... its small shape up to this many
 constexpr int RANK_NARROW_MID = 2048;    // ... its middle shape up to this many
+constexpr int RANK_WIDE_SMALL = 1024;    // wider chunks of at most this many elements count their columns with
+                                         // the small wide shape
 
 // Accumulator of a final chunk of `len` elements over `width` columns.
 // Chunks of at most W columns: above RANK_NARROW_CAP elements the dense
@@ -364,7 +366,9 @@ __global__ void k_leaf_classes(LeafSet L, const int64_t *leaf_nnz, int64_t tau, 
         else if (width < 32 && (len > tau || len >= width / 16))
             c = len >= DENSE_BIG_LEN ? LEAF_DENSE_BIG : LEAF_DENSE;
         else if (width <= (1 << RANK_MAX_LOG2) && width >= 32 && len >= RANK_MIN_LEN)
-            c = (leaf_nnz && leaf_nnz[i] > RANK_SMALL) ? LEAF_RANK_L : LEAF_RANK;
+            // symbolic: the small wide shape for small chunks; numeric: by distinct columns
+            c = !leaf_nnz ? (len <= RANK_WIDE_SMALL ? LEAF_RANK : LEAF_RANK_L)
+                          : (leaf_nnz[i] > RANK_SMALL ? LEAF_RANK_XL : LEAF_RANK_L);
         else
             c = (uint8_t)(LEAF_H0 + (leaf_nnz ? hash_bin_num(leaf_nnz[i]) : hash_bin_sym(len)));
         cls[i] = c;
@@ -828,6 +832,8 @@ __global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(8))) void
 // 512 threads with up to 2^18 columns for the wide light chunks.
 constexpr int RANK_BLOCK = 512;
 constexpr int RANK_EPT = 16;  // RANK_BLOCK * RANK_EPT >= tau_limit()
+constexpr int RANK_WBLOCK = 256, RANK_WEPT = 4;  // the small wide shape
+static_assert(RANK_WBLOCK * RANK_WEPT >= RANK_WIDE_SMALL, "the small wide shape holds its chunks");
 constexpr int RANK_SBLOCK = 256, RANK_SWORDS = 256, RANK_SCAP = 512, RANK_SEPT = 2, RANK_LEPT = 8;
 static_assert(RANK_SBLOCK * RANK_SEPT >= RANK_NARROW_SMALL && RANK_SCAP >= RANK_NARROW_SMALL,
               "the small narrow shape holds its chunks");
@@ -1084,6 +1090,12 @@ void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *items, int64_t n, 
         else if (width <= DENSE_MAX)
             launch_items(k_leaf_rank_sym<RANK_XBLOCK, RANK_SWORDS, RANK_LEPT>, RANK_XBLOCK, n, s, L, items, width,
                          leaf_nnz, slot_cnt);
+        else if (width <= (1 << 17) && bin == LEAF_RANK)
+            launch_items(k_leaf_rank_sym<RANK_WBLOCK, W17, RANK_WEPT>, RANK_WBLOCK, n, s, L, items, width, leaf_nnz,
+                         slot_cnt);
+        else if (bin == LEAF_RANK)
+            launch_items(k_leaf_rank_sym<RANK_WBLOCK, W18, RANK_WEPT>, RANK_WBLOCK, n, s, L, items, width, leaf_nnz,
+                         slot_cnt);
         else if (width <= (1 << 17))
             launch_items(k_leaf_rank_sym<RANK_BLOCK, W17, RANK_EPT>, RANK_BLOCK, n, s, L, items, width, leaf_nnz,
                          slot_cnt);
@@ -1135,9 +1147,9 @@ void leaf_numeric(const LeafSet &L, int bin, const LeafTask *items, int64_t n, i
         else if (width <= DENSE_MAX)  // at most RANK_NARROW_CAP elements
             launch_items(k_leaf_rank_num<RANK_XBLOCK, RANK_SWORDS, RANK_NARROW_CAP, RANK_LEPT>, RANK_XBLOCK, n, s, L,
                          items, width, o);
-        else if (bin == LEAF_RANK && narrow)
+        else if (bin != LEAF_RANK_XL && narrow)  // at most RANK_SMALL distinct columns
             launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_SMALL, RANK_EPT>, RANK_BLOCK, n, s, L, items, width, o);
-        else if (bin == LEAF_RANK)
+        else if (bin != LEAF_RANK_XL)
             launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_SMALL, RANK_EPT>, RANK_BLOCK, n, s, L, items, width, o);
         else if (narrow)
             launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_NNZ_MAX, RANK_EPT>, RANK_BLOCK, n, s, L, items, width,
