@@ -172,7 +172,7 @@ def main():
                     help="maximum intermediate products per row panel")
     ap.add_argument("--cpu-products", type=float, default=2.5e9, help="oracle sample size for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--serial", action="store_true", help="run heavy and light work on one stream")
+    ap.add_argument("--concurrent", action="store_true", help="run heavy and light work on two streams")
     ap.add_argument("--paper-expansion", action="store_true",
                     help="expand C-hat row by row and split it afterwards (the paper's order)")
     ap.add_argument("--slice-split", action="store_true",
@@ -209,7 +209,7 @@ def main():
     log("%d row panels (max %.2g products each)" % (len(bounds) - 1, args.panel_products))
     acc_warm = {}
     c_bufs = [None, None]
-    extra = ((g.FLAG_SERIAL_STREAMS if args.serial else 0) | (g.FLAG_PAPER_EXPANSION if args.paper_expansion else 0) |
+    extra = ((g.FLAG_CONCURRENT_STREAMS if args.concurrent else 0) | (g.FLAG_PAPER_EXPANSION if args.paper_expansion else 0) |
              (g.FLAG_SLICE_SPLIT if args.slice_split else 0) | (g.FLAG_LEVEL_BY_LEVEL if args.level_by_level else 0))
     for w in range(args.warmup):
         t = time.perf_counter()

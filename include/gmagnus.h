@@ -81,7 +81,8 @@ typedef struct {
 } gmagnus_options_t;
 
 #define GMAGNUS_FLAG_TIMING 1u         /* record per-phase device times (HIP events) into the plan info */
-#define GMAGNUS_FLAG_SERIAL_STREAMS 2u /* run heavy and light work on one stream (no concurrency) */
+#define GMAGNUS_FLAG_SERIAL_STREAMS 2u /* run heavy and light work on one stream (the default; kept so callers
+                                          that ask for it explicitly keep working) */
 #define GMAGNUS_FLAG_NO_WINDOW 4u      /* never use the dense-window accumulator for light rows */
 #define GMAGNUS_FLAG_PAPER_HISTOGRAM 8u /* level-0 histogram by a pass over C-hat's columns (the paper's
                                            kernel) instead of from the structure of A and B;
@@ -90,6 +91,10 @@ typedef struct {
                                             paper's order), instead of splitting during the expansion */
 #define GMAGNUS_FLAG_SLICE_SPLIT 32u /* split during the expansion in the paper's slice order (runs written at
                                         atomic cursors) instead of the chunk-major row order */
+#define GMAGNUS_FLAG_CONCURRENT_STREAMS 128u /* run the heavy rows and the light rows on two streams joined
+                                               with events (Algorithm 3's two queues) instead of one after the
+                                               other; measured slower on R-MAT scale 22, where the light rows'
+                                               kernels take CU slots from the bandwidth-bound heavy kernels */
 #define GMAGNUS_FLAG_LEVEL_BY_LEVEL 64u /* with two multisplit levels, write the first level's heavy chunks out
                                            and split them in a pass of their own, instead of splitting them again
                                            inside the expansion and writing the final chunks directly */

@@ -382,7 +382,7 @@ void do_plan(gmagnus_plan_s *p, const gmagnus_csr_t *A, const gmagnus_csr_t *B, 
     p->n = p->r1 - p->r0;
     p->stream = stream;
     p->timing = (o.flags & GMAGNUS_FLAG_TIMING) != 0;
-    if (o.flags & GMAGNUS_FLAG_SERIAL_STREAMS) {
+    if ((o.flags & GMAGNUS_FLAG_CONCURRENT_STREAMS) == 0 || (o.flags & GMAGNUS_FLAG_SERIAL_STREAMS)) {
         p->s_heavy = p->s_light = stream;
     } else {
         GM_HIP(hipStreamCreateWithFlags(&p->s_heavy, hipStreamNonBlocking));

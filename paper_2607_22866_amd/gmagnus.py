@@ -21,6 +21,7 @@ K_NAMES = ["setup", "csc", "expand", "histogram", "multisplit", "chunk_symbolic"
            "light_symbolic", "light_numeric", "rowptr"]
 FLAG_TIMING = 1
 FLAG_SERIAL_STREAMS = 2
+FLAG_CONCURRENT_STREAMS = 128
 FLAG_NO_WINDOW = 4
 FLAG_PAPER_HISTOGRAM = 8
 FLAG_PAPER_EXPANSION = 16

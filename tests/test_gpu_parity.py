@@ -250,6 +250,13 @@ def test_numeric_before_symbolic_rejected(g):
         assert e.value.status == 4
 
 
+@pytest.mark.parametrize("opts", [dict(), dict(tau=300, dense_width_log2=7, chunks_max_log2=3)])
+def test_concurrent_streams(g, opts):
+    # heavy and light rows on two streams joined by events give the same C
+    A = RMAT12.make()
+    check(g, A, A, flags=g.FLAG_CONCURRENT_STREAMS, **opts)
+
+
 def test_serial_streams_and_timing_flags(g):
     A = RMAT12.make()
     # three levels: the levels after the first run the multisplit kernel
