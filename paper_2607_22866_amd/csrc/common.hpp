@@ -44,6 +44,25 @@ GM_DEV T wave_incl_scan(T x) {
     return x;
 }
 
+// 32-bit values: the same scan with DPP moves (VALU only, no LDS permute).
+// row_shr:1,2,4,8 scan each row of 16 lanes (lanes whose source lies before
+// the row read 0); row_bcast:15 then adds lane 15's sum to row 1 and lane 47's
+// to row 3, and row_bcast:31 adds lane 31's sum to rows 2 and 3.
+template <>
+GM_DEV int32_t wave_incl_scan<int32_t>(int32_t x) {
+    x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);  // row_shr:1
+    x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);  // row_shr:2
+    x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);  // row_shr:4
+    x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);  // row_shr:8
+    x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15, rows 1 and 3
+    x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31, rows 2 and 3
+    return x;
+}
+
+// Value held by the previous lane of the wave (lane 0 gets `first`): one DPP
+// move with wave_shr:1.
+GM_DEV int32_t prev_lane(int32_t x, int32_t first) { return __builtin_amdgcn_update_dpp(first, x, 0x138, 0xf, 0xf, false); }
+
 template <typename T>
 GM_DEV T wave_reduce_sum(T x) {
 #pragma unroll

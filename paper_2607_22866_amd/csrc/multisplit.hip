@@ -81,7 +81,7 @@ __global__ __launch_bounds__(HIST_BLOCK) void k_histogram(int64_t n_in, int64_t 
         for (int u = 0; u < HIST_ILP; ++u) {
             const int64_t p = pb + u * HIST_BLOCK + tid;
             const int k = c[u] >= 0 ? local_row(rb, R, p) * n_chunks + (c[u] >> shift) : -1;
-            const int kprev = __shfl_up(k, 1, GM_WAVE);
+            const int kprev = prev_lane(k, k);
             const uint64_t starts = ballot(lane == 0 || k != kprev);
             if (k >= 0 && ((starts >> lane) & 1)) {
                 const uint64_t above = starts & ~le_mask;
@@ -195,7 +195,7 @@ __global__ __launch_bounds__(BLOCK) void k_multisplit(int64_t n_in, int64_t elem
 #pragma unroll
     for (int j = 0; j < E; ++j) {
         const int k = key[j];
-        const int kprev = __shfl_up(k, 1, GM_WAVE);
+        const int kprev = prev_lane(k, k);
         const uint64_t starts = ballot(lane == 0 || k != kprev);
         const int first = 63 - __clzll((long long)(starts & le_mask));
         const uint64_t above = starts & ~le_mask;
@@ -206,7 +206,7 @@ __global__ __launch_bounds__(BLOCK) void k_multisplit(int64_t n_in, int64_t elem
         rank[j] = base + (lane - first);
         if (fuse_next) {
             const int k2 = k >= 0 ? k * next_chunks + ((col[j] & mask) >> next_shift) : -1;
-            const int k2prev = __shfl_up(k2, 1, GM_WAVE);
+            const int k2prev = prev_lane(k2, k2);
             const uint64_t s2 = ballot(lane == 0 || k2 != k2prev);
             const uint64_t a2 = s2 & ~le_mask;
             if (k2 >= 0 && ((s2 >> lane) & 1)) {

@@ -345,7 +345,7 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows(RsArgs a) {
                 if (fuse_next) {
                     // next-level (region, sub-chunk) counts, one LDS atomic per run of equal keys
                     const int key = rg[u] >= 0 ? rg[u] * a.next_nc + (col[u] >> a.next_shift) : -1;
-                    const int kprev = __shfl_up(key, 1, GM_WAVE);
+                    const int kprev = prev_lane(key, key);
                     const uint64_t starts = ballot(lane == 0 || key != kprev);
                     if (key >= 0 && ((starts >> lane) & 1)) {
                         const uint64_t above = starts & ~le_mask;
@@ -665,7 +665,7 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args a) {
 #pragma unroll
             for (int u = 0; u < RS2_E; ++u) {
                 const int k = key[u];
-                const int kprev = __shfl_up(k, 1, GM_WAVE);
+                const int kprev = prev_lane(k, k);
                 const uint64_t starts = ballot(lane == 0 || k != kprev);
                 const int first = 63 - __clzll((long long)(starts & le_mask));
                 const uint64_t above = starts & ~le_mask;
