@@ -70,6 +70,12 @@ GM_DEV T wave_reduce_sum(T x) {
     return x;
 }
 
+// 32-bit values: the DPP scan's last lane holds the sum.
+template <>
+GM_DEV int32_t wave_reduce_sum<int32_t>(int32_t x) {
+    return __builtin_amdgcn_readlane(wave_incl_scan<int32_t>(x), GM_WAVE - 1);
+}
+
 // Exclusive scan over the block in thread order. `smem` holds BLOCK/64
 // entries; the block total is returned through *total when not null.
 // Contains __syncthreads: every thread of the block must call it.
