@@ -345,10 +345,11 @@ constexpr int RANK_WIDE_SMALL = 1024;    // wider chunks of at most this many el
 // Accumulator of a final chunk of `len` elements over `width` columns.
 // Chunks of at most W columns: above RANK_NARROW_CAP elements the dense
 // accumulator (a persistent kernel with the W-column value array in LDS);
-// from RANK_MIN_LEN up to RANK_NARROW_CAP the bitmap-rank accumulator, one
-// work group per chunk with LDS sized by the chunk, so many chunks run on a
-// CU at once (the dense kernel pays a chain of memory latencies per chunk,
-// and holds two work groups per CU); smaller chunks the hash map. Wider
+// up to RANK_NARROW_CAP the bitmap-rank accumulator, one work group per
+// chunk with LDS sized by the chunk, so many chunks run on a CU at once (the
+// dense kernel pays a chain of memory latencies per chunk, and holds two work
+// groups per CU); chunks below RANK_MIN_LEN take a one-wave shape whose word
+// ranks come from a single wave scan (no hash table to sort). Wider
 // chunks: the bitmap-rank accumulator while the bitmap fits LDS, else the
 // hash map.
 __global__ void k_leaf_classes(LeafSet L, const int64_t *leaf_nnz, int64_t tau, int width, uint8_t *cls) {
@@ -359,7 +360,9 @@ __global__ void k_leaf_classes(LeafSet L, const int64_t *leaf_nnz, int64_t tau, 
         uint8_t c;
         if (len == 0)
             c = LEAF_EMPTY;
-        else if (width <= DENSE_MAX && width >= 32 && len >= RANK_MIN_LEN && len <= RANK_NARROW_CAP)
+        else if (width <= DENSE_MAX && width >= 32 && len < RANK_MIN_LEN)
+            c = LEAF_RANK_T;
+        else if (width <= DENSE_MAX && width >= 32 && len <= RANK_NARROW_CAP)
             c = len > RANK_NARROW_MID ? LEAF_RANK_XL : len > RANK_NARROW_SMALL ? LEAF_RANK_L : LEAF_RANK;
         else if (width <= DENSE_MAX && width >= 32 && len > RANK_NARROW_CAP)
             c = len >= DENSE_BIG_LEN ? LEAF_DENSE_BIG : LEAF_DENSE;
@@ -841,6 +844,8 @@ static_assert(RANK_SBLOCK * RANK_LEPT >= RANK_NARROW_MID, "the middle narrow sha
 constexpr int RANK_XBLOCK = 512;
 static_assert(RANK_XBLOCK * RANK_LEPT >= RANK_NARROW_CAP, "the large narrow shape holds its chunks");
 static_assert(RANK_SWORDS * 32 == DENSE_MAX, "narrow bitmap covers the dense width");
+constexpr int RANK_TBLOCK = 64, RANK_TEPT = 4;  // one wave for narrow chunks below RANK_MIN_LEN elements
+static_assert(RANK_TBLOCK * RANK_TEPT >= RANK_MIN_LEN, "the one-wave shape holds its chunks");
 
 template <int BLOCK, int EPT>
 GM_DEV void rank_load(const LeafSet &L, int64_t s, int64_t e, int32_t (&c)[EPT], double (&v)[EPT], bool vals) {
@@ -1076,6 +1081,11 @@ void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *items, int64_t n, 
         GM_REQUIRE(n <= 0 || width <= DENSE_MAX, GMAGNUS_ERROR_UNSUPPORTED, "dense accumulator wider than LDS allows");
         launch_items(k_leaf_dense_sym<512>, 512, n, s, L, items, width, leaf_nnz, slot_cnt);
         break;
+    case LEAF_RANK_T:
+        GM_REQUIRE(n <= 0 || width <= DENSE_MAX, GMAGNUS_ERROR_UNSUPPORTED, "one-wave rank shape is for narrow chunks");
+        launch_items(k_leaf_rank_sym<RANK_TBLOCK, RANK_SWORDS, RANK_TEPT>, RANK_TBLOCK, n, s, L, items, width, leaf_nnz,
+                     slot_cnt);
+        break;
     case LEAF_RANK:
     case LEAF_RANK_L:
     case LEAF_RANK_XL: {
@@ -1131,6 +1141,11 @@ void leaf_numeric(const LeafSet &L, int bin, const LeafTask *items, int64_t n, i
                                0, s, L, items, n, width, o, counter);
             GM_CHECK_LAUNCH();
         }
+        break;
+    case LEAF_RANK_T:
+        GM_REQUIRE(n <= 0 || width <= DENSE_MAX, GMAGNUS_ERROR_UNSUPPORTED, "one-wave rank shape is for narrow chunks");
+        launch_items(k_leaf_rank_num<RANK_TBLOCK, RANK_SWORDS, RANK_MIN_LEN, RANK_TEPT>, RANK_TBLOCK, n, s, L, items,
+                     width, o);
         break;
     case LEAF_RANK:
     case LEAF_RANK_L:

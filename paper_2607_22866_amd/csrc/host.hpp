@@ -256,7 +256,7 @@ struct LeafSet {
 };
 enum LeafBin : uint8_t {
     LEAF_EMPTY = 0, LEAF_H0, LEAF_H1, LEAF_H2, LEAF_H3, LEAF_DENSE_BIG, LEAF_DENSE, LEAF_RANK, LEAF_RANK_L, LEAF_RANK_XL,
-    LEAF_NBINS
+    LEAF_RANK_T, LEAF_NBINS
 };
 enum LightBin : uint8_t {
     LIGHT_EMPTY = 0, LIGHT_HEAVY, LIGHT_W0, LIGHT_W1, LIGHT_H0, LIGHT_H1, LIGHT_H2, LIGHT_H3, LIGHT_NBINS

@@ -896,7 +896,8 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                 leaf_symbolic(lv.set, b, tasks + b0, cnt, lv.width, lv.leaf_nnz, p->slot, s);
                 if (cnt) p->info.kernel_launches[GMAGNUS_K_CHUNK_SYM] += 1;
                 if (b == LEAF_DENSE) p->info.n_leaves_dense += cnt;
-                else if (b == LEAF_RANK || b == LEAF_RANK_L || b == LEAF_RANK_XL) p->info.n_leaves_rank += cnt;
+                else if (b == LEAF_RANK || b == LEAF_RANK_L || b == LEAF_RANK_XL || b == LEAF_RANK_T)
+                    p->info.n_leaves_rank += cnt;
                 else p->info.n_leaves_hash += cnt;
             }
             add_bytes(p, GMAGNUS_K_CHUNK_SYM, (lv.set.col16 ? 2.0 : 4.0) * lv.elems + 16.0 * nl);
