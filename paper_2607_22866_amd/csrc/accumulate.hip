@@ -293,11 +293,16 @@ GM_DEV int hash_bin_sym(int64_t n) {
 GM_DEV int hash_bin_num(int64_t nnz) {
     return nnz <= HN_CAP[0] ? 0 : nnz <= HN_CAP[1] ? 1 : nnz <= HN_CAP[2] ? 2 : 3;
 }
-// Numeric light rows: the two small bins hash (by distinct columns); the two
-// large ones sort all products (by product count, SORT_CAP).
+// Numeric light rows: few distinct columns hash (table of HN_CAP[0]); rows of
+// at most SORT_SMALL products radix-sort them in one wave; then hashing for
+// rows with at most HN_CAP[1] distinct columns; larger rows sort all products
+// (by product count, SORT_CAP). Sorting a few hundred products with an LDS
+// radix sort (three 8-bit passes) costs far less LDS traffic than the bitonic
+// sort of the hash table's occupied slots.
+constexpr int SORT_SMALL = 512;
 constexpr int SORT_CAP[2] = {2048, 6912};
 GM_DEV int light_bin_num(int64_t nnz, int64_t ip) {
-    return nnz <= HN_CAP[0] ? 0 : nnz <= HN_CAP[1] ? 1 : ip <= SORT_CAP[0] ? 2 : 3;
+    return nnz <= HN_CAP[0] ? 0 : ip <= SORT_SMALL ? 1 : nnz <= HN_CAP[1] ? 2 : ip <= SORT_CAP[0] ? 3 : 4;
 }
 
 // Window choice for a light row: span = max column - min column + 1.
@@ -1040,13 +1045,17 @@ void light_numeric(const Csr &A, const Csr &B, int64_t r0, int bin, const int64_
         launch_items(k_light_hash_num<64, 256>, 64, n, s, A, B, r0, items, c_row_ptr, c_col, c_val, err);
         break;
     case LIGHT_H1:
-        launch_items(k_light_hash_num<64, 1024>, 64, n, s, A, B, r0, items, c_row_ptr, c_col, c_val, err);
+        launch_items(k_light_sort_num<64, SORT_SMALL>, 64, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col, c_val,
+                     err);
         break;
     case LIGHT_H2:
+        launch_items(k_light_hash_num<64, 1024>, 64, n, s, A, B, r0, items, c_row_ptr, c_col, c_val, err);
+        break;
+    case LIGHT_H3:
         launch_items(k_light_sort_num<256, SORT_CAP[0]>, 256, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col,
                      c_val, err);
         break;
-    case LIGHT_H3:
+    case LIGHT_H4:
         launch_items(k_light_sort_num<512, SORT_CAP[1]>, 512, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col,
                      c_val, err);
         break;
