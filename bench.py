@@ -76,12 +76,28 @@ def run_step(g, dA, bounds, timing, acc, c_bufs, extra_flags=0):
         nnz += n
         if info is not None:
             products += info.products_total
+            # inputs of the unfused byte model (see unfused_model_bytes)
+            m = acc.setdefault("_model", [0, 0, 0])
+            m[0] += info.products_heavy
+            m[1] += sum(info.level_elems_in[i] for i in range(1, info.levels_run))
+            m[2] += info.c_nnz_heavy
             for i, k in enumerate(g.K_NAMES):
                 acc.setdefault(k, [0.0, 0, 0.0])
                 acc[k][0] += info.kernel_ms[i]
                 acc[k][1] += info.kernel_launches[i]
                 acc[k][2] += info.kernel_bytes[i]
     return products, nnz
+
+
+def unfused_model_bytes(products_heavy, elems_deeper_levels, c_nnz_heavy):
+    """Bytes the paper's unfused sequence of heavy-row kernels moves
+    (Algorithm 3 with Algorithms 4 and 5): C-hat written once (12 B per
+    product), at every multisplit level a 4 B histogram read plus a 12 B read
+    and a 12 B write of each element entering it (the first level takes all
+    products), the final chunks' symbolic (4 B) and numeric (12 B) reads, and
+    12 B per C entry written. The fused path here skips most of these passes,
+    so this figure over its time is a work rate, not bytes it moved."""
+    return (12.0 + 28.0 + 16.0) * products_heavy + 28.0 * elems_deeper_levels + 12.0 * c_nnz_heavy
 
 
 def copy_peak(torch, nbytes=4 << 30, reps=5):
@@ -234,7 +250,7 @@ def main():
 
     kernels = {}
     for k, (ms, launches, byts) in acc.items():
-        if launches == 0 and ms == 0:
+        if k == "_model" or (launches == 0 and ms == 0):
             continue
         kernels[k] = {"ms_per_step": ms / args.steps, "launches_per_step": launches / args.steps,
                       "gb_per_step": byts / args.steps / 1e9,
@@ -261,6 +277,8 @@ def main():
     heavy_ms = sum(kernels[k]["ms_per_step"] for k in HEAVY_KERNELS if k in kernels)
     heavy_gb = sum(kernels[k]["gb_per_step"] for k in HEAVY_KERNELS if k in kernels)
     all_ms = sum(v["ms_per_step"] for v in kernels.values())
+    mh = acc.get("_model", [0, 0, 0])
+    model_gbs = (unfused_model_bytes(*mh) / args.steps / 1e9 / (heavy_ms / 1000.0)) if heavy_ms and mh[0] else None
     all_gb = sum(v["gb_per_step"] for v in kernels.values())
 
     out = {
@@ -284,6 +302,8 @@ def main():
                              "heavy_path_frac_of_copy": (heavy_gb / (heavy_ms / 1000.0)) / copy_gbs
                              if heavy_ms else None,
                              "copy_peak": copy_gbs,
+                             "unfused_model_equivalent": model_gbs,
+                             "unfused_model_frac": model_gbs / HBM_PEAK_GBS if model_gbs else None,
                              "all_kernels": all_gb / (all_ms / 1000.0) if all_ms else None,
                              "end_to_end": all_gb / (elapsed / args.steps)},
         "roofline": roofline,

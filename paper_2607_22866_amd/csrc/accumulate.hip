@@ -957,6 +957,73 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const LeafTa
     for (int q = threadIdx.x; q < m; q += BLOCK) o.c_val[dst + q] = vals[q];
 }
 
+// Symbolic of the bitmap-rank bins, one wave per chunk: the wave clears its
+// own bitmap, reads the chunk's columns with 16-byte loads (aligned blocks,
+// elements outside the chunk masked), and counts the columns whose bit it
+// set first. Waves do not wait for each other, so a CU keeps up to 32
+// chunks' loads in flight (8 with work-group-wide kernels), which is what
+// bounds these small, latency-bound chunks.
+constexpr int WSYM_U = 2;  // 16-byte blocks per lane per pass
+
+template <int NWORDS, int WAVES, typename ColT>
+__global__ __launch_bounds__(WAVES * GM_WAVE) void k_leaf_wave_sym(const ColT *col, const LeafTask *tasks,
+                                                                   int64_t n_tasks, int64_t e_end, int64_t *leaf_nnz,
+                                                                   int64_t *slot_cnt) {
+    static_assert(NWORDS % (4 * GM_WAVE) == 0, "bitmap cleared with 16-byte stores");
+    constexpr int PER = 16 / (int)sizeof(ColT);  // elements per 16-byte block
+    __shared__ __align__(16) uint32_t bits_all[WAVES][NWORDS];
+    const int lane = threadIdx.x & (GM_WAVE - 1), w = threadIdx.x / GM_WAVE;
+    const int64_t k = (int64_t)blockIdx.x * WAVES + w;
+    if (k >= n_tasks) return;  // the whole wave; no work-group barrier below
+    uint32_t *bits = bits_all[w];
+    for (int i = lane * 4; i < NWORDS; i += GM_WAVE * 4) *(uint4 *)&bits[i] = make_uint4(0u, 0u, 0u, 0u);
+    const LeafTask tk = tasks[k];
+    wave_lds_fence();
+    int fresh = 0;
+    for (int64_t b = (tk.s & ~(int64_t)(PER - 1)) + (int64_t)lane * PER; b < tk.e; b += (int64_t)GM_WAVE * PER * WSYM_U) {
+        ColT v[WSYM_U][PER];
+#pragma unroll
+        for (int u = 0; u < WSYM_U; ++u) {
+            const int64_t blk = b + (int64_t)u * GM_WAVE * PER;
+            if (blk + PER <= e_end) {
+                typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+                const u32x4 q = __builtin_nontemporal_load((const u32x4 *)(col + blk));
+                __builtin_memcpy(v[u], &q, 16);
+            } else {
+#pragma unroll
+                for (int j = 0; j < PER; ++j) v[u][j] = blk + j < tk.e ? col[blk + j] : (ColT)0;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < WSYM_U; ++u)
+#pragma unroll
+            for (int j = 0; j < PER; ++j) {
+                const int64_t t = b + (int64_t)u * GM_WAVE * PER + j;
+                if (t >= tk.s && t < tk.e) {
+                    const int32_t c = (int32_t)v[u][j];
+                    const uint32_t bit = 1u << (c & 31);
+                    if (!(atomicOr(&bits[c >> 5], bit) & bit)) ++fresh;
+                }
+            }
+    }
+    const int32_t n = wave_reduce_sum<int32_t>(fresh);
+    if (lane == 0) {
+        leaf_nnz[tk.a] = n;
+        slot_cnt[tk.t] = n;
+    }
+}
+
+template <int NWORDS, int WAVES, typename ColT>
+void launch_wave_sym(const ColT *col, const LeafTask *tasks, int64_t n, int64_t e_end, int64_t *leaf_nnz,
+                     int64_t *slot_cnt, hipStream_t s) {
+    if (n <= 0) return;
+    const int64_t blocks = (n + WAVES - 1) / WAVES;
+    GM_REQUIRE(blocks < (int64_t)1 << 31, GMAGNUS_ERROR_UNSUPPORTED, "too many work items for one launch");
+    hipLaunchKernelGGL((k_leaf_wave_sym<NWORDS, WAVES, ColT>), dim3((unsigned)blocks), dim3(WAVES * GM_WAVE), 0, s,
+                       col, tasks, n, e_end, leaf_nnz, slot_cnt);
+    GM_CHECK_LAUNCH();
+}
+
 // -------------------------------------------------------------- slot scan
 constexpr int SLOT_BLOCK = 256;
 
@@ -1079,8 +1146,20 @@ void leaf_tasks_num(const LeafSet &L, const int64_t *items, int64_t n, const int
     GM_CHECK_LAUNCH();
 }
 
-void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *items, int64_t n, int width, int64_t *leaf_nnz,
-                   int64_t *slot_cnt, hipStream_t s) {
+void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *items, int64_t n, int width, int64_t e_end,
+                   int64_t *leaf_nnz, int64_t *slot_cnt, hipStream_t s) {
+    const bool rank_bin = bin == LEAF_RANK || bin == LEAF_RANK_L || bin == LEAF_RANK_XL || bin == LEAF_RANK_T;
+    const void *colp = L.col16 ? (const void *)L.col16 : (const void *)L.col;
+    if (rank_bin && width >= 32 && width <= DENSE_MAX && ((uintptr_t)colp & 15) == 0) {
+        // narrow chunks: one wave per chunk, 16-byte column loads (for the
+        // wide light chunks of a first level, whose 16 KB bitmaps leave room
+        // for 10 waves per CU, the work-group kernels below were faster)
+        if (L.col16)
+            launch_wave_sym<DENSE_MAX / 32, 4>(L.col16, items, n, e_end, leaf_nnz, slot_cnt, s);
+        else
+            launch_wave_sym<DENSE_MAX / 32, 4>(L.col, items, n, e_end, leaf_nnz, slot_cnt, s);
+        return;
+    }
     switch (bin) {
     case LEAF_H0: launch_items(k_leaf_hash_sym<64, 2 * HS_CAP[0]>, 64, n, s, L, items, leaf_nnz, slot_cnt); break;
     case LEAF_H1: launch_items(k_leaf_hash_sym<64, 2 * HS_CAP[1]>, 64, n, s, L, items, leaf_nnz, slot_cnt); break;

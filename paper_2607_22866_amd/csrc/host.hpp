@@ -286,8 +286,9 @@ void leaf_tasks_num(const LeafSet &L, const int64_t *items, int64_t n, const int
 // leaves first (they start early instead of finishing last).
 constexpr int64_t DENSE_BIG_LEN = 32768;
 // Leaf symbolic: leaf_nnz[leaf] and slot_cnt[slot] for the n tasks of a bin.
-void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *tasks, int64_t n, int width, int64_t *leaf_nnz,
-                   int64_t *slot_cnt, hipStream_t s);
+// (e_end: end of the level's elements in the column array; column loads stay below it)
+void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *tasks, int64_t n, int width, int64_t e_end,
+                   int64_t *leaf_nnz, int64_t *slot_cnt, hipStream_t s);
 // Leaf numeric: writes C at each task's position.
 // counter: one device int32 the dense bin uses to hand out chunks.
 void leaf_numeric(const LeafSet &L, int bin, const LeafTask *tasks, int64_t n, int width, int32_t *c_col,

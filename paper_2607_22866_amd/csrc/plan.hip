@@ -893,7 +893,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                 if (b == LEAF_DENSE_BIG) continue;  // launched together with LEAF_DENSE, first
                 const int64_t b0 = b == LEAF_DENSE ? lv.bins_sym[LEAF_DENSE_BIG] : lv.bins_sym[b];
                 const int64_t cnt = lv.bins_sym[b + 1] - b0;
-                leaf_symbolic(lv.set, b, tasks + b0, cnt, lv.width, lv.leaf_nnz, p->slot, s);
+                leaf_symbolic(lv.set, b, tasks + b0, cnt, lv.width, e1, lv.leaf_nnz, p->slot, s);
                 if (cnt) p->info.kernel_launches[GMAGNUS_K_CHUNK_SYM] += 1;
                 if (b == LEAF_DENSE) p->info.n_leaves_dense += cnt;
                 else if (b == LEAF_RANK || b == LEAF_RANK_L || b == LEAF_RANK_XL || b == LEAF_RANK_T)
