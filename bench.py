@@ -81,6 +81,7 @@ def run_step(g, dA, bounds, timing, acc, c_bufs, extra_flags=0):
             m[0] += info.products_heavy
             m[1] += sum(info.level_elems_in[i] for i in range(1, info.levels_run))
             m[2] += info.c_nnz_heavy
+            acc.setdefault("_levels", set()).add(info.params.n_levels)
             for i, k in enumerate(g.K_NAMES):
                 acc.setdefault(k, [0.0, 0, 0.0])
                 acc[k][0] += info.kernel_ms[i]
@@ -249,8 +250,11 @@ def main():
     gflops = 2.0 * products / (elapsed / args.steps) / 1e9
 
     kernels = {}
-    for k, (ms, launches, byts) in acc.items():
-        if k == "_model" or (launches == 0 and ms == 0):
+    for k, rec in acc.items():
+        if k.startswith("_"):
+            continue
+        ms, launches, byts = rec
+        if launches == 0 and ms == 0:
             continue
         kernels[k] = {"ms_per_step": ms / args.steps, "launches_per_step": launches / args.steps,
                       "gb_per_step": byts / args.steps / 1e9,
@@ -261,11 +265,12 @@ def main():
     if dom:
         d = kernels[dom]
         kname = SINGLE_KERNEL_CLASSES[dom]
-        if dom == "expand" and args.paper_expansion:
-            kname = "k_expand"
+        levels = acc.get("_levels", set())
+        if dom == "expand" and (args.paper_expansion or levels == {0}):
+            kname = "k_expand"  # also the only expansion without a multisplit level
         elif dom == "expand" and args.slice_split:
             kname = "k_expand_split"
-        elif dom == "expand" and args.level_by_level:
+        elif dom == "expand" and (args.level_by_level or levels != {2}):
             kname = "k_expand_rows"
         bpl = d["gb_per_step"] * 1e9 / d["launches_per_step"]
         ms = d["ms_per_step"] / d["launches_per_step"]

@@ -446,6 +446,7 @@ GM_DEV void radix_sort_lds(uint32_t *&keys, uint16_t *&idx, uint32_t *&keys_alt,
         int rk[NB];
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
+            if (w * S + b * GM_WAVE >= n) break;  // the wave's remaining batches are empty
             const int i = w * S + b * GM_WAVE + lane;
             const bool valid = i < n;
             const uint32_t d = valid ? (keys[i] >> shift) & 255u : 0u;
@@ -483,6 +484,7 @@ GM_DEV void radix_sort_lds(uint32_t *&keys, uint16_t *&idx, uint32_t *&keys_alt,
         __syncthreads();
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
+            if (w * S + b * GM_WAVE >= n) break;
             const int i = w * S + b * GM_WAVE + lane;
             if (i < n) {
                 const uint32_t k = keys[i];
