@@ -294,15 +294,21 @@ GM_DEV int hash_bin_num(int64_t nnz) {
     return nnz <= HN_CAP[0] ? 0 : nnz <= HN_CAP[1] ? 1 : nnz <= HN_CAP[2] ? 2 : 3;
 }
 // Numeric light rows: few distinct columns hash (table of HN_CAP[0]); rows of
-// at most SORT_SMALL products radix-sort them in one wave; then hashing for
-// rows with at most HN_CAP[1] distinct columns; larger rows sort all products
-// (by product count, SORT_CAP). Sorting a few hundred products with an LDS
-// radix sort (three 8-bit passes) costs far less LDS traffic than the bitonic
-// sort of the hash table's occupied slots.
-constexpr int SORT_SMALL = 512;
+// at most SORT_SMALL[1] products sort them in one wave (with LDS sized for
+// SORT_SMALL[0] or SORT_SMALL[1] products, so the smaller rows fit more work
+// groups per CU); then hashing for rows with at most HN_CAP[1] distinct
+// columns; larger rows sort all products (by product count, SORT_CAP).
+// Sorting a few hundred products in LDS (one or three 8-bit passes) costs far
+// less LDS traffic than the bitonic sort of the hash table's occupied slots.
+constexpr int SORT_SMALL[2] = {256, 512};
 constexpr int SORT_CAP[2] = {2048, 6912};
 GM_DEV int light_bin_num(int64_t nnz, int64_t ip) {
-    return nnz <= HN_CAP[0] ? 0 : ip <= SORT_SMALL ? 1 : nnz <= HN_CAP[1] ? 2 : ip <= SORT_CAP[0] ? 3 : 4;
+    return nnz <= HN_CAP[0]        ? 0
+           : ip <= SORT_SMALL[0]   ? 1
+           : ip <= SORT_SMALL[1]   ? 2
+           : nnz <= HN_CAP[1]      ? 3
+           : ip <= SORT_CAP[0]     ? 4
+                                   : 5;
 }
 
 // Window choice for a light row: span = max column - min column + 1.
@@ -503,6 +509,120 @@ GM_DEV void radix_sort_lds(uint32_t *&keys, uint16_t *&idx, uint32_t *&keys_alt,
     }
 }
 
+// Rows of at most a few hundred products whose columns spread evenly (ER-like)
+// need one pass, not three: a stable scatter by the top 8 bits of the key
+// leaves buckets of a few elements, and each element's final place is its
+// bucket's start plus the number of smaller keys (or equal keys placed
+// earlier) in its bucket. Returns false, with keys and idx untouched, when a
+// bucket holds more than MSD_MAXB elements (the caller then radix-sorts).
+constexpr int MSD_MAXB = 16;
+
+GM_DEV int32_t wave_reduce_max(int32_t x) {
+#pragma unroll
+    for (int d = GM_WAVE / 2; d >= 1; d >>= 1) {
+        const int32_t y = __shfl_xor(x, d, GM_WAVE);
+        x = x > y ? x : y;
+    }
+    return x;
+}
+
+template <int BLOCK, int CAP>
+GM_DEV bool msd_sort_lds(uint32_t *keys, uint16_t *idx, uint32_t *keys_alt, uint16_t *idx_alt, int n, int bits,
+                         int32_t *hist, int32_t *scan_sm) {
+    constexpr int NW = BLOCK / GM_WAVE;
+    constexpr int NB = (CAP + BLOCK - 1) / BLOCK;
+    constexpr int S = NB * GM_WAVE;
+    constexpr int NH = NW * 256;
+    constexpr int HPT = NH / BLOCK;
+    const int tid = threadIdx.x, lane = tid & (GM_WAVE - 1), w = tid / GM_WAVE;
+    const uint64_t lt = lanemask_lt();
+    const int shift = bits > 8 ? bits - 8 : 0;
+    for (int i = tid; i < NH; i += BLOCK) hist[i] = 0;
+    __syncthreads();
+    int rk[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+        if (w * S + b * GM_WAVE >= n) break;
+        const int i = w * S + b * GM_WAVE + lane;
+        const bool valid = i < n;
+        const uint32_t d = valid ? (keys[i] >> shift) & 255u : 0u;
+        uint64_t peers = ballot(valid);
+#pragma unroll
+        for (int bit = 0; bit < 8; ++bit) {
+            const uint64_t m = ballot((d >> bit) & 1u);
+            peers &= ((d >> bit) & 1u) ? m : ~m;
+        }
+        const int leader = peers ? __ffsll((long long)peers) - 1 : lane;
+        int base = 0;
+        if (valid && lane == leader) {
+            base = hist[d * NW + w];
+            hist[d * NW + w] = base + __popcll(peers);
+        }
+        base = __shfl(base, leader, GM_WAVE);
+        rk[b] = base + __popcll(peers & lt);
+    }
+    __syncthreads();
+    // largest bucket
+    int big = 0;
+    for (int d = tid; d < 256; d += BLOCK) {
+        int sz = 0;
+#pragma unroll
+        for (int q = 0; q < NW; ++q) sz += hist[d * NW + q];
+        big = big > sz ? big : sz;
+    }
+    big = (int)wave_reduce_max(big);
+    if (lane == 0) scan_sm[w] = big;
+    __syncthreads();
+    big = 0;
+#pragma unroll
+    for (int q = 0; q < NW; ++q) big = big > scan_sm[q] ? big : scan_sm[q];
+    __syncthreads();
+    if (big > MSD_MAXB) return false;  // uniform across the work group
+    // stable scatter by bucket into the alternate buffers
+    {
+        int32_t v[HPT], sum = 0;
+#pragma unroll
+        for (int j = 0; j < HPT; ++j) {
+            v[j] = hist[tid * HPT + j];
+            sum += v[j];
+        }
+        int32_t run = block_excl_scan<BLOCK>(sum, scan_sm);
+#pragma unroll
+        for (int j = 0; j < HPT; ++j) {
+            hist[tid * HPT + j] = run;
+            run += v[j];
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+        if (w * S + b * GM_WAVE >= n) break;
+        const int i = w * S + b * GM_WAVE + lane;
+        if (i < n) {
+            const uint32_t k = keys[i];
+            const int pos = hist[((k >> shift) & 255u) * NW + w] + rk[b];
+            keys_alt[pos] = k;
+            idx_alt[pos] = idx[i];
+        }
+    }
+    __syncthreads();
+    // place inside the bucket, back into keys/idx
+    for (int p = tid; p < n; p += BLOCK) {
+        const uint32_t k = keys_alt[p];
+        const uint32_t d = (k >> shift) & 255u;
+        const int b0 = hist[d * NW], b1 = d < 255 ? hist[(d + 1) * NW] : n;
+        int r = b0;
+        for (int q = b0; q < b1; ++q) {
+            const uint32_t kq = keys_alt[q];
+            r += (kq < k || (kq == k && q < p)) ? 1 : 0;
+        }
+        keys[r] = k;
+        idx[r] = idx_alt[p];
+    }
+    __syncthreads();
+    return true;
+}
+
 template <int BLOCK, int CAP>
 struct SortLds {
     uint32_t keys[2][CAP];
@@ -581,7 +701,8 @@ __global__ __launch_bounds__(BLOCK) void k_light_sort_num(Csr A, Csr B, int64_t 
     const int bits = span == 0 ? 0 : 32 - __clz((int)span);
     uint32_t *keys = L.keys[0], *keys_alt = L.keys[1];
     uint16_t *idx = L.idx[0], *idx_alt = L.idx[1];
-    radix_sort_lds<BLOCK, CAP>(keys, idx, keys_alt, idx_alt, n, bits, L.hist, L.scan);
+    if (CAP > 512 || !msd_sort_lds<BLOCK, CAP>(keys, idx, keys_alt, idx_alt, n, bits, L.hist, L.scan))
+        radix_sort_lds<BLOCK, CAP>(keys, idx, keys_alt, idx_alt, n, bits, L.hist, L.scan);
     // runs of equal columns: heads counted per thread over a contiguous
     // range, their output positions kept in the free index buffer, then the
     // heads are written with consecutive lanes on consecutive positions
@@ -1114,17 +1235,21 @@ void light_numeric(const Csr &A, const Csr &B, int64_t r0, int bin, const int64_
         launch_items(k_light_hash_num<64, 256>, 64, n, s, A, B, r0, items, c_row_ptr, c_col, c_val, err);
         break;
     case LIGHT_H1:
-        launch_items(k_light_sort_num<64, SORT_SMALL>, 64, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col, c_val,
-                     err);
+        launch_items(k_light_sort_num<64, SORT_SMALL[0]>, 64, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col,
+                     c_val, err);
         break;
     case LIGHT_H2:
-        launch_items(k_light_hash_num<64, 1024>, 64, n, s, A, B, r0, items, c_row_ptr, c_col, c_val, err);
+        launch_items(k_light_sort_num<64, SORT_SMALL[1]>, 64, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col,
+                     c_val, err);
         break;
     case LIGHT_H3:
+        launch_items(k_light_hash_num<64, 1024>, 64, n, s, A, B, r0, items, c_row_ptr, c_col, c_val, err);
+        break;
+    case LIGHT_H4:
         launch_items(k_light_sort_num<256, SORT_CAP[0]>, 256, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col,
                      c_val, err);
         break;
-    case LIGHT_H4:
+    case LIGHT_H5:
         launch_items(k_light_sort_num<512, SORT_CAP[1]>, 512, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col,
                      c_val, err);
         break;
