@@ -637,6 +637,48 @@ struct SortLds {
 
 constexpr int SORT_ILP = 4;
 
+// Writes the sums of the runs of equal keys of a sorted (keys, idx) array in
+// key order: heads counted per thread over a contiguous range, their output
+// positions kept in idx_free, then each head sums its run into out_val at its
+// position (consecutive lanes on consecutive positions) and writes
+// key + base_col to out_col. Sets err_bit in *err when the run count differs
+// from nnz (the symbolic count).
+template <int BLOCK, int CAP>
+GM_DEV void sorted_runs_emit(const uint32_t *keys, const uint16_t *idx, uint16_t *idx_free, const double *vals, int n,
+                             int64_t nnz, int32_t base_col, int32_t *out_col, double *out_val, int32_t *err,
+                             int err_bit, int32_t *scan_sm) {
+    const int tid = threadIdx.x;
+    constexpr int PT = (CAP + BLOCK - 1) / BLOCK;
+    const int p0 = tid * PT;
+    int32_t cnt = 0;
+#pragma unroll
+    for (int j = 0; j < PT; ++j) {
+        const int p = p0 + j;
+        if (p < n && (p == 0 || keys[p] != keys[p - 1])) ++cnt;
+    }
+    int32_t total;
+    int32_t pos = block_excl_scan<BLOCK>(cnt, scan_sm, &total);
+#pragma unroll
+    for (int j = 0; j < PT; ++j) {
+        const int p = p0 + j;
+        if (p < n && (p == 0 || keys[p] != keys[p - 1])) idx_free[p] = (uint16_t)pos++;
+    }
+    __syncthreads();
+    if (tid == 0 && total != nnz) atomicOr(err, err_bit);
+    for (int p = tid; p < n; p += BLOCK) {
+        const uint32_t k = keys[p];
+        if (p == 0 || k != keys[p - 1]) {
+            const int o = idx_free[p];
+            double sum = vals[idx[p]];
+            for (int q = p + 1; q < n && keys[q] == k; ++q) sum += vals[idx[q]];
+            if (o < nnz) {
+                out_col[o] = (int32_t)k + base_col;
+                out_val[o] = sum;
+            }
+        }
+    }
+}
+
 template <int BLOCK, int CAP>
 __global__ __launch_bounds__(BLOCK) void k_light_sort_num(Csr A, Csr B, int64_t r0, const int64_t *items,
                                                           const int32_t *minc, const int32_t *maxc,
@@ -703,38 +745,8 @@ __global__ __launch_bounds__(BLOCK) void k_light_sort_num(Csr A, Csr B, int64_t 
     uint16_t *idx = L.idx[0], *idx_alt = L.idx[1];
     if (CAP > 512 || !msd_sort_lds<BLOCK, CAP>(keys, idx, keys_alt, idx_alt, n, bits, L.hist, L.scan))
         radix_sort_lds<BLOCK, CAP>(keys, idx, keys_alt, idx_alt, n, bits, L.hist, L.scan);
-    // runs of equal columns: heads counted per thread over a contiguous
-    // range, their output positions kept in the free index buffer, then the
-    // heads are written with consecutive lanes on consecutive positions
-    constexpr int PT = (CAP + BLOCK - 1) / BLOCK;
-    const int p0 = tid * PT;
-    int32_t cnt = 0;
-#pragma unroll
-    for (int j = 0; j < PT; ++j) {
-        const int p = p0 + j;
-        if (p < n && (p == 0 || keys[p] != keys[p - 1])) ++cnt;
-    }
-    int32_t total;
-    int32_t pos = block_excl_scan<BLOCK>(cnt, L.scan, &total);
-#pragma unroll
-    for (int j = 0; j < PT; ++j) {
-        const int p = p0 + j;
-        if (p < n && (p == 0 || keys[p] != keys[p - 1])) idx_alt[p] = (uint16_t)pos++;
-    }
-    __syncthreads();
-    if (tid == 0 && total != nnz) atomicOr(err, 1);
-    for (int p = tid; p < n; p += BLOCK) {
-        const uint32_t k = keys[p];
-        if (p == 0 || k != keys[p - 1]) {
-            const int o = idx_alt[p];
-            double sum = L.vals[idx[p]];
-            for (int q = p + 1; q < n && keys[q] == k; ++q) sum += L.vals[idx[q]];
-            if (o < nnz) {
-                c_col[dst + o] = (int32_t)k + base_col;
-                c_val[dst + o] = sum;
-            }
-        }
-    }
+    sorted_runs_emit<BLOCK, CAP>(keys, idx, idx_alt, L.vals, n, nnz, base_col, c_col + dst, c_val + dst, err, 1,
+                                 L.scan);
 }
 
 template <int BLOCK, int WMAX>
@@ -1080,6 +1092,37 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const LeafTa
     for (int q = threadIdx.x; q < m; q += BLOCK) o.c_val[dst + q] = vals[q];
 }
 
+// Small wide chunks (fewer than RANK_MIN_LEN elements, columns too wide for
+// a cheap bitmap): the chunk's elements are sorted in LDS by column (one
+// bucket pass when they spread evenly, else an LSD radix sort) and the runs
+// summed, instead of a hash table followed by a bitonic sort of all its slots.
+template <int BLOCK, int CAP>
+__global__ __launch_bounds__(BLOCK) void k_leaf_sort_num(LeafSet L, const LeafTask *tasks, int width, LeafOut o) {
+    static_assert(CAP < 65536, "16-bit element indices");
+    __shared__ SortLds<BLOCK, CAP> S;
+    const int tid = threadIdx.x;
+    const LeafTask tk = tasks[blockIdx.x];
+    const int64_t len = tk.e - tk.s;
+    if (len > CAP) {  // cannot happen for the chunks of this bin (fewer than RANK_MIN_LEN elements)
+        if (tid == 0) atomicOr(o.err, 4);
+        return;
+    }
+    const int n = (int)len;
+    for (int i = tid; i < n; i += BLOCK) {
+        S.keys[0][i] = (uint32_t)leaf_col_nt(L, tk.s + i);
+        S.vals[i] = __builtin_nontemporal_load(&L.val[tk.s + i]);
+        S.idx[0][i] = (uint16_t)i;
+    }
+    __syncthreads();
+    const int bits = width <= 1 ? 0 : 32 - __clz(width - 1);
+    uint32_t *keys = S.keys[0], *keys_alt = S.keys[1];
+    uint16_t *idx = S.idx[0], *idx_alt = S.idx[1];
+    if (!msd_sort_lds<BLOCK, CAP>(keys, idx, keys_alt, idx_alt, n, bits, S.hist, S.scan))
+        radix_sort_lds<BLOCK, CAP>(keys, idx, keys_alt, idx_alt, n, bits, S.hist, S.scan);
+    sorted_runs_emit<BLOCK, CAP>(keys, idx, idx_alt, S.vals, n, tk.a, tk.b, o.c_col + tk.t, o.c_val + tk.t, o.err, 4,
+                                 S.scan);
+}
+
 // Symbolic of the bitmap-rank bins, one wave per chunk: the wave clears its
 // own bitmap, reads the chunk's columns with 16-byte loads (aligned blocks,
 // elements outside the chunk masked), and counts the columns whose bit it
@@ -1337,8 +1380,16 @@ void leaf_numeric(const LeafSet &L, int bin, const LeafTask *items, int64_t n, i
                   double *c_val, int32_t *err, int32_t *counter, hipStream_t s) {
     LeafOut o{0, nullptr, nullptr, nullptr, 0, c_col, c_val, err};
     switch (bin) {
-    case LEAF_H0: launch_items(k_leaf_hash_num<64, 256>, 64, n, s, L, items, o); break;
-    case LEAF_H1: launch_items(k_leaf_hash_num<64, 1024>, 64, n, s, L, items, o); break;
+    case LEAF_H0:
+    case LEAF_H1:
+        // bitmap-rank-wide levels send only chunks of fewer than RANK_MIN_LEN elements here
+        if (width <= (1 << RANK_MAX_LOG2))
+            launch_items(k_leaf_sort_num<64, RANK_MIN_LEN>, 64, n, s, L, items, width, o);
+        else if (bin == LEAF_H0)
+            launch_items(k_leaf_hash_num<64, 256>, 64, n, s, L, items, o);
+        else
+            launch_items(k_leaf_hash_num<64, 1024>, 64, n, s, L, items, o);
+        break;
     case LEAF_H2: launch_items(k_leaf_hash_num<256, 4096>, 256, n, s, L, items, o); break;
     case LEAF_H3: launch_items(k_leaf_hash_num<512, 8192>, 512, n, s, L, items, o); break;
     case LEAF_DENSE:

@@ -103,7 +103,8 @@ void fill(T *p, T v, int64_t n, hipStream_t s) {
 }
 
 // ----------------------------------------------------------------- setup.hip
-// Fills ip/minc/maxc for rows [r0, r1) of A (local index r - r0).
+// Fills ip/minc/maxc for rows [r0, r1) of A (local index r - r0); with minc
+// and maxc null only ip (no reads of B's columns).
 void row_products(const Csr &A, const Csr &B, int64_t r0, int64_t r1, int64_t panel_nnz, int64_t *ip, int32_t *minc,
                   int32_t *maxc, hipStream_t s);
 // Checks canonical CSR; sets *flag (device int32) to nonzero on violation.

@@ -1182,9 +1182,7 @@ gmagnus_status_t gmagnus_row_products(const gmagnus_csr_t *A, const gmagnus_csr_
         GM_REQUIRE(ip != nullptr || A->n_rows == 0, GMAGNUS_ERROR_INVALID_VALUE, "NULL ip");
         if (A->n_rows == 0) return;
         hipStream_t s = (hipStream_t)hip_stream;
-        Workspace ws(nullptr, s);
-        int32_t *mn = ws.alloc<int32_t>(A->n_rows), *mx = ws.alloc<int32_t>(A->n_rows);
-        row_products(to_csr(A), to_csr(B), 0, A->n_rows, A->nnz, ip, mn, mx, s);
+        row_products(to_csr(A), to_csr(B), 0, A->n_rows, A->nnz, ip, nullptr, nullptr, s);
         GM_HIP(hipStreamSynchronize(s));
     });
 }
@@ -1204,8 +1202,7 @@ gmagnus_status_t gmagnus_split_panels(const gmagnus_csr_t *A, const gmagnus_csr_
             Workspace ws(nullptr, s);
             int64_t *ip = ws.alloc<int64_t>(n), *sc = ws.alloc<int64_t>(n + 1);
             int64_t *scratch = ws.alloc<int64_t>(scan_scratch_elems(n));
-            int32_t *mn = ws.alloc<int32_t>(n), *mx = ws.alloc<int32_t>(n);
-            row_products(to_csr(A), to_csr(B), 0, n, A->nnz, ip, mn, mx, s);
+            row_products(to_csr(A), to_csr(B), 0, n, A->nnz, ip, nullptr, nullptr, s);
             scan_i64(ip, n, sc, scratch, s);
             GM_HIP(hipMemcpyAsync(pre.data(), sc, sizeof(int64_t) * (n + 1), hipMemcpyDeviceToHost, s));
             GM_HIP(hipStreamSynchronize(s));

@@ -14,7 +14,9 @@ constexpr int FLAT_ITEMS = 8;  // consecutive entries per thread
 // nonzeros of A, adding nnz(B[k,:]) to its current row and tracking the
 // smallest first column and largest last column of the B rows it touches
 // (the row's column span, used to pick a dense window for light rows).
-// A row split across threads is merged with atomics.
+// A row split across threads is merged with atomics. Without SPAN only the
+// counts are taken (one B.rp pair per entry, no reads of B's columns).
+template <bool SPAN>
 __global__ __launch_bounds__(FLAT_BLOCK) void k_row_products(Csr A, Csr B, int64_t r0, int64_t r1, int64_t *ip,
                                                              int32_t *minc, int32_t *maxc) {
     const int64_t e_begin = A.rp[r0], e_end = A.rp[r1];
@@ -28,7 +30,7 @@ __global__ __launch_bounds__(FLAT_BLOCK) void k_row_products(Csr A, Csr B, int64
     for (int64_t e = e0; e < e1; ++e) {
         while (e >= row_end) {  // flush and move to the next nonempty row
             if (acc) atomicAdd((unsigned long long *)&ip[row - r0], (unsigned long long)acc);
-            if (hi >= 0) {
+            if (SPAN && hi >= 0) {
                 atomicMin(&minc[row - r0], lo);
                 atomicMax(&maxc[row - r0], hi);
             }
@@ -42,13 +44,15 @@ __global__ __launch_bounds__(FLAT_BLOCK) void k_row_products(Csr A, Csr B, int64
         const int64_t b0 = B.rp[k], b1 = B.rp[k + 1];
         if (b1 > b0) {
             acc += b1 - b0;
-            const int32_t f = B.ci[b0], l = B.ci[b1 - 1];
-            lo = f < lo ? f : lo;
-            hi = l > hi ? l : hi;
+            if (SPAN) {
+                const int32_t f = B.ci[b0], l = B.ci[b1 - 1];
+                lo = f < lo ? f : lo;
+                hi = l > hi ? l : hi;
+            }
         }
     }
     if (acc) atomicAdd((unsigned long long *)&ip[row - r0], (unsigned long long)acc);
-    if (hi >= 0) {
+    if (SPAN && hi >= 0) {
         atomicMin(&minc[row - r0], lo);
         atomicMax(&maxc[row - r0], hi);
     }
@@ -253,11 +257,17 @@ void row_products(const Csr &A, const Csr &B, int64_t r0, int64_t r1, int64_t pa
     const int64_t n = r1 - r0;
     if (n <= 0) return;
     fill<int64_t>(ip, 0, n, s);
-    fill<int32_t>(minc, INT32_MAX, n, s);
-    fill<int32_t>(maxc, -1, n, s);
+    if (minc) {
+        fill<int32_t>(minc, INT32_MAX, n, s);
+        fill<int32_t>(maxc, -1, n, s);
+    }
     if (panel_nnz <= 0) return;
-    hipLaunchKernelGGL(k_row_products, dim3(flat_grid(panel_nnz)), dim3(FLAT_BLOCK), 0, s, A, B, r0, r1, ip, minc,
-                       maxc);
+    if (minc)
+        hipLaunchKernelGGL(k_row_products<true>, dim3(flat_grid(panel_nnz)), dim3(FLAT_BLOCK), 0, s, A, B, r0, r1, ip,
+                           minc, maxc);
+    else
+        hipLaunchKernelGGL(k_row_products<false>, dim3(flat_grid(panel_nnz)), dim3(FLAT_BLOCK), 0, s, A, B, r0, r1,
+                           ip, minc, maxc);
     GM_CHECK_LAUNCH();
 }
 
