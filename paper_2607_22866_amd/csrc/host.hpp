@@ -197,8 +197,8 @@ void expand_rows(const Csr &B, const RowEntries &ent, const uint32_t *pre, const
 int64_t fine_bounds_words(int64_t n_slices, int nf);
 void fine_bounds(const Csr &B, const int32_t *slice_k, int64_t n_slices, int nf, int fshift, int32_t *bndf,
                  hipStream_t s);
-void fine_counts(const RowEntries &ent, int64_t n_ent, const int32_t *bndf, int nf, int64_t n_heavy, int64_t *F,
-                 hipStream_t s);
+void fine_counts(const Csr &B, const RowEntries &ent, int64_t n_ent, const int32_t *bndf, int nf, int fshift,
+                 int64_t n_heavy, int64_t *F, hipStream_t s);
 void level1_counts(const int64_t *perm, int64_t n_regions, int64_t n_heavy, const int64_t *F, int nf, int nc1,
                    int64_t *counts1, hipStream_t s);
 // whether the fused second level's keys fit the work group

@@ -394,9 +394,12 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows(RsArgs a) {
 // faster with nontemporal stores).
 
 // Fine boundaries: bndf[s * (nf + 1) + f] = offset in B[k,:] of the first
-// column >= f << fshift (f = 0..nf). One wave per slice; a row of at most 64
-// elements is searched in registers (lane i holds element i), a longer one
-// by binary search in memory.
+// column >= f << fshift (f = 0..nf), for the slices whose B row is longer
+// than FB_SHORT (the fine counts read the columns of the shorter rows
+// instead: at most FB_SHORT reads against nf + 1). One wave per slice, binary
+// search per boundary.
+constexpr int FB_SHORT = 64;
+
 __global__ __launch_bounds__(256) void k_fine_bounds(Csr B, const int32_t *slice_k, int64_t n_slices, int nf,
                                                      int fshift, int32_t *bndf) {
     const int lane = threadIdx.x & (GM_WAVE - 1);
@@ -404,82 +407,97 @@ __global__ __launch_bounds__(256) void k_fine_bounds(Csr B, const int32_t *slice
     for (int64_t s = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / GM_WAVE; s < n_slices; s += nwaves) {
         const int32_t k = slice_k[s];
         const int64_t b0 = B.rp[k], len = B.rp[k + 1] - b0;
+        if (len <= FB_SHORT) continue;
         int32_t *out = bndf + s * (nf + 1);
-        if (len <= GM_WAVE) {
-            // fine chunk of element `lane`, padded past the row's end; every lane
-            // runs every shuffle (uniform trip counts, fixed-step search)
-            const int32_t fl = lane < len ? (B.ci[b0 + lane] >> fshift) : INT32_MAX;
-            for (int fb = 0; fb <= nf; fb += GM_WAVE) {
-                const int f = fb + lane;
-                // number of lanes whose chunk is below f (chunks ascend over lanes)
-                int pos = 0;
-#pragma unroll
-                for (int step = GM_WAVE / 2; step >= 1; step >>= 1)
-                    if (__shfl(fl, pos + step - 1, GM_WAVE) < f) pos += step;
-                if (__shfl(fl, pos, GM_WAVE) < f) ++pos;
-                if (f <= nf) out[f] = pos < len ? pos : (int32_t)len;
+        for (int f = lane; f <= nf; f += GM_WAVE) {
+            int64_t lo = b0, hi = b0 + len;
+            const int64_t bound = (int64_t)f << fshift;
+            while (lo < hi) {
+                const int64_t mid = lo + ((hi - lo) >> 1);
+                if ((int64_t)B.ci[mid] < bound)
+                    lo = mid + 1;
+                else
+                    hi = mid;
             }
-        } else {
-            for (int f = lane; f <= nf; f += GM_WAVE) {
-                int64_t lo = b0, hi = b0 + len;
-                const int64_t bound = (int64_t)f << fshift;
-                while (lo < hi) {
-                    const int64_t mid = lo + ((hi - lo) >> 1);
-                    if ((int64_t)B.ci[mid] < bound)
-                        lo = mid + 1;
-                    else
-                        hi = mid;
-                }
-                out[f] = (int32_t)(lo - b0);
-            }
+            out[f] = (int32_t)(lo - b0);
         }
     }
 }
 
 // F[h * nf + f] += fine chunk f's products of heavy row h: each work group
 // takes FC_ENTRIES consecutive row-ordered entries, thread t owns the fine
-// chunks t, t + FC_BLOCK, ..., and a row's partial sums are flushed with one
-// atomic per nonzero counter when the row changes.
+// chunks t, t + FC_BLOCK, ... for entries with long B rows (sizes from the
+// fine boundaries), the first wave histograms the columns of short B rows in
+// LDS, and a row's counts are flushed with one atomic per nonzero counter
+// when the row changes.
 constexpr int FC_BLOCK = 256, FC_ENTRIES = 256, FC_MAXF = 1024;
 
-__global__ __launch_bounds__(FC_BLOCK) void k_fine_counts(RowEntries ent, int64_t n_ent, const int32_t *bndf, int nf,
-                                                          int64_t *F) {
+__global__ __launch_bounds__(FC_BLOCK) void k_fine_counts(Csr B, RowEntries ent, int64_t n_ent, const int32_t *bndf,
+                                                          int nf, int fshift, int64_t *F) {
     constexpr int FPT = FC_MAXF / FC_BLOCK;
-    __shared__ int32_t es[FC_ENTRIES], eh[FC_ENTRIES];
+    __shared__ int32_t es[FC_ENTRIES], eh[FC_ENTRIES], el[FC_ENTRIES];
+    __shared__ int64_t eb[FC_ENTRIES];
+    __shared__ int32_t sh[FC_MAXF];  // the current row's counts from short B rows
+    const int tid = threadIdx.x, lane = tid & (GM_WAVE - 1);
     const int64_t e0 = blockIdx.x * (int64_t)FC_ENTRIES;
     const int ne = (int)(n_ent - e0 < FC_ENTRIES ? n_ent - e0 : FC_ENTRIES);
-    if (threadIdx.x < ne) {
-        es[threadIdx.x] = ent.s[e0 + threadIdx.x];
-        eh[threadIdx.x] = ent.h[e0 + threadIdx.x];
+    if (tid < ne) {
+        const int32_t sl = ent.s[e0 + tid];
+        es[tid] = sl;
+        eh[tid] = ent.h[e0 + tid];
+        int64_t b0 = 0, len = 0;
+        if (sl >= 0) {
+            const int32_t k = ent.k[e0 + tid];
+            b0 = B.rp[k];
+            len = B.rp[k + 1] - b0;
+        }
+        eb[tid] = b0;
+        el[tid] = (int32_t)(len < INT32_MAX ? len : INT32_MAX);
     }
+    for (int f = tid; f < FC_MAXF; f += FC_BLOCK) sh[f] = 0;
     __syncthreads();
     int64_t acc[FPT];
 #pragma unroll
     for (int j = 0; j < FPT; ++j) acc[j] = 0;
     int32_t cur = eh[0];
-    for (int i = 0; i < ne; ++i) {
-        const int32_t h = eh[i], sl = es[i];
-        if (h != cur) {
+    for (int i = 0; i <= ne; ++i) {
+        const int32_t h = i < ne ? eh[i] : -1;
+        if (h != cur) {  // uniform: flush the row's counts
+            __syncthreads();
 #pragma unroll
             for (int j = 0; j < FPT; ++j) {
-                const int f = threadIdx.x + j * FC_BLOCK;
-                if (f < nf && acc[j]) atomicAdd((unsigned long long *)&F[(int64_t)cur * nf + f], (unsigned long long)acc[j]);
+                const int f = tid + j * FC_BLOCK;
+                if (f < nf) {
+                    const int64_t v = acc[j] + sh[f];
+                    if (v) atomicAdd((unsigned long long *)&F[(int64_t)cur * nf + f], (unsigned long long)v);
+                    sh[f] = 0;
+                }
                 acc[j] = 0;
             }
+            __syncthreads();
             cur = h;
         }
-        if (sl < 0) continue;
-        const int32_t *bq = bndf + (int64_t)sl * (nf + 1);
+        if (i == ne) break;
+        const int32_t sl = es[i], len = el[i];
+        if (sl < 0 || len == 0) continue;
+        if (len > FB_SHORT) {
+            const int32_t *bq = bndf + (int64_t)sl * (nf + 1);
 #pragma unroll
-        for (int j = 0; j < FPT; ++j) {
-            const int f = threadIdx.x + j * FC_BLOCK;
-            if (f < nf) acc[j] += bq[f + 1] - bq[f];
+            for (int j = 0; j < FPT; ++j) {
+                const int f = tid + j * FC_BLOCK;
+                if (f < nf) acc[j] += bq[f + 1] - bq[f];
+            }
+        } else if (tid < GM_WAVE) {
+            // one lane per element; a run of equal chunks adds its length once
+            const int f = lane < len ? (B.ci[eb[i] + lane] >> fshift) : -1;
+            const int fp = prev_lane(f, -2);
+            const uint64_t starts = ballot(f >= 0 && f != fp);
+            if (f >= 0 && ((starts >> lane) & 1)) {
+                const uint64_t above = starts & ~((lanemask_lt() << 1) | 1ull);
+                const int end = above ? __ffsll((long long)above) - 1 : (len < GM_WAVE ? len : GM_WAVE);
+                atomicAdd(&sh[f], end - lane);
+            }
         }
-    }
-#pragma unroll
-    for (int j = 0; j < FPT; ++j) {
-        const int f = threadIdx.x + j * FC_BLOCK;
-        if (f < nf && acc[j]) atomicAdd((unsigned long long *)&F[(int64_t)cur * nf + f], (unsigned long long)acc[j]);
     }
 }
 
@@ -810,14 +828,14 @@ void fine_bounds(const Csr &B, const int32_t *slice_k, int64_t n_slices, int nf,
     GM_CHECK_LAUNCH();
 }
 
-void fine_counts(const RowEntries &ent, int64_t n_ent, const int32_t *bndf, int nf, int64_t n_heavy, int64_t *F,
-                 hipStream_t s) {
+void fine_counts(const Csr &B, const RowEntries &ent, int64_t n_ent, const int32_t *bndf, int nf, int fshift,
+                 int64_t n_heavy, int64_t *F, hipStream_t s) {
     fill<int64_t>(F, 0, n_heavy * nf, s);
     if (n_ent <= 0) return;
     GM_REQUIRE(nf >= 1 && nf <= FC_MAXF, GMAGNUS_ERROR_UNSUPPORTED, "fine counts: too many fine chunks");
     const int64_t blocks = (n_ent + FC_ENTRIES - 1) / FC_ENTRIES;
     GM_REQUIRE(blocks < (int64_t)1 << 31, GMAGNUS_ERROR_UNSUPPORTED, "fine counts: too many entries");
-    hipLaunchKernelGGL(k_fine_counts, dim3((unsigned)blocks), dim3(FC_BLOCK), 0, s, ent, n_ent, bndf, nf, F);
+    hipLaunchKernelGGL(k_fine_counts, dim3((unsigned)blocks), dim3(FC_BLOCK), 0, s, B, ent, n_ent, bndf, nf, fshift, F);
     GM_CHECK_LAUNCH();
 }
 
