@@ -345,7 +345,8 @@ constexpr int DENSE_MAX = 8192;          // columns of the LDS dense accumulator
 constexpr int RANK_MAX_LOG2 = 18;        // columns of the bitmap-rank accumulator
 constexpr int RANK_NNZ_MAX = 6912;       // distinct columns it holds (>= tau; two work groups per CU at 2^17 columns)
 constexpr int RANK_MIN_LEN = 256;        // smaller chunks go to the hash map
-constexpr int RANK_SMALL = 2048;         // distinct columns of the small rank variant
+constexpr int RANK_SMALL = 1792;         // distinct columns of the small wide rank variant (its LDS
+                                         // stays under 32 KB: five work groups per CU)
 constexpr int RANK_NARROW_CAP = 4096;    // chunks of at most DENSE_MAX columns and at most this many elements use
                                          // a rank accumulator (one work group per chunk, LDS sized by the chunk)
 constexpr int RANK_NARROW_SMALL = 512;   // ... its small shape up to this many
@@ -976,6 +977,10 @@ __global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(8))) void
 constexpr int RANK_BLOCK = 512;
 constexpr int RANK_EPT = 16;  // RANK_BLOCK * RANK_EPT >= tau_limit()
 constexpr int RANK_WBLOCK = 256, RANK_WEPT = 4;  // the small wide shape
+constexpr int RANK_LBLOCK = 256, RANK_LWEPT = 27;  // wide numeric, at most RANK_SMALL columns: 4 waves and
+                                                   // under 32 KB of LDS, so five work groups share a CU
+static_assert(RANK_LBLOCK * RANK_LWEPT >= SORT_CAP[1] && RANK_BLOCK * RANK_EPT >= SORT_CAP[1],
+              "the wide shapes hold a light chunk of up to the largest tau");
 static_assert(RANK_WBLOCK * RANK_WEPT >= RANK_WIDE_SMALL, "the small wide shape holds its chunks");
 constexpr int RANK_SBLOCK = 256, RANK_SWORDS = 256, RANK_SCAP = 512, RANK_SEPT = 2, RANK_LEPT = 8;
 static_assert(RANK_SBLOCK * RANK_SEPT >= RANK_NARROW_SMALL && RANK_SCAP >= RANK_NARROW_SMALL,
@@ -1043,11 +1048,16 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_rank_sym(LeafSet L, const LeafTa
     }
 }
 
+// Wide bitmaps keep one rank per group of 8 words instead of one per word
+// (a sixteenth of the LDS; an element reads its group's 8 words), so more
+// work groups fit a CU.
 template <int BLOCK, int NWORDS, int CAP, int EPT>
 __global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const LeafTask *tasks, int width, LeafOut o) {
-    constexpr int WPT = (NWORDS + BLOCK - 1) / BLOCK;  // bitmap words per thread in the rank scan
-    __shared__ uint32_t bits[NWORDS];
-    __shared__ uint16_t wpre[NWORDS];  // rank of each word's first set bit (ranks < CAP <= 65535)
+    constexpr bool GROUPED = NWORDS >= 1024;
+    constexpr int NPRE = GROUPED ? NWORDS / 8 : NWORDS;
+    constexpr int WPT = (NPRE + BLOCK - 1) / BLOCK;  // rank entries per thread in the scan
+    __shared__ __align__(16) uint32_t bits[NWORDS];
+    __shared__ uint16_t wpre[NPRE];  // rank of each word's (group's) first set bit (ranks < CAP <= 65535)
     __shared__ double vals[CAP];
     __shared__ int32_t scan_sm[BLOCK / GM_WAVE];
     __shared__ int32_t count;
@@ -1063,19 +1073,32 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const LeafTa
     const int n = total < CAP ? total : CAP;
     const int m = n < nnz ? n : (int)nnz;
     if (threadIdx.x == 0 && (total != nnz || total > CAP)) atomicOr(o.err, 4);
-    // word ranks: thread t owns words [t*WPT, t*WPT + WPT)
+    // word (group) ranks: thread t owns entries [t*WPT, t*WPT + WPT)
     {
+        const int npre = GROUPED ? nwords / 8 : nwords;
         const int w0 = threadIdx.x * WPT;
-        int32_t sum = 0;
+        int32_t cnt[WPT], sum = 0;
 #pragma unroll
-        for (int j = 0; j < WPT; ++j)
-            if (w0 + j < nwords) sum += __popc(bits[w0 + j]);
+        for (int j = 0; j < WPT; ++j) {
+            cnt[j] = 0;
+            if (w0 + j < npre) {
+                if (GROUPED) {
+                    const uint4 a = *(const uint4 *)&bits[(w0 + j) * 8];
+                    const uint4 b = *(const uint4 *)&bits[(w0 + j) * 8 + 4];
+                    cnt[j] = __popc(a.x) + __popc(a.y) + __popc(a.z) + __popc(a.w) + __popc(b.x) + __popc(b.y) +
+                             __popc(b.z) + __popc(b.w);
+                } else {
+                    cnt[j] = __popc(bits[w0 + j]);
+                }
+            }
+            sum += cnt[j];
+        }
         int32_t r = block_excl_scan<BLOCK>(sum, scan_sm);
 #pragma unroll
         for (int j = 0; j < WPT; ++j)
-            if (w0 + j < nwords) {
+            if (w0 + j < npre) {
                 wpre[w0 + j] = (uint16_t)(r < 65535 ? r : 65535);
-                r += __popc(bits[w0 + j]);
+                r += cnt[j];
             }
     }
     for (int q = threadIdx.x; q < n; q += BLOCK) vals[q] = 0.0;
@@ -1084,7 +1107,19 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const LeafTa
     for (int q = 0; q < EPT; ++q)
         if (c[q] >= 0) {
             const int w = c[q] >> 5;
-            const int rk = wpre[w] + __popc(bits[w] & ((1u << (c[q] & 31)) - 1u));
+            int rk;
+            if (GROUPED) {
+                const int g = w >> 3, j0 = w & 7;
+                const uint4 a = *(const uint4 *)&bits[g * 8];
+                const uint4 b = *(const uint4 *)&bits[g * 8 + 4];
+                const uint32_t ws[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+                rk = wpre[g];
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    rk += __popc(ws[j] & (j < j0 ? ~0u : j == j0 ? (1u << (c[q] & 31)) - 1u : 0u));
+            } else {
+                rk = wpre[w] + __popc(bits[w] & ((1u << (c[q] & 31)) - 1u));
+            }
             if (rk < n) __hip_atomic_fetch_add(&vals[rk], v[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
             if (((fresh >> q) & 1u) && rk < m) o.c_col[dst + rk] = base + c[q];
         }
@@ -1429,9 +1464,11 @@ void leaf_numeric(const LeafSet &L, int bin, const LeafTask *items, int64_t n, i
             launch_items(k_leaf_rank_num<RANK_XBLOCK, RANK_SWORDS, RANK_NARROW_CAP, RANK_LEPT>, RANK_XBLOCK, n, s, L,
                          items, width, o);
         else if (bin != LEAF_RANK_XL && narrow)  // at most RANK_SMALL distinct columns
-            launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_SMALL, RANK_EPT>, RANK_BLOCK, n, s, L, items, width, o);
+            launch_items(k_leaf_rank_num<RANK_LBLOCK, W17, RANK_SMALL, RANK_LWEPT>, RANK_LBLOCK, n, s, L, items, width,
+                         o);
         else if (bin != LEAF_RANK_XL)
-            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_SMALL, RANK_EPT>, RANK_BLOCK, n, s, L, items, width, o);
+            launch_items(k_leaf_rank_num<RANK_LBLOCK, W18, RANK_SMALL, RANK_LWEPT>, RANK_LBLOCK, n, s, L, items, width,
+                         o);
         else if (narrow)
             launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_NNZ_MAX, RANK_EPT>, RANK_BLOCK, n, s, L, items, width,
                          o);

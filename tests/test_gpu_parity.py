@@ -127,6 +127,17 @@ def test_rmat_scales(g, seed):
     check(g, A, A, tau=256, dense_width_log2=7, chunks_max_log2=3)
 
 
+@pytest.mark.parametrize("chunks_max_log2,levels", [(2, [4, 2]), (1, [2, 2, 2])])
+def test_wide_final_chunks(g, chunks_max_log2, levels):
+    # 2^16 columns with at most 4 (or 2) chunks per level: the first level's
+    # light chunks are final and wider than the dense width, so the wide
+    # accumulators run (bitmap rank, the small-chunk sort, hashing); with two
+    # levels the fused expansion writes them, with three the row-order one
+    A = wl.rmat(16, 4, 0.57, 0.19, 0.19, 16)
+    info = check(g, A, A, tau=300, chunks_max_log2=chunks_max_log2)
+    assert info.params.levels == levels
+
+
 def test_distinct_a_b_non_square(g):
     A = wl.rmat(11, 8, 0.57, 0.19, 0.19, 7)
     B = wl.erdos_renyi(A.n_cols, 3000, 12, 8)  # 2048 x 3000, C.m not a power of two
