@@ -863,30 +863,51 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_hash_num(LeafSet L, const LeafTa
     hash_emit_sorted<BLOCK, TS>(keys, vals, nnz, base, o.c_col + dst, o.c_val + dst, scan_sm, o.err);
 }
 
-// Elements of a chunk are read in batches of LEAF_EPT per thread, all loads
-// of a batch issued before any LDS update, so the global-memory latency is
-// paid once per batch rather than once per element.
-constexpr int LEAF_EPT = 8;
+
+// Calls f(column) for the elements [s, e) of a column array, reading it in
+// aligned 16-byte blocks (elements outside [s, e) skipped); a block that
+// would reach past e_end, the end of the array's valid elements, is read
+// element by element.
+template <int BLOCK, int U, typename ColT, typename F>
+GM_DEV void for_each_col_vec(const ColT *col, int64_t s, int64_t e, int64_t e_end, F f) {
+    constexpr int PER = 16 / (int)sizeof(ColT);
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    for (int64_t b = (s & ~(int64_t)(PER - 1)) + (int64_t)threadIdx.x * PER; b < e; b += (int64_t)BLOCK * PER * U) {
+        ColT v[U][PER];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t blk = b + (int64_t)u * BLOCK * PER;
+            if (blk + PER <= e_end) {
+                const u32x4 q = __builtin_nontemporal_load((const u32x4 *)(col + blk));
+                __builtin_memcpy(v[u], &q, 16);
+            } else {
+#pragma unroll
+                for (int j = 0; j < PER; ++j) v[u][j] = blk + j < e ? col[blk + j] : (ColT)0;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int j = 0; j < PER; ++j) {
+                const int64_t t = b + (int64_t)u * BLOCK * PER + j;
+                if (t >= s && t < e) f((int32_t)v[u][j]);
+            }
+    }
+}
 
 template <int BLOCK>
-__global__ __launch_bounds__(BLOCK) void k_leaf_dense_sym(LeafSet L, const LeafTask *tasks, int width,
+__global__ __launch_bounds__(BLOCK) void k_leaf_dense_sym(LeafSet L, const LeafTask *tasks, int width, int64_t e_end,
                                                           int64_t *leaf_nnz, int64_t *slot_cnt) {
     __shared__ DenseBits<BLOCK, DENSE_MAX> D;
     const LeafTask tk = tasks[blockIdx.x];
     const int64_t s = tk.s, e = tk.e;
     dense_clear(D, width, false);
     __syncthreads();
-    for (int64_t b = s; b < e; b += BLOCK * 2 * LEAF_EPT) {
-        int32_t c[2 * LEAF_EPT];
-#pragma unroll
-        for (int q = 0; q < 2 * LEAF_EPT; ++q) {
-            const int64_t t = b + q * BLOCK + threadIdx.x;
-            c[q] = t < e ? leaf_col_nt(L, t) : -1;
-        }
-#pragma unroll
-        for (int q = 0; q < 2 * LEAF_EPT; ++q)
-            if (c[q] >= 0) dense_set(D, c[q]);
-    }
+    // 16-byte column loads (the caller checked the column array's alignment)
+    if (L.col16)
+        for_each_col_vec<BLOCK, 2>(L.col16, s, e, e_end, [&](int32_t c) { dense_set(D, c); });
+    else
+        for_each_col_vec<BLOCK, 2>(L.col, s, e, e_end, [&](int32_t c) { dense_set(D, c); });
     __syncthreads();
     const int32_t cnt = dense_count(D, width);
     if (threadIdx.x == 0) {
@@ -1372,7 +1393,8 @@ void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *items, int64_t n, 
     case LEAF_H3: launch_items(k_leaf_hash_sym<512, 2 * HS_CAP[3]>, 512, n, s, L, items, leaf_nnz, slot_cnt); break;
     case LEAF_DENSE:
         GM_REQUIRE(n <= 0 || width <= DENSE_MAX, GMAGNUS_ERROR_UNSUPPORTED, "dense accumulator wider than LDS allows");
-        launch_items(k_leaf_dense_sym<512>, 512, n, s, L, items, width, leaf_nnz, slot_cnt);
+        GM_REQUIRE(((uintptr_t)colp & 15) == 0, GMAGNUS_ERROR_INVALID_VALUE, "column array not 16-byte aligned");
+        launch_items(k_leaf_dense_sym<512>, 512, n, s, L, items, width, e_end, leaf_nnz, slot_cnt);
         break;
     case LEAF_RANK_T:
         GM_REQUIRE(n <= 0 || width <= DENSE_MAX, GMAGNUS_ERROR_UNSUPPORTED, "one-wave rank shape is for narrow chunks");
