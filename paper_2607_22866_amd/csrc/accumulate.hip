@@ -1421,8 +1421,8 @@ void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *items, int64_t n, 
         else if (bin == LEAF_RANK)
             launch_items(k_leaf_rank_sym<RANK_WBLOCK, W18, RANK_WEPT>, RANK_WBLOCK, n, s, L, items, width, leaf_nnz,
                          slot_cnt);
-        else if (width <= (1 << 17))
-            launch_items(k_leaf_rank_sym<RANK_BLOCK, W17, RANK_EPT>, RANK_BLOCK, n, s, L, items, width, leaf_nnz,
+        else if (width <= (1 << 17))  // 4 waves per work group: 8 of them (chunks) per CU
+            launch_items(k_leaf_rank_sym<RANK_LBLOCK, W17, RANK_LWEPT>, RANK_LBLOCK, n, s, L, items, width, leaf_nnz,
                          slot_cnt);
         else
             launch_items(k_leaf_rank_sym<RANK_BLOCK, W18, RANK_EPT>, RANK_BLOCK, n, s, L, items, width, leaf_nnz,
