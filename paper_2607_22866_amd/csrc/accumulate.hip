@@ -1053,31 +1053,49 @@ GM_DEV uint32_t rank_mark(uint32_t *bits, int nwords, const int32_t (&c)[EPT], i
     return fresh;
 }
 
-template <int BLOCK, int NWORDS, int EPT>
+// A chunk's column range of (at most) NWORDS * 32 columns is covered in
+// PASSES consecutive parts with a bitmap of NWORDS / PASSES words, so a
+// 2^18-column range needs 16 KB of LDS instead of 32 KB.
+template <int EPT>
+GM_DEV void rank_part(const int32_t (&c)[EPT], int32_t (&cp)[EPT], int lo, int cols) {
+#pragma unroll
+    for (int q = 0; q < EPT; ++q) cp[q] = (c[q] >= lo && c[q] - lo < cols) ? c[q] - lo : -1;
+}
+
+template <int BLOCK, int NWORDS, int EPT, int PASSES = 1>
 __global__ __launch_bounds__(BLOCK) void k_leaf_rank_sym(LeafSet L, const LeafTask *tasks, int width,
                                                          int64_t *leaf_nnz, int64_t *slot_cnt) {
-    __shared__ uint32_t bits[NWORDS];
+    __shared__ uint32_t bits[NWORDS / PASSES];
     __shared__ int32_t count;
     const LeafTask tk = tasks[blockIdx.x];
     int32_t c[EPT];
     double v[EPT];
     rank_load<BLOCK, EPT>(L, tk.s, tk.e, c, v, false);
-    rank_mark<BLOCK, EPT>(bits, width >> 5, c, &count);
+    const int cols = width / PASSES;
+    int32_t total = 0;
+    for (int p = 0; p < PASSES; ++p) {
+        int32_t cp[EPT];
+        rank_part(c, cp, p * cols, cols);
+        rank_mark<BLOCK, EPT>(bits, cols >> 5, cp, &count);
+        total += count;
+        __syncthreads();  // count and bits are reused by the next part
+    }
     if (threadIdx.x == 0) {
-        leaf_nnz[tk.a] = count;
-        slot_cnt[tk.t] = count;
+        leaf_nnz[tk.a] = total;
+        slot_cnt[tk.t] = total;
     }
 }
 
 // Wide bitmaps keep one rank per group of 8 words instead of one per word
 // (a sixteenth of the LDS; an element reads its group's 8 words), so more
 // work groups fit a CU.
-template <int BLOCK, int NWORDS, int CAP, int EPT>
+template <int BLOCK, int NWORDS, int CAP, int EPT, int PASSES = 1>
 __global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const LeafTask *tasks, int width, LeafOut o) {
-    constexpr bool GROUPED = NWORDS >= 1024;
-    constexpr int NPRE = GROUPED ? NWORDS / 8 : NWORDS;
+    constexpr int NWP = NWORDS / PASSES;  // bitmap words of one part
+    constexpr bool GROUPED = NWP >= 1024;
+    constexpr int NPRE = GROUPED ? NWP / 8 : NWP;
     constexpr int WPT = (NPRE + BLOCK - 1) / BLOCK;  // rank entries per thread in the scan
-    __shared__ __align__(16) uint32_t bits[NWORDS];
+    __shared__ __align__(16) uint32_t bits[NWP];
     __shared__ uint16_t wpre[NPRE];  // rank of each word's (group's) first set bit (ranks < CAP <= 65535)
     __shared__ double vals[CAP];
     __shared__ int32_t scan_sm[BLOCK / GM_WAVE];
@@ -1085,66 +1103,74 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const LeafTa
     const LeafTask tk = tasks[blockIdx.x];
     const int64_t dst = tk.t, nnz = tk.a;
     const int32_t base = tk.b;
-    const int nwords = width >> 5;
+    const int cols = width / PASSES;
+    const int nwords = cols >> 5;
+    const int m = nnz < CAP ? (int)nnz : CAP;  // ranks at or above m are never written (count checked below)
     int32_t c[EPT];
     double v[EPT];
     rank_load<BLOCK, EPT>(L, tk.s, tk.e, c, v, true);
-    const uint32_t fresh = rank_mark<BLOCK, EPT>(bits, nwords, c, &count);
-    const int32_t total = count;
-    const int n = total < CAP ? total : CAP;
-    const int m = n < nnz ? n : (int)nnz;
-    if (threadIdx.x == 0 && (total != nnz || total > CAP)) atomicOr(o.err, 4);
-    // word (group) ranks: thread t owns entries [t*WPT, t*WPT + WPT)
-    {
-        const int npre = GROUPED ? nwords / 8 : nwords;
-        const int w0 = threadIdx.x * WPT;
-        int32_t cnt[WPT], sum = 0;
+    for (int q = threadIdx.x; q < m; q += BLOCK) vals[q] = 0.0;
+    int32_t done = 0;  // distinct columns of the parts before this one
+    for (int pass = 0; pass < PASSES; ++pass) {
+        int32_t cp[EPT];
+        rank_part(c, cp, pass * cols, cols);
+        const uint32_t fresh = rank_mark<BLOCK, EPT>(bits, nwords, cp, &count);
+        // word (group) ranks: thread t owns entries [t*WPT, t*WPT + WPT)
+        {
+            const int npre = GROUPED ? nwords / 8 : nwords;
+            const int w0 = threadIdx.x * WPT;
+            int32_t cnt[WPT], sum = 0;
 #pragma unroll
-        for (int j = 0; j < WPT; ++j) {
-            cnt[j] = 0;
-            if (w0 + j < npre) {
+            for (int j = 0; j < WPT; ++j) {
+                cnt[j] = 0;
+                if (w0 + j < npre) {
+                    if (GROUPED) {
+                        const uint4 a = *(const uint4 *)&bits[(w0 + j) * 8];
+                        const uint4 b = *(const uint4 *)&bits[(w0 + j) * 8 + 4];
+                        cnt[j] = __popc(a.x) + __popc(a.y) + __popc(a.z) + __popc(a.w) + __popc(b.x) + __popc(b.y) +
+                                 __popc(b.z) + __popc(b.w);
+                    } else {
+                        cnt[j] = __popc(bits[w0 + j]);
+                    }
+                }
+                sum += cnt[j];
+            }
+            int32_t r = block_excl_scan<BLOCK>(sum, scan_sm);
+#pragma unroll
+            for (int j = 0; j < WPT; ++j)
+                if (w0 + j < npre) {
+                    wpre[w0 + j] = (uint16_t)(r < 65535 ? r : 65535);
+                    r += cnt[j];
+                }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < EPT; ++q)
+            if (cp[q] >= 0) {
+                const int w = cp[q] >> 5;
+                int rk;
                 if (GROUPED) {
-                    const uint4 a = *(const uint4 *)&bits[(w0 + j) * 8];
-                    const uint4 b = *(const uint4 *)&bits[(w0 + j) * 8 + 4];
-                    cnt[j] = __popc(a.x) + __popc(a.y) + __popc(a.z) + __popc(a.w) + __popc(b.x) + __popc(b.y) +
-                             __popc(b.z) + __popc(b.w);
+                    const int g = w >> 3, j0 = w & 7;
+                    const uint4 a = *(const uint4 *)&bits[g * 8];
+                    const uint4 b = *(const uint4 *)&bits[g * 8 + 4];
+                    const uint32_t ws[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+                    rk = wpre[g];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j)
+                        rk += __popc(ws[j] & (j < j0 ? ~0u : j == j0 ? (1u << (cp[q] & 31)) - 1u : 0u));
                 } else {
-                    cnt[j] = __popc(bits[w0 + j]);
+                    rk = wpre[w] + __popc(bits[w] & ((1u << (cp[q] & 31)) - 1u));
+                }
+                rk += done;
+                if (rk < m) {
+                    __hip_atomic_fetch_add(&vals[rk], v[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                    if ((fresh >> q) & 1u) o.c_col[dst + rk] = base + c[q];
                 }
             }
-            sum += cnt[j];
-        }
-        int32_t r = block_excl_scan<BLOCK>(sum, scan_sm);
-#pragma unroll
-        for (int j = 0; j < WPT; ++j)
-            if (w0 + j < npre) {
-                wpre[w0 + j] = (uint16_t)(r < 65535 ? r : 65535);
-                r += cnt[j];
-            }
+        done += count;
+        __syncthreads();  // bits, wpre and count are reused by the next part
     }
-    for (int q = threadIdx.x; q < n; q += BLOCK) vals[q] = 0.0;
-    __syncthreads();
-#pragma unroll
-    for (int q = 0; q < EPT; ++q)
-        if (c[q] >= 0) {
-            const int w = c[q] >> 5;
-            int rk;
-            if (GROUPED) {
-                const int g = w >> 3, j0 = w & 7;
-                const uint4 a = *(const uint4 *)&bits[g * 8];
-                const uint4 b = *(const uint4 *)&bits[g * 8 + 4];
-                const uint32_t ws[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-                rk = wpre[g];
-#pragma unroll
-                for (int j = 0; j < 8; ++j)
-                    rk += __popc(ws[j] & (j < j0 ? ~0u : j == j0 ? (1u << (c[q] & 31)) - 1u : 0u));
-            } else {
-                rk = wpre[w] + __popc(bits[w] & ((1u << (c[q] & 31)) - 1u));
-            }
-            if (rk < n) __hip_atomic_fetch_add(&vals[rk], v[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-            if (((fresh >> q) & 1u) && rk < m) o.c_col[dst + rk] = base + c[q];
-        }
-    __syncthreads();
+    if (threadIdx.x == 0 && (done != nnz || done > CAP)) atomicOr(o.err, 4);
     for (int q = threadIdx.x; q < m; q += BLOCK) o.c_val[dst + q] = vals[q];
 }
 
@@ -1419,13 +1445,13 @@ void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *items, int64_t n, 
             launch_items(k_leaf_rank_sym<RANK_WBLOCK, W17, RANK_WEPT>, RANK_WBLOCK, n, s, L, items, width, leaf_nnz,
                          slot_cnt);
         else if (bin == LEAF_RANK)
-            launch_items(k_leaf_rank_sym<RANK_WBLOCK, W18, RANK_WEPT>, RANK_WBLOCK, n, s, L, items, width, leaf_nnz,
+            launch_items(k_leaf_rank_sym<RANK_WBLOCK, W18, RANK_WEPT, 2>, RANK_WBLOCK, n, s, L, items, width, leaf_nnz,
                          slot_cnt);
         else if (width <= (1 << 17))  // 4 waves per work group: 8 of them (chunks) per CU
             launch_items(k_leaf_rank_sym<RANK_LBLOCK, W17, RANK_LWEPT>, RANK_LBLOCK, n, s, L, items, width, leaf_nnz,
                          slot_cnt);
         else
-            launch_items(k_leaf_rank_sym<RANK_BLOCK, W18, RANK_EPT>, RANK_BLOCK, n, s, L, items, width, leaf_nnz,
+            launch_items(k_leaf_rank_sym<RANK_LBLOCK, W18, RANK_LWEPT, 2>, RANK_LBLOCK, n, s, L, items, width, leaf_nnz,
                          slot_cnt);
         break;
     }
@@ -1489,13 +1515,13 @@ void leaf_numeric(const LeafSet &L, int bin, const LeafTask *items, int64_t n, i
             launch_items(k_leaf_rank_num<RANK_LBLOCK, W17, RANK_SMALL, RANK_LWEPT>, RANK_LBLOCK, n, s, L, items, width,
                          o);
         else if (bin != LEAF_RANK_XL)
-            launch_items(k_leaf_rank_num<RANK_LBLOCK, W18, RANK_SMALL, RANK_LWEPT>, RANK_LBLOCK, n, s, L, items, width,
+            launch_items(k_leaf_rank_num<RANK_LBLOCK, W18, RANK_SMALL, RANK_LWEPT, 2>, RANK_LBLOCK, n, s, L, items, width,
                          o);
         else if (narrow)
             launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_NNZ_MAX, RANK_EPT>, RANK_BLOCK, n, s, L, items, width,
                          o);
         else
-            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_NNZ_MAX, RANK_EPT>, RANK_BLOCK, n, s, L, items, width,
+            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_NNZ_MAX, RANK_EPT, 2>, RANK_BLOCK, n, s, L, items, width,
                          o);
         break;
     }
