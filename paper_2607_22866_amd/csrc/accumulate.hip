@@ -1026,8 +1026,10 @@ GM_DEV void rank_load(const LeafSet &L, int64_t s, int64_t e, int32_t (&c)[EPT],
 // Marks the chunk's columns in the bitmap; returns, one bit per element
 // slot, the elements that found their column's bit clear (each column's
 // first element), and through *count the number of distinct columns.
+// (only the columns in [lo, lo + cols) are marked, at c - lo)
 template <int BLOCK, int EPT>
-GM_DEV uint32_t rank_mark(uint32_t *bits, int nwords, const int32_t (&c)[EPT], int32_t *count) {
+GM_DEV uint32_t rank_mark(uint32_t *bits, int nwords, const int32_t (&c)[EPT], int32_t *count, int lo = 0,
+                          int cols = INT32_MAX) {
     static_assert(EPT <= 32, "one fresh bit per element slot");
     for (int w = threadIdx.x; w < nwords; w += BLOCK) bits[w] = 0;
     if (threadIdx.x == 0) *count = 0;
@@ -1036,9 +1038,10 @@ GM_DEV uint32_t rank_mark(uint32_t *bits, int nwords, const int32_t (&c)[EPT], i
     int n_fresh = 0;
 #pragma unroll
     for (int q = 0; q < EPT; ++q)
-        if (c[q] >= 0) {
-            const int w = c[q] >> 5;
-            const uint32_t bit = 1u << (c[q] & 31);
+        if (c[q] >= 0 && (cols == INT32_MAX || (c[q] >= lo && c[q] - lo < cols))) {
+            const int cq = c[q] - lo;
+            const int w = cq >> 5;
+            const uint32_t bit = 1u << (cq & 31);
             if (!(((volatile uint32_t *)bits)[w] & bit)) {
                 const uint32_t old = atomicOr(&bits[w], bit);
                 if (!(old & bit)) {
@@ -1056,11 +1059,6 @@ GM_DEV uint32_t rank_mark(uint32_t *bits, int nwords, const int32_t (&c)[EPT], i
 // A chunk's column range of (at most) NWORDS * 32 columns is covered in
 // PASSES consecutive parts with a bitmap of NWORDS / PASSES words, so a
 // 2^18-column range needs 16 KB of LDS instead of 32 KB.
-template <int EPT>
-GM_DEV void rank_part(const int32_t (&c)[EPT], int32_t (&cp)[EPT], int lo, int cols) {
-#pragma unroll
-    for (int q = 0; q < EPT; ++q) cp[q] = (c[q] >= lo && c[q] - lo < cols) ? c[q] - lo : -1;
-}
 
 template <int BLOCK, int NWORDS, int EPT, int PASSES = 1>
 __global__ __launch_bounds__(BLOCK) void k_leaf_rank_sym(LeafSet L, const LeafTask *tasks, int width,
@@ -1073,12 +1071,16 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_rank_sym(LeafSet L, const LeafTa
     rank_load<BLOCK, EPT>(L, tk.s, tk.e, c, v, false);
     const int cols = width / PASSES;
     int32_t total = 0;
-    for (int p = 0; p < PASSES; ++p) {
-        int32_t cp[EPT];
-        rank_part(c, cp, p * cols, cols);
-        rank_mark<BLOCK, EPT>(bits, cols >> 5, cp, &count);
-        total += count;
-        __syncthreads();  // count and bits are reused by the next part
+    if constexpr (PASSES == 1) {
+        rank_mark<BLOCK, EPT>(bits, cols >> 5, c, &count);
+        total = count;
+    } else {
+#pragma unroll 1
+        for (int p = 0; p < PASSES; ++p) {
+            rank_mark<BLOCK, EPT>(bits, cols >> 5, c, &count, p * cols, cols);
+            total += count;
+            __syncthreads();  // count and bits are reused by the next part
+        }
     }
     if (threadIdx.x == 0) {
         leaf_nnz[tk.a] = total;
@@ -1109,12 +1111,11 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const LeafTa
     int32_t c[EPT];
     double v[EPT];
     rank_load<BLOCK, EPT>(L, tk.s, tk.e, c, v, true);
-    for (int q = threadIdx.x; q < m; q += BLOCK) vals[q] = 0.0;
     int32_t done = 0;  // distinct columns of the parts before this one
-    for (int pass = 0; pass < PASSES; ++pass) {
-        int32_t cp[EPT];
-        rank_part(c, cp, pass * cols, cols);
-        const uint32_t fresh = rank_mark<BLOCK, EPT>(bits, nwords, cp, &count);
+    auto part = [&](int pass) {
+        const int lo = pass * cols;
+        const uint32_t fresh = PASSES == 1 ? rank_mark<BLOCK, EPT>(bits, nwords, c, &count)
+                                           : rank_mark<BLOCK, EPT>(bits, nwords, c, &count, lo, cols);
         // word (group) ranks: thread t owns entries [t*WPT, t*WPT + WPT)
         {
             const int npre = GROUPED ? nwords / 8 : nwords;
@@ -1143,11 +1144,14 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const LeafTa
                     r += cnt[j];
                 }
         }
+        if (pass == 0)
+            for (int q = threadIdx.x; q < m; q += BLOCK) vals[q] = 0.0;
         __syncthreads();
 #pragma unroll
         for (int q = 0; q < EPT; ++q)
-            if (cp[q] >= 0) {
-                const int w = cp[q] >> 5;
+            if (c[q] >= 0 && (PASSES == 1 || (c[q] >= lo && c[q] - lo < cols))) {
+                const int cq = c[q] - lo;
+                const int w = cq >> 5;
                 int rk;
                 if (GROUPED) {
                     const int g = w >> 3, j0 = w & 7;
@@ -1157,9 +1161,9 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const LeafTa
                     rk = wpre[g];
 #pragma unroll
                     for (int j = 0; j < 8; ++j)
-                        rk += __popc(ws[j] & (j < j0 ? ~0u : j == j0 ? (1u << (cp[q] & 31)) - 1u : 0u));
+                        rk += __popc(ws[j] & (j < j0 ? ~0u : j == j0 ? (1u << (cq & 31)) - 1u : 0u));
                 } else {
-                    rk = wpre[w] + __popc(bits[w] & ((1u << (cp[q] & 31)) - 1u));
+                    rk = wpre[w] + __popc(bits[w] & ((1u << (cq & 31)) - 1u));
                 }
                 rk += done;
                 if (rk < m) {
@@ -1168,7 +1172,16 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const LeafTa
                 }
             }
         done += count;
-        __syncthreads();  // bits, wpre and count are reused by the next part
+    };
+    if constexpr (PASSES == 1) {
+        part(0);
+        __syncthreads();  // every value summed before the write-out
+    } else {
+#pragma unroll
+        for (int pass = 0; pass < PASSES; ++pass) {
+            part(pass);
+            __syncthreads();  // every value of the part summed; bits, wpre and count reused by the next
+        }
     }
     if (threadIdx.x == 0 && (done != nnz || done > CAP)) atomicOr(o.err, 4);
     for (int q = threadIdx.x; q < m; q += BLOCK) o.c_val[dst + q] = vals[q];
