@@ -301,14 +301,17 @@ GM_DEV int hash_bin_num(int64_t nnz) {
 // Sorting a few hundred products in LDS (one or three 8-bit passes) costs far
 // less LDS traffic than the bitonic sort of the hash table's occupied slots.
 constexpr int SORT_SMALL[2] = {256, 512};
-constexpr int SORT_CAP[2] = {2048, 6912};
+// (the middle cap keeps two 256-thread work groups per CU; the largest
+// needs almost all of a CU's LDS)
+constexpr int SORT_CAP[3] = {2048, 3456, 6912};
 GM_DEV int light_bin_num(int64_t nnz, int64_t ip) {
     return nnz <= HN_CAP[0]        ? 0
            : ip <= SORT_SMALL[0]   ? 1
            : ip <= SORT_SMALL[1]   ? 2
            : nnz <= HN_CAP[1]      ? 3
            : ip <= SORT_CAP[0]     ? 4
-                                   : 5;
+           : ip <= SORT_CAP[1]     ? 5
+                                   : 6;
 }
 
 // Window choice for a light row: span = max column - min column + 1.
@@ -1000,7 +1003,7 @@ constexpr int RANK_EPT = 16;  // RANK_BLOCK * RANK_EPT >= tau_limit()
 constexpr int RANK_WBLOCK = 256, RANK_WEPT = 4;  // the small wide shape
 constexpr int RANK_LBLOCK = 256, RANK_LWEPT = 27;  // wide numeric, at most RANK_SMALL columns: 4 waves and
                                                    // under 32 KB of LDS, so five work groups share a CU
-static_assert(RANK_LBLOCK * RANK_LWEPT >= SORT_CAP[1] && RANK_BLOCK * RANK_EPT >= SORT_CAP[1],
+static_assert(RANK_LBLOCK * RANK_LWEPT >= SORT_CAP[2] && RANK_BLOCK * RANK_EPT >= SORT_CAP[2],
               "the wide shapes hold a light chunk of up to the largest tau");
 static_assert(RANK_WBLOCK * RANK_WEPT >= RANK_WIDE_SMALL, "the small wide shape holds its chunks");
 constexpr int RANK_SBLOCK = 256, RANK_SWORDS = 256, RANK_SCAP = 512, RANK_SEPT = 2, RANK_LEPT = 8;
@@ -1388,7 +1391,11 @@ void light_numeric(const Csr &A, const Csr &B, int64_t r0, int bin, const int64_
                      c_val, err);
         break;
     case LIGHT_H5:
-        launch_items(k_light_sort_num<512, SORT_CAP[1]>, 512, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col,
+        launch_items(k_light_sort_num<256, SORT_CAP[1]>, 256, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col,
+                     c_val, err);
+        break;
+    case LIGHT_H6:
+        launch_items(k_light_sort_num<512, SORT_CAP[2]>, 512, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col,
                      c_val, err);
         break;
     default: break;
@@ -1553,7 +1560,7 @@ void slot_scan(int64_t *slot, int64_t n_heavy, int64_t n_slots, const int64_t *h
 
 int64_t tau_limit() {
     int64_t t = HN_CAP[3] < RANK_NNZ_MAX ? HN_CAP[3] : RANK_NNZ_MAX;
-    return t < SORT_CAP[1] ? t : SORT_CAP[1];
+    return t < SORT_CAP[2] ? t : SORT_CAP[2];
 }
 
 }  // namespace gm
