@@ -396,10 +396,14 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows(RsArgs a) {
 // Fine boundaries: bndf[s * (nf + 1) + f] = offset in B[k,:] of the first
 // column >= f << fshift (f = 0..nf), for the slices whose B row is longer
 // than FB_SHORT (the fine counts read the columns of the shorter rows
-// instead: at most FB_SHORT reads against nf + 1). One wave per slice, binary
-// search per boundary.
+// instead: at most FB_SHORT reads against nf + 1). One wave per slice; lane i
+// searches the boundaries i, i + 64, ... (PER of them), all its searches
+// stepping together so their loads overlap (a hub row's searches would
+// otherwise be PER dependent chains of about 17 loads each, one after the
+// other).
 constexpr int FB_SHORT = 64;
 
+template <int PER>
 __global__ __launch_bounds__(256) void k_fine_bounds(Csr B, const int32_t *slice_k, int64_t n_slices, int nf,
                                                      int fshift, int32_t *bndf) {
     const int lane = threadIdx.x & (GM_WAVE - 1);
@@ -409,17 +413,34 @@ __global__ __launch_bounds__(256) void k_fine_bounds(Csr B, const int32_t *slice
         const int64_t b0 = B.rp[k], len = B.rp[k + 1] - b0;
         if (len <= FB_SHORT) continue;
         int32_t *out = bndf + s * (nf + 1);
-        for (int f = lane; f <= nf; f += GM_WAVE) {
-            int64_t lo = b0, hi = b0 + len;
-            const int64_t bound = (int64_t)f << fshift;
-            while (lo < hi) {
-                const int64_t mid = lo + ((hi - lo) >> 1);
-                if ((int64_t)B.ci[mid] < bound)
-                    lo = mid + 1;
-                else
-                    hi = mid;
+        const int32_t *row = B.ci + b0;
+        // bit length of len halvings shrink every range to a point
+        const int steps = 64 - __clzll((unsigned long long)len);
+        for (int f0 = 0; f0 <= nf; f0 += PER * GM_WAVE) {  // PER boundaries per lane at a time
+            int32_t lo[PER], hi[PER];
+#pragma unroll
+            for (int j = 0; j < PER; ++j) {
+                lo[j] = 0;
+                hi[j] = f0 + lane + j * GM_WAVE <= nf ? (int32_t)len : 0;  // past nf: empty range
             }
-            out[f] = (int32_t)(lo - b0);
+            for (int st = 0; st < steps; ++st) {
+#pragma unroll
+                for (int j = 0; j < PER; ++j) {
+                    const int32_t mid = (lo[j] + hi[j]) >> 1;
+                    const bool go = lo[j] < hi[j];
+                    const int32_t col = go ? row[mid] : 0;
+                    const bool below = (int64_t)col < ((int64_t)(f0 + lane + j * GM_WAVE) << fshift);
+                    if (go) {
+                        if (below)
+                            lo[j] = mid + 1;
+                        else
+                            hi[j] = mid;
+                    }
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < PER; ++j)
+                if (f0 + lane + j * GM_WAVE <= nf) out[f0 + lane + j * GM_WAVE] = lo[j];
         }
     }
 }
@@ -823,7 +844,10 @@ int64_t fine_bounds_words(int64_t n_slices, int nf) { return n_slices * (nf + 1)
 void fine_bounds(const Csr &B, const int32_t *slice_k, int64_t n_slices, int nf, int fshift, int32_t *bndf,
                  hipStream_t s) {
     if (n_slices <= 0) return;
-    hipLaunchKernelGGL(k_fine_bounds, dim3(grid_for(n_slices, 4, 65536)), dim3(256), 0, s, B, slice_k, n_slices, nf,
+    GM_REQUIRE(nf >= 1 && nf <= FC_MAXF && (int64_t)B.nnz < ((int64_t)1 << 31), GMAGNUS_ERROR_UNSUPPORTED,
+               "fine boundaries: too many fine chunks or B too large");
+    // 9 boundaries per lane cover nf = 512 (R-MAT 22's 32 x 16 chunks) in one round
+    hipLaunchKernelGGL(k_fine_bounds<9>, dim3(grid_for(n_slices, 4, 65536)), dim3(256), 0, s, B, slice_k, n_slices, nf,
                        fshift, bndf);
     GM_CHECK_LAUNCH();
 }
