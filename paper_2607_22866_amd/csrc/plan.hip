@@ -290,11 +290,54 @@ struct Timed {
     }
 };
 
-template <typename T>
-T read_scalar(const T *dev, hipStream_t s) {
-    T v{};
-    GM_HIP(hipMemcpyAsync(&v, dev, sizeof(T), hipMemcpyDeviceToHost, s));
-    GM_HIP(hipStreamSynchronize(s));
+// Pinned host staging for the small device-to-host reads of counts and bin
+// boundaries (a copy into pageable memory goes through the runtime's own
+// staging and costs more per read). One buffer per host thread: every read
+// has completed when its call returns, so reads never overlap on it. The
+// buffer lives until the process ends.
+constexpr int READ_SLOTS = 64;
+
+int64_t *read_buffer() {
+    thread_local int64_t *buf = nullptr;
+    if (!buf) GM_HIP(hipHostMalloc((void **)&buf, sizeof(int64_t) * READ_SLOTS, hipHostMallocDefault));
+    return buf;
+}
+
+// Several reads, one stream synchronisation: add() queues a copy into the
+// staging buffer, wait() synchronises once and copies the values out.
+class HostReads {
+  public:
+    explicit HostReads(hipStream_t s) : s_(s), buf_(read_buffer()) {}
+    void add(const int64_t *dev, int n, int64_t *host) {
+        GM_REQUIRE(used_ + n <= READ_SLOTS && n_ < MAXR, GMAGNUS_ERROR_INVALID_VALUE, "too many host reads at once");
+        GM_HIP(hipMemcpyAsync(buf_ + used_, dev, sizeof(int64_t) * n, hipMemcpyDeviceToHost, s_));
+        r_[n_++] = Read{host, n, used_};
+        used_ += n;
+    }
+    void wait() {
+        GM_HIP(hipStreamSynchronize(s_));
+        for (int i = 0; i < n_; ++i)
+            for (int j = 0; j < r_[i].n; ++j) r_[i].host[j] = buf_[r_[i].at + j];
+        n_ = used_ = 0;
+    }
+
+  private:
+    struct Read {
+        int64_t *host;
+        int n, at;
+    };
+    static constexpr int MAXR = 8;
+    hipStream_t s_;
+    int64_t *buf_;
+    Read r_[MAXR];
+    int n_ = 0, used_ = 0;
+};
+
+int64_t read_scalar(const int64_t *dev, hipStream_t s) {
+    int64_t v = 0;
+    HostReads r(s);
+    r.add(dev, 1, &v);
+    r.wait();
     return v;
 }
 
@@ -321,8 +364,9 @@ int64_t lds_bytes_of(const gmagnus_options_t &o) {
 
 // Reads bin boundaries of a partition into host memory.
 void read_bins(const int64_t *dev, int nb, int64_t *host, hipStream_t s) {
-    GM_HIP(hipMemcpyAsync(host, dev, sizeof(int64_t) * (nb + 1), hipMemcpyDeviceToHost, s));
-    GM_HIP(hipStreamSynchronize(s));
+    HostReads r(s);
+    r.add(dev, nb + 1, host);
+    r.wait();
 }
 
 // Chooses the multisplit tile (elements) and rows per tile for a level.
@@ -411,9 +455,12 @@ void do_plan(gmagnus_plan_s *p, const gmagnus_csr_t *A, const gmagnus_csr_t *B, 
     if (n == 0) return;
 
     int64_t rp2[2] = {0, 0};
-    GM_HIP(hipMemcpyAsync(&rp2[0], A->row_ptr + p->r0, sizeof(int64_t), hipMemcpyDeviceToHost, stream));
-    GM_HIP(hipMemcpyAsync(&rp2[1], A->row_ptr + p->r1, sizeof(int64_t), hipMemcpyDeviceToHost, stream));
-    GM_HIP(hipStreamSynchronize(stream));
+    {
+        HostReads r(stream);
+        r.add(A->row_ptr + p->r0, 1, &rp2[0]);
+        r.add(A->row_ptr + p->r1, 1, &rp2[1]);
+        r.wait();
+    }
     const int64_t panel_nnz = rp2[1] - rp2[0];
 
     Timed t(p, GMAGNUS_K_SETUP, stream);
@@ -431,8 +478,12 @@ void do_plan(gmagnus_plan_s *p, const gmagnus_csr_t *A, const gmagnus_csr_t *B, 
     // products of all rows and of the heavy rows (C-hat row pointers)
     int64_t *ip_scan = ws.alloc<int64_t>(n + 1);
     scan_i64(p->ip, n, ip_scan, scratch, stream);
-    read_bins(bins, LIGHT_NBINS, p->bins_sym, stream);
-    p->products_total = read_scalar(ip_scan + n, stream);
+    {
+        HostReads r(stream);
+        r.add(bins, LIGHT_NBINS + 1, p->bins_sym);
+        r.add(ip_scan + n, 1, &p->products_total);
+        r.wait();
+    }
     p->n_heavy = p->bins_sym[LIGHT_HEAVY + 1] - p->bins_sym[LIGHT_HEAVY];
     p->heavy_rows = p->perm + p->bins_sym[LIGHT_HEAVY];
     p->chat_ptr = ws.alloc<int64_t>(p->n_heavy + 1);
@@ -517,10 +568,13 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         slice_lengths(p->B, sl.slice_k, sl.n_slices, cnt_s, s);
         scan_i64(cnt_s, sl.n_slices, blen_scan, sc2, s);
         int64_t tot[3];
-        GM_HIP(hipMemcpyAsync(&tot[0], sl.col_ptr + sl.n_slices, sizeof(int64_t), hipMemcpyDeviceToHost, s));
-        GM_HIP(hipMemcpyAsync(&tot[1], sl.slice_off + sl.n_slices, sizeof(int64_t), hipMemcpyDeviceToHost, s));
-        GM_HIP(hipMemcpyAsync(&tot[2], blen_scan + sl.n_slices, sizeof(int64_t), hipMemcpyDeviceToHost, s));
-        GM_HIP(hipStreamSynchronize(s));
+        {
+            HostReads r(s);
+            r.add(sl.col_ptr + sl.n_slices, 1, &tot[0]);
+            r.add(sl.slice_off + sl.n_slices, 1, &tot[1]);
+            r.add(blen_scan + sl.n_slices, 1, &tot[2]);
+            r.wait();
+        }
         ws.free(blen_scan);
         sl.nnz = tot[0];
         blen_total = tot[2];
@@ -878,12 +932,15 @@ void heavy_symbolic(gmagnus_plan_s *p) {
             fill<int64_t>(lv.leaf_nnz, 0, nl, s);
             leaf_classes_sym(lv.set, P.tau, lv.width, lc, s);
             partition_u8(lc, nl, LEAF_NBINS, lv.items_sym, nullptr, bins, sc, s);
-            read_bins(bins, LEAF_NBINS, lv.bins_sym, s);
         }
         int64_t e0 = 0, e1 = 0;
-        GM_HIP(hipMemcpyAsync(&e0, lv.set.ptr + lv.set.lo, sizeof(int64_t), hipMemcpyDeviceToHost, s));
-        GM_HIP(hipMemcpyAsync(&e1, lv.set.ptr + lv.set.hi, sizeof(int64_t), hipMemcpyDeviceToHost, s));
-        GM_HIP(hipStreamSynchronize(s));
+        {
+            HostReads r(s);
+            r.add(bins, LEAF_NBINS + 1, lv.bins_sym);
+            r.add(lv.set.ptr + lv.set.lo, 1, &e0);
+            r.add(lv.set.ptr + lv.set.hi, 1, &e1);
+            r.wait();
+        }
         lv.elems = e1 - e0;
         {
             LeafTask *tasks = ws.alloc<LeafTask>(nl);
@@ -975,13 +1032,16 @@ void do_symbolic(gmagnus_plan_s *p, int64_t *c_row_ptr, int64_t *c_nnz) {
         Timed t(p, GMAGNUS_K_ROWPTR, p->stream);
         int64_t *sc = ws.alloc<int64_t>(scan_scratch_elems(n));
         scan_i64(p->row_nnz, n, c_row_ptr, sc, p->stream);
-        p->c_nnz = read_scalar(c_row_ptr + n, p->stream);
+        int64_t *hs = nullptr;
+        HostReads r(p->stream);
+        r.add(c_row_ptr + n, 1, &p->c_nnz);
         if (p->n_heavy > 0) {
-            int64_t *hs = ws.alloc<int64_t>(p->n_heavy + 1);
-            scan_gather_i64(p->row_nnz, p->heavy_rows, p->n_heavy, hs, sc, p->stream);
-            p->info.c_nnz_heavy = read_scalar(hs + p->n_heavy, p->stream);
-            ws.free(hs);
+            hs = ws.alloc<int64_t>(p->n_heavy + 1);
+            scan_gather_i64(p->row_nnz, p->heavy_rows, p->n_heavy, hs, sc, p->stream);  // sc: after the first scan
+            r.add(hs + p->n_heavy, 1, &p->info.c_nnz_heavy);
         }
+        r.wait();
+        ws.free(hs);
         ws.free(sc);
         add_bytes(p, GMAGNUS_K_ROWPTR, 16.0 * n);
     }
