@@ -57,7 +57,7 @@ def log(msg):
     print("[bench] " + msg, file=sys.stderr, flush=True)
 
 
-def run_step(g, dA, bounds, timing, acc, c_bufs, extra_flags=0):
+def run_step(g, dA, bounds, timing, acc, c_bufs, extra_flags=0, tau=0):
     """One full product; returns (products, nnz(C))."""
     import torch
 
@@ -65,7 +65,7 @@ def run_step(g, dA, bounds, timing, acc, c_bufs, extra_flags=0):
     nnz = 0
     flags = (g.FLAG_TIMING if timing else 0) | extra_flags
     for a, b in zip(bounds[:-1], bounds[1:]):
-        with g.Plan(dA, dA, row_begin=a, row_end=b, flags=flags) as p:
+        with g.Plan(dA, dA, row_begin=a, row_end=b, flags=flags, tau=tau) as p:
             rp, n = p.symbolic()
             if c_bufs[0] is None or c_bufs[0].numel() < n:
                 c_bufs[0] = c_bufs[1] = None
@@ -196,6 +196,7 @@ def main():
                     help="split at the first level during a slice-order expansion (atomic cursors)")
     ap.add_argument("--level-by-level", action="store_true",
                     help="with two levels, write the first level out and split it in a pass of its own")
+    ap.add_argument("--tau", type=int, default=0, help="heavy threshold (0: the planner's)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build measures the single-GPU hot path "
@@ -230,7 +231,7 @@ def main():
              (g.FLAG_SLICE_SPLIT if args.slice_split else 0) | (g.FLAG_LEVEL_BY_LEVEL if args.level_by_level else 0))
     for w in range(args.warmup):
         t = time.perf_counter()
-        run_step(g, dA, bounds, False, acc_warm, c_bufs, extra)
+        run_step(g, dA, bounds, False, acc_warm, c_bufs, extra, args.tau)
         torch.cuda.synchronize()
         log("warmup %d: %.3fs" % (w, time.perf_counter() - t))
 
@@ -241,7 +242,7 @@ def main():
     for s in range(args.steps):
         t = time.perf_counter()
         bounds = g.split_panels(dA, dA, int(args.panel_products))
-        products, nnz = run_step(g, dA, bounds, True, acc, c_bufs, extra)
+        products, nnz = run_step(g, dA, bounds, True, acc, c_bufs, extra, args.tau)
         torch.cuda.synchronize()
         log("step %d: %.3fs" % (s, time.perf_counter() - t))
     torch.cuda.synchronize()

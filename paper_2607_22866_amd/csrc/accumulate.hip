@@ -348,6 +348,7 @@ constexpr int DENSE_MAX = 8192;          // columns of the LDS dense accumulator
 constexpr int RANK_MAX_LOG2 = 18;        // columns of the bitmap-rank accumulator
 constexpr int RANK_NNZ_MAX = 6912;       // distinct columns it holds (>= tau; two work groups per CU at 2^17 columns)
 constexpr int RANK_MIN_LEN = 256;        // smaller chunks go to the hash map
+constexpr int RANK_MID = 3584;           // distinct columns of the middle wide variant (three per CU)
 constexpr int RANK_SMALL = 1792;         // distinct columns of the small wide rank variant (its LDS
                                          // stays under 32 KB: five work groups per CU)
 constexpr int RANK_NARROW_CAP = 4096;    // chunks of at most DENSE_MAX columns and at most this many elements use
@@ -385,8 +386,11 @@ __global__ void k_leaf_classes(LeafSet L, const int64_t *leaf_nnz, int64_t tau, 
             c = len >= DENSE_BIG_LEN ? LEAF_DENSE_BIG : LEAF_DENSE;
         else if (width <= (1 << RANK_MAX_LOG2) && width >= 32 && len >= RANK_MIN_LEN)
             // symbolic: the small wide shape for small chunks; numeric: by distinct columns
+            // (for wide numeric chunks LEAF_RANK is the middle size, up to RANK_MID columns)
             c = !leaf_nnz ? (len <= RANK_WIDE_SMALL ? LEAF_RANK : LEAF_RANK_L)
-                          : (leaf_nnz[i] > RANK_SMALL ? LEAF_RANK_XL : LEAF_RANK_L);
+                          : (leaf_nnz[i] <= RANK_SMALL ? LEAF_RANK_L
+                             : leaf_nnz[i] <= RANK_MID ? LEAF_RANK
+                                                       : LEAF_RANK_XL);
         else
             c = (uint8_t)(LEAF_H0 + (leaf_nnz ? hash_bin_num(leaf_nnz[i]) : hash_bin_sym(len)));
         cls[i] = c;
@@ -1531,6 +1535,10 @@ void leaf_numeric(const LeafSet &L, int bin, const LeafTask *items, int64_t n, i
         else if (width <= DENSE_MAX)  // at most RANK_NARROW_CAP elements
             launch_items(k_leaf_rank_num<RANK_XBLOCK, RANK_SWORDS, RANK_NARROW_CAP, RANK_LEPT>, RANK_XBLOCK, n, s, L,
                          items, width, o);
+        else if (bin == LEAF_RANK && narrow)  // wide, at most RANK_MID distinct columns
+            launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_MID, RANK_EPT>, RANK_BLOCK, n, s, L, items, width, o);
+        else if (bin == LEAF_RANK)
+            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_MID, RANK_EPT, 2>, RANK_BLOCK, n, s, L, items, width, o);
         else if (bin != LEAF_RANK_XL && narrow)  // at most RANK_SMALL distinct columns
             launch_items(k_leaf_rank_num<RANK_LBLOCK, W17, RANK_SMALL, RANK_LWEPT>, RANK_LBLOCK, n, s, L, items, width,
                          o);
