@@ -138,6 +138,14 @@ def test_wide_final_chunks(g, chunks_max_log2, levels):
     assert info.params.levels == levels
 
 
+def test_first_level_chunks_of_2_18_columns(g):
+    # 2^19 columns, at most 2 chunks per level: the first level's light chunks
+    # span 2^18 columns, which the bitmap-rank kernels cover in two halves
+    A = wl.rmat(19, 2, 0.57, 0.19, 0.19, 19)
+    info = check(g, A, A, tau=300, chunks_max_log2=1, row_begin=0, row_end=65536)
+    assert info.params.levels[0] == 2 and info.levels_run >= 2
+
+
 def test_distinct_a_b_non_square(g):
     A = wl.rmat(11, 8, 0.57, 0.19, 0.19, 7)
     B = wl.erdos_renyi(A.n_cols, 3000, 12, 8)  # 2048 x 3000, C.m not a power of two
