@@ -1270,9 +1270,15 @@ __global__ __launch_bounds__(WAVES * GM_WAVE) void k_leaf_wave_sym(const ColT *c
                 if (t >= tk.s && t < tk.e) {
                     const int32_t c = (int32_t)v[u][j];
                     const uint32_t bit = 1u << (c & 31);
-                    if (!(atomicOr(&bits[c >> 5], bit) & bit)) ++fresh;
+                    // no return value needed: the distinct count comes from the bitmap
+                    __hip_atomic_fetch_or(&bits[c >> 5], bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
                 }
             }
+    }
+    wave_lds_fence();
+    for (int i = lane * 4; i < NWORDS; i += GM_WAVE * 4) {
+        const uint4 q = *(const uint4 *)&bits[i];
+        fresh += __popc(q.x) + __popc(q.y) + __popc(q.z) + __popc(q.w);
     }
     const int32_t n = wave_reduce_sum<int32_t>(fresh);
     if (lane == 0) {
