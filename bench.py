@@ -1,4 +1,4 @@
-"""Benchmark: SpGEMM C = A*A on one MI355X through the C ABI.
+"""Benchmark: SpGEMM C = A*A (C = A*B for the R-MAT pairs) on one MI355X through the C ABI.
 
 One step = the whole product for the workload: row-panel split by product
 counts, then per panel the setup (row products, light/heavy split), the
@@ -36,6 +36,13 @@ WORKLOADS = {
     "rmat22": "R-MAT scale 22 (2^22 x 2^22), edge factor 16, (a,b,c,d)=(0.57,0.19,0.19,0.05), fp64 U(0,1), C=A*A",
     "rmat23": "R-MAT scale 23 (2^23 x 2^23), edge factor 8, (a,b,c,d)=(0.60,0.17,0.17,0.06), fp64 U(0,1), C=A*A",
 }
+# A*B pairs (two R-MAT matrices of one scale, different edge factors); not the headline workload.
+PAIR_WORKLOADS = {
+    "rmat20_a32_b8": "R-MAT scale 20, A edge factor 32 times B edge factor 8, (a,b,c,d)=(0.57,0.19,0.19,0.05), "
+                     "fp64 U(0,1), C=A*B",
+    "rmat20_a64_b16": "R-MAT scale 20, A edge factor 64 times B edge factor 16, (a,b,c,d)=(0.57,0.19,0.19,0.05), "
+                      "fp64 U(0,1), C=A*B",
+}
 HEAVY_KERNELS = ["expand", "histogram", "multisplit", "chunk_symbolic", "chunk_numeric"]
 # Timing classes that are exactly one kernel launch per panel: the roofline is
 # reported for the one of these with the largest device time.
@@ -57,7 +64,7 @@ def log(msg):
     print("[bench] " + msg, file=sys.stderr, flush=True)
 
 
-def run_step(g, dA, bounds, timing, acc, c_bufs, extra_flags=0, tau=0):
+def run_step(g, dA, dB, bounds, timing, acc, c_bufs, extra_flags=0, tau=0):
     """One full product; returns (products, nnz(C))."""
     import torch
 
@@ -65,7 +72,7 @@ def run_step(g, dA, bounds, timing, acc, c_bufs, extra_flags=0, tau=0):
     nnz = 0
     flags = (g.FLAG_TIMING if timing else 0) | extra_flags
     for a, b in zip(bounds[:-1], bounds[1:]):
-        with g.Plan(dA, dA, row_begin=a, row_end=b, flags=flags, tau=tau) as p:
+        with g.Plan(dA, dB, row_begin=a, row_end=b, flags=flags, tau=tau) as p:
             rp, n = p.symbolic()
             if c_bufs[0] is None or c_bufs[0].numel() < n:
                 c_bufs[0] = c_bufs[1] = None
@@ -154,7 +161,7 @@ def measured_traffic(kernel, config):
     return float(vals["bytes_per_launch"])
 
 
-def cpu_baseline(A, ip, budget_products, seed=0):
+def cpu_baseline(A, B, ip, budget_products, seed=0):
     """Times the oracle on a random sample of rows (about budget_products products)."""
     import numpy as np
 
@@ -167,7 +174,7 @@ def cpu_baseline(A, ip, budget_products, seed=0):
     rows = np.sort(order[:k])
     sample_products = int(ip[rows].sum())
     t0 = time.perf_counter()
-    oracle.spgemm(A, A, rows=rows)
+    oracle.spgemm(A, B, rows=rows)
     dt = time.perf_counter() - t0
     return {
         "value": 2.0 * sample_products / dt / 1e9,
@@ -184,7 +191,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--config", default="rmat22", choices=sorted(WORKLOADS))
+    ap.add_argument("--config", default="rmat22", choices=sorted(WORKLOADS) + sorted(PAIR_WORKLOADS))
     ap.add_argument("--panel-products", type=float, default=4e9,
                     help="maximum intermediate products per row panel")
     ap.add_argument("--cpu-products", type=float, default=2.5e9, help="oracle sample size for the CPU baseline")
@@ -214,16 +221,22 @@ def main():
     if not torch.cuda.is_available():
         raise RuntimeError("no GPU visible")
     torch.cuda.set_device(0)
-    cfg = workloads.CONFIGS[args.config]
+    pair = args.config in PAIR_WORKLOADS
+    cfg = workloads.PAIRS[args.config] if pair else workloads.CONFIGS[args.config]
     t0 = time.perf_counter()
-    A = cfg.make()
-    log("generated %s: n=%d nnz=%d in %.1fs" % (args.config, A.n_rows, A.nnz, time.perf_counter() - t0))
+    if pair:
+        A, B = cfg.make()
+    else:
+        A = B = cfg.make()
+    log("generated %s: n=%d nnz(A)=%d nnz(B)=%d in %.1fs" % (args.config, A.n_rows, A.nnz, B.nnz,
+                                                             time.perf_counter() - t0))
     dA = g.DeviceCSR.from_host(A)
+    dB = g.DeviceCSR.from_host(B) if pair else dA
     torch.cuda.synchronize()
     copy_gbs = copy_peak(torch)
     log("device copy bandwidth %.0f GB/s" % copy_gbs)
 
-    bounds = g.split_panels(dA, dA, int(args.panel_products))
+    bounds = g.split_panels(dA, dB, int(args.panel_products))
     log("%d row panels (max %.2g products each)" % (len(bounds) - 1, args.panel_products))
     acc_warm = {}
     c_bufs = [None, None]
@@ -231,7 +244,7 @@ def main():
              (g.FLAG_SLICE_SPLIT if args.slice_split else 0) | (g.FLAG_LEVEL_BY_LEVEL if args.level_by_level else 0))
     for w in range(args.warmup):
         t = time.perf_counter()
-        run_step(g, dA, bounds, False, acc_warm, c_bufs, extra, args.tau)
+        run_step(g, dA, dB, bounds, False, acc_warm, c_bufs, extra, args.tau)
         torch.cuda.synchronize()
         log("warmup %d: %.3fs" % (w, time.perf_counter() - t))
 
@@ -241,8 +254,8 @@ def main():
     t_start = time.perf_counter()
     for s in range(args.steps):
         t = time.perf_counter()
-        bounds = g.split_panels(dA, dA, int(args.panel_products))
-        products, nnz = run_step(g, dA, bounds, True, acc, c_bufs, extra, args.tau)
+        bounds = g.split_panels(dA, dB, int(args.panel_products))
+        products, nnz = run_step(g, dA, dB, bounds, True, acc, c_bufs, extra, args.tau)
         torch.cuda.synchronize()
         log("step %d: %.3fs" % (s, time.perf_counter() - t))
     torch.cuda.synchronize()
@@ -288,7 +301,7 @@ def main():
     all_gb = sum(v["gb_per_step"] for v in kernels.values())
 
     out = {
-        "metric": METRIC,
+        "metric": METRIC.replace("A·A", "A·B") if pair else METRIC,
         "value": gflops,
         "unit": "GFLOP/s",
         "n_gpus": 1,
@@ -300,8 +313,8 @@ def main():
         "vs_baseline": None,
         "dtype": "f64",
         "data": "synthetic",
-        "config": {"workload": WORKLOADS[args.config], "name": args.config, "seed": cfg.seed, "n": A.n_rows,
-                   "nnz_a": A.nnz, "products": products, "nnz_c": nnz, "panels": len(bounds) - 1,
+        "config": {"workload": (PAIR_WORKLOADS if pair else WORKLOADS)[args.config], "name": args.config,
+                   "seed": cfg.seed, "n": A.n_rows, "nnz_a": A.nnz, "nnz_b": B.nnz, "products": products, "nnz_c": nnz, "panels": len(bounds) - 1,
                    "panel_products": args.panel_products},
         "achieved_hbm_gbs": {"heavy_path_kernels": heavy_gb / (heavy_ms / 1000.0) if heavy_ms else None,
                              "heavy_path_frac": (heavy_gb / (heavy_ms / 1000.0)) / HBM_PEAK_GBS if heavy_ms else None,
@@ -316,9 +329,9 @@ def main():
         "kernels": kernels,
     }
     if not args.no_cpu_baseline:
-        ip = g.row_products(dA, dA).cpu().numpy()
+        ip = g.row_products(dA, dB).cpu().numpy()
         log("timing the oracle on a sample of about %.2g products" % args.cpu_products)
-        out["cpu_baseline"] = cpu_baseline(A, ip, args.cpu_products)
+        out["cpu_baseline"] = cpu_baseline(A, B, ip, args.cpu_products)
         del np
     print(json.dumps(out), flush=True)
 

@@ -1,4 +1,4 @@
-"""Parity at the five benchmark workloads' full sizes, in the benchmark's
+"""Parity at the five benchmark workloads' full sizes (and one R-MAT A*B pair), in the benchmark's
 launch configuration (row panels of at most 4e9 products): the whole product
 runs on the GPU, and sampled rows (random rows plus the heaviest rows) are
 compared with the oracle, which computes them one by one. Properties that
@@ -36,16 +36,18 @@ def sample_rows(ip, n_random, n_heaviest, seed):
     return np.array(sorted(rows), dtype=np.int64)
 
 
-def run_sampled(g, A, rows, panel_products=PANEL_PRODUCTS):
-    """Runs C = A*A panel by panel; returns the sampled rows' CSR and totals."""
+def run_sampled(g, A, rows, panel_products=PANEL_PRODUCTS, B=None):
+    """Runs C = A*A (A*B when B is given) panel by panel; returns the sampled
+    rows' CSR and totals."""
     dA = g.DeviceCSR.from_host(A)
-    bounds = g.split_panels(dA, dA, panel_products)
+    dB = dA if B is None else g.DeviceCSR.from_host(B)
+    bounds = g.split_panels(dA, dB, panel_products)
     out_rp = [0]
     out_col, out_val = [], []
     total_nnz = total_products = 0
     for a, b in zip(bounds[:-1], bounds[1:]):
         sel = rows[(rows >= a) & (rows < b)]
-        with g.Plan(dA, dA, row_begin=a, row_end=b) as p:
+        with g.Plan(dA, dB, row_begin=a, row_end=b) as p:
             rp, nnz = p.symbolic()
             col, val = p.numeric()
             info = p.info()
@@ -97,3 +99,16 @@ def test_rmat22_full(g):
 
 def test_rmat23_full(g):
     check_config(g, "rmat23", 400, 3)
+
+
+def test_rmat20_pair_full(g):
+    # C = A*B, R-MAT scale 20 with A edge factor 32 and B edge factor 8
+    A, B = wl.PAIRS["rmat20_a32_b8"].make()
+    ip = oracle.row_products(A, B)
+    rows = sample_rows(ip, 400, 3, seed=20)
+    rp, col, val, nnz, products, panels = run_sampled(g, A, rows, B=B)
+    assert products == int(ip.sum())
+    ref = oracle.spgemm(A, B, rows=rows)
+    worst = compare_rows(np.arange(rows.size), rp, col, val, ref)
+    print("rmat20_a32_b8: panels=%d products=%d nnz(C)=%d sampled_rows=%d max_rel_err=%.2e" % (
+        panels, products, nnz, rows.size, worst))

@@ -153,6 +153,20 @@ def test_distinct_a_b_non_square(g):
     check(g, A, B, tau=300, dense_width_log2=6, chunks_max_log2=3)
 
 
+@pytest.mark.parametrize("a_ef,b_ef", [(4, 4), (4, 16), (16, 8), (64, 16)])
+def test_rmat_pair_grid(g, a_ef, b_ef):
+    # C = A*B with two R-MAT matrices of scale 15 and different densities
+    # (the paper's RMat grid, Section IV-A, at a size the oracle finishes);
+    # every row is compared, with the planner's depth and with a forced
+    # two-level split
+    A = wl.rmat(15, a_ef, 0.57, 0.19, 0.19, 1000 + a_ef)
+    B = wl.rmat(15, b_ef, 0.57, 0.19, 0.19, 1001 + b_ef)
+    check(g, A, B)
+    if a_ef == 16:
+        info = check(g, A, B, tau=2048, dense_width_log2=9, chunks_max_log2=3)
+        assert len(info.params.levels) >= 2
+
+
 @pytest.mark.parametrize("shape,density", [((1, 1, 1), 1.0), ((37, 50, 61), 0.1), ((200, 300, 150), 0.05),
                                            ((64, 64, 64), 0.0), ((130, 5, 700), 0.5)])
 def test_uniform_small(g, shape, density):

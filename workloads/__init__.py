@@ -169,6 +169,30 @@ class Config:
         raise ValueError(self.kind)
 
 
+@dataclass(frozen=True)
+class PairConfig:
+    """C = A*B with two R-MAT matrices of one scale and different densities
+    (edge factors), Graph500 parameters a = 0.57, b = c = 0.19, as in the
+    paper's RMat grid (Section IV-A)."""
+
+    name: str
+    scale: int
+    a_edge_factor: int
+    b_edge_factor: int
+    seed: int
+
+    def make(self) -> tuple:
+        A = rmat(self.scale, self.a_edge_factor, 0.57, 0.19, 0.19, self.seed, "u01")
+        B = rmat(self.scale, self.b_edge_factor, 0.57, 0.19, 0.19, self.seed + 1, "u01")
+        return A, B
+
+
+# A*B pairs of the RMat grid (A density 4..64, B density 4..16, scales 15..20).
+PAIRS = {
+    "rmat20_a32_b8": PairConfig("rmat20_a32_b8", 20, 32, 8, 2032),
+    "rmat20_a64_b16": PairConfig("rmat20_a64_b16", 20, 64, 16, 2064),
+}
+
 # The five workloads, each multiplied by itself (C = A*A).
 CONFIGS = {
     "rmat12": Config("rmat12", "rmat", (12, 8, 0.57, 0.19, 0.19), 12, "u01"),
