@@ -97,6 +97,37 @@ def run_step(g, dA, dB, bounds, timing, acc, c_bufs, extra_flags=0, tau=0):
     return products, nnz
 
 
+def reuse_pass(g, dA, dB, bounds, c_bufs, extra_flags=0, tau=0):
+    """Pattern reuse, panel by panel: the full product (plan, symbolic,
+    numeric) on a plan that keeps its pattern, then new values of A and B
+    (gmagnus_update_values) and numeric again. Returns the summed seconds of
+    the full products and of the values-only re-runs."""
+    import torch
+
+    va = (dA.val * 0.5 + 0.25).contiguous()
+    vb = va if dB is dA else (dB.val * 0.5 + 0.25).contiguous()
+    t_full = t_vals = 0.0
+    for a, b in zip(bounds[:-1], bounds[1:]):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        with g.Plan(dA, dB, row_begin=a, row_end=b, flags=g.FLAG_KEEP_PATTERN | extra_flags, tau=tau) as p:
+            rp, n = p.symbolic()
+            if c_bufs[0] is None or c_bufs[0].numel() < n:
+                c_bufs[0] = c_bufs[1] = None
+                c_bufs[0] = torch.empty(max(n, 1), dtype=torch.int32, device="cuda")
+                c_bufs[1] = torch.empty(max(n, 1), dtype=torch.float64, device="cuda")
+            p.numeric(c_bufs[0], c_bufs[1])
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            p.update_values(va, vb)
+            p.numeric(c_bufs[0], c_bufs[1])
+            torch.cuda.synchronize()
+            t2 = time.perf_counter()
+        t_full += t1 - t0
+        t_vals += t2 - t1
+    return t_full, t_vals
+
+
 def unfused_model_bytes(products_heavy, elems_deeper_levels, c_nnz_heavy):
     """Bytes the paper's unfused sequence of heavy-row kernels moves
     (Algorithm 3 with Algorithms 4 and 5): C-hat written once (12 B per
@@ -204,6 +235,9 @@ def main():
     ap.add_argument("--level-by-level", action="store_true",
                     help="with two levels, write the first level out and split it in a pass of its own")
     ap.add_argument("--tau", type=int, default=0, help="heavy threshold (0: the planner's)")
+    ap.add_argument("--pattern-reuse", action="store_true",
+                    help="after the timed steps, also time one values-only re-run per panel (new values of A "
+                         "and B on the kept patterns) against the full product on the same plans")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build measures the single-GPU hot path "
@@ -328,6 +362,13 @@ def main():
         "roofline": roofline,
         "kernels": kernels,
     }
+    if args.pattern_reuse:
+        t_full, t_vals = reuse_pass(g, dA, dB, bounds, c_bufs, extra, args.tau)
+        out["pattern_reuse"] = {"full_ms": 1000.0 * t_full, "values_only_ms": 1000.0 * t_vals,
+                                "values_only_gflops": 2.0 * products / t_vals / 1e9,
+                                "speedup": t_full / t_vals,
+                                "note": "panel by panel, synchronised around each phase; full = plan + symbolic + "
+                                        "numeric with the pattern kept, values only = gmagnus_update_values + numeric"}
     if not args.no_cpu_baseline:
         ip = g.row_products(dA, dB).cpu().numpy()
         log("timing the oracle on a sample of about %.2g products" % args.cpu_products)

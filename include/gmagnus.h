@@ -98,6 +98,9 @@ typedef struct {
 #define GMAGNUS_FLAG_LEVEL_BY_LEVEL 64u /* with two multisplit levels, write the first level's heavy chunks out
                                            and split them in a pass of their own, instead of splitting them again
                                            inside the expansion and writing the final chunks directly */
+#define GMAGNUS_FLAG_KEEP_PATTERN 256u /* keep the heavy path's structural buffers after symbolic so that
+                                          gmagnus_update_values can recompute C for new values of A and B
+                                          on the same patterns (costs the memory of those buffers) */
 
 #define GMAGNUS_MAX_LEVELS 8
 
@@ -191,6 +194,25 @@ gmagnus_status_t gmagnus_spgemm_symbolic(gmagnus_plan_t plan, int64_t *c_row_ptr
  * Errors: INVALID_VALUE (NULL), NOT_READY (symbolic has not run), HIP. */
 gmagnus_status_t gmagnus_spgemm_numeric(gmagnus_plan_t plan, const int64_t *c_row_ptr, int32_t *c_col_idx,
                                         double *c_val);
+
+/* Pattern reuse: the symbolic phase depends on the nonzero patterns of A and
+ * B only (Section II-A: it fixes C.rowPtr and C.nnz; the numeric phase fills
+ * the values), so repeated products on fixed patterns with changing values
+ * (algebraic multigrid's Galerkin products, Section I) need the symbolic
+ * work once. This call replaces the values of A and B the plan reads with
+ * a_val (A.nnz doubles, in A's CSR order) and b_val (B.nnz doubles, in B's
+ * CSR order), device pointers the caller keeps alive and unchanged until the
+ * plan's next numeric phase has finished (they may be the arrays given at
+ * gmagnus_plan, and a_val may equal b_val when A and B are one matrix). It
+ * redoes only the value-producing passes of the heavy rows (the outer-product
+ * expansion and the multisplit levels, on the layout symbolic computed);
+ * gmagnus_spgemm_numeric then writes C for the new values into the structure
+ * symbolic produced, with the same c_row_ptr. Asynchronous on the plan's
+ * stream. Requires GMAGNUS_FLAG_KEEP_PATTERN at gmagnus_plan.
+ * Errors: INVALID_VALUE (NULL values with nonzeros present, or the plan was
+ * made without GMAGNUS_FLAG_KEEP_PATTERN), NOT_READY (symbolic has not run),
+ * HIP. */
+gmagnus_status_t gmagnus_update_values(gmagnus_plan_t plan, const double *a_val, const double *b_val);
 
 /* Copies the plan's parameters, counts and (with GMAGNUS_FLAG_TIMING) kernel
  * timings. Synchronises the stream when timings are requested. */

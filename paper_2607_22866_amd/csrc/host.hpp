@@ -59,7 +59,10 @@ class Workspace {
     T *alloc(int64_t n) {
         return static_cast<T *>(alloc_bytes(sizeof(T) * (size_t)(n > 0 ? n : 1)));
     }
+    // While held, free() keeps blocks in use (a plan that must keep every
+    // buffer its recorded launches read).
     void free(void *p);
+    void hold(bool h) { hold_ = h; }
     void release_all();
     size_t bytes_in_use() const { return in_use_; }
 
@@ -75,6 +78,7 @@ class Workspace {
     std::vector<Block> blocks_;  // owned, in use
     std::vector<Block> spare_;   // owned, freed by the plan
     size_t in_use_ = 0;
+    bool hold_ = false;
 };
 
 void cache_release();

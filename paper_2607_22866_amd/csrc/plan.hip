@@ -5,6 +5,7 @@
 // the numeric phase. Also the library's caching device allocator.
 #include <algorithm>
 #include <cstring>
+#include <functional>
 #include <map>
 #include <memory>
 #include <mutex>
@@ -119,7 +120,7 @@ void *Workspace::alloc_bytes(size_t bytes) {
 }
 
 void Workspace::free(void *p) {
-    if (!p) return;
+    if (!p || hold_) return;
     for (size_t i = 0; i < blocks_.size(); ++i)
         if (blocks_[i].p == p) {
             in_use_ -= blocks_[i].bytes;
@@ -243,6 +244,9 @@ struct gmagnus_plan_s {
     int n_slots_log2 = 0, slot_width_log2 = 0;
     int64_t *slot = nullptr;
     std::vector<LeafLevel> leaves;
+    // value-producing launches of the heavy path in their order, recorded
+    // under GMAGNUS_FLAG_KEEP_PATTERN and replayed by gmagnus_update_values
+    std::vector<std::function<void(const Csr &, const Csr &, hipStream_t)>> replay;
     bool symbolic_done = false;
     int64_t c_nnz = 0;
     gmagnus_plan_info_t info{};
@@ -512,6 +516,21 @@ void heavy_symbolic(gmagnus_plan_s *p) {
     p->n_slots = P.n_levels > 0 ? P.chunks_required : 1;
     p->n_slots_log2 = ilog2(p->n_slots);
     p->slot_width_log2 = c_bits - p->n_slots_log2;
+    // With a kept pattern nothing is freed (every buffer a recorded step
+    // reads stays valid) and each value-producing step is recorded; the
+    // steps reset the cursors they consume, so a replay repeats them exactly.
+    const bool keep = (p->opts.flags & GMAGNUS_FLAG_KEEP_PATTERN) != 0;
+    ws.hold(keep);
+    struct Unhold {
+        Workspace &w;
+        ~Unhold() { w.hold(false); }
+    } unhold{ws};
+    auto values_step = [&](std::function<void(const Csr &, const Csr &, hipStream_t)> f) {
+        f(p->A, p->B, s);
+        if (keep) p->replay.push_back(std::move(f));
+    };
+    const int64_t *heavy_rows = p->heavy_rows;
+    const int64_t r0 = p->r0;
 
     const bool paper_hist = (p->opts.flags & GMAGNUS_FLAG_PAPER_HISTOGRAM) != 0;
     // split at the first level while expanding, unless the paper's order is asked for
@@ -582,17 +601,21 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         int64_t *cursor = nullptr;
         if (!rows_order) {
             cursor = ws.alloc<int64_t>(std::max<int64_t>(sl.n_slices, 1));
-            fill<int64_t>(cursor, 0, sl.n_slices, s);
             sl.row_h = ws.alloc<int32_t>(sl.nnz);
             sl.a_val = ws.alloc<double>(sl.nnz);
-            csc_fill(p->A, p->B, p->heavy_rows, nh, p->r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, sl.col_ptr,
-                     cursor, sl.row_h, sl.a_val, s);
+            values_step([=](const Csr &A, const Csr &B, hipStream_t st) {
+                fill<int64_t>(cursor, 0, sl.n_slices, st);
+                csc_fill(A, B, heavy_rows, nh, r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, sl.col_ptr, cursor,
+                         sl.row_h, sl.a_val, st);
+            });
         } else {
             ent.k = ws.alloc<int32_t>(nnz_heavy_all);
             ent.s = ws.alloc<int32_t>(nnz_heavy_all);
             ent.h = ws.alloc<int32_t>(nnz_heavy_all);
             ent.a = ws.alloc<double>(nnz_heavy_all);
-            heavy_entries(p->A, p->heavy_rows, nh, p->r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, ent, s);
+            values_step([=](const Csr &A, const Csr &, hipStream_t st) {
+                heavy_entries(A, heavy_rows, nh, r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, ent, st);
+            });
         }
         if (P.n_levels > 0 && !paper_hist) {
             // level-0 (row, chunk) counts from the structure of A~ and B
@@ -672,10 +695,15 @@ void heavy_symbolic(gmagnus_plan_s *p) {
     };
     if (!fused) {
         int64_t *cursor = ws.alloc<int64_t>(nh);
-        copy_i64(cursor, p->chat_ptr, nh, s);
         {
             Timed t(p, GMAGNUS_K_EXPAND, s);
-            expand(p->B, sl, H, exp_tiles, cursor, col_buf[0], val_buf[0], s);
+            const int64_t *chat_ptr = p->chat_ptr;
+            int32_t *oc = col_buf[0];
+            double *ov = val_buf[0];
+            values_step([=](const Csr &, const Csr &B, hipStream_t st) {
+                copy_i64(cursor, chat_ptr, nh, st);
+                expand(B, sl, H, exp_tiles, cursor, oc, ov, st);
+            });
         }
         ws.free(cursor);
         p->info.kernel_launches[GMAGNUS_K_EXPAND] += 1;
@@ -761,8 +789,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                                                 : multisplit_next_fits(g.group_rows * nc, g.next_chunks);
         if (!last && nh_out > 0 && next_fused) {
             // the multisplit (or the chunk-major expansion) takes the next level's histogram on the way
-            next_counts = ws.alloc<int64_t>(nh_out * g.next_chunks);
-            fill<int64_t>(next_counts, 0, nh_out * g.next_chunks, s);
+            next_counts = ws.alloc<int64_t>(nh_out * g.next_chunks);  // zeroed by the step that fills it
         }
         const int nxt = split_in_expand ? 0 : 1 - cur;
         if (!col_buf[nxt]) {
@@ -818,7 +845,6 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                     partition_u8(ccls1, n_out1, 2, perm1, x_map1, cb1, sc1, s);
                     chunk_reorder(counts1, x_map1, n_out1, nc1, origin_out, slots1, 0, out_cnt1, origin_out1, s);
                     scan_i64(out_cnt1, n_out1, out_ptr1, sc1, s);
-                    gather_i64(out_ptr1, x_map1, n_out1, cursor1, s);
                     elems1 = read_scalar(out_ptr + nh_out, s);
                 }
                 // sized like the first level's buffers, so panels reuse the same blocks
@@ -826,9 +852,18 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                 val_buf[1] = ws.alloc<double>(H);
                 {
                     Timed t(p, GMAGNUS_K_EXPAND, s);
-                    expand_rows2(p->B, ent, pre, sbnd, out_ptr, seg_base, reg_c, reg_efirst, reg_ne, n_out, nh_out, H,
-                                 nc, g.shift, nc1, shift1, P.tau, cursor1, elems1, p->err, exp_tiles, col_buf[0],
-                                 val_buf[0], (uint16_t *)col_buf[1], val_buf[1], s);
+                    int32_t *oc0 = col_buf[0], *oc1 = col_buf[1];
+                    double *ov0 = val_buf[0], *ov1 = val_buf[1];
+                    const int shift0 = g.shift;
+                    const int64_t tau = P.tau;
+                    int32_t *err = p->err;
+                    values_step([=](const Csr &, const Csr &B, hipStream_t st) {
+                        // the second level's cursors start at its regions' offsets
+                        gather_i64(out_ptr1, x_map1, n_out1, cursor1, st);
+                        expand_rows2(B, ent, pre, sbnd, out_ptr, seg_base, reg_c, reg_efirst, reg_ne, n_out, nh_out,
+                                     H, nc, shift0, nc1, shift1, tau, cursor1, elems1, err, exp_tiles, oc0, ov0,
+                                     (uint16_t *)oc1, ov1, st);
+                    });
                 }
                 p->info.kernel_launches[GMAGNUS_K_EXPAND] += 1;
                 // products (the final chunks' columns in 16 bits), entries, offsets, B rows, row records
@@ -851,9 +886,14 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                 ws.free(cursor1);
             } else {
                 Timed t(p, GMAGNUS_K_EXPAND, s);
-                expand_rows(p->B, ent, pre, sbnd, out_ptr, seg_base, reg_c, reg_efirst, reg_ne, n_out, nh_out, H, nc,
-                            g.shift, last ? 0 : g.next_chunks, g.next_shift, next_counts, exp_tiles, col_buf[nxt],
-                            val_buf[nxt], s);
+                const int nn = last ? 0 : g.next_chunks, nshift = g.next_shift, shift0 = g.shift;
+                int32_t *oc = col_buf[nxt];
+                double *ov = val_buf[nxt];
+                values_step([=](const Csr &, const Csr &B, hipStream_t st) {
+                    if (next_counts) fill<int64_t>(next_counts, 0, nh_out * nn, st);
+                    expand_rows(B, ent, pre, sbnd, out_ptr, seg_base, reg_c, reg_efirst, reg_ne, n_out, nh_out, H, nc,
+                                shift0, nn, nshift, next_counts, exp_tiles, oc, ov, st);
+                });
                 p->info.kernel_launches[GMAGNUS_K_EXPAND] += 1;
                 add_bytes(p, GMAGNUS_K_EXPAND,
                           12.0 * H + 20.0 * nnz_heavy_all + 4.0 * nnz_heavy_all * nc + 12.0 * blen_total + 24.0 * n_out);
@@ -866,10 +906,15 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         } else if (split_in_expand) {
             // cursor of output row (h, c), indexed h * nc + c
             int64_t *cursor = ws.alloc<int64_t>(n_out);
-            gather_i64(out_ptr, x_map, n_out, cursor, s);
             {
                 Timed t(p, GMAGNUS_K_EXPAND, s);
-                expand_split(p->B, sl, H, exp_tiles, sbnd, nc, g.shift, cursor, col_buf[nxt], val_buf[nxt], s);
+                const int shift0 = g.shift;
+                int32_t *oc = col_buf[nxt];
+                double *ov = val_buf[nxt];
+                values_step([=](const Csr &, const Csr &B, hipStream_t st) {
+                    gather_i64(out_ptr, x_map, n_out, cursor, st);
+                    expand_split(B, sl, H, exp_tiles, sbnd, nc, shift0, cursor, oc, ov, st);
+                });
             }
             ws.free(cursor);
             p->info.kernel_launches[GMAGNUS_K_EXPAND] += 1;
@@ -877,11 +922,18 @@ void heavy_symbolic(gmagnus_plan_s *p) {
             free_slices();
         } else {
             int64_t *cursor = ws.alloc<int64_t>(n_out);
-            copy_i64(cursor, out_ptr, n_out, s);
             {
                 Timed t(p, GMAGNUS_K_MULTISPLIT, s);
-                multisplit(g, in_ptr, tile_row, col_buf[cur], val_buf[cur], x_map, cursor, col_buf[nxt],
-                           val_buf[nxt], nh_out, next_counts, s);
+                const int32_t *ic = col_buf[cur];
+                const double *iv = val_buf[cur];
+                int32_t *oc = col_buf[nxt];
+                double *ov = val_buf[nxt];
+                const int nn = g.next_chunks;
+                values_step([=](const Csr &, const Csr &, hipStream_t st) {
+                    copy_i64(cursor, out_ptr, n_out, st);
+                    if (next_counts) fill<int64_t>(next_counts, 0, nh_out * nn, st);
+                    multisplit(g, in_ptr, tile_row, ic, iv, x_map, cursor, oc, ov, nh_out, next_counts, st);
+                });
             }
             ws.free(cursor);
             p->info.kernel_launches[GMAGNUS_K_MULTISPLIT] += 1;
@@ -1127,6 +1179,38 @@ void do_numeric(gmagnus_plan_s *p, const int64_t *c_row_ptr, int32_t *c_col, dou
     add_bytes(p, GMAGNUS_K_LIGHT_NUM, 12.0 * (double)(p->c_nnz - p->info.c_nnz_heavy));
 }
 
+// New values on the kept patterns: the light rows read A and B directly in
+// the numeric phase; the heavy rows' recorded steps rewrite the expansion and
+// multisplit buffers that the final chunks' numeric kernels read.
+void do_update_values(gmagnus_plan_s *p, const double *a_val, const double *b_val) {
+    GM_REQUIRE((p->opts.flags & GMAGNUS_FLAG_KEEP_PATTERN) != 0, GMAGNUS_ERROR_INVALID_VALUE,
+               "plan made without GMAGNUS_FLAG_KEEP_PATTERN");
+    GM_REQUIRE(p->symbolic_done, GMAGNUS_ERROR_NOT_READY, "values updated before symbolic");
+    GM_REQUIRE((a_val || p->A.nnz == 0) && (b_val || p->B.nnz == 0), GMAGNUS_ERROR_INVALID_VALUE, "NULL values");
+    p->A.v = a_val;
+    p->B.v = b_val;
+    if (p->replay.empty()) return;
+    hipEvent_t fork, join;
+    GM_HIP(hipEventCreateWithFlags(&fork, hipEventDisableTiming));
+    GM_HIP(hipEventCreateWithFlags(&join, hipEventDisableTiming));
+    struct EvGuard {
+        hipEvent_t a, b;
+        ~EvGuard() {
+            (void)hipEventDestroy(a);
+            (void)hipEventDestroy(b);
+        }
+    } guard{fork, join};
+    const hipStream_t s = p->s_heavy;
+    GM_HIP(hipEventRecord(fork, p->stream));
+    if (s != p->stream) GM_HIP(hipStreamWaitEvent(s, fork, 0));
+    {
+        Timed t(p, GMAGNUS_K_EXPAND, s);
+        for (auto &f : p->replay) f(p->A, p->B, s);
+    }
+    GM_HIP(hipEventRecord(join, s));
+    if (s != p->stream) GM_HIP(hipStreamWaitEvent(p->stream, join, 0));
+}
+
 template <class F>
 gmagnus_status_t guarded(F &&f) {
     try {
@@ -1200,6 +1284,14 @@ gmagnus_status_t gmagnus_spgemm_numeric(gmagnus_plan_t plan, const int64_t *c_ro
         return GMAGNUS_ERROR_INVALID_VALUE;
     }
     return guarded([&] { do_numeric(plan, c_row_ptr, c_col_idx, c_val); });
+}
+
+gmagnus_status_t gmagnus_update_values(gmagnus_plan_t plan, const double *a_val, const double *b_val) {
+    if (!plan) {
+        set_last_error("NULL plan");
+        return GMAGNUS_ERROR_INVALID_VALUE;
+    }
+    return guarded([&] { do_update_values(plan, a_val, b_val); });
 }
 
 gmagnus_status_t gmagnus_plan_info(gmagnus_plan_t plan, gmagnus_plan_info_t *out) {

@@ -27,6 +27,7 @@ FLAG_PAPER_HISTOGRAM = 8
 FLAG_PAPER_EXPANSION = 16
 FLAG_SLICE_SPLIT = 32
 FLAG_LEVEL_BY_LEVEL = 64
+FLAG_KEEP_PATTERN = 256
 
 STATUS = {0: "SUCCESS", 1: "INVALID_VALUE", 2: "INVALID_CSR", 3: "OUT_OF_MEMORY", 4: "NOT_READY", 5: "HIP",
           6: "UNSUPPORTED"}
@@ -94,7 +95,8 @@ class PlanInfo(ctypes.Structure):
 
 EXPORTS = ["gmagnus_options_init", "gmagnus_get_params", "gmagnus_plan", "gmagnus_spgemm_symbolic",
            "gmagnus_spgemm_numeric", "gmagnus_plan_info", "gmagnus_plan_destroy", "gmagnus_row_products",
-           "gmagnus_split_panels", "gmagnus_release_cache", "gmagnus_last_error", "gmagnus_status_string"]
+           "gmagnus_split_panels", "gmagnus_release_cache", "gmagnus_last_error", "gmagnus_status_string",
+           "gmagnus_update_values"]
 
 _lib = None
 
@@ -115,6 +117,7 @@ def load(path: str = LIB_PATH):
                                  ctypes.POINTER(Options), P]
     lib.gmagnus_spgemm_symbolic.argtypes = [P, P, ctypes.POINTER(ctypes.c_int64)]
     lib.gmagnus_spgemm_numeric.argtypes = [P, P, P, P]
+    lib.gmagnus_update_values.argtypes = [P, P, P]
     lib.gmagnus_plan_info.argtypes = [P, ctypes.POINTER(PlanInfo)]
     lib.gmagnus_plan_destroy.argtypes = [P]
     lib.gmagnus_plan_destroy.restype = None
@@ -127,7 +130,7 @@ def load(path: str = LIB_PATH):
     lib.gmagnus_status_string.argtypes = [ctypes.c_int]
     lib.gmagnus_status_string.restype = ctypes.c_char_p
     for f in ("gmagnus_get_params", "gmagnus_plan", "gmagnus_spgemm_symbolic", "gmagnus_spgemm_numeric",
-              "gmagnus_plan_info", "gmagnus_row_products", "gmagnus_split_panels"):
+              "gmagnus_update_values", "gmagnus_plan_info", "gmagnus_row_products", "gmagnus_split_panels"):
         getattr(lib, f).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -235,6 +238,22 @@ class Plan:
                                                 col.data_ptr() if self.nnz else None,
                                                 val.data_ptr() if self.nnz else None))
         return col, val
+
+    def update_values(self, a_val: torch.Tensor, b_val: Optional[torch.Tensor] = None):
+        """New values of A and B (float64 device arrays in their CSR order) on
+        the same patterns; needs flags=FLAG_KEEP_PATTERN at construction. The next
+        numeric() writes C for these values. b_val defaults to a_val when the
+        plan's A and B are one matrix."""
+        if b_val is None:
+            if self.B is not self.A:
+                raise ValueError("b_val is required when A and B differ")
+            b_val = a_val
+        for t, m, name in ((a_val, self.A, "a_val"), (b_val, self.B, "b_val")):
+            if t.dtype != torch.float64 or not t.is_contiguous() or t.numel() < m.nnz:
+                raise ValueError("%s must be a contiguous float64 array of at least nnz entries" % name)
+        self._vals = (a_val, b_val)  # borrowed by the library until the next numeric phase ends
+        _check(self._lib.gmagnus_update_values(self._h, a_val.data_ptr() if self.A.nnz else None,
+                                               b_val.data_ptr() if self.B.nnz else None))
 
     def info(self) -> PlanInfo:
         out = PlanInfo()

@@ -36,20 +36,28 @@ def sample_rows(ip, n_random, n_heaviest, seed):
     return np.array(sorted(rows), dtype=np.int64)
 
 
-def run_sampled(g, A, rows, panel_products=PANEL_PRODUCTS, B=None):
+def run_sampled(g, A, rows, panel_products=PANEL_PRODUCTS, B=None, new_values=None):
     """Runs C = A*A (A*B when B is given) panel by panel; returns the sampled
-    rows' CSR and totals."""
+    rows' CSR and totals. With new_values = (a_val, b_val) every panel's plan
+    keeps its pattern, and C is recomputed for those values after the first
+    numeric phase (the sampled rows are those of the second result)."""
     dA = g.DeviceCSR.from_host(A)
     dB = dA if B is None else g.DeviceCSR.from_host(B)
     bounds = g.split_panels(dA, dB, panel_products)
+    if new_values is not None:
+        va = torch.from_numpy(new_values[0]).cuda()
+        vb = va if B is None else torch.from_numpy(new_values[1]).cuda()
     out_rp = [0]
     out_col, out_val = [], []
     total_nnz = total_products = 0
     for a, b in zip(bounds[:-1], bounds[1:]):
         sel = rows[(rows >= a) & (rows < b)]
-        with g.Plan(dA, dB, row_begin=a, row_end=b) as p:
+        with g.Plan(dA, dB, row_begin=a, row_end=b, flags=0 if new_values is None else g.FLAG_KEEP_PATTERN) as p:
             rp, nnz = p.symbolic()
             col, val = p.numeric()
+            if new_values is not None:
+                p.update_values(va, vb)
+                p.numeric(col, val)
             info = p.info()
         assert info.check_flags == 0
         total_nnz += nnz
@@ -112,3 +120,19 @@ def test_rmat20_pair_full(g):
     worst = compare_rows(np.arange(rows.size), rp, col, val, ref)
     print("rmat20_a32_b8: panels=%d products=%d nnz(C)=%d sampled_rows=%d max_rel_err=%.2e" % (
         panels, products, nnz, rows.size, worst))
+
+
+def test_rmat20_pair_pattern_reuse_full(g):
+    # the same pair at full size, every panel recomputed for new values of A
+    # and B on its kept pattern; sampled rows against the oracle's for the new values
+    A, B = wl.PAIRS["rmat20_a32_b8"].make()
+    rng = np.random.default_rng(21)
+    A2 = A.with_values(rng.uniform(-1.0, 1.0, A.nnz))
+    B2 = B.with_values(rng.uniform(-1.0, 1.0, B.nnz))
+    ip = oracle.row_products(A, B)
+    rows = sample_rows(ip, 300, 3, seed=21)
+    rp, col, val, nnz, products, panels = run_sampled(g, A, rows, B=B, new_values=(A2.val, B2.val))
+    assert products == int(ip.sum())
+    worst = compare_rows(np.arange(rows.size), rp, col, val, oracle.spgemm(A2, B2, rows=rows))
+    print("rmat20_a32_b8 new values: panels=%d nnz(C)=%d sampled_rows=%d max_rel_err=%.2e" % (
+        panels, nnz, rows.size, worst))

@@ -309,3 +309,58 @@ def test_sampled_rows_helper(g):
     rp, col, val, _ = run(g, A, A)
     rows = np.random.default_rng(0).choice(A.n_rows, 300, replace=False)
     compare_rows(rows, rp, col, val, oracle.spgemm(A, A, rows=rows))
+
+
+REUSE_CASES = [
+    ("no split", 0, {}),
+    ("one level", 0, dict(tau=600, dense_width_log2=8, chunks_max_log2=4)),
+    ("two levels in one pass", 0, dict(tau=300, dense_width_log2=7, chunks_max_log2=3)),
+    ("three levels", 0, dict(tau=200, dense_width_log2=6, chunks_max_log2=2)),
+    ("paper order", 16, dict(tau=200, dense_width_log2=6, chunks_max_log2=2)),
+    ("slice order", 32, dict(tau=300, dense_width_log2=7, chunks_max_log2=3)),
+    ("level by level", 64, dict(tau=300, dense_width_log2=7, chunks_max_log2=3)),
+]
+
+
+@pytest.mark.parametrize("name,flags,opts", REUSE_CASES, ids=[c[0] for c in REUSE_CASES])
+@pytest.mark.parametrize("same", [True, False], ids=["A*A", "A*B"])
+def test_pattern_reuse(g, name, flags, opts, same):
+    # symbolic once, then numeric for three value sets on the same patterns
+    # (new values through gmagnus_update_values): each C equals the oracle's
+    # for that value set, on the structure the first symbolic produced
+    A = RMAT12.make()
+    B = A if same else wl.rmat(12, 4, 0.57, 0.19, 0.19, 77)
+    dA = g.DeviceCSR.from_host(A)
+    dB = dA if same else g.DeviceCSR.from_host(B)
+    rng = np.random.default_rng(5)
+    with g.Plan(dA, dB, flags=flags | g.FLAG_KEEP_PATTERN, **opts) as p:
+        rp, nnz = p.symbolic()
+        rp_h = rp.cpu().numpy()
+        for it in range(3):
+            if it == 0:
+                A2, B2 = A, B
+            else:
+                A2 = A.with_values(rng.uniform(-1.0, 1.0, A.nnz))
+                B2 = A2 if same else B.with_values(rng.uniform(-1.0, 1.0, B.nnz))
+                va = torch.from_numpy(A2.val).cuda()
+                vb = va if same else torch.from_numpy(B2.val).cuda()
+                p.update_values(va, None if same else vb)
+            col, val = p.numeric()
+            info = p.info()
+            torch.cuda.synchronize()
+            assert info.check_flags == 0, info.check_flags
+            compare_full(rp_h, col.cpu().numpy(), val.cpu().numpy(), oracle.spgemm(A2, B2))
+        if opts:
+            assert info.levels_run >= 1
+
+
+def test_update_values_errors(g):
+    A = RMAT12.make()
+    dA = g.DeviceCSR.from_host(A)
+    with g.Plan(dA, dA, tau=300, dense_width_log2=7, chunks_max_log2=3) as p:
+        p.symbolic()
+        with pytest.raises(g.GmagnusError):
+            p.update_values(dA.val)  # plan made without FLAG_KEEP_PATTERN
+    with g.Plan(dA, dA, flags=g.FLAG_KEEP_PATTERN) as p:
+        with pytest.raises(g.GmagnusError):
+            p.update_values(dA.val)  # before symbolic
