@@ -395,6 +395,45 @@ __global__ void k_affine(int64_t *p, int64_t n, int64_t a) {
         p[i] = i * a;
 }
 
+// Greedy row panels from the row products' prefix sums pre[0..n]: from row
+// r a panel ends at the last e with pre[e] - pre[r] <= max_products (one row
+// at least). One work group; each search step tests SPLIT_BLOCK evenly
+// spaced rows of the remaining range at once (the sums are nondecreasing),
+// so a panel takes about log_256(n) steps. out[0] = the panel count (-1 when
+// max_panels do not reach row n); out[1 + i] = bound i.
+constexpr int SPLIT_BLOCK = 256;
+__global__ __launch_bounds__(SPLIT_BLOCK) void k_split_panels(const int64_t *pre, int64_t n, int64_t max_products,
+                                                              int64_t max_panels, int64_t *out) {
+    __shared__ int best;
+    const int t = threadIdx.x;
+    int64_t r = 0, cnt = 0;
+    if (t == 0) out[1] = 0;
+    while (r < n && cnt < max_panels) {
+        const int64_t target = pre[r] + max_products;
+        int64_t lo = r + 1, hi = n, e = r;  // the answer is the last e in [lo, hi] with pre[e] <= target, else r
+        while (lo <= hi) {
+            const int64_t span = hi - lo + 1;
+            const bool ok = pre[lo + span * t / SPLIT_BLOCK] <= target;
+            if (t == 0) best = -1;
+            __syncthreads();
+            if (ok) atomicMax(&best, t);
+            __syncthreads();
+            const int b = best;
+            __syncthreads();
+            if (b < 0) break;  // pre[lo] is past the target
+            e = lo + span * b / SPLIT_BLOCK;
+            const int64_t next = b + 1 < SPLIT_BLOCK ? lo + span * (b + 1) / SPLIT_BLOCK : hi + 1;
+            lo = e + 1;
+            hi = next - 1;
+        }
+        if (e <= r) e = r + 1;
+        ++cnt;
+        if (t == 0) out[1 + cnt] = e;
+        r = e;
+    }
+    if (t == 0) out[0] = r < n ? -1 : cnt;
+}
+
 __global__ void k_copy_i64(int64_t *dst, const int64_t *src, int64_t n) {
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
         dst[i] = src[i];
@@ -1349,25 +1388,33 @@ gmagnus_status_t gmagnus_split_panels(const gmagnus_csr_t *A, const gmagnus_csr_
                    "bad panel arguments");
         const int64_t n = A->n_rows;
         hipStream_t s = (hipStream_t)hip_stream;
-        std::vector<int64_t> pre(n + 1, 0);
-        if (n > 0) {
-            Workspace ws(nullptr, s);
-            int64_t *ip = ws.alloc<int64_t>(n), *sc = ws.alloc<int64_t>(n + 1);
-            int64_t *scratch = ws.alloc<int64_t>(scan_scratch_elems(n));
-            row_products(to_csr(A), to_csr(B), 0, n, A->nnz, ip, nullptr, nullptr, s);
-            scan_i64(ip, n, sc, scratch, s);
-            GM_HIP(hipMemcpyAsync(pre.data(), sc, sizeof(int64_t) * (n + 1), hipMemcpyDeviceToHost, s));
-            GM_HIP(hipStreamSynchronize(s));
-        }
-        int64_t cnt = 0, r = 0;
         bounds[0] = 0;
-        while (r < n) {
-            // furthest end e > r with pre[e] - pre[r] <= max_products (at least one row)
-            int64_t e = std::upper_bound(pre.begin() + r + 1, pre.end(), pre[r] + max_products) - pre.begin() - 1;
-            if (e <= r) e = r + 1;
-            GM_REQUIRE(cnt < max_panels, GMAGNUS_ERROR_INVALID_VALUE, "more panels needed than max_panels");
-            bounds[++cnt] = e;
-            r = e;
+        *n_panels = 0;
+        if (n == 0) return;
+        Workspace ws(nullptr, s);
+        int64_t *ip = ws.alloc<int64_t>(n), *sc = ws.alloc<int64_t>(n + 1);
+        int64_t *scratch = ws.alloc<int64_t>(scan_scratch_elems(n));
+        int64_t *out = ws.alloc<int64_t>(max_panels + 2);
+        row_products(to_csr(A), to_csr(B), 0, n, A->nnz, ip, nullptr, nullptr, s);
+        scan_i64(ip, n, sc, scratch, s);
+        hipLaunchKernelGGL(k_split_panels, dim3(1), dim3(SPLIT_BLOCK), 0, s, sc, n, max_products, max_panels, out);
+        GM_CHECK_LAUNCH();
+        // the count and the first bounds in one read; more panels than that in a second
+        const int64_t first = std::min<int64_t>(max_panels + 2, READ_SLOTS);
+        std::vector<int64_t> head(first);
+        {
+            HostReads r(s);
+            r.add(out, (int)first, head.data());
+            r.wait();
+        }
+        const int64_t cnt = head[0];
+        GM_REQUIRE(cnt >= 1, GMAGNUS_ERROR_INVALID_VALUE, "more panels needed than max_panels");
+        const int64_t have = std::min<int64_t>(cnt + 1, first - 1);
+        std::copy(head.begin() + 1, head.begin() + 1 + have, bounds);
+        if (cnt + 1 > have) {
+            GM_HIP(hipMemcpyAsync(bounds + have, out + 1 + have, sizeof(int64_t) * (cnt + 1 - have),
+                                  hipMemcpyDeviceToHost, s));
+            GM_HIP(hipStreamSynchronize(s));
         }
         *n_panels = cnt;
     });

@@ -251,6 +251,32 @@ def test_panels_concatenate_to_full(g):
         assert np.all(np.abs(val - ref.val[s:e]) <= 1e-12 * ref.bound[s:e])
 
 
+def greedy_panels(pre, max_products):
+    """The split the header specifies: from row r, the furthest end e with
+    pre[e] - pre[r] <= max_products, at least one row."""
+    n = pre.size - 1
+    out, r = [0], 0
+    while r < n:
+        e = int(np.searchsorted(pre, pre[r] + max_products, side="right")) - 1
+        r = max(e, r + 1)
+        out.append(r)
+    return out
+
+
+def test_split_panels_greedy_bounds(g):
+    # exact bounds for limits from one row per panel (4096 panels: more than
+    # one read of the bounds) to a single panel, with empty rows in between
+    A = wl.rmat(12, 8, 0.57, 0.19, 0.19, 12)
+    dA = g.DeviceCSR.from_host(A)
+    pre = np.concatenate([[0], np.cumsum(oracle.row_products(A, A))])
+    for mp in (1, 37, 5_000, 200_000, int(pre[-1]) - 1, int(pre[-1]), 1 << 40):
+        assert g.split_panels(dA, dA, mp) == greedy_panels(pre, mp), mp
+    n_need = len(greedy_panels(pre, 5_000)) - 1
+    assert len(g.split_panels(dA, dA, 5_000, max_panels=n_need)) == n_need + 1
+    with pytest.raises(g.GmagnusError):
+        g.split_panels(dA, dA, 5_000, max_panels=n_need - 1)
+
+
 def test_row_products_abi(g):
     A = wl.rmat(13, 16, 0.57, 0.19, 0.19, 77)
     dA = g.DeviceCSR.from_host(A)
