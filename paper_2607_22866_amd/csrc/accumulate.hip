@@ -36,6 +36,8 @@ struct GusLds {
     int32_t scan[BLOCK / GM_WAVE];
 };
 
+constexpr int GUS_ILP = 4;
+
 // Calls f(col, product) for every intermediate product of the A entries
 // [j0, j1) (one row of A), A entries taken in batches of BLOCK.
 template <int BLOCK, bool NUM, class F>
@@ -55,14 +57,25 @@ GM_DEV void gustavson_row(const Csr &A, const Csr &B, int64_t j0, int64_t j1, Gu
         const int32_t ex = block_excl_scan<BLOCK>(len, L.scan, &tot);
         if (tid < nb) L.off[tid] = ex;
         __syncthreads();
-        for (int32_t t = tid; t < tot; t += BLOCK) {
-            const int q = (int)find_row(L.off, 0, nb, t);
-            const int64_t src = L.bst[q] + (t - L.off[q]);
-            const int32_t c = B.ci[src];
-            if (NUM)
-                f(c, L.av[q] * B.v[src]);
-            else
-                f(c, 0.0);
+        // GUS_ILP products per thread are loaded before any is accumulated, so
+        // a row's B loads overlap instead of each waiting for the previous
+        // product's accumulator update
+        for (int32_t tb = tid; tb < tot; tb += BLOCK * GUS_ILP) {
+            int32_t c[GUS_ILP];
+            double v[GUS_ILP];
+#pragma unroll
+            for (int u = 0; u < GUS_ILP; ++u) {
+                const int32_t t = tb + u * BLOCK;
+                if (t < tot) {
+                    const int q = (int)find_row(L.off, 0, nb, t);
+                    const int64_t src = L.bst[q] + (t - L.off[q]);
+                    c[u] = B.ci[src];
+                    v[u] = NUM ? L.av[q] * B.v[src] : 0.0;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < GUS_ILP; ++u)
+                if (tb + u * BLOCK < tot) f(c[u], v[u]);
         }
         __syncthreads();
     }
