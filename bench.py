@@ -240,7 +240,7 @@ def main():
                          "and B on the kept patterns) against the full product on the same plans")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: this build measures the single-GPU hot path "
+        print("bench.py runs on one GPU only: it measures the single-GPU hot path "
               "(row panels are independent; a multi-GPU run would shard panels, which is not built)",
               file=sys.stderr)
         sys.exit(2)
