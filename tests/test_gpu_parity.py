@@ -345,6 +345,8 @@ REUSE_CASES = [
     ("paper order", 16, dict(tau=200, dense_width_log2=6, chunks_max_log2=2)),
     ("slice order", 32, dict(tau=300, dense_width_log2=7, chunks_max_log2=3)),
     ("level by level", 64, dict(tau=300, dense_width_log2=7, chunks_max_log2=3)),
+    # the replay runs on the heavy rows' own stream, joined to the plan's by events
+    ("two streams", 128, dict(tau=300, dense_width_log2=7, chunks_max_log2=3)),
 ]
 
 
