@@ -10,6 +10,8 @@ Contents
 - :func:`spgemm` / :func:`row_products` -- plain Gustavson with a sorted,
   compensated per-row accumulator (C code in ``spgemm_oracle.c``; paper
   Section II-B, Eq. gustav and Algorithm 1).
+- :func:`row_counts` -- the symbolic phase alone (distinct columns per row)
+  by column marking, fast enough for whole R-MAT scale-22/23 products.
 - :mod:`oracle.params` -- the parameter selection of Section III-D
   (``GetMagnusParams``), pinned to the chunk counts the paper prints.
 - :mod:`oracle.reference` -- small numpy references for the heavy-row
@@ -60,6 +62,8 @@ def _load():
         lib.oracle_fill_rows.argtypes = [P, P, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
         lib.oracle_fill_rows.restype = ctypes.c_int
+        lib.oracle_row_counts.argtypes = [P, P, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
+        lib.oracle_row_counts.restype = ctypes.c_int
         lib.oracle_threads.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -86,6 +90,22 @@ def row_products(A, B) -> np.ndarray:
     ip = np.empty(A.n_rows, np.int64)
     _load().oracle_row_products(ctypes.byref(da), ctypes.byref(db), ip.ctypes.data)
     return ip
+
+
+def row_counts(A, B, row_begin=0, row_end=None) -> np.ndarray:
+    """Distinct columns of each row of C = A*B in [row_begin, row_end) (the
+    symbolic phase, Section II-B), counted by marking columns; no products are
+    formed, so whole R-MAT products take minutes on a few cores."""
+    _check_inner(A, B)
+    row_end = A.n_rows if row_end is None else row_end
+    if not 0 <= row_begin <= row_end <= A.n_rows:
+        raise ValueError("bad row range")
+    da, ka = _desc(A)
+    db, kb = _desc(B)
+    counts = np.empty(row_end - row_begin, np.int64)
+    if _load().oracle_row_counts(ctypes.byref(da), ctypes.byref(db), row_begin, row_end, counts.ctypes.data):
+        raise MemoryError("oracle could not allocate its column stamps")
+    return counts
 
 
 @dataclass

@@ -164,4 +164,49 @@ int oracle_fill_rows(const oracle_csr *A, const oracle_csr *B, const int64_t *ro
     return failed ? -1 : 0;
 }
 
+/* Symbolic by marking, for whole matrices: counts[i - row_begin] = number of
+ * distinct columns of C[i, :] for i in [row_begin, row_end). Each thread
+ * keeps one stamp per column of C, the last row that reached that column; a
+ * product adds one to its row's count when it is the first to reach its
+ * column for that row. This is the distinct-column count of the symbolic
+ * phase (Section II-B) without forming or sorting the products, so it
+ * finishes whole R-MAT products on a few cores. Returns 0, or -1 when the
+ * stamp arrays cannot be allocated. */
+int oracle_row_counts(const oracle_csr *A, const oracle_csr *B, int64_t row_begin, int64_t row_end,
+                      int64_t *counts) {
+    int failed = 0;
+    if (row_end - row_begin > ((int64_t)1 << 31) - 2) return -1;
+#pragma omp parallel
+    {
+        int32_t *stamp = (int32_t *)malloc((size_t)(B->n_cols > 0 ? B->n_cols : 1) * sizeof(int32_t));
+        if (!stamp) {
+#pragma omp atomic write
+            failed = 1;
+        } else {
+            for (int64_t c = 0; c < B->n_cols; ++c) stamp[c] = -1;
+        }
+#pragma omp barrier
+        if (!failed) {
+#pragma omp for schedule(dynamic, 64)
+            for (int64_t i = row_begin; i < row_end; ++i) {
+                const int32_t mark = (int32_t)(i - row_begin);
+                int64_t n = 0;
+                for (int64_t p = A->row_ptr[i]; p < A->row_ptr[i + 1]; ++p) {
+                    const int32_t j = A->col[p];
+                    for (int64_t r = B->row_ptr[j]; r < B->row_ptr[j + 1]; ++r) {
+                        const int32_t c = B->col[r];
+                        if (stamp[c] != mark) {
+                            stamp[c] = mark;
+                            ++n;
+                        }
+                    }
+                }
+                counts[i - row_begin] = n;
+            }
+        }
+        free(stamp);
+    }
+    return failed ? -1 : 0;
+}
+
 int oracle_threads(void) { return omp_get_max_threads(); }

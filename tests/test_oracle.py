@@ -14,7 +14,6 @@ import pytest
 
 import oracle
 import workloads as wl
-from oracle import reference
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 
@@ -268,38 +267,71 @@ def test_planner_mi355x_values():
     assert get_magnus_params(1 << 20, 233472).group_rows == 2
 
 
-# ------------------------------------------------------ reorder-step references
+# ------------------------------------------------- symbolic counts by marking
 
-def test_reference_multisplit_figure1_example():
-    # Section III-A: two heavy rows, C.m = 8, two chunks, one level -> four
-    # C_reord rows; the upper chunks (1 and 3) move columns [4, 8) to [0, 4).
-    rows = [(np.array([0, 5, 3, 7, 5]), np.array([1.0, 2.0, 3.0, 4.0, 5.0])),
-            (np.array([6, 1, 4]), np.array([6.0, 7.0, 8.0]))]
-    chunks, order, nh = reference.multisplit(rows, 8, 2, tau=None)
-    assert nh == 0 and order == [(0, 0), (0, 1), (1, 0), (1, 1)]
-    assert list(chunks[(0, 0)][0]) == [0, 3]
-    assert list(chunks[(0, 1)][0]) == [1, 1, 3] and list(chunks[(0, 1)][1]) == [2.0, 5.0, 4.0]
-    assert list(chunks[(1, 0)][0]) == [1]
-    assert list(chunks[(1, 1)][0]) == [0, 2]
-    # conservation: every element lands in exactly one chunk
-    assert sum(c[0].size for c in chunks.values()) == 8
-    # heavy-first ordering with a threshold
-    chunks, order, nh = reference.multisplit(rows, 8, 2, tau=2)
-    assert nh == 1 and order[0] == (0, 1)
+@pytest.mark.parametrize("make", [
+    lambda: (wl.rmat(11, 8, 0.57, 0.19, 0.19, 7),) * 2,
+    lambda: (wl.uniform(300, 200, 0.05, 8), wl.uniform(200, 500, 0.03, 9)),
+    lambda: (wl.banded(3000, 13, 10),) * 2,
+    lambda: (wl.erdos_renyi(2000, 2000, 16, 11),) * 2,
+    lambda: (wl.empty(7, 5), wl.uniform(5, 9, 0.5, 12)),
+])
+def test_row_counts_match_sorted_runs(make):
+    # two independent ways to the symbolic result: runs of the stably sorted
+    # products (spgemm) and column marking without any product (row_counts)
+    A, B = make()
+    C = oracle.spgemm(A, B)
+    counts = oracle.row_counts(A, B)
+    assert np.array_equal(counts, np.diff(C.row_ptr))
+    # a row range gives the same counts as the whole
+    a, b = A.n_rows // 3, A.n_rows - A.n_rows // 4
+    assert np.array_equal(oracle.row_counts(A, B, a, b), counts[a:b])
 
 
-def test_reference_expand_matches_oracle_sums():
-    A = wl.rmat(8, 8, 0.57, 0.19, 0.19, 3)
-    ip = oracle.row_products(A, A)
-    heavy, light = reference.split_rows(ip, 40)
-    assert heavy.size + light.size == A.n_rows and np.all(ip[heavy] > 40)
-    ex = reference.expand(A, A, heavy)
-    C = oracle.spgemm(A, A, rows=heavy)
-    for t, (cols, vals) in enumerate(ex):
-        assert cols.size == ip[heavy[t]]
-        c, v, b = C.row(t)
-        u, inv = np.unique(cols, return_inverse=True)
-        sums = np.zeros(u.size)
-        np.add.at(sums, inv, vals)
-        assert np.array_equal(u, c)
-        assert np.all(np.abs(sums - v) <= 1e-13 * b)
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_row_counts_dense_pattern(seed):
+    A = wl.uniform(40, 30, 0.15, seed)
+    B = wl.uniform(30, 50, 0.1, seed + 10)
+    pattern = (A.pattern_dense().astype(np.int64) @ B.pattern_dense().astype(np.int64)) > 0
+    assert np.array_equal(oracle.row_counts(A, B), pattern.sum(axis=1))
+
+
+def test_row_counts_banded_closed_form():
+    # half-width 13: row i of C spans columns max(0, i-26) .. min(n-1, i+26)
+    n = 1 << 16
+    A = wl.banded(n, 13, 3)
+    counts = oracle.row_counts(A, A)
+    i = np.arange(n)
+    assert np.array_equal(counts, np.minimum(n - 1, i + 26) - np.maximum(0, i - 26) + 1)
+    assert int(counts.sum()) == 53 * n - 702
+
+
+def test_structure_golden_files():
+    # the stored digests of the full-size workloads are internally consistent
+    # and agree with the closed forms where one exists
+    from oracle import golden_structure
+
+    for name in golden_structure.DEFAULT:
+        g = golden_structure.read(name)
+        assert g["config"] == name and len(g["blocks"]) == g["n_blocks"]
+        assert sum(b[2] for b in g["blocks"]) == g["nnz_c"]
+        assert g["blocks"][0][0] == 0 and g["blocks"][-1][1] == g["n_rows"]
+        assert all(x[1] == y[0] for x, y in zip(g["blocks"][:-1], g["blocks"][1:]))
+    b = golden_structure.read("banded20")
+    n = b["n_rows"]
+    assert b["nnz_c"] == 53 * n - 702 and b["products"] == 729 * n - 8190 and b["nnz_a"] == 27 * n - 182
+    e = golden_structure.read("er22")
+    assert e["products"] == 1 << 30 and (1 << 30) - 100_000 < e["nnz_c"] <= 1 << 30
+
+
+def test_structure_digests_small():
+    # the digest of a small matrix's counts, recomputed from its row pointers
+    import hashlib
+
+    from oracle import golden_structure
+
+    A = wl.rmat(10, 8, 0.57, 0.19, 0.19, 4)
+    C = oracle.spgemm(A, A)
+    whole, per = golden_structure.structure_digests(oracle.row_counts(A, A), 8)
+    assert whole == hashlib.sha256(np.ascontiguousarray(C.row_ptr, "<i8").tobytes()).hexdigest()
+    assert sum(p[2] for p in per) == C.row_ptr[-1]
