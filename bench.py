@@ -82,12 +82,11 @@ def run_step(g, dA, dB, bounds, timing, acc, c_bufs, extra_flags=0, tau=0):
             info = p.info() if timing else None
         nnz += n
         if info is not None:
+            if info.check_flags != 0:
+                raise RuntimeError("panel [%d, %d): the library's consistency flags are %d (a kernel's output "
+                                   "disagreed with the symbolic phase); the step's result is wrong" % (
+                                       a, b, info.check_flags))
             products += info.products_total
-            # inputs of the unfused byte model (see unfused_model_bytes)
-            m = acc.setdefault("_model", [0, 0, 0])
-            m[0] += info.products_heavy
-            m[1] += sum(info.level_elems_in[i] for i in range(1, info.levels_run))
-            m[2] += info.c_nnz_heavy
             acc.setdefault("_levels", set()).add(info.params.n_levels)
             for i, k in enumerate(g.K_NAMES):
                 acc.setdefault(k, [0.0, 0, 0.0])
@@ -128,34 +127,33 @@ def reuse_pass(g, dA, dB, bounds, c_bufs, extra_flags=0, tau=0):
     return t_full, t_vals
 
 
-def unfused_model_bytes(products_heavy, elems_deeper_levels, c_nnz_heavy):
-    """Bytes the paper's unfused sequence of heavy-row kernels moves
-    (Algorithm 3 with Algorithms 4 and 5): C-hat written once (12 B per
-    product), at every multisplit level a 4 B histogram read plus a 12 B read
-    and a 12 B write of each element entering it (the first level takes all
-    products), the final chunks' symbolic (4 B) and numeric (12 B) reads, and
-    12 B per C entry written. The fused path here skips most of these passes,
-    so this figure over its time is a work rate, not bytes it moved."""
-    return (12.0 + 28.0 + 16.0) * products_heavy + 28.0 * elems_deeper_levels + 12.0 * c_nnz_heavy
+def measured_peaks(g):
+    """Streaming bandwidths of the library's probe kernels (4 GiB, 5 runs
+    each): the measured peaks the paper divides by in its speed-of-light
+    comparison (copy), with read-only and write-only ceilings beside it."""
+    import torch
 
-
-def copy_peak(torch, nbytes=4 << 30, reps=5):
-    """Device-to-device copy bandwidth (read + write bytes / time): the measured
-    peak the paper divides by in its speed-of-light comparison."""
-    src = torch.ones(nbytes // 8, dtype=torch.float64, device="cuda")
-    dst = torch.empty_like(src)
-    dst.copy_(src)
-    torch.cuda.synchronize()
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record()
-    for _ in range(reps):
-        dst.copy_(src)
-    b.record()
-    torch.cuda.synchronize()
-    gbs = 2.0 * nbytes * reps / (a.elapsed_time(b) / 1000.0) / 1e9
-    del src, dst
+    out = {k: g.bandwidth_probe(k) for k in ("read", "read_nt", "write", "write_nt", "copy")}
     torch.cuda.empty_cache()
-    return gbs
+    return out
+
+
+def cpu_description():
+    """Model name of the host CPU and the logical CPUs this process may use."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        logical = len(os.sched_getaffinity(0))
+    except AttributeError:
+        logical = os.cpu_count()
+    return model, logical
 
 
 def source_hash(kernel):
@@ -207,10 +205,15 @@ def cpu_baseline(A, B, ip, budget_products, seed=0):
     t0 = time.perf_counter()
     oracle.spgemm(A, B, rows=rows)
     dt = time.perf_counter() - t0
+    model, logical = cpu_description()
     return {
         "value": 2.0 * sample_products / dt / 1e9,
         "unit": "GFLOP/s",
         "cores": oracle.threads(),
+        "cores_meaning": "OpenMP threads the oracle ran with, one per logical CPU (hardware thread) this "
+                         "process may use",
+        "cpu_model": model,
+        "logical_cpus_visible": logical,
         "kind": "oracle",
         "sample": "%d rows drawn uniformly at random (seed %d), %d intermediate products, %.1f s" % (
             rows.size, seed, sample_products, dt),
@@ -267,8 +270,9 @@ def main():
     dA = g.DeviceCSR.from_host(A)
     dB = g.DeviceCSR.from_host(B) if pair else dA
     torch.cuda.synchronize()
-    copy_gbs = copy_peak(torch)
-    log("device copy bandwidth %.0f GB/s" % copy_gbs)
+    peaks = measured_peaks(g)
+    copy_gbs = peaks["copy"]
+    log("probe bandwidths (GB/s): " + ", ".join("%s %.0f" % kv for kv in peaks.items()))
 
     bounds = g.split_panels(dA, dB, int(args.panel_products))
     log("%d row panels (max %.2g products each)" % (len(bounds) - 1, args.panel_products))
@@ -330,8 +334,6 @@ def main():
     heavy_ms = sum(kernels[k]["ms_per_step"] for k in HEAVY_KERNELS if k in kernels)
     heavy_gb = sum(kernels[k]["gb_per_step"] for k in HEAVY_KERNELS if k in kernels)
     all_ms = sum(v["ms_per_step"] for v in kernels.values())
-    mh = acc.get("_model", [0, 0, 0])
-    model_gbs = (unfused_model_bytes(*mh) / args.steps / 1e9 / (heavy_ms / 1000.0)) if heavy_ms and mh[0] else None
     all_gb = sum(v["gb_per_step"] for v in kernels.values())
 
     out = {
@@ -355,12 +357,13 @@ def main():
                              "heavy_path_frac_of_copy": (heavy_gb / (heavy_ms / 1000.0)) / copy_gbs
                              if heavy_ms else None,
                              "copy_peak": copy_gbs,
-                             "unfused_model_equivalent": model_gbs,
-                             "unfused_model_frac": model_gbs / HBM_PEAK_GBS if model_gbs else None,
+                             "probe_peaks": peaks,
                              "all_kernels": all_gb / (all_ms / 1000.0) if all_ms else None,
                              "end_to_end": all_gb / (elapsed / args.steps)},
         "roofline": roofline,
         "kernels": kernels,
+        "kernel_ms_sum_per_step": all_ms,
+        "check_flags": 0,
     }
     if args.pattern_reuse:
         t_full, t_vals = reuse_pass(g, dA, dB, bounds, c_bufs, extra, args.tau)

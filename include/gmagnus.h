@@ -78,6 +78,10 @@ typedef struct {
     void *(*alloc)(size_t bytes, void *stream, void *ctx);
     void (*free)(void *ptr, void *stream, void *ctx);
     void *alloc_ctx;
+    /* Bound on the device workspace one plan holds at any time, in bytes
+     * (0 = none). A plan that would need more fails with
+     * GMAGNUS_ERROR_OUT_OF_MEMORY and releases what it holds. */
+    int64_t workspace_limit_bytes;
 } gmagnus_options_t;
 
 #define GMAGNUS_FLAG_TIMING 1u         /* record per-phase device times (HIP events) into the plan info */
@@ -151,12 +155,24 @@ typedef struct {
     int64_t c_nnz;                 /* nonzeros of the panel of C (after symbolic) */
     int64_t c_nnz_heavy;           /* of which in heavy rows */
     int32_t check_flags;           /* nonzero: a kernel's output count disagreed with symbolic (a bug) */
+    int32_t expansion_path;        /* GMAGNUS_PATH_* the heavy rows took */
+    int64_t workspace_peak_bytes;  /* largest device workspace the plan has held */
     /* Under GMAGNUS_FLAG_TIMING: summed device milliseconds, launches and
      * algorithmic (compulsory) HBM bytes per kernel class. */
     double kernel_ms[GMAGNUS_K_COUNT];
     int64_t kernel_launches[GMAGNUS_K_COUNT];
     double kernel_bytes[GMAGNUS_K_COUNT];
 } gmagnus_plan_info_t;
+
+/* Expansion orders of the heavy rows (Section III-B), as chosen by
+ * gmagnus_expansion_path and reported in gmagnus_plan_info_t. */
+enum {
+    GMAGNUS_PATH_NONE = 0,           /* no heavy rows */
+    GMAGNUS_PATH_PAPER = 1,          /* C-hat written row by row (Algorithm 4), then split level by level */
+    GMAGNUS_PATH_SLICE_SPLIT = 2,    /* first level split during a slice-order expansion (atomic cursors) */
+    GMAGNUS_PATH_ROWS = 3,           /* first level split during a chunk-major row-order expansion */
+    GMAGNUS_PATH_ROWS_TWO_LEVEL = 4  /* both levels of a two-level hierarchy split during the row-order expansion */
+};
 
 typedef struct gmagnus_plan_s *gmagnus_plan_t;
 
@@ -169,6 +185,13 @@ void gmagnus_options_init(gmagnus_options_t *opts);
  * Errors: INVALID_VALUE for c_m < 1, lds_bytes < 1024 or inconsistent overrides. */
 gmagnus_status_t gmagnus_get_params(int64_t c_m, int64_t lds_bytes, const gmagnus_options_t *opts,
                                     gmagnus_params_t *out);
+
+/* Host-only: the expansion order a plan with these parameters takes for a
+ * panel with n_heavy heavy rows holding products_heavy products, with B
+ * holding b_nnz entries and the given GMAGNUS_FLAG_* bits. No device is
+ * touched. NULL params gives GMAGNUS_PATH_NONE. */
+int32_t gmagnus_expansion_path(const gmagnus_params_t *params, int64_t n_heavy, int64_t products_heavy,
+                               int64_t b_nnz, int32_t flags);
 
 /* Setup phase of Algorithm 3 for rows [row_begin, row_end) of C = A*B:
  * parameter selection, per-row product counts (InterOffsets) and the
@@ -237,6 +260,29 @@ gmagnus_status_t gmagnus_row_products(const gmagnus_csr_t *A, const gmagnus_csr_
  * max_panels panels are needed), OUT_OF_MEMORY, HIP. */
 gmagnus_status_t gmagnus_split_panels(const gmagnus_csr_t *A, const gmagnus_csr_t *B, int64_t max_products,
                                       int64_t *bounds, int64_t max_panels, int64_t *n_panels, void *hip_stream);
+
+/* Streaming bandwidth probe (the measured peak of the speed-of-light
+ * comparison, Section IV-C): runs one kernel of the given kind over `bytes`
+ * bytes (16-byte elements, grid-stride loop over `grid` work groups of 256
+ * threads; grid <= 0 picks one), once to warm up and then `reps` times, and
+ * returns the mean time of one run in *ms (host). Kinds:
+ *   READ, READ_NT   read src (ordinary / nontemporal loads); dst is a sink of
+ *                   at least 8 bytes that is written only if the loaded values
+ *                   sum to -1
+ *   WRITE, WRITE_NT write dst (ordinary / nontemporal stores)
+ *   COPY            copy src to dst (bytes read plus bytes written moved)
+ * src and dst are device pointers, 16-byte aligned, of `bytes` bytes (dst: 8
+ * bytes for the read kinds). Synchronises the stream.
+ * Errors: INVALID_VALUE (kind, sizes, alignment, NULL), HIP. */
+enum {
+    GMAGNUS_PROBE_READ = 0,
+    GMAGNUS_PROBE_READ_NT = 1,
+    GMAGNUS_PROBE_WRITE = 2,
+    GMAGNUS_PROBE_WRITE_NT = 3,
+    GMAGNUS_PROBE_COPY = 4
+};
+gmagnus_status_t gmagnus_bandwidth_probe(int32_t kind, void *dst, const void *src, int64_t bytes, int32_t grid,
+                                         int32_t reps, void *hip_stream, double *ms);
 
 /* Frees device blocks cached by the library's allocator (no plan may be alive). */
 void gmagnus_release_cache(void);

@@ -49,6 +49,7 @@ class Workspace {
             ufree_ = opts->free;
             uctx_ = opts->alloc_ctx;
         }
+        if (opts) limit_ = (size_t)(opts->workspace_limit_bytes > 0 ? opts->workspace_limit_bytes : 0);
     }
     ~Workspace() { release_all(); }
     Workspace(const Workspace &) = delete;
@@ -65,6 +66,8 @@ class Workspace {
     void hold(bool h) { hold_ = h; }
     void release_all();
     size_t bytes_in_use() const { return in_use_; }
+    size_t bytes_owned() const { return owned_; }
+    size_t peak_bytes() const { return peak_; }
 
   private:
     struct Block {
@@ -78,10 +81,23 @@ class Workspace {
     std::vector<Block> blocks_;  // owned, in use
     std::vector<Block> spare_;   // owned, freed by the plan
     size_t in_use_ = 0;
+    size_t owned_ = 0;           // bytes of blocks_ and spare_
+    size_t peak_ = 0;            // largest owned_
+    size_t limit_ = 0;           // bound on owned_ (0: none)
+    void give_back(const Block &b);
     bool hold_ = false;
 };
 
 void cache_release();
+
+// Builds a plan (gmagnus_plan); with no_alloc the plan's workspace comes only
+// from opts' callbacks and its host reads use pageable memory.
+gmagnus_status_t make_plan(gmagnus_plan_t *out, const gmagnus_csr_t *A, const gmagnus_csr_t *B,
+                           const gmagnus_options_t *opts, void *hip_stream, bool no_alloc);
+
+// Raises a kernel's dynamic LDS limit to `bytes` on the current device, once
+// per (device, kernel); thread-safe.
+void allow_dynamic_lds(const void *kernel, int bytes);
 
 // ----------------------------------------------------------------- prims.hip
 // Exclusive scan of n int64 values; out has n+1 entries (out[n] = total).

@@ -324,12 +324,7 @@ void launch_multisplit(const LevelGeom &g, const int64_t *in_ptr, const int64_t 
     const int K = g.group_rows << cbits;
     const int lds = ms_lds_bytes<BLOCK, TE>(K, next_counts ? g.next_chunks : 0, g.group_rows);
     GM_REQUIRE(lds <= MS_LDS_MAX, GMAGNUS_ERROR_UNSUPPORTED, "multisplit: work-group LDS above 160 KB");
-    static bool attr_set = false;
-    if (!attr_set) {
-        GM_HIP(hipFuncSetAttribute((const void *)k_multisplit<BLOCK, TE>,
-                                   hipFuncAttributeMaxDynamicSharedMemorySize, MS_LDS_MAX));
-        attr_set = true;
-    }
+    allow_dynamic_lds((const void *)k_multisplit<BLOCK, TE>, MS_LDS_MAX);
     hipLaunchKernelGGL((k_multisplit<BLOCK, TE>), dim3((unsigned)n_tiles), dim3(BLOCK), lds, s, g.n_in, g.elems,
                        in_ptr, tile_row, n_tiles, in_col, in_val, g.n_chunks, cbits, g.shift, g.group_rows, rbits,
                        x_map, cursor, out_col, out_val, n_heavy_out, g.next_chunks, g.next_shift, next_counts);

@@ -89,6 +89,26 @@ void cache_release() {
     c.free_blocks.clear();
 }
 
+void Workspace::give_back(const Block &b) {
+    if (ufree_)
+        ufree_(b.p, (void *)stream_, uctx_);
+    else
+        cache_free(b.p);
+    owned_ -= b.bytes;
+}
+
+void allow_dynamic_lds(const void *kernel, int bytes) {
+    static std::mutex m;
+    static std::map<std::pair<int, const void *>, int> done;  // (device, kernel) -> bytes allowed
+    int dev = 0;
+    GM_HIP(hipGetDevice(&dev));
+    std::lock_guard<std::mutex> lk(m);
+    auto it = done.find({dev, kernel});
+    if (it != done.end() && it->second >= bytes) return;
+    GM_HIP(hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes));
+    done[{dev, kernel}] = bytes;
+}
+
 void *Workspace::alloc_bytes(size_t bytes) {
     const size_t want = round_bytes(bytes);
     for (size_t i = 0; i < spare_.size(); ++i)
@@ -100,22 +120,36 @@ void *Workspace::alloc_bytes(size_t bytes) {
             in_use_ += b.bytes;
             return b.p;
         }
+    if (limit_ && owned_ + want > limit_) {
+        // blocks this plan freed count against the limit too: return them first
+        for (auto &b : spare_) give_back(b);
+        spare_.clear();
+        if (owned_ + want > limit_)
+            throw Error{GMAGNUS_ERROR_OUT_OF_MEMORY,
+                        "workspace limit of " + std::to_string(limit_) + " bytes reached: " + std::to_string(owned_) +
+                            " bytes in use, " + std::to_string(want) + " more requested"};
+    }
     void *p = nullptr;
     if (ualloc_) {
         p = ualloc_(want, (void *)stream_, uctx_);
-        if (!p) throw Error{GMAGNUS_ERROR_OUT_OF_MEMORY, "user allocator returned NULL"};
+        if (!p)
+            throw Error{GMAGNUS_ERROR_OUT_OF_MEMORY, "the workspace allocator returned NULL for " +
+                                                         std::to_string(want) + " bytes (" + std::to_string(owned_) +
+                                                         " bytes held by the plan)"};
     } else {
         try {
             p = cache_alloc(want);
         } catch (const Error &) {
             // give this plan's spare blocks back and retry once
-            for (auto &b : spare_) cache_free(b.p);
+            for (auto &b : spare_) give_back(b);
             spare_.clear();
             p = cache_alloc(want);
         }
     }
     blocks_.push_back({p, want});
     in_use_ += want;
+    owned_ += want;
+    peak_ = std::max(peak_, owned_);
     return p;
 }
 
@@ -133,15 +167,11 @@ void Workspace::free(void *p) {
 
 void Workspace::release_all() {
     for (auto *v : {&blocks_, &spare_})
-        for (auto &b : *v) {
-            if (ufree_)
-                ufree_(b.p, (void *)stream_, uctx_);
-            else
-                cache_free(b.p);
-        }
+        for (auto &b : *v) give_back(b);
     blocks_.clear();
     spare_.clear();
     in_use_ = 0;
+    owned_ = 0;
 }
 
 // --------------------------------------------------------------- planner
@@ -203,6 +233,10 @@ void compute_params(int64_t c_m, int64_t s_lm, const gmagnus_options_t *o, gmagn
 using namespace gm;
 
 // ------------------------------------------------------------------ plan
+namespace {
+struct Timed;
+}
+
 struct LeafLevel {
     LeafSet set;
     int width = 0;
@@ -251,7 +285,9 @@ struct gmagnus_plan_s {
     int64_t c_nnz = 0;
     gmagnus_plan_info_t info{};
     std::vector<TimedEvent> timers;
+    std::vector<Timed *> open_timers;  // timed scopes open now, innermost last
     bool timing = false;
+    bool no_alloc = false;  // workspace from the caller's callbacks only, host reads through pageable memory
 
     ~gmagnus_plan_s() {
         (void)hipStreamSynchronize(stream);
@@ -271,27 +307,62 @@ struct gmagnus_plan_s {
 
 namespace {
 
-// Records a pair of events around a group of launches of one kernel class.
+// Records events around a group of launches of one kernel class. Scopes do
+// not overlap in time: opening a scope pauses the one already open (its
+// interval ends where the inner one starts and resumes where it ends), and a
+// host read pauses every open scope for the time the host waits, so each
+// class's time is device time between its own launches, and the classes'
+// times add up to no more than the wall time.
 struct Timed {
     gmagnus_plan_s *p;
     int cls;
     hipStream_t s;
-    hipEvent_t a = nullptr, b = nullptr;
+    hipEvent_t a = nullptr;
     Timed(gmagnus_plan_s *p_, int cls_, hipStream_t s_) : p(p_), cls(cls_), s(s_) {
         if (!p->timing) return;
-        GM_HIP(hipEventCreate(&a));
-        GM_HIP(hipEventCreate(&b));
-        GM_HIP(hipEventRecord(a, s));
+        if (!p->open_timers.empty()) p->open_timers.back()->pause();
+        p->open_timers.push_back(this);
+        resume();
     }
     ~Timed() {
-        if (!p->timing || !a) return;
-        if (hipEventRecord(b, s) == hipSuccess)
-            p->timers.push_back({cls, a, b});
-        else {
+        if (!p->timing) return;
+        pause();
+        p->open_timers.pop_back();
+        if (!p->open_timers.empty()) p->open_timers.back()->resume();
+    }
+    Timed(const Timed &) = delete;
+    Timed &operator=(const Timed &) = delete;
+    void resume() {
+        if (hipEventCreate(&a) != hipSuccess) {
+            a = nullptr;
+            return;
+        }
+        if (hipEventRecord(a, s) != hipSuccess) {
             (void)hipEventDestroy(a);
-            (void)hipEventDestroy(b);
+            a = nullptr;
         }
     }
+    void pause() {
+        if (!a) return;
+        hipEvent_t b = nullptr;
+        if (hipEventCreate(&b) == hipSuccess && hipEventRecord(b, s) == hipSuccess) {
+            p->timers.push_back({cls, a, b});
+        } else {
+            (void)hipEventDestroy(a);
+            if (b) (void)hipEventDestroy(b);
+        }
+        a = nullptr;
+    }
+};
+
+// The plan whose entry point is running (set for the duration of each entry
+// point that runs a plan's phases): host reads pause its timed scopes, and
+// read through pageable memory for plans that must not allocate.
+thread_local gmagnus_plan_s *t_plan = nullptr;
+struct TimedPlanScope {
+    gmagnus_plan_s *prev;
+    explicit TimedPlanScope(gmagnus_plan_s *p) : prev(t_plan) { t_plan = p; }
+    ~TimedPlanScope() { t_plan = prev; }
 };
 
 // Pinned host staging for the small device-to-host reads of counts and bin
@@ -311,15 +382,23 @@ int64_t *read_buffer() {
 // staging buffer, wait() synchronises once and copies the values out.
 class HostReads {
   public:
-    explicit HostReads(hipStream_t s) : s_(s), buf_(read_buffer()) {}
+    explicit HostReads(hipStream_t s)
+        : s_(s), buf_(t_plan && t_plan->no_alloc ? local_ : read_buffer()) {}
+    ~HostReads() { resume_timers(); }
     void add(const int64_t *dev, int n, int64_t *host) {
         GM_REQUIRE(used_ + n <= READ_SLOTS && n_ < MAXR, GMAGNUS_ERROR_INVALID_VALUE, "too many host reads at once");
+        // the open timed scopes stop before the copies and resume after the host's wait
+        if (!tp_ && t_plan && t_plan->timing && !t_plan->open_timers.empty()) {
+            tp_ = t_plan;
+            tp_->open_timers.back()->pause();  // the innermost scope is the one running
+        }
         GM_HIP(hipMemcpyAsync(buf_ + used_, dev, sizeof(int64_t) * n, hipMemcpyDeviceToHost, s_));
         r_[n_++] = Read{host, n, used_};
         used_ += n;
     }
     void wait() {
         GM_HIP(hipStreamSynchronize(s_));
+        resume_timers();
         for (int i = 0; i < n_; ++i)
             for (int j = 0; j < r_[i].n; ++j) r_[i].host[j] = buf_[r_[i].at + j];
         n_ = used_ = 0;
@@ -330,11 +409,18 @@ class HostReads {
         int64_t *host;
         int n, at;
     };
+    void resume_timers() {
+        if (!tp_) return;
+        if (!tp_->open_timers.empty()) tp_->open_timers.back()->resume();
+        tp_ = nullptr;
+    }
     static constexpr int MAXR = 8;
     hipStream_t s_;
     int64_t *buf_;
     Read r_[MAXR];
     int n_ = 0, used_ = 0;
+    gmagnus_plan_s *tp_ = nullptr;  // plan whose timed scopes this read paused
+    int64_t local_[READ_SLOTS];     // pageable staging (plans that must not allocate)
 };
 
 int64_t read_scalar(const int64_t *dev, hipStream_t s) {
@@ -409,7 +495,8 @@ __global__ __launch_bounds__(SPLIT_BLOCK) void k_split_panels(const int64_t *pre
     int64_t r = 0, cnt = 0;
     if (t == 0) out[1] = 0;
     while (r < n && cnt < max_panels) {
-        const int64_t target = pre[r] + max_products;
+        // saturated: a limit near INT64_MAX means "no limit"
+        const int64_t target = max_products > INT64_MAX - pre[r] ? INT64_MAX : pre[r] + max_products;
         int64_t lo = r + 1, hi = n, e = r;  // the answer is the last e in [lo, hi] with pre[e] <= target, else r
         while (lo <= hi) {
             const int64_t span = hi - lo + 1;
@@ -543,6 +630,33 @@ void do_plan(gmagnus_plan_s *p, const gmagnus_csr_t *A, const gmagnus_csr_t *B, 
 
 void add_bytes(gmagnus_plan_s *p, int cls, double bytes) { p->info.kernel_bytes[cls] += bytes; }
 
+}  // namespace
+
+namespace gm {
+// Which expansion the heavy rows take (gmagnus_expansion_path). Without a
+// multisplit level, or when the paper's order is asked for, C-hat is written
+// row by row (Algorithm 4); otherwise the first level is split during the
+// expansion: in chunk-major row order when the offsets inside a (chunk, row)
+// region fit 32 bits, else in slice order. A hierarchy of exactly two levels
+// runs both levels inside the row-order expansion when its keys fit the work
+// group's LDS and B's entries can be indexed in 32 bits (the fine boundaries).
+int32_t expansion_path(const gmagnus_params_t &P, int64_t n_heavy, int64_t products_heavy, int64_t b_nnz,
+                       int32_t flags) {
+    if (n_heavy <= 0) return GMAGNUS_PATH_NONE;
+    const bool paper_hist = (flags & GMAGNUS_FLAG_PAPER_HISTOGRAM) != 0;
+    const bool fused = P.n_levels > 0 && !paper_hist && (flags & GMAGNUS_FLAG_PAPER_EXPANSION) == 0;
+    if (!fused) return GMAGNUS_PATH_PAPER;
+    const bool rows_order = (flags & GMAGNUS_FLAG_SLICE_SPLIT) == 0 && products_heavy < ((int64_t)1 << 32) &&
+                            n_heavy < ((int64_t)1 << 31);
+    if (!rows_order) return GMAGNUS_PATH_SLICE_SPLIT;
+    const bool two = P.n_levels == 2 && (flags & GMAGNUS_FLAG_LEVEL_BY_LEVEL) == 0 && b_nnz < ((int64_t)1 << 31) &&
+                     rows2_fits(P.tau, P.v_chunks[1], P.v_chunks[0] * P.v_chunks[1]);
+    return two ? GMAGNUS_PATH_ROWS_TWO_LEVEL : GMAGNUS_PATH_ROWS;
+}
+}  // namespace gm
+
+namespace {
+
 // Heavy path of the symbolic phase: masked CSC, expansion, multisplit
 // levels, final-chunk symbolic, fragment offsets. Runs on p->s_heavy.
 void heavy_symbolic(gmagnus_plan_s *p) {
@@ -572,15 +686,15 @@ void heavy_symbolic(gmagnus_plan_s *p) {
     const int64_t r0 = p->r0;
 
     const bool paper_hist = (p->opts.flags & GMAGNUS_FLAG_PAPER_HISTOGRAM) != 0;
+    const int32_t path = expansion_path(P, nh, H, p->B.nnz, p->opts.flags);
+    p->info.expansion_path = path;
     // split at the first level while expanding, unless the paper's order is asked for
-    const bool fused = P.n_levels > 0 && !paper_hist && (p->opts.flags & GMAGNUS_FLAG_PAPER_EXPANSION) == 0;
+    const bool fused = path != GMAGNUS_PATH_PAPER;
     // the fused split in chunk-major row order (32-bit offsets inside a row's chunk), else in slice order
-    const bool rows_order = fused && (p->opts.flags & GMAGNUS_FLAG_SLICE_SPLIT) == 0 &&
-                            H < ((int64_t)1 << 32) && nh < ((int64_t)1 << 31);
+    const bool rows_order = path == GMAGNUS_PATH_ROWS || path == GMAGNUS_PATH_ROWS_TWO_LEVEL;
     // a hierarchy of exactly two levels in one pass: the expansion splits its
     // heavy regions again and writes the final chunks directly
-    const bool two_level = rows_order && P.n_levels == 2 && (p->opts.flags & GMAGNUS_FLAG_LEVEL_BY_LEVEL) == 0 &&
-                           rows2_fits(P.tau, P.v_chunks[1], P.v_chunks[0] * P.v_chunks[1]);
+    const bool two_level = path == GMAGNUS_PATH_ROWS_TWO_LEVEL;
     int64_t *counts0 = nullptr;  // level-0 counts when computed from the structure
     int32_t *sbnd = nullptr;     // per-slice level-0 chunk boundaries (kept for the fused expansion)
     RowEntries ent;              // chunk-major row order: entries, their chunk offsets, the row pointers of A~
@@ -1269,6 +1383,33 @@ gmagnus_status_t guarded(F &&f) {
 
 }  // namespace
 
+namespace gm {
+gmagnus_status_t make_plan(gmagnus_plan_t *out, const gmagnus_csr_t *A, const gmagnus_csr_t *B,
+                           const gmagnus_options_t *opts, void *hip_stream, bool no_alloc) {
+    if (!out) {
+        set_last_error("NULL plan output");
+        return GMAGNUS_ERROR_INVALID_VALUE;
+    }
+    *out = nullptr;
+    gmagnus_plan_s *p = nullptr;
+    gmagnus_status_t st = guarded([&] {
+        p = new gmagnus_plan_s();
+        p->no_alloc = no_alloc;
+        TimedPlanScope tps(p);
+        if (no_alloc)
+            GM_REQUIRE(opts && opts->alloc && opts->free, GMAGNUS_ERROR_INVALID_VALUE,
+                       "a plan that must not allocate needs workspace callbacks");
+        do_plan(p, A, B, opts, (hipStream_t)hip_stream);
+    });
+    if (st != GMAGNUS_SUCCESS) {
+        delete p;
+        return st;
+    }
+    *out = p;
+    return st;
+}
+}  // namespace gm
+
 // =================================================================== C ABI
 extern "C" {
 
@@ -1288,24 +1429,15 @@ gmagnus_status_t gmagnus_get_params(int64_t c_m, int64_t lds_bytes, const gmagnu
     });
 }
 
+int32_t gmagnus_expansion_path(const gmagnus_params_t *params, int64_t n_heavy, int64_t products_heavy,
+                               int64_t b_nnz, int32_t flags) {
+    if (!params) return GMAGNUS_PATH_NONE;
+    return expansion_path(*params, n_heavy, products_heavy, b_nnz, flags);
+}
+
 gmagnus_status_t gmagnus_plan(gmagnus_plan_t *out, const gmagnus_csr_t *A, const gmagnus_csr_t *B,
                               const gmagnus_options_t *opts, void *hip_stream) {
-    if (!out) {
-        set_last_error("NULL plan output");
-        return GMAGNUS_ERROR_INVALID_VALUE;
-    }
-    *out = nullptr;
-    gmagnus_plan_s *p = nullptr;
-    gmagnus_status_t st = guarded([&] {
-        p = new gmagnus_plan_s();
-        do_plan(p, A, B, opts, (hipStream_t)hip_stream);
-    });
-    if (st != GMAGNUS_SUCCESS) {
-        delete p;
-        return st;
-    }
-    *out = p;
-    return st;
+    return gm::make_plan(out, A, B, opts, hip_stream, false);
 }
 
 gmagnus_status_t gmagnus_spgemm_symbolic(gmagnus_plan_t plan, int64_t *c_row_ptr, int64_t *c_nnz) {
@@ -1313,7 +1445,10 @@ gmagnus_status_t gmagnus_spgemm_symbolic(gmagnus_plan_t plan, int64_t *c_row_ptr
         set_last_error("NULL plan");
         return GMAGNUS_ERROR_INVALID_VALUE;
     }
-    return guarded([&] { do_symbolic(plan, c_row_ptr, c_nnz); });
+    return guarded([&] {
+        TimedPlanScope tps(plan);
+        do_symbolic(plan, c_row_ptr, c_nnz);
+    });
 }
 
 gmagnus_status_t gmagnus_spgemm_numeric(gmagnus_plan_t plan, const int64_t *c_row_ptr, int32_t *c_col_idx,
@@ -1322,7 +1457,10 @@ gmagnus_status_t gmagnus_spgemm_numeric(gmagnus_plan_t plan, const int64_t *c_ro
         set_last_error("NULL plan");
         return GMAGNUS_ERROR_INVALID_VALUE;
     }
-    return guarded([&] { do_numeric(plan, c_row_ptr, c_col_idx, c_val); });
+    return guarded([&] {
+        TimedPlanScope tps(plan);
+        do_numeric(plan, c_row_ptr, c_col_idx, c_val);
+    });
 }
 
 gmagnus_status_t gmagnus_update_values(gmagnus_plan_t plan, const double *a_val, const double *b_val) {
@@ -1330,7 +1468,10 @@ gmagnus_status_t gmagnus_update_values(gmagnus_plan_t plan, const double *a_val,
         set_last_error("NULL plan");
         return GMAGNUS_ERROR_INVALID_VALUE;
     }
-    return guarded([&] { do_update_values(plan, a_val, b_val); });
+    return guarded([&] {
+        TimedPlanScope tps(plan);
+        do_update_values(plan, a_val, b_val);
+    });
 }
 
 gmagnus_status_t gmagnus_plan_info(gmagnus_plan_t plan, gmagnus_plan_info_t *out) {
@@ -1359,6 +1500,7 @@ gmagnus_status_t gmagnus_plan_info(gmagnus_plan_t plan, gmagnus_plan_info_t *out
             GM_HIP(hipMemcpy(&f, plan->err, sizeof(f), hipMemcpyDeviceToHost));
             plan->info.check_flags = f;
         }
+        if (plan->ws) plan->info.workspace_peak_bytes = (int64_t)plan->ws->peak_bytes();
         *out = plan->info;
     });
 }

@@ -900,12 +900,7 @@ void expand_rows2(const Csr &B, const RowEntries &ent, const uint32_t *pre, cons
                        reg_c, reg_efirst, reg_ne, pre, nc, total, n_tiles, info);
     GM_CHECK_LAUNCH();
     const int lds = rs2_layout(K).total;
-    static bool attr_set = false;
-    if (!attr_set) {
-        GM_HIP(hipFuncSetAttribute((const void *)k_expand_rows2, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                   rs2_layout(RS2_KMAX).total));
-        attr_set = true;
-    }
+    allow_dynamic_lds((const void *)k_expand_rows2, rs2_layout(RS2_KMAX).total);
     Rs2Args a{B,       ent,   pre,   bnd,  out_ptr, seg_base, reg_c,    reg_efirst, n_out,   n_heavy_out,
               total,   n_tiles, info, nc,  shift,   nc1,      shift1,   R,          cursor1, n_out1_elems,
               err,     out_col0, out_val0, out_col1, out_val1};

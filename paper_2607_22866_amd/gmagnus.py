@@ -28,6 +28,7 @@ FLAG_PAPER_EXPANSION = 16
 FLAG_SLICE_SPLIT = 32
 FLAG_LEVEL_BY_LEVEL = 64
 FLAG_KEEP_PATTERN = 256
+PATH_NAMES = {0: "none", 1: "paper", 2: "slice_split", 3: "rows", 4: "rows_two_level"}
 
 STATUS = {0: "SUCCESS", 1: "INVALID_VALUE", 2: "INVALID_CSR", 3: "OUT_OF_MEMORY", 4: "NOT_READY", 5: "HIP",
           6: "UNSUPPORTED"}
@@ -52,7 +53,8 @@ class Options(ctypes.Structure):
     _fields_ = [("struct_size", ctypes.c_size_t), ("row_begin", ctypes.c_int64), ("row_end", ctypes.c_int64),
                 ("lds_bytes", ctypes.c_int64), ("tau", ctypes.c_int64), ("dense_width_log2", ctypes.c_int32),
                 ("chunks_max_log2", ctypes.c_int32), ("validate", ctypes.c_int32), ("flags", ctypes.c_int32),
-                ("alloc", ALLOC_FN), ("free", FREE_FN), ("alloc_ctx", ctypes.c_void_p)]
+                ("alloc", ALLOC_FN), ("free", FREE_FN), ("alloc_ctx", ctypes.c_void_p),
+                ("workspace_limit_bytes", ctypes.c_int64)]
 
 
 class Params(ctypes.Structure):
@@ -74,6 +76,7 @@ class PlanInfo(ctypes.Structure):
                 ("n_leaves_dense", ctypes.c_int64), ("n_leaves_hash", ctypes.c_int64),
                 ("n_leaves_rank", ctypes.c_int64), ("c_nnz", ctypes.c_int64),
                 ("c_nnz_heavy", ctypes.c_int64), ("check_flags", ctypes.c_int32),
+                ("expansion_path", ctypes.c_int32), ("workspace_peak_bytes", ctypes.c_int64),
                 ("kernel_ms", ctypes.c_double * len(K_NAMES)), ("kernel_launches", ctypes.c_int64 * len(K_NAMES)),
                 ("kernel_bytes", ctypes.c_double * len(K_NAMES))]
 
@@ -96,7 +99,7 @@ class PlanInfo(ctypes.Structure):
 EXPORTS = ["gmagnus_options_init", "gmagnus_get_params", "gmagnus_plan", "gmagnus_spgemm_symbolic",
            "gmagnus_spgemm_numeric", "gmagnus_plan_info", "gmagnus_plan_destroy", "gmagnus_row_products",
            "gmagnus_split_panels", "gmagnus_release_cache", "gmagnus_last_error", "gmagnus_status_string",
-           "gmagnus_update_values"]
+           "gmagnus_update_values", "gmagnus_expansion_path", "gmagnus_bandwidth_probe"]
 
 _lib = None
 
@@ -124,6 +127,12 @@ def load(path: str = LIB_PATH):
     lib.gmagnus_row_products.argtypes = [ctypes.POINTER(CsrDesc), ctypes.POINTER(CsrDesc), P, P]
     lib.gmagnus_split_panels.argtypes = [ctypes.POINTER(CsrDesc), ctypes.POINTER(CsrDesc), ctypes.c_int64, P,
                                          ctypes.c_int64, ctypes.POINTER(ctypes.c_int64), P]
+    lib.gmagnus_expansion_path.argtypes = [ctypes.POINTER(Params), ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                                           ctypes.c_int32]
+    lib.gmagnus_expansion_path.restype = ctypes.c_int32
+    lib.gmagnus_bandwidth_probe.argtypes = [ctypes.c_int32, P, P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P,
+                                            ctypes.POINTER(ctypes.c_double)]
+    lib.gmagnus_bandwidth_probe.restype = ctypes.c_int
     lib.gmagnus_release_cache.argtypes = []
     lib.gmagnus_release_cache.restype = None
     lib.gmagnus_last_error.restype = ctypes.c_char_p
@@ -159,6 +168,21 @@ def get_params(c_m: int, lds_bytes: int = 163840, **overrides) -> Params:
     o = make_options(**overrides)
     _check(load().gmagnus_get_params(c_m, lds_bytes, ctypes.byref(o), ctypes.byref(p)))
     return p
+
+
+def expansion_path(params: Params, n_heavy: int, products_heavy: int, b_nnz: int, flags: int = 0) -> str:
+    """Host-only: the expansion order a plan with these parameters takes (a PATH_NAMES value)."""
+    return PATH_NAMES[int(load().gmagnus_expansion_path(ctypes.byref(params), n_heavy, products_heavy, b_nnz,
+                                                        flags))]
+
+
+def _require_device(t: torch.Tensor, device: torch.device, name: str):
+    """The library reads and writes device memory only: a host tensor's pointer
+    handed to a kernel would fault the GPU, so it is refused here."""
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError("%s must be a CUDA tensor" % name)
+    if t.device != device:
+        raise ValueError("%s is on %s, the plan's matrices on %s" % (name, t.device, device))
 
 
 @dataclass
@@ -209,8 +233,9 @@ class Plan:
         self._opts = make_options(**options)
         self._stream = stream
         self._h = ctypes.c_void_p()
-        _check(self._lib.gmagnus_plan(ctypes.byref(self._h), ctypes.byref(self._da), ctypes.byref(self._db),
-                                      ctypes.byref(self._opts), _stream(stream)))
+        make = self._lib.gmagnus_plan
+        _check(make(ctypes.byref(self._h), ctypes.byref(self._da), ctypes.byref(self._db), ctypes.byref(self._opts),
+                    _stream(stream)))
         rb = self._opts.row_begin
         re = self._opts.row_end if self._opts.row_end > 0 else A.n_rows
         self.n_rows = re - rb
@@ -232,6 +257,10 @@ class Plan:
             col = torch.empty(self.nnz, dtype=torch.int32, device=dev)
         if val is None:
             val = torch.empty(self.nnz, dtype=torch.float64, device=dev)
+        for t, dt, name in ((col, torch.int32, "col"), (val, torch.float64, "val")):
+            _require_device(t, dev, name)
+            if t.dtype != dt or not t.is_contiguous():
+                raise ValueError("%s must be a contiguous %s array" % (name, dt))
         if col.numel() < self.nnz or val.numel() < self.nnz:
             raise ValueError("output arrays smaller than nnz")
         _check(self._lib.gmagnus_spgemm_numeric(self._h, self.row_ptr.data_ptr(),
@@ -249,6 +278,7 @@ class Plan:
                 raise ValueError("b_val is required when A and B differ")
             b_val = a_val
         for t, m, name in ((a_val, self.A, "a_val"), (b_val, self.B, "b_val")):
+            _require_device(t, self.A.row_ptr.device, name)
             if t.dtype != torch.float64 or not t.is_contiguous() or t.numel() < m.nnz:
                 raise ValueError("%s must be a contiguous float64 array of at least nnz entries" % name)
         self._vals = (a_val, b_val)  # borrowed by the library until the next numeric phase ends
@@ -301,6 +331,24 @@ def split_panels(A: DeviceCSR, B: DeviceCSR, max_products: int, max_panels: int 
     _check(load().gmagnus_split_panels(ctypes.byref(da), ctypes.byref(db), max_products, bounds, max_panels,
                                        ctypes.byref(n), _stream(stream)))
     return [int(bounds[i]) for i in range(n.value + 1)]
+
+
+PROBE_KINDS = {"read": 0, "read_nt": 1, "write": 2, "write_nt": 3, "copy": 4}
+
+
+def bandwidth_probe(kind: str, nbytes: int = 4 << 30, reps: int = 5, grid: int = 0, stream=None) -> float:
+    """Streaming bandwidth of one probe kernel in GB/s (bytes moved / time; a
+    copy moves its bytes twice)."""
+    k = PROBE_KINDS[kind]
+    src = torch.ones(nbytes // 8, dtype=torch.float64, device="cuda")
+    dst = torch.empty_like(src) if kind not in ("read", "read_nt") else torch.zeros(1, dtype=torch.float64,
+                                                                                 device="cuda")
+    ms = ctypes.c_double()
+    _check(load().gmagnus_bandwidth_probe(k, dst.data_ptr(), src.data_ptr(), nbytes, grid, reps, _stream(stream),
+                                          ctypes.byref(ms)))
+    del src, dst
+    moved = 2 * nbytes if kind == "copy" else nbytes
+    return moved / (ms.value / 1000.0) / 1e9
 
 
 def release_cache():

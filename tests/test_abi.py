@@ -141,3 +141,57 @@ def test_plan_argument_validation_without_device(lib):
 def test_status_strings(lib):
     for code, name in gm.STATUS.items():
         assert lib.gmagnus_status_string(code).decode() == "GMAGNUS_" + ("SUCCESS" if code == 0 else "ERROR_" + name)
+
+
+def test_expansion_path_predicate(lib):
+    # the routing of the heavy rows (host-only): paper order without a level or
+    # when asked; row order when its 32-bit offsets fit; both levels fused only
+    # for two-level hierarchies whose B can be indexed in 32 bits
+    p2 = gm.get_params(1 << 22)  # [32, 16]
+    p1 = gm.get_params(1 << 17)  # one level
+    p0 = gm.get_params(4096)     # no level
+    path = gm.expansion_path
+    assert path(p2, 0, 0, 100) == "none"
+    assert path(p0, 10, 10_000, 100) == "paper"
+    assert path(p2, 10, 10_000, 100, gm.FLAG_PAPER_EXPANSION) == "paper"
+    assert path(p2, 10, 10_000, 100, gm.FLAG_PAPER_HISTOGRAM) == "paper"
+    assert path(p2, 10, 10_000, 100, gm.FLAG_SLICE_SPLIT) == "slice_split"
+    assert path(p2, 10, 1 << 32, 100) == "slice_split"          # offsets past 32 bits
+    assert path(p2, 10, (1 << 32) - 1, 100) == "rows_two_level"
+    assert path(p2, 10, 10_000, 100) == "rows_two_level"
+    assert path(p2, 10, 10_000, 100, gm.FLAG_LEVEL_BY_LEVEL) == "rows"
+    assert path(p2, 10, 10_000, (1 << 31) - 1) == "rows_two_level"
+    assert path(p2, 10, 10_000, 1 << 31) == "rows"               # B.nnz past 32-bit fine boundaries
+    assert path(p1, 10, 10_000, 100) == "rows"
+    assert path(gm.get_params(1 << 23), 10, 10_000, 100) == "rows_two_level"
+    assert path(gm.get_params(4096, tau=200, dense_width_log2=6, chunks_max_log2=2), 10, 10_000, 100) == "rows"
+
+
+def test_binding_refuses_host_tensors(lib):
+    # a host tensor's pointer in a kernel would fault the GPU: the binding
+    # refuses it before any library call (the plan below has no library)
+    import types
+
+    import torch
+
+    p = gm.Plan.__new__(gm.Plan)
+    p._lib = None  # any library call would raise AttributeError, not ValueError
+    p._h = ctypes.c_void_p()
+    m = types.SimpleNamespace(row_ptr=torch.zeros(3, dtype=torch.int64), nnz=2)
+    p.A = p.B = m
+    p.nnz = 2
+    p.row_ptr = torch.zeros(3, dtype=torch.int64)
+    col, val = torch.zeros(2, dtype=torch.int32), torch.zeros(2, dtype=torch.float64)
+    with pytest.raises(ValueError, match="CUDA tensor"):
+        p.numeric(col, val)
+    with pytest.raises(ValueError, match="CUDA tensor"):
+        p.update_values(val, val)
+
+
+def test_probe_argument_validation(lib):
+    ms = ctypes.c_double()
+    assert lib.gmagnus_bandwidth_probe(9, 0x1000, 0x1000, 1 << 20, 0, 1, None, ctypes.byref(ms)) == 1
+    assert lib.gmagnus_bandwidth_probe(4, 0x1000, 0x1000, 17, 0, 1, None, ctypes.byref(ms)) == 1
+    assert lib.gmagnus_bandwidth_probe(4, 0x1000, None, 1 << 20, 0, 1, None, ctypes.byref(ms)) == 1
+    assert lib.gmagnus_bandwidth_probe(4, 0x1008, 0x1000, 1 << 20, 0, 1, None, ctypes.byref(ms)) == 1
+    assert lib.gmagnus_bandwidth_probe(4, 0x1000, 0x1000, 1 << 20, 0, 0, None, ctypes.byref(ms)) == 1

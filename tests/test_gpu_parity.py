@@ -392,3 +392,125 @@ def test_update_values_errors(g):
     with g.Plan(dA, dA, flags=g.FLAG_KEEP_PATTERN) as p:
         with pytest.raises(g.GmagnusError):
             p.update_values(dA.val)  # before symbolic
+
+
+class _CountingAllocator:
+    """Device workspace through torch's caching allocator; call number
+    `fail_at` (1-based) returns NULL. Tracks the blocks still outstanding."""
+
+    def __init__(self, g, fail_at=0):
+        self.fail_at, self.calls, self.live = fail_at, 0, set()
+        self.alloc = g.ALLOC_FN(self._alloc)
+        self.free = g.FREE_FN(self._free)
+
+    def _alloc(self, nbytes, stream, ctx):
+        self.calls += 1
+        if self.calls == self.fail_at:
+            return None
+        p = torch.cuda.caching_allocator_alloc(nbytes)
+        self.live.add(p)
+        return p
+
+    def _free(self, ptr, stream, ctx):
+        self.live.discard(ptr)
+        torch.cuda.caching_allocator_delete(ptr)
+
+
+def _run_with_allocator(g, dA, al, **opts):
+    """plan + symbolic + numeric with the allocator; returns (status, C or None)."""
+    try:
+        with g.Plan(dA, dA, alloc=al.alloc, free=al.free, **opts) as p:
+            rp, nnz = p.symbolic()
+            col, val = p.numeric()
+            info = p.info()
+            torch.cuda.synchronize()
+            assert info.check_flags == 0
+            return 0, (rp.cpu().numpy(), col.cpu().numpy(), val.cpu().numpy())
+    except g.GmagnusError as e:
+        return e.status, None
+
+
+@pytest.mark.parametrize("opts", [dict(), dict(tau=300, dense_width_log2=7, chunks_max_log2=3)],
+                         ids=["default", "two levels"])
+def test_user_allocator_failure_releases_everything(g, opts):
+    # a user allocator that returns NULL on its N-th call: the call that needed
+    # the block fails with OUT_OF_MEMORY, and every block handed out before is
+    # given back once the plan is destroyed (nothing leaks); without a failure
+    # the same allocator gives the oracle's C
+    A = RMAT12.make()
+    dA = g.DeviceCSR.from_host(A)
+    ok = _CountingAllocator(g)
+    st, C = _run_with_allocator(g, dA, ok, **opts)
+    assert st == 0 and not ok.live
+    compare_full(*C, oracle.spgemm(A, A))
+    total = ok.calls
+    assert total >= 10
+    for n in sorted({1, 2, 3, total // 4, total // 2, total - 1, total}):
+        al = _CountingAllocator(g, fail_at=n)
+        st, _ = _run_with_allocator(g, dA, al, **opts)
+        assert st == 3, (n, st)
+        assert not al.live, "call %d failed: %d blocks not given back" % (n, len(al.live))
+    torch.cuda.synchronize()
+
+
+def test_workspace_limit(g):
+    A = RMAT12.make()
+    dA = g.DeviceCSR.from_host(A)
+    opts = dict(tau=300, dense_width_log2=7, chunks_max_log2=3)
+    with g.Plan(dA, dA, **opts) as p:
+        p.symbolic()
+        p.numeric()
+        peak = p.info().workspace_peak_bytes
+    assert peak > 0
+    # a limit below what the plan needs fails cleanly
+    with pytest.raises(g.GmagnusError) as e:
+        with g.Plan(dA, dA, workspace_limit_bytes=peak // 4, **opts) as p:
+            p.symbolic()
+            p.numeric()
+    assert e.value.status == 3 and "workspace limit" in str(e.value)
+    # at the peak it runs, stays within the limit and gives the oracle's C
+    info = check(g, A, A, workspace_limit_bytes=peak, **opts)
+    assert 0 < info.workspace_peak_bytes <= peak
+
+
+def test_timed_classes_fit_in_wall_time(g):
+    # the per-class device times of one plan do not overlap: their sum stays
+    # within the wall time of the calls that produced them
+    import time
+
+    A = wl.rmat(15, 16, 0.57, 0.19, 0.19, 3)
+    dA = g.DeviceCSR.from_host(A)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    with g.Plan(dA, dA, flags=g.FLAG_TIMING) as p:
+        p.symbolic()
+        p.numeric()
+        torch.cuda.synchronize()
+        wall_ms = 1000.0 * (time.perf_counter() - t0)
+        info = p.info()
+    total = sum(info.kernel_ms[i] for i in range(len(g.K_NAMES)))
+    assert info.expansion_path == 3  # one level (C.m = 2^15), split during the row-order expansion
+    assert 0 < total <= wall_ms, (total, wall_ms)
+    assert info.kernel_ms[2] > 0 and info.kernel_ms[6] > 0
+
+
+@pytest.mark.parametrize("kind", ["read", "read_nt", "write", "write_nt", "copy"])
+def test_bandwidth_probe(g, kind):
+    import ctypes
+
+    n = 1 << 22
+    src = torch.arange(n, dtype=torch.float64, device="cuda")
+    dst = torch.full((n,), -7.0, dtype=torch.float64, device="cuda")
+    ms = ctypes.c_double()
+    st = g.load().gmagnus_bandwidth_probe(g.PROBE_KINDS[kind], dst.data_ptr(), src.data_ptr(), 8 * n, 0, 3,
+                                          torch.cuda.current_stream().cuda_stream, ctypes.byref(ms))
+    assert st == 0 and ms.value > 0
+    if kind == "copy":
+        assert torch.equal(dst, src)
+    elif kind.startswith("write"):
+        # element i of 16 bytes holds (1.0, i)
+        assert torch.equal(dst[0::2], torch.ones(n // 2, dtype=torch.float64, device="cuda"))
+        assert torch.equal(dst[1::2], torch.arange(n // 2, dtype=torch.float64, device="cuda"))
+    else:
+        assert torch.equal(dst, torch.full((n,), -7.0, dtype=torch.float64, device="cuda"))  # sink untouched
+    assert 10.0 < g.bandwidth_probe(kind, nbytes=1 << 28) < 20000.0
