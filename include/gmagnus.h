@@ -202,6 +202,27 @@ int32_t gmagnus_expansion_path(const gmagnus_params_t *params, int64_t n_heavy, 
 gmagnus_status_t gmagnus_plan(gmagnus_plan_t *out, const gmagnus_csr_t *A, const gmagnus_csr_t *B,
                               const gmagnus_options_t *opts, void *hip_stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops or harnesses that forbid allocation): the same plan
+ * as gmagnus_plan, with its whole device workspace carved from a static
+ * device array of GMAGNUS_STATIC_WORKSPACE_MIB MiB that each device holds
+ * from the first call on it until the process ends. Neither this call nor
+ * symbolic / numeric / update_values on the plan calls hipMalloc, hipFree or
+ * any other allocating routine of HIP (host reads use pageable memory);
+ * A, B and C stay the caller's. Plans made this way on one device take
+ * disjoint blocks of the array, so they may coexist, but together they are
+ * bounded by its size; blocks go back when the plan is destroyed, and hold
+ * whatever the last plan wrote (nothing relies on their contents).
+ * opts must not set alloc / free; workspace_limit_bytes is capped at the
+ * array's size. Errors: as gmagnus_plan; UNSUPPORTED when the panel has more
+ * rows than the array could hold the setup work of (about 3.2 million rows
+ * for 128 MiB); OUT_OF_MEMORY from this call or a later phase when the
+ * array cannot hold the next block the plan needs (the plan then fails
+ * cleanly and gives its blocks back). */
+#define GMAGNUS_STATIC_WORKSPACE_MIB 128
+gmagnus_status_t gmagnus_plan_static(gmagnus_plan_t *out, const gmagnus_csr_t *A, const gmagnus_csr_t *B,
+                                     const gmagnus_options_t *opts, void *hip_stream);
+
 /* Symbolic phase: runs the heavy-row expansion and hierarchical multisplit
  * (Algorithm 3, outer product and reorder), counts the distinct columns of
  * every light row and final chunk, and writes the panel's row pointers:

@@ -32,7 +32,7 @@ FLAGS = [
 ]
 
 SOURCES = ["prims.hip", "setup.hip", "expand.hip", "rowsplit.hip", "multisplit.hip", "accumulate.hip",
-           "plan.hip", "probe.hip"]
+           "plan.hip", "probe.hip", "static_plan.hip"]
 
 
 def _compile(src: str) -> str:

@@ -99,7 +99,7 @@ class PlanInfo(ctypes.Structure):
 EXPORTS = ["gmagnus_options_init", "gmagnus_get_params", "gmagnus_plan", "gmagnus_spgemm_symbolic",
            "gmagnus_spgemm_numeric", "gmagnus_plan_info", "gmagnus_plan_destroy", "gmagnus_row_products",
            "gmagnus_split_panels", "gmagnus_release_cache", "gmagnus_last_error", "gmagnus_status_string",
-           "gmagnus_update_values", "gmagnus_expansion_path", "gmagnus_bandwidth_probe"]
+           "gmagnus_update_values", "gmagnus_expansion_path", "gmagnus_bandwidth_probe", "gmagnus_plan_static"]
 
 _lib = None
 
@@ -118,6 +118,7 @@ def load(path: str = LIB_PATH):
     lib.gmagnus_get_params.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.POINTER(Options), ctypes.POINTER(Params)]
     lib.gmagnus_plan.argtypes = [ctypes.POINTER(P), ctypes.POINTER(CsrDesc), ctypes.POINTER(CsrDesc),
                                  ctypes.POINTER(Options), P]
+    lib.gmagnus_plan_static.argtypes = lib.gmagnus_plan.argtypes
     lib.gmagnus_spgemm_symbolic.argtypes = [P, P, ctypes.POINTER(ctypes.c_int64)]
     lib.gmagnus_spgemm_numeric.argtypes = [P, P, P, P]
     lib.gmagnus_update_values.argtypes = [P, P, P]
@@ -138,7 +139,7 @@ def load(path: str = LIB_PATH):
     lib.gmagnus_last_error.restype = ctypes.c_char_p
     lib.gmagnus_status_string.argtypes = [ctypes.c_int]
     lib.gmagnus_status_string.restype = ctypes.c_char_p
-    for f in ("gmagnus_get_params", "gmagnus_plan", "gmagnus_spgemm_symbolic", "gmagnus_spgemm_numeric",
+    for f in ("gmagnus_get_params", "gmagnus_plan", "gmagnus_plan_static", "gmagnus_spgemm_symbolic", "gmagnus_spgemm_numeric",
               "gmagnus_update_values", "gmagnus_plan_info", "gmagnus_row_products", "gmagnus_split_panels"):
         getattr(lib, f).restype = ctypes.c_int
     _lib = lib
@@ -224,16 +225,18 @@ def _stream(stream) -> int:
 
 
 class Plan:
-    """One row panel of C = A*B: setup on construction, then symbolic and numeric."""
+    """One row panel of C = A*B: setup on construction, then symbolic and numeric.
+    static_workspace=True builds it with gmagnus_plan_static (no device
+    allocation by the library: its workspace is a static device array)."""
 
-    def __init__(self, A: DeviceCSR, B: DeviceCSR, stream=None, **options):
+    def __init__(self, A: DeviceCSR, B: DeviceCSR, stream=None, static_workspace: bool = False, **options):
         self._lib = load()
         self.A, self.B = A, B  # borrowed by the library until close()
         self._da, self._db = A.desc(), B.desc()
         self._opts = make_options(**options)
         self._stream = stream
         self._h = ctypes.c_void_p()
-        make = self._lib.gmagnus_plan
+        make = self._lib.gmagnus_plan_static if static_workspace else self._lib.gmagnus_plan
         _check(make(ctypes.byref(self._h), ctypes.byref(self._da), ctypes.byref(self._db), ctypes.byref(self._opts),
                     _stream(stream)))
         rb = self._opts.row_begin
