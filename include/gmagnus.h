@@ -19,7 +19,10 @@
  * Conventions shared by every entry point
  *   - All matrix arrays are DEVICE pointers (hipMalloc'ed or torch tensors on
  *     the current device). Sizes and scalars are host values.
- *   - Index types: int64 row pointers, int32 column indices, fp64 values.
+ *   - Index types: int64 row pointers; int32 column indices and fp64 values
+ *     through gmagnus_csr_t, or int32 / int64 column indices and fp64 / fp32
+ *     values through gmagnus_matrix_t and the *_typed entry points (C takes
+ *     the types of A and B, which must agree).
  *   - Input CSR must be canonical: row_ptr[0] = 0, non-decreasing,
  *     row_ptr[n_rows] = nnz, columns in [0, n_cols) and strictly increasing
  *     within each row. options.validate = 1 checks this on the device.
@@ -60,6 +63,24 @@ typedef struct {
     const int32_t *col_idx; /* device, nnz */
     const double *val;      /* device, nnz */
 } gmagnus_csr_t;
+
+/* Column-index and value types (the s_col and s_val of Section III-D). */
+typedef enum { GMAGNUS_INDEX_INT32 = 0, GMAGNUS_INDEX_INT64 = 1 } gmagnus_index_type_t;
+typedef enum { GMAGNUS_VALUE_FP64 = 0, GMAGNUS_VALUE_FP32 = 1 } gmagnus_value_type_t;
+
+/* A CSR matrix in device memory with its types named. With int64 column
+ * indices B (and C) may have up to 2^35 columns; every other dimension,
+ * A's columns included, stays below 2^31. */
+typedef struct {
+    int64_t n_rows;
+    int64_t n_cols;
+    int64_t nnz;
+    const int64_t *row_ptr; /* device, n_rows + 1 */
+    const void *col_idx;    /* device, nnz int32_t or int64_t (index_type) */
+    const void *val;        /* device, nnz double or float (value_type) */
+    int32_t index_type;     /* gmagnus_index_type_t */
+    int32_t value_type;     /* gmagnus_value_type_t */
+} gmagnus_matrix_t;
 
 /* Options. Zero fields mean "derive" (Section III-D); initialise with
  * gmagnus_options_init. The overrides exist so tests can force any number of
@@ -157,6 +178,8 @@ typedef struct {
     int32_t check_flags;           /* nonzero: a kernel's output count disagreed with symbolic (a bug) */
     int32_t expansion_path;        /* GMAGNUS_PATH_* the heavy rows took */
     int64_t workspace_peak_bytes;  /* largest device workspace the plan has held */
+    int32_t index_type;            /* gmagnus_index_type_t of A, B and C */
+    int32_t value_type;            /* gmagnus_value_type_t of A, B and C */
     /* Under GMAGNUS_FLAG_TIMING: summed device milliseconds, launches and
      * algorithmic (compulsory) HBM bytes per kernel class. */
     double kernel_ms[GMAGNUS_K_COUNT];
@@ -186,6 +209,16 @@ void gmagnus_options_init(gmagnus_options_t *opts);
 gmagnus_status_t gmagnus_get_params(int64_t c_m, int64_t lds_bytes, const gmagnus_options_t *opts,
                                     gmagnus_params_t *out);
 
+/* Host-only parameter selection for the given column-index and value types
+ * (Section III-D: tau from s_col + s_val, W from s_val, the multisplit group
+ * and chunk limits from both). The library caps tau at the light-row
+ * accumulators' capacity (6912 products) and W at 8192 columns (its dense
+ * accumulator and narrow bitmap shapes); fp32 values derive tau = 10240 and
+ * W = 16384 at 160 KB and are capped. Errors as gmagnus_get_params, plus
+ * INVALID_VALUE for an unknown type and c_m beyond the index type's range. */
+gmagnus_status_t gmagnus_get_params_typed(int64_t c_m, int64_t lds_bytes, int32_t index_type, int32_t value_type,
+                                          const gmagnus_options_t *opts, gmagnus_params_t *out);
+
 /* Host-only: the expansion order a plan with these parameters takes for a
  * panel with n_heavy heavy rows holding products_heavy products, with B
  * holding b_nnz entries and the given GMAGNUS_FLAG_* bits. No device is
@@ -201,6 +234,13 @@ int32_t gmagnus_expansion_path(const gmagnus_params_t *params, int64_t n_heavy, 
  * (n_cols >= 2^31), INVALID_CSR (validate), OUT_OF_MEMORY, HIP. */
 gmagnus_status_t gmagnus_plan(gmagnus_plan_t *out, const gmagnus_csr_t *A, const gmagnus_csr_t *B,
                               const gmagnus_options_t *opts, void *hip_stream);
+
+/* gmagnus_plan for typed matrices (Section III-D's type sizes): A and B must
+ * have the same index and value types, which C takes. Errors as gmagnus_plan,
+ * plus INVALID_VALUE for unknown or mismatched types, UNSUPPORTED beyond the
+ * limits of gmagnus_matrix_t. */
+gmagnus_status_t gmagnus_plan_typed(gmagnus_plan_t *out, const gmagnus_matrix_t *A, const gmagnus_matrix_t *B,
+                                    const gmagnus_options_t *opts, void *hip_stream);
 
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, serving loops or harnesses that forbid allocation): the same plan
@@ -239,6 +279,13 @@ gmagnus_status_t gmagnus_spgemm_symbolic(gmagnus_plan_t plan, int64_t *c_row_ptr
 gmagnus_status_t gmagnus_spgemm_numeric(gmagnus_plan_t plan, const int64_t *c_row_ptr, int32_t *c_col_idx,
                                         double *c_val);
 
+/* gmagnus_spgemm_numeric for any plan: c_col_idx and c_val have the plan's
+ * index and value types (int32 / int64, double / float). gmagnus_spgemm_numeric
+ * itself accepts only plans of int32 columns and fp64 values
+ * (INVALID_VALUE otherwise). */
+gmagnus_status_t gmagnus_spgemm_numeric_typed(gmagnus_plan_t plan, const int64_t *c_row_ptr, void *c_col_idx,
+                                              void *c_val);
+
 /* Pattern reuse: the symbolic phase depends on the nonzero patterns of A and
  * B only (Section II-A: it fixes C.rowPtr and C.nnz; the numeric phase fills
  * the values), so repeated products on fixed patterns with changing values
@@ -258,6 +305,10 @@ gmagnus_status_t gmagnus_spgemm_numeric(gmagnus_plan_t plan, const int64_t *c_ro
  * HIP. */
 gmagnus_status_t gmagnus_update_values(gmagnus_plan_t plan, const double *a_val, const double *b_val);
 
+/* gmagnus_update_values for any plan: a_val and b_val hold the plan's value
+ * type (gmagnus_update_values itself requires fp64 values). */
+gmagnus_status_t gmagnus_update_values_typed(gmagnus_plan_t plan, const void *a_val, const void *b_val);
+
 /* Copies the plan's parameters, counts and (with GMAGNUS_FLAG_TIMING) kernel
  * timings. Synchronises the stream when timings are requested. */
 gmagnus_status_t gmagnus_plan_info(gmagnus_plan_t plan, gmagnus_plan_info_t *out);
@@ -272,6 +323,11 @@ void gmagnus_plan_destroy(gmagnus_plan_t plan);
 gmagnus_status_t gmagnus_row_products(const gmagnus_csr_t *A, const gmagnus_csr_t *B, int64_t *ip,
                                       void *hip_stream);
 
+/* gmagnus_row_products for typed matrices (only A's columns and B's row
+ * pointers are read). */
+gmagnus_status_t gmagnus_row_products_typed(const gmagnus_matrix_t *A, const gmagnus_matrix_t *B, int64_t *ip,
+                                            void *hip_stream);
+
 /* Splits the rows of A into consecutive panels whose product counts stay at
  * or below max_products each (a row above the limit gets a panel of its own)
  * so that C can be produced panel by panel when it does not fit in memory.
@@ -281,6 +337,10 @@ gmagnus_status_t gmagnus_row_products(const gmagnus_csr_t *A, const gmagnus_csr_
  * max_panels panels are needed), OUT_OF_MEMORY, HIP. */
 gmagnus_status_t gmagnus_split_panels(const gmagnus_csr_t *A, const gmagnus_csr_t *B, int64_t max_products,
                                       int64_t *bounds, int64_t max_panels, int64_t *n_panels, void *hip_stream);
+
+/* gmagnus_split_panels for typed matrices. */
+gmagnus_status_t gmagnus_split_panels_typed(const gmagnus_matrix_t *A, const gmagnus_matrix_t *B, int64_t max_products,
+                                            int64_t *bounds, int64_t max_panels, int64_t *n_panels, void *hip_stream);
 
 /* Streaming bandwidth probe (the measured peak of the speed-of-light
  * comparison, Section IV-C): runs one kernel of the given kind over `bytes`

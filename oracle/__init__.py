@@ -60,7 +60,7 @@ def _load():
         lib.oracle_count_rows.argtypes = [P, P, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
         lib.oracle_count_rows.restype = ctypes.c_int
         lib.oracle_fill_rows.argtypes = [P, P, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
-                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
         lib.oracle_fill_rows.restype = ctypes.c_int
         lib.oracle_row_counts.argtypes = [P, P, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
         lib.oracle_row_counts.restype = ctypes.c_int
@@ -71,7 +71,7 @@ def _load():
 
 def _desc(m):
     rp = np.ascontiguousarray(m.row_ptr, np.int64)
-    col = np.ascontiguousarray(m.col, np.int32)
+    col = np.ascontiguousarray(m.col, np.int64)  # widened: the oracle reads 64-bit columns
     val = np.ascontiguousarray(m.val, np.float64)
     keep = (rp, col, val)
     return _Csr(m.n_rows, m.n_cols, rp.ctypes.data, col.ctypes.data, val.ctypes.data), keep
@@ -104,7 +104,7 @@ def row_counts(A, B, row_begin=0, row_end=None) -> np.ndarray:
     db, kb = _desc(B)
     counts = np.empty(row_end - row_begin, np.int64)
     if _load().oracle_row_counts(ctypes.byref(da), ctypes.byref(db), row_begin, row_end, counts.ctypes.data):
-        raise MemoryError("oracle could not allocate its column stamps")
+        raise MemoryError("oracle could not allocate its column stamps (or C has more than 2^31 columns)")
     return counts
 
 
@@ -114,13 +114,17 @@ class OracleRows:
 
     rows: np.ndarray  # int64 row ids
     row_ptr: np.ndarray  # int64, len(rows)+1
-    col: np.ndarray  # int32
+    col: np.ndarray  # int64
     val: np.ndarray  # float64
     bound: np.ndarray  # float64, sum |a*b| per entry
+    terms: np.ndarray  # int64, products summed per entry
 
     def row(self, t):
         s, e = self.row_ptr[t], self.row_ptr[t + 1]
         return self.col[s:e], self.val[s:e], self.bound[s:e]
+
+    def row_terms(self, t):
+        return self.terms[self.row_ptr[t]:self.row_ptr[t + 1]]
 
 
 def spgemm(A, B, rows=None) -> OracleRows:
@@ -140,13 +144,14 @@ def spgemm(A, B, rows=None) -> OracleRows:
     rp = np.zeros(rows.size + 1, np.int64)
     np.cumsum(counts, out=rp[1:])
     nnz = int(rp[-1])
-    col = np.empty(nnz, np.int32)
+    col = np.empty(nnz, np.int64)
     val = np.empty(nnz, np.float64)
     bound = np.empty(nnz, np.float64)
+    terms = np.empty(nnz, np.int64)
     if lib.oracle_fill_rows(ctypes.byref(da), ctypes.byref(db), rows.ctypes.data, rows.size, rp.ctypes.data,
-                            col.ctypes.data, val.ctypes.data, bound.ctypes.data):
+                            col.ctypes.data, val.ctypes.data, bound.ctypes.data, terms.ctypes.data):
         raise MemoryError("oracle could not expand a row")
-    return OracleRows(rows, rp, col, val, bound)
+    return OracleRows(rows, rp, col, val, bound, terms)
 
 
 def threads() -> int:

@@ -72,15 +72,24 @@ class MagnusParams:
         return "%d: %s" % (self.chunks_required, ", ".join(str(v) for v in self.v_chunks))
 
 
-def get_magnus_params(c_m: int, s_lm: int, n_subgroups: int = 16) -> MagnusParams:
-    tau = s_lm // (ALPHA * (S_COL + S_VAL))
+def get_magnus_params(c_m: int, s_lm: int, n_subgroups: int = 16, s_col: int = S_COL, s_val: int = S_VAL,
+                      dense_width_max: int = 0, tau_max: int = 0) -> MagnusParams:
+    """s_col / s_val: byte sizes of the stored column index and value (4 and
+    8 unless given). dense_width_max / tau_max (0: none) cap W and tau the
+    way an implementation whose accumulators hold less would; chunk counts
+    then follow the capped W."""
+    tau = s_lm // (ALPHA * (s_col + s_val))
     # dense accumulator: one value plus one bitmap bit per column, alpha headroom
-    dense_width = floor_pow2((8 * s_lm) // (ALPHA * (8 * S_VAL + 1)))
+    dense_width = floor_pow2((8 * s_lm) // (ALPHA * (8 * s_val + 1)))
+    if dense_width_max:
+        dense_width = min(dense_width, dense_width_max)
     chunks_required = max(1, ceil_pow2(c_m) // dense_width)
     # half of local memory holds the locally permuted elements
-    min_group_elems = s_lm // (2 * (S_COL + S_VAL))
+    min_group_elems = s_lm // (2 * (s_col + s_val))
     group_rows = -(-(min_group_elems - 1) // tau) + 1
-    eq = (s_lm - min_group_elems * (S_COL + S_VAL) - S_HISTO) // (group_rows * (n_subgroups * S_HISTO + S_ROWPTR))
+    if tau_max:
+        tau = min(tau, tau_max)
+    eq = (s_lm - min_group_elems * (s_col + s_val) - S_HISTO) // (group_rows * (n_subgroups * S_HISTO + S_ROWPTR))
     chunks_max = min(floor_pow2(eq), floor_pow2(min_group_elems // (group_rows * MIN_LOCAL_CHUNK)))
     if chunks_required == 1:
         v = []

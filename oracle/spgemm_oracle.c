@@ -20,7 +20,12 @@
  *   - each run is reduced with Neumaier's compensated summation, so the
  *     oracle's own rounding error is far below the comparison tolerance;
  *   - bound[e] = sum of |A[i,j]*B[j,k]| over the run, the scale of the
- *     per-entry tolerance |c - c_ref| <= 1e-12 * bound.
+ *     per-entry tolerance, and terms[e] = the run's length (the number of
+ *     products summed into the entry);
+ *   - column indices are 64-bit (32-bit inputs are widened by the caller) and
+ *     values fp64: for fp32 inputs, widened exactly, every product is exact
+ *     in fp64 (24 + 24 significant bits) and the compensated sum is the
+ *     exact result to about one fp64 rounding.
  *
  * Rows are processed in parallel (OpenMP, dynamic schedule); each row is
  * computed by one thread in a fixed order, so results do not depend on the
@@ -34,7 +39,7 @@
 typedef struct {
     int64_t n_rows, n_cols;
     const int64_t *row_ptr;
-    const int32_t *col;
+    const int64_t *col;
     const double *val;
 } oracle_csr;
 
@@ -42,7 +47,7 @@ typedef struct {
 static int64_t row_products(const oracle_csr *A, const oracle_csr *B, int64_t i) {
     int64_t n = 0;
     for (int64_t p = A->row_ptr[i]; p < A->row_ptr[i + 1]; ++p) {
-        int32_t j = A->col[p];
+        int64_t j = A->col[p];
         n += B->row_ptr[j + 1] - B->row_ptr[j];
     }
     return n;
@@ -53,22 +58,28 @@ void oracle_row_products(const oracle_csr *A, const oracle_csr *B, int64_t *ip) 
     for (int64_t i = 0; i < A->n_rows; ++i) ip[i] = row_products(A, B, i);
 }
 
-static int cmp_u64(const void *a, const void *b) {
-    uint64_t x = *(const uint64_t *)a, y = *(const uint64_t *)b;
-    return (x > y) - (x < y);
+/* A product's sort key: its column, then its position q in (j, k) order,
+ * so sorting by (col, q) is stable. */
+typedef struct {
+    int64_t col;
+    int64_t q;
+} oracle_key;
+
+static int cmp_key(const void *a, const void *b) {
+    const oracle_key *x = (const oracle_key *)a, *y = (const oracle_key *)b;
+    if (x->col != y->col) return (x->col > y->col) - (x->col < y->col);
+    return (x->q > y->q) - (x->q < y->q);
 }
 
-/* Forms the products of row i in (j, k) order and sorts them by column.
- * keys[q] = column << 32 | q, where q is the product's position in (j,k)
- * order, so the sort is stable; prod[q] is the product itself. Returns the
- * product count, or -1 on allocation failure / more than 2^32 products. */
-static int64_t expand_sorted(const oracle_csr *A, const oracle_csr *B, int64_t i, uint64_t **keys_out,
+/* Forms the products of row i in (j, k) order and sorts them by column
+ * (stable); prod[q] is the product at position q. Returns the product count,
+ * or -1 on allocation failure. */
+static int64_t expand_sorted(const oracle_csr *A, const oracle_csr *B, int64_t i, oracle_key **keys_out,
                              double **prod_out) {
     int64_t n = row_products(A, B, i);
     *keys_out = NULL;
     *prod_out = NULL;
-    if (n >= ((int64_t)1 << 32)) return -1;
-    uint64_t *keys = (uint64_t *)malloc((size_t)(n > 0 ? n : 1) * sizeof(uint64_t));
+    oracle_key *keys = (oracle_key *)malloc((size_t)(n > 0 ? n : 1) * sizeof(oracle_key));
     double *prod = (double *)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
     if (!keys || !prod) {
         free(keys);
@@ -77,15 +88,16 @@ static int64_t expand_sorted(const oracle_csr *A, const oracle_csr *B, int64_t i
     }
     int64_t q = 0;
     for (int64_t p = A->row_ptr[i]; p < A->row_ptr[i + 1]; ++p) {
-        int32_t j = A->col[p];
+        int64_t j = A->col[p];
         double a = A->val[p];
         for (int64_t r = B->row_ptr[j]; r < B->row_ptr[j + 1]; ++r) {
-            keys[q] = ((uint64_t)(uint32_t)B->col[r] << 32) | (uint64_t)q;
+            keys[q].col = B->col[r];
+            keys[q].q = q;
             prod[q] = a * B->val[r];
             ++q;
         }
     }
-    qsort(keys, (size_t)n, sizeof(uint64_t), cmp_u64);
+    qsort(keys, (size_t)n, sizeof(oracle_key), cmp_key);
     *keys_out = keys;
     *prod_out = prod;
     return n;
@@ -98,7 +110,7 @@ int oracle_count_rows(const oracle_csr *A, const oracle_csr *B, const int64_t *r
     int failed = 0;
 #pragma omp parallel for schedule(dynamic, 16)
     for (int64_t t = 0; t < n_list; ++t) {
-        uint64_t *keys;
+        oracle_key *keys;
         double *prod;
         int64_t n = expand_sorted(A, B, rows[t], &keys, &prod);
         if (n < 0) {
@@ -108,7 +120,7 @@ int oracle_count_rows(const oracle_csr *A, const oracle_csr *B, const int64_t *r
         }
         int64_t runs = 0;
         for (int64_t q = 0; q < n; ++q)
-            if (q == 0 || (keys[q] >> 32) != (keys[q - 1] >> 32)) ++runs;
+            if (q == 0 || keys[q].col != keys[q - 1].col) ++runs;
         counts[t] = runs;
         free(keys);
         free(prod);
@@ -116,34 +128,37 @@ int oracle_count_rows(const oracle_csr *A, const oracle_csr *B, const int64_t *r
     return failed ? -1 : 0;
 }
 
-/* Numeric: row rows[t] is written at positions offsets[t] .. of col/val/bound. */
+/* Numeric: row rows[t] is written at positions offsets[t] .. of col, val,
+ * bound and terms (terms may be NULL). */
 int oracle_fill_rows(const oracle_csr *A, const oracle_csr *B, const int64_t *rows, int64_t n_list,
-                     const int64_t *offsets, int32_t *col, double *val, double *bound) {
+                     const int64_t *offsets, int64_t *col, double *val, double *bound, int64_t *terms) {
     int failed = 0;
 #pragma omp parallel for schedule(dynamic, 16)
     for (int64_t t = 0; t < n_list; ++t) {
-        uint64_t *keys;
+        oracle_key *keys;
         double *prod;
         int64_t n = expand_sorted(A, B, rows[t], &keys, &prod);
         if (n < 0) {
             failed = 1;
             continue;
         }
-        int64_t out = offsets[t] - 1;
+        int64_t out = offsets[t] - 1, run = 0;
         double s = 0.0, comp = 0.0, mag = 0.0;
         for (int64_t q = 0; q < n; ++q) {
-            uint32_t c = (uint32_t)(keys[q] >> 32);
-            double x = prod[keys[q] & 0xFFFFFFFFULL];
-            if (q == 0 || c != (uint32_t)(keys[q - 1] >> 32)) {
+            const int64_t c = keys[q].col;
+            double x = prod[keys[q].q];
+            if (q == 0 || c != keys[q - 1].col) {
                 if (q > 0) {
                     val[out] = s + comp;
                     bound[out] = mag;
+                    if (terms) terms[out] = run;
                 }
                 ++out;
-                col[out] = (int32_t)c;
+                col[out] = c;
                 s = 0.0;
                 comp = 0.0;
                 mag = 0.0;
+                run = 0;
             }
             /* Neumaier: carry the low-order part lost by s + x. */
             double t2 = s + x;
@@ -153,10 +168,12 @@ int oracle_fill_rows(const oracle_csr *A, const oracle_csr *B, const int64_t *ro
                 comp += (x - t2) + s;
             s = t2;
             mag += fabs(x);
+            ++run;
         }
         if (n > 0) {
             val[out] = s + comp;
             bound[out] = mag;
+            if (terms) terms[out] = run;
         }
         free(keys);
         free(prod);
@@ -175,7 +192,7 @@ int oracle_fill_rows(const oracle_csr *A, const oracle_csr *B, const int64_t *ro
 int oracle_row_counts(const oracle_csr *A, const oracle_csr *B, int64_t row_begin, int64_t row_end,
                       int64_t *counts) {
     int failed = 0;
-    if (row_end - row_begin > ((int64_t)1 << 31) - 2) return -1;
+    if (row_end - row_begin > ((int64_t)1 << 31) - 2 || B->n_cols > ((int64_t)1 << 31)) return -1;
 #pragma omp parallel
     {
         int32_t *stamp = (int32_t *)malloc((size_t)(B->n_cols > 0 ? B->n_cols : 1) * sizeof(int32_t));
@@ -192,9 +209,9 @@ int oracle_row_counts(const oracle_csr *A, const oracle_csr *B, int64_t row_begi
                 const int32_t mark = (int32_t)(i - row_begin);
                 int64_t n = 0;
                 for (int64_t p = A->row_ptr[i]; p < A->row_ptr[i + 1]; ++p) {
-                    const int32_t j = A->col[p];
+                    const int64_t j = A->col[p];
                     for (int64_t r = B->row_ptr[j]; r < B->row_ptr[j + 1]; ++r) {
-                        const int32_t c = B->col[r];
+                        const int64_t c = B->col[r];
                         if (stamp[c] != mark) {
                             stamp[c] = mark;
                             ++n;

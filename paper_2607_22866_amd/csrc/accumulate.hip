@@ -28,26 +28,29 @@ GM_DEV int32_t leaf_col_nt(const LeafSet &L, int64_t t) {
 }
 
 // --------------------------------------------------------------- sources
-template <int BLOCK>
+template <int BLOCK, typename V>
 struct GusLds {
     int32_t off[BLOCK + 1];
     int64_t bst[BLOCK];
-    double av[BLOCK];
+    V av[BLOCK];
     int32_t scan[BLOCK / GM_WAVE];
 };
 
 constexpr int GUS_ILP = 4;
 
-// Calls f(col, product) for every intermediate product of the A entries
-// [j0, j1) (one row of A), A entries taken in batches of BLOCK.
-template <int BLOCK, bool NUM, class F>
-GM_DEV void gustavson_row(const Csr &A, const Csr &B, int64_t j0, int64_t j1, GusLds<BLOCK> &L, F &&f) {
+// Calls f(col - base, product) for every intermediate product of the A
+// entries [j0, j1) (one row of A), A entries taken in batches of BLOCK.
+// (base: 0, or the row's smallest column when columns are 64-bit; the row's
+// columns then span less than 2^31, so the offsets fit 32 bits)
+template <int BLOCK, bool NUM, typename CI, typename V, class F>
+GM_DEV void gustavson_row(const CsrV<CI, V> &A, const CsrV<CI, V> &B, int64_t j0, int64_t j1, CI base,
+                          GusLds<BLOCK, V> &L, F &&f) {
     const int tid = threadIdx.x;
     for (int64_t jb = j0; jb < j1; jb += BLOCK) {
         const int nb = (int)(j1 - jb < BLOCK ? j1 - jb : BLOCK);
         int32_t len = 0;
         if (tid < nb) {
-            const int32_t k = A.ci[jb + tid];
+            const int64_t k = (int64_t)A.ci[jb + tid];
             const int64_t bs = B.rp[k];
             len = (int32_t)(B.rp[k + 1] - bs);
             L.bst[tid] = bs;
@@ -62,15 +65,15 @@ GM_DEV void gustavson_row(const Csr &A, const Csr &B, int64_t j0, int64_t j1, Gu
         // product's accumulator update
         for (int32_t tb = tid; tb < tot; tb += BLOCK * GUS_ILP) {
             int32_t c[GUS_ILP];
-            double v[GUS_ILP];
+            V v[GUS_ILP];
 #pragma unroll
             for (int u = 0; u < GUS_ILP; ++u) {
                 const int32_t t = tb + u * BLOCK;
                 if (t < tot) {
                     const int q = (int)find_row(L.off, 0, nb, t);
                     const int64_t src = L.bst[q] + (t - L.off[q]);
-                    c[u] = B.ci[src];
-                    v[u] = NUM ? L.av[q] * B.v[src] : 0.0;
+                    c[u] = (int32_t)(B.ci[src] - base);
+                    v[u] = NUM ? (V)(L.av[q] * B.v[src]) : (V)0;
                 }
             }
 #pragma unroll
@@ -110,8 +113,8 @@ GM_DEV void hash_insert_key(int32_t *keys, int32_t c, int32_t *counter) {
     }
 }
 
-template <int TS>
-GM_DEV void hash_insert_add(int32_t *keys, double *vals, int32_t c, double v) {
+template <int TS, typename V>
+GM_DEV void hash_insert_add(int32_t *keys, V *vals, int32_t c, V v) {
     uint32_t h = hash_slot<TS>(c);
     for (int probe = 0; probe < TS; ++probe) {
         int32_t old = ((volatile int32_t *)keys)[h];
@@ -127,25 +130,25 @@ GM_DEV void hash_insert_add(int32_t *keys, double *vals, int32_t c, double v) {
     }
 }
 
-template <int BLOCK, int TS>
-GM_DEV void hash_clear(int32_t *keys, double *vals) {
+template <int BLOCK, int TS, typename V = double>
+GM_DEV void hash_clear(int32_t *keys, V *vals) {
     for (int i = threadIdx.x; i < TS; i += BLOCK) {
         keys[i] = -1;
-        if (vals) vals[i] = 0.0;
+        if (vals) vals[i] = (V)0;
     }
 }
 
 // Compacts the occupied slots to the front, sorts them by column (bitonic)
 // and writes at most `nnz` entries (the symbolic count) with the column base
 // added. Returns nothing; a count mismatch is flagged in *err.
-template <int BLOCK, int TS>
-GM_DEV void hash_emit_sorted(int32_t *keys, double *vals, int64_t nnz, int32_t col_base, int32_t *out_col,
-                             double *out_val, int32_t *scan_sm, int32_t *err) {
+template <int BLOCK, int TS, typename V, typename CI>
+GM_DEV void hash_emit_sorted(int32_t *keys, V *vals, int64_t nnz, CI col_base, CI *out_col, V *out_val,
+                             int32_t *scan_sm, int32_t *err) {
     constexpr int PER = TS / BLOCK;
     static_assert(PER * BLOCK == TS, "table size must be a multiple of the block");
     const int tid = threadIdx.x;
     int32_t k[PER];
-    double v[PER];
+    V v[PER];
     int cnt = 0;
 #pragma unroll
     for (int q = 0; q < PER; ++q) {
@@ -176,7 +179,7 @@ GM_DEV void hash_emit_sorted(int32_t *keys, double *vals, int64_t nnz, int32_t c
                     if ((a > b) == up) {
                         keys[i] = b;
                         keys[ixj] = a;
-                        const double t = vals[i];
+                        const V t = vals[i];
                         vals[i] = vals[ixj];
                         vals[ixj] = t;
                     }
@@ -187,7 +190,7 @@ GM_DEV void hash_emit_sorted(int32_t *keys, double *vals, int64_t nnz, int32_t c
     if (tid == 0 && total != nnz) atomicOr(err, 1);
     const int n_out = (int64_t)total < nnz ? total : (int)nnz;
     for (int i = tid; i < n_out; i += BLOCK) {
-        out_col[i] = keys[i] + col_base;
+        out_col[i] = (CI)keys[i] + col_base;
         out_val[i] = vals[i];
     }
 }
@@ -195,38 +198,38 @@ GM_DEV void hash_emit_sorted(int32_t *keys, double *vals, int64_t nnz, int32_t c
 // ------------------------------------------------------ dense accumulator
 // VALS = false keeps only the bitmap (symbolic passes), so more work groups
 // fit a CU.
-template <int BLOCK, int WMAX, bool VALS>
+template <int BLOCK, int WMAX, bool VALS, typename V = double>
 struct DenseLdsT {
-    double vals[VALS ? WMAX : 1];
+    V vals[VALS ? WMAX : 1];
     uint32_t bits[(WMAX + 31) / 32];
     int32_t scan[BLOCK / GM_WAVE];
 };
-template <int BLOCK, int WMAX>
-using DenseLds = DenseLdsT<BLOCK, WMAX, true>;
+template <int BLOCK, int WMAX, typename V>
+using DenseLds = DenseLdsT<BLOCK, WMAX, true, V>;
 template <int BLOCK, int WMAX>
 using DenseBits = DenseLdsT<BLOCK, WMAX, false>;
 
-template <int BLOCK, int WMAX, bool VALS>
-GM_DEV void dense_clear(DenseLdsT<BLOCK, WMAX, VALS> &L, int width, bool num) {
+template <int BLOCK, int WMAX, bool VALS, typename V>
+GM_DEV void dense_clear(DenseLdsT<BLOCK, WMAX, VALS, V> &L, int width, bool num) {
     for (int i = threadIdx.x; i < (width + 31) / 32; i += BLOCK) L.bits[i] = 0;
     if (VALS && num)
-        for (int i = threadIdx.x; i < width; i += BLOCK) L.vals[i] = 0.0;
+        for (int i = threadIdx.x; i < width; i += BLOCK) L.vals[i] = (V)0;
 }
 
-template <int BLOCK, int WMAX, bool VALS>
-GM_DEV void dense_set(DenseLdsT<BLOCK, WMAX, VALS> &L, int c) {
+template <int BLOCK, int WMAX, bool VALS, typename V>
+GM_DEV void dense_set(DenseLdsT<BLOCK, WMAX, VALS, V> &L, int c) {
     const uint32_t bit = 1u << (c & 31);
     if (!(((volatile uint32_t *)L.bits)[c >> 5] & bit)) atomicOr(&L.bits[c >> 5], bit);
 }
 
-template <int BLOCK, int WMAX>
-GM_DEV void dense_add(DenseLds<BLOCK, WMAX> &L, int c, double v) {
+template <int BLOCK, int WMAX, typename V>
+GM_DEV void dense_add(DenseLds<BLOCK, WMAX, V> &L, int c, V v) {
     dense_set(L, c);
     __hip_atomic_fetch_add(&L.vals[c], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
-template <int BLOCK, int WMAX, bool VALS>
-GM_DEV int32_t dense_count(DenseLdsT<BLOCK, WMAX, VALS> &L, int width) {
+template <int BLOCK, int WMAX, bool VALS, typename V>
+GM_DEV int32_t dense_count(DenseLdsT<BLOCK, WMAX, VALS, V> &L, int width) {
     int32_t c = 0;
     for (int i = threadIdx.x; i < (width + 31) / 32; i += BLOCK) c += __popc(L.bits[i]);
     return block_reduce_sum<BLOCK>(c, L.scan);
@@ -234,9 +237,9 @@ GM_DEV int32_t dense_count(DenseLdsT<BLOCK, WMAX, VALS> &L, int width) {
 
 // Writes the present columns in increasing order: wave w owns a contiguous
 // range of columns and walks it 64 columns at a time, one per lane.
-template <int BLOCK, int WMAX>
-GM_DEV void dense_emit(DenseLds<BLOCK, WMAX> &L, int width, int64_t nnz, int32_t col_base, int32_t *out_col,
-                       double *out_val, int32_t *err) {
+template <int BLOCK, int WMAX, typename V, typename CI>
+GM_DEV void dense_emit(DenseLds<BLOCK, WMAX, V> &L, int width, int64_t nnz, CI col_base, CI *out_col, V *out_val,
+                       int32_t *err) {
     constexpr int NW = BLOCK / GM_WAVE;
     const int lane = threadIdx.x & (GM_WAVE - 1), w = threadIdx.x / GM_WAVE;
     const int span = ((width + NW - 1) / NW + GM_WAVE - 1) / GM_WAVE * GM_WAVE;
@@ -254,7 +257,7 @@ GM_DEV void dense_emit(DenseLds<BLOCK, WMAX> &L, int width, int64_t nnz, int32_t
         const uint64_t m = ballot(p);
         const int pos = base + __popcll(m & lanemask_lt());
         if (p && pos < nnz) {
-            out_col[pos] = c + col_base;
+            out_col[pos] = (CI)c + col_base;
             out_val[pos] = L.vals[c];
         }
         base += __popcll(m);
@@ -263,9 +266,9 @@ GM_DEV void dense_emit(DenseLds<BLOCK, WMAX> &L, int width, int64_t nnz, int32_t
 
 // dense_emit that also leaves the accumulator zeroed (values of the present
 // columns and this wave's bitmap words), so the next chunk needs no clear.
-template <int BLOCK, int WMAX>
-GM_DEV void dense_emit_clear(DenseLds<BLOCK, WMAX> &L, int width, int64_t nnz, int32_t col_base, int32_t *out_col,
-                             double *out_val, int32_t *err) {
+template <int BLOCK, int WMAX, typename V, typename CI>
+GM_DEV void dense_emit_clear(DenseLds<BLOCK, WMAX, V> &L, int width, int64_t nnz, CI col_base, CI *out_col,
+                             V *out_val, int32_t *err) {
     constexpr int NW = BLOCK / GM_WAVE;
     const int lane = threadIdx.x & (GM_WAVE - 1), w = threadIdx.x / GM_WAVE;
     const int span = ((width + NW - 1) / NW + GM_WAVE - 1) / GM_WAVE * GM_WAVE;  // multiple of 64 columns
@@ -284,10 +287,10 @@ GM_DEV void dense_emit_clear(DenseLds<BLOCK, WMAX> &L, int width, int64_t nnz, i
         const int pos = base + __popcll(m & lanemask_lt());
         if (p) {
             if (pos < nnz) {
-                out_col[pos] = c + col_base;
+                out_col[pos] = (CI)c + col_base;
                 out_val[pos] = L.vals[c];
             }
-            L.vals[c] = 0.0;
+            L.vals[c] = (V)0;
         }
         base += __popcll(m);
     }
@@ -337,14 +340,18 @@ GM_DEV int window_bin(int64_t ip, int64_t span, bool window) {
     return -1;
 }
 
-__global__ void k_light_classes(const int64_t *ip, const int64_t *row_nnz, const int32_t *minc, const int32_t *maxc,
-                                int64_t n, int64_t tau, int window, uint8_t *cls) {
+// A row whose columns span 2^31 or more (possible with 64-bit columns only)
+// cannot be keyed by 32-bit column offsets: it goes to the heavy path,
+// whose chunks are at most 2^31 columns wide.
+template <typename CI>
+__global__ void k_light_classes(const int64_t *ip, const int64_t *row_nnz, const CI *minc, const CI *maxc, int64_t n,
+                                int64_t tau, int window, uint8_t *cls) {
     for (int64_t r = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; r < n; r += (int64_t)gridDim.x * blockDim.x) {
         const int64_t p = ip[r];
         uint8_t c;
         if (p == 0)
             c = LIGHT_EMPTY;
-        else if (p > tau)
+        else if (p > tau || (int64_t)maxc[r] - (int64_t)minc[r] >= (int64_t)INT32_MAX)
             c = LIGHT_HEAVY;
         else {
             const int wb = window_bin(p, (int64_t)maxc[r] - minc[r] + 1, window != 0);
@@ -381,7 +388,7 @@ constexpr int RANK_WIDE_SMALL = 1024;    // wider chunks of at most this many el
 // ranks come from a single wave scan (no hash table to sort). Wider
 // chunks: the bitmap-rank accumulator while the bitmap fits LDS, else the
 // hash map.
-__global__ void k_leaf_classes(LeafSet L, const int64_t *leaf_nnz, int64_t tau, int width, uint8_t *cls) {
+__global__ void k_leaf_classes(LeafSet L, const int64_t *leaf_nnz, int64_t tau, int64_t width, uint8_t *cls) {
     const int64_t n = L.hi - L.lo;
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
         const int64_t j = L.lo + i;
@@ -411,35 +418,44 @@ __global__ void k_leaf_classes(LeafSet L, const int64_t *leaf_nnz, int64_t tau, 
 }
 
 // ------------------------------------------------------------- light rows
-template <int BLOCK, int TS>
-__global__ __launch_bounds__(BLOCK) void k_light_hash_sym(Csr A, Csr B, int64_t r0, const int64_t *items,
-                                                          int64_t *row_nnz) {
+// Key base of a light row: 0 for 32-bit columns (keys are the columns), the
+// row's smallest column for 64-bit ones (keys are offsets from it).
+template <typename CI>
+GM_DEV CI light_base(const CI *minc, int64_t r) {
+    return sizeof(CI) == 8 ? minc[r] : (CI)0;
+}
+
+template <int BLOCK, int TS, typename CI>
+__global__ __launch_bounds__(BLOCK) void k_light_hash_sym(CsrV<CI, NoV> A, CsrV<CI, NoV> B, int64_t r0,
+                                                          const int64_t *items, const CI *minc, int64_t *row_nnz) {
     __shared__ int32_t keys[TS];
-    __shared__ GusLds<BLOCK> G;
+    __shared__ GusLds<BLOCK, NoV> G;
     __shared__ int32_t counter;
     const int64_t r = items[blockIdx.x];
-    hash_clear<BLOCK, TS>(keys, nullptr);
+    hash_clear<BLOCK, TS, double>(keys, nullptr);
     if (threadIdx.x == 0) counter = 0;
     __syncthreads();
-    gustavson_row<BLOCK, false>(A, B, A.rp[r0 + r], A.rp[r0 + r + 1], G,
-                                [&](int32_t c, double) { hash_insert_key<TS>(keys, c, &counter); });
+    gustavson_row<BLOCK, false>(A, B, A.rp[r0 + r], A.rp[r0 + r + 1], light_base(minc, r), G,
+                                [&](int32_t c, NoV) { hash_insert_key<TS>(keys, c, &counter); });
     if (threadIdx.x == 0) row_nnz[r] = counter;
 }
 
-template <int BLOCK, int TS>
-__global__ __launch_bounds__(BLOCK) void k_light_hash_num(Csr A, Csr B, int64_t r0, const int64_t *items,
-                                                          const int64_t *c_row_ptr, int32_t *c_col, double *c_val,
+template <int BLOCK, int TS, typename CI, typename V>
+__global__ __launch_bounds__(BLOCK) void k_light_hash_num(CsrV<CI, V> A, CsrV<CI, V> B, int64_t r0,
+                                                          const int64_t *items, const CI *minc,
+                                                          const int64_t *c_row_ptr, CI *c_col, V *c_val,
                                                           int32_t *err) {
     __shared__ int32_t keys[TS];
-    __shared__ double vals[TS];
-    __shared__ GusLds<BLOCK> G;
+    __shared__ V vals[TS];
+    __shared__ GusLds<BLOCK, V> G;
     const int64_t r = items[blockIdx.x];
+    const CI base = light_base(minc, r);
     hash_clear<BLOCK, TS>(keys, vals);
     __syncthreads();
-    gustavson_row<BLOCK, true>(A, B, A.rp[r0 + r], A.rp[r0 + r + 1], G,
-                               [&](int32_t c, double v) { hash_insert_add<TS>(keys, vals, c, v); });
+    gustavson_row<BLOCK, true>(A, B, A.rp[r0 + r], A.rp[r0 + r + 1], base, G,
+                               [&](int32_t c, V v) { hash_insert_add<TS>(keys, vals, c, v); });
     const int64_t dst = c_row_ptr[r];
-    hash_emit_sorted<BLOCK, TS>(keys, vals, c_row_ptr[r + 1] - dst, 0, c_col + dst, c_val + dst, G.scan, err);
+    hash_emit_sorted<BLOCK, TS>(keys, vals, c_row_ptr[r + 1] - dst, base, c_col + dst, c_val + dst, G.scan, err);
 }
 
 // ------------------------------------------------ sort-based light rows
@@ -644,15 +660,15 @@ GM_DEV bool msd_sort_lds(uint32_t *keys, uint16_t *idx, uint32_t *keys_alt, uint
     return true;
 }
 
-template <int BLOCK, int CAP>
+template <int BLOCK, int CAP, typename V>
 struct SortLds {
     uint32_t keys[2][CAP];
-    double vals[CAP];
+    V vals[CAP];
     uint16_t idx[2][CAP];
     int32_t hist[(BLOCK / GM_WAVE) * 256];
     int32_t off[BLOCK + 1];
     int64_t bst[BLOCK];
-    double av[BLOCK];
+    V av[BLOCK];
     int32_t scan[BLOCK / GM_WAVE];
 };
 
@@ -664,10 +680,10 @@ constexpr int SORT_ILP = 4;
 // position (consecutive lanes on consecutive positions) and writes
 // key + base_col to out_col. Sets err_bit in *err when the run count differs
 // from nnz (the symbolic count).
-template <int BLOCK, int CAP>
-GM_DEV void sorted_runs_emit(const uint32_t *keys, const uint16_t *idx, uint16_t *idx_free, const double *vals, int n,
-                             int64_t nnz, int32_t base_col, int32_t *out_col, double *out_val, int32_t *err,
-                             int err_bit, int32_t *scan_sm) {
+template <int BLOCK, int CAP, typename V, typename CI>
+GM_DEV void sorted_runs_emit(const uint32_t *keys, const uint16_t *idx, uint16_t *idx_free, const V *vals, int n,
+                             int64_t nnz, CI base_col, CI *out_col, V *out_val, int32_t *err, int err_bit,
+                             int32_t *scan_sm) {
     const int tid = threadIdx.x;
     constexpr int PT = (CAP + BLOCK - 1) / BLOCK;
     const int p0 = tid * PT;
@@ -690,26 +706,26 @@ GM_DEV void sorted_runs_emit(const uint32_t *keys, const uint16_t *idx, uint16_t
         const uint32_t k = keys[p];
         if (p == 0 || k != keys[p - 1]) {
             const int o = idx_free[p];
-            double sum = vals[idx[p]];
+            V sum = vals[idx[p]];
             for (int q = p + 1; q < n && keys[q] == k; ++q) sum += vals[idx[q]];
             if (o < nnz) {
-                out_col[o] = (int32_t)k + base_col;
+                out_col[o] = (CI)k + base_col;
                 out_val[o] = sum;
             }
         }
     }
 }
 
-template <int BLOCK, int CAP>
-__global__ __launch_bounds__(BLOCK) void k_light_sort_num(Csr A, Csr B, int64_t r0, const int64_t *items,
-                                                          const int32_t *minc, const int32_t *maxc,
-                                                          const int64_t *c_row_ptr, int32_t *c_col, double *c_val,
+template <int BLOCK, int CAP, typename CI, typename V>
+__global__ __launch_bounds__(BLOCK) void k_light_sort_num(CsrV<CI, V> A, CsrV<CI, V> B, int64_t r0,
+                                                          const int64_t *items, const CI *minc, const CI *maxc,
+                                                          const int64_t *c_row_ptr, CI *c_col, V *c_val,
                                                           int32_t *err) {
     static_assert(CAP < 65536, "16-bit product indices");
-    __shared__ SortLds<BLOCK, CAP> L;
+    __shared__ SortLds<BLOCK, CAP, V> L;
     const int tid = threadIdx.x;
     const int64_t r = items[blockIdx.x];
-    const int32_t base_col = minc[r];
+    const CI base_col = minc[r];
     const uint32_t span = (uint32_t)(maxc[r] - base_col);
     const int64_t j0 = A.rp[r0 + r], j1 = A.rp[r0 + r + 1];
     const int64_t dst = c_row_ptr[r], nnz = c_row_ptr[r + 1] - dst;
@@ -719,7 +735,7 @@ __global__ __launch_bounds__(BLOCK) void k_light_sort_num(Csr A, Csr B, int64_t 
         const int nb = (int)(j1 - jb < BLOCK ? j1 - jb : BLOCK);
         int32_t len = 0;
         if (tid < nb) {
-            const int32_t k = A.ci[jb + tid];
+            const int64_t k = (int64_t)A.ci[jb + tid];
             const int64_t bs = B.rp[k];
             len = (int32_t)(B.rp[k + 1] - bs);
             L.bst[tid] = bs;
@@ -735,8 +751,8 @@ __global__ __launch_bounds__(BLOCK) void k_light_sort_num(Csr A, Csr B, int64_t 
         }
         int q_prev = 0;
         for (int tb = tid; tb < tot; tb += BLOCK * SORT_ILP) {
-            int32_t c[SORT_ILP];
-            double v[SORT_ILP];
+            CI c[SORT_ILP];
+            V v[SORT_ILP];
 #pragma unroll
             for (int u = 0; u < SORT_ILP; ++u) {
                 const int t = tb + u * BLOCK;
@@ -766,41 +782,41 @@ __global__ __launch_bounds__(BLOCK) void k_light_sort_num(Csr A, Csr B, int64_t 
     uint16_t *idx = L.idx[0], *idx_alt = L.idx[1];
     if (CAP > 512 || !msd_sort_lds<BLOCK, CAP>(keys, idx, keys_alt, idx_alt, n, bits, L.hist, L.scan))
         radix_sort_lds<BLOCK, CAP>(keys, idx, keys_alt, idx_alt, n, bits, L.hist, L.scan);
-    sorted_runs_emit<BLOCK, CAP>(keys, idx, idx_alt, L.vals, n, nnz, base_col, c_col + dst, c_val + dst, err, 1,
-                                 L.scan);
+    sorted_runs_emit<BLOCK, CAP>(keys, idx, idx_alt, (const V *)L.vals, n, nnz, base_col, c_col + dst, c_val + dst,
+                                 err, 1, L.scan);
 }
 
-template <int BLOCK, int WMAX>
-__global__ __launch_bounds__(BLOCK) void k_light_win_sym(Csr A, Csr B, int64_t r0, const int64_t *items,
-                                                         const int32_t *minc, const int32_t *maxc,
+template <int BLOCK, int WMAX, typename CI>
+__global__ __launch_bounds__(BLOCK) void k_light_win_sym(CsrV<CI, NoV> A, CsrV<CI, NoV> B, int64_t r0,
+                                                         const int64_t *items, const CI *minc, const CI *maxc,
                                                          int64_t *row_nnz) {
     __shared__ DenseBits<BLOCK, WMAX> D;
-    __shared__ GusLds<BLOCK> G;
+    __shared__ GusLds<BLOCK, NoV> G;
     const int64_t r = items[blockIdx.x];
-    const int32_t base = minc[r];
-    const int width = maxc[r] - base + 1;
+    const CI base = minc[r];
+    const int width = (int)(maxc[r] - base + 1);
     dense_clear(D, width, false);
     __syncthreads();
-    gustavson_row<BLOCK, false>(A, B, A.rp[r0 + r], A.rp[r0 + r + 1], G,
-                                [&](int32_t c, double) { dense_set(D, c - base); });
+    gustavson_row<BLOCK, false>(A, B, A.rp[r0 + r], A.rp[r0 + r + 1], base, G,
+                                [&](int32_t c, NoV) { dense_set(D, c); });
     const int32_t cnt = dense_count(D, width);
     if (threadIdx.x == 0) row_nnz[r] = cnt;
 }
 
-template <int BLOCK, int WMAX>
-__global__ __launch_bounds__(BLOCK) void k_light_win_num(Csr A, Csr B, int64_t r0, const int64_t *items,
-                                                         const int32_t *minc, const int32_t *maxc,
-                                                         const int64_t *c_row_ptr, int32_t *c_col, double *c_val,
+template <int BLOCK, int WMAX, typename CI, typename V>
+__global__ __launch_bounds__(BLOCK) void k_light_win_num(CsrV<CI, V> A, CsrV<CI, V> B, int64_t r0,
+                                                         const int64_t *items, const CI *minc, const CI *maxc,
+                                                         const int64_t *c_row_ptr, CI *c_col, V *c_val,
                                                          int32_t *err) {
-    __shared__ DenseLds<BLOCK, WMAX> D;
-    __shared__ GusLds<BLOCK> G;
+    __shared__ DenseLds<BLOCK, WMAX, V> D;
+    __shared__ GusLds<BLOCK, V> G;
     const int64_t r = items[blockIdx.x];
-    const int32_t base = minc[r];
-    const int width = maxc[r] - base + 1;
+    const CI base = minc[r];
+    const int width = (int)(maxc[r] - base + 1);
     dense_clear(D, width, true);
     __syncthreads();
-    gustavson_row<BLOCK, true>(A, B, A.rp[r0 + r], A.rp[r0 + r + 1], G,
-                               [&](int32_t c, double v) { dense_add(D, c - base, v); });
+    gustavson_row<BLOCK, true>(A, B, A.rp[r0 + r], A.rp[r0 + r + 1], base, G,
+                               [&](int32_t c, V v) { dense_add(D, c, v); });
     const int64_t dst = c_row_ptr[r];
     dense_emit(D, width, c_row_ptr[r + 1] - dst, base, c_col + dst, c_val + dst, err);
 }
@@ -813,7 +829,7 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_hash_sym(LeafSet L, const LeafTa
     __shared__ int32_t counter;
     const LeafTask tk = tasks[blockIdx.x];
     const int64_t s = tk.s, e = tk.e;
-    hash_clear<BLOCK, TS>(keys, nullptr);
+    hash_clear<BLOCK, TS, double>(keys, nullptr);
     if (threadIdx.x == 0) counter = 0;
     __syncthreads();
     for (int64_t t = s + threadIdx.x; t < e; t += BLOCK) hash_insert_key<TS>(keys, leaf_col(L, t), &counter);
@@ -824,24 +840,31 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_hash_sym(LeafSet L, const LeafTa
     }
 }
 
+// Where a leaf's output goes: the slot grid of the heavy rows.
 struct LeafOut {
     int64_t n_slots_log2;
     const int64_t *heavy_rows;
     const int64_t *c_row_ptr;
     const int64_t *slot_off;
-    int64_t slot_width_log2;
-    int32_t *c_col;
-    double *c_val;
-    int32_t *err;
 };
 
-GM_DEV void leaf_target(const LeafOut &o, int64_t origin, int64_t &dst, int64_t &nnz_cap, int32_t &col_base) {
+// C's arrays for the numeric leaf kernels; a leaf's first column is its
+// slot << slot_width_log2.
+template <typename CI, typename V>
+struct LeafDst {
+    CI *c_col;
+    V *c_val;
+    int32_t *err;
+    int slot_width_log2;
+    GM_DEV CI base(const LeafTask &tk) const { return (CI)tk.b << slot_width_log2; }
+};
+
+GM_DEV void leaf_target(const LeafOut &o, int64_t origin, int64_t &dst, int64_t &nnz_cap, int32_t &slot) {
     const int64_t h = origin >> o.n_slots_log2;
-    const int64_t slot = origin & ((int64_t(1) << o.n_slots_log2) - 1);
+    slot = (int32_t)(origin & ((int64_t(1) << o.n_slots_log2) - 1));
     const int64_t row = o.heavy_rows[h];
     dst = o.c_row_ptr[row] + o.slot_off[origin];
     nnz_cap = o.c_row_ptr[row + 1] - dst;
-    col_base = (int32_t)(slot << o.slot_width_log2);
 }
 
 // Per-leaf launch records, in the order of a bin partition, so every leaf
@@ -860,27 +883,27 @@ __global__ void k_leaf_tasks_num(LeafSet L, const int64_t *items, int64_t n, con
         const int64_t i = items[k];
         const int64_t j = L.lo + i;
         int64_t dst, cap;
-        int32_t base;
-        leaf_target(o, L.origin[j], dst, cap, base);
+        int32_t slot;
+        leaf_target(o, L.origin[j], dst, cap, slot);
         const int64_t nnz = leaf_nnz[i] < cap ? leaf_nnz[i] : cap;
-        tasks[k] = LeafTask{L.ptr[j], L.ptr[j + 1], dst, (int32_t)nnz, base};
+        tasks[k] = LeafTask{L.ptr[j], L.ptr[j + 1], dst, (int32_t)nnz, slot};
     }
 }
 
-template <int BLOCK, int TS>
-__global__ __launch_bounds__(BLOCK) void k_leaf_hash_num(LeafSet L, const LeafTask *tasks, LeafOut o) {
+template <int BLOCK, int TS, typename CI, typename V>
+__global__ __launch_bounds__(BLOCK) void k_leaf_hash_num(LeafSet L, const LeafTask *tasks, LeafDst<CI, V> o) {
     __shared__ int32_t keys[TS];
-    __shared__ double vals[TS];
+    __shared__ V vals[TS];
     __shared__ int32_t scan_sm[BLOCK / GM_WAVE];
     const LeafTask tk = tasks[blockIdx.x];
     const int64_t s = tk.s, e = tk.e;
+    const V *lv = static_cast<const V *>(L.val);
     hash_clear<BLOCK, TS>(keys, vals);
     __syncthreads();
-    for (int64_t t = s + threadIdx.x; t < e; t += BLOCK) hash_insert_add<TS>(keys, vals, leaf_col(L, t), L.val[t]);
+    for (int64_t t = s + threadIdx.x; t < e; t += BLOCK) hash_insert_add<TS>(keys, vals, leaf_col(L, t), lv[t]);
     __syncthreads();
     const int64_t dst = tk.t, nnz = tk.a;
-    const int32_t base = tk.b;
-    hash_emit_sorted<BLOCK, TS>(keys, vals, nnz, base, o.c_col + dst, o.c_val + dst, scan_sm, o.err);
+    hash_emit_sorted<BLOCK, TS>(keys, vals, nnz, o.base(tk), o.c_col + dst, o.c_val + dst, scan_sm, o.err);
 }
 
 
@@ -946,21 +969,22 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_dense_sym(LeafSet L, const LeafT
 // the current batch's LDS atomics.
 constexpr int DENSE_BLOCK = 1024, DENSE_EPT = 2, DENSE_GROUPS_PER_CU = 2;
 
-template <int BLOCK, int EPT>
-GM_DEV void dense_load(const LeafSet &L, int64_t b, int64_t e, int32_t (&c)[EPT], double (&v)[EPT]) {
+template <int BLOCK, int EPT, typename V>
+GM_DEV void dense_load(const LeafSet &L, int64_t b, int64_t e, int32_t (&c)[EPT], V (&v)[EPT]) {
+    const V *lv = static_cast<const V *>(L.val);
 #pragma unroll
     for (int q = 0; q < EPT; ++q) {
         const int64_t t = b + q * BLOCK + threadIdx.x;
         c[q] = t < e ? leaf_col_nt(L, t) : -1;
-        v[q] = t < e ? __builtin_nontemporal_load(&L.val[t]) : 0.0;
+        v[q] = t < e ? __builtin_nontemporal_load(&lv[t]) : (V)0;
     }
 }
 
 // (at most 64 VGPRs: two 16-wave work groups per CU need 8 waves per SIMD)
-template <int BLOCK, int EPT>
+template <int BLOCK, int EPT, typename CI, typename V>
 __global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(8))) void k_leaf_dense_num(
-    LeafSet L, const LeafTask *tasks, int64_t n_tasks, int width, LeafOut o, int32_t *counter) {
-    __shared__ DenseLds<BLOCK, DENSE_MAX> D;
+    LeafSet L, const LeafTask *tasks, int64_t n_tasks, int width, LeafDst<CI, V> o, int32_t *counter) {
+    __shared__ DenseLds<BLOCK, DENSE_MAX, V> D;
     __shared__ int32_t grabbed;
     constexpr int STEP = BLOCK * EPT;
     if (threadIdx.x == 0) grabbed = atomicAdd(counter, 1);
@@ -970,14 +994,14 @@ __global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(8))) void
     if (cur >= n_tasks) return;  // uniform across the work group
     LeafTask tk = tasks[cur];
     int32_t c[EPT];
-    double v[EPT];
+    V v[EPT];
     dense_load<BLOCK, EPT>(L, tk.s, tk.e, c, v);
     while (true) {
         __syncthreads();  // the accumulator is clear and everyone has read `grabbed`
         if (threadIdx.x == 0) grabbed = atomicAdd(counter, 1);
         for (int64_t b = tk.s; b < tk.e; b += STEP) {
             int32_t cn[EPT];
-            double vn[EPT];
+            V vn[EPT];
             dense_load<BLOCK, EPT>(L, b + STEP, tk.e, cn, vn);
 #pragma unroll
             for (int q = 0; q < EPT; ++q)
@@ -995,7 +1019,7 @@ __global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(8))) void
             tn = tasks[nxt];
             dense_load<BLOCK, EPT>(L, tn.s, tn.e, c, v);  // in flight during the write-out
         }
-        dense_emit_clear(D, width, tk.a, tk.b, o.c_col + tk.t, o.c_val + tk.t, o.err);
+        dense_emit_clear(D, width, tk.a, o.base(tk), o.c_col + tk.t, o.c_val + tk.t, o.err);
         if (nxt >= n_tasks) break;
         tk = tn;
     }
@@ -1033,13 +1057,14 @@ static_assert(RANK_SWORDS * 32 == DENSE_MAX, "narrow bitmap covers the dense wid
 constexpr int RANK_TBLOCK = 64, RANK_TEPT = 4;  // one wave for narrow chunks below RANK_MIN_LEN elements
 static_assert(RANK_TBLOCK * RANK_TEPT >= RANK_MIN_LEN, "the one-wave shape holds its chunks");
 
-template <int BLOCK, int EPT>
-GM_DEV void rank_load(const LeafSet &L, int64_t s, int64_t e, int32_t (&c)[EPT], double (&v)[EPT], bool vals) {
+template <int BLOCK, int EPT, typename V>
+GM_DEV void rank_load(const LeafSet &L, int64_t s, int64_t e, int32_t (&c)[EPT], V (&v)[EPT], bool vals) {
+    const V *lv = static_cast<const V *>(L.val);
 #pragma unroll
     for (int q = 0; q < EPT; ++q) {
         const int64_t t = s + q * BLOCK + threadIdx.x;
         c[q] = t < e ? leaf_col_nt(L, t) : -1;
-        if (vals) v[q] = t < e ? __builtin_nontemporal_load(&L.val[t]) : 0.0;
+        if (vals) v[q] = t < e ? __builtin_nontemporal_load(&lv[t]) : (V)0;
     }
 }
 
@@ -1087,7 +1112,7 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_rank_sym(LeafSet L, const LeafTa
     __shared__ int32_t count;
     const LeafTask tk = tasks[blockIdx.x];
     int32_t c[EPT];
-    double v[EPT];
+    float v[EPT];  // not loaded: symbolic
     rank_load<BLOCK, EPT>(L, tk.s, tk.e, c, v, false);
     const int cols = width / PASSES;
     int32_t total = 0;
@@ -1111,25 +1136,26 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_rank_sym(LeafSet L, const LeafTa
 // Wide bitmaps keep one rank per group of 8 words instead of one per word
 // (a sixteenth of the LDS; an element reads its group's 8 words), so more
 // work groups fit a CU.
-template <int BLOCK, int NWORDS, int CAP, int EPT, int PASSES = 1>
-__global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const LeafTask *tasks, int width, LeafOut o) {
+template <int BLOCK, int NWORDS, int CAP, int EPT, int PASSES, typename CI, typename V>
+__global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const LeafTask *tasks, int width,
+                                                         LeafDst<CI, V> o) {
     constexpr int NWP = NWORDS / PASSES;  // bitmap words of one part
     constexpr bool GROUPED = NWP >= 1024;
     constexpr int NPRE = GROUPED ? NWP / 8 : NWP;
     constexpr int WPT = (NPRE + BLOCK - 1) / BLOCK;  // rank entries per thread in the scan
     __shared__ __align__(16) uint32_t bits[NWP];
     __shared__ uint16_t wpre[NPRE];  // rank of each word's (group's) first set bit (ranks < CAP <= 65535)
-    __shared__ double vals[CAP];
+    __shared__ V vals[CAP];
     __shared__ int32_t scan_sm[BLOCK / GM_WAVE];
     __shared__ int32_t count;
     const LeafTask tk = tasks[blockIdx.x];
     const int64_t dst = tk.t, nnz = tk.a;
-    const int32_t base = tk.b;
+    const CI base = o.base(tk);
     const int cols = width / PASSES;
     const int nwords = cols >> 5;
     const int m = nnz < CAP ? (int)nnz : CAP;  // ranks at or above m are never written (count checked below)
     int32_t c[EPT];
-    double v[EPT];
+    V v[EPT];
     rank_load<BLOCK, EPT>(L, tk.s, tk.e, c, v, true);
     int32_t done = 0;  // distinct columns of the parts before this one
     auto part = [&](int pass) {
@@ -1165,7 +1191,7 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const LeafTa
                 }
         }
         if (pass == 0)
-            for (int q = threadIdx.x; q < m; q += BLOCK) vals[q] = 0.0;
+            for (int q = threadIdx.x; q < m; q += BLOCK) vals[q] = (V)0;
         __syncthreads();
 #pragma unroll
         for (int q = 0; q < EPT; ++q)
@@ -1188,7 +1214,7 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const LeafTa
                 rk += done;
                 if (rk < m) {
                     __hip_atomic_fetch_add(&vals[rk], v[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-                    if ((fresh >> q) & 1u) o.c_col[dst + rk] = base + c[q];
+                    if ((fresh >> q) & 1u) o.c_col[dst + rk] = base + (CI)c[q];
                 }
             }
         done += count;
@@ -1211,10 +1237,11 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_rank_num(LeafSet L, const LeafTa
 // a cheap bitmap): the chunk's elements are sorted in LDS by column (one
 // bucket pass when they spread evenly, else an LSD radix sort) and the runs
 // summed, instead of a hash table followed by a bitonic sort of all its slots.
-template <int BLOCK, int CAP>
-__global__ __launch_bounds__(BLOCK) void k_leaf_sort_num(LeafSet L, const LeafTask *tasks, int width, LeafOut o) {
+template <int BLOCK, int CAP, typename CI, typename V>
+__global__ __launch_bounds__(BLOCK) void k_leaf_sort_num(LeafSet L, const LeafTask *tasks, int width,
+                                                         LeafDst<CI, V> o) {
     static_assert(CAP < 65536, "16-bit element indices");
-    __shared__ SortLds<BLOCK, CAP> S;
+    __shared__ SortLds<BLOCK, CAP, V> S;
     const int tid = threadIdx.x;
     const LeafTask tk = tasks[blockIdx.x];
     const int64_t len = tk.e - tk.s;
@@ -1225,7 +1252,7 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_sort_num(LeafSet L, const LeafTa
     const int n = (int)len;
     for (int i = tid; i < n; i += BLOCK) {
         S.keys[0][i] = (uint32_t)leaf_col_nt(L, tk.s + i);
-        S.vals[i] = __builtin_nontemporal_load(&L.val[tk.s + i]);
+        S.vals[i] = __builtin_nontemporal_load(&static_cast<const V *>(L.val)[tk.s + i]);
         S.idx[0][i] = (uint16_t)i;
     }
     __syncthreads();
@@ -1234,8 +1261,8 @@ __global__ __launch_bounds__(BLOCK) void k_leaf_sort_num(LeafSet L, const LeafTa
     uint16_t *idx = S.idx[0], *idx_alt = S.idx[1];
     if (!msd_sort_lds<BLOCK, CAP>(keys, idx, keys_alt, idx_alt, n, bits, S.hist, S.scan))
         radix_sort_lds<BLOCK, CAP>(keys, idx, keys_alt, idx_alt, n, bits, S.hist, S.scan);
-    sorted_runs_emit<BLOCK, CAP>(keys, idx, idx_alt, S.vals, n, tk.a, tk.b, o.c_col + tk.t, o.c_val + tk.t, o.err, 4,
-                                 S.scan);
+    sorted_runs_emit<BLOCK, CAP>(keys, idx, idx_alt, (const V *)S.vals, n, tk.a, o.base(tk), o.c_col + tk.t,
+                                 o.c_val + tk.t, o.err, 4, S.scan);
 }
 
 // Symbolic of the bitmap-rank bins, one wave per chunk: the wave clears its
@@ -1340,30 +1367,30 @@ void launch_items(K kernel, int block, int64_t n, hipStream_t s, Args... args) {
 
 }  // namespace
 
-void light_classes_sym(const int64_t *ip, const int32_t *minc, const int32_t *maxc, int64_t n, int64_t tau,
+void light_classes_sym(const int64_t *ip, const void *minc, const void *maxc, bool ci64, int64_t n, int64_t tau,
                        bool window, uint8_t *cls, hipStream_t s) {
-    if (n <= 0) return;
-    hipLaunchKernelGGL(k_light_classes, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, ip, nullptr, minc, maxc, n,
-                       tau, (int)window, cls);
-    GM_CHECK_LAUNCH();
+    light_classes_num(ip, nullptr, minc, maxc, ci64, n, tau, window, cls, s);
 }
 
-void light_classes_num(const int64_t *ip, const int64_t *row_nnz, const int32_t *minc, const int32_t *maxc,
+void light_classes_num(const int64_t *ip, const int64_t *row_nnz, const void *minc, const void *maxc, bool ci64,
                        int64_t n, int64_t tau, bool window, uint8_t *cls, hipStream_t s) {
     if (n <= 0) return;
-    hipLaunchKernelGGL(k_light_classes, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, ip, row_nnz, minc, maxc, n,
-                       tau, (int)window, cls);
-    GM_CHECK_LAUNCH();
+    with_index_type(ci64, [&](auto ci) {
+        using CI = decltype(ci);
+        hipLaunchKernelGGL(k_light_classes<CI>, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, ip, row_nnz,
+                           static_cast<const CI *>(minc), static_cast<const CI *>(maxc), n, tau, (int)window, cls);
+        GM_CHECK_LAUNCH();
+    });
 }
 
-void leaf_classes_sym(const LeafSet &L, int64_t tau, int width, uint8_t *cls, hipStream_t s) {
+void leaf_classes_sym(const LeafSet &L, int64_t tau, int64_t width, uint8_t *cls, hipStream_t s) {
     const int64_t n = L.hi - L.lo;
     if (n <= 0) return;
     hipLaunchKernelGGL(k_leaf_classes, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, L, nullptr, tau, width, cls);
     GM_CHECK_LAUNCH();
 }
 
-void leaf_classes_num(const LeafSet &L, const int64_t *leaf_nnz, int64_t tau, int width, uint8_t *cls,
+void leaf_classes_num(const LeafSet &L, const int64_t *leaf_nnz, int64_t tau, int64_t width, uint8_t *cls,
                       hipStream_t s) {
     const int64_t n = L.hi - L.lo;
     if (n <= 0) return;
@@ -1372,57 +1399,87 @@ void leaf_classes_num(const LeafSet &L, const int64_t *leaf_nnz, int64_t tau, in
 }
 
 void light_symbolic(const Csr &A, const Csr &B, int64_t r0, int bin, const int64_t *items, int64_t n,
-                    const int32_t *minc, const int32_t *maxc, int64_t *row_nnz, hipStream_t s) {
-    switch (bin) {
-    case LIGHT_W0: launch_items(k_light_win_sym<64, WIN0>, 64, n, s, A, B, r0, items, minc, maxc, row_nnz); break;
-    case LIGHT_W1: launch_items(k_light_win_sym<256, WIN1>, 256, n, s, A, B, r0, items, minc, maxc, row_nnz); break;
-    case LIGHT_H0: launch_items(k_light_hash_sym<64, 2 * HS_CAP[0]>, 64, n, s, A, B, r0, items, row_nnz); break;
-    case LIGHT_H1: launch_items(k_light_hash_sym<64, 2 * HS_CAP[1]>, 64, n, s, A, B, r0, items, row_nnz); break;
-    case LIGHT_H2: launch_items(k_light_hash_sym<256, 2 * HS_CAP[2]>, 256, n, s, A, B, r0, items, row_nnz); break;
-    case LIGHT_H3: launch_items(k_light_hash_sym<512, 2 * HS_CAP[3]>, 512, n, s, A, B, r0, items, row_nnz); break;
-    default: break;
-    }
+                    const void *minc_v, const void *maxc_v, int64_t *row_nnz, hipStream_t s) {
+    with_index_type(B.ci64, [&](auto ci) {
+        using CI = decltype(ci);
+        const auto a = typed<CI, NoV>(A);
+        const auto b = typed<CI, NoV>(B);
+        const CI *minc = static_cast<const CI *>(minc_v), *maxc = static_cast<const CI *>(maxc_v);
+        switch (bin) {
+        case LIGHT_W0:
+            launch_items(k_light_win_sym<64, WIN0, CI>, 64, n, s, a, b, r0, items, minc, maxc, row_nnz);
+            break;
+        case LIGHT_W1:
+            launch_items(k_light_win_sym<256, WIN1, CI>, 256, n, s, a, b, r0, items, minc, maxc, row_nnz);
+            break;
+        case LIGHT_H0:
+            launch_items(k_light_hash_sym<64, 2 * HS_CAP[0], CI>, 64, n, s, a, b, r0, items, minc, row_nnz);
+            break;
+        case LIGHT_H1:
+            launch_items(k_light_hash_sym<64, 2 * HS_CAP[1], CI>, 64, n, s, a, b, r0, items, minc, row_nnz);
+            break;
+        case LIGHT_H2:
+            launch_items(k_light_hash_sym<256, 2 * HS_CAP[2], CI>, 256, n, s, a, b, r0, items, minc, row_nnz);
+            break;
+        case LIGHT_H3:
+            launch_items(k_light_hash_sym<512, 2 * HS_CAP[3], CI>, 512, n, s, a, b, r0, items, minc, row_nnz);
+            break;
+        default: break;
+        }
+    });
 }
 
 void light_numeric(const Csr &A, const Csr &B, int64_t r0, int bin, const int64_t *items, int64_t n,
-                   const int32_t *minc, const int32_t *maxc, const int64_t *c_row_ptr, int32_t *c_col, double *c_val,
+                   const void *minc_v, const void *maxc_v, const int64_t *c_row_ptr, void *c_col_v, void *c_val_v,
                    int32_t *err, hipStream_t s) {
-    switch (bin) {
-    case LIGHT_W0:
-        launch_items(k_light_win_num<64, WIN0>, 64, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col, c_val, err);
-        break;
-    case LIGHT_W1:
-        launch_items(k_light_win_num<256, WIN1>, 256, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col, c_val,
-                     err);
-        break;
-    case LIGHT_H0:
-        launch_items(k_light_hash_num<64, 256>, 64, n, s, A, B, r0, items, c_row_ptr, c_col, c_val, err);
-        break;
-    case LIGHT_H1:
-        launch_items(k_light_sort_num<64, SORT_SMALL[0]>, 64, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col,
-                     c_val, err);
-        break;
-    case LIGHT_H2:
-        launch_items(k_light_sort_num<64, SORT_SMALL[1]>, 64, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col,
-                     c_val, err);
-        break;
-    case LIGHT_H3:
-        launch_items(k_light_hash_num<64, 1024>, 64, n, s, A, B, r0, items, c_row_ptr, c_col, c_val, err);
-        break;
-    case LIGHT_H4:
-        launch_items(k_light_sort_num<256, SORT_CAP[0]>, 256, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col,
-                     c_val, err);
-        break;
-    case LIGHT_H5:
-        launch_items(k_light_sort_num<256, SORT_CAP[1]>, 256, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col,
-                     c_val, err);
-        break;
-    case LIGHT_H6:
-        launch_items(k_light_sort_num<512, SORT_CAP[2]>, 512, n, s, A, B, r0, items, minc, maxc, c_row_ptr, c_col,
-                     c_val, err);
-        break;
-    default: break;
-    }
+    with_types(B, [&](auto ci, auto v) {
+        using CI = decltype(ci);
+        using V = decltype(v);
+        const auto a = typed<CI, V>(A);
+        const auto b = typed<CI, V>(B);
+        const CI *minc = static_cast<const CI *>(minc_v), *maxc = static_cast<const CI *>(maxc_v);
+        CI *c_col = static_cast<CI *>(c_col_v);
+        V *c_val = static_cast<V *>(c_val_v);
+        switch (bin) {
+        case LIGHT_W0:
+            launch_items(k_light_win_num<64, WIN0, CI, V>, 64, n, s, a, b, r0, items, minc, maxc, c_row_ptr, c_col,
+                         c_val, err);
+            break;
+        case LIGHT_W1:
+            launch_items(k_light_win_num<256, WIN1, CI, V>, 256, n, s, a, b, r0, items, minc, maxc, c_row_ptr, c_col,
+                         c_val, err);
+            break;
+        case LIGHT_H0:
+            launch_items(k_light_hash_num<64, 256, CI, V>, 64, n, s, a, b, r0, items, minc, c_row_ptr, c_col, c_val,
+                         err);
+            break;
+        case LIGHT_H1:
+            launch_items(k_light_sort_num<64, SORT_SMALL[0], CI, V>, 64, n, s, a, b, r0, items, minc, maxc, c_row_ptr,
+                         c_col, c_val, err);
+            break;
+        case LIGHT_H2:
+            launch_items(k_light_sort_num<64, SORT_SMALL[1], CI, V>, 64, n, s, a, b, r0, items, minc, maxc, c_row_ptr,
+                         c_col, c_val, err);
+            break;
+        case LIGHT_H3:
+            launch_items(k_light_hash_num<64, 1024, CI, V>, 64, n, s, a, b, r0, items, minc, c_row_ptr, c_col, c_val,
+                         err);
+            break;
+        case LIGHT_H4:
+            launch_items(k_light_sort_num<256, SORT_CAP[0], CI, V>, 256, n, s, a, b, r0, items, minc, maxc, c_row_ptr,
+                         c_col, c_val, err);
+            break;
+        case LIGHT_H5:
+            launch_items(k_light_sort_num<256, SORT_CAP[1], CI, V>, 256, n, s, a, b, r0, items, minc, maxc, c_row_ptr,
+                         c_col, c_val, err);
+            break;
+        case LIGHT_H6:
+            launch_items(k_light_sort_num<512, SORT_CAP[2], CI, V>, 512, n, s, a, b, r0, items, minc, maxc, c_row_ptr,
+                         c_col, c_val, err);
+            break;
+        default: break;
+        }
+    });
 }
 
 void leaf_tasks_sym(const LeafSet &L, const int64_t *items, int64_t n, LeafTask *tasks, hipStream_t s) {
@@ -1435,14 +1492,17 @@ void leaf_tasks_num(const LeafSet &L, const int64_t *items, int64_t n, const int
                     const int64_t *heavy_rows, const int64_t *c_row_ptr, const int64_t *slot_off,
                     int slot_width_log2, LeafTask *tasks, hipStream_t s) {
     if (n <= 0) return;
-    LeafOut o{n_slots_log2, heavy_rows, c_row_ptr, slot_off, slot_width_log2, nullptr, nullptr, nullptr};
+    (void)slot_width_log2;
+    LeafOut o{n_slots_log2, heavy_rows, c_row_ptr, slot_off};
     hipLaunchKernelGGL(k_leaf_tasks_num, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, L, items, n, leaf_nnz, o,
                        tasks);
     GM_CHECK_LAUNCH();
 }
 
-void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *items, int64_t n, int width, int64_t e_end,
+void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *items, int64_t n, int64_t width64, int64_t e_end,
                    int64_t *leaf_nnz, int64_t *slot_cnt, hipStream_t s) {
+    // the kernels that read the width (dense and rank shapes) take chunks of at most 2^18 columns
+    const int width = (int)(width64 < ((int64_t)1 << 30) ? width64 : ((int64_t)1 << 30));
     const bool rank_bin = bin == LEAF_RANK || bin == LEAF_RANK_L || bin == LEAF_RANK_XL || bin == LEAF_RANK_T;
     const void *colp = L.col16 ? (const void *)L.col16 : (const void *)L.col;
     if (rank_bin && width >= 32 && width <= DENSE_MAX && ((uintptr_t)colp & 15) == 0) {
@@ -1502,42 +1562,39 @@ void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *items, int64_t n, 
     }
 }
 
-void leaf_numeric(const LeafSet &L, int bin, const LeafTask *items, int64_t n, int width, int32_t *c_col,
-                  double *c_val, int32_t *err, int32_t *counter, hipStream_t s) {
-    LeafOut o{0, nullptr, nullptr, nullptr, 0, c_col, c_val, err};
+template <typename CI, typename V>
+void leaf_numeric_typed(const LeafSet &L, int bin, const LeafTask *items, int64_t n, int width, LeafDst<CI, V> o,
+                        int32_t *counter, hipStream_t s) {
     switch (bin) {
     case LEAF_H0:
     case LEAF_H1:
         // bitmap-rank-wide levels send only chunks of fewer than RANK_MIN_LEN elements here
         if (width <= (1 << RANK_MAX_LOG2))
-            launch_items(k_leaf_sort_num<64, RANK_MIN_LEN>, 64, n, s, L, items, width, o);
+            launch_items(k_leaf_sort_num<64, RANK_MIN_LEN, CI, V>, 64, n, s, L, items, width, o);
         else if (bin == LEAF_H0)
-            launch_items(k_leaf_hash_num<64, 256>, 64, n, s, L, items, o);
+            launch_items(k_leaf_hash_num<64, 256, CI, V>, 64, n, s, L, items, o);
         else
-            launch_items(k_leaf_hash_num<64, 1024>, 64, n, s, L, items, o);
+            launch_items(k_leaf_hash_num<64, 1024, CI, V>, 64, n, s, L, items, o);
         break;
-    case LEAF_H2: launch_items(k_leaf_hash_num<256, 4096>, 256, n, s, L, items, o); break;
-    case LEAF_H3: launch_items(k_leaf_hash_num<512, 8192>, 512, n, s, L, items, o); break;
+    case LEAF_H2: launch_items(k_leaf_hash_num<256, 4096, CI, V>, 256, n, s, L, items, o); break;
+    case LEAF_H3: launch_items(k_leaf_hash_num<512, 8192, CI, V>, 512, n, s, L, items, o); break;
     case LEAF_DENSE:
         GM_REQUIRE(n <= 0 || width <= DENSE_MAX, GMAGNUS_ERROR_UNSUPPORTED, "dense accumulator wider than LDS allows");
         if (n > 0) {
-            static int n_cu = 0;
-            if (n_cu == 0) {
-                int dev = 0;
-                GM_HIP(hipGetDevice(&dev));
-                GM_HIP(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev));
-            }
+            int dev = 0, n_cu = 0;
+            GM_HIP(hipGetDevice(&dev));
+            GM_HIP(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev));
             fill<int32_t>(counter, 0, 1, s);
             const int64_t groups = std::min<int64_t>(n, (int64_t)n_cu * DENSE_GROUPS_PER_CU);
-            hipLaunchKernelGGL((k_leaf_dense_num<DENSE_BLOCK, DENSE_EPT>), dim3((unsigned)groups), dim3(DENSE_BLOCK),
-                               0, s, L, items, n, width, o, counter);
+            hipLaunchKernelGGL((k_leaf_dense_num<DENSE_BLOCK, DENSE_EPT, CI, V>), dim3((unsigned)groups),
+                               dim3(DENSE_BLOCK), 0, s, L, items, n, width, o, counter);
             GM_CHECK_LAUNCH();
         }
         break;
     case LEAF_RANK_T:
         GM_REQUIRE(n <= 0 || width <= DENSE_MAX, GMAGNUS_ERROR_UNSUPPORTED, "one-wave rank shape is for narrow chunks");
-        launch_items(k_leaf_rank_num<RANK_TBLOCK, RANK_SWORDS, RANK_MIN_LEN, RANK_TEPT>, RANK_TBLOCK, n, s, L, items,
-                     width, o);
+        launch_items(k_leaf_rank_num<RANK_TBLOCK, RANK_SWORDS, RANK_MIN_LEN, RANK_TEPT, 1, CI, V>, RANK_TBLOCK, n, s, L,
+                     items, width, o);
         break;
     case LEAF_RANK:
     case LEAF_RANK_L:
@@ -1546,34 +1603,47 @@ void leaf_numeric(const LeafSet &L, int bin, const LeafTask *items, int64_t n, i
         constexpr int W17 = (1 << 17) / 32, W18 = (1 << 18) / 32;
         const bool narrow = width <= (1 << 17);
         if (width <= DENSE_MAX && bin == LEAF_RANK)  // at most RANK_NARROW_SMALL elements
-            launch_items(k_leaf_rank_num<RANK_SBLOCK, RANK_SWORDS, RANK_SCAP, RANK_SEPT>, RANK_SBLOCK, n, s, L, items,
-                         width, o);
+            launch_items(k_leaf_rank_num<RANK_SBLOCK, RANK_SWORDS, RANK_SCAP, RANK_SEPT, 1, CI, V>, RANK_SBLOCK, n, s, L,
+                         items, width, o);
         else if (width <= DENSE_MAX && bin == LEAF_RANK_L)  // at most RANK_NARROW_MID elements
-            launch_items(k_leaf_rank_num<RANK_SBLOCK, RANK_SWORDS, RANK_NARROW_MID, RANK_LEPT>, RANK_SBLOCK, n, s, L,
-                         items, width, o);
+            launch_items(k_leaf_rank_num<RANK_SBLOCK, RANK_SWORDS, RANK_NARROW_MID, RANK_LEPT, 1, CI, V>, RANK_SBLOCK,
+                         n, s, L, items, width, o);
         else if (width <= DENSE_MAX)  // at most RANK_NARROW_CAP elements
-            launch_items(k_leaf_rank_num<RANK_XBLOCK, RANK_SWORDS, RANK_NARROW_CAP, RANK_LEPT>, RANK_XBLOCK, n, s, L,
-                         items, width, o);
+            launch_items(k_leaf_rank_num<RANK_XBLOCK, RANK_SWORDS, RANK_NARROW_CAP, RANK_LEPT, 1, CI, V>, RANK_XBLOCK,
+                         n, s, L, items, width, o);
         else if (bin == LEAF_RANK && narrow)  // wide, at most RANK_MID distinct columns
-            launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_MID, RANK_EPT>, RANK_BLOCK, n, s, L, items, width, o);
+            launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_MID, RANK_EPT, 1, CI, V>, RANK_BLOCK, n, s, L, items,
+                         width, o);
         else if (bin == LEAF_RANK)
-            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_MID, RANK_EPT, 2>, RANK_BLOCK, n, s, L, items, width, o);
+            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_MID, RANK_EPT, 2, CI, V>, RANK_BLOCK, n, s, L, items,
+                         width, o);
         else if (bin != LEAF_RANK_XL && narrow)  // at most RANK_SMALL distinct columns
-            launch_items(k_leaf_rank_num<RANK_LBLOCK, W17, RANK_SMALL, RANK_LWEPT>, RANK_LBLOCK, n, s, L, items, width,
-                         o);
+            launch_items(k_leaf_rank_num<RANK_LBLOCK, W17, RANK_SMALL, RANK_LWEPT, 1, CI, V>, RANK_LBLOCK, n, s, L,
+                         items, width, o);
         else if (bin != LEAF_RANK_XL)
-            launch_items(k_leaf_rank_num<RANK_LBLOCK, W18, RANK_SMALL, RANK_LWEPT, 2>, RANK_LBLOCK, n, s, L, items, width,
-                         o);
+            launch_items(k_leaf_rank_num<RANK_LBLOCK, W18, RANK_SMALL, RANK_LWEPT, 2, CI, V>, RANK_LBLOCK, n, s, L,
+                         items, width, o);
         else if (narrow)
-            launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_NNZ_MAX, RANK_EPT>, RANK_BLOCK, n, s, L, items, width,
-                         o);
+            launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_NNZ_MAX, RANK_EPT, 1, CI, V>, RANK_BLOCK, n, s, L, items,
+                         width, o);
         else
-            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_NNZ_MAX, RANK_EPT, 2>, RANK_BLOCK, n, s, L, items, width,
-                         o);
+            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_NNZ_MAX, RANK_EPT, 2, CI, V>, RANK_BLOCK, n, s, L, items,
+                         width, o);
         break;
     }
     default: break;
     }
+}
+
+void leaf_numeric(const LeafSet &L, int bin, const LeafTask *items, int64_t n, int64_t width64, void *c_col, bool ci64,
+                  int slot_width_log2, void *c_val, int32_t *err, int32_t *counter, hipStream_t s) {
+    const int width = (int)(width64 < ((int64_t)1 << 30) ? width64 : ((int64_t)1 << 30));
+    with_types(ci64, L.v32, [&](auto ci, auto v) {
+        using CI = decltype(ci);
+        using V = decltype(v);
+        LeafDst<CI, V> o{static_cast<CI *>(c_col), static_cast<V *>(c_val), err, slot_width_log2};
+        leaf_numeric_typed<CI, V>(L, bin, items, n, width, o, counter, s);
+    });
 }
 
 void slot_scan(int64_t *slot, int64_t n_heavy, int64_t n_slots, const int64_t *heavy_rows, int64_t *row_nnz,

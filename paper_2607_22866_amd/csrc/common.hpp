@@ -10,13 +10,69 @@
 
 namespace gm {
 
-// Read-only view of a device CSR matrix.
+// Read-only view of a device CSR matrix with its column-index and value
+// types chosen at run time (int32 / int64 columns, fp64 / fp32 values).
 struct Csr {
     int64_t n_rows, n_cols, nnz;
     const int64_t *rp;
-    const int32_t *ci;
-    const double *v;
+    const void *ci;
+    const void *v;
+    bool ci64 = false;  // column indices are int64
+    bool v32 = false;   // values are fp32
 };
+
+// The same view with its types fixed, as kernels take it.
+template <typename CI, typename V>
+struct CsrV {
+    int64_t n_rows, n_cols, nnz;
+    const int64_t *rp;
+    const CI *ci;
+    const V *v;
+};
+
+template <typename CI, typename V>
+inline CsrV<CI, V> typed(const Csr &m) {
+    return CsrV<CI, V>{m.n_rows, m.n_cols, m.nnz, m.rp, static_cast<const CI *>(m.ci), static_cast<const V *>(m.v)};
+}
+
+// Value type of views whose kernels never read values.
+using NoV = unsigned char;
+
+// Calls f(CI{}, V{}) with the column-index and value types of a view.
+template <class F>
+inline void with_types(bool ci64, bool v32, F &&f) {
+    if (ci64) {
+        if (v32)
+            f(int64_t{}, float{});
+        else
+            f(int64_t{}, double{});
+    } else {
+        if (v32)
+            f(int32_t{}, float{});
+        else
+            f(int32_t{}, double{});
+    }
+}
+template <class F>
+inline void with_types(const Csr &m, F &&f) {
+    with_types(m.ci64, m.v32, static_cast<F &&>(f));
+}
+// Calls f(CI{}) with the column-index type.
+template <class F>
+inline void with_index_type(bool ci64, F &&f) {
+    if (ci64)
+        f(int64_t{});
+    else
+        f(int32_t{});
+}
+// Calls f(V{}) with the value type.
+template <class F>
+inline void with_value_type(bool v32, F &&f) {
+    if (v32)
+        f(float{});
+    else
+        f(double{});
+}
 
 GM_DEV int lane_id() { return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0)); }
 

@@ -49,16 +49,17 @@ __global__ void k_expand_tiles(Csr B, const int64_t *col_ptr, const int64_t *sli
     }
 }
 
-__global__ __launch_bounds__(EXP_BLOCK) void k_expand(Csr B, const int64_t *col_ptr, const int64_t *slice_off,
+template <typename CI, typename V>
+__global__ __launch_bounds__(EXP_BLOCK) void k_expand(CsrV<CI, V> B, const int64_t *col_ptr, const int64_t *slice_off,
                                                       const int32_t *slice_k, const int32_t *row_h,
-                                                      const double *a_val, int64_t n_slices, int64_t total,
+                                                      const V *a_val, int64_t n_slices, int64_t total,
                                                       int64_t n_tiles, const TileInfo *info, int64_t *cursor,
-                                                      int32_t *chat_col, double *chat_val) {
+                                                      int32_t *chat_col, V *chat_val) {
     __shared__ int64_t cp[EXP_BLOCK + 1];   // col_ptr window of the current batch's slices
     __shared__ int32_t seg_lo[EXP_BLOCK + 1];  // tile-local first product of each segment
     __shared__ int64_t seg_dst[EXP_BLOCK];  // C-hat position minus tile-local index
     __shared__ int64_t seg_src[EXP_BLOCK];  // B position minus tile-local index
-    __shared__ double seg_a[EXP_BLOCK];
+    __shared__ V seg_a[EXP_BLOCK];
     __shared__ int64_t next_base;
 
     const int tid = threadIdx.x;
@@ -102,7 +103,7 @@ __global__ __launch_bounds__(EXP_BLOCK) void k_expand(Csr B, const int64_t *col_
         int q_prev = 0;
         for (int tb = t0 + tid; tb < t1; tb += EXP_BLOCK * EXP_ILP) {
             int32_t c[EXP_ILP];
-            double bv[EXP_ILP], av[EXP_ILP];
+            V bv[EXP_ILP], av[EXP_ILP];
             int64_t d[EXP_ILP];
 #pragma unroll
             for (int u = 0; u < EXP_ILP; ++u) {
@@ -111,7 +112,7 @@ __global__ __launch_bounds__(EXP_BLOCK) void k_expand(Csr B, const int64_t *col_
                     const int q = (int)find_row(seg_lo, q_prev, nb, t);
                     q_prev = q;
                     const int64_t src = seg_src[q] + t;
-                    c[u] = B.ci[src];
+                    c[u] = (int32_t)B.ci[src];  // C.m < 2^31 on this path
                     bv[u] = B.v[src];
                     av[u] = seg_a[q];
                     d[u] = seg_dst[q] + t;
@@ -147,14 +148,15 @@ __global__ __launch_bounds__(EXP_BLOCK) void k_expand(Csr B, const int64_t *col_
 constexpr int EXP_WORDS = (int)(EXP_TILE / 32);
 static_assert(EXP_WORDS == EXP_BLOCK, "one bitmap word per thread");
 
+template <typename CI, typename V>
 __global__ __launch_bounds__(EXP_BLOCK) void k_expand_split(
-    Csr B, const int64_t *col_ptr, const int64_t *slice_off, const int32_t *slice_k, const int32_t *row_h,
-    const double *a_val, int64_t n_slices, int64_t total, int64_t n_tiles, const TileInfo *info, const int32_t *bnd,
-    int nc, int shift, int64_t *cursor, int32_t *out_col, double *out_val) {
+    CsrV<CI, V> B, const int64_t *col_ptr, const int64_t *slice_off, const int32_t *slice_k, const int32_t *row_h,
+    const V *a_val, int64_t n_slices, int64_t total, int64_t n_tiles, const TileInfo *info, const int32_t *bnd,
+    int nc, int shift, int64_t *cursor, int32_t *out_col, V *out_val) {
     __shared__ int64_t cp[EXP_BLOCK + 1];
     __shared__ int64_t sg_b[EXP_BLOCK];     // B.rp[k] of the segment's slice
     __shared__ int64_t sg_hc[EXP_BLOCK];    // heavy row * nc
-    __shared__ double sg_a[EXP_BLOCK];
+    __shared__ V sg_a[EXP_BLOCK];
     __shared__ int32_t sg_s[EXP_BLOCK];     // slice
     __shared__ int32_t sg_loc[EXP_BLOCK];   // tile-local index of the segment's first product
     __shared__ int32_t sg_off[EXP_BLOCK];   // its offset in the B row
@@ -163,7 +165,7 @@ __global__ __launch_bounds__(EXP_BLOCK) void k_expand_split(
     __shared__ int32_t run_base[EXP_BLOCK + 1];
     __shared__ int64_t rn_dst[EXP_BLOCK];   // output position minus tile-local index (compacted runs)
     __shared__ int64_t rn_src[EXP_BLOCK];   // B position minus tile-local index
-    __shared__ double rn_a[EXP_BLOCK];
+    __shared__ V rn_a[EXP_BLOCK];
     __shared__ uint32_t start_bits[EXP_WORDS];
     __shared__ int32_t word_pre[EXP_WORDS];
     __shared__ int32_t scan_sm[EXP_BLOCK / GM_WAVE];
@@ -192,8 +194,8 @@ __global__ __launch_bounds__(EXP_BLOCK) void k_expand_split(
             const int64_t lo = seg_g > g0 ? seg_g : g0;
             const int64_t hi = seg_g + L < g1 ? seg_g + L : g1;
             const int32_t off0 = (int32_t)(lo - seg_g), off1 = (int32_t)(hi - seg_g);
-            const int32_t c0 = B.ci[bstart + off0] >> shift;
-            const int32_t c1 = B.ci[bstart + off1 - 1] >> shift;
+            const int32_t c0 = (int32_t)(B.ci[bstart + off0] >> shift);
+            const int32_t c1 = (int32_t)(B.ci[bstart + off1 - 1] >> shift);
             nr = c1 - c0 + 1;
             sg_b[tid] = bstart;
             sg_hc[tid] = (int64_t)row_h[e] * nc;
@@ -216,7 +218,7 @@ __global__ __launch_bounds__(EXP_BLOCK) void k_expand_split(
             start_bits[tid] = 0u;
             int32_t loc = 0, len = 0;
             int64_t dst = 0, src = 0;
-            double av = 0.0;
+            V av = 0;
             if (tid < nrb) {
                 const int gr = rb + tid;
                 const int q = (int)find_row(run_base, 0, nb, gr);
@@ -251,8 +253,8 @@ __global__ __launch_bounds__(EXP_BLOCK) void k_expand_split(
             __syncthreads();
             const int t0 = n_ne > 0 ? range[0] : 0, t1 = n_ne > 0 ? range[1] : 0;
             for (int tb = t0 + tid; tb < t1; tb += EXP_BLOCK * EXP_ILP) {
-                int32_t c[EXP_ILP];
-                double bv[EXP_ILP], a[EXP_ILP];
+                CI c[EXP_ILP];
+                V bv[EXP_ILP], a[EXP_ILP];
                 int64_t d[EXP_ILP];
 #pragma unroll
                 for (int u = 0; u < EXP_ILP; ++u) {
@@ -271,7 +273,7 @@ __global__ __launch_bounds__(EXP_BLOCK) void k_expand_split(
 #pragma unroll
                 for (int u = 0; u < EXP_ILP; ++u) {
                     if (tb + u * EXP_BLOCK < t1) {
-                        out_col[d[u]] = c[u] & mask;
+                        out_col[d[u]] = (int32_t)(c[u] & (CI)mask);
                         out_val[d[u]] = a[u] * bv[u];
                     }
                 }
@@ -300,25 +302,37 @@ void expand_tiles(const Csr &B, const SliceArrays &sl, int64_t total, int64_t *i
 }
 
 void expand(const Csr &B, const SliceArrays &sl, int64_t total, const int64_t *info_words, int64_t *chat_cursor,
-            int32_t *chat_col, double *chat_val, hipStream_t s) {
+            int32_t *chat_col, void *chat_val, hipStream_t s) {
     if (total <= 0 || sl.n_slices <= 0) return;
+    GM_REQUIRE(B.n_cols < ((int64_t)1 << 31), GMAGNUS_ERROR_UNSUPPORTED,
+               "C-hat row by row holds whole columns: B must have fewer than 2^31 columns");
     const int64_t n_tiles = (total + EXP_TILE - 1) / EXP_TILE;
-    hipLaunchKernelGGL(k_expand, dim3((unsigned)n_tiles), dim3(EXP_BLOCK), 0, s, B, sl.col_ptr, sl.slice_off,
-                       sl.slice_k, sl.row_h, sl.a_val, sl.n_slices, total, n_tiles, (const TileInfo *)info_words,
-                       chat_cursor, chat_col, chat_val);
-    GM_CHECK_LAUNCH();
+    with_types(B, [&](auto ci, auto v) {
+        using CI = decltype(ci);
+        using V = decltype(v);
+        hipLaunchKernelGGL((k_expand<CI, V>), dim3((unsigned)n_tiles), dim3(EXP_BLOCK), 0, s, typed<CI, V>(B),
+                           sl.col_ptr, sl.slice_off, sl.slice_k, sl.row_h, static_cast<const V *>(sl.a_val),
+                           sl.n_slices, total, n_tiles, (const TileInfo *)info_words, chat_cursor, chat_col,
+                           static_cast<V *>(chat_val));
+        GM_CHECK_LAUNCH();
+    });
 }
 
 void expand_split(const Csr &B, const SliceArrays &sl, int64_t total, const int64_t *info_words, const int32_t *bnd,
-                  int nc, int shift, int64_t *cursor, int32_t *out_col, double *out_val, hipStream_t s) {
+                  int nc, int shift, int64_t *cursor, int32_t *out_col, void *out_val, hipStream_t s) {
     if (total <= 0 || sl.n_slices <= 0) return;
     GM_REQUIRE(nc >= 1 && nc < GM_WAVE && shift >= 0 && shift < 31, GMAGNUS_ERROR_UNSUPPORTED,
                "fused expansion: unsupported first-level chunking");
     const int64_t n_tiles = (total + EXP_TILE - 1) / EXP_TILE;
-    hipLaunchKernelGGL(k_expand_split, dim3((unsigned)n_tiles), dim3(EXP_BLOCK), 0, s, B, sl.col_ptr, sl.slice_off,
-                       sl.slice_k, sl.row_h, sl.a_val, sl.n_slices, total, n_tiles, (const TileInfo *)info_words, bnd,
-                       nc, shift, cursor, out_col, out_val);
-    GM_CHECK_LAUNCH();
+    with_types(B, [&](auto ci, auto v) {
+        using CI = decltype(ci);
+        using V = decltype(v);
+        hipLaunchKernelGGL((k_expand_split<CI, V>), dim3((unsigned)n_tiles), dim3(EXP_BLOCK), 0, s, typed<CI, V>(B),
+                           sl.col_ptr, sl.slice_off, sl.slice_k, sl.row_h, static_cast<const V *>(sl.a_val),
+                           sl.n_slices, total, n_tiles, (const TileInfo *)info_words, bnd, nc, shift, cursor, out_col,
+                           static_cast<V *>(out_val));
+        GM_CHECK_LAUNCH();
+    });
 }
 
 }  // namespace gm

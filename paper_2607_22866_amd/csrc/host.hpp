@@ -92,7 +92,7 @@ void cache_release();
 
 // Builds a plan (gmagnus_plan); with no_alloc the plan's workspace comes only
 // from opts' callbacks and its host reads use pageable memory.
-gmagnus_status_t make_plan(gmagnus_plan_t *out, const gmagnus_csr_t *A, const gmagnus_csr_t *B,
+gmagnus_status_t make_plan(gmagnus_plan_t *out, const gmagnus_matrix_t *A, const gmagnus_matrix_t *B,
                            const gmagnus_options_t *opts, void *hip_stream, bool no_alloc);
 
 // Raises a kernel's dynamic LDS limit to `bytes` on the current device, once
@@ -124,9 +124,10 @@ void fill(T *p, T v, int64_t n, hipStream_t s) {
 
 // ----------------------------------------------------------------- setup.hip
 // Fills ip/minc/maxc for rows [r0, r1) of A (local index r - r0); with minc
-// and maxc null only ip (no reads of B's columns).
-void row_products(const Csr &A, const Csr &B, int64_t r0, int64_t r1, int64_t panel_nnz, int64_t *ip, int32_t *minc,
-                  int32_t *maxc, hipStream_t s);
+// and maxc null only ip (no reads of B's columns). minc / maxc hold B's
+// column type (int32 or int64).
+void row_products(const Csr &A, const Csr &B, int64_t r0, int64_t r1, int64_t panel_nnz, int64_t *ip, void *minc,
+                  void *maxc, hipStream_t s);
 // Checks canonical CSR; sets *flag (device int32) to nonzero on violation.
 void validate_csr(const Csr &M, int32_t *flag, hipStream_t s);
 
@@ -139,7 +140,7 @@ struct SliceArrays {
     int64_t *slice_off = nullptr; // n_slices + 1 (products)
     int32_t *slice_k = nullptr;   // n_slices: column of A / row of B
     int32_t *row_h = nullptr;     // nnz: heavy-local row index
-    double *a_val = nullptr;      // nnz
+    void *a_val = nullptr;        // nnz values of A's type
 };
 void csc_count(const Csr &A, const Csr &B, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
                const int64_t *a_heavy_ptr, int64_t nnz_heavy_all, int64_t *colcnt, hipStream_t s);
@@ -148,7 +149,7 @@ void slice_build(const Csr &B, const int64_t *colcnt, const int64_t *slice_perm,
                  int32_t *slice_k, int64_t *cnt_out, int64_t *ip_out, int32_t *k_to_slice, hipStream_t s);
 void csc_fill(const Csr &A, const Csr &B, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
               const int64_t *a_heavy_ptr, int64_t nnz_heavy_all, const int32_t *k_to_slice,
-              const int64_t *col_ptr, int64_t *fill_cursor, int32_t *row_h, double *a_val, hipStream_t s);
+              const int64_t *col_ptr, int64_t *fill_cursor, int32_t *row_h, void *a_val, hipStream_t s);
 // len[s] = nnz(B[slice_k[s], :]).
 void slice_lengths(const Csr &B, const int32_t *slice_k, int64_t n, int64_t *len, hipStream_t s);
 // Level-0 histogram from the structure: per-slice chunk boundaries in its B
@@ -169,13 +170,13 @@ void gather_i64(const int64_t *src, const int64_t *idx, int64_t n, int64_t *out,
 int64_t expand_tile_words(int64_t total);
 void expand_tiles(const Csr &B, const SliceArrays &sl, int64_t total, int64_t *info_words, hipStream_t s);
 void expand(const Csr &B, const SliceArrays &sl, int64_t total, const int64_t *info_words, int64_t *chat_cursor,
-            int32_t *chat_col, double *chat_val, hipStream_t s);
+            int32_t *chat_col, void *chat_val, hipStream_t s);
 // Expansion fused with the first level's split into nc chunks of 2^shift
 // columns: bnd are the slices' chunk boundaries (slice_chunk_bounds), cursor
 // the next free position of output row (h, c) at h * nc + c; columns are
 // written chunk-local.
 void expand_split(const Csr &B, const SliceArrays &sl, int64_t total, const int64_t *info_words, const int32_t *bnd,
-                  int nc, int shift, int64_t *cursor, int32_t *out_col, double *out_val, hipStream_t s);
+                  int nc, int shift, int64_t *cursor, int32_t *out_col, void *out_val, hipStream_t s);
 
 // ------------------------------------------------------------- rowsplit.hip
 // The heavy rows' A entries in row order: B row, its slice (-1 for an empty
@@ -184,7 +185,7 @@ struct RowEntries {
     int32_t *k = nullptr;
     int32_t *s = nullptr;
     int32_t *h = nullptr;
-    double *a = nullptr;
+    void *a = nullptr;  // A's value type
 };
 void heavy_entries(const Csr &A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0, const int64_t *a_heavy_ptr,
                    int64_t nnz_heavy_all, const int32_t *k_to_slice, const RowEntries &ent, hipStream_t s);
@@ -204,7 +205,7 @@ bool rows_next_fits(int next_nc);
 void expand_rows(const Csr &B, const RowEntries &ent, const uint32_t *pre, const int32_t *bnd, const int64_t *out_ptr,
                  const int64_t *seg_base, const int32_t *reg_c, const int64_t *reg_efirst, const int64_t *reg_ne,
                  int64_t n_out, int64_t n_heavy_out, int64_t total, int nc, int shift, int next_nc, int next_shift,
-                 int64_t *next_counts, int64_t *tile_words, int32_t *out_col, double *out_val, hipStream_t s);
+                 int64_t *next_counts, int64_t *tile_words, int32_t *out_col, void *out_val, hipStream_t s);
 
 // Two levels in one pass (the hierarchy has exactly two levels): the
 // expansion splits the products of the first level's heavy regions by the
@@ -230,7 +231,7 @@ void expand_rows2(const Csr &B, const RowEntries &ent, const uint32_t *pre, cons
                   const int64_t *out_ptr, const int64_t *seg_base, const int32_t *reg_c, const int64_t *reg_efirst,
                   const int64_t *reg_ne, int64_t n_out, int64_t n_heavy_out, int64_t total, int nc, int shift,
                   int nc1, int shift1, int64_t tau, int64_t *cursor1, int64_t n_out1_elems, int32_t *err,
-                  int64_t *tile_words, int32_t *out_col0, double *out_val0, uint16_t *out_col1, double *out_val1,
+                  int64_t *tile_words, int32_t *out_col0, void *out_val0, uint16_t *out_col1, void *out_val1,
                   hipStream_t s);
 
 // ------------------------------------------------------------ multisplit.hip
@@ -262,7 +263,7 @@ void chunk_classes(const int64_t *counts, int64_t n, int64_t tau, bool last, uin
 void chunk_reorder(const int64_t *counts, const int64_t *inv, int64_t n, int n_chunks, const int64_t *origin_in,
                    int64_t stride, int64_t cmajor_rows, int64_t *out_cnt, int64_t *origin_out, hipStream_t s);
 void multisplit(const LevelGeom &g, const int64_t *in_ptr, const int64_t *tile_row, const int32_t *in_col,
-                const double *in_val, const int64_t *x_map, int64_t *cursor, int32_t *out_col, double *out_val,
+                const void *in_val, bool v32, const int64_t *x_map, int64_t *cursor, int32_t *out_col, void *out_val,
                 int64_t n_heavy_out, int64_t *next_counts, hipStream_t s);
 
 // ------------------------------------------------------------ accumulate.hip
@@ -270,10 +271,11 @@ void multisplit(const LevelGeom &g, const int64_t *in_ptr, const int64_t *tile_r
 struct LeafSet {
     const int64_t *ptr;    // chunk row pointers of that level's output
     const int32_t *col;    // chunk-local columns (or col16)
-    const double *val;
+    const void *val;       // values: fp32 when v32, else fp64
     const int64_t *origin; // slot id h * n_slots + slot, per chunk row
     int64_t lo, hi;
     const uint16_t *col16 = nullptr;  // chunk-local columns stored in 16 bits (final chunks of at most 2^16 columns)
+    bool v32 = false;
 };
 enum LeafBin : uint8_t {
     LEAF_EMPTY = 0, LEAF_H0, LEAF_H1, LEAF_H2, LEAF_H3, LEAF_DENSE_BIG, LEAF_DENSE, LEAF_RANK, LEAF_RANK_L, LEAF_RANK_XL,
@@ -284,16 +286,19 @@ enum LightBin : uint8_t {
 };
 // Largest tau the light accumulators can hold.
 int64_t tau_limit();
-void light_classes_sym(const int64_t *ip, const int32_t *minc, const int32_t *maxc, int64_t n, int64_t tau,
+// (minc / maxc of B's column type: int64 when ci64; a row whose column span
+// does not fit 31 bits is sent to the heavy path)
+void light_classes_sym(const int64_t *ip, const void *minc, const void *maxc, bool ci64, int64_t n, int64_t tau,
                        bool window, uint8_t *cls, hipStream_t s);
-void light_classes_num(const int64_t *ip, const int64_t *row_nnz, const int32_t *minc, const int32_t *maxc,
+void light_classes_num(const int64_t *ip, const int64_t *row_nnz, const void *minc, const void *maxc, bool ci64,
                        int64_t n, int64_t tau, bool window, uint8_t *cls, hipStream_t s);
-void leaf_classes_sym(const LeafSet &L, int64_t tau, int width, uint8_t *cls, hipStream_t s);
-void leaf_classes_num(const LeafSet &L, const int64_t *leaf_nnz, int64_t tau, int width, uint8_t *cls,
+void leaf_classes_sym(const LeafSet &L, int64_t tau, int64_t width, uint8_t *cls, hipStream_t s);
+void leaf_classes_num(const LeafSet &L, const int64_t *leaf_nnz, int64_t tau, int64_t width, uint8_t *cls,
                       hipStream_t s);
 // Launch record of one leaf, built in bin-partition order: element range
 // [s, e); symbolic: t = slot id, a = leaf index; numeric: t = first C
-// position, a = nnz written, b = column base of the slot.
+// position, a = nnz written, b = the slot within the row (its first column is
+// b << slot width).
 struct LeafTask {
     int64_t s, e, t;
     int32_t a, b;
@@ -308,17 +313,19 @@ void leaf_tasks_num(const LeafSet &L, const int64_t *items, int64_t n, const int
 constexpr int64_t DENSE_BIG_LEN = 32768;
 // Leaf symbolic: leaf_nnz[leaf] and slot_cnt[slot] for the n tasks of a bin.
 // (e_end: end of the level's elements in the column array; column loads stay below it)
-void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *tasks, int64_t n, int width, int64_t e_end,
+void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *tasks, int64_t n, int64_t width, int64_t e_end,
                    int64_t *leaf_nnz, int64_t *slot_cnt, hipStream_t s);
 // Leaf numeric: writes C at each task's position.
 // counter: one device int32 the dense bin uses to hand out chunks.
-void leaf_numeric(const LeafSet &L, int bin, const LeafTask *tasks, int64_t n, int width, int32_t *c_col,
-                  double *c_val, int32_t *err, int32_t *counter, hipStream_t s);
+// (c_col of C's column type: int64 when ci64; c_val of the leaf set's value type)
+void leaf_numeric(const LeafSet &L, int bin, const LeafTask *tasks, int64_t n, int64_t width, void *c_col, bool ci64,
+                  int slot_width_log2, void *c_val, int32_t *err, int32_t *counter, hipStream_t s);
 // Light rows (local index r): symbolic count into row_nnz[r]; numeric into C.
+// (minc / maxc of B's column type; C's columns and values of A's and B's types)
 void light_symbolic(const Csr &A, const Csr &B, int64_t r0, int bin, const int64_t *items, int64_t n,
-                    const int32_t *minc, const int32_t *maxc, int64_t *row_nnz, hipStream_t s);
+                    const void *minc, const void *maxc, int64_t *row_nnz, hipStream_t s);
 void light_numeric(const Csr &A, const Csr &B, int64_t r0, int bin, const int64_t *items, int64_t n,
-                   const int32_t *minc, const int32_t *maxc, const int64_t *c_row_ptr, int32_t *c_col, double *c_val,
+                   const void *minc, const void *maxc, const int64_t *c_row_ptr, void *c_col, void *c_val,
                    int32_t *err, hipStream_t s);
 // Per heavy row h: in-place exclusive scan of slot[h*n_slots .. +n_slots),
 // row total into row_nnz[heavy_rows[h]].

@@ -135,12 +135,13 @@ __host__ __device__ inline MsLayout ms_layout(int te, int nw, int K, int next, i
     return L;
 }
 
-template <int BLOCK, int TE>
+// (the value buffer keeps 8 bytes per element for either value type)
+template <int BLOCK, int TE, typename V>
 __global__ __launch_bounds__(BLOCK) void k_multisplit(int64_t n_in, int64_t elems, const int64_t *in_ptr,
                                                       const int64_t *tile_row, int64_t n_tiles,
-                                                      const int32_t *in_col, const double *in_val, int n_chunks,
+                                                      const int32_t *in_col, const V *in_val, int n_chunks,
                                                       int cbits, int shift, int R, int rbits, const int64_t *x_map,
-                                                      int64_t *cursor, int32_t *out_col, double *out_val,
+                                                      int64_t *cursor, int32_t *out_col, V *out_val,
                                                       int64_t n_heavy_out, int next_chunks, int next_shift,
                                                       int64_t *next_counts) {
     constexpr int NW = BLOCK / GM_WAVE;
@@ -149,7 +150,7 @@ __global__ __launch_bounds__(BLOCK) void k_multisplit(int64_t n_in, int64_t elem
     const int K = R << cbits;
     const bool fuse_next = next_counts != nullptr;
     const MsLayout Lo = ms_layout(TE, NW, K, fuse_next ? next_chunks : 0, R);
-    double *val_buf = (double *)(ms_smem + Lo.val);
+    V *val_buf = (V *)(ms_smem + Lo.val);
     int64_t *key_delta = (int64_t *)(ms_smem + Lo.key_delta);  // global position - local position
     int64_t *key_out = (int64_t *)(ms_smem + Lo.key_out);      // output chunk row
     int64_t *rb = (int64_t *)(ms_smem + Lo.rb);
@@ -174,7 +175,7 @@ __global__ __launch_bounds__(BLOCK) void k_multisplit(int64_t n_in, int64_t elem
     __syncthreads();
 
     int32_t col[E];
-    double val[E];
+    V val[E];
     int key[E];
     int rank[E];
 #pragma unroll
@@ -182,7 +183,7 @@ __global__ __launch_bounds__(BLOCK) void k_multisplit(int64_t n_in, int64_t elem
         const int p = j * BLOCK + tid;
         const bool valid = p < n;
         col[j] = valid ? __builtin_nontemporal_load(&in_col[g0 + p]) : 0;
-        val[j] = valid ? __builtin_nontemporal_load(&in_val[g0 + p]) : 0.0;
+        val[j] = valid ? __builtin_nontemporal_load(&in_val[g0 + p]) : (V)0;
         key[j] = valid ? (local_row(rb, R, g0 + p) << cbits) | (col[j] >> shift) : -1;
     }
     // Ranks inside (wave, key) buckets. Rows of C-hat are made of sorted B-row
@@ -314,18 +315,18 @@ int ms_lds_bytes(int K, int next, int R) {
     return ms_layout(TE, BLOCK / GM_WAVE, K, next, R).total;
 }
 
-template <int BLOCK, int TE>
+template <int BLOCK, int TE, typename V>
 void launch_multisplit(const LevelGeom &g, const int64_t *in_ptr, const int64_t *tile_row, const int32_t *in_col,
-                       const double *in_val, const int64_t *x_map, int64_t *cursor, int32_t *out_col,
-                       double *out_val, int64_t n_heavy_out, int64_t *next_counts, int cbits, int rbits,
+                       const V *in_val, const int64_t *x_map, int64_t *cursor, int32_t *out_col,
+                       V *out_val, int64_t n_heavy_out, int64_t *next_counts, int cbits, int rbits,
                        hipStream_t s) {
     const int64_t n_tiles = (g.elems + TE - 1) / TE;
     GM_REQUIRE(n_tiles < (int64_t)1 << 31, GMAGNUS_ERROR_UNSUPPORTED, "multisplit: too many tiles");
     const int K = g.group_rows << cbits;
     const int lds = ms_lds_bytes<BLOCK, TE>(K, next_counts ? g.next_chunks : 0, g.group_rows);
     GM_REQUIRE(lds <= MS_LDS_MAX, GMAGNUS_ERROR_UNSUPPORTED, "multisplit: work-group LDS above 160 KB");
-    allow_dynamic_lds((const void *)k_multisplit<BLOCK, TE>, MS_LDS_MAX);
-    hipLaunchKernelGGL((k_multisplit<BLOCK, TE>), dim3((unsigned)n_tiles), dim3(BLOCK), lds, s, g.n_in, g.elems,
+    allow_dynamic_lds((const void *)k_multisplit<BLOCK, TE, V>, MS_LDS_MAX);
+    hipLaunchKernelGGL((k_multisplit<BLOCK, TE, V>), dim3((unsigned)n_tiles), dim3(BLOCK), lds, s, g.n_in, g.elems,
                        in_ptr, tile_row, n_tiles, in_col, in_val, g.n_chunks, cbits, g.shift, g.group_rows, rbits,
                        x_map, cursor, out_col, out_val, n_heavy_out, g.next_chunks, g.next_shift, next_counts);
     GM_CHECK_LAUNCH();
@@ -385,7 +386,7 @@ void chunk_reorder(const int64_t *counts, const int64_t *inv, int64_t n, int n_c
 }
 
 void multisplit(const LevelGeom &g, const int64_t *in_ptr, const int64_t *tile_row, const int32_t *in_col,
-                const double *in_val, const int64_t *x_map, int64_t *cursor, int32_t *out_col, double *out_val,
+                const void *in_val_v, bool v32, const int64_t *x_map, int64_t *cursor, int32_t *out_col, void *out_val_v,
                 int64_t n_heavy_out, int64_t *next_counts, hipStream_t s) {
     if (g.elems <= 0) return;
     const int cbits = ilog2(g.n_chunks);
@@ -399,25 +400,30 @@ void multisplit(const LevelGeom &g, const int64_t *in_ptr, const int64_t *tile_r
         GM_REQUIRE(multisplit_next_fits(g.group_rows << cbits, g.next_chunks), GMAGNUS_ERROR_UNSUPPORTED,
                    "multisplit: next-level histogram does not fit");
     int64_t *nc = fuse ? next_counts : nullptr;
+    with_value_type(v32, [&](auto v) {
+        using V = decltype(v);
+        const V *in_val = static_cast<const V *>(in_val_v);
+        V *out_val = static_cast<V *>(out_val_v);
     switch (g.group_elems) {
     case 1024:
-        launch_multisplit<128, 1024>(g, in_ptr, tile_row, in_col, in_val, x_map, cursor, out_col, out_val,
+        launch_multisplit<128, 1024, V>(g, in_ptr, tile_row, in_col, in_val, x_map, cursor, out_col, out_val,
                                      n_heavy_out, nc, cbits, rbits, s);
         break;
     case 4096:
-        launch_multisplit<256, 4096>(g, in_ptr, tile_row, in_col, in_val, x_map, cursor, out_col, out_val,
+        launch_multisplit<256, 4096, V>(g, in_ptr, tile_row, in_col, in_val, x_map, cursor, out_col, out_val,
                                      n_heavy_out, nc, cbits, rbits, s);
         break;
     case 2048:
-        launch_multisplit<256, 2048>(g, in_ptr, tile_row, in_col, in_val, x_map, cursor, out_col, out_val,
+        launch_multisplit<256, 2048, V>(g, in_ptr, tile_row, in_col, in_val, x_map, cursor, out_col, out_val,
                                      n_heavy_out, nc, cbits, rbits, s);
         break;
     case 512:
-        launch_multisplit<256, 512>(g, in_ptr, tile_row, in_col, in_val, x_map, cursor, out_col, out_val,
+        launch_multisplit<256, 512, V>(g, in_ptr, tile_row, in_col, in_val, x_map, cursor, out_col, out_val,
                                     n_heavy_out, nc, cbits, rbits, s);
         break;
     default: throw Error{GMAGNUS_ERROR_INVALID_VALUE, "multisplit: unsupported tile size"};
     }
+    });
 }
 
 }  // namespace gm

@@ -176,13 +176,21 @@ void Workspace::release_all() {
 
 // --------------------------------------------------------------- planner
 namespace {
-constexpr int64_t S_COL = 4, S_VAL = 8, S_ROWPTR = 8, S_HISTO = 4, ALPHA = 2, N_SUBGROUPS = 16;
+constexpr int64_t S_ROWPTR = 8, S_HISTO = 4, ALPHA = 2, N_SUBGROUPS = 16;
 constexpr int64_t MIN_LOCAL_CHUNK = 64;  // mean elements per local chunk of a multisplit group
 constexpr int MAX_DENSE_LOG2 = 13;       // 8192 fp64 values + bitmap per work group
 constexpr int MAX_CHUNKS_LOG2 = 6;       // chunks per level the multisplit kernel supports
 
-void compute_params(int64_t c_m, int64_t s_lm, const gmagnus_options_t *o, gmagnus_params_t *p) {
-    GM_REQUIRE(c_m >= 1 && c_m < ((int64_t)1 << 31), GMAGNUS_ERROR_INVALID_VALUE, "C must have 1..2^31-1 columns");
+// Largest column count of C for an index type. With int64 columns every
+// multisplit level stores chunk-local columns in 32 bits: 2^35 columns in 32
+// first-level chunks leave chunks of 2^30 columns.
+int64_t max_columns(int64_t s_col) { return s_col == 8 ? ((int64_t)1 << 35) : ((int64_t)1 << 31) - 1; }
+
+// s_col / s_val: byte sizes of the column index and value types.
+void compute_params(int64_t c_m, int64_t s_lm, int64_t S_COL, int64_t S_VAL, const gmagnus_options_t *o,
+                    gmagnus_params_t *p) {
+    GM_REQUIRE(c_m >= 1 && c_m <= max_columns(S_COL), GMAGNUS_ERROR_INVALID_VALUE,
+               S_COL == 8 ? "C must have 1..2^35 columns" : "C must have 1..2^31-1 columns");
     GM_REQUIRE(s_lm >= 1024, GMAGNUS_ERROR_INVALID_VALUE, "local memory size below 1 KB");
     std::memset(p, 0, sizeof(*p));
     // tau: alpha*tau hash slots of (column, value) fill the local memory
@@ -239,7 +247,7 @@ struct Timed;
 
 struct LeafLevel {
     LeafSet set;
-    int width = 0;
+    int64_t width = 0;
     int64_t *leaf_nnz = nullptr;
     int64_t *items_sym = nullptr, *items_num = nullptr;
     int64_t bins_sym[LEAF_NBINS + 1] = {0};
@@ -263,7 +271,8 @@ struct gmagnus_plan_s {
     int32_t *err = nullptr;  // device consistency flags
     // setup
     int64_t *ip = nullptr;
-    int32_t *minc = nullptr, *maxc = nullptr;
+    void *minc = nullptr, *maxc = nullptr;  // B's column type
+    int64_t vsize = 8, csize = 4;          // bytes of a value and of a column index
     int64_t *perm = nullptr;          // rows grouped by symbolic light bin (heavy class included)
     int64_t bins_sym[LIGHT_NBINS + 1] = {0};
     int64_t *perm_num = nullptr;      // rows grouped by numeric bin
@@ -431,18 +440,50 @@ int64_t read_scalar(const int64_t *dev, hipStream_t s) {
     return v;
 }
 
-Csr to_csr(const gmagnus_csr_t *m) { return Csr{m->n_rows, m->n_cols, m->nnz, m->row_ptr, m->col_idx, m->val}; }
+gmagnus_matrix_t typed_desc(const gmagnus_csr_t *m) {
+    gmagnus_matrix_t t{};
+    if (m) t = gmagnus_matrix_t{m->n_rows, m->n_cols, m->nnz, m->row_ptr, m->col_idx, m->val, GMAGNUS_INDEX_INT32,
+                                GMAGNUS_VALUE_FP64};
+    return t;
+}
 
-void check_csr_desc(const gmagnus_csr_t *m, const char *name) {
+Csr to_csr(const gmagnus_matrix_t *m) {
+    Csr c{m->n_rows, m->n_cols, m->nnz, m->row_ptr, m->col_idx, m->val};
+    c.ci64 = m->index_type == GMAGNUS_INDEX_INT64;
+    c.v32 = m->value_type == GMAGNUS_VALUE_FP32;
+    return c;
+}
+
+// is_b: the right operand, whose column count (C's) may reach 2^35 with
+// int64 indices; every other dimension stays below 2^31.
+void check_csr_desc(const gmagnus_matrix_t *m, const char *name, bool is_b) {
     GM_REQUIRE(m != nullptr, GMAGNUS_ERROR_INVALID_VALUE, std::string(name) + " is NULL");
+    GM_REQUIRE(m->index_type == GMAGNUS_INDEX_INT32 || m->index_type == GMAGNUS_INDEX_INT64,
+               GMAGNUS_ERROR_INVALID_VALUE, std::string(name) + ": unknown index type");
+    GM_REQUIRE(m->value_type == GMAGNUS_VALUE_FP64 || m->value_type == GMAGNUS_VALUE_FP32,
+               GMAGNUS_ERROR_INVALID_VALUE, std::string(name) + ": unknown value type");
     GM_REQUIRE(m->n_rows >= 0 && m->n_cols >= 0 && m->nnz >= 0, GMAGNUS_ERROR_INVALID_VALUE,
                std::string(name) + ": negative size");
-    GM_REQUIRE(m->n_cols < ((int64_t)1 << 31) && m->n_rows < ((int64_t)1 << 31), GMAGNUS_ERROR_UNSUPPORTED,
-               std::string(name) + ": dimensions must be below 2^31");
+    const bool wide = is_b && m->index_type == GMAGNUS_INDEX_INT64;
+    GM_REQUIRE(m->n_rows < ((int64_t)1 << 31) && (wide ? m->n_cols <= max_columns(8) : m->n_cols < ((int64_t)1 << 31)),
+               GMAGNUS_ERROR_UNSUPPORTED,
+               std::string(name) + (wide ? ": rows must be below 2^31 and columns at most 2^35"
+                                         : ": dimensions must be below 2^31"));
     GM_REQUIRE(m->row_ptr != nullptr, GMAGNUS_ERROR_INVALID_VALUE, std::string(name) + ": row_ptr is NULL");
     GM_REQUIRE(m->nnz == 0 || (m->col_idx && m->val), GMAGNUS_ERROR_INVALID_VALUE,
                std::string(name) + ": col_idx/val is NULL");
 }
+
+void check_pair(const gmagnus_matrix_t *A, const gmagnus_matrix_t *B) {
+    check_csr_desc(A, "A", false);
+    check_csr_desc(B, "B", true);
+    GM_REQUIRE(A->n_cols == B->n_rows, GMAGNUS_ERROR_INVALID_VALUE, "A.n_cols must equal B.n_rows");
+    GM_REQUIRE(A->index_type == B->index_type && A->value_type == B->value_type, GMAGNUS_ERROR_INVALID_VALUE,
+               "A and B must have the same index and value types");
+}
+
+int64_t index_bytes(int32_t t) { return t == GMAGNUS_INDEX_INT64 ? 8 : 4; }
+int64_t value_bytes(int32_t t) { return t == GMAGNUS_VALUE_FP32 ? 4 : 8; }
 
 int64_t lds_bytes_of(const gmagnus_options_t &o) {
     if (o.lds_bytes > 0) return o.lds_bytes;
@@ -533,11 +574,9 @@ void copy_i64(int64_t *dst, const int64_t *src, int64_t n, hipStream_t s) {
 }
 
 // ----------------------------------------------------------- plan phases
-void do_plan(gmagnus_plan_s *p, const gmagnus_csr_t *A, const gmagnus_csr_t *B, const gmagnus_options_t *opts,
+void do_plan(gmagnus_plan_s *p, const gmagnus_matrix_t *A, const gmagnus_matrix_t *B, const gmagnus_options_t *opts,
              hipStream_t stream) {
-    check_csr_desc(A, "A");
-    check_csr_desc(B, "B");
-    GM_REQUIRE(A->n_cols == B->n_rows, GMAGNUS_ERROR_INVALID_VALUE, "A.n_cols must equal B.n_rows");
+    check_pair(A, B);
     if (opts) {
         GM_REQUIRE(opts->struct_size == sizeof(gmagnus_options_t), GMAGNUS_ERROR_INVALID_VALUE,
                    "options.struct_size mismatch");
@@ -563,7 +602,11 @@ void do_plan(gmagnus_plan_s *p, const gmagnus_csr_t *A, const gmagnus_csr_t *B, 
         GM_HIP(hipStreamCreateWithFlags(&p->s_light, hipStreamNonBlocking));
         p->own_streams = true;
     }
-    compute_params(std::max<int64_t>(B->n_cols, 1), lds_bytes_of(o), &o, &p->params);
+    p->csize = index_bytes(A->index_type);
+    p->vsize = value_bytes(A->value_type);
+    p->info.index_type = A->index_type;
+    p->info.value_type = A->value_type;
+    compute_params(std::max<int64_t>(B->n_cols, 1), lds_bytes_of(o), p->csize, p->vsize, &o, &p->params);
     p->ws.reset(new Workspace(&o, stream));
     Workspace &ws = *p->ws;
     p->err = ws.alloc<int32_t>(1);
@@ -595,12 +638,12 @@ void do_plan(gmagnus_plan_s *p, const gmagnus_csr_t *A, const gmagnus_csr_t *B, 
 
     Timed t(p, GMAGNUS_K_SETUP, stream);
     p->ip = ws.alloc<int64_t>(n);
-    p->minc = ws.alloc<int32_t>(n);
-    p->maxc = ws.alloc<int32_t>(n);
+    p->minc = ws.alloc_bytes(p->csize * n);
+    p->maxc = ws.alloc_bytes(p->csize * n);
     row_products(p->A, p->B, p->r0, p->r1, panel_nnz, p->ip, p->minc, p->maxc, stream);
     const bool window = (o.flags & GMAGNUS_FLAG_NO_WINDOW) == 0;
     uint8_t *cls = ws.alloc<uint8_t>(n);
-    light_classes_sym(p->ip, p->minc, p->maxc, n, p->params.tau, window, cls, stream);
+    light_classes_sym(p->ip, p->minc, p->maxc, p->B.ci64, n, p->params.tau, window, cls, stream);
     p->perm = ws.alloc<int64_t>(n);
     int64_t *bins = ws.alloc<int64_t>(LIGHT_NBINS + 1);
     int64_t *scratch = ws.alloc<int64_t>(std::max(partition_scratch_elems(n, LIGHT_NBINS), scan_scratch_elems(n)));
@@ -634,8 +677,8 @@ void add_bytes(gmagnus_plan_s *p, int cls, double bytes) { p->info.kernel_bytes[
 
 namespace gm {
 // Which expansion the heavy rows take (gmagnus_expansion_path). Without a
-// multisplit level, or when the paper's order is asked for, C-hat is written
-// row by row (Algorithm 4); otherwise the first level is split during the
+// multisplit level, with 64 or more first-level chunks, or when the paper's
+// order is asked for, C-hat is written row by row (Algorithm 4); otherwise the first level is split during the
 // expansion: in chunk-major row order when the offsets inside a (chunk, row)
 // region fit 32 bits, else in slice order. A hierarchy of exactly two levels
 // runs both levels inside the row-order expansion when its keys fit the work
@@ -644,7 +687,9 @@ int32_t expansion_path(const gmagnus_params_t &P, int64_t n_heavy, int64_t produ
                        int32_t flags) {
     if (n_heavy <= 0) return GMAGNUS_PATH_NONE;
     const bool paper_hist = (flags & GMAGNUS_FLAG_PAPER_HISTOGRAM) != 0;
-    const bool fused = P.n_levels > 0 && !paper_hist && (flags & GMAGNUS_FLAG_PAPER_EXPANSION) == 0;
+    // the fused first-level split handles up to 63 chunks (one lane per chunk boundary)
+    const bool fused = P.n_levels > 0 && P.v_chunks[0] < GM_WAVE && !paper_hist &&
+                       (flags & GMAGNUS_FLAG_PAPER_EXPANSION) == 0;
     if (!fused) return GMAGNUS_PATH_PAPER;
     const bool rows_order = (flags & GMAGNUS_FLAG_SLICE_SPLIT) == 0 && products_heavy < ((int64_t)1 << 32) &&
                             n_heavy < ((int64_t)1 << 31);
@@ -688,6 +733,11 @@ void heavy_symbolic(gmagnus_plan_s *p) {
     const bool paper_hist = (p->opts.flags & GMAGNUS_FLAG_PAPER_HISTOGRAM) != 0;
     const int32_t path = expansion_path(P, nh, H, p->B.nnz, p->opts.flags);
     p->info.expansion_path = path;
+    GM_REQUIRE(path != GMAGNUS_PATH_PAPER || p->B.n_cols < ((int64_t)1 << 31), GMAGNUS_ERROR_UNSUPPORTED,
+               "C-hat row by row holds whole columns: with 2^31 or more columns of C the first level must be split "
+               "during the expansion (no paper-order flags, at most 63 first-level chunks)");
+    const int64_t VS = p->vsize;   // bytes of a value
+    const double CS = (double)p->csize;  // bytes of a column index of A, B and C (internal columns take 4 or 2)
     // split at the first level while expanding, unless the paper's order is asked for
     const bool fused = path != GMAGNUS_PATH_PAPER;
     // the fused split in chunk-major row order (32-bit offsets inside a row's chunk), else in slice order
@@ -755,7 +805,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         if (!rows_order) {
             cursor = ws.alloc<int64_t>(std::max<int64_t>(sl.n_slices, 1));
             sl.row_h = ws.alloc<int32_t>(sl.nnz);
-            sl.a_val = ws.alloc<double>(sl.nnz);
+            sl.a_val = ws.alloc_bytes(VS * sl.nnz);
             values_step([=](const Csr &A, const Csr &B, hipStream_t st) {
                 fill<int64_t>(cursor, 0, sl.n_slices, st);
                 csc_fill(A, B, heavy_rows, nh, r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, sl.col_ptr, cursor,
@@ -765,7 +815,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
             ent.k = ws.alloc<int32_t>(nnz_heavy_all);
             ent.s = ws.alloc<int32_t>(nnz_heavy_all);
             ent.h = ws.alloc<int32_t>(nnz_heavy_all);
-            ent.a = ws.alloc<double>(nnz_heavy_all);
+            ent.a = ws.alloc_bytes(VS * nnz_heavy_all);
             values_step([=](const Csr &A, const Csr &, hipStream_t st) {
                 heavy_entries(A, heavy_rows, nh, r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, ent, st);
             });
@@ -798,7 +848,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                 sbnd = nullptr;
             }
             p->info.kernel_launches[GMAGNUS_K_HISTOGRAM] += 1;
-            add_bytes(p, GMAGNUS_K_HISTOGRAM, 12.0 * nnz_heavy_all + 4.0 * sl.n_slices * (nc0 + 1) + 8.0 * nh * nc0);
+            add_bytes(p, GMAGNUS_K_HISTOGRAM, (CS + 8.0) * nnz_heavy_all + 4.0 * sl.n_slices * (nc0 + 1) + 8.0 * nh * nc0);
         }
         ws.free(cursor);
         ws.free(colcnt);
@@ -815,7 +865,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         else
             ws.free(a_heavy_ptr);
         ws.free(scratch);
-        add_bytes(p, GMAGNUS_K_CSC, 12.0 * nnz_heavy_all + 12.0 * sl.nnz + 8.0 * (p->A.n_cols + sl.n_slices));
+        add_bytes(p, GMAGNUS_K_CSC, (CS + VS) * nnz_heavy_all + (4.0 + VS) * sl.nnz + 8.0 * (p->A.n_cols + sl.n_slices));
     }
     p->info.n_slices = sl.n_slices;
     p->info.nnz_a_heavy = sl.nnz;
@@ -823,7 +873,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
     // ---- outer-product expansion into buffer 0 (C-hat row by row, or
     // already split into the first level's chunks when fused)
     int32_t *col_buf[2] = {ws.alloc<int32_t>(H), nullptr};
-    double *val_buf[2] = {ws.alloc<double>(H), nullptr};
+    void *val_buf[2] = {ws.alloc_bytes(VS * H), nullptr};
     int64_t *exp_tiles =
         ws.alloc<int64_t>(std::max<int64_t>(rows_order ? rows_tile_words(H) : expand_tile_words(H), 1));
     if (!rows_order) {
@@ -852,7 +902,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
             Timed t(p, GMAGNUS_K_EXPAND, s);
             const int64_t *chat_ptr = p->chat_ptr;
             int32_t *oc = col_buf[0];
-            double *ov = val_buf[0];
+            void *ov = val_buf[0];
             values_step([=](const Csr &, const Csr &B, hipStream_t st) {
                 copy_i64(cursor, chat_ptr, nh, st);
                 expand(B, sl, H, exp_tiles, cursor, oc, ov, st);
@@ -860,7 +910,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         }
         ws.free(cursor);
         p->info.kernel_launches[GMAGNUS_K_EXPAND] += 1;
-        add_bytes(p, GMAGNUS_K_EXPAND, 12.0 * H + 12.0 * sl.nnz + 12.0 * blen_total + 8.0 * nh);
+        add_bytes(p, GMAGNUS_K_EXPAND, (4.0 + VS) * H + (4.0 + VS) * sl.nnz + (CS + VS) * blen_total + 8.0 * nh);
         free_slices();
     }
 
@@ -877,7 +927,8 @@ void heavy_symbolic(gmagnus_plan_s *p) {
     if (P.n_levels == 0) {
         LeafLevel lv;
         lv.set = LeafSet{p->chat_ptr, col_buf[0], val_buf[0], origin_in, 0, nh};
-        lv.width = 1 << c_bits;
+        lv.set.v32 = p->B.v32;
+        lv.width = (int64_t)1 << c_bits;
         lv.elems = H;
         p->leaves.push_back(lv);
     }
@@ -947,7 +998,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         const int nxt = split_in_expand ? 0 : 1 - cur;
         if (!col_buf[nxt]) {
             col_buf[nxt] = ws.alloc<int32_t>(H);
-            val_buf[nxt] = ws.alloc<double>(H);
+            val_buf[nxt] = ws.alloc_bytes(VS * H);
         }
         if (split_in_expand && rows_order) {
             // chunk-major regions: chunk, first entry and entry count of each, segment bases
@@ -979,7 +1030,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                     p->info.kernel_launches[GMAGNUS_K_HISTOGRAM] += 1;
                     // B rows of the slices; fine boundaries written and read once per
                     // entry; per-row fine counts; the heavy regions' counts
-                    add_bytes(p, GMAGNUS_K_HISTOGRAM, 4.0 * blen_total + 4.0 * (nf + 1) * sl.n_slices +
+                    add_bytes(p, GMAGNUS_K_HISTOGRAM, CS * blen_total + 4.0 * (nf + 1) * sl.n_slices +
                                                           (8.0 + 4.0 * (nf + 1)) * nnz_heavy_all + 8.0 * nh * nf +
                                                           16.0 * n_out1);
                 }
@@ -1002,11 +1053,11 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                 }
                 // sized like the first level's buffers, so panels reuse the same blocks
                 col_buf[1] = ws.alloc<int32_t>(H);
-                val_buf[1] = ws.alloc<double>(H);
+                val_buf[1] = ws.alloc_bytes(VS * H);
                 {
                     Timed t(p, GMAGNUS_K_EXPAND, s);
                     int32_t *oc0 = col_buf[0], *oc1 = col_buf[1];
-                    double *ov0 = val_buf[0], *ov1 = val_buf[1];
+                    void *ov0 = val_buf[0], *ov1 = val_buf[1];
                     const int shift0 = g.shift;
                     const int64_t tau = P.tau;
                     int32_t *err = p->err;
@@ -1020,14 +1071,15 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                 }
                 p->info.kernel_launches[GMAGNUS_K_EXPAND] += 1;
                 // products (the final chunks' columns in 16 bits), entries, offsets, B rows, row records
-                add_bytes(p, GMAGNUS_K_EXPAND, 12.0 * H - 2.0 * elems1 + 20.0 * nnz_heavy_all +
-                                                   4.0 * nnz_heavy_all * nc + 12.0 * blen_total + 24.0 * n_out +
+                add_bytes(p, GMAGNUS_K_EXPAND, (4.0 + VS) * H - 2.0 * elems1 + (12.0 + VS) * nnz_heavy_all +
+                                                   4.0 * nnz_heavy_all * nc + (CS + VS) * blen_total + 24.0 * n_out +
                                                    8.0 * n_out1);
                 p->info.level_rows_in[1] = nh_out;
                 p->info.level_elems_in[1] = elems1;
                 p->info.level_heavy_out[1] = 0;
                 two_done.set = LeafSet{out_ptr1, nullptr, val_buf[1], origin_out1, 0, n_out1, (const uint16_t *)col_buf[1]};
-                two_done.width = 1 << shift1;
+                two_done.set.v32 = p->B.v32;
+                two_done.width = (int64_t)1 << shift1;
                 two_done.elems = elems1;
                 ws.free(counts1);
                 ws.free(ccls1);
@@ -1041,7 +1093,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                 Timed t(p, GMAGNUS_K_EXPAND, s);
                 const int nn = last ? 0 : g.next_chunks, nshift = g.next_shift, shift0 = g.shift;
                 int32_t *oc = col_buf[nxt];
-                double *ov = val_buf[nxt];
+                void *ov = val_buf[nxt];
                 values_step([=](const Csr &, const Csr &B, hipStream_t st) {
                     if (next_counts) fill<int64_t>(next_counts, 0, nh_out * nn, st);
                     expand_rows(B, ent, pre, sbnd, out_ptr, seg_base, reg_c, reg_efirst, reg_ne, n_out, nh_out, H, nc,
@@ -1049,7 +1101,8 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                 });
                 p->info.kernel_launches[GMAGNUS_K_EXPAND] += 1;
                 add_bytes(p, GMAGNUS_K_EXPAND,
-                          12.0 * H + 20.0 * nnz_heavy_all + 4.0 * nnz_heavy_all * nc + 12.0 * blen_total + 24.0 * n_out);
+                          (4.0 + VS) * H + (12.0 + VS) * nnz_heavy_all + 4.0 * nnz_heavy_all * nc +
+                              (CS + VS) * blen_total + 24.0 * n_out);
             }
             ws.free(reg_c);
             ws.free(reg_efirst);
@@ -1063,7 +1116,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                 Timed t(p, GMAGNUS_K_EXPAND, s);
                 const int shift0 = g.shift;
                 int32_t *oc = col_buf[nxt];
-                double *ov = val_buf[nxt];
+                void *ov = val_buf[nxt];
                 values_step([=](const Csr &, const Csr &B, hipStream_t st) {
                     gather_i64(out_ptr, x_map, n_out, cursor, st);
                     expand_split(B, sl, H, exp_tiles, sbnd, nc, shift0, cursor, oc, ov, st);
@@ -1071,31 +1124,33 @@ void heavy_symbolic(gmagnus_plan_s *p) {
             }
             ws.free(cursor);
             p->info.kernel_launches[GMAGNUS_K_EXPAND] += 1;
-            add_bytes(p, GMAGNUS_K_EXPAND, 12.0 * H + 12.0 * sl.nnz + 12.0 * blen_total + 8.0 * n_out);
+            add_bytes(p, GMAGNUS_K_EXPAND, (4.0 + VS) * H + (4.0 + VS) * sl.nnz + (CS + VS) * blen_total + 8.0 * n_out);
             free_slices();
         } else {
             int64_t *cursor = ws.alloc<int64_t>(n_out);
             {
                 Timed t(p, GMAGNUS_K_MULTISPLIT, s);
                 const int32_t *ic = col_buf[cur];
-                const double *iv = val_buf[cur];
+                const void *iv = val_buf[cur];
                 int32_t *oc = col_buf[nxt];
-                double *ov = val_buf[nxt];
+                void *ov = val_buf[nxt];
                 const int nn = g.next_chunks;
+                const bool v32 = p->B.v32;
                 values_step([=](const Csr &, const Csr &, hipStream_t st) {
                     copy_i64(cursor, out_ptr, n_out, st);
                     if (next_counts) fill<int64_t>(next_counts, 0, nh_out * nn, st);
-                    multisplit(g, in_ptr, tile_row, ic, iv, x_map, cursor, oc, ov, nh_out, next_counts, st);
+                    multisplit(g, in_ptr, tile_row, ic, iv, v32, x_map, cursor, oc, ov, nh_out, next_counts, st);
                 });
             }
             ws.free(cursor);
             p->info.kernel_launches[GMAGNUS_K_MULTISPLIT] += 1;
-            add_bytes(p, GMAGNUS_K_MULTISPLIT, 24.0 * elems + 8.0 * (n_in + 1) + 8.0 * n_out);
+            add_bytes(p, GMAGNUS_K_MULTISPLIT, 2.0 * (4.0 + VS) * elems + 8.0 * (n_in + 1) + 8.0 * n_out);
         }
         p->info.levels_run = lvl + 1;
         LeafLevel lv;
         lv.set = LeafSet{out_ptr, col_buf[nxt], val_buf[nxt], origin_out, last ? 0 : nh_out, n_out};
-        lv.width = 1 << g.shift;
+        lv.set.v32 = p->B.v32;
+        lv.width = (int64_t)1 << g.shift;
         p->leaves.push_back(lv);
         if (two_done.set.ptr) {
             p->leaves.push_back(two_done);
@@ -1194,7 +1249,7 @@ void light_symbolic_all(gmagnus_plan_s *p) {
         if (cnt) p->info.kernel_launches[GMAGNUS_K_LIGHT_SYM] += 1;
     }
     ips = (double)(p->products_total - p->products_heavy);
-    add_bytes(p, GMAGNUS_K_LIGHT_SYM, 4.0 * ips);
+    add_bytes(p, GMAGNUS_K_LIGHT_SYM, (double)p->csize * ips);
 }
 
 void do_symbolic(gmagnus_plan_s *p, int64_t *c_row_ptr, int64_t *c_nnz) {
@@ -1258,7 +1313,7 @@ void do_symbolic(gmagnus_plan_s *p, int64_t *c_row_ptr, int64_t *c_nnz) {
         int64_t *bins = ws.alloc<int64_t>(LIGHT_NBINS + 1);
         int64_t *sc = ws.alloc<int64_t>(partition_scratch_elems(n, LIGHT_NBINS));
         p->perm_num = ws.alloc<int64_t>(n);
-        light_classes_num(p->ip, p->row_nnz, p->minc, p->maxc, n, p->params.tau, window, cls, p->stream);
+        light_classes_num(p->ip, p->row_nnz, p->minc, p->maxc, p->B.ci64, n, p->params.tau, window, cls, p->stream);
         partition_u8(cls, n, LIGHT_NBINS, p->perm_num, nullptr, bins, sc, p->stream);
         read_bins(bins, LIGHT_NBINS, p->bins_num, p->stream);
         ws.free(cls);
@@ -1270,7 +1325,7 @@ void do_symbolic(gmagnus_plan_s *p, int64_t *c_row_ptr, int64_t *c_nnz) {
     p->symbolic_done = true;
 }
 
-void do_numeric(gmagnus_plan_s *p, const int64_t *c_row_ptr, int32_t *c_col, double *c_val) {
+void do_numeric(gmagnus_plan_s *p, const int64_t *c_row_ptr, void *c_col, void *c_val) {
     GM_REQUIRE(p->symbolic_done, GMAGNUS_ERROR_NOT_READY, "numeric called before symbolic");
     GM_REQUIRE(c_row_ptr != nullptr, GMAGNUS_ERROR_INVALID_VALUE, "NULL c_row_ptr");
     GM_REQUIRE(p->c_nnz == 0 || (c_col && c_val), GMAGNUS_ERROR_INVALID_VALUE, "NULL C output arrays");
@@ -1304,12 +1359,13 @@ void do_numeric(gmagnus_plan_s *p, const int64_t *c_row_ptr, int32_t *c_col, dou
                 if (b == LEAF_DENSE_BIG) continue;  // launched together with LEAF_DENSE, first
                 const int64_t b0 = b == LEAF_DENSE ? lv.bins_num[LEAF_DENSE_BIG] : lv.bins_num[b];
                 const int64_t cnt = lv.bins_num[b + 1] - b0;
-                leaf_numeric(lv.set, b, tasks + b0, cnt, lv.width, c_col, c_val, p->err, counter, s);
+                leaf_numeric(lv.set, b, tasks + b0, cnt, lv.width, c_col, p->B.ci64, p->slot_width_log2, c_val,
+                             p->err, counter, s);
                 if (cnt) p->info.kernel_launches[GMAGNUS_K_CHUNK_NUM] += 1;
             }
             p->ws->free(tasks);
             p->ws->free(counter);
-            add_bytes(p, GMAGNUS_K_CHUNK_NUM, (lv.set.col16 ? 10.0 : 12.0) * lv.elems);
+            add_bytes(p, GMAGNUS_K_CHUNK_NUM, ((lv.set.col16 ? 2.0 : 4.0) + p->vsize) * lv.elems);
         }
     }
     {
@@ -1321,21 +1377,22 @@ void do_numeric(gmagnus_plan_s *p, const int64_t *c_row_ptr, int32_t *c_col, dou
                           c_val, p->err, s);
             if (cnt) p->info.kernel_launches[GMAGNUS_K_LIGHT_NUM] += 1;
         }
-        add_bytes(p, GMAGNUS_K_LIGHT_NUM, 12.0 * (double)(p->products_total - p->products_heavy));
+        add_bytes(p, GMAGNUS_K_LIGHT_NUM, (double)(p->csize + p->vsize) * (double)(p->products_total - p->products_heavy));
     }
     GM_HIP(hipEventRecord(jl, p->s_light));
     GM_HIP(hipEventRecord(jh, p->s_heavy));
     GM_HIP(hipStreamWaitEvent(p->stream, jl, 0));
     GM_HIP(hipStreamWaitEvent(p->stream, jh, 0));
     // output bytes of C, split by the rows they belong to
-    add_bytes(p, GMAGNUS_K_CHUNK_NUM, 12.0 * (double)p->info.c_nnz_heavy);
-    add_bytes(p, GMAGNUS_K_LIGHT_NUM, 12.0 * (double)(p->c_nnz - p->info.c_nnz_heavy));
+    const double cb = (double)(p->csize + p->vsize);  // bytes of an entry of C
+    add_bytes(p, GMAGNUS_K_CHUNK_NUM, cb * (double)p->info.c_nnz_heavy);
+    add_bytes(p, GMAGNUS_K_LIGHT_NUM, cb * (double)(p->c_nnz - p->info.c_nnz_heavy));
 }
 
 // New values on the kept patterns: the light rows read A and B directly in
 // the numeric phase; the heavy rows' recorded steps rewrite the expansion and
 // multisplit buffers that the final chunks' numeric kernels read.
-void do_update_values(gmagnus_plan_s *p, const double *a_val, const double *b_val) {
+void do_update_values(gmagnus_plan_s *p, const void *a_val, const void *b_val) {
     GM_REQUIRE((p->opts.flags & GMAGNUS_FLAG_KEEP_PATTERN) != 0, GMAGNUS_ERROR_INVALID_VALUE,
                "plan made without GMAGNUS_FLAG_KEEP_PATTERN");
     GM_REQUIRE(p->symbolic_done, GMAGNUS_ERROR_NOT_READY, "values updated before symbolic");
@@ -1384,7 +1441,7 @@ gmagnus_status_t guarded(F &&f) {
 }  // namespace
 
 namespace gm {
-gmagnus_status_t make_plan(gmagnus_plan_t *out, const gmagnus_csr_t *A, const gmagnus_csr_t *B,
+gmagnus_status_t make_plan(gmagnus_plan_t *out, const gmagnus_matrix_t *A, const gmagnus_matrix_t *B,
                            const gmagnus_options_t *opts, void *hip_stream, bool no_alloc) {
     if (!out) {
         set_last_error("NULL plan output");
@@ -1419,14 +1476,23 @@ void gmagnus_options_init(gmagnus_options_t *opts) {
     opts->struct_size = sizeof(gmagnus_options_t);
 }
 
-gmagnus_status_t gmagnus_get_params(int64_t c_m, int64_t lds_bytes, const gmagnus_options_t *opts,
-                                    gmagnus_params_t *out) {
+gmagnus_status_t gmagnus_get_params_typed(int64_t c_m, int64_t lds_bytes, int32_t index_type, int32_t value_type,
+                                          const gmagnus_options_t *opts, gmagnus_params_t *out) {
     return guarded([&] {
         GM_REQUIRE(out != nullptr, GMAGNUS_ERROR_INVALID_VALUE, "NULL output");
         GM_REQUIRE(!opts || opts->struct_size == sizeof(gmagnus_options_t), GMAGNUS_ERROR_INVALID_VALUE,
                    "options.struct_size mismatch");
-        compute_params(c_m, lds_bytes, opts, out);
+        GM_REQUIRE(index_type == GMAGNUS_INDEX_INT32 || index_type == GMAGNUS_INDEX_INT64, GMAGNUS_ERROR_INVALID_VALUE,
+                   "unknown index type");
+        GM_REQUIRE(value_type == GMAGNUS_VALUE_FP64 || value_type == GMAGNUS_VALUE_FP32, GMAGNUS_ERROR_INVALID_VALUE,
+                   "unknown value type");
+        compute_params(c_m, lds_bytes, index_bytes(index_type), value_bytes(value_type), opts, out);
     });
+}
+
+gmagnus_status_t gmagnus_get_params(int64_t c_m, int64_t lds_bytes, const gmagnus_options_t *opts,
+                                    gmagnus_params_t *out) {
+    return gmagnus_get_params_typed(c_m, lds_bytes, GMAGNUS_INDEX_INT32, GMAGNUS_VALUE_FP64, opts, out);
 }
 
 int32_t gmagnus_expansion_path(const gmagnus_params_t *params, int64_t n_heavy, int64_t products_heavy,
@@ -1435,9 +1501,15 @@ int32_t gmagnus_expansion_path(const gmagnus_params_t *params, int64_t n_heavy, 
     return expansion_path(*params, n_heavy, products_heavy, b_nnz, flags);
 }
 
+gmagnus_status_t gmagnus_plan_typed(gmagnus_plan_t *out, const gmagnus_matrix_t *A, const gmagnus_matrix_t *B,
+                                    const gmagnus_options_t *opts, void *hip_stream) {
+    return gm::make_plan(out, A, B, opts, hip_stream, false);
+}
+
 gmagnus_status_t gmagnus_plan(gmagnus_plan_t *out, const gmagnus_csr_t *A, const gmagnus_csr_t *B,
                               const gmagnus_options_t *opts, void *hip_stream) {
-    return gm::make_plan(out, A, B, opts, hip_stream, false);
+    const gmagnus_matrix_t a = typed_desc(A), b = typed_desc(B);
+    return gm::make_plan(out, A ? &a : nullptr, B ? &b : nullptr, opts, hip_stream, false);
 }
 
 gmagnus_status_t gmagnus_spgemm_symbolic(gmagnus_plan_t plan, int64_t *c_row_ptr, int64_t *c_nnz) {
@@ -1451,8 +1523,8 @@ gmagnus_status_t gmagnus_spgemm_symbolic(gmagnus_plan_t plan, int64_t *c_row_ptr
     });
 }
 
-gmagnus_status_t gmagnus_spgemm_numeric(gmagnus_plan_t plan, const int64_t *c_row_ptr, int32_t *c_col_idx,
-                                        double *c_val) {
+gmagnus_status_t gmagnus_spgemm_numeric_typed(gmagnus_plan_t plan, const int64_t *c_row_ptr, void *c_col_idx,
+                                              void *c_val) {
     if (!plan) {
         set_last_error("NULL plan");
         return GMAGNUS_ERROR_INVALID_VALUE;
@@ -1463,7 +1535,16 @@ gmagnus_status_t gmagnus_spgemm_numeric(gmagnus_plan_t plan, const int64_t *c_ro
     });
 }
 
-gmagnus_status_t gmagnus_update_values(gmagnus_plan_t plan, const double *a_val, const double *b_val) {
+gmagnus_status_t gmagnus_spgemm_numeric(gmagnus_plan_t plan, const int64_t *c_row_ptr, int32_t *c_col_idx,
+                                        double *c_val) {
+    if (plan && (plan->B.ci64 || plan->B.v32)) {
+        set_last_error("the plan's matrices have int64 columns or fp32 values: use gmagnus_spgemm_numeric_typed");
+        return GMAGNUS_ERROR_INVALID_VALUE;
+    }
+    return gmagnus_spgemm_numeric_typed(plan, c_row_ptr, c_col_idx, c_val);
+}
+
+gmagnus_status_t gmagnus_update_values_typed(gmagnus_plan_t plan, const void *a_val, const void *b_val) {
     if (!plan) {
         set_last_error("NULL plan");
         return GMAGNUS_ERROR_INVALID_VALUE;
@@ -1472,6 +1553,14 @@ gmagnus_status_t gmagnus_update_values(gmagnus_plan_t plan, const double *a_val,
         TimedPlanScope tps(plan);
         do_update_values(plan, a_val, b_val);
     });
+}
+
+gmagnus_status_t gmagnus_update_values(gmagnus_plan_t plan, const double *a_val, const double *b_val) {
+    if (plan && plan->B.v32) {
+        set_last_error("the plan's values are fp32: use gmagnus_update_values_typed");
+        return GMAGNUS_ERROR_INVALID_VALUE;
+    }
+    return gmagnus_update_values_typed(plan, a_val, b_val);
 }
 
 gmagnus_status_t gmagnus_plan_info(gmagnus_plan_t plan, gmagnus_plan_info_t *out) {
@@ -1508,10 +1597,14 @@ gmagnus_status_t gmagnus_plan_info(gmagnus_plan_t plan, gmagnus_plan_info_t *out
 void gmagnus_plan_destroy(gmagnus_plan_t plan) { delete plan; }
 
 gmagnus_status_t gmagnus_row_products(const gmagnus_csr_t *A, const gmagnus_csr_t *B, int64_t *ip, void *hip_stream) {
+    const gmagnus_matrix_t a = typed_desc(A), b = typed_desc(B);
+    return gmagnus_row_products_typed(A ? &a : nullptr, B ? &b : nullptr, ip, hip_stream);
+}
+
+gmagnus_status_t gmagnus_row_products_typed(const gmagnus_matrix_t *A, const gmagnus_matrix_t *B, int64_t *ip,
+                                            void *hip_stream) {
     return guarded([&] {
-        check_csr_desc(A, "A");
-        check_csr_desc(B, "B");
-        GM_REQUIRE(A->n_cols == B->n_rows, GMAGNUS_ERROR_INVALID_VALUE, "A.n_cols must equal B.n_rows");
+        check_pair(A, B);
         GM_REQUIRE(ip != nullptr || A->n_rows == 0, GMAGNUS_ERROR_INVALID_VALUE, "NULL ip");
         if (A->n_rows == 0) return;
         hipStream_t s = (hipStream_t)hip_stream;
@@ -1522,10 +1615,16 @@ gmagnus_status_t gmagnus_row_products(const gmagnus_csr_t *A, const gmagnus_csr_
 
 gmagnus_status_t gmagnus_split_panels(const gmagnus_csr_t *A, const gmagnus_csr_t *B, int64_t max_products,
                                       int64_t *bounds, int64_t max_panels, int64_t *n_panels, void *hip_stream) {
+    const gmagnus_matrix_t a = typed_desc(A), b = typed_desc(B);
+    return gmagnus_split_panels_typed(A ? &a : nullptr, B ? &b : nullptr, max_products, bounds, max_panels, n_panels,
+                                      hip_stream);
+}
+
+gmagnus_status_t gmagnus_split_panels_typed(const gmagnus_matrix_t *A, const gmagnus_matrix_t *B,
+                                            int64_t max_products, int64_t *bounds, int64_t max_panels,
+                                            int64_t *n_panels, void *hip_stream) {
     return guarded([&] {
-        check_csr_desc(A, "A");
-        check_csr_desc(B, "B");
-        GM_REQUIRE(A->n_cols == B->n_rows, GMAGNUS_ERROR_INVALID_VALUE, "A.n_cols must equal B.n_rows");
+        check_pair(A, B);
         GM_REQUIRE(bounds && n_panels && max_panels >= 1 && max_products >= 1, GMAGNUS_ERROR_INVALID_VALUE,
                    "bad panel arguments");
         const int64_t n = A->n_rows;

@@ -36,18 +36,19 @@ constexpr int PRE_ENTRIES = 256;  // entries per wave in the offset scan
 constexpr int RS_HREG = 8;        // heavy regions per tile with LDS counters (more go to global atomics)
 constexpr int RS_NEXT_MAX = 64;   // next-level chunks
 
-__global__ void k_heavy_entries(Csr A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
+template <typename CI, typename V>
+__global__ void k_heavy_entries(CsrV<CI, V> A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
                                 const int64_t *a_heavy_ptr, int64_t total, const int32_t *k_to_slice,
                                 RowEntries ent) {
     for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total;
          e += (int64_t)gridDim.x * blockDim.x) {
         const int64_t h = find_row(a_heavy_ptr, 0, n_heavy + 1, e);
         const int64_t j = A.rp[r0 + heavy_rows[h]] + (e - a_heavy_ptr[h]);
-        const int32_t k = A.ci[j];
+        const int32_t k = (int32_t)A.ci[j];
         ent.k[e] = k;
         ent.s[e] = k_to_slice[k];
         ent.h[e] = (int32_t)h;
-        ent.a[e] = A.v[j];
+        static_cast<V *>(ent.a)[e] = A.v[j];
     }
 }
 
@@ -221,8 +222,9 @@ __global__ void k_rs_tiles(const int64_t *out_ptr, int64_t n_out, const int64_t 
     }
 }
 
+template <typename CI, typename V>
 struct RsArgs {
-    Csr B;
+    CsrV<CI, V> B;
     RowEntries ent;
     const uint32_t *pre;
     const int32_t *bnd;
@@ -239,13 +241,14 @@ struct RsArgs {
     int next_nc, next_shift;  // next level (0: none)
     int64_t *next_counts;     // n_heavy_out * next_nc
     int32_t *out_col;
-    double *out_val;
+    V *out_val;
 };
 
-__global__ __launch_bounds__(RS_BLOCK) void k_expand_rows(RsArgs a) {
+template <typename CI, typename V>
+__global__ __launch_bounds__(RS_BLOCK) void k_expand_rows(RsArgs<CI, V> a) {
     __shared__ int64_t sb[RS_BLOCK + 2];   // seg_base window of the batch's regions
     __shared__ int64_t rn_src[RS_BLOCK];   // compacted non-empty segments: B position minus tile-local index
-    __shared__ double rn_a[RS_BLOCK];
+    __shared__ V rn_a[RS_BLOCK];
     __shared__ int32_t rn_reg[RS_BLOCK];
     __shared__ uint32_t start_bits[RS_WORDS];
     __shared__ int32_t word_pre[RS_WORDS];
@@ -259,7 +262,7 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows(RsArgs a) {
     const int64_t g0 = tile * RS_TILE;
     const int64_t g1 = g0 + RS_TILE < a.total ? g0 + RS_TILE : a.total;
     const RsTile ti = a.info[tile];
-    const int32_t mask = (int32_t)((1u << a.shift) - 1u);
+    const CI mask = (CI)((1u << a.shift) - 1u);
     const bool fuse_next = a.next_counts != nullptr;
     const int64_t hreg0 = ti.r0;  // heavy-region slots are regions hreg0 .. hreg0 + RS_HREG - 1
     if (fuse_next)
@@ -277,7 +280,7 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows(RsArgs a) {
         __syncthreads();
         int32_t loc = -1, len = 0, reg = -1;
         int64_t src = 0;
-        double av = 0.0;
+        V av = 0;
         if (tid < nb) {
             const int64_t S = sfirst + tid;
             const int64_t r = rb + find_row(sb, 0, nb + 2, S);
@@ -292,7 +295,7 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows(RsArgs a) {
             if (hi > lo) {
                 const int32_t s = a.ent.s[e];
                 src = a.B.rp[a.ent.k[e]] + a.bnd[(int64_t)s * (a.nc + 1) + c] + (lo - seg_g);
-                av = a.ent.a[e];
+                av = static_cast<const V *>(a.ent.a)[e];
                 loc = (int32_t)(lo - g0);
                 len = (int32_t)(hi - lo);
                 reg = (fuse_next && r < a.n_heavy_out) ? (int32_t)(r - hreg0) : -1;
@@ -318,7 +321,7 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows(RsArgs a) {
         // uniform trip count (ballots below need the whole wave)
         for (int tb = t0; tb < t1; tb += RS_BLOCK * RS_ILP) {
             int32_t col[RS_ILP], rg[RS_ILP];
-            double bv[RS_ILP], am[RS_ILP];
+            V bv[RS_ILP], am[RS_ILP];
 #pragma unroll
             for (int u = 0; u < RS_ILP; ++u) {
                 const int t = tb + u * RS_BLOCK + tid;
@@ -329,7 +332,7 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows(RsArgs a) {
                     const uint32_t below = bit == 31 ? ~0u : (2u << bit) - 1u;
                     const int q = word_pre[w] + __popc(start_bits[w] & below) - 1;
                     const int64_t sp = rn_src[q] + t;
-                    col[u] = a.B.ci[sp] & mask;
+                    col[u] = (int32_t)(a.B.ci[sp] & mask);
                     bv[u] = a.B.v[sp];
                     am[u] = rn_a[q];
                     rg[u] = rn_reg[q];
@@ -403,8 +406,8 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows(RsArgs a) {
 // other).
 constexpr int FB_SHORT = 64;
 
-template <int PER>
-__global__ __launch_bounds__(256) void k_fine_bounds(Csr B, const int32_t *slice_k, int64_t n_slices, int nf,
+template <int PER, typename CI>
+__global__ __launch_bounds__(256) void k_fine_bounds(CsrV<CI, NoV> B, const int32_t *slice_k, int64_t n_slices, int nf,
                                                      int fshift, int32_t *bndf) {
     const int lane = threadIdx.x & (GM_WAVE - 1);
     const int64_t nwaves = (int64_t)gridDim.x * (blockDim.x / GM_WAVE);
@@ -413,7 +416,7 @@ __global__ __launch_bounds__(256) void k_fine_bounds(Csr B, const int32_t *slice
         const int64_t b0 = B.rp[k], len = B.rp[k + 1] - b0;
         if (len <= FB_SHORT) continue;
         int32_t *out = bndf + s * (nf + 1);
-        const int32_t *row = B.ci + b0;
+        const CI *row = B.ci + b0;
         // bit length of len halvings shrink every range to a point
         const int steps = 64 - __clzll((unsigned long long)len);
         for (int f0 = 0; f0 <= nf; f0 += PER * GM_WAVE) {  // PER boundaries per lane at a time
@@ -428,7 +431,7 @@ __global__ __launch_bounds__(256) void k_fine_bounds(Csr B, const int32_t *slice
                 for (int j = 0; j < PER; ++j) {
                     const int32_t mid = (lo[j] + hi[j]) >> 1;
                     const bool go = lo[j] < hi[j];
-                    const int32_t col = go ? row[mid] : 0;
+                    const CI col = go ? row[mid] : (CI)0;
                     const bool below = (int64_t)col < ((int64_t)(f0 + lane + j * GM_WAVE) << fshift);
                     if (go) {
                         if (below)
@@ -453,8 +456,9 @@ __global__ __launch_bounds__(256) void k_fine_bounds(Csr B, const int32_t *slice
 // when the row changes.
 constexpr int FC_BLOCK = 256, FC_ENTRIES = 256, FC_MAXF = 1024;
 
-__global__ __launch_bounds__(FC_BLOCK) void k_fine_counts(Csr B, RowEntries ent, int64_t n_ent, const int32_t *bndf,
-                                                          int nf, int fshift, int64_t *F) {
+template <typename CI>
+__global__ __launch_bounds__(FC_BLOCK) void k_fine_counts(CsrV<CI, NoV> B, RowEntries ent, int64_t n_ent,
+                                                          const int32_t *bndf, int nf, int fshift, int64_t *F) {
     constexpr int FPT = FC_MAXF / FC_BLOCK;
     __shared__ int32_t es[FC_ENTRIES], eh[FC_ENTRIES], el[FC_ENTRIES];
     __shared__ int64_t eb[FC_ENTRIES];
@@ -510,7 +514,7 @@ __global__ __launch_bounds__(FC_BLOCK) void k_fine_counts(Csr B, RowEntries ent,
             }
         } else if (tid < GM_WAVE) {
             // one lane per element; a run of equal chunks adds its length once
-            const int f = lane < len ? (B.ci[eb[i] + lane] >> fshift) : -1;
+            const int f = lane < len ? (int)(B.ci[eb[i] + lane] >> fshift) : -1;
             const int fp = prev_lane(f, -2);
             const uint64_t starts = ballot(f >= 0 && f != fp);
             if (f >= 0 && ((starts >> lane) & 1)) {
@@ -543,11 +547,11 @@ constexpr int RS2_NW = RS_BLOCK / GM_WAVE;
 struct Rs2Layout {
     int whist, key_start, key_delta, col, val, key, total;
 };
-__host__ __device__ inline Rs2Layout rs2_layout(int K) {
+__host__ __device__ inline Rs2Layout rs2_layout(int K, int vsize) {
     Rs2Layout L;
     int o = 0;
     L.key_delta = o;  o += 8 * K;
-    L.val = o;        o += 8 * RS2_SUB;
+    L.val = o;        o += vsize * RS2_SUB;
     L.whist = o;      o += 4 * RS2_NW * K;
     L.key_start = o;  o += 4 * (K + 1);
     L.col = o;        o += 4 * RS2_SUB;
@@ -556,8 +560,9 @@ __host__ __device__ inline Rs2Layout rs2_layout(int K) {
     return L;
 }
 
+template <typename CI, typename V>
 struct Rs2Args {
-    Csr B;
+    CsrV<CI, V> B;
     RowEntries ent;
     const uint32_t *pre;
     const int32_t *bnd;
@@ -576,15 +581,16 @@ struct Rs2Args {
     int64_t n_out1_elems;    // size of the second level's output
     int32_t *err;            // set when a key or a place falls outside its range (a bug)
     int32_t *out_col0;       // first level (light regions)
-    double *out_val0;
+    V *out_val0;
     uint16_t *out_col1;      // second level (final chunks: at most 2^16 columns)
-    double *out_val1;
+    V *out_val1;
 };
 
-__global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args a) {
+template <typename CI, typename V>
+__global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args<CI, V> a) {
     __shared__ int64_t sb[RS_BLOCK + 2];
     __shared__ int64_t rn_src[RS_BLOCK];
-    __shared__ double rn_a[RS_BLOCK];
+    __shared__ V rn_a[RS_BLOCK];
     __shared__ int32_t rn_reg[RS_BLOCK];   // region minus the tile's first region
     __shared__ uint32_t start_bits[RS_WORDS];
     __shared__ int32_t word_pre[RS_WORDS];
@@ -594,9 +600,9 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args a) {
     extern __shared__ __align__(16) unsigned char rs2_smem[];
 
     const int K = a.R * a.nc1;
-    const Rs2Layout Lo = rs2_layout(K);
+    const Rs2Layout Lo = rs2_layout(K, (int)sizeof(V));
     int64_t *key_delta = (int64_t *)(rs2_smem + Lo.key_delta);
-    double *val_buf = (double *)(rs2_smem + Lo.val);
+    V *val_buf = (V *)(rs2_smem + Lo.val);
     int32_t *whist = (int32_t *)(rs2_smem + Lo.whist);
     int32_t *key_start = (int32_t *)(rs2_smem + Lo.key_start);
     int32_t *col_buf = (int32_t *)(rs2_smem + Lo.col);
@@ -607,7 +613,7 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args a) {
     const int64_t g0 = tile * RS_TILE;
     const int64_t g1 = g0 + RS_TILE < a.total ? g0 + RS_TILE : a.total;
     const RsTile ti = a.info[tile];
-    const int32_t mask = (int32_t)((1u << a.shift) - 1u);
+    const CI mask = (CI)((1u << a.shift) - 1u);
     const int32_t mask1 = (int32_t)((1u << a.shift1) - 1u);
     const int64_t rt = ti.r0;  // keys are (region - rt) * nc1 + second-level chunk
     const uint64_t le_mask = lanemask_lt() | (uint64_t(1) << lane);
@@ -623,7 +629,7 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args a) {
         __syncthreads();
         int32_t loc = -1, len = 0, reg = 0;
         int64_t src = 0;
-        double av = 0.0;
+        V av = 0;
         if (tid < nb) {
             const int64_t S = sfirst + tid;
             const int64_t r = rb + find_row(sb, 0, nb + 2, S);
@@ -638,7 +644,7 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args a) {
             if (hi > lo) {
                 const int32_t s = a.ent.s[e];
                 src = a.B.rp[a.ent.k[e]] + a.bnd[(int64_t)s * (a.nc + 1) + c] + (lo - seg_g);
-                av = a.ent.a[e];
+                av = static_cast<const V *>(a.ent.a)[e];
                 loc = (int32_t)(lo - g0);
                 len = (int32_t)(hi - lo);
                 reg = (int32_t)(r - rt);
@@ -663,20 +669,20 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args a) {
         // barriers need the whole work group)
         for (int sbt = t0; sbt < t1; sbt += RS2_SUB) {
             int32_t col[RS2_E];
-            double val[RS2_E];
+            V val[RS2_E];
             int key[RS2_E];
 #pragma unroll
             for (int u = 0; u < RS2_E; ++u) {
                 const int t = sbt + u * RS_BLOCK + tid;
                 key[u] = -1;
                 col[u] = 0;
-                val[u] = 0.0;
+                val[u] = 0;
                 if (t < t1) {
                     const int wd = t >> 5, bit = t & 31;
                     const uint32_t below = bit == 31 ? ~0u : (2u << bit) - 1u;
                     const int q = word_pre[wd] + __popc(start_bits[wd] & below) - 1;
                     const int64_t sp = rn_src[q] + t;
-                    col[u] = a.B.ci[sp] & mask;
+                    col[u] = (int32_t)(a.B.ci[sp] & mask);
                     val[u] = rn_a[q] * a.B.v[sp];
                     const int rl = rn_reg[q];
                     if (rt + rl < a.n_heavy_out) {
@@ -781,9 +787,13 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args a) {
 void heavy_entries(const Csr &A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0, const int64_t *a_heavy_ptr,
                    int64_t nnz_heavy_all, const int32_t *k_to_slice, const RowEntries &ent, hipStream_t s) {
     if (n_heavy <= 0 || nnz_heavy_all <= 0) return;
-    hipLaunchKernelGGL(k_heavy_entries, dim3(grid_for(nnz_heavy_all, 256, 65536)), dim3(256), 0, s, A, heavy_rows,
-                       n_heavy, r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, ent);
-    GM_CHECK_LAUNCH();
+    with_types(A, [&](auto ci, auto v) {
+        using CI = decltype(ci);
+        using V = decltype(v);
+        hipLaunchKernelGGL((k_heavy_entries<CI, V>), dim3(grid_for(nnz_heavy_all, 256, 65536)), dim3(256), 0, s,
+                           typed<CI, V>(A), heavy_rows, n_heavy, r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, ent);
+        GM_CHECK_LAUNCH();
+    });
 }
 
 int64_t entry_offset_waves(int64_t n_ent) { return (n_ent + PRE_ENTRIES - 1) / PRE_ENTRIES; }
@@ -820,7 +830,7 @@ bool rows_next_fits(int next_nc) { return next_nc <= RS_NEXT_MAX; }
 void expand_rows(const Csr &B, const RowEntries &ent, const uint32_t *pre, const int32_t *bnd, const int64_t *out_ptr,
                  const int64_t *seg_base, const int32_t *reg_c, const int64_t *reg_efirst, const int64_t *reg_ne,
                  int64_t n_out, int64_t n_heavy_out, int64_t total, int nc, int shift, int next_nc, int next_shift,
-                 int64_t *next_counts, int64_t *tile_words, int32_t *out_col, double *out_val, hipStream_t s) {
+                 int64_t *next_counts, int64_t *tile_words, int32_t *out_col, void *out_val, hipStream_t s) {
     if (total <= 0) return;
     GM_REQUIRE(nc >= 1 && nc < GM_WAVE && shift >= 0 && shift < 31, GMAGNUS_ERROR_UNSUPPORTED,
                "fused expansion: unsupported first-level chunking");
@@ -832,10 +842,16 @@ void expand_rows(const Csr &B, const RowEntries &ent, const uint32_t *pre, const
     hipLaunchKernelGGL(k_rs_tiles, dim3(grid_for(n_tiles, 256, 65536)), dim3(256), 0, s, out_ptr, n_out, seg_base,
                        reg_c, reg_efirst, reg_ne, pre, nc, total, n_tiles, info);
     GM_CHECK_LAUNCH();
-    RsArgs a{B,       ent,  pre,   bnd,   out_ptr,   seg_base,   reg_c,       reg_efirst, n_out,  n_heavy_out,
-             total,   n_tiles, info, nc,  shift,     next_nc,    next_shift,  next_counts, out_col, out_val};
-    hipLaunchKernelGGL(k_expand_rows, dim3((unsigned)n_tiles), dim3(RS_BLOCK), 0, s, a);
-    GM_CHECK_LAUNCH();
+    with_types(B, [&](auto ci, auto v) {
+        using CI = decltype(ci);
+        using V = decltype(v);
+        RsArgs<CI, V> a{typed<CI, V>(B), ent,        pre,         bnd,         out_ptr, seg_base,
+                        reg_c,           reg_efirst, n_out,       n_heavy_out, total,   n_tiles,
+                        info,            nc,         shift,       next_nc,     next_shift, next_counts,
+                        out_col,         static_cast<V *>(out_val)};
+        hipLaunchKernelGGL((k_expand_rows<CI, V>), dim3((unsigned)n_tiles), dim3(RS_BLOCK), 0, s, a);
+        GM_CHECK_LAUNCH();
+    });
 }
 
 // ------------------------------------------------------------ two levels
@@ -847,9 +863,12 @@ void fine_bounds(const Csr &B, const int32_t *slice_k, int64_t n_slices, int nf,
     GM_REQUIRE(nf >= 1 && nf <= FC_MAXF && (int64_t)B.nnz < ((int64_t)1 << 31), GMAGNUS_ERROR_UNSUPPORTED,
                "fine boundaries: too many fine chunks or B too large");
     // 9 boundaries per lane cover nf = 512 (R-MAT 22's 32 x 16 chunks) in one round
-    hipLaunchKernelGGL(k_fine_bounds<9>, dim3(grid_for(n_slices, 4, 65536)), dim3(256), 0, s, B, slice_k, n_slices, nf,
-                       fshift, bndf);
-    GM_CHECK_LAUNCH();
+    with_index_type(B.ci64, [&](auto ci) {
+        using CI = decltype(ci);
+        hipLaunchKernelGGL((k_fine_bounds<9, CI>), dim3(grid_for(n_slices, 4, 65536)), dim3(256), 0, s,
+                           typed<CI, NoV>(B), slice_k, n_slices, nf, fshift, bndf);
+        GM_CHECK_LAUNCH();
+    });
 }
 
 void fine_counts(const Csr &B, const RowEntries &ent, int64_t n_ent, const int32_t *bndf, int nf, int fshift,
@@ -859,8 +878,12 @@ void fine_counts(const Csr &B, const RowEntries &ent, int64_t n_ent, const int32
     GM_REQUIRE(nf >= 1 && nf <= FC_MAXF, GMAGNUS_ERROR_UNSUPPORTED, "fine counts: too many fine chunks");
     const int64_t blocks = (n_ent + FC_ENTRIES - 1) / FC_ENTRIES;
     GM_REQUIRE(blocks < (int64_t)1 << 31, GMAGNUS_ERROR_UNSUPPORTED, "fine counts: too many entries");
-    hipLaunchKernelGGL(k_fine_counts, dim3((unsigned)blocks), dim3(FC_BLOCK), 0, s, B, ent, n_ent, bndf, nf, fshift, F);
-    GM_CHECK_LAUNCH();
+    with_index_type(B.ci64, [&](auto ci) {
+        using CI = decltype(ci);
+        hipLaunchKernelGGL(k_fine_counts<CI>, dim3((unsigned)blocks), dim3(FC_BLOCK), 0, s, typed<CI, NoV>(B), ent,
+                           n_ent, bndf, nf, fshift, F);
+        GM_CHECK_LAUNCH();
+    });
 }
 
 void level1_counts(const int64_t *perm, int64_t n_regions, int64_t n_heavy, const int64_t *F, int nf, int nc1,
@@ -885,7 +908,7 @@ void expand_rows2(const Csr &B, const RowEntries &ent, const uint32_t *pre, cons
                   const int64_t *out_ptr, const int64_t *seg_base, const int32_t *reg_c, const int64_t *reg_efirst,
                   const int64_t *reg_ne, int64_t n_out, int64_t n_heavy_out, int64_t total, int nc, int shift,
                   int nc1, int shift1, int64_t tau, int64_t *cursor1, int64_t n_out1_elems, int32_t *err,
-                  int64_t *tile_words, int32_t *out_col0, double *out_val0, uint16_t *out_col1, double *out_val1,
+                  int64_t *tile_words, int32_t *out_col0, void *out_val0, uint16_t *out_col1, void *out_val1,
                   hipStream_t s) {
     if (total <= 0) return;
     GM_REQUIRE(nc >= 1 && nc < GM_WAVE && shift >= 0 && shift < 31 && shift1 >= 0 && shift1 <= shift && shift1 <= 16,
@@ -899,13 +922,19 @@ void expand_rows2(const Csr &B, const RowEntries &ent, const uint32_t *pre, cons
     hipLaunchKernelGGL(k_rs_tiles, dim3(grid_for(n_tiles, 256, 65536)), dim3(256), 0, s, out_ptr, n_out, seg_base,
                        reg_c, reg_efirst, reg_ne, pre, nc, total, n_tiles, info);
     GM_CHECK_LAUNCH();
-    const int lds = rs2_layout(K).total;
-    allow_dynamic_lds((const void *)k_expand_rows2, rs2_layout(RS2_KMAX).total);
-    Rs2Args a{B,       ent,   pre,   bnd,  out_ptr, seg_base, reg_c,    reg_efirst, n_out,   n_heavy_out,
-              total,   n_tiles, info, nc,  shift,   nc1,      shift1,   R,          cursor1, n_out1_elems,
-              err,     out_col0, out_val0, out_col1, out_val1};
-    hipLaunchKernelGGL(k_expand_rows2, dim3((unsigned)n_tiles), dim3(RS_BLOCK), lds, s, a);
-    GM_CHECK_LAUNCH();
+    with_types(B, [&](auto ci, auto v) {
+        using CI = decltype(ci);
+        using V = decltype(v);
+        const int lds = rs2_layout(K, (int)sizeof(V)).total;
+        allow_dynamic_lds((const void *)k_expand_rows2<CI, V>, rs2_layout(RS2_KMAX, (int)sizeof(V)).total);
+        Rs2Args<CI, V> a{typed<CI, V>(B), ent,      pre,     bnd,         out_ptr,  seg_base,
+                         reg_c,           reg_efirst, n_out, n_heavy_out, total,    n_tiles,
+                         info,            nc,       shift,   nc1,         shift1,   R,
+                         cursor1,         n_out1_elems, err, out_col0,    static_cast<V *>(out_val0), out_col1,
+                         static_cast<V *>(out_val1)};
+        hipLaunchKernelGGL((k_expand_rows2<CI, V>), dim3((unsigned)n_tiles), dim3(RS_BLOCK), lds, s, a);
+        GM_CHECK_LAUNCH();
+    });
 }
 
 }  // namespace gm

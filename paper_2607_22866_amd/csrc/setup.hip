@@ -16,9 +16,10 @@ constexpr int FLAT_ITEMS = 8;  // consecutive entries per thread
 // (the row's column span, used to pick a dense window for light rows).
 // A row split across threads is merged with atomics. Without SPAN only the
 // counts are taken (one B.rp pair per entry, no reads of B's columns).
-template <bool SPAN>
-__global__ __launch_bounds__(FLAT_BLOCK) void k_row_products(Csr A, Csr B, int64_t r0, int64_t r1, int64_t *ip,
-                                                             int32_t *minc, int32_t *maxc) {
+template <bool SPAN, typename CI>
+__global__ __launch_bounds__(FLAT_BLOCK) void k_row_products(CsrV<CI, NoV> A, CsrV<CI, NoV> B, int64_t r0, int64_t r1,
+                                                             int64_t *ip, CI *minc, CI *maxc) {
+    constexpr CI CI_MAX = sizeof(CI) == 8 ? (CI)INT64_MAX : (CI)INT32_MAX;
     const int64_t e_begin = A.rp[r0], e_end = A.rp[r1];
     const int64_t e0 = e_begin + (blockIdx.x * (int64_t)FLAT_BLOCK + threadIdx.x) * FLAT_ITEMS;
     if (e0 >= e_end) return;
@@ -26,26 +27,26 @@ __global__ __launch_bounds__(FLAT_BLOCK) void k_row_products(Csr A, Csr B, int64
     int64_t row = find_row(A.rp, r0, r1 + 1, e0);
     int64_t row_end = A.rp[row + 1];
     int64_t acc = 0;
-    int32_t lo = INT32_MAX, hi = -1;
+    CI lo = CI_MAX, hi = -1;
     for (int64_t e = e0; e < e1; ++e) {
         while (e >= row_end) {  // flush and move to the next nonempty row
             if (acc) atomicAdd((unsigned long long *)&ip[row - r0], (unsigned long long)acc);
             if (SPAN && hi >= 0) {
-                atomicMin(&minc[row - r0], lo);
-                atomicMax(&maxc[row - r0], hi);
+                __hip_atomic_fetch_min(&minc[row - r0], lo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_fetch_max(&maxc[row - r0], hi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
             acc = 0;
-            lo = INT32_MAX;
+            lo = CI_MAX;
             hi = -1;
             ++row;
             row_end = A.rp[row + 1];
         }
-        const int32_t k = A.ci[e];
+        const int64_t k = (int64_t)A.ci[e];
         const int64_t b0 = B.rp[k], b1 = B.rp[k + 1];
         if (b1 > b0) {
             acc += b1 - b0;
             if (SPAN) {
-                const int32_t f = B.ci[b0], l = B.ci[b1 - 1];
+                const CI f = B.ci[b0], l = B.ci[b1 - 1];
                 lo = f < lo ? f : lo;
                 hi = l > hi ? l : hi;
             }
@@ -53,12 +54,13 @@ __global__ __launch_bounds__(FLAT_BLOCK) void k_row_products(Csr A, Csr B, int64
     }
     if (acc) atomicAdd((unsigned long long *)&ip[row - r0], (unsigned long long)acc);
     if (SPAN && hi >= 0) {
-        atomicMin(&minc[row - r0], lo);
-        atomicMax(&maxc[row - r0], hi);
+        __hip_atomic_fetch_min(&minc[row - r0], lo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_fetch_max(&maxc[row - r0], hi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 }
 
-__global__ void k_validate_rows(Csr M, int32_t *flag) {
+template <typename CI>
+__global__ void k_validate_rows(CsrV<CI, NoV> M, int32_t *flag) {
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < M.n_rows;
          i += (int64_t)gridDim.x * blockDim.x) {
         const int64_t s = M.rp[i], e = M.rp[i + 1];
@@ -68,9 +70,9 @@ __global__ void k_validate_rows(Csr M, int32_t *flag) {
             atomicOr(flag, 4);
             continue;
         }
-        int32_t prev = -1;
+        int64_t prev = -1;
         for (int64_t p = s; p < e && p < M.nnz; ++p) {
-            const int32_t c = M.ci[p];
+            const int64_t c = (int64_t)M.ci[p];
             if (c < 0 || c >= M.n_cols) atomicOr(flag, 8);
             if (c <= prev) atomicOr(flag, 16);
             prev = c;
@@ -81,8 +83,8 @@ __global__ void k_validate_rows(Csr M, int32_t *flag) {
 // Visits the nonzeros of the heavy rows of A in the flattened order given
 // by a_heavy_ptr (exclusive scan of the heavy rows' lengths); calls
 // f(h, j) with the heavy index h and the position j in A.
-template <class F>
-GM_DEV void for_heavy_entries(const Csr &A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
+template <class M, class F>
+GM_DEV void for_heavy_entries(const M &A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
                               const int64_t *a_heavy_ptr, int64_t total, F f) {
     const int64_t e0 = (blockIdx.x * (int64_t)FLAT_BLOCK + threadIdx.x) * FLAT_ITEMS;
     if (e0 >= total) return;
@@ -100,11 +102,12 @@ GM_DEV void for_heavy_entries(const Csr &A, const int64_t *heavy_rows, int64_t n
     }
 }
 
-__global__ __launch_bounds__(FLAT_BLOCK) void k_csc_count(Csr A, Csr B, const int64_t *heavy_rows, int64_t n_heavy,
-                                                          int64_t r0, const int64_t *a_heavy_ptr, int64_t total,
-                                                          int64_t *colcnt) {
+template <typename CI>
+__global__ __launch_bounds__(FLAT_BLOCK) void k_csc_count(CsrV<CI, NoV> A, Csr B, const int64_t *heavy_rows,
+                                                          int64_t n_heavy, int64_t r0, const int64_t *a_heavy_ptr,
+                                                          int64_t total, int64_t *colcnt) {
     for_heavy_entries(A, heavy_rows, n_heavy, r0, a_heavy_ptr, total, [&](int64_t, int64_t j, int64_t) {
-        const int32_t k = A.ci[j];
+        const int64_t k = (int64_t)A.ci[j];
         if (B.rp[k + 1] > B.rp[k]) atomicAdd((unsigned long long *)&colcnt[k], 1ull);
     });
 }
@@ -126,12 +129,13 @@ __global__ void k_slice_build(Csr B, const int64_t *colcnt, const int64_t *perm,
     }
 }
 
-__global__ __launch_bounds__(FLAT_BLOCK) void k_csc_fill(Csr A, const int64_t *heavy_rows, int64_t n_heavy,
+template <typename CI, typename V>
+__global__ __launch_bounds__(FLAT_BLOCK) void k_csc_fill(CsrV<CI, V> A, const int64_t *heavy_rows, int64_t n_heavy,
                                                          int64_t r0, const int64_t *a_heavy_ptr, int64_t total,
                                                          const int32_t *k_to_slice, const int64_t *col_ptr,
-                                                         int64_t *fill_cursor, int32_t *row_h, double *a_val) {
+                                                         int64_t *fill_cursor, int32_t *row_h, V *a_val) {
     for_heavy_entries(A, heavy_rows, n_heavy, r0, a_heavy_ptr, total, [&](int64_t h, int64_t j, int64_t) {
-        const int32_t s = k_to_slice[A.ci[j]];
+        const int32_t s = k_to_slice[(int64_t)A.ci[j]];
         if (s < 0) return;
         const int64_t pos =
             col_ptr[s] + (int64_t)atomicAdd((unsigned long long *)&fill_cursor[s], 1ull);
@@ -149,8 +153,9 @@ __global__ void k_slice_lengths(Csr B, const int32_t *slice_k, int64_t n, int64_
 // offset in B[k,:] of the row's first column >= c << shift (c = 0..nc). The
 // row is sorted, so lane c of a wave finds it by binary search; chunk c of
 // the row is [bnd[c], bnd[c + 1]).
-__global__ __launch_bounds__(256) void k_slice_chunk_bounds(Csr B, const int32_t *slice_k, int64_t n_slices, int nc,
-                                                            int shift, int32_t *bnd) {
+template <typename CI>
+__global__ __launch_bounds__(256) void k_slice_chunk_bounds(CsrV<CI, NoV> B, const int32_t *slice_k, int64_t n_slices,
+                                                            int nc, int shift, int32_t *bnd) {
     const int lane = threadIdx.x & (GM_WAVE - 1);
     const int64_t nwaves = (int64_t)gridDim.x * (blockDim.x / GM_WAVE);
     for (int64_t s = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / GM_WAVE; s < n_slices; s += nwaves) {
@@ -179,7 +184,8 @@ __global__ __launch_bounds__(256) void k_slice_chunk_bounds(Csr B, const int32_t
 // chunk c, and flushes at row ends.
 constexpr int SH_ENTRIES = 256;
 
-__global__ __launch_bounds__(256) void k_struct_hist(Csr A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
+template <typename CI>
+__global__ __launch_bounds__(256) void k_struct_hist(CsrV<CI, NoV> A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
                                                      const int64_t *a_heavy_ptr, int64_t total,
                                                      const int32_t *k_to_slice, const int32_t *bnd, int nc,
                                                      int64_t cmajor_rows, int64_t *counts) {
@@ -202,7 +208,7 @@ __global__ __launch_bounds__(256) void k_struct_hist(Csr A, const int64_t *heavy
                 h_end = a_heavy_ptr[h + 1];
                 a_base = A.rp[r0 + heavy_rows[h]] - a_heavy_ptr[h];
             }
-            s = k_to_slice[A.ci[a_base + e]];
+            s = k_to_slice[(int64_t)A.ci[a_base + e]];
         }
         const int cnt = (int)(e1 - eb < GM_WAVE ? e1 - eb : GM_WAVE);
         for (int q = 0; q < cnt; ++q) {
@@ -252,39 +258,50 @@ unsigned flat_grid(int64_t total) {
 
 }  // namespace
 
-void row_products(const Csr &A, const Csr &B, int64_t r0, int64_t r1, int64_t panel_nnz, int64_t *ip, int32_t *minc,
-                  int32_t *maxc, hipStream_t s) {
+void row_products(const Csr &A, const Csr &B, int64_t r0, int64_t r1, int64_t panel_nnz, int64_t *ip, void *minc,
+                  void *maxc, hipStream_t s) {
     const int64_t n = r1 - r0;
     if (n <= 0) return;
     fill<int64_t>(ip, 0, n, s);
-    if (minc) {
-        fill<int32_t>(minc, INT32_MAX, n, s);
-        fill<int32_t>(maxc, -1, n, s);
-    }
-    if (panel_nnz <= 0) return;
-    if (minc)
-        hipLaunchKernelGGL(k_row_products<true>, dim3(flat_grid(panel_nnz)), dim3(FLAT_BLOCK), 0, s, A, B, r0, r1, ip,
-                           minc, maxc);
-    else
-        hipLaunchKernelGGL(k_row_products<false>, dim3(flat_grid(panel_nnz)), dim3(FLAT_BLOCK), 0, s, A, B, r0, r1,
-                           ip, minc, maxc);
-    GM_CHECK_LAUNCH();
+    with_index_type(B.ci64, [&](auto ci) {
+        using CI = decltype(ci);
+        CI *mn = static_cast<CI *>(minc), *mx = static_cast<CI *>(maxc);
+        if (mn) {
+            fill<CI>(mn, sizeof(CI) == 8 ? (CI)INT64_MAX : (CI)INT32_MAX, n, s);
+            fill<CI>(mx, (CI)-1, n, s);
+        }
+        if (panel_nnz <= 0) return;
+        if (mn)
+            hipLaunchKernelGGL((k_row_products<true, CI>), dim3(flat_grid(panel_nnz)), dim3(FLAT_BLOCK), 0, s,
+                               typed<CI, NoV>(A), typed<CI, NoV>(B), r0, r1, ip, mn, mx);
+        else
+            hipLaunchKernelGGL((k_row_products<false, CI>), dim3(flat_grid(panel_nnz)), dim3(FLAT_BLOCK), 0, s,
+                               typed<CI, NoV>(A), typed<CI, NoV>(B), r0, r1, ip, mn, mx);
+        GM_CHECK_LAUNCH();
+    });
 }
 
 void validate_csr(const Csr &M, int32_t *flag, hipStream_t s) {
     fill<int32_t>(flag, 0, 1, s);
     if (M.n_rows <= 0) return;
-    hipLaunchKernelGGL(k_validate_rows, dim3(grid_for(M.n_rows, 256, 8192)), dim3(256), 0, s, M, flag);
-    GM_CHECK_LAUNCH();
+    with_index_type(M.ci64, [&](auto ci) {
+        using CI = decltype(ci);
+        hipLaunchKernelGGL(k_validate_rows<CI>, dim3(grid_for(M.n_rows, 256, 8192)), dim3(256), 0, s,
+                           typed<CI, NoV>(M), flag);
+        GM_CHECK_LAUNCH();
+    });
 }
 
 void csc_count(const Csr &A, const Csr &B, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
                const int64_t *a_heavy_ptr, int64_t nnz_heavy_all, int64_t *colcnt, hipStream_t s) {
     fill<int64_t>(colcnt, 0, A.n_cols, s);
     if (n_heavy <= 0 || nnz_heavy_all <= 0) return;
-    hipLaunchKernelGGL(k_csc_count, dim3(flat_grid(nnz_heavy_all)), dim3(FLAT_BLOCK), 0, s, A, B, heavy_rows, n_heavy,
-                       r0, a_heavy_ptr, nnz_heavy_all, colcnt);
-    GM_CHECK_LAUNCH();
+    with_index_type(A.ci64, [&](auto ci) {
+        using CI = decltype(ci);
+        hipLaunchKernelGGL(k_csc_count<CI>, dim3(flat_grid(nnz_heavy_all)), dim3(FLAT_BLOCK), 0, s, typed<CI, NoV>(A),
+                           B, heavy_rows, n_heavy, r0, a_heavy_ptr, nnz_heavy_all, colcnt);
+        GM_CHECK_LAUNCH();
+    });
 }
 
 void slice_flags(const Csr &B, const int64_t *colcnt, int64_t n_k, uint8_t *cls, hipStream_t s) {
@@ -304,12 +321,17 @@ void slice_build(const Csr &B, const int64_t *colcnt, const int64_t *slice_perm,
 
 void csc_fill(const Csr &A, const Csr &B, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
               const int64_t *a_heavy_ptr, int64_t nnz_heavy_all, const int32_t *k_to_slice,
-              const int64_t *col_ptr, int64_t *fill_cursor, int32_t *row_h, double *a_val, hipStream_t s) {
+              const int64_t *col_ptr, int64_t *fill_cursor, int32_t *row_h, void *a_val, hipStream_t s) {
     (void)B;
     if (n_heavy <= 0 || nnz_heavy_all <= 0) return;
-    hipLaunchKernelGGL(k_csc_fill, dim3(flat_grid(nnz_heavy_all)), dim3(FLAT_BLOCK), 0, s, A, heavy_rows, n_heavy,
-                       r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, col_ptr, fill_cursor, row_h, a_val);
-    GM_CHECK_LAUNCH();
+    with_types(A, [&](auto ci, auto v) {
+        using CI = decltype(ci);
+        using V = decltype(v);
+        hipLaunchKernelGGL((k_csc_fill<CI, V>), dim3(flat_grid(nnz_heavy_all)), dim3(FLAT_BLOCK), 0, s,
+                           typed<CI, V>(A), heavy_rows, n_heavy, r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, col_ptr,
+                           fill_cursor, row_h, static_cast<V *>(a_val));
+        GM_CHECK_LAUNCH();
+    });
 }
 
 void slice_lengths(const Csr &B, const int32_t *slice_k, int64_t n, int64_t *len, hipStream_t s) {
@@ -321,9 +343,12 @@ void slice_lengths(const Csr &B, const int32_t *slice_k, int64_t n, int64_t *len
 void slice_chunk_bounds(const Csr &B, const SliceArrays &sl, int nc, int shift, int32_t *bnd, hipStream_t s) {
     if (sl.n_slices <= 0) return;
     GM_REQUIRE(nc >= 1 && nc < GM_WAVE, GMAGNUS_ERROR_UNSUPPORTED, "level-0 chunk count must be below 64");
-    hipLaunchKernelGGL(k_slice_chunk_bounds, dim3(grid_for(sl.n_slices, 4, 65536)), dim3(256), 0, s, B, sl.slice_k,
-                       sl.n_slices, nc, shift, bnd);
-    GM_CHECK_LAUNCH();
+    with_index_type(B.ci64, [&](auto ci) {
+        using CI = decltype(ci);
+        hipLaunchKernelGGL(k_slice_chunk_bounds<CI>, dim3(grid_for(sl.n_slices, 4, 65536)), dim3(256), 0, s,
+                           typed<CI, NoV>(B), sl.slice_k, sl.n_slices, nc, shift, bnd);
+        GM_CHECK_LAUNCH();
+    });
 }
 
 void struct_hist(const Csr &A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0, const int64_t *a_heavy_ptr,
@@ -332,10 +357,13 @@ void struct_hist(const Csr &A, const int64_t *heavy_rows, int64_t n_heavy, int64
     fill<int64_t>(counts, 0, n_heavy * nc, s);
     if (n_heavy <= 0 || nnz_heavy_all <= 0) return;
     const int64_t waves = (nnz_heavy_all + SH_ENTRIES - 1) / SH_ENTRIES;
-    hipLaunchKernelGGL(k_struct_hist, dim3(grid_for(waves, 4, (int64_t)1 << 30)), dim3(256), 0, s, A, heavy_rows,
-                       n_heavy, r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, bnd, nc, cmajor ? n_heavy : (int64_t)0,
-                       counts);
-    GM_CHECK_LAUNCH();
+    with_index_type(A.ci64, [&](auto ci) {
+        using CI = decltype(ci);
+        hipLaunchKernelGGL(k_struct_hist<CI>, dim3(grid_for(waves, 4, (int64_t)1 << 30)), dim3(256), 0, s,
+                           typed<CI, NoV>(A), heavy_rows, n_heavy, r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, bnd, nc,
+                           cmajor ? n_heavy : (int64_t)0, counts);
+        GM_CHECK_LAUNCH();
+    });
 }
 
 void gather_row_len(const int64_t *row_ptr, const int64_t *rows, int64_t n, int64_t r0, int64_t *out,

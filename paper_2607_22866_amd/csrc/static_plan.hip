@@ -131,5 +131,10 @@ extern "C" gmagnus_status_t gmagnus_plan_static(gmagnus_plan_t *out, const gmagn
     o.alloc_ctx = arena;
     if (o.workspace_limit_bytes <= 0 || o.workspace_limit_bytes > (int64_t)STATIC_WORKSPACE_BYTES)
         o.workspace_limit_bytes = (int64_t)STATIC_WORKSPACE_BYTES;
-    return gm::make_plan(out, A, B, &o, hip_stream, true);
+    gmagnus_matrix_t a{}, b{};
+    if (A) a = gmagnus_matrix_t{A->n_rows, A->n_cols, A->nnz, A->row_ptr, A->col_idx, A->val, GMAGNUS_INDEX_INT32,
+                                GMAGNUS_VALUE_FP64};
+    if (B) b = gmagnus_matrix_t{B->n_rows, B->n_cols, B->nnz, B->row_ptr, B->col_idx, B->val, GMAGNUS_INDEX_INT32,
+                                GMAGNUS_VALUE_FP64};
+    return gm::make_plan(out, &a, B ? &b : nullptr, &o, hip_stream, true);
 }

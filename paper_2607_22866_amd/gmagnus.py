@@ -45,6 +45,16 @@ class CsrDesc(ctypes.Structure):
                 ("row_ptr", ctypes.c_void_p), ("col_idx", ctypes.c_void_p), ("val", ctypes.c_void_p)]
 
 
+INDEX_TYPES = {torch.int32: 0, torch.int64: 1}
+VALUE_TYPES = {torch.float64: 0, torch.float32: 1}
+
+
+class MatrixDesc(ctypes.Structure):
+    _fields_ = [("n_rows", ctypes.c_int64), ("n_cols", ctypes.c_int64), ("nnz", ctypes.c_int64),
+                ("row_ptr", ctypes.c_void_p), ("col_idx", ctypes.c_void_p), ("val", ctypes.c_void_p),
+                ("index_type", ctypes.c_int32), ("value_type", ctypes.c_int32)]
+
+
 ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p)
 FREE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p)
 
@@ -77,6 +87,7 @@ class PlanInfo(ctypes.Structure):
                 ("n_leaves_rank", ctypes.c_int64), ("c_nnz", ctypes.c_int64),
                 ("c_nnz_heavy", ctypes.c_int64), ("check_flags", ctypes.c_int32),
                 ("expansion_path", ctypes.c_int32), ("workspace_peak_bytes", ctypes.c_int64),
+                ("index_type", ctypes.c_int32), ("value_type", ctypes.c_int32),
                 ("kernel_ms", ctypes.c_double * len(K_NAMES)), ("kernel_launches", ctypes.c_int64 * len(K_NAMES)),
                 ("kernel_bytes", ctypes.c_double * len(K_NAMES))]
 
@@ -99,7 +110,9 @@ class PlanInfo(ctypes.Structure):
 EXPORTS = ["gmagnus_options_init", "gmagnus_get_params", "gmagnus_plan", "gmagnus_spgemm_symbolic",
            "gmagnus_spgemm_numeric", "gmagnus_plan_info", "gmagnus_plan_destroy", "gmagnus_row_products",
            "gmagnus_split_panels", "gmagnus_release_cache", "gmagnus_last_error", "gmagnus_status_string",
-           "gmagnus_update_values", "gmagnus_expansion_path", "gmagnus_bandwidth_probe", "gmagnus_plan_static"]
+           "gmagnus_update_values", "gmagnus_expansion_path", "gmagnus_bandwidth_probe", "gmagnus_plan_static",
+           "gmagnus_get_params_typed", "gmagnus_plan_typed", "gmagnus_spgemm_numeric_typed",
+           "gmagnus_update_values_typed", "gmagnus_row_products_typed", "gmagnus_split_panels_typed"]
 
 _lib = None
 
@@ -119,6 +132,15 @@ def load(path: str = LIB_PATH):
     lib.gmagnus_plan.argtypes = [ctypes.POINTER(P), ctypes.POINTER(CsrDesc), ctypes.POINTER(CsrDesc),
                                  ctypes.POINTER(Options), P]
     lib.gmagnus_plan_static.argtypes = lib.gmagnus_plan.argtypes
+    M = ctypes.POINTER(MatrixDesc)
+    lib.gmagnus_get_params_typed.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                             ctypes.POINTER(Options), ctypes.POINTER(Params)]
+    lib.gmagnus_plan_typed.argtypes = [ctypes.POINTER(P), M, M, ctypes.POINTER(Options), P]
+    lib.gmagnus_spgemm_numeric_typed.argtypes = [P, P, P, P]
+    lib.gmagnus_update_values_typed.argtypes = [P, P, P]
+    lib.gmagnus_row_products_typed.argtypes = [M, M, P, P]
+    lib.gmagnus_split_panels_typed.argtypes = [M, M, ctypes.c_int64, P, ctypes.c_int64, ctypes.POINTER(ctypes.c_int64),
+                                               P]
     lib.gmagnus_spgemm_symbolic.argtypes = [P, P, ctypes.POINTER(ctypes.c_int64)]
     lib.gmagnus_spgemm_numeric.argtypes = [P, P, P, P]
     lib.gmagnus_update_values.argtypes = [P, P, P]
@@ -140,7 +162,9 @@ def load(path: str = LIB_PATH):
     lib.gmagnus_status_string.argtypes = [ctypes.c_int]
     lib.gmagnus_status_string.restype = ctypes.c_char_p
     for f in ("gmagnus_get_params", "gmagnus_plan", "gmagnus_plan_static", "gmagnus_spgemm_symbolic", "gmagnus_spgemm_numeric",
-              "gmagnus_update_values", "gmagnus_plan_info", "gmagnus_row_products", "gmagnus_split_panels"):
+              "gmagnus_update_values", "gmagnus_plan_info", "gmagnus_row_products", "gmagnus_split_panels",
+              "gmagnus_get_params_typed", "gmagnus_plan_typed", "gmagnus_spgemm_numeric_typed",
+              "gmagnus_update_values_typed", "gmagnus_row_products_typed", "gmagnus_split_panels_typed"):
         getattr(lib, f).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -163,11 +187,14 @@ def make_options(**kw) -> Options:
     return o
 
 
-def get_params(c_m: int, lds_bytes: int = 163840, **overrides) -> Params:
-    """Host-only parameter selection of the library (no GPU needed)."""
+def get_params(c_m: int, lds_bytes: int = 163840, index_dtype=torch.int32, value_dtype=torch.float64,
+               **overrides) -> Params:
+    """Host-only parameter selection of the library (no GPU needed) for the
+    given column-index and value types."""
     p = Params()
     o = make_options(**overrides)
-    _check(load().gmagnus_get_params(c_m, lds_bytes, ctypes.byref(o), ctypes.byref(p)))
+    _check(load().gmagnus_get_params_typed(c_m, lds_bytes, INDEX_TYPES[index_dtype], VALUE_TYPES[value_dtype],
+                                           ctypes.byref(o), ctypes.byref(p)))
     return p
 
 
@@ -188,7 +215,8 @@ def _require_device(t: torch.Tensor, device: torch.device, name: str):
 
 @dataclass
 class DeviceCSR:
-    """CSR on the GPU: int64 row_ptr, int32 col, float64 val (torch tensors)."""
+    """CSR on the GPU (torch tensors): int64 row_ptr, int32 or int64 col,
+    float64 or float32 val."""
 
     n_rows: int
     n_cols: int
@@ -201,19 +229,43 @@ class DeviceCSR:
         return int(self.col.numel())
 
     @staticmethod
-    def from_host(m, device="cuda") -> "DeviceCSR":
-        """Copies a host CSR (numpy or torch arrays) to the device."""
+    def from_host(m, device="cuda", index_dtype=torch.int32, value_dtype=torch.float64) -> "DeviceCSR":
+        """Copies a host CSR (numpy or torch arrays) to the device, converting
+        its columns and values to the given types."""
         rp = torch.as_tensor(m.row_ptr, dtype=torch.int64).to(device)
-        col = torch.as_tensor(m.col, dtype=torch.int32).to(device)
-        val = torch.as_tensor(m.val, dtype=torch.float64).to(device)
+        col = torch.as_tensor(m.col).to(index_dtype).to(device)
+        val = torch.as_tensor(m.val).to(value_dtype).to(device)
         return DeviceCSR(int(m.n_rows), int(m.n_cols), rp, col, val)
 
+    @property
+    def index_dtype(self):
+        return self.col.dtype
+
+    @property
+    def value_dtype(self):
+        return self.val.dtype
+
+    def _check_arrays(self):
+        if (not all(t.is_cuda and t.is_contiguous() for t in (self.row_ptr, self.col, self.val))
+                or self.row_ptr.dtype != torch.int64 or self.col.dtype not in INDEX_TYPES
+                or self.val.dtype not in VALUE_TYPES):
+            raise ValueError("DeviceCSR arrays must be contiguous CUDA tensors: int64 row_ptr, int32/int64 col, "
+                             "float64/float32 val")
+
     def desc(self) -> CsrDesc:
-        for t, dt in ((self.row_ptr, torch.int64), (self.col, torch.int32), (self.val, torch.float64)):
-            if not t.is_cuda or t.dtype != dt or not t.is_contiguous():
-                raise ValueError("DeviceCSR arrays must be contiguous CUDA tensors of int64/int32/float64")
+        """The int32 / fp64 descriptor of gmagnus_csr_t."""
+        self._check_arrays()
+        if self.col.dtype != torch.int32 or self.val.dtype != torch.float64:
+            raise ValueError("gmagnus_csr_t takes int32 columns and float64 values")
         return CsrDesc(self.n_rows, self.n_cols, self.nnz, self.row_ptr.data_ptr(),
                        self.col.data_ptr() if self.nnz else None, self.val.data_ptr() if self.nnz else None)
+
+    def mdesc(self) -> MatrixDesc:
+        """The typed descriptor of gmagnus_matrix_t."""
+        self._check_arrays()
+        return MatrixDesc(self.n_rows, self.n_cols, self.nnz, self.row_ptr.data_ptr(),
+                          self.col.data_ptr() if self.nnz else None, self.val.data_ptr() if self.nnz else None,
+                          INDEX_TYPES[self.col.dtype], VALUE_TYPES[self.val.dtype])
 
     def to_host(self):
         return self.row_ptr.cpu().numpy(), self.col.cpu().numpy(), self.val.cpu().numpy()
@@ -232,11 +284,15 @@ class Plan:
     def __init__(self, A: DeviceCSR, B: DeviceCSR, stream=None, static_workspace: bool = False, **options):
         self._lib = load()
         self.A, self.B = A, B  # borrowed by the library until close()
-        self._da, self._db = A.desc(), B.desc()
         self._opts = make_options(**options)
         self._stream = stream
         self._h = ctypes.c_void_p()
-        make = self._lib.gmagnus_plan_static if static_workspace else self._lib.gmagnus_plan
+        if static_workspace:
+            self._da, self._db = A.desc(), B.desc()
+            make = self._lib.gmagnus_plan_static
+        else:
+            self._da, self._db = A.mdesc(), B.mdesc()
+            make = self._lib.gmagnus_plan_typed
         _check(make(ctypes.byref(self._h), ctypes.byref(self._da), ctypes.byref(self._db), ctypes.byref(self._opts),
                     _stream(stream)))
         rb = self._opts.row_begin
@@ -257,16 +313,16 @@ class Plan:
         """Fills (and returns) C's column and value arrays for the panel."""
         dev = self.A.row_ptr.device
         if col is None:
-            col = torch.empty(self.nnz, dtype=torch.int32, device=dev)
+            col = torch.empty(self.nnz, dtype=self.A.col.dtype, device=dev)
         if val is None:
-            val = torch.empty(self.nnz, dtype=torch.float64, device=dev)
-        for t, dt, name in ((col, torch.int32, "col"), (val, torch.float64, "val")):
+            val = torch.empty(self.nnz, dtype=self.A.val.dtype, device=dev)
+        for t, dt, name in ((col, self.A.col.dtype, "col"), (val, self.A.val.dtype, "val")):
             _require_device(t, dev, name)
             if t.dtype != dt or not t.is_contiguous():
                 raise ValueError("%s must be a contiguous %s array" % (name, dt))
         if col.numel() < self.nnz or val.numel() < self.nnz:
             raise ValueError("output arrays smaller than nnz")
-        _check(self._lib.gmagnus_spgemm_numeric(self._h, self.row_ptr.data_ptr(),
+        _check(self._lib.gmagnus_spgemm_numeric_typed(self._h, self.row_ptr.data_ptr(),
                                                 col.data_ptr() if self.nnz else None,
                                                 val.data_ptr() if self.nnz else None))
         return col, val
@@ -282,10 +338,10 @@ class Plan:
             b_val = a_val
         for t, m, name in ((a_val, self.A, "a_val"), (b_val, self.B, "b_val")):
             _require_device(t, self.A.row_ptr.device, name)
-            if t.dtype != torch.float64 or not t.is_contiguous() or t.numel() < m.nnz:
-                raise ValueError("%s must be a contiguous float64 array of at least nnz entries" % name)
+            if t.dtype != m.val.dtype or not t.is_contiguous() or t.numel() < m.nnz:
+                raise ValueError("%s must be a contiguous %s array of at least nnz entries" % (name, m.val.dtype))
         self._vals = (a_val, b_val)  # borrowed by the library until the next numeric phase ends
-        _check(self._lib.gmagnus_update_values(self._h, a_val.data_ptr() if self.A.nnz else None,
+        _check(self._lib.gmagnus_update_values_typed(self._h, a_val.data_ptr() if self.A.nnz else None,
                                                b_val.data_ptr() if self.B.nnz else None))
 
     def info(self) -> PlanInfo:
@@ -321,8 +377,8 @@ def spgemm(A: DeviceCSR, B: DeviceCSR, stream=None, **options):
 
 def row_products(A: DeviceCSR, B: DeviceCSR, stream=None) -> torch.Tensor:
     ip = torch.empty(A.n_rows, dtype=torch.int64, device=A.row_ptr.device)
-    da, db = A.desc(), B.desc()
-    _check(load().gmagnus_row_products(ctypes.byref(da), ctypes.byref(db), ip.data_ptr() if A.n_rows else None,
+    da, db = A.mdesc(), B.mdesc()
+    _check(load().gmagnus_row_products_typed(ctypes.byref(da), ctypes.byref(db), ip.data_ptr() if A.n_rows else None,
                                        _stream(stream)))
     return ip
 
@@ -330,8 +386,8 @@ def row_products(A: DeviceCSR, B: DeviceCSR, stream=None) -> torch.Tensor:
 def split_panels(A: DeviceCSR, B: DeviceCSR, max_products: int, max_panels: int = 1 << 16, stream=None):
     bounds = (ctypes.c_int64 * (max_panels + 1))()
     n = ctypes.c_int64()
-    da, db = A.desc(), B.desc()
-    _check(load().gmagnus_split_panels(ctypes.byref(da), ctypes.byref(db), max_products, bounds, max_panels,
+    da, db = A.mdesc(), B.mdesc()
+    _check(load().gmagnus_split_panels_typed(ctypes.byref(da), ctypes.byref(db), max_products, bounds, max_panels,
                                        ctypes.byref(n), _stream(stream)))
     return [int(bounds[i]) for i in range(n.value + 1)]
 

@@ -177,7 +177,8 @@ def test_binding_refuses_host_tensors(lib):
     p = gm.Plan.__new__(gm.Plan)
     p._lib = None  # any library call would raise AttributeError, not ValueError
     p._h = ctypes.c_void_p()
-    m = types.SimpleNamespace(row_ptr=torch.zeros(3, dtype=torch.int64), nnz=2)
+    m = types.SimpleNamespace(row_ptr=torch.zeros(3, dtype=torch.int64), col=torch.zeros(2, dtype=torch.int32),
+                              val=torch.zeros(2, dtype=torch.float64), nnz=2)
     p.A = p.B = m
     p.nnz = 2
     p.row_ptr = torch.zeros(3, dtype=torch.int64)
@@ -195,3 +196,63 @@ def test_probe_argument_validation(lib):
     assert lib.gmagnus_bandwidth_probe(4, 0x1000, None, 1 << 20, 0, 1, None, ctypes.byref(ms)) == 1
     assert lib.gmagnus_bandwidth_probe(4, 0x1008, 0x1000, 1 << 20, 0, 1, None, ctypes.byref(ms)) == 1
     assert lib.gmagnus_bandwidth_probe(4, 0x1000, 0x1000, 1 << 20, 0, 0, None, ctypes.byref(ms)) == 1
+
+
+TYPE_SIZES = [("int32", "float64", 4, 8), ("int32", "float32", 4, 4), ("int64", "float64", 8, 8),
+              ("int64", "float32", 8, 4)]
+
+
+@pytest.mark.parametrize("idt,vdt,s_col,s_val", TYPE_SIZES)
+def test_typed_planner_matches_oracle_planner(lib, idt, vdt, s_col, s_val):
+    # tau, W and the chunk limits from the type sizes (Section III-D), with the
+    # library's caps on tau (light-row capacity) and W (dense accumulator)
+    import torch
+
+    from oracle.params import get_magnus_params
+
+    it, vt = getattr(torch, idt), getattr(torch, vdt)
+    for s_lm in (65536, 131072, 163840, 233472):
+        for cm in (1, 100, 4096, 8193, 65536, 1 << 20, (1 << 22) + 3, 1 << 23, 2_000_000_000):
+            a = gm.get_params(cm, s_lm, it, vt)
+            b = get_magnus_params(cm, s_lm, s_col=s_col, s_val=s_val, dense_width_max=8192, tau_max=6912)
+            assert (a.tau, a.dense_width, a.chunks_required, a.chunks_max) == (b.tau, b.dense_width,
+                                                                               b.chunks_required, b.chunks_max)
+            assert a.levels == b.v_chunks, (cm, s_lm)
+
+
+def test_typed_planner_values_at_160kb(lib):
+    import torch
+
+    p = gm.get_params(1 << 22, 163840, torch.int64, torch.float64)
+    assert (p.tau, p.dense_width, p.chunks_max, p.levels) == (5120, 8192, 32, [32, 16])
+    p = gm.get_params(1 << 22, 163840, torch.int32, torch.float32)  # tau 10240 and W 16384 derived, then capped
+    assert (p.tau, p.dense_width, p.chunks_max, p.levels) == (6912, 8192, 64, [64, 8])
+    p = gm.get_params(1 << 22, 163840, torch.int64, torch.float32)
+    assert (p.tau, p.dense_width, p.chunks_max, p.levels) == (6826, 8192, 32, [32, 16])
+    # int64 columns reach 2^35 columns of C; int32 stays below 2^31
+    assert gm.get_params(1 << 35, 163840, torch.int64, torch.float64).levels == [32, 32, 32, 32, 4]
+    for cm, it in (((1 << 35) + 1, torch.int64), (1 << 31, torch.int32)):
+        with pytest.raises(gm.GmagnusError) as e:
+            gm.get_params(cm, 163840, it, torch.float64)
+        assert e.value.status == 1
+
+
+def test_typed_plan_validation_without_device(lib):
+    h = ctypes.c_void_p()
+
+    def md(n_rows, n_cols, it=0, vt=0):
+        return gm.MatrixDesc(n_rows, n_cols, 0, 0x1000, None, None, it, vt)
+    # mismatched types
+    assert lib.gmagnus_plan_typed(ctypes.byref(h), ctypes.byref(md(4, 5, 0, 0)), ctypes.byref(md(5, 3, 1, 0)), None,
+                                  None) == 1
+    assert lib.gmagnus_plan_typed(ctypes.byref(h), ctypes.byref(md(4, 5, 0, 0)), ctypes.byref(md(5, 3, 0, 1)), None,
+                                  None) == 1
+    # unknown types
+    assert lib.gmagnus_plan_typed(ctypes.byref(h), ctypes.byref(md(4, 5, 2, 0)), ctypes.byref(md(5, 3, 2, 0)), None,
+                                  None) == 1
+    # int64 columns allow B (C) up to 2^35 columns, never A
+    assert lib.gmagnus_plan_typed(ctypes.byref(h), ctypes.byref(md(4, 1 << 31, 1)), ctypes.byref(md(1 << 31, 3, 1)),
+                                  None, None) == 6
+    assert lib.gmagnus_plan_typed(ctypes.byref(h), ctypes.byref(md(4, 5, 1)), ctypes.byref(md(5, (1 << 35) + 1, 1)),
+                                  None, None) == 6
+    assert not h.value

@@ -62,6 +62,9 @@ def test_dense_bruteforce(shape, density):
     # bound = sum of |a*b| = |A| @ |B|
     absd = (np.abs(A.to_dense()) if k else np.zeros((m, 0))) @ np.abs(B.to_dense())
     assert np.allclose(C.bound, absd[rows, C.col], rtol=1e-14, atol=0)
+    # terms = number of products per entry = the integer product of the patterns
+    counts = pa @ pb
+    assert np.array_equal(C.terms, counts[rows, C.col])
 
 
 def test_identity_and_permutation_exact():
@@ -265,6 +268,52 @@ def test_planner_mi355x_values():
     # paper: n_groupRows = 2 in its experiments
     assert get_magnus_params(1 << 20, 131072).group_rows == 2
     assert get_magnus_params(1 << 20, 233472).group_rows == 2
+
+
+# ------------------------------------------------------ 64-bit column indices
+
+def test_wide_columns_bruteforce():
+    # B with columns spread over 2^33: each row of C accumulated in a Python
+    # dict from the definition (Section II-B, Eq. gustav), compared entry by
+    # entry (columns exact, values within a few roundings, term counts exact)
+    A = wl.uniform(25, 30, 0.2, 41)
+    for B in (wl.wide(30, 1 << 33, 6, 42), wl.wide(30, 1 << 33, 9, 43, window=40)):
+        C = oracle.spgemm(A, B)
+        for i in range(A.n_rows):
+            acc, mag, cnt = {}, {}, {}
+            for p in range(A.row_ptr[i], A.row_ptr[i + 1]):
+                k = int(A.col[p])
+                for r in range(B.row_ptr[k], B.row_ptr[k + 1]):
+                    c = int(B.col[r])
+                    x = float(A.val[p]) * float(B.val[r])
+                    acc[c] = acc.get(c, 0.0) + x
+                    mag[c] = mag.get(c, 0.0) + abs(x)
+                    cnt[c] = cnt.get(c, 0) + 1
+            cols = sorted(acc)
+            c_ref, v_ref, b_ref = C.row(i)
+            assert list(c_ref) == cols
+            assert np.allclose(v_ref, [acc[c] for c in cols], rtol=0, atol=1e-14 * max(mag.values(), default=1))
+            assert list(C.row_terms(i)) == [cnt[c] for c in cols]
+
+
+def test_column_shift_moves_columns_only():
+    # shifting every column of B by 2^32 shifts the columns of C by 2^32 and
+    # leaves values, bounds and term counts unchanged
+    A = wl.rmat(8, 8, 0.57, 0.19, 0.19, 44)
+    C = oracle.spgemm(A, A)
+    B2 = wl.CSR(A.n_rows, A.n_cols + (1 << 32), A.row_ptr, A.col.astype(np.int64) + (1 << 32), A.val)
+    C2 = oracle.spgemm(A, B2)
+    assert np.array_equal(C2.row_ptr, C.row_ptr) and np.array_equal(C2.col, C.col + (1 << 32))
+    assert np.array_equal(C2.val, C.val) and np.array_equal(C2.bound, C.bound)
+    assert np.array_equal(C2.terms, C.terms)
+
+
+def test_terms_sum_to_row_products():
+    A = wl.rmat(10, 8, 0.57, 0.19, 0.19, 45)
+    C = oracle.spgemm(A, A)
+    ip = oracle.row_products(A, A)
+    cs = np.concatenate([[0], np.cumsum(C.terms)])
+    assert np.array_equal(cs[C.row_ptr[1:]] - cs[C.row_ptr[:-1]], ip)
 
 
 # ------------------------------------------------- symbolic counts by marking

@@ -2,7 +2,8 @@
 
 Only input generation lives here (no SpGEMM arithmetic). Matrices are returned
 as :class:`CSR` holding numpy arrays: ``row_ptr`` int64 (n_rows+1), ``col``
-int32 (sorted, unique within a row) and ``val`` float64.
+int32 (int64 for :func:`wide`; sorted, unique within a row) and ``val``
+float64.
 
 The five benchmark workloads are named in :data:`CONFIGS`; they stand in for
 the paper's R-MAT pairs and SuiteSparse set (Section IV-A), which are not
@@ -73,7 +74,7 @@ class CSR:
     n_rows: int
     n_cols: int
     row_ptr: np.ndarray  # int64, n_rows + 1
-    col: np.ndarray  # int32, nnz
+    col: np.ndarray  # int32 (int64 for column counts of 2^31 and more), nnz
     val: np.ndarray  # float64, nnz
 
     @property
@@ -132,6 +133,28 @@ def uniform(n_rows: int, n_cols: int, density: float, seed: int, values: str = "
 
 def identity(n: int) -> CSR:
     return CSR(n, n, np.arange(n + 1, dtype=np.int64), np.arange(n, dtype=np.int32), np.ones(n))
+
+
+def wide(n_rows: int, n_cols: int, per_row: int, seed: int, window: int = 0, base: int = -1) -> CSR:
+    """CSR with int64 columns over a column range that may exceed 2^31: each
+    row holds `per_row` distinct columns drawn uniformly (numpy's seeded
+    generator) from the whole range, or, with window > 0, from a window of
+    that many columns starting at `base` (placed at random per row when base
+    is negative); values U(-1, 1)."""
+    rng = np.random.default_rng(seed)
+    cols = []
+    for _ in range(n_rows):
+        if window:
+            lo = base if base >= 0 else int(rng.integers(0, max(n_cols - window, 1)))
+            c = lo + rng.choice(min(window, n_cols), size=min(per_row, window), replace=False)
+        else:
+            c = rng.choice(n_cols, size=per_row, replace=False) if n_cols < (1 << 24) else \
+                np.unique(rng.integers(0, n_cols, size=per_row))
+        cols.append(np.sort(np.asarray(c, np.int64)))
+    rp = np.zeros(n_rows + 1, np.int64)
+    np.cumsum([c.size for c in cols], out=rp[1:])
+    col = np.concatenate(cols) if cols else np.zeros(0, np.int64)
+    return CSR(n_rows, n_cols, rp, col, rng.uniform(-1.0, 1.0, col.size))
 
 
 def permutation(n: int, seed: int) -> CSR:
