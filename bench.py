@@ -87,6 +87,7 @@ def run_step(g, dA, dB, bounds, timing, acc, c_bufs, extra_flags=0, tau=0):
                                    "disagreed with the symbolic phase); the step's result is wrong" % (
                                        a, b, info.check_flags))
             products += info.products_total
+            acc["_heavy"] = acc.get("_heavy", 0) + info.products_heavy
             acc.setdefault("_levels", set()).add(info.params.n_levels)
             for i, k in enumerate(g.K_NAMES):
                 acc.setdefault(k, [0.0, 0, 0.0])
@@ -350,7 +351,8 @@ def main():
         "dtype": "f64",
         "data": "synthetic",
         "config": {"workload": (PAIR_WORKLOADS if pair else WORKLOADS)[args.config], "name": args.config,
-                   "seed": cfg.seed, "n": A.n_rows, "nnz_a": A.nnz, "nnz_b": B.nnz, "products": products, "nnz_c": nnz, "panels": len(bounds) - 1,
+                   "seed": cfg.seed, "n": A.n_rows, "nnz_a": A.nnz, "nnz_b": B.nnz, "products": products,
+                   "products_heavy": acc.get("_heavy", 0) // max(args.steps, 1), "nnz_c": nnz, "panels": len(bounds) - 1,
                    "panel_products": args.panel_products},
         "achieved_hbm_gbs": {"heavy_path_kernels": heavy_gb / (heavy_ms / 1000.0) if heavy_ms else None,
                              "heavy_path_frac": (heavy_gb / (heavy_ms / 1000.0)) / HBM_PEAK_GBS if heavy_ms else None,
