@@ -30,13 +30,25 @@ GM_DEV int32_t leaf_col_nt(const LeafSet &L, int64_t t) {
 // --------------------------------------------------------------- sources
 template <int BLOCK, typename V>
 struct GusLds {
-    int32_t off[BLOCK + 1];
+    int32_t off[BLOCK];  // product offsets of the batch's entries; INT32_MAX past the last one
     int64_t bst[BLOCK];
     V av[BLOCK];
     int32_t scan[BLOCK / GM_WAVE];
 };
 
 constexpr int GUS_ILP = 4;
+
+// Entry of product t in a batch: the largest q < BLOCK with off[q] <= t
+// (off[0] = 0, off non-decreasing, INT32_MAX past the batch's entries), by a
+// branch-free power-of-two search (every step one LDS read, no loop exit to
+// wait for, so the searches of several products overlap).
+template <int BLOCK>
+GM_DEV int entry_of(const int32_t *off, int32_t t) {
+    int q = 0;
+#pragma unroll
+    for (int step = BLOCK / 2; step >= 1; step >>= 1) q = off[q + step] <= t ? q + step : q;
+    return q;
+}
 
 // Calls f(col - base, product) for every intermediate product of the A
 // entries [j0, j1) (one row of A), A entries taken in batches of BLOCK.
@@ -58,27 +70,31 @@ GM_DEV void gustavson_row(const CsrV<CI, V> &A, const CsrV<CI, V> &B, int64_t j0
         }
         int32_t tot;
         const int32_t ex = block_excl_scan<BLOCK>(len, L.scan, &tot);
-        if (tid < nb) L.off[tid] = ex;
+        L.off[tid] = tid < nb ? ex : INT32_MAX;
         __syncthreads();
-        // GUS_ILP products per thread are loaded before any is accumulated, so
-        // a row's B loads overlap instead of each waiting for the previous
-        // product's accumulator update
+        // GUS_ILP products per thread: the searches, then every load, then the
+        // accumulation, with no branch between the loads (past the end a thread
+        // re-reads the batch's last product and drops it), so one thread's loads
+        // are in flight together
         for (int32_t tb = tid; tb < tot; tb += BLOCK * GUS_ILP) {
-            int32_t c[GUS_ILP];
+            int32_t q[GUS_ILP];
+            int64_t src[GUS_ILP];
+#pragma unroll
+            for (int u = 0; u < GUS_ILP; ++u) {
+                const int32_t t = tb + u * BLOCK < tot ? tb + u * BLOCK : tot - 1;
+                q[u] = entry_of<BLOCK>(L.off, t);
+                src[u] = L.bst[q[u]] + (t - L.off[q[u]]);
+            }
+            CI c[GUS_ILP];
             V v[GUS_ILP];
 #pragma unroll
             for (int u = 0; u < GUS_ILP; ++u) {
-                const int32_t t = tb + u * BLOCK;
-                if (t < tot) {
-                    const int q = (int)find_row(L.off, 0, nb, t);
-                    const int64_t src = L.bst[q] + (t - L.off[q]);
-                    c[u] = (int32_t)(B.ci[src] - base);
-                    v[u] = NUM ? (V)(L.av[q] * B.v[src]) : (V)0;
-                }
+                c[u] = B.ci[src[u]];
+                if (NUM) v[u] = B.v[src[u]];
             }
 #pragma unroll
             for (int u = 0; u < GUS_ILP; ++u)
-                if (tb + u * BLOCK < tot) f(c[u], v[u]);
+                if (tb + u * BLOCK < tot) f((int32_t)(c[u] - base), NUM ? (V)(L.av[q[u]] * v[u]) : (V)0);
         }
         __syncthreads();
     }
@@ -743,27 +759,31 @@ __global__ __launch_bounds__(BLOCK) void k_light_sort_num(CsrV<CI, V> A, CsrV<CI
         }
         int32_t tot;
         const int32_t ex = block_excl_scan<BLOCK>(len, L.scan, &tot);
-        if (tid < nb) L.off[tid] = ex;
+        L.off[tid] = tid < nb ? ex : INT32_MAX;
         __syncthreads();
         if (n + tot > CAP) {  // cannot happen for a light row of this bin (ip <= CAP)
             if (tid == 0) atomicOr(err, 8);
             return;
         }
-        int q_prev = 0;
+        // as in gustavson_row: searches, then every load, with no branch between them
         for (int tb = tid; tb < tot; tb += BLOCK * SORT_ILP) {
+            int q[SORT_ILP];
+            int64_t src[SORT_ILP];
+#pragma unroll
+            for (int u = 0; u < SORT_ILP; ++u) {
+                const int t = tb + u * BLOCK < tot ? tb + u * BLOCK : tot - 1;
+                q[u] = entry_of<BLOCK>(L.off, t);
+                src[u] = L.bst[q[u]] + (t - L.off[q[u]]);
+            }
             CI c[SORT_ILP];
             V v[SORT_ILP];
 #pragma unroll
             for (int u = 0; u < SORT_ILP; ++u) {
-                const int t = tb + u * BLOCK;
-                if (t < tot) {
-                    const int q = (int)find_row(L.off, q_prev, nb, t);
-                    q_prev = q;
-                    const int64_t src = L.bst[q] + (t - L.off[q]);
-                    c[u] = B.ci[src];
-                    v[u] = L.av[q] * B.v[src];
-                }
+                c[u] = B.ci[src[u]];
+                v[u] = B.v[src[u]];
             }
+#pragma unroll
+            for (int u = 0; u < SORT_ILP; ++u) v[u] *= L.av[q[u]];
 #pragma unroll
             for (int u = 0; u < SORT_ILP; ++u) {
                 const int t = tb + u * BLOCK;
@@ -786,20 +806,78 @@ __global__ __launch_bounds__(BLOCK) void k_light_sort_num(CsrV<CI, V> A, CsrV<CI
                                  err, 1, L.scan);
 }
 
+// Dense window of a light row: one presence byte per column, set with a
+// plain LDS store (every product of a column stores the same 1, so no atomic
+// and no read are needed; the columns of a banded row repeat many times), and
+// for the numeric phase a value per column added with an LDS atomic.
+template <int BLOCK, int WMAX, bool VALS, typename V = double>
+struct WinLds {
+    V vals[VALS ? WMAX : 1];
+    uint8_t flag[WMAX];
+    int32_t scan[BLOCK / GM_WAVE];
+};
+
+template <int BLOCK, int WMAX, bool VALS, typename V>
+GM_DEV void win_clear(WinLds<BLOCK, WMAX, VALS, V> &L, int width) {
+    uint32_t *f = (uint32_t *)L.flag;
+    for (int i = threadIdx.x; i < (width + 3) / 4; i += BLOCK) f[i] = 0u;
+    if (VALS)
+        for (int i = threadIdx.x; i < width; i += BLOCK) L.vals[i] = (V)0;
+}
+
+// number of present columns (flag words read 4 bytes at a time)
+template <int BLOCK, int WMAX, bool VALS, typename V>
+GM_DEV int32_t win_count(WinLds<BLOCK, WMAX, VALS, V> &L, int width) {
+    const uint32_t *f = (const uint32_t *)L.flag;
+    int32_t c = 0;
+    for (int i = threadIdx.x; i < (width + 3) / 4; i += BLOCK) c += __popc(f[i]);  // each present byte is 0x01
+    return block_reduce_sum<BLOCK>(c, L.scan);
+}
+
+// Writes the present columns in increasing order (as dense_emit, with the
+// presence bytes in place of the bitmap).
+template <int BLOCK, int WMAX, typename V, typename CI>
+GM_DEV void win_emit(WinLds<BLOCK, WMAX, true, V> &L, int width, int64_t nnz, CI col_base, CI *out_col, V *out_val,
+                     int32_t *err) {
+    constexpr int NW = BLOCK / GM_WAVE;
+    const int lane = threadIdx.x & (GM_WAVE - 1), w = threadIdx.x / GM_WAVE;
+    const int span = ((width + NW - 1) / NW + GM_WAVE - 1) / GM_WAVE * GM_WAVE;
+    const int c0 = w * span, c1 = c0 + span < width ? c0 + span : width;
+    int32_t cnt = 0;
+    for (int c = c0 + lane; c < c1; c += GM_WAVE) cnt += L.flag[c];
+    cnt = wave_reduce_sum(cnt);
+    int32_t total;
+    int32_t base = block_excl_scan<BLOCK>(lane == 0 ? cnt : 0, L.scan, &total);
+    base = __shfl(base, 0, GM_WAVE);
+    if (threadIdx.x == 0 && total != nnz) atomicOr(err, 2);
+    for (int g = c0; g < c1; g += GM_WAVE) {
+        const int c = g + lane;
+        const bool p = c < c1 && L.flag[c];
+        const uint64_t m = ballot(p);
+        const int pos = base + __popcll(m & lanemask_lt());
+        if (p && pos < nnz) {
+            out_col[pos] = (CI)c + col_base;
+            out_val[pos] = L.vals[c];
+        }
+        base += __popcll(m);
+    }
+}
+
 template <int BLOCK, int WMAX, typename CI>
 __global__ __launch_bounds__(BLOCK) void k_light_win_sym(CsrV<CI, NoV> A, CsrV<CI, NoV> B, int64_t r0,
                                                          const int64_t *items, const CI *minc, const CI *maxc,
                                                          int64_t *row_nnz) {
-    __shared__ DenseBits<BLOCK, WMAX> D;
+    __shared__ WinLds<BLOCK, WMAX, false> D;
     __shared__ GusLds<BLOCK, NoV> G;
     const int64_t r = items[blockIdx.x];
     const CI base = minc[r];
     const int width = (int)(maxc[r] - base + 1);
-    dense_clear(D, width, false);
+    win_clear(D, width);
     __syncthreads();
     gustavson_row<BLOCK, false>(A, B, A.rp[r0 + r], A.rp[r0 + r + 1], base, G,
-                                [&](int32_t c, NoV) { dense_set(D, c); });
-    const int32_t cnt = dense_count(D, width);
+                                [&](int32_t c, NoV) { D.flag[c] = 1; });
+    __syncthreads();
+    const int32_t cnt = win_count(D, width);
     if (threadIdx.x == 0) row_nnz[r] = cnt;
 }
 
@@ -808,17 +886,20 @@ __global__ __launch_bounds__(BLOCK) void k_light_win_num(CsrV<CI, V> A, CsrV<CI,
                                                          const int64_t *items, const CI *minc, const CI *maxc,
                                                          const int64_t *c_row_ptr, CI *c_col, V *c_val,
                                                          int32_t *err) {
-    __shared__ DenseLds<BLOCK, WMAX, V> D;
+    __shared__ WinLds<BLOCK, WMAX, true, V> D;
     __shared__ GusLds<BLOCK, V> G;
     const int64_t r = items[blockIdx.x];
     const CI base = minc[r];
     const int width = (int)(maxc[r] - base + 1);
-    dense_clear(D, width, true);
+    win_clear(D, width);
     __syncthreads();
-    gustavson_row<BLOCK, true>(A, B, A.rp[r0 + r], A.rp[r0 + r + 1], base, G,
-                               [&](int32_t c, V v) { dense_add(D, c, v); });
+    gustavson_row<BLOCK, true>(A, B, A.rp[r0 + r], A.rp[r0 + r + 1], base, G, [&](int32_t c, V v) {
+        D.flag[c] = 1;
+        __hip_atomic_fetch_add(&D.vals[c], v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    });
+    __syncthreads();
     const int64_t dst = c_row_ptr[r];
-    dense_emit(D, width, c_row_ptr[r + 1] - dst, base, c_col + dst, c_val + dst, err);
+    win_emit(D, width, c_row_ptr[r + 1] - dst, base, c_col + dst, c_val + dst, err);
 }
 
 // ------------------------------------------------------------------ leaves
