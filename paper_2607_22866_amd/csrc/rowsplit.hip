@@ -322,21 +322,29 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows(RsArgs<CI, V> a) {
         for (int tb = t0; tb < t1; tb += RS_BLOCK * RS_ILP) {
             int32_t col[RS_ILP], rg[RS_ILP];
             V bv[RS_ILP], am[RS_ILP];
+            // as in the two-level kernel: every load of the thread's products in flight together
+            int qs[RS_ILP];
+            int64_t sp[RS_ILP];
 #pragma unroll
             for (int u = 0; u < RS_ILP; ++u) {
-                const int t = tb + u * RS_BLOCK + tid;
-                rg[u] = -1;
-                col[u] = -1;
-                if (t < t1) {
-                    const int w = t >> 5, bit = t & 31;
-                    const uint32_t below = bit == 31 ? ~0u : (2u << bit) - 1u;
-                    const int q = word_pre[w] + __popc(start_bits[w] & below) - 1;
-                    const int64_t sp = rn_src[q] + t;
-                    col[u] = (int32_t)(a.B.ci[sp] & mask);
-                    bv[u] = a.B.v[sp];
-                    am[u] = rn_a[q];
-                    rg[u] = rn_reg[q];
-                }
+                const int t = tb + u * RS_BLOCK + tid < t1 ? tb + u * RS_BLOCK + tid : t1 - 1;
+                const int w = t >> 5, bit = t & 31;
+                const uint32_t below = bit == 31 ? ~0u : (2u << bit) - 1u;
+                qs[u] = word_pre[w] + __popc(start_bits[w] & below) - 1;
+                sp[u] = rn_src[qs[u]] + t;
+            }
+            CI cb[RS_ILP];
+#pragma unroll
+            for (int u = 0; u < RS_ILP; ++u) {
+                cb[u] = a.B.ci[sp[u]];
+                bv[u] = a.B.v[sp[u]];
+            }
+#pragma unroll
+            for (int u = 0; u < RS_ILP; ++u) {
+                const bool ok = tb + u * RS_BLOCK + tid < t1;
+                col[u] = ok ? (int32_t)(cb[u] & mask) : -1;
+                am[u] = rn_a[qs[u]];
+                rg[u] = ok ? rn_reg[qs[u]] : -1;
             }
 #pragma unroll
             for (int u = 0; u < RS_ILP; ++u) {
@@ -671,19 +679,35 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args<CI, V> a) {
             int32_t col[RS2_E];
             V val[RS2_E];
             int key[RS2_E];
+            // segments and B positions of the thread's products, then all their
+            // loads with no branch in between (past the end a thread re-reads the
+            // sub-batch's last product and drops it), so they are in flight together
+            int qs[RS2_E];
+            int64_t sp[RS2_E];
 #pragma unroll
             for (int u = 0; u < RS2_E; ++u) {
-                const int t = sbt + u * RS_BLOCK + tid;
+                const int t = sbt + u * RS_BLOCK + tid < t1 ? sbt + u * RS_BLOCK + tid : t1 - 1;
+                const int wd = t >> 5, bit = t & 31;
+                const uint32_t below = bit == 31 ? ~0u : (2u << bit) - 1u;
+                qs[u] = word_pre[wd] + __popc(start_bits[wd] & below) - 1;
+                sp[u] = rn_src[qs[u]] + t;
+            }
+            CI cb[RS2_E];
+            V bb[RS2_E];
+#pragma unroll
+            for (int u = 0; u < RS2_E; ++u) {
+                cb[u] = a.B.ci[sp[u]];
+                bb[u] = a.B.v[sp[u]];
+            }
+#pragma unroll
+            for (int u = 0; u < RS2_E; ++u) {
                 key[u] = -1;
                 col[u] = 0;
                 val[u] = 0;
-                if (t < t1) {
-                    const int wd = t >> 5, bit = t & 31;
-                    const uint32_t below = bit == 31 ? ~0u : (2u << bit) - 1u;
-                    const int q = word_pre[wd] + __popc(start_bits[wd] & below) - 1;
-                    const int64_t sp = rn_src[q] + t;
-                    col[u] = (int32_t)(a.B.ci[sp] & mask);
-                    val[u] = rn_a[q] * a.B.v[sp];
+                if (sbt + u * RS_BLOCK + tid < t1) {
+                    const int q = qs[u];
+                    col[u] = (int32_t)(cb[u] & mask);
+                    val[u] = rn_a[q] * bb[u];
                     const int rl = rn_reg[q];
                     if (rt + rl < a.n_heavy_out) {
                         key[u] = rl * a.nc1 + (col[u] >> a.shift1);
