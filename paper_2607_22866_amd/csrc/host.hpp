@@ -180,20 +180,23 @@ void expand_split(const Csr &B, const SliceArrays &sl, int64_t total, const int6
 
 // ------------------------------------------------------------- rowsplit.hip
 // The heavy rows' A entries in row order: B row, its slice (-1 for an empty
-// B row), heavy row, value.
+// B row), heavy row, start of the B row, value.
 struct RowEntries {
     int32_t *k = nullptr;
     int32_t *s = nullptr;
     int32_t *h = nullptr;
+    int64_t *b0 = nullptr;
     void *a = nullptr;  // A's value type
 };
-void heavy_entries(const Csr &A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0, const int64_t *a_heavy_ptr,
-                   int64_t nnz_heavy_all, const int32_t *k_to_slice, const RowEntries &ent, hipStream_t s);
-// pre[e * nc + c]: offset of entry e's chunk-c part inside region (c, row of e)
-// (segmented scan; scratch: agg and carry n_waves * nc, wfirst/wlast n_waves).
+void heavy_entries(const Csr &A, const Csr &B, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
+                   const int64_t *a_heavy_ptr, int64_t nnz_heavy_all, const int32_t *k_to_slice, const RowEntries &ent,
+                   hipStream_t s);
+// pb[c * n_ent + e] = (offset of entry e's chunk-c part inside region (c, row
+// of e), offset of that part in e's B row); chunk-major (segmented scan;
+// scratch: agg and carry n_waves * nc, wfirst/wlast n_waves).
 int64_t entry_offset_waves(int64_t n_ent);
 void entry_offsets(const RowEntries &ent, int64_t n_ent, const int32_t *bnd, int nc, int64_t *agg, int32_t *wfirst,
-                   int32_t *wlast, int64_t *carry, uint32_t *pre, hipStream_t s);
+                   int32_t *wlast, int64_t *carry, uint2 *pb, hipStream_t s);
 // Region r of the chunk-major level-0 output (perm: position -> c * n_heavy + h).
 void region_records(const int64_t *perm, int64_t n_out, int64_t n_heavy, const int64_t *a_heavy_ptr, int32_t *reg_c,
                     int64_t *reg_efirst, int64_t *reg_ne, hipStream_t s);
@@ -202,7 +205,7 @@ bool rows_next_fits(int next_nc);
 // Chunk-major row-order expansion with the level-0 split: writes the level-0
 // output (chunk-local columns) and, when next_counts is given, the next
 // level's counts of the heavy regions.
-void expand_rows(const Csr &B, const RowEntries &ent, const uint32_t *pre, const int32_t *bnd, const int64_t *out_ptr,
+void expand_rows(const Csr &B, const RowEntries &ent, const uint2 *pb, int64_t n_ent, const int64_t *out_ptr,
                  const int64_t *seg_base, const int32_t *reg_c, const int64_t *reg_efirst, const int64_t *reg_ne,
                  int64_t n_out, int64_t n_heavy_out, int64_t total, int nc, int shift, int next_nc, int next_shift,
                  int64_t *next_counts, int64_t *tile_words, int32_t *out_col, void *out_val, hipStream_t s);
@@ -227,7 +230,7 @@ bool rows2_fits(int64_t tau, int nc1, int nf);
 // cursor1: next free place of second-level row r * nc1 + c1 (starts at its
 // row pointer); light regions are written to out_*0 at their first-level place;
 // the final chunks' columns (at most 2^16 wide) are stored in 16 bits.
-void expand_rows2(const Csr &B, const RowEntries &ent, const uint32_t *pre, const int32_t *bnd,
+void expand_rows2(const Csr &B, const RowEntries &ent, const uint2 *pb, int64_t n_ent,
                   const int64_t *out_ptr, const int64_t *seg_base, const int32_t *reg_c, const int64_t *reg_efirst,
                   const int64_t *reg_ne, int64_t n_out, int64_t n_heavy_out, int64_t total, int nc, int shift,
                   int nc1, int shift1, int64_t tau, int64_t *cursor1, int64_t n_out1_elems, int32_t *err,

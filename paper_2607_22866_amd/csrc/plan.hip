@@ -748,7 +748,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
     int64_t *counts0 = nullptr;  // level-0 counts when computed from the structure
     int32_t *sbnd = nullptr;     // per-slice level-0 chunk boundaries (kept for the fused expansion)
     RowEntries ent;              // chunk-major row order: entries, their chunk offsets, the row pointers of A~
-    uint32_t *pre = nullptr;
+    uint2 *pb = nullptr;         // chunk-major offsets of the entries' chunk parts (region, B row)
     int64_t *a_heavy_keep = nullptr;
 
     // ---- masked CSR -> CSC of the heavy rows and slice offsets
@@ -815,9 +815,10 @@ void heavy_symbolic(gmagnus_plan_s *p) {
             ent.k = ws.alloc<int32_t>(nnz_heavy_all);
             ent.s = ws.alloc<int32_t>(nnz_heavy_all);
             ent.h = ws.alloc<int32_t>(nnz_heavy_all);
+            ent.b0 = ws.alloc<int64_t>(nnz_heavy_all);
             ent.a = ws.alloc_bytes(VS * nnz_heavy_all);
-            values_step([=](const Csr &A, const Csr &, hipStream_t st) {
-                heavy_entries(A, heavy_rows, nh, r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, ent, st);
+            values_step([=](const Csr &A, const Csr &B, hipStream_t st) {
+                heavy_entries(A, B, heavy_rows, nh, r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, ent, st);
             });
         }
         if (P.n_levels > 0 && !paper_hist) {
@@ -835,13 +836,13 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                 const int64_t nw = entry_offset_waves(nnz_heavy_all);
                 int64_t *agg = ws.alloc<int64_t>(nw * nc0), *carry = ws.alloc<int64_t>(nw * nc0);
                 int32_t *wfirst = ws.alloc<int32_t>(nw), *wlast = ws.alloc<int32_t>(nw);
-                pre = ws.alloc<uint32_t>(nnz_heavy_all * nc0);
-                entry_offsets(ent, nnz_heavy_all, sbnd, nc0, agg, wfirst, wlast, carry, pre, s);
+                pb = ws.alloc<uint2>(nnz_heavy_all * nc0);
+                entry_offsets(ent, nnz_heavy_all, sbnd, nc0, agg, wfirst, wlast, carry, pb, s);
                 ws.free(agg);
                 ws.free(carry);
                 ws.free(wfirst);
                 ws.free(wlast);
-                add_bytes(p, GMAGNUS_K_HISTOGRAM, 8.0 * nnz_heavy_all + 4.0 * nnz_heavy_all * nc0);
+                add_bytes(p, GMAGNUS_K_HISTOGRAM, 8.0 * nnz_heavy_all + 8.0 * nnz_heavy_all * nc0);
             }
             if (!fused) {
                 ws.free(sbnd);
@@ -890,8 +891,9 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         ws.free(ent.k);
         ws.free(ent.s);
         ws.free(ent.h);
+        ws.free(ent.b0);
         ws.free(ent.a);
-        ws.free(pre);
+        ws.free(pb);
         ws.free(a_heavy_keep);
         if (sbnd) ws.free(sbnd);
         sbnd = nullptr;
@@ -1064,15 +1066,16 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                     values_step([=](const Csr &, const Csr &B, hipStream_t st) {
                         // the second level's cursors start at its regions' offsets
                         gather_i64(out_ptr1, x_map1, n_out1, cursor1, st);
-                        expand_rows2(B, ent, pre, sbnd, out_ptr, seg_base, reg_c, reg_efirst, reg_ne, n_out, nh_out,
-                                     H, nc, shift0, nc1, shift1, tau, cursor1, elems1, err, exp_tiles, oc0, ov0,
-                                     (uint16_t *)oc1, ov1, st);
+                        expand_rows2(B, ent, pb, nnz_heavy_all, out_ptr, seg_base, reg_c, reg_efirst, reg_ne, n_out,
+                                     nh_out, H, nc, shift0, nc1, shift1, tau, cursor1, elems1, err, exp_tiles, oc0,
+                                     ov0, (uint16_t *)oc1, ov1, st);
                     });
                 }
                 p->info.kernel_launches[GMAGNUS_K_EXPAND] += 1;
-                // products (the final chunks' columns in 16 bits), entries, offsets, B rows, row records
-                add_bytes(p, GMAGNUS_K_EXPAND, (4.0 + VS) * H - 2.0 * elems1 + (12.0 + VS) * nnz_heavy_all +
-                                                   4.0 * nnz_heavy_all * nc + (CS + VS) * blen_total + 24.0 * n_out +
+                // products (the final chunks' columns in 16 bits), entries (B row start,
+                // value), their chunk offsets (region, B row), B rows, row records
+                add_bytes(p, GMAGNUS_K_EXPAND, (4.0 + VS) * H - 2.0 * elems1 + (8.0 + VS) * nnz_heavy_all +
+                                                   8.0 * nnz_heavy_all * nc + (CS + VS) * blen_total + 24.0 * n_out +
                                                    8.0 * n_out1);
                 p->info.level_rows_in[1] = nh_out;
                 p->info.level_elems_in[1] = elems1;
@@ -1096,12 +1099,12 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                 void *ov = val_buf[nxt];
                 values_step([=](const Csr &, const Csr &B, hipStream_t st) {
                     if (next_counts) fill<int64_t>(next_counts, 0, nh_out * nn, st);
-                    expand_rows(B, ent, pre, sbnd, out_ptr, seg_base, reg_c, reg_efirst, reg_ne, n_out, nh_out, H, nc,
-                                shift0, nn, nshift, next_counts, exp_tiles, oc, ov, st);
+                    expand_rows(B, ent, pb, nnz_heavy_all, out_ptr, seg_base, reg_c, reg_efirst, reg_ne, n_out,
+                                nh_out, H, nc, shift0, nn, nshift, next_counts, exp_tiles, oc, ov, st);
                 });
                 p->info.kernel_launches[GMAGNUS_K_EXPAND] += 1;
                 add_bytes(p, GMAGNUS_K_EXPAND,
-                          (4.0 + VS) * H + (12.0 + VS) * nnz_heavy_all + 4.0 * nnz_heavy_all * nc +
+                          (4.0 + VS) * H + (8.0 + VS) * nnz_heavy_all + 8.0 * nnz_heavy_all * nc +
                               (CS + VS) * blen_total + 24.0 * n_out);
             }
             ws.free(reg_c);

@@ -8,9 +8,9 @@
 // per entry e = (h, k), by position in the chunk-c part of B[k,:]. So every
 // product has a fixed place:
 //
-//   out_ptr[r] + pre[e][c] + j,
+//   out_ptr[r] + pre[c][e] + j,
 //
-// where pre[e][c] is the exclusive prefix, over the entries of row h before
+// where pre[c][e] is the exclusive prefix, over the entries of row h before
 // e, of their chunk-c part sizes (a segmented scan over the row-ordered
 // entries, one lane per chunk). The expansion cuts the output range itself
 // into equal tiles: a tile writes one contiguous range of the output with no
@@ -37,8 +37,8 @@ constexpr int RS_HREG = 8;        // heavy regions per tile with LDS counters (m
 constexpr int RS_NEXT_MAX = 64;   // next-level chunks
 
 template <typename CI, typename V>
-__global__ void k_heavy_entries(CsrV<CI, V> A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
-                                const int64_t *a_heavy_ptr, int64_t total, const int32_t *k_to_slice,
+__global__ void k_heavy_entries(CsrV<CI, V> A, const int64_t *b_rp, const int64_t *heavy_rows, int64_t n_heavy,
+                                int64_t r0, const int64_t *a_heavy_ptr, int64_t total, const int32_t *k_to_slice,
                                 RowEntries ent) {
     for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total;
          e += (int64_t)gridDim.x * blockDim.x) {
@@ -48,6 +48,7 @@ __global__ void k_heavy_entries(CsrV<CI, V> A, const int64_t *heavy_rows, int64_
         ent.k[e] = k;
         ent.s[e] = k_to_slice[k];
         ent.h[e] = (int32_t)h;
+        ent.b0[e] = b_rp[k];
         static_cast<V *>(ent.a)[e] = A.v[j];
     }
 }
@@ -139,33 +140,62 @@ __global__ __launch_bounds__(PRE_CARRY_BLOCK) void k_pre_carry(const int64_t *ag
     }
 }
 
-// Offset scan, pass 3: pre[e * nc + c] = exclusive prefix of the chunk-c
-// sizes over the earlier entries of e's row.
+// Offset scan, pass 3: pb[c * n_ent + e] = (exclusive prefix of the chunk-c
+// sizes over the earlier entries of e's row, offset of the chunk-c part in
+// e's B row). Chunk-major, so the expansion reads consecutive entries of a
+// region from consecutive places. Lane = entry: for every chunk a wave takes a
+// segmented scan (by row) of its 64 entries' chunk sizes and stores 64
+// consecutive pairs. The sums are taken modulo 2^32 (DPP scan): the offsets
+// inside one (chunk, row) region are below 2^32, so the stored values are
+// exact. Lane c keeps the chunk-c total of the row that is open at the end of
+// the group (pass 2's carry at the wave's first row).
+GM_DEV uint32_t wave_incl_scan_u32(uint32_t x) {
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, false);  // row_shr:1
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, false);  // row_shr:2
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, false);  // row_shr:4
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, false);  // row_shr:8
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);  // row_bcast:31
+    return x;
+}
+
 __global__ __launch_bounds__(256) void k_pre_write(RowEntries ent, int64_t n_ent, const int32_t *bnd, int nc,
-                                                   const int64_t *carry, uint32_t *pre) {
+                                                   const int64_t *carry, uint2 *pb) {
     const int lane = threadIdx.x & (GM_WAVE - 1);
     const int64_t w = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / GM_WAVE;
     const int64_t e0 = w * PRE_ENTRIES;
-    if (e0 >= n_ent) return;
+    if (e0 >= n_ent) return;  // uniform across the wave
     const int64_t e1 = e0 + PRE_ENTRIES < n_ent ? e0 + PRE_ENTRIES : n_ent;
-    int32_t cur = ent.h[e0];
-    int64_t acc = lane < nc ? carry[w * nc + lane] : 0;
+    uint32_t open = lane < nc ? (uint32_t)carry[w * nc + lane] : 0u;  // lane c: chunk c of the open row
+    int32_t hopen = ent.h[e0];                                        // the open row
+    const uint64_t le_mask = lanemask_lt() | (uint64_t(1) << lane);
     for (int64_t eb = e0; eb < e1; eb += GM_WAVE) {
-        const int64_t e = eb + lane;
-        const int32_t hl = e < e1 ? ent.h[e] : -1;
-        const int32_t sl = e < e1 ? ent.s[e] : -1;
         const int cnt = (int)(e1 - eb < GM_WAVE ? e1 - eb : GM_WAVE);
-        for (int q = 0; q < cnt; ++q) {
-            const int32_t hq = __shfl(hl, q, GM_WAVE), sq = __shfl(sl, q, GM_WAVE);
-            if (hq != cur) {
-                acc = 0;
-                cur = hq;
+        const bool in = lane < cnt;
+        const int64_t e = eb + lane;
+        const int32_t h = in ? ent.h[e] : -1;
+        const int32_t sl = in ? ent.s[e] : -1;
+        const int32_t *bq = bnd + (int64_t)(sl < 0 ? 0 : sl) * (nc + 1);
+        const int32_t hp = prev_lane(h, hopen);
+        const uint64_t heads = ballot(h != hp);
+        const uint64_t mine = heads & le_mask;
+        const bool cont = mine == 0;  // no row start at or before this lane: the open row continues
+        const int seg0 = cont ? 0 : 63 - __clzll((long long)mine);
+        for (int c = 0; c < nc; ++c) {
+            uint32_t lo = 0, size = 0;
+            if (sl >= 0) {
+                lo = (uint32_t)bq[c];
+                size = (uint32_t)bq[c + 1] - lo;
             }
-            if (lane < nc) {
-                pre[(eb + q) * nc + lane] = (uint32_t)acc;
-                acc += entry_chunk_size(bnd, sq, nc, lane);
-            }
+            const uint32_t incl = wave_incl_scan_u32(size);
+            const uint32_t before = (uint32_t)__shfl((int)incl, seg0 > 0 ? seg0 - 1 : 0, GM_WAVE);
+            const uint32_t carry_c = (uint32_t)__builtin_amdgcn_readlane((int)open, c);
+            const uint32_t excl = incl - size - (seg0 > 0 ? before : 0u) + (cont ? carry_c : 0u);
+            if (in) pb[(int64_t)c * n_ent + e] = make_uint2(excl, lo);
+            const uint32_t last = (uint32_t)__builtin_amdgcn_readlane((int)(excl + size), cnt - 1);
+            if (lane == c) open = last;
         }
+        hopen = __builtin_amdgcn_readlane(h, cnt - 1);
     }
 }
 
@@ -185,15 +215,15 @@ __global__ void k_region_records(const int64_t *perm, int64_t n_out, int64_t n_h
 // Segment of output position g: region r (largest with out_ptr[r] <= g) and
 // the entry of r's row whose chunk part holds g (largest e with pre <= g - start).
 GM_DEV int64_t segment_of(int64_t g, const int64_t *out_ptr, int64_t n_out, const int64_t *seg_base,
-                          const int32_t *reg_c, const int64_t *reg_efirst, const int64_t *reg_ne, const uint32_t *pre,
-                          int nc, int64_t *region) {
+                          const int32_t *reg_c, const int64_t *reg_efirst, const int64_t *reg_ne, const uint2 *pb,
+                          int64_t n_ent, int64_t *region) {
     const int64_t r = find_row(out_ptr, 0, n_out + 1, g);
     const int64_t o = g - out_ptr[r];
     const int c = reg_c[r];
     int64_t lo = reg_efirst[r], hi = lo + reg_ne[r];
     while (hi - lo > 1) {
         const int64_t mid = lo + ((hi - lo) >> 1);
-        if ((int64_t)pre[mid * nc + c] <= o)
+        if ((int64_t)pb[(int64_t)c * n_ent + mid].x <= o)
             lo = mid;
         else
             hi = mid;
@@ -209,15 +239,15 @@ struct RsTile {
 };
 
 __global__ void k_rs_tiles(const int64_t *out_ptr, int64_t n_out, const int64_t *seg_base, const int32_t *reg_c,
-                           const int64_t *reg_efirst, const int64_t *reg_ne, const uint32_t *pre, int nc,
+                           const int64_t *reg_efirst, const int64_t *reg_ne, const uint2 *pb, int64_t n_ent,
                            int64_t total, int64_t n_tiles, RsTile *info) {
     for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < n_tiles;
          t += (int64_t)gridDim.x * blockDim.x) {
         const int64_t g0 = t * RS_TILE;
         const int64_t g1 = g0 + RS_TILE < total ? g0 + RS_TILE : total;
         int64_t r0, r1;
-        const int64_t s0 = segment_of(g0, out_ptr, n_out, seg_base, reg_c, reg_efirst, reg_ne, pre, nc, &r0);
-        const int64_t s1 = segment_of(g1 - 1, out_ptr, n_out, seg_base, reg_c, reg_efirst, reg_ne, pre, nc, &r1);
+        const int64_t s0 = segment_of(g0, out_ptr, n_out, seg_base, reg_c, reg_efirst, reg_ne, pb, n_ent, &r0);
+        const int64_t s1 = segment_of(g1 - 1, out_ptr, n_out, seg_base, reg_c, reg_efirst, reg_ne, pb, n_ent, &r1);
         info[t] = RsTile{r0, s0, s1 - s0 + 1};
     }
 }
@@ -226,8 +256,8 @@ template <typename CI, typename V>
 struct RsArgs {
     CsrV<CI, V> B;
     RowEntries ent;
-    const uint32_t *pre;
-    const int32_t *bnd;
+    const uint2 *pb;
+    int64_t n_ent;
     const int64_t *out_ptr;
     const int64_t *seg_base;
     const int32_t *reg_c;
@@ -288,13 +318,13 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows(RsArgs<CI, V> a) {
             const int64_t e = a.reg_efirst[r] + (S - sb[r - rb]);
             const bool last = S + 1 == sb[r - rb + 1];
             const int64_t start = a.out_ptr[r];
-            const int64_t seg_g = start + a.pre[e * a.nc + c];
-            const int64_t seg_e = last ? a.out_ptr[r + 1] : start + a.pre[(e + 1) * a.nc + c];
+            const uint2 pe = a.pb[(int64_t)c * a.n_ent + e];
+            const int64_t seg_g = start + pe.x;
+            const int64_t seg_e = last ? a.out_ptr[r + 1] : start + a.pb[(int64_t)c * a.n_ent + e + 1].x;
             const int64_t lo = seg_g > g0 ? seg_g : g0;
             const int64_t hi = seg_e < g1 ? seg_e : g1;
             if (hi > lo) {
-                const int32_t s = a.ent.s[e];
-                src = a.B.rp[a.ent.k[e]] + a.bnd[(int64_t)s * (a.nc + 1) + c] + (lo - seg_g);
+                src = a.ent.b0[e] + pe.y + (lo - seg_g);
                 av = static_cast<const V *>(a.ent.a)[e];
                 loc = (int32_t)(lo - g0);
                 len = (int32_t)(hi - lo);
@@ -572,8 +602,8 @@ template <typename CI, typename V>
 struct Rs2Args {
     CsrV<CI, V> B;
     RowEntries ent;
-    const uint32_t *pre;
-    const int32_t *bnd;
+    const uint2 *pb;
+    int64_t n_ent;
     const int64_t *out_ptr;  // first level's region pointers
     const int64_t *seg_base;
     const int32_t *reg_c;
@@ -645,13 +675,13 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args<CI, V> a) {
             const int64_t e = a.reg_efirst[r] + (S - sb[r - rb]);
             const bool last = S + 1 == sb[r - rb + 1];
             const int64_t start = a.out_ptr[r];
-            const int64_t seg_g = start + a.pre[e * a.nc + c];
-            const int64_t seg_e = last ? a.out_ptr[r + 1] : start + a.pre[(e + 1) * a.nc + c];
+            const uint2 pe = a.pb[(int64_t)c * a.n_ent + e];
+            const int64_t seg_g = start + pe.x;
+            const int64_t seg_e = last ? a.out_ptr[r + 1] : start + a.pb[(int64_t)c * a.n_ent + e + 1].x;
             const int64_t lo = seg_g > g0 ? seg_g : g0;
             const int64_t hi = seg_e < g1 ? seg_e : g1;
             if (hi > lo) {
-                const int32_t s = a.ent.s[e];
-                src = a.B.rp[a.ent.k[e]] + a.bnd[(int64_t)s * (a.nc + 1) + c] + (lo - seg_g);
+                src = a.ent.b0[e] + pe.y + (lo - seg_g);
                 av = static_cast<const V *>(a.ent.a)[e];
                 loc = (int32_t)(lo - g0);
                 len = (int32_t)(hi - lo);
@@ -808,14 +838,16 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args<CI, V> a) {
 
 }  // namespace
 
-void heavy_entries(const Csr &A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0, const int64_t *a_heavy_ptr,
-                   int64_t nnz_heavy_all, const int32_t *k_to_slice, const RowEntries &ent, hipStream_t s) {
+void heavy_entries(const Csr &A, const Csr &B, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
+                   const int64_t *a_heavy_ptr, int64_t nnz_heavy_all, const int32_t *k_to_slice, const RowEntries &ent,
+                   hipStream_t s) {
     if (n_heavy <= 0 || nnz_heavy_all <= 0) return;
     with_types(A, [&](auto ci, auto v) {
         using CI = decltype(ci);
         using V = decltype(v);
         hipLaunchKernelGGL((k_heavy_entries<CI, V>), dim3(grid_for(nnz_heavy_all, 256, 65536)), dim3(256), 0, s,
-                           typed<CI, V>(A), heavy_rows, n_heavy, r0, a_heavy_ptr, nnz_heavy_all, k_to_slice, ent);
+                           typed<CI, V>(A), B.rp, heavy_rows, n_heavy, r0, a_heavy_ptr, nnz_heavy_all, k_to_slice,
+                           ent);
         GM_CHECK_LAUNCH();
     });
 }
@@ -823,7 +855,7 @@ void heavy_entries(const Csr &A, const int64_t *heavy_rows, int64_t n_heavy, int
 int64_t entry_offset_waves(int64_t n_ent) { return (n_ent + PRE_ENTRIES - 1) / PRE_ENTRIES; }
 
 void entry_offsets(const RowEntries &ent, int64_t n_ent, const int32_t *bnd, int nc, int64_t *agg, int32_t *wfirst,
-                   int32_t *wlast, int64_t *carry, uint32_t *pre, hipStream_t s) {
+                   int32_t *wlast, int64_t *carry, uint2 *pb, hipStream_t s) {
     if (n_ent <= 0) return;
     GM_REQUIRE(nc >= 1 && nc < GM_WAVE, GMAGNUS_ERROR_UNSUPPORTED, "level-0 chunk count must be below 64");
     const int64_t waves = entry_offset_waves(n_ent);
@@ -832,7 +864,7 @@ void entry_offsets(const RowEntries &ent, int64_t n_ent, const int32_t *bnd, int
     GM_CHECK_LAUNCH();
     hipLaunchKernelGGL(k_pre_carry, dim3(nc), dim3(PRE_CARRY_BLOCK), 0, s, agg, wfirst, wlast, waves, nc, carry);
     GM_CHECK_LAUNCH();
-    hipLaunchKernelGGL(k_pre_write, dim3(blocks), dim3(256), 0, s, ent, n_ent, bnd, nc, carry, pre);
+    hipLaunchKernelGGL(k_pre_write, dim3(blocks), dim3(256), 0, s, ent, n_ent, bnd, nc, carry, pb);
     GM_CHECK_LAUNCH();
 }
 
@@ -851,7 +883,7 @@ int64_t rows_tile_words(int64_t total) {
 
 bool rows_next_fits(int next_nc) { return next_nc <= RS_NEXT_MAX; }
 
-void expand_rows(const Csr &B, const RowEntries &ent, const uint32_t *pre, const int32_t *bnd, const int64_t *out_ptr,
+void expand_rows(const Csr &B, const RowEntries &ent, const uint2 *pb, int64_t n_ent, const int64_t *out_ptr,
                  const int64_t *seg_base, const int32_t *reg_c, const int64_t *reg_efirst, const int64_t *reg_ne,
                  int64_t n_out, int64_t n_heavy_out, int64_t total, int nc, int shift, int next_nc, int next_shift,
                  int64_t *next_counts, int64_t *tile_words, int32_t *out_col, void *out_val, hipStream_t s) {
@@ -864,12 +896,12 @@ void expand_rows(const Csr &B, const RowEntries &ent, const uint32_t *pre, const
     GM_REQUIRE(n_tiles < (int64_t)1 << 31, GMAGNUS_ERROR_UNSUPPORTED, "expansion: too many tiles for one panel");
     RsTile *info = (RsTile *)tile_words;
     hipLaunchKernelGGL(k_rs_tiles, dim3(grid_for(n_tiles, 256, 65536)), dim3(256), 0, s, out_ptr, n_out, seg_base,
-                       reg_c, reg_efirst, reg_ne, pre, nc, total, n_tiles, info);
+                       reg_c, reg_efirst, reg_ne, pb, n_ent, total, n_tiles, info);
     GM_CHECK_LAUNCH();
     with_types(B, [&](auto ci, auto v) {
         using CI = decltype(ci);
         using V = decltype(v);
-        RsArgs<CI, V> a{typed<CI, V>(B), ent,        pre,         bnd,         out_ptr, seg_base,
+        RsArgs<CI, V> a{typed<CI, V>(B), ent,        pb,          n_ent,       out_ptr, seg_base,
                         reg_c,           reg_efirst, n_out,       n_heavy_out, total,   n_tiles,
                         info,            nc,         shift,       next_nc,     next_shift, next_counts,
                         out_col,         static_cast<V *>(out_val)};
@@ -928,7 +960,7 @@ bool rows2_fits(int64_t tau, int nc1, int nf) {
     return K <= RS2_KMAX && nf <= FC_MAXF && nc1 >= 1;
 }
 
-void expand_rows2(const Csr &B, const RowEntries &ent, const uint32_t *pre, const int32_t *bnd,
+void expand_rows2(const Csr &B, const RowEntries &ent, const uint2 *pb, int64_t n_ent,
                   const int64_t *out_ptr, const int64_t *seg_base, const int32_t *reg_c, const int64_t *reg_efirst,
                   const int64_t *reg_ne, int64_t n_out, int64_t n_heavy_out, int64_t total, int nc, int shift,
                   int nc1, int shift1, int64_t tau, int64_t *cursor1, int64_t n_out1_elems, int32_t *err,
@@ -944,14 +976,14 @@ void expand_rows2(const Csr &B, const RowEntries &ent, const uint32_t *pre, cons
     GM_REQUIRE(n_tiles < (int64_t)1 << 31, GMAGNUS_ERROR_UNSUPPORTED, "expansion: too many tiles for one panel");
     RsTile *info = (RsTile *)tile_words;
     hipLaunchKernelGGL(k_rs_tiles, dim3(grid_for(n_tiles, 256, 65536)), dim3(256), 0, s, out_ptr, n_out, seg_base,
-                       reg_c, reg_efirst, reg_ne, pre, nc, total, n_tiles, info);
+                       reg_c, reg_efirst, reg_ne, pb, n_ent, total, n_tiles, info);
     GM_CHECK_LAUNCH();
     with_types(B, [&](auto ci, auto v) {
         using CI = decltype(ci);
         using V = decltype(v);
         const int lds = rs2_layout(K, (int)sizeof(V)).total;
         allow_dynamic_lds((const void *)k_expand_rows2<CI, V>, rs2_layout(RS2_KMAX, (int)sizeof(V)).total);
-        Rs2Args<CI, V> a{typed<CI, V>(B), ent,      pre,     bnd,         out_ptr,  seg_base,
+        Rs2Args<CI, V> a{typed<CI, V>(B), ent,      pb,      n_ent,       out_ptr,  seg_base,
                          reg_c,           reg_efirst, n_out, n_heavy_out, total,    n_tiles,
                          info,            nc,       shift,   nc1,         shift1,   R,
                          cursor1,         n_out1_elems, err, out_col0,    static_cast<V *>(out_val0), out_col1,
