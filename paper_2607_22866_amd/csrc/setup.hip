@@ -16,20 +16,59 @@ constexpr int FLAT_ITEMS = 8;  // consecutive entries per thread
 // (the row's column span, used to pick a dense window for light rows).
 // A row split across threads is merged with atomics. Without SPAN only the
 // counts are taken (one B.rp pair per entry, no reads of B's columns).
+// The rows of the work group's entries are found once (two searches of
+// A.rp), their row pointers staged in LDS when they are few, and each thread
+// issues all its loads of one kind together (entries, then B.rp pairs, then
+// the first and last columns) instead of one dependent chain per entry.
+constexpr int RP_ROWS = 1024;  // row pointers a work group stages in LDS
+
 template <bool SPAN, typename CI>
 __global__ __launch_bounds__(FLAT_BLOCK) void k_row_products(CsrV<CI, NoV> A, CsrV<CI, NoV> B, int64_t r0, int64_t r1,
                                                              int64_t *ip, CI *minc, CI *maxc) {
     constexpr CI CI_MAX = sizeof(CI) == 8 ? (CI)INT64_MAX : (CI)INT32_MAX;
+    __shared__ int64_t rp_s[RP_ROWS + 1];
+    __shared__ int64_t rows[2];
     const int64_t e_begin = A.rp[r0], e_end = A.rp[r1];
-    const int64_t e0 = e_begin + (blockIdx.x * (int64_t)FLAT_BLOCK + threadIdx.x) * FLAT_ITEMS;
-    if (e0 >= e_end) return;
-    const int64_t e1 = e0 + FLAT_ITEMS < e_end ? e0 + FLAT_ITEMS : e_end;
-    int64_t row = find_row(A.rp, r0, r1 + 1, e0);
-    int64_t row_end = A.rp[row + 1];
+    const int64_t blk0 = e_begin + blockIdx.x * (int64_t)FLAT_BLOCK * FLAT_ITEMS;
+    const int64_t blk1 = blk0 + (int64_t)FLAT_BLOCK * FLAT_ITEMS < e_end ? blk0 + (int64_t)FLAT_BLOCK * FLAT_ITEMS : e_end;
+    if (threadIdx.x == 0) rows[0] = find_row(A.rp, r0, r1 + 1, blk0);
+    if (threadIdx.x == GM_WAVE) rows[1] = find_row(A.rp, r0, r1 + 1, blk1 - 1);
+    __syncthreads();
+    const int64_t ra = rows[0], rb = rows[1];  // rows of the group's first and last entry
+    const int64_t nr = rb - ra + 1;
+    const bool staged = nr <= RP_ROWS;
+    if (staged)
+        for (int64_t q = threadIdx.x; q <= nr; q += FLAT_BLOCK) rp_s[q] = A.rp[ra + q];
+    __syncthreads();
+    const int64_t e0 = blk0 + (int64_t)threadIdx.x * FLAT_ITEMS;
+    if (e0 >= blk1) return;
+    const int64_t e1 = e0 + FLAT_ITEMS < blk1 ? e0 + FLAT_ITEMS : blk1;
+    const int ne = (int)(e1 - e0);
+    int64_t kk[FLAT_ITEMS], b0[FLAT_ITEMS], b1[FLAT_ITEMS];
+    CI f[FLAT_ITEMS], l[FLAT_ITEMS];
+#pragma unroll
+    for (int i = 0; i < FLAT_ITEMS; ++i) kk[i] = (int64_t)A.ci[i < ne ? e0 + i : e0];
+#pragma unroll
+    for (int i = 0; i < FLAT_ITEMS; ++i) {
+        b0[i] = B.rp[kk[i]];
+        b1[i] = B.rp[kk[i] + 1];
+    }
+    if (SPAN) {
+#pragma unroll
+        for (int i = 0; i < FLAT_ITEMS; ++i) {
+            const bool nonempty = b1[i] > b0[i];  // (an empty B may have no column array)
+            f[i] = nonempty ? B.ci[b0[i]] : (CI)0;
+            l[i] = nonempty ? B.ci[b1[i] - 1] : (CI)0;
+        }
+    }
+    int64_t row = staged ? ra + find_row(rp_s, 0, nr + 1, e0) : find_row(A.rp, ra, rb + 1, e0);
+    int64_t row_end = staged ? rp_s[row - ra + 1] : A.rp[row + 1];
     int64_t acc = 0;
     CI lo = CI_MAX, hi = -1;
-    for (int64_t e = e0; e < e1; ++e) {
-        while (e >= row_end) {  // flush and move to the next nonempty row
+#pragma unroll
+    for (int i = 0; i < FLAT_ITEMS; ++i) {
+        if (i >= ne) break;
+        while (e0 + i >= row_end) {  // flush and move to the next nonempty row
             if (acc) atomicAdd((unsigned long long *)&ip[row - r0], (unsigned long long)acc);
             if (SPAN && hi >= 0) {
                 __hip_atomic_fetch_min(&minc[row - r0], lo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -39,16 +78,13 @@ __global__ __launch_bounds__(FLAT_BLOCK) void k_row_products(CsrV<CI, NoV> A, Cs
             lo = CI_MAX;
             hi = -1;
             ++row;
-            row_end = A.rp[row + 1];
+            row_end = staged ? rp_s[row - ra + 1] : A.rp[row + 1];
         }
-        const int64_t k = (int64_t)A.ci[e];
-        const int64_t b0 = B.rp[k], b1 = B.rp[k + 1];
-        if (b1 > b0) {
-            acc += b1 - b0;
+        if (b1[i] > b0[i]) {
+            acc += b1[i] - b0[i];
             if (SPAN) {
-                const CI f = B.ci[b0], l = B.ci[b1 - 1];
-                lo = f < lo ? f : lo;
-                hi = l > hi ? l : hi;
+                lo = f[i] < lo ? f[i] : lo;
+                hi = l[i] > hi ? l[i] : hi;
             }
         }
     }
