@@ -902,6 +902,59 @@ __global__ __launch_bounds__(BLOCK) void k_light_win_num(CsrV<CI, V> A, CsrV<CI,
     win_emit(D, width, c_row_ptr[r + 1] - dst, base, c_col + dst, c_val + dst, err);
 }
 
+// Narrow-window symbolic from B-row column masks. A light row whose columns
+// span at most WIN0 = 64 uses only B rows that span at most 64 columns, so
+// each such B row k is summarized once by (its first column, a 64-bit mask of
+// its columns relative to that one); the row's distinct columns are then the
+// popcount of the OR of its entries' masks shifted to the row's smallest
+// column: one mask read per A entry instead of one column read per product.
+// Rows of B that are empty or span more than 64 columns get mask 0 (such a
+// row never reaches a narrow-window row of A, except empty ones, which add nothing).
+template <typename CI>
+__global__ void k_brow_masks(CsrV<CI, NoV> B, uint64_t *mask, CI *first) {
+    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < B.n_rows;
+         k += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t b0 = B.rp[k], b1 = B.rp[k + 1];
+        uint64_t m = 0;
+        CI f = 0;
+        if (b1 > b0) {
+            f = B.ci[b0];
+            if ((int64_t)B.ci[b1 - 1] - (int64_t)f < WIN0)
+                for (int64_t j = b0; j < b1; ++j) m |= uint64_t(1) << (int)(B.ci[j] - f);
+        }
+        mask[k] = m;
+        first[k] = f;
+    }
+}
+
+template <typename CI>
+__global__ void k_light_win0_sym_masks(CsrV<CI, NoV> A, int64_t r0, const int64_t *items, int64_t n, const CI *minc,
+                                       const uint64_t *mask, const CI *first, int64_t *row_nnz) {
+    constexpr int U = 8;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t r = items[i];
+        const CI base = minc[r];
+        const int64_t j0 = A.rp[r0 + r], j1 = A.rp[r0 + r + 1];
+        uint64_t acc = 0;
+        for (int64_t jb = j0; jb < j1; jb += U) {
+            int64_t k[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) k[u] = (int64_t)A.ci[jb + u < j1 ? jb + u : j0];
+            uint64_t m[U];
+            CI f[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                m[u] = mask[k[u]];
+                f[u] = first[k[u]];
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                if (jb + u < j1 && m[u]) acc |= m[u] << (int)(f[u] - base);
+        }
+        row_nnz[r] = __popcll(acc);
+    }
+}
+
 // ------------------------------------------------------------------ leaves
 template <int BLOCK, int TS>
 __global__ __launch_bounds__(BLOCK) void k_leaf_hash_sym(LeafSet L, const LeafTask *tasks, int64_t *leaf_nnz,
@@ -1477,6 +1530,26 @@ void leaf_classes_num(const LeafSet &L, const int64_t *leaf_nnz, int64_t tau, in
     if (n <= 0) return;
     hipLaunchKernelGGL(k_leaf_classes, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, L, leaf_nnz, tau, width, cls);
     GM_CHECK_LAUNCH();
+}
+
+int64_t brow_mask_bytes(const Csr &B) { return B.n_rows * (8 + (B.ci64 ? 8 : 4)); }
+
+void light_symbolic_narrow(const Csr &A, const Csr &B, int64_t r0, const int64_t *items, int64_t n,
+                           const void *minc_v, void *masks, int64_t *row_nnz, hipStream_t s) {
+    if (n <= 0) return;
+    with_index_type(B.ci64, [&](auto ci) {
+        using CI = decltype(ci);
+        uint64_t *mask = static_cast<uint64_t *>(masks);
+        CI *first = reinterpret_cast<CI *>(mask + B.n_rows);
+        if (B.n_rows > 0) {
+            hipLaunchKernelGGL(k_brow_masks<CI>, dim3(grid_for(B.n_rows, 256, 65536)), dim3(256), 0, s,
+                               typed<CI, NoV>(B), mask, first);
+            GM_CHECK_LAUNCH();
+        }
+        hipLaunchKernelGGL(k_light_win0_sym_masks<CI>, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s,
+                           typed<CI, NoV>(A), r0, items, n, static_cast<const CI *>(minc_v), mask, first, row_nnz);
+        GM_CHECK_LAUNCH();
+    });
 }
 
 void light_symbolic(const Csr &A, const Csr &B, int64_t r0, int bin, const int64_t *items, int64_t n,

@@ -125,9 +125,13 @@ void fill(T *p, T v, int64_t n, hipStream_t s) {
 // ----------------------------------------------------------------- setup.hip
 // Fills ip/minc/maxc for rows [r0, r1) of A (local index r - r0); with minc
 // and maxc null only ip (no reads of B's columns). minc / maxc hold B's
-// column type (int32 or int64).
+// column type (int32 or int64). binfo (brow_info_bytes(B) of workspace, or
+// null): a per-B-row summary is built there first and read instead of B's
+// row pointers and columns (worth it when the panel has many more A entries
+// than B has rows).
+int64_t brow_info_bytes(const Csr &B);
 void row_products(const Csr &A, const Csr &B, int64_t r0, int64_t r1, int64_t panel_nnz, int64_t *ip, void *minc,
-                  void *maxc, hipStream_t s);
+                  void *maxc, hipStream_t s, void *binfo = nullptr);
 // Checks canonical CSR; sets *flag (device int32) to nonzero on violation.
 void validate_csr(const Csr &M, int32_t *flag, hipStream_t s);
 
@@ -325,6 +329,11 @@ void leaf_numeric(const LeafSet &L, int bin, const LeafTask *tasks, int64_t n, i
                   int slot_width_log2, void *c_val, int32_t *err, int32_t *counter, hipStream_t s);
 // Light rows (local index r): symbolic count into row_nnz[r]; numeric into C.
 // (minc / maxc of B's column type; C's columns and values of A's and B's types)
+// Symbolic of the narrowest window bin (rows spanning at most 64 columns)
+// from per-B-row column masks; masks: brow_mask_bytes(B) of workspace.
+int64_t brow_mask_bytes(const Csr &B);
+void light_symbolic_narrow(const Csr &A, const Csr &B, int64_t r0, const int64_t *items, int64_t n,
+                           const void *minc, void *masks, int64_t *row_nnz, hipStream_t s);
 void light_symbolic(const Csr &A, const Csr &B, int64_t r0, int bin, const int64_t *items, int64_t n,
                     const void *minc, const void *maxc, int64_t *row_nnz, hipStream_t s);
 void light_numeric(const Csr &A, const Csr &B, int64_t r0, int bin, const int64_t *items, int64_t n,

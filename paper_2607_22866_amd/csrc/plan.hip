@@ -640,7 +640,13 @@ void do_plan(gmagnus_plan_s *p, const gmagnus_matrix_t *A, const gmagnus_matrix_
     p->ip = ws.alloc<int64_t>(n);
     p->minc = ws.alloc_bytes(p->csize * n);
     p->maxc = ws.alloc_bytes(p->csize * n);
-    row_products(p->A, p->B, p->r0, p->r1, panel_nnz, p->ip, p->minc, p->maxc, stream);
+    {
+        // many more A entries than B rows: summarize B's rows once (length, first
+        // and last column), one random read per A entry instead of three
+        void *binfo = panel_nnz >= 4 * p->B.n_rows ? ws.alloc_bytes(brow_info_bytes(p->B)) : nullptr;
+        row_products(p->A, p->B, p->r0, p->r1, panel_nnz, p->ip, p->minc, p->maxc, stream, binfo);
+        ws.free(binfo);
+    }
     const bool window = (o.flags & GMAGNUS_FLAG_NO_WINDOW) == 0;
     uint8_t *cls = ws.alloc<uint8_t>(n);
     light_classes_sym(p->ip, p->minc, p->maxc, p->B.ci64, n, p->params.tau, window, cls, stream);
@@ -1242,13 +1248,22 @@ void heavy_symbolic(gmagnus_plan_s *p) {
     // the other buffer (if only level 0 wrote into it, or never used) stays until numeric
 }
 
-void light_symbolic_all(gmagnus_plan_s *p) {
+// (*keep: a workspace block the light stream's kernels still use, freed by the
+// caller after the streams join)
+void light_symbolic_all(gmagnus_plan_s *p, void **keep) {
     const hipStream_t s = p->s_light;
     Timed t(p, GMAGNUS_K_LIGHT_SYM, s);
     double ips = 0;
     for (int b = LIGHT_W0; b < LIGHT_NBINS; ++b) {
         const int64_t cnt = p->bins_sym[b + 1] - p->bins_sym[b];
-        light_symbolic(p->A, p->B, p->r0, b, p->perm + p->bins_sym[b], cnt, p->minc, p->maxc, p->row_nnz, s);
+        if (b == LIGHT_W0 && cnt > 0 && cnt >= p->B.n_rows / 8) {
+            // many narrow rows: summarize B's rows once, then one mask per A entry
+            void *masks = p->ws->alloc_bytes(brow_mask_bytes(p->B));
+            light_symbolic_narrow(p->A, p->B, p->r0, p->perm + p->bins_sym[b], cnt, p->minc, masks, p->row_nnz, s);
+            *keep = masks;
+        } else {
+            light_symbolic(p->A, p->B, p->r0, b, p->perm + p->bins_sym[b], cnt, p->minc, p->maxc, p->row_nnz, s);
+        }
         if (cnt) p->info.kernel_launches[GMAGNUS_K_LIGHT_SYM] += 1;
     }
     ips = (double)(p->products_total - p->products_heavy);
@@ -1285,12 +1300,14 @@ void do_symbolic(gmagnus_plan_s *p, int64_t *c_row_ptr, int64_t *c_nnz) {
     if (p->s_light != p->stream) GM_HIP(hipStreamWaitEvent(p->s_light, fork, 0));
     if (p->s_heavy != p->stream) GM_HIP(hipStreamWaitEvent(p->s_heavy, fork, 0));
     // light work is enqueued first so it overlaps the heavy path's host round trips
-    light_symbolic_all(p);
+    void *light_keep = nullptr;
+    light_symbolic_all(p, &light_keep);
     if (p->n_heavy > 0) heavy_symbolic(p);
     GM_HIP(hipEventRecord(jl, p->s_light));
     GM_HIP(hipEventRecord(jh, p->s_heavy));
     GM_HIP(hipStreamWaitEvent(p->stream, jl, 0));
     GM_HIP(hipStreamWaitEvent(p->stream, jh, 0));
+    ws.free(light_keep);
     {
         Timed t(p, GMAGNUS_K_ROWPTR, p->stream);
         int64_t *sc = ws.alloc<int64_t>(scan_scratch_elems(n));

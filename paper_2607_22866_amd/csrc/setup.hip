@@ -22,8 +22,32 @@ constexpr int FLAT_ITEMS = 8;  // consecutive entries per thread
 // the first and last columns) instead of one dependent chain per entry.
 constexpr int RP_ROWS = 1024;  // row pointers a work group stages in LDS
 
-template <bool SPAN, typename CI>
-__global__ __launch_bounds__(FLAT_BLOCK) void k_row_products(CsrV<CI, NoV> A, CsrV<CI, NoV> B, int64_t r0, int64_t r1,
+// Per-B-row summary (length, first and last column) in one 16-byte record
+// (int32 columns), so that an A entry's B-row facts come from one random read
+// instead of the row pointer pair plus two column reads; built when the
+// panel has many more A entries than B has rows.
+template <typename CI>
+struct BRowInfo {
+    int64_t len;
+    CI first, last;
+};
+
+template <typename CI>
+__global__ void k_brow_info(CsrV<CI, NoV> B, BRowInfo<CI> *info) {
+    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < B.n_rows;
+         k += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t b0 = B.rp[k], b1 = B.rp[k + 1];
+        BRowInfo<CI> r;
+        r.len = b1 - b0;
+        r.first = b1 > b0 ? B.ci[b0] : (CI)0;
+        r.last = b1 > b0 ? B.ci[b1 - 1] : (CI)0;
+        info[k] = r;
+    }
+}
+
+template <bool SPAN, bool INFO, typename CI>
+__global__ __launch_bounds__(FLAT_BLOCK) void k_row_products(CsrV<CI, NoV> A, CsrV<CI, NoV> B,
+                                                             const BRowInfo<CI> *binfo, int64_t r0, int64_t r1,
                                                              int64_t *ip, CI *minc, CI *maxc) {
     constexpr CI CI_MAX = sizeof(CI) == 8 ? (CI)INT64_MAX : (CI)INT32_MAX;
     __shared__ int64_t rp_s[RP_ROWS + 1];
@@ -48,17 +72,28 @@ __global__ __launch_bounds__(FLAT_BLOCK) void k_row_products(CsrV<CI, NoV> A, Cs
     CI f[FLAT_ITEMS], l[FLAT_ITEMS];
 #pragma unroll
     for (int i = 0; i < FLAT_ITEMS; ++i) kk[i] = (int64_t)A.ci[i < ne ? e0 + i : e0];
-#pragma unroll
-    for (int i = 0; i < FLAT_ITEMS; ++i) {
-        b0[i] = B.rp[kk[i]];
-        b1[i] = B.rp[kk[i] + 1];
-    }
-    if (SPAN) {
+    if (INFO) {
 #pragma unroll
         for (int i = 0; i < FLAT_ITEMS; ++i) {
-            const bool nonempty = b1[i] > b0[i];  // (an empty B may have no column array)
-            f[i] = nonempty ? B.ci[b0[i]] : (CI)0;
-            l[i] = nonempty ? B.ci[b1[i] - 1] : (CI)0;
+            const BRowInfo<CI> r = binfo[kk[i]];
+            b0[i] = 0;
+            b1[i] = r.len;
+            f[i] = r.first;
+            l[i] = r.last;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < FLAT_ITEMS; ++i) {
+            b0[i] = B.rp[kk[i]];
+            b1[i] = B.rp[kk[i] + 1];
+        }
+        if (SPAN) {
+#pragma unroll
+            for (int i = 0; i < FLAT_ITEMS; ++i) {
+                const bool nonempty = b1[i] > b0[i];  // (an empty B may have no column array)
+                f[i] = nonempty ? B.ci[b0[i]] : (CI)0;
+                l[i] = nonempty ? B.ci[b1[i] - 1] : (CI)0;
+            }
         }
     }
     int64_t row = staged ? ra + find_row(rp_s, 0, nr + 1, e0) : find_row(A.rp, ra, rb + 1, e0);
@@ -294,8 +329,10 @@ unsigned flat_grid(int64_t total) {
 
 }  // namespace
 
+int64_t brow_info_bytes(const Csr &B) { return B.n_rows * (B.ci64 ? 24 : 16); }
+
 void row_products(const Csr &A, const Csr &B, int64_t r0, int64_t r1, int64_t panel_nnz, int64_t *ip, void *minc,
-                  void *maxc, hipStream_t s) {
+                  void *maxc, hipStream_t s, void *binfo) {
     const int64_t n = r1 - r0;
     if (n <= 0) return;
     fill<int64_t>(ip, 0, n, s);
@@ -307,12 +344,20 @@ void row_products(const Csr &A, const Csr &B, int64_t r0, int64_t r1, int64_t pa
             fill<CI>(mx, (CI)-1, n, s);
         }
         if (panel_nnz <= 0) return;
-        if (mn)
-            hipLaunchKernelGGL((k_row_products<true, CI>), dim3(flat_grid(panel_nnz)), dim3(FLAT_BLOCK), 0, s,
-                               typed<CI, NoV>(A), typed<CI, NoV>(B), r0, r1, ip, mn, mx);
-        else
-            hipLaunchKernelGGL((k_row_products<false, CI>), dim3(flat_grid(panel_nnz)), dim3(FLAT_BLOCK), 0, s,
-                               typed<CI, NoV>(A), typed<CI, NoV>(B), r0, r1, ip, mn, mx);
+        BRowInfo<CI> *bi = static_cast<BRowInfo<CI> *>(binfo);
+        if (mn && bi) {
+            hipLaunchKernelGGL(k_brow_info<CI>, dim3(grid_for(B.n_rows, 256, 65536)), dim3(256), 0, s,
+                               typed<CI, NoV>(B), bi);
+            GM_CHECK_LAUNCH();
+            hipLaunchKernelGGL((k_row_products<true, true, CI>), dim3(flat_grid(panel_nnz)), dim3(FLAT_BLOCK), 0, s,
+                               typed<CI, NoV>(A), typed<CI, NoV>(B), bi, r0, r1, ip, mn, mx);
+        } else if (mn) {
+            hipLaunchKernelGGL((k_row_products<true, false, CI>), dim3(flat_grid(panel_nnz)), dim3(FLAT_BLOCK), 0, s,
+                               typed<CI, NoV>(A), typed<CI, NoV>(B), bi, r0, r1, ip, mn, mx);
+        } else {
+            hipLaunchKernelGGL((k_row_products<false, false, CI>), dim3(flat_grid(panel_nnz)), dim3(FLAT_BLOCK), 0, s,
+                               typed<CI, NoV>(A), typed<CI, NoV>(B), bi, r0, r1, ip, mn, mx);
+        }
         GM_CHECK_LAUNCH();
     });
 }

@@ -186,6 +186,41 @@ def test_banded_window_and_hash(g):
     check(g, W, W)
 
 
+def _drop_rows(A, rows):
+    """A with the given rows emptied (host CSR surgery for edge cases)."""
+    keep = np.ones(A.n_rows, dtype=bool)
+    keep[rows] = False
+    lens = np.diff(A.row_ptr) * keep
+    rp = np.zeros(A.n_rows + 1, dtype=np.int64)
+    rp[1:] = np.cumsum(lens)
+    mask = np.repeat(keep, np.diff(A.row_ptr))
+    return wl.CSR(A.n_rows, A.n_cols, rp, np.ascontiguousarray(A.col[mask]), np.ascontiguousarray(A.val[mask]))
+
+
+def _stack_rows(X, Y):
+    """Rows of X followed by rows of Y (same column count)."""
+    rp = np.concatenate([X.row_ptr, X.row_ptr[-1] + Y.row_ptr[1:]])
+    return wl.CSR(X.n_rows + Y.n_rows, X.n_cols, rp, np.concatenate([X.col, Y.col]), np.concatenate([X.val, Y.val]))
+
+
+def test_narrow_windows(g):
+    # rows spanning at most 64 columns: with many of them the symbolic counts
+    # come from per-B-row column masks, with few from the per-product window;
+    # empty B rows reached from narrow rows add nothing
+    A = _drop_rows(wl.banded(3000, 9, 7), np.arange(100, 400, 3))
+    info = check(g, A, A)
+    assert info.n_heavy_rows == 0
+    B = _drop_rows(wl.banded(3000, 20, 8), np.arange(0, 3000, 5))
+    check(g, A, B)
+    # a few narrow rows among wide ones (fewer than an eighth of B's rows:
+    # the per-product window kernel)
+    Nb = wl.banded(3000, 9, 9)
+    top = wl.CSR(300, 3000, Nb.row_ptr[:301].copy(), Nb.col[:Nb.row_ptr[300]].copy(), Nb.val[:Nb.row_ptr[300]].copy())
+    M = _stack_rows(top, wl.erdos_renyi(3 * 3000, 3000, 12, 10))
+    N = wl.banded(3000, 9, 11)
+    check(g, M, N)
+
+
 def test_erdos_renyi(g):
     A = wl.erdos_renyi(1 << 14, 1 << 14, 16, 5)
     info = check(g, A, A)
