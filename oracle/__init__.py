@@ -14,9 +14,8 @@ Contents
   by column marking, fast enough for whole R-MAT scale-22/23 products.
 - :mod:`oracle.params` -- the parameter selection of Section III-D
   (``GetMagnusParams``), pinned to the chunk counts the paper prints.
-- :mod:`oracle.reference` -- small numpy references for the heavy-row
-  reorder steps (outer-product expansion, one multisplit level), used to pin
-  intermediate semantics on toy inputs.
+- ``golden_structure.py`` -- writes the stored structure digests (nnz(C) and
+  row-pointer hashes) of the large workloads from :func:`row_counts`.
 """
 from __future__ import annotations
 
