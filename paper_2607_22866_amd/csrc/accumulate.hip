@@ -317,7 +317,7 @@ GM_DEV void dense_emit_clear(DenseLds<BLOCK, WMAX, V> &L, int width, int64_t nnz
 // Hash bins: (max elements or nnz, table slots, block).
 constexpr int HS_CAP[4] = {128, 512, 2048, 8192};   // symbolic: elements (load <= 1/2)
 constexpr int HN_CAP[4] = {128, 512, 2048, 7168};   // numeric: distinct columns
-constexpr int WIN0 = 64, WIN1 = 2048;
+constexpr int WIN0 = 64, WIN1 = 2048, WIN2 = 8192;  // window bins: columns spanned
 
 GM_DEV int hash_bin_sym(int64_t n) {
     return n <= HS_CAP[0] ? 0 : n <= HS_CAP[1] ? 1 : n <= HS_CAP[2] ? 2 : 3;
@@ -353,6 +353,7 @@ GM_DEV int window_bin(int64_t ip, int64_t span, bool window) {
     int64_t p2 = 1;
     while (p2 < ip) p2 <<= 1;
     if (span <= WIN1 && span <= 4 * p2) return 1;
+    if (span <= WIN2 && span <= 4 * p2) return 2;  // (a 64 KB value window: rows of at least 2048 products)
     return -1;
 }
 
@@ -1566,6 +1567,9 @@ void light_symbolic(const Csr &A, const Csr &B, int64_t r0, int bin, const int64
         case LIGHT_W1:
             launch_items(k_light_win_sym<256, WIN1, CI>, 256, n, s, a, b, r0, items, minc, maxc, row_nnz);
             break;
+        case LIGHT_W2:
+            launch_items(k_light_win_sym<512, WIN2, CI>, 512, n, s, a, b, r0, items, minc, maxc, row_nnz);
+            break;
         case LIGHT_H0:
             launch_items(k_light_hash_sym<64, 2 * HS_CAP[0], CI>, 64, n, s, a, b, r0, items, minc, row_nnz);
             break;
@@ -1601,6 +1605,10 @@ void light_numeric(const Csr &A, const Csr &B, int64_t r0, int bin, const int64_
             break;
         case LIGHT_W1:
             launch_items(k_light_win_num<256, WIN1, CI, V>, 256, n, s, a, b, r0, items, minc, maxc, c_row_ptr, c_col,
+                         c_val, err);
+            break;
+        case LIGHT_W2:
+            launch_items(k_light_win_num<512, WIN2, CI, V>, 512, n, s, a, b, r0, items, minc, maxc, c_row_ptr, c_col,
                          c_val, err);
             break;
         case LIGHT_H0:

@@ -289,7 +289,7 @@ enum LeafBin : uint8_t {
     LEAF_RANK_T, LEAF_NBINS
 };
 enum LightBin : uint8_t {
-    LIGHT_EMPTY = 0, LIGHT_HEAVY, LIGHT_W0, LIGHT_W1, LIGHT_H0, LIGHT_H1, LIGHT_H2, LIGHT_H3, LIGHT_H4, LIGHT_H5, LIGHT_H6, LIGHT_NBINS
+    LIGHT_EMPTY = 0, LIGHT_HEAVY, LIGHT_W0, LIGHT_W1, LIGHT_W2, LIGHT_H0, LIGHT_H1, LIGHT_H2, LIGHT_H3, LIGHT_H4, LIGHT_H5, LIGHT_H6, LIGHT_NBINS
 };
 // Largest tau the light accumulators can hold.
 int64_t tau_limit();
