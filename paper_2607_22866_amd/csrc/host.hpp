@@ -223,8 +223,8 @@ void expand_rows(const Csr &B, const RowEntries &ent, const uint2 *pb, int64_t n
 // level1_counts: counts of the second level's rows r * nc1 + c1 for the
 // first level's heavy regions (perm: region -> c * n_heavy + h).
 int64_t fine_bounds_words(int64_t n_slices, int nf);
-void fine_bounds(const Csr &B, const int32_t *slice_k, int64_t n_slices, int nf, int fshift, int32_t *bndf,
-                 hipStream_t s);
+void fine_bounds(const Csr &B, const int32_t *slice_k, int64_t n_slices, int nf, int fshift, const int32_t *sbnd,
+                 int nc, int32_t *bndf, hipStream_t s);
 void fine_counts(const Csr &B, const RowEntries &ent, int64_t n_ent, const int32_t *bndf, int nf, int fshift,
                  int64_t n_heavy, int64_t *F, hipStream_t s);
 void level1_counts(const int64_t *perm, int64_t n_regions, int64_t n_heavy, const int64_t *F, int nf, int nc1,

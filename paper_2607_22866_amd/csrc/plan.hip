@@ -1030,7 +1030,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                     Timed t(p, GMAGNUS_K_HISTOGRAM, s);
                     int32_t *bndf = ws.alloc<int32_t>(fine_bounds_words(sl.n_slices, nf));
                     int64_t *F = ws.alloc<int64_t>(nh * nf);
-                    fine_bounds(p->B, sl.slice_k, sl.n_slices, nf, shift1, bndf, s);
+                    fine_bounds(p->B, sl.slice_k, sl.n_slices, nf, shift1, sbnd, nc, bndf, s);
                     fine_counts(p->B, ent, nnz_heavy_all, bndf, nf, shift1, nh, F, s);
                     level1_counts(perm2, nh_out, nh, F, nf, nc1, counts1, s);
                     ws.free(bndf);

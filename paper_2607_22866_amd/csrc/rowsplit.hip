@@ -441,29 +441,42 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows(RsArgs<CI, V> a) {
 // searches the boundaries i, i + 64, ... (PER of them), all its searches
 // stepping together so their loads overlap (a hub row's searches would
 // otherwise be PER dependent chains of about 17 loads each, one after the
-// other).
+// other). Each search starts from its first-level chunk's part of the row
+// (the slice's coarse bounds), about five steps shorter than the whole row.
 constexpr int FB_SHORT = 64;
 
 template <int PER, typename CI>
 __global__ __launch_bounds__(256) void k_fine_bounds(CsrV<CI, NoV> B, const int32_t *slice_k, int64_t n_slices, int nf,
-                                                     int fshift, int32_t *bndf) {
+                                                     int fshift, const int32_t *sbnd, int nc, int32_t *bndf) {
     const int lane = threadIdx.x & (GM_WAVE - 1);
+    const int nc1 = nf / nc;
     const int64_t nwaves = (int64_t)gridDim.x * (blockDim.x / GM_WAVE);
     for (int64_t s = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / GM_WAVE; s < n_slices; s += nwaves) {
         const int32_t k = slice_k[s];
         const int64_t b0 = B.rp[k], len = B.rp[k + 1] - b0;
         if (len <= FB_SHORT) continue;
         int32_t *out = bndf + s * (nf + 1);
+        const int32_t *cb = sbnd + s * (nc + 1);  // the row's first-level chunk bounds
         const CI *row = B.ci + b0;
-        // bit length of len halvings shrink every range to a point
-        const int steps = 64 - __clzll((unsigned long long)len);
         for (int f0 = 0; f0 <= nf; f0 += PER * GM_WAVE) {  // PER boundaries per lane at a time
             int32_t lo[PER], hi[PER];
 #pragma unroll
             for (int j = 0; j < PER; ++j) {
-                lo[j] = 0;
-                hi[j] = f0 + lane + j * GM_WAVE <= nf ? (int32_t)len : 0;  // past nf: empty range
+                const int f = f0 + lane + j * GM_WAVE;
+                // boundary f lies inside its first-level chunk's part of the row
+                const int c = f < nf ? f / nc1 : nc;
+                lo[j] = f <= nf ? cb[c] : 0;
+                hi[j] = f < nf ? cb[c + 1] : lo[j];  // f = nf: the row's end; past nf: empty
             }
+            // bit length of the widest range: that many halvings close every search
+            int32_t rng = 0;
+#pragma unroll
+            for (int j = 0; j < PER; ++j) rng = hi[j] - lo[j] > rng ? hi[j] - lo[j] : rng;
+            for (int d = GM_WAVE / 2; d >= 1; d >>= 1) {
+                const int32_t o = __shfl_xor(rng, d, GM_WAVE);
+                rng = o > rng ? o : rng;
+            }
+            const int steps = 32 - __clz(rng);
             for (int st = 0; st < steps; ++st) {
 #pragma unroll
                 for (int j = 0; j < PER; ++j) {
@@ -913,16 +926,17 @@ void expand_rows(const Csr &B, const RowEntries &ent, const uint2 *pb, int64_t n
 // ------------------------------------------------------------ two levels
 int64_t fine_bounds_words(int64_t n_slices, int nf) { return n_slices * (nf + 1); }
 
-void fine_bounds(const Csr &B, const int32_t *slice_k, int64_t n_slices, int nf, int fshift, int32_t *bndf,
-                 hipStream_t s) {
+void fine_bounds(const Csr &B, const int32_t *slice_k, int64_t n_slices, int nf, int fshift, const int32_t *sbnd,
+                 int nc, int32_t *bndf, hipStream_t s) {
     if (n_slices <= 0) return;
     GM_REQUIRE(nf >= 1 && nf <= FC_MAXF && (int64_t)B.nnz < ((int64_t)1 << 31), GMAGNUS_ERROR_UNSUPPORTED,
                "fine boundaries: too many fine chunks or B too large");
+    GM_REQUIRE(nc >= 1 && nf % nc == 0, GMAGNUS_ERROR_UNSUPPORTED, "fine boundaries: fine chunks must refine the first level");
     // 9 boundaries per lane cover nf = 512 (R-MAT 22's 32 x 16 chunks) in one round
     with_index_type(B.ci64, [&](auto ci) {
         using CI = decltype(ci);
         hipLaunchKernelGGL((k_fine_bounds<9, CI>), dim3(grid_for(n_slices, 4, 65536)), dim3(256), 0, s,
-                           typed<CI, NoV>(B), slice_k, n_slices, nf, fshift, bndf);
+                           typed<CI, NoV>(B), slice_k, n_slices, nf, fshift, sbnd, nc, bndf);
         GM_CHECK_LAUNCH();
     });
 }
