@@ -159,8 +159,12 @@ GM_DEV uint32_t wave_incl_scan_u32(uint32_t x) {
     return x;
 }
 
-__global__ __launch_bounds__(256) void k_pre_write(RowEntries ent, int64_t n_ent, const int32_t *bnd, int nc,
+// (NC > 0: the chunk count fixed at compile time, so a lane's chunk bounds
+// are read once into registers; NC = 0: any count, read per chunk)
+template <int NC>
+__global__ __launch_bounds__(256) void k_pre_write(RowEntries ent, int64_t n_ent, const int32_t *bnd, int nc_rt,
                                                    const int64_t *carry, uint2 *pb) {
+    const int nc = NC > 0 ? NC : nc_rt;
     const int lane = threadIdx.x & (GM_WAVE - 1);
     const int64_t w = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / GM_WAVE;
     const int64_t e0 = w * PRE_ENTRIES;
@@ -181,12 +185,7 @@ __global__ __launch_bounds__(256) void k_pre_write(RowEntries ent, int64_t n_ent
         const uint64_t mine = heads & le_mask;
         const bool cont = mine == 0;  // no row start at or before this lane: the open row continues
         const int seg0 = cont ? 0 : 63 - __clzll((long long)mine);
-        for (int c = 0; c < nc; ++c) {
-            uint32_t lo = 0, size = 0;
-            if (sl >= 0) {
-                lo = (uint32_t)bq[c];
-                size = (uint32_t)bq[c + 1] - lo;
-            }
+        auto chunk = [&](int c, uint32_t lo, uint32_t size) {
             const uint32_t incl = wave_incl_scan_u32(size);
             const uint32_t before = (uint32_t)__shfl((int)incl, seg0 > 0 ? seg0 - 1 : 0, GM_WAVE);
             const uint32_t carry_c = (uint32_t)__builtin_amdgcn_readlane((int)open, c);
@@ -194,6 +193,22 @@ __global__ __launch_bounds__(256) void k_pre_write(RowEntries ent, int64_t n_ent
             if (in) pb[(int64_t)c * n_ent + e] = make_uint2(excl, lo);
             const uint32_t last = (uint32_t)__builtin_amdgcn_readlane((int)(excl + size), cnt - 1);
             if (lane == c) open = last;
+        };
+        if constexpr (NC > 0) {
+            uint32_t bv[NC + 1];
+#pragma unroll
+            for (int c = 0; c <= NC; ++c) bv[c] = sl >= 0 ? (uint32_t)bq[c] : 0u;
+#pragma unroll
+            for (int c = 0; c < NC; ++c) chunk(c, bv[c], bv[c + 1] - bv[c]);
+        } else {
+            for (int c = 0; c < nc; ++c) {
+                uint32_t lo = 0, size = 0;
+                if (sl >= 0) {
+                    lo = (uint32_t)bq[c];
+                    size = (uint32_t)bq[c + 1] - lo;
+                }
+                chunk(c, lo, size);
+            }
         }
         hopen = __builtin_amdgcn_readlane(h, cnt - 1);
     }
@@ -877,7 +892,10 @@ void entry_offsets(const RowEntries &ent, int64_t n_ent, const int32_t *bnd, int
     GM_CHECK_LAUNCH();
     hipLaunchKernelGGL(k_pre_carry, dim3(nc), dim3(PRE_CARRY_BLOCK), 0, s, agg, wfirst, wlast, waves, nc, carry);
     GM_CHECK_LAUNCH();
-    hipLaunchKernelGGL(k_pre_write, dim3(blocks), dim3(256), 0, s, ent, n_ent, bnd, nc, carry, pb);
+    if (nc == 32)
+        hipLaunchKernelGGL(k_pre_write<32>, dim3(blocks), dim3(256), 0, s, ent, n_ent, bnd, nc, carry, pb);
+    else
+        hipLaunchKernelGGL(k_pre_write<0>, dim3(blocks), dim3(256), 0, s, ent, n_ent, bnd, nc, carry, pb);
     GM_CHECK_LAUNCH();
 }
 
