@@ -517,9 +517,9 @@ __global__ __launch_bounds__(256) void k_fine_bounds(CsrV<CI, NoV> B, const int3
 // F[h * nf + f] += fine chunk f's products of heavy row h: each work group
 // takes FC_ENTRIES consecutive row-ordered entries, thread t owns the fine
 // chunks t, t + FC_BLOCK, ... for entries with long B rows (sizes from the
-// fine boundaries), the first wave histograms the columns of short B rows in
-// LDS, and a row's counts are flushed with one atomic per nonzero counter
-// when the row changes.
+// fine boundaries), the waves take turns to histogram the columns of short B
+// rows in LDS, and a row's counts are flushed with one atomic per nonzero
+// counter when the row changes.
 constexpr int FC_BLOCK = 256, FC_ENTRIES = 256, FC_MAXF = 1024;
 
 template <typename CI>
@@ -578,8 +578,9 @@ __global__ __launch_bounds__(FC_BLOCK) void k_fine_counts(CsrV<CI, NoV> B, RowEn
                 const int f = tid + j * FC_BLOCK;
                 if (f < nf) acc[j] += bq[f + 1] - bq[f];
             }
-        } else if (tid < GM_WAVE) {
-            // one lane per element; a run of equal chunks adds its length once
+        } else if (tid / GM_WAVE == (i & (FC_BLOCK / GM_WAVE - 1))) {
+            // short B rows go to the waves in turn; one lane per element, a
+            // run of equal chunks adds its length once
             const int f = lane < len ? (int)(B.ci[eb[i] + lane] >> fshift) : -1;
             const int fp = prev_lane(f, -2);
             const uint64_t starts = ballot(f >= 0 && f != fp);
