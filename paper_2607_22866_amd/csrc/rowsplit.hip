@@ -621,7 +621,7 @@ __host__ __device__ inline Rs2Layout rs2_layout(int K, int vsize) {
     L.val = o;        o += vsize * RS2_SUB;
     L.whist = o;      o += 4 * RS2_NW * K;
     L.key_start = o;  o += 4 * (K + 1);
-    L.col = o;        o += 4 * RS2_SUB;
+    L.col = o;        o += 2 * RS2_SUB;  // final chunks' columns: 16 bits
     L.key = o;        o += 2 * RS2_SUB;
     L.total = (o + 15) & ~15;
     return L;
@@ -656,7 +656,7 @@ struct Rs2Args {
 template <typename CI, typename V>
 __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args<CI, V> a) {
     __shared__ int64_t sb[RS_BLOCK + 2];
-    __shared__ int64_t rn_src[RS_BLOCK];
+    __shared__ int32_t rn_src[RS_BLOCK];  // B position minus tile-local index (B has fewer than 2^31 entries)
     __shared__ V rn_a[RS_BLOCK];
     __shared__ int32_t rn_reg[RS_BLOCK];   // region minus the tile's first region
     __shared__ uint32_t start_bits[RS_WORDS];
@@ -672,7 +672,7 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args<CI, V> a) {
     V *val_buf = (V *)(rs2_smem + Lo.val);
     int32_t *whist = (int32_t *)(rs2_smem + Lo.whist);
     int32_t *key_start = (int32_t *)(rs2_smem + Lo.key_start);
-    int32_t *col_buf = (int32_t *)(rs2_smem + Lo.col);
+    uint16_t *col_buf = (uint16_t *)(rs2_smem + Lo.col);
     uint16_t *key_buf = (uint16_t *)(rs2_smem + Lo.key);
 
     const int tid = threadIdx.x, lane = tid & (GM_WAVE - 1), w = tid / GM_WAVE;
@@ -721,7 +721,7 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args<CI, V> a) {
         int n_ne = 0;
         const int slot = block_excl_scan<RS_BLOCK, int>(len > 0 ? 1 : 0, scan_sm, &n_ne);
         if (len > 0) {
-            rn_src[slot] = src - loc;
+            rn_src[slot] = (int32_t)(src - loc);
             rn_a[slot] = av;
             rn_reg[slot] = reg;
             atomicOr(&start_bits[loc >> 5], 1u << (loc & 31));
@@ -841,7 +841,7 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args<CI, V> a) {
             for (int u = 0; u < RS2_E; ++u) {
                 if (key[u] >= 0) {
                     const int pos = wh[key[u]] + rank[u];
-                    col_buf[pos] = col[u] & mask1;
+                    col_buf[pos] = (uint16_t)(col[u] & mask1);
                     val_buf[pos] = val[u];
                     key_buf[pos] = (uint16_t)key[u];
                 }
@@ -854,7 +854,7 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args<CI, V> a) {
                     atomicOr(a.err, 8);
                     continue;
                 }
-                __builtin_nontemporal_store((uint16_t)col_buf[p], &a.out_col1[d]);
+                __builtin_nontemporal_store(col_buf[p], &a.out_col1[d]);
                 __builtin_nontemporal_store(val_buf[p], &a.out_val1[d]);
             }
             for (int k = tid; k < RS2_NW * K; k += RS_BLOCK) whist[k] = 0;
@@ -1005,6 +1005,8 @@ void expand_rows2(const Csr &B, const RowEntries &ent, const uint2 *pb, int64_t 
     const int R = rows2_regions(tau);
     const int K = R * nc1;
     GM_REQUIRE(K <= RS2_KMAX && K < 65536, GMAGNUS_ERROR_UNSUPPORTED, "two-level expansion: too many keys");
+    GM_REQUIRE((int64_t)B.nnz < ((int64_t)1 << 31), GMAGNUS_ERROR_UNSUPPORTED,
+               "two-level expansion: B positions are kept in 32 bits");
     const int64_t n_tiles = (total + RS_TILE - 1) / RS_TILE;
     GM_REQUIRE(n_tiles < (int64_t)1 << 31, GMAGNUS_ERROR_UNSUPPORTED, "expansion: too many tiles for one panel");
     RsTile *info = (RsTile *)tile_words;
