@@ -160,8 +160,8 @@ enum {
 typedef struct {
     gmagnus_params_t params;
     int64_t n_rows;                /* rows in the panel */
-    int64_t n_heavy_rows;          /* rows with more than tau products */
-    int64_t n_light_rows;          /* rows with 1..tau products */
+    int64_t n_heavy_rows;          /* rows with more than row_tau products */
+    int64_t n_light_rows;          /* rows with 1..row_tau products */
     int64_t products_total;        /* sum of products over the panel's rows */
     int64_t products_heavy;        /* products of heavy rows = nnz of C-hat */
     int64_t n_slices;              /* outer-product slices (columns of the masked A) */
@@ -185,6 +185,10 @@ typedef struct {
     double kernel_ms[GMAGNUS_K_COUNT];
     int64_t kernel_launches[GMAGNUS_K_COUNT];
     double kernel_bytes[GMAGNUS_K_COUNT];
+    /* Light/heavy row threshold: min(tau, 3456). Rows of 3457..tau products
+     * take the heavy path (their chunks are all light); chunks are classified
+     * by tau itself. */
+    int64_t row_tau;
 } gmagnus_plan_info_t;
 
 /* Expansion orders of the heavy rows (Section III-B), as chosen by

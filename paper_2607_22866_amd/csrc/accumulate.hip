@@ -1822,4 +1822,9 @@ int64_t tau_limit() {
     return t < SORT_CAP[2] ? t : SORT_CAP[2];
 }
 
+// Rows of more products take the heavy path even when they are below tau:
+// one 512-thread group per CU sorting up to 6912 products in LDS is slower
+// than expanding and splitting them.
+int64_t light_row_limit() { return SORT_CAP[1]; }
+
 }  // namespace gm

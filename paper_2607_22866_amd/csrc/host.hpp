@@ -293,6 +293,8 @@ enum LightBin : uint8_t {
 };
 // Largest tau the light accumulators can hold.
 int64_t tau_limit();
+// light/heavy row threshold: min(tau, light_row_limit())
+int64_t light_row_limit();
 // (minc / maxc of B's column type: int64 when ci64; a row whose column span
 // does not fit 31 bits is sent to the heavy path)
 void light_classes_sym(const int64_t *ip, const void *minc, const void *maxc, bool ci64, int64_t n, int64_t tau,

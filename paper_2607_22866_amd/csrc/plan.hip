@@ -625,6 +625,7 @@ void do_plan(gmagnus_plan_s *p, const gmagnus_matrix_t *A, const gmagnus_matrix_
     const int64_t n = p->n;
     p->info.n_rows = n;
     p->info.params = p->params;
+    p->info.row_tau = std::min(p->params.tau, light_row_limit());
     if (n == 0) return;
 
     int64_t rp2[2] = {0, 0};
@@ -649,7 +650,7 @@ void do_plan(gmagnus_plan_s *p, const gmagnus_matrix_t *A, const gmagnus_matrix_
     }
     const bool window = (o.flags & GMAGNUS_FLAG_NO_WINDOW) == 0;
     uint8_t *cls = ws.alloc<uint8_t>(n);
-    light_classes_sym(p->ip, p->minc, p->maxc, p->B.ci64, n, p->params.tau, window, cls, stream);
+    light_classes_sym(p->ip, p->minc, p->maxc, p->B.ci64, n, p->info.row_tau, window, cls, stream);
     p->perm = ws.alloc<int64_t>(n);
     int64_t *bins = ws.alloc<int64_t>(LIGHT_NBINS + 1);
     int64_t *scratch = ws.alloc<int64_t>(std::max(partition_scratch_elems(n, LIGHT_NBINS), scan_scratch_elems(n)));
@@ -1333,7 +1334,8 @@ void do_symbolic(gmagnus_plan_s *p, int64_t *c_row_ptr, int64_t *c_nnz) {
         int64_t *bins = ws.alloc<int64_t>(LIGHT_NBINS + 1);
         int64_t *sc = ws.alloc<int64_t>(partition_scratch_elems(n, LIGHT_NBINS));
         p->perm_num = ws.alloc<int64_t>(n);
-        light_classes_num(p->ip, p->row_nnz, p->minc, p->maxc, p->B.ci64, n, p->params.tau, window, cls, p->stream);
+        light_classes_num(p->ip, p->row_nnz, p->minc, p->maxc, p->B.ci64, n, p->info.row_tau, window, cls,
+                          p->stream);
         partition_u8(cls, n, LIGHT_NBINS, p->perm_num, nullptr, bins, sc, p->stream);
         read_bins(bins, LIGHT_NBINS, p->bins_num, p->stream);
         ws.free(cls);

@@ -89,7 +89,7 @@ class PlanInfo(ctypes.Structure):
                 ("expansion_path", ctypes.c_int32), ("workspace_peak_bytes", ctypes.c_int64),
                 ("index_type", ctypes.c_int32), ("value_type", ctypes.c_int32),
                 ("kernel_ms", ctypes.c_double * len(K_NAMES)), ("kernel_launches", ctypes.c_int64 * len(K_NAMES)),
-                ("kernel_bytes", ctypes.c_double * len(K_NAMES))]
+                ("kernel_bytes", ctypes.c_double * len(K_NAMES)), ("row_tau", ctypes.c_int64)]
 
     def to_dict(self) -> dict:
         d = {f: getattr(self, f) for f, _ in self._fields_ if f not in (

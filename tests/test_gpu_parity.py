@@ -64,10 +64,13 @@ def test_rmat12_every_depth(g, opts, levels):
     info = check(g, A, A, **opts)
     assert info.params.levels == levels
     ip = oracle.row_products(A, A)
+    # rows are heavy above min(tau, 3456) products (the light accumulators'
+    # efficient range); chunks are classified by tau
     tau = info.params.tau
-    assert info.n_heavy_rows == int((ip > tau).sum())
+    assert info.row_tau == min(tau, 3456)
+    assert info.n_heavy_rows == int((ip > info.row_tau).sum())
     assert info.products_total == int(ip.sum())
-    assert info.products_heavy == int(ip[ip > tau].sum())
+    assert info.products_heavy == int(ip[ip > info.row_tau].sum())
     if levels:
         assert info.levels_run >= 1
 
