@@ -32,6 +32,15 @@ DeviceCache &cache() {
 
 size_t round_bytes(size_t b) {
     if (b < ((size_t)1 << 20)) return (b + 255) & ~(size_t)255;
+    if (b >= ((size_t)1 << 30)) {
+        // eight size classes per power of two: row panels of slightly
+        // different sizes then ask for the same block, which the cache hands
+        // back, instead of a fresh hipMalloc of tens of GB (about a second)
+        size_t top = (size_t)1 << 30;
+        while (top * 2 <= b) top *= 2;
+        const size_t step = top / 8;
+        return (b + step - 1) / step * step;
+    }
     const size_t g = (size_t)2 << 20;
     return (b + g - 1) / g * g;
 }
