@@ -74,10 +74,45 @@ __global__ __launch_bounds__(SCAN_BLOCK) void k_scan_apply(In in, int64_t n, con
     if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) out[n] = partial[gridDim.x];
 }
 
+// Small inputs: one work group walks the array in pieces of 8192 with a
+// running carry (one launch instead of three; launches dominate below ~64K).
+constexpr int SCAN1_BLOCK = 1024;
+constexpr int64_t SCAN1_MAX = 65536;
+
+template <class In>
+__global__ __launch_bounds__(SCAN1_BLOCK) void k_scan_single(In in, int64_t n, int64_t *out) {
+    __shared__ int64_t sm[SCAN1_BLOCK / GM_WAVE];
+    int64_t carry = 0;
+    for (int64_t b0 = 0; b0 < n; b0 += (int64_t)SCAN1_BLOCK * SCAN_ITEMS) {
+        const int64_t base = b0 + threadIdx.x * SCAN_ITEMS;
+        int64_t v[SCAN_ITEMS];
+        int64_t sum = 0;
+#pragma unroll
+        for (int j = 0; j < SCAN_ITEMS; ++j) {
+            v[j] = base + j < n ? in(base + j) : 0;
+            sum += v[j];
+        }
+        int64_t tot;
+        int64_t run = carry + block_excl_scan<SCAN1_BLOCK>(sum, sm, &tot);
+#pragma unroll
+        for (int j = 0; j < SCAN_ITEMS; ++j) {
+            if (base + j < n) out[base + j] = run;
+            run += v[j];
+        }
+        carry += tot;
+    }
+    if (threadIdx.x == 0) out[n] = carry;
+}
+
 template <class In>
 void scan_impl(In in, int64_t n, int64_t *out, int64_t *scratch, hipStream_t s) {
     if (n <= 0) {
         fill<int64_t>(out, 0, 1, s);
+        return;
+    }
+    if (n <= SCAN1_MAX) {
+        hipLaunchKernelGGL(k_scan_single<In>, dim3(1), dim3(SCAN1_BLOCK), 0, s, in, n, out);
+        GM_CHECK_LAUNCH();
         return;
     }
     const int64_t tiles = (n + SCAN_TILE - 1) / SCAN_TILE;
@@ -111,16 +146,14 @@ __global__ __launch_bounds__(PART_BLOCK) void k_part_count(const uint8_t *cls, i
 
 // Each thread owns PART_ITEMS consecutive items; per-class counts of the
 // threads are scanned in thread order (four 16-bit class counters per int64
-// word), so positions are stable in item order.
-__global__ __launch_bounds__(PART_BLOCK) void k_part_scatter(const uint8_t *cls, int64_t n, int nc, int64_t n_tiles,
-                                                             const int64_t *tile_off, int64_t *perm, int64_t *inv) {
-    __shared__ int64_t sm[PART_BLOCK / GM_WAVE];
-    __shared__ int64_t base_off[PART_MAX_CLASSES];
-    const int64_t base = blockIdx.x * PART_TILE + (int64_t)threadIdx.x * PART_ITEMS;
+// word), so positions are stable in item order. base_off[c]: position of the
+// tile's first item of class c.
+GM_DEV void part_tile_scatter(const uint8_t *cls, int64_t n, int nc, int64_t tile, const int64_t *base_off,
+                              int64_t *sm, int64_t *perm, int64_t *inv) {
+    const int64_t base = tile * PART_TILE + (int64_t)threadIdx.x * PART_ITEMS;
     uint8_t c[PART_ITEMS];
 #pragma unroll
     for (int j = 0; j < PART_ITEMS; ++j) c[j] = base + j < n ? cls[base + j] : 0xFF;
-    if (threadIdx.x < nc) base_off[threadIdx.x] = tile_off[threadIdx.x * n_tiles + blockIdx.x];
     int prefix[PART_MAX_CLASSES];
 #pragma unroll
     for (int g = 0; g < PART_MAX_CLASSES / 4; ++g) {
@@ -159,6 +192,48 @@ __global__ __launch_bounds__(PART_BLOCK) void k_part_scatter(const uint8_t *cls,
     }
 }
 
+__global__ __launch_bounds__(PART_BLOCK) void k_part_scatter(const uint8_t *cls, int64_t n, int nc, int64_t n_tiles,
+                                                             const int64_t *tile_off, int64_t *perm, int64_t *inv) {
+    __shared__ int64_t sm[PART_BLOCK / GM_WAVE];
+    __shared__ int64_t base_off[PART_MAX_CLASSES];
+    if (threadIdx.x < nc) base_off[threadIdx.x] = tile_off[threadIdx.x * n_tiles + blockIdx.x];
+    part_tile_scatter(cls, n, nc, blockIdx.x, base_off, sm, perm, inv);
+}
+
+// Small inputs: one work group counts the classes, then scatters tile by tile
+// with running per-class offsets (one launch instead of six).
+constexpr int64_t PART1_MAX = 65536;
+
+__global__ __launch_bounds__(PART_BLOCK) void k_part_single(const uint8_t *cls, int64_t n, int nc, int64_t *perm,
+                                                            int64_t *inv, int64_t *class_start) {
+    __shared__ int64_t sm[PART_BLOCK / GM_WAVE];
+    __shared__ int cnt[PART_MAX_CLASSES];
+    __shared__ int64_t off[PART_MAX_CLASSES + 1];
+    if (threadIdx.x < PART_MAX_CLASSES) cnt[threadIdx.x] = 0;
+    __syncthreads();
+    for (int64_t i = threadIdx.x; i < n; i += PART_BLOCK) atomicAdd(&cnt[cls[i]], 1);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        off[0] = 0;
+        for (int c = 0; c < nc; ++c) off[c + 1] = off[c] + cnt[c];
+        for (int c = 0; c <= nc; ++c) class_start[c] = off[c];
+    }
+    __syncthreads();
+    const int64_t tiles = (n + PART_TILE - 1) / PART_TILE;
+    for (int64_t t = 0; t < tiles; ++t) {
+        part_tile_scatter(cls, n, nc, t, off, sm, perm, inv);
+        __syncthreads();
+        // advance every class offset by this tile's count of it
+        if (threadIdx.x < PART_MAX_CLASSES) cnt[threadIdx.x] = 0;
+        __syncthreads();
+        for (int64_t i = t * PART_TILE + threadIdx.x; i < n && i < (t + 1) * PART_TILE; i += PART_BLOCK)
+            atomicAdd(&cnt[cls[i]], 1);
+        __syncthreads();
+        if (threadIdx.x < nc) off[threadIdx.x] += cnt[threadIdx.x];
+        __syncthreads();
+    }
+}
+
 __global__ void k_class_starts(const int64_t *tile_off, int nc, int64_t n_tiles, int64_t *class_start) {
     const int c = threadIdx.x;
     if (c <= nc) class_start[c] = tile_off[(int64_t)c * n_tiles];
@@ -189,6 +264,11 @@ void partition_u8(const uint8_t *cls, int64_t n, int nc, int64_t *perm, int64_t 
     const int64_t tiles = (n + PART_TILE - 1) / PART_TILE;
     if (n <= 0) {
         fill<int64_t>(class_start, 0, nc + 1, s);
+        return;
+    }
+    if (n <= PART1_MAX) {
+        hipLaunchKernelGGL(k_part_single, dim3(1), dim3(PART_BLOCK), 0, s, cls, n, nc, perm, inv, class_start);
+        GM_CHECK_LAUNCH();
         return;
     }
     const int64_t m = tiles * nc;
