@@ -139,6 +139,20 @@ def measured_peaks(g):
     return out
 
 
+def cache_probe(g):
+    """Rate of random 128-byte line reads (the expansion's B-row gathers)
+    against the size of the working set they fall in, GB/s: sizes the L2s
+    (4 MB per XCD) hold run far above HBM, larger ones at the memory side's
+    rate."""
+    import torch
+
+    out = {}
+    for log2 in range(21, 33):
+        out["%d MiB" % (1 << (log2 - 20))] = g.bandwidth_probe("gather", nbytes=1 << log2, reps=3)
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_description():
     """Model name of the host CPU and the logical CPUs this process may use."""
     model = "unknown"
@@ -242,6 +256,9 @@ def main():
     ap.add_argument("--pattern-reuse", action="store_true",
                     help="after the timed steps, also time one values-only re-run per panel (new values of A "
                          "and B on the kept patterns) against the full product on the same plans")
+    ap.add_argument("--cache-probe", action="store_true",
+                    help="also report the rate of random 128-byte line reads against the working-set size "
+                         "(2 MiB .. 4 GiB)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: it measures the single-GPU hot path "
@@ -374,6 +391,8 @@ def main():
                                 "speedup": t_full / t_vals,
                                 "note": "panel by panel, synchronised around each phase; full = plan + symbolic + "
                                         "numeric with the pattern kept, values only = gmagnus_update_values + numeric"}
+    if args.cache_probe:
+        out["cache_probe_gbs"] = cache_probe(g)
     if not args.no_cpu_baseline:
         ip = g.row_products(dA, dB).cpu().numpy()
         log("timing the oracle on a sample of about %.2g products" % args.cpu_products)

@@ -356,6 +356,11 @@ gmagnus_status_t gmagnus_split_panels_typed(const gmagnus_matrix_t *A, const gma
  *                   sum to -1
  *   WRITE, WRITE_NT write dst (ordinary / nontemporal stores)
  *   COPY            copy src to dst (bytes read plus bytes written moved)
+ *   GATHER          read 4 GiB as random 128-byte lines of the first `bytes`
+ *                   bytes of src (a power of two, 4 KiB .. 128 GiB; grid is
+ *                   ignored): the rate of line gathers from a working set of
+ *                   that size, i.e. what the caches in front of HBM serve;
+ *                   dst is a sink as for READ
  * src and dst are device pointers, 16-byte aligned, of `bytes` bytes (dst: 8
  * bytes for the read kinds). Synchronises the stream.
  * Errors: INVALID_VALUE (kind, sizes, alignment, NULL), HIP. */
@@ -364,7 +369,8 @@ enum {
     GMAGNUS_PROBE_READ_NT = 1,
     GMAGNUS_PROBE_WRITE = 2,
     GMAGNUS_PROBE_WRITE_NT = 3,
-    GMAGNUS_PROBE_COPY = 4
+    GMAGNUS_PROBE_COPY = 4,
+    GMAGNUS_PROBE_GATHER = 5
 };
 gmagnus_status_t gmagnus_bandwidth_probe(int32_t kind, void *dst, const void *src, int64_t bytes, int32_t grid,
                                          int32_t reps, void *hip_stream, double *ms);

@@ -2,7 +2,10 @@
 // speed-of-light figures divide by (Section IV-C measures it with a copy
 // kernel). Grid-stride loops over 16-byte elements, each wave touching
 // 1 KiB of consecutive memory per access; variants for ordinary and
-// nontemporal loads and stores.
+// nontemporal loads and stores. A gather variant reads random 128-byte lines
+// of a working set of a given size, the access of the expansion's B-row
+// gathers, so its rate against the working-set size shows which sizes the
+// L2s (4 MB per XCD) and the Infinity Cache serve faster than HBM.
 #include "host.hpp"
 
 namespace gm {
@@ -45,6 +48,32 @@ __global__ __launch_bounds__(PROBE_BLOCK) void k_probe_write_nt(V2 *__restrict__
     }
 }
 
+// Each group of 8 lanes reads one random line of the working set (16 bytes a
+// lane), four lines in flight per lane; xorshift32 line indices (the 8 lanes
+// of a group share the generator, so they read the same line).
+constexpr unsigned GATHER_GRID = 2048;
+constexpr int GATHER_ITERS = 512;  // 2048 groups x 256 lanes x 512 x 16 B = 4 GiB per run
+
+__global__ __launch_bounds__(PROBE_BLOCK) void k_probe_gather(const V2 *__restrict__ a, uint32_t lines_mask,
+                                                              double *sink) {
+    const int lane = threadIdx.x & 7;
+    uint32_t x = ((blockIdx.x * PROBE_BLOCK + threadIdx.x) >> 3) * 2654435761u + 0x9E3779B9u;
+    double s = 0.0;
+    for (int it = 0; it < GATHER_ITERS; it += 4) {
+        V2 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            x ^= x << 13;
+            x ^= x >> 17;
+            x ^= x << 5;
+            v[u] = a[(uint64_t)(x & lines_mask) * 8 + lane];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) s += v[u].x + v[u].y;
+    }
+    if (s == -1.0) sink[0] = s;
+}
+
 __global__ __launch_bounds__(PROBE_BLOCK) void k_probe_copy(const V2 *__restrict__ a, V2 *__restrict__ b, int64_t n) {
     for (int64_t i = blockIdx.x * (int64_t)PROBE_BLOCK + threadIdx.x; i < n; i += (int64_t)gridDim.x * PROBE_BLOCK)
         b[i] = a[i];
@@ -58,12 +87,15 @@ using namespace gm;
 extern "C" gmagnus_status_t gmagnus_bandwidth_probe(int32_t kind, void *dst, const void *src, int64_t bytes,
                                                     int32_t grid, int32_t reps, void *hip_stream, double *ms) {
     try {
-        GM_REQUIRE(kind >= GMAGNUS_PROBE_READ && kind <= GMAGNUS_PROBE_COPY, GMAGNUS_ERROR_INVALID_VALUE,
+        GM_REQUIRE(kind >= GMAGNUS_PROBE_READ && kind <= GMAGNUS_PROBE_GATHER, GMAGNUS_ERROR_INVALID_VALUE,
                    "unknown probe kind");
+        GM_REQUIRE(kind != GMAGNUS_PROBE_GATHER ||
+                       (bytes >= 4096 && bytes <= ((int64_t)1 << 37) && (bytes & (bytes - 1)) == 0),
+                   GMAGNUS_ERROR_INVALID_VALUE, "gather probe: the working set must be a power of two, 4 KiB .. 128 GiB");
         GM_REQUIRE(ms != nullptr && reps >= 1 && bytes >= 16 && bytes % 16 == 0, GMAGNUS_ERROR_INVALID_VALUE,
                    "probe: bytes must be a positive multiple of 16, reps >= 1, ms not NULL");
         const bool reads = kind != GMAGNUS_PROBE_WRITE && kind != GMAGNUS_PROBE_WRITE_NT;
-        const bool writes = kind != GMAGNUS_PROBE_READ && kind != GMAGNUS_PROBE_READ_NT;
+        const bool writes = kind != GMAGNUS_PROBE_READ && kind != GMAGNUS_PROBE_READ_NT && kind != GMAGNUS_PROBE_GATHER;
         GM_REQUIRE((!reads || src) && dst, GMAGNUS_ERROR_INVALID_VALUE, "probe: NULL buffer");
         GM_REQUIRE(((uintptr_t)dst % 16) == 0 && ((uintptr_t)src % 16) == 0, GMAGNUS_ERROR_INVALID_VALUE,
                    "probe: buffers must be 16-byte aligned");
@@ -96,6 +128,10 @@ extern "C" gmagnus_status_t gmagnus_bandwidth_probe(int32_t kind, void *dst, con
                 break;
             case GMAGNUS_PROBE_WRITE_NT:
                 hipLaunchKernelGGL(k_probe_write_nt, dim3(g), dim3(PROBE_BLOCK), 0, s, (V2 *)dst, n);
+                break;
+            case GMAGNUS_PROBE_GATHER:
+                hipLaunchKernelGGL(k_probe_gather, dim3(GATHER_GRID), dim3(PROBE_BLOCK), 0, s, (const V2 *)src,
+                                   (uint32_t)(bytes / 128 - 1), (double *)dst);
                 break;
             default:
                 hipLaunchKernelGGL(k_probe_copy, dim3(g), dim3(PROBE_BLOCK), 0, s, (const V2 *)src, (V2 *)dst, n);

@@ -392,21 +392,23 @@ def split_panels(A: DeviceCSR, B: DeviceCSR, max_products: int, max_panels: int 
     return [int(bounds[i]) for i in range(n.value + 1)]
 
 
-PROBE_KINDS = {"read": 0, "read_nt": 1, "write": 2, "write_nt": 3, "copy": 4}
+PROBE_KINDS = {"read": 0, "read_nt": 1, "write": 2, "write_nt": 3, "copy": 4, "gather": 5}
+GATHER_PROBE_BYTES = 4 << 30  # bytes one gather probe run reads
 
 
 def bandwidth_probe(kind: str, nbytes: int = 4 << 30, reps: int = 5, grid: int = 0, stream=None) -> float:
-    """Streaming bandwidth of one probe kernel in GB/s (bytes moved / time; a
-    copy moves its bytes twice)."""
+    """Bandwidth of one probe kernel in GB/s (bytes moved / time; a copy moves
+    its bytes twice; "gather" reads GATHER_PROBE_BYTES as random lines of a
+    working set of nbytes bytes)."""
     k = PROBE_KINDS[kind]
     src = torch.ones(nbytes // 8, dtype=torch.float64, device="cuda")
-    dst = torch.empty_like(src) if kind not in ("read", "read_nt") else torch.zeros(1, dtype=torch.float64,
-                                                                                 device="cuda")
+    dst = torch.empty_like(src) if kind not in ("read", "read_nt", "gather") else torch.zeros(
+        1, dtype=torch.float64, device="cuda")
     ms = ctypes.c_double()
     _check(load().gmagnus_bandwidth_probe(k, dst.data_ptr(), src.data_ptr(), nbytes, grid, reps, _stream(stream),
                                           ctypes.byref(ms)))
     del src, dst
-    moved = 2 * nbytes if kind == "copy" else nbytes
+    moved = 2 * nbytes if kind == "copy" else GATHER_PROBE_BYTES if kind == "gather" else nbytes
     return moved / (ms.value / 1000.0) / 1e9
 
 

@@ -532,7 +532,7 @@ def test_timed_classes_fit_in_wall_time(g):
     assert info.kernel_ms[2] > 0 and info.kernel_ms[6] > 0
 
 
-@pytest.mark.parametrize("kind", ["read", "read_nt", "write", "write_nt", "copy"])
+@pytest.mark.parametrize("kind", ["read", "read_nt", "write", "write_nt", "copy", "gather"])
 def test_bandwidth_probe(g, kind):
     import ctypes
 
@@ -552,3 +552,7 @@ def test_bandwidth_probe(g, kind):
     else:
         assert torch.equal(dst, torch.full((n,), -7.0, dtype=torch.float64, device="cuda"))  # sink untouched
     assert 10.0 < g.bandwidth_probe(kind, nbytes=1 << 28) < 20000.0
+    if kind == "gather":  # the working set must be a power of two
+        st = g.load().gmagnus_bandwidth_probe(g.PROBE_KINDS[kind], dst.data_ptr(), src.data_ptr(), 3 << 20, 0, 1,
+                                              torch.cuda.current_stream().cuda_stream, ctypes.byref(ms))
+        assert st == 1
