@@ -75,9 +75,10 @@ __global__ __launch_bounds__(SCAN_BLOCK) void k_scan_apply(In in, int64_t n, con
 }
 
 // Small inputs: one work group walks the array in pieces of 8192 with a
-// running carry (one launch instead of three; launches dominate below ~64K).
+// running carry (one launch instead of three; below ~16K items the launches
+// cost more than the work).
 constexpr int SCAN1_BLOCK = 1024;
-constexpr int64_t SCAN1_MAX = 65536;
+constexpr int64_t SCAN1_MAX = 16384;
 
 template <class In>
 __global__ __launch_bounds__(SCAN1_BLOCK) void k_scan_single(In in, int64_t n, int64_t *out) {
@@ -149,7 +150,7 @@ __global__ __launch_bounds__(PART_BLOCK) void k_part_count(const uint8_t *cls, i
 // word), so positions are stable in item order. base_off[c]: position of the
 // tile's first item of class c.
 GM_DEV void part_tile_scatter(const uint8_t *cls, int64_t n, int nc, int64_t tile, const int64_t *base_off,
-                              int64_t *sm, int64_t *perm, int64_t *inv) {
+                              int64_t *sm, int64_t *perm, int64_t *inv, int64_t *tile_tot = nullptr) {
     const int64_t base = tile * PART_TILE + (int64_t)threadIdx.x * PART_ITEMS;
     uint8_t c[PART_ITEMS];
 #pragma unroll
@@ -168,9 +169,11 @@ GM_DEV void part_tile_scatter(const uint8_t *cls, int64_t n, int nc, int64_t til
             const int q = (int)c[j] - 4 * g;
             if (c[j] != 0xFF && q >= 0 && q < 4) packed += uint64_t(1) << (16 * q);
         }
-        const uint64_t ex = (uint64_t)block_excl_scan<PART_BLOCK>((int64_t)packed, sm);
+        int64_t tot = 0;
+        const uint64_t ex = (uint64_t)block_excl_scan<PART_BLOCK>((int64_t)packed, sm, &tot);
 #pragma unroll
         for (int q = 0; q < 4; ++q) prefix[4 * g + q] = (int)((ex >> (16 * q)) & 0xFFFF);
+        if (tile_tot && threadIdx.x < 4) tile_tot[4 * g + threadIdx.x] = ((uint64_t)tot >> (16 * threadIdx.x)) & 0xFFFF;
     }
     __syncthreads();
     int run[PART_MAX_CLASSES];
@@ -202,34 +205,43 @@ __global__ __launch_bounds__(PART_BLOCK) void k_part_scatter(const uint8_t *cls,
 
 // Small inputs: one work group counts the classes, then scatters tile by tile
 // with running per-class offsets (one launch instead of six).
-constexpr int64_t PART1_MAX = 65536;
+constexpr int64_t PART1_MAX = 16384;
 
 __global__ __launch_bounds__(PART_BLOCK) void k_part_single(const uint8_t *cls, int64_t n, int nc, int64_t *perm,
                                                             int64_t *inv, int64_t *class_start) {
     __shared__ int64_t sm[PART_BLOCK / GM_WAVE];
-    __shared__ int cnt[PART_MAX_CLASSES];
     __shared__ int64_t off[PART_MAX_CLASSES + 1];
-    if (threadIdx.x < PART_MAX_CLASSES) cnt[threadIdx.x] = 0;
-    __syncthreads();
-    for (int64_t i = threadIdx.x; i < n; i += PART_BLOCK) atomicAdd(&cnt[cls[i]], 1);
+    __shared__ int64_t tile_tot[PART_MAX_CLASSES];
+    // class counts in one pass: per thread two 32-bit counters per int64 word
+    // (no LDS atomics: a few classes would serialise them)
+    constexpr int NG = PART_MAX_CLASSES / 2;
+    uint64_t packed[NG];
+#pragma unroll
+    for (int g = 0; g < NG; ++g) packed[g] = 0;
+    for (int64_t i = threadIdx.x; i < n; i += PART_BLOCK) {
+        const int c = cls[i];
+#pragma unroll
+        for (int g = 0; g < NG; ++g) packed[g] += (c >> 1) == g ? uint64_t(1) << (32 * (c & 1)) : 0;
+    }
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+        if (2 * g >= nc) break;  // nc is uniform over the block
+        const int64_t tot = block_reduce_sum<PART_BLOCK>((int64_t)packed[g], sm);
+        if (threadIdx.x < 2 && 2 * g + (int)threadIdx.x < nc)
+            off[2 * g + threadIdx.x + 1] = ((uint64_t)tot >> (32 * threadIdx.x)) & 0xFFFFFFFFu;
+    }
     __syncthreads();
     if (threadIdx.x == 0) {
         off[0] = 0;
-        for (int c = 0; c < nc; ++c) off[c + 1] = off[c] + cnt[c];
+        for (int c = 0; c < nc; ++c) off[c + 1] += off[c];
         for (int c = 0; c <= nc; ++c) class_start[c] = off[c];
     }
     __syncthreads();
     const int64_t tiles = (n + PART_TILE - 1) / PART_TILE;
     for (int64_t t = 0; t < tiles; ++t) {
-        part_tile_scatter(cls, n, nc, t, off, sm, perm, inv);
+        part_tile_scatter(cls, n, nc, t, off, sm, perm, inv, tile_tot);
         __syncthreads();
-        // advance every class offset by this tile's count of it
-        if (threadIdx.x < PART_MAX_CLASSES) cnt[threadIdx.x] = 0;
-        __syncthreads();
-        for (int64_t i = t * PART_TILE + threadIdx.x; i < n && i < (t + 1) * PART_TILE; i += PART_BLOCK)
-            atomicAdd(&cnt[cls[i]], 1);
-        __syncthreads();
-        if (threadIdx.x < nc) off[threadIdx.x] += cnt[threadIdx.x];
+        if (threadIdx.x < nc) off[threadIdx.x] += tile_tot[threadIdx.x];  // running offsets past this tile
         __syncthreads();
     }
 }
