@@ -538,6 +538,22 @@ __global__ void k_affine(int64_t *p, int64_t n, int64_t a) {
 // so a panel takes about log_256(n) steps. out[0] = the panel count (-1 when
 // max_panels do not reach row n); out[1 + i] = bound i.
 constexpr int SPLIT_BLOCK = 256;
+
+// *out = the longest row of a CSR row-pointer array (out zeroed before)
+__global__ __launch_bounds__(256) void k_max_row_len(const int64_t *rp, int64_t n_rows, unsigned long long *out) {
+    int64_t m = 0;
+    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < n_rows; k += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t len = rp[k + 1] - rp[k];
+        m = len > m ? len : m;
+    }
+#pragma unroll
+    for (int d = GM_WAVE / 2; d >= 1; d >>= 1) {
+        const int64_t o = __shfl_xor(m, d, GM_WAVE);
+        m = o > m ? o : m;
+    }
+    if ((threadIdx.x & (GM_WAVE - 1)) == 0 && m > 0) atomicMax(out, (unsigned long long)m);
+}
+
 __global__ __launch_bounds__(SPLIT_BLOCK) void k_split_panels(const int64_t *pre, int64_t n, int64_t max_products,
                                                               int64_t max_panels, int64_t *out) {
     __shared__ int best;
@@ -1664,6 +1680,22 @@ gmagnus_status_t gmagnus_split_panels_typed(const gmagnus_matrix_t *A, const gma
         *n_panels = 0;
         if (n == 0) return;
         Workspace ws(nullptr, s);
+        {
+            // no row can have more products than its A entries times B's longest
+            // row: when nnz(A) times that stays within the limit, the whole
+            // matrix is one panel and the row products need not be formed
+            int64_t *mx = ws.alloc<int64_t>(1);
+            fill<int64_t>(mx, 0, 1, s);
+            hipLaunchKernelGGL(k_max_row_len, dim3(grid_for(B->n_rows, 256, 4096)), dim3(256), 0, s, B->row_ptr,
+                               B->n_rows, (unsigned long long *)mx);
+            GM_CHECK_LAUNCH();
+            const int64_t maxlen = read_scalar(mx, s);
+            if (maxlen == 0 || A->nnz <= max_products / maxlen) {
+                bounds[1] = n;
+                *n_panels = 1;
+                return;
+            }
+        }
         int64_t *ip = ws.alloc<int64_t>(n), *sc = ws.alloc<int64_t>(n + 1);
         int64_t *scratch = ws.alloc<int64_t>(scan_scratch_elems(n));
         int64_t *out = ws.alloc<int64_t>(max_panels + 2);

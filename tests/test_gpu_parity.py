@@ -307,7 +307,10 @@ def test_split_panels_greedy_bounds(g):
     A = wl.rmat(12, 8, 0.57, 0.19, 0.19, 12)
     dA = g.DeviceCSR.from_host(A)
     pre = np.concatenate([[0], np.cumsum(oracle.row_products(A, A))])
-    for mp in (1, 37, 5_000, 200_000, int(pre[-1]) - 1, int(pre[-1]), 1 << 40):
+    # the limits around nnz(A) * (longest B row) take the one-panel shortcut
+    # on one side and the row products on the other
+    bound = int(A.nnz) * int(np.diff(A.row_ptr).max())
+    for mp in (1, 37, 5_000, 200_000, int(pre[-1]) - 1, int(pre[-1]), bound - 1, bound, 1 << 40):
         assert g.split_panels(dA, dA, mp) == greedy_panels(pre, mp), mp
     n_need = len(greedy_panels(pre, 5_000)) - 1
     assert len(g.split_panels(dA, dA, 5_000, max_panels=n_need)) == n_need + 1
