@@ -683,6 +683,7 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args<CI, V> a) {
     const CI mask = (CI)((1u << a.shift) - 1u);
     const int32_t mask1 = (int32_t)((1u << a.shift1) - 1u);
     const int64_t rt = ti.r0;  // keys are (region - rt) * nc1 + second-level chunk
+    const bool tile_heavy = rt < a.n_heavy_out;  // uniform over the work group
     const uint64_t le_mask = lanemask_lt() | (uint64_t(1) << lane);
     int32_t *wh = whist + w * K;
     for (int k = tid; k < RS2_NW * K; k += RS_BLOCK) whist[k] = 0;
@@ -788,77 +789,81 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args<CI, V> a) {
                     key[u] = -1;
                 }
             }
-            // ranks inside (wave, key) buckets, one LDS atomic per run of equal keys
-            int rank[RS2_E];
+            // the split: only tiles that hold heavy regions (heavy regions come
+            // first, so a tile whose first region is light holds none)
+            if (tile_heavy) {
+                // ranks inside (wave, key) buckets, one LDS atomic per run of equal keys
+                int rank[RS2_E];
 #pragma unroll
-            for (int u = 0; u < RS2_E; ++u) {
-                const int k = key[u];
-                const int kprev = prev_lane(k, k);
-                const uint64_t starts = ballot(lane == 0 || k != kprev);
-                const int first = 63 - __clzll((long long)(starts & le_mask));
-                const uint64_t above = starts & ~le_mask;
-                const int rl = (above ? __ffsll((long long)above) - 1 : GM_WAVE) - first;
-                int base = 0;
-                if (k >= 0 && lane == first) base = atomicAdd(&wh[k], rl);
-                base = __shfl(base, first, GM_WAVE);
-                rank[u] = base + (lane - first);
-            }
-            __syncthreads();
-            // exclusive scan over the buckets in (key, wave) order
-            {
-                const int M = RS2_NW * K;
-                const int per = (M + RS_BLOCK - 1) / RS_BLOCK;
-                int sum = 0;
-                for (int q = 0; q < per; ++q) {
-                    const int idx = tid * per + q;
-                    if (idx < M) sum += whist[(idx % RS2_NW) * K + idx / RS2_NW];
+                for (int u = 0; u < RS2_E; ++u) {
+                    const int k = key[u];
+                    const int kprev = prev_lane(k, k);
+                    const uint64_t starts = ballot(lane == 0 || k != kprev);
+                    const int first = 63 - __clzll((long long)(starts & le_mask));
+                    const uint64_t above = starts & ~le_mask;
+                    const int rl = (above ? __ffsll((long long)above) - 1 : GM_WAVE) - first;
+                    int base = 0;
+                    if (k >= 0 && lane == first) base = atomicAdd(&wh[k], rl);
+                    base = __shfl(base, first, GM_WAVE);
+                    rank[u] = base + (lane - first);
                 }
-                int tot = 0;
-                int run = block_excl_scan<RS_BLOCK>(sum, scan_sm, &tot);
-                for (int q = 0; q < per; ++q) {
-                    const int idx = tid * per + q;
-                    if (idx < M) {
-                        const int ad = (idx % RS2_NW) * K + idx / RS2_NW;
-                        const int v = whist[ad];
-                        whist[ad] = run;
-                        if (idx % RS2_NW == 0) key_start[idx / RS2_NW] = run;
-                        run += v;
+                __syncthreads();
+                // exclusive scan over the buckets in (key, wave) order
+                {
+                    const int M = RS2_NW * K;
+                    const int per = (M + RS_BLOCK - 1) / RS_BLOCK;
+                    int sum = 0;
+                    for (int q = 0; q < per; ++q) {
+                        const int idx = tid * per + q;
+                        if (idx < M) sum += whist[(idx % RS2_NW) * K + idx / RS2_NW];
+                    }
+                    int tot = 0;
+                    int run = block_excl_scan<RS_BLOCK>(sum, scan_sm, &tot);
+                    for (int q = 0; q < per; ++q) {
+                        const int idx = tid * per + q;
+                        if (idx < M) {
+                            const int ad = (idx % RS2_NW) * K + idx / RS2_NW;
+                            const int v = whist[ad];
+                            whist[ad] = run;
+                            if (idx % RS2_NW == 0) key_start[idx / RS2_NW] = run;
+                            run += v;
+                        }
+                    }
+                    if (tid == 0) key_start[K] = tot;
+                }
+                __syncthreads();
+                // reserve each key's range in its final chunk
+                for (int k = tid; k < K; k += RS_BLOCK) {
+                    const int cnt = key_start[k + 1] - key_start[k];
+                    if (cnt > 0) {
+                        const int64_t row = (rt + k / a.nc1) * a.nc1 + (k % a.nc1);
+                        const int64_t d = (int64_t)atomicAdd((unsigned long long *)&a.cursor1[row], (unsigned long long)cnt);
+                        key_delta[k] = d - key_start[k];
                     }
                 }
-                if (tid == 0) key_start[K] = tot;
-            }
-            __syncthreads();
-            // reserve each key's range in its final chunk
-            for (int k = tid; k < K; k += RS_BLOCK) {
-                const int cnt = key_start[k + 1] - key_start[k];
-                if (cnt > 0) {
-                    const int64_t row = (rt + k / a.nc1) * a.nc1 + (k % a.nc1);
-                    const int64_t d = (int64_t)atomicAdd((unsigned long long *)&a.cursor1[row], (unsigned long long)cnt);
-                    key_delta[k] = d - key_start[k];
-                }
-            }
 #pragma unroll
-            for (int u = 0; u < RS2_E; ++u) {
-                if (key[u] >= 0) {
-                    const int pos = wh[key[u]] + rank[u];
-                    col_buf[pos] = (uint16_t)(col[u] & mask1);
-                    val_buf[pos] = val[u];
-                    key_buf[pos] = (uint16_t)key[u];
+                for (int u = 0; u < RS2_E; ++u) {
+                    if (key[u] >= 0) {
+                        const int pos = wh[key[u]] + rank[u];
+                        col_buf[pos] = (uint16_t)(col[u] & mask1);
+                        val_buf[pos] = val[u];
+                        key_buf[pos] = (uint16_t)key[u];
+                    }
                 }
-            }
-            __syncthreads();
-            const int nh = key_start[K];
-            for (int p = tid; p < nh; p += RS_BLOCK) {
-                const int64_t d = key_delta[key_buf[p]] + p;
-                if (d < 0 || d >= a.n_out1_elems) {
-                    atomicOr(a.err, 8);
-                    continue;
+                __syncthreads();
+                const int nh = key_start[K];
+                for (int p = tid; p < nh; p += RS_BLOCK) {
+                    const int64_t d = key_delta[key_buf[p]] + p;
+                    if (d < 0 || d >= a.n_out1_elems) {
+                        atomicOr(a.err, 8);
+                        continue;
+                    }
+                    __builtin_nontemporal_store(col_buf[p], &a.out_col1[d]);
+                    __builtin_nontemporal_store(val_buf[p], &a.out_val1[d]);
                 }
-                __builtin_nontemporal_store(col_buf[p], &a.out_col1[d]);
-                __builtin_nontemporal_store(val_buf[p], &a.out_val1[d]);
+                for (int k = tid; k < RS2_NW * K; k += RS_BLOCK) whist[k] = 0;
+                __syncthreads();
             }
-            for (int k = tid; k < RS2_NW * K; k += RS_BLOCK) whist[k] = 0;
-            __syncthreads();
         }
         rb = next_rb;
         __syncthreads();
