@@ -1716,7 +1716,7 @@ void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *items, int64_t n, 
             launch_items(k_leaf_rank_sym<RANK_LBLOCK, W17, RANK_LWEPT>, RANK_LBLOCK, n, s, L, items, width, leaf_nnz,
                          slot_cnt);
         else
-            launch_items(k_leaf_rank_sym<RANK_LBLOCK, W18, RANK_LWEPT, 2>, RANK_LBLOCK, n, s, L, items, width, leaf_nnz,
+            launch_items(k_leaf_rank_sym<RANK_LBLOCK, W18, RANK_LWEPT, 1>, RANK_LBLOCK, n, s, L, items, width, leaf_nnz,
                          slot_cnt);
         break;
     }
@@ -1783,7 +1783,7 @@ void leaf_numeric_typed(const LeafSet &L, int bin, const LeafTask *items, int64_
             launch_items(k_leaf_rank_num<RANK_LBLOCK, W17, RANK_SMALL, RANK_LWEPT, 1, CI, V>, RANK_LBLOCK, n, s, L,
                          items, width, o);
         else if (bin != LEAF_RANK_XL)
-            launch_items(k_leaf_rank_num<RANK_LBLOCK, W18, RANK_SMALL, RANK_LWEPT, 2, CI, V>, RANK_LBLOCK, n, s, L,
+            launch_items(k_leaf_rank_num<RANK_LBLOCK, W18, RANK_SMALL, RANK_LWEPT, 1, CI, V>, RANK_LBLOCK, n, s, L,
                          items, width, o);
         else if (narrow)
             launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_NNZ_MAX, RANK_EPT, 1, CI, V>, RANK_BLOCK, n, s, L, items,
