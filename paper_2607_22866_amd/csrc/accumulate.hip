@@ -1710,7 +1710,7 @@ void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *items, int64_t n, 
             launch_items(k_leaf_rank_sym<RANK_WBLOCK, W17, RANK_WEPT>, RANK_WBLOCK, n, s, L, items, width, leaf_nnz,
                          slot_cnt);
         else if (bin == LEAF_RANK)
-            launch_items(k_leaf_rank_sym<RANK_WBLOCK, W18, RANK_WEPT, 2>, RANK_WBLOCK, n, s, L, items, width, leaf_nnz,
+            launch_items(k_leaf_rank_sym<RANK_WBLOCK, W18, RANK_WEPT, 1>, RANK_WBLOCK, n, s, L, items, width, leaf_nnz,
                          slot_cnt);
         else if (width <= (1 << 17))  // 4 waves per work group: 8 of them (chunks) per CU
             launch_items(k_leaf_rank_sym<RANK_LBLOCK, W17, RANK_LWEPT>, RANK_LBLOCK, n, s, L, items, width, leaf_nnz,
@@ -1777,7 +1777,7 @@ void leaf_numeric_typed(const LeafSet &L, int bin, const LeafTask *items, int64_
             launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_MID, RANK_EPT, 1, CI, V>, RANK_BLOCK, n, s, L, items,
                          width, o);
         else if (bin == LEAF_RANK)
-            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_MID, RANK_EPT, 2, CI, V>, RANK_BLOCK, n, s, L, items,
+            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_MID, RANK_EPT, 1, CI, V>, RANK_BLOCK, n, s, L, items,
                          width, o);
         else if (bin != LEAF_RANK_XL && narrow)  // at most RANK_SMALL distinct columns
             launch_items(k_leaf_rank_num<RANK_LBLOCK, W17, RANK_SMALL, RANK_LWEPT, 1, CI, V>, RANK_LBLOCK, n, s, L,
