@@ -290,6 +290,7 @@ struct gmagnus_plan_s {
     const int64_t *heavy_rows = nullptr;
     int64_t *chat_ptr = nullptr;      // n_heavy + 1
     int64_t products_total = 0, products_heavy = 0;
+    int64_t nnz_heavy = 0;            // A entries of the heavy rows
     // symbolic
     int64_t *row_nnz = nullptr;
     int64_t n_slots = 1;
@@ -414,6 +415,8 @@ class HostReads {
         r_[n_++] = Read{host, n, used_};
         used_ += n;
     }
+    // whether `reads` more reads of `values` values in all fit before a wait() is needed
+    bool room(int values, int reads) const { return used_ + values <= READ_SLOTS && n_ + reads <= MAXR; }
     void wait() {
         GM_HIP(hipStreamSynchronize(s_));
         resume_timers();
@@ -539,8 +542,47 @@ __global__ void k_affine(int64_t *p, int64_t n, int64_t a) {
 // max_panels do not reach row n); out[1 + i] = bound i.
 constexpr int SPLIT_BLOCK = 256;
 
-// *out = the longest row of a CSR row-pointer array (out zeroed before)
-__global__ __launch_bounds__(256) void k_max_row_len(const int64_t *rp, int64_t n_rows, unsigned long long *out) {
+// *out = the longest row of a CSR row-pointer array (out zeroed before).
+// One atomic per work group at most, and none when the maximum already
+// stored is as large: every wave's atomic on the one word serialised at the
+// L2 (16384 of them took 0.19 ms for 2^22 rows).
+// out[0] += products of the rows of class LIGHT_HEAVY, out[1] += their A
+// entries (out zeroed before): the two sizes the heavy path allocates by,
+// read together with the row bins instead of in round trips of their own.
+constexpr int HT_BLOCK = 256, HT_GRID = 1024;
+__global__ __launch_bounds__(HT_BLOCK) void k_heavy_totals(const uint8_t *cls, const int64_t *ip, const int64_t *rp,
+                                                           int64_t n, unsigned long long *out) {
+    __shared__ int64_t sm[2][HT_BLOCK / GM_WAVE];
+    int64_t prod = 0, ent = 0;
+    for (int64_t r = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; r < n; r += (int64_t)gridDim.x * blockDim.x)
+        if (cls[r] == LIGHT_HEAVY) {
+            prod += ip[r];
+            ent += rp[r + 1] - rp[r];
+        }
+#pragma unroll
+    for (int d = GM_WAVE / 2; d >= 1; d >>= 1) {
+        prod += __shfl_xor(prod, d, GM_WAVE);
+        ent += __shfl_xor(ent, d, GM_WAVE);
+    }
+    if ((threadIdx.x & (GM_WAVE - 1)) == 0) {
+        sm[0][threadIdx.x / GM_WAVE] = prod;
+        sm[1][threadIdx.x / GM_WAVE] = ent;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < HT_BLOCK / GM_WAVE; ++w) {
+            prod += sm[0][w];
+            ent += sm[1][w];
+        }
+        if (prod) atomicAdd(&out[0], (unsigned long long)prod);
+        if (ent) atomicAdd(&out[1], (unsigned long long)ent);
+    }
+}
+
+constexpr int MAXLEN_BLOCK = 256, MAXLEN_GRID = 1024;
+__global__ __launch_bounds__(MAXLEN_BLOCK) void k_max_row_len(const int64_t *rp, int64_t n_rows,
+                                                             unsigned long long *out) {
+    __shared__ int64_t wmax[MAXLEN_BLOCK / GM_WAVE];
     int64_t m = 0;
     for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < n_rows; k += (int64_t)gridDim.x * blockDim.x) {
         const int64_t len = rp[k + 1] - rp[k];
@@ -551,7 +593,14 @@ __global__ __launch_bounds__(256) void k_max_row_len(const int64_t *rp, int64_t 
         const int64_t o = __shfl_xor(m, d, GM_WAVE);
         m = o > m ? o : m;
     }
-    if ((threadIdx.x & (GM_WAVE - 1)) == 0 && m > 0) atomicMax(out, (unsigned long long)m);
+    if ((threadIdx.x & (GM_WAVE - 1)) == 0) wmax[threadIdx.x / GM_WAVE] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+#pragma unroll
+        for (int w = 1; w < MAXLEN_BLOCK / GM_WAVE; ++w) m = wmax[w] > m ? wmax[w] : m;
+        if (m > 0 && (unsigned long long)m > __hip_atomic_load(out, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+            atomicMax(out, (unsigned long long)m);
+    }
 }
 
 __global__ __launch_bounds__(SPLIT_BLOCK) void k_split_panels(const int64_t *pre, int64_t n, int64_t max_products,
@@ -595,6 +644,15 @@ __global__ void k_copy_i64(int64_t *dst, const int64_t *src, int64_t n) {
 void copy_i64(int64_t *dst, const int64_t *src, int64_t n, hipStream_t s) {
     if (n <= 0) return;
     hipLaunchKernelGGL(k_copy_i64, dim3(grid_for(n, 256, 65536)), dim3(256), 0, s, dst, src, n);
+    GM_CHECK_LAUNCH();
+}
+
+// *dst = src[*at]: a value whose index is itself on the device, fetched
+// there so that both come back in one host read
+__global__ void k_pick_i64(const int64_t *src, const int64_t *at, int64_t *dst) { *dst = src[*at]; }
+
+void pick_i64(const int64_t *src, const int64_t *at, int64_t *dst, hipStream_t s) {
+    hipLaunchKernelGGL(k_pick_i64, dim3(1), dim3(1), 0, s, src, at, dst);
     GM_CHECK_LAUNCH();
 }
 
@@ -683,17 +741,26 @@ void do_plan(gmagnus_plan_s *p, const gmagnus_matrix_t *A, const gmagnus_matrix_
     // products of all rows and of the heavy rows (C-hat row pointers)
     int64_t *ip_scan = ws.alloc<int64_t>(n + 1);
     scan_i64(p->ip, n, ip_scan, scratch, stream);
+    int64_t *heavy_tot = ws.alloc<int64_t>(2);
+    fill<int64_t>(heavy_tot, 0, 2, stream);
+    hipLaunchKernelGGL(k_heavy_totals, dim3(grid_for(n, HT_BLOCK, HT_GRID)), dim3(HT_BLOCK), 0, stream, cls, p->ip,
+                       p->A.rp + p->r0, n, (unsigned long long *)heavy_tot);
+    GM_CHECK_LAUNCH();
     {
+        int64_t tot[2] = {0, 0};
         HostReads r(stream);
         r.add(bins, LIGHT_NBINS + 1, p->bins_sym);
         r.add(ip_scan + n, 1, &p->products_total);
+        r.add(heavy_tot, 2, tot);
         r.wait();
+        p->products_heavy = tot[0];
+        p->nnz_heavy = tot[1];
     }
     p->n_heavy = p->bins_sym[LIGHT_HEAVY + 1] - p->bins_sym[LIGHT_HEAVY];
     p->heavy_rows = p->perm + p->bins_sym[LIGHT_HEAVY];
     p->chat_ptr = ws.alloc<int64_t>(p->n_heavy + 1);
     scan_gather_i64(p->ip, p->heavy_rows, p->n_heavy, p->chat_ptr, scratch, stream);
-    p->products_heavy = read_scalar(p->chat_ptr + p->n_heavy, stream);
+    ws.free(heavy_tot);
     ws.free(ip_scan);
     ws.free(scratch);
     ws.free(cls);
@@ -796,7 +863,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                                               (int64_t)16}));
         gather_row_len(p->A.rp, p->heavy_rows, nh, p->r0, row_len, s);
         scan_i64(row_len, nh, a_heavy_ptr, scratch, s);
-        nnz_heavy_all = read_scalar(a_heavy_ptr + nh, s);
+        nnz_heavy_all = p->nnz_heavy;  // summed over the same rows at plan time (checked below)
         int64_t *colcnt = ws.alloc<int64_t>(n_k);
         csc_count(p->A, p->B, p->heavy_rows, nh, p->r0, a_heavy_ptr, nnz_heavy_all, colcnt, s);
         uint8_t *kcls = ws.alloc<uint8_t>(n_k);
@@ -821,18 +888,20 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         int64_t *blen_scan = ws.alloc<int64_t>(sl.n_slices + 1);
         slice_lengths(p->B, sl.slice_k, sl.n_slices, cnt_s, s);
         scan_i64(cnt_s, sl.n_slices, blen_scan, sc2, s);
-        int64_t tot[3];
+        int64_t tot[4];
         {
             HostReads r(s);
             r.add(sl.col_ptr + sl.n_slices, 1, &tot[0]);
             r.add(sl.slice_off + sl.n_slices, 1, &tot[1]);
             r.add(blen_scan + sl.n_slices, 1, &tot[2]);
+            r.add(a_heavy_ptr + nh, 1, &tot[3]);
             r.wait();
         }
         ws.free(blen_scan);
         sl.nnz = tot[0];
         blen_total = tot[2];
         GM_REQUIRE(tot[1] == H, GMAGNUS_ERROR_HIP, "slice products disagree with the row products");
+        GM_REQUIRE(tot[3] == nnz_heavy_all, GMAGNUS_ERROR_HIP, "heavy rows' entries disagree with the plan's count");
         int64_t *cursor = nullptr;
         if (!rows_order) {
             cursor = ws.alloc<int64_t>(std::max<int64_t>(sl.n_slices, 1));
@@ -989,7 +1058,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         int64_t *sc = ws.alloc<int64_t>(std::max(partition_scratch_elems(n_out, 2), scan_scratch_elems(n_out)));
         int64_t *x_map = ws.alloc<int64_t>(n_out);
         int64_t *perm2 = ws.alloc<int64_t>(n_out);
-        int64_t *cb = ws.alloc<int64_t>(3);
+        int64_t *cb = ws.alloc<int64_t>(4);  // class bounds, then the heavy chunks' element count
         int64_t *out_cnt = ws.alloc<int64_t>(n_out);
         int64_t *origin_out = ws.alloc<int64_t>(n_out);
         int64_t *out_ptr = ws.alloc<int64_t>(n_out + 1);
@@ -1009,7 +1078,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
             p->info.kernel_launches[GMAGNUS_K_HISTOGRAM] += 1;
             add_bytes(p, GMAGNUS_K_HISTOGRAM, 4.0 * elems + 8.0 * (n_in + 1) + 8.0 * n_out);
         }
-        int64_t cbh[3];
+        int64_t cbh[4];
         {
             Timed t(p, GMAGNUS_K_SETUP, s);
             chunk_classes(counts, n_out, P.tau, last, ccls, s);
@@ -1017,7 +1086,8 @@ void heavy_symbolic(gmagnus_plan_s *p) {
             chunk_reorder(counts, x_map, n_out, nc, origin_in, slots_per_chunk, (rows_order && lvl == 0) ? nh : 0,
                           out_cnt, origin_out, s);
             scan_i64(out_cnt, n_out, out_ptr, sc, s);
-            read_bins(cb, 2, cbh, s);
+            pick_i64(out_ptr, cb + 1, cb + 3, s);  // out_ptr[nh_out]: the heavy chunks hold the first places
+            read_bins(cb, 3, cbh, s);
         }
         const int64_t nh_out = cbh[1];
         p->info.level_heavy_out[lvl] = nh_out;
@@ -1083,7 +1153,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                     partition_u8(ccls1, n_out1, 2, perm1, x_map1, cb1, sc1, s);
                     chunk_reorder(counts1, x_map1, n_out1, nc1, origin_out, slots1, 0, out_cnt1, origin_out1, s);
                     scan_i64(out_cnt1, n_out1, out_ptr1, sc1, s);
-                    elems1 = read_scalar(out_ptr + nh_out, s);
+                    elems1 = cbh[3];
                 }
                 // sized like the first level's buffers, so panels reuse the same blocks
                 col_buf[1] = ws.alloc<int32_t>(H);
@@ -1203,7 +1273,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
         if (last || nh_out == 0 || two_done.set.ptr) break;
         in_ptr = out_ptr;
         n_in = nh_out;
-        elems = read_scalar(out_ptr + nh_out, s);
+        elems = cbh[3];
         origin_in = origin_out;
         m_in_log2 = g.shift;
         cur = nxt;
@@ -1213,30 +1283,49 @@ void heavy_symbolic(gmagnus_plan_s *p) {
     // ---- final chunks: symbolic
     p->slot = ws.alloc<int64_t>(nh * p->n_slots);
     fill<int64_t>(p->slot, 0, nh * p->n_slots, s);
-    for (auto &lv : p->leaves) {
+    // Every level's classes first, then one host read of all their bins and
+    // element ranges; every level's symbolic launches and numeric classes,
+    // then one read of all numeric bins (two round trips, not two per level).
+    struct LeafTmp {
+        int64_t *sc = nullptr, *bins = nullptr;
+        uint8_t *lc = nullptr;
+        int64_t e0 = 0, e1 = 0;
+    };
+    std::vector<LeafTmp> tmp(p->leaves.size());
+    for (size_t i = 0; i < p->leaves.size(); ++i) {
+        LeafLevel &lv = p->leaves[i];
         const int64_t nl = lv.set.hi - lv.set.lo;
         if (nl <= 0) continue;
+        LeafTmp &tl = tmp[i];
         lv.leaf_nnz = ws.alloc<int64_t>(nl);
         lv.items_sym = ws.alloc<int64_t>(nl);
         lv.items_num = ws.alloc<int64_t>(nl);
-        int64_t *sc = ws.alloc<int64_t>(partition_scratch_elems(nl, LEAF_NBINS));
-        int64_t *bins = ws.alloc<int64_t>(LEAF_NBINS + 1);
-        uint8_t *lc = ws.alloc<uint8_t>(nl);
-        {
-            Timed t(p, GMAGNUS_K_SETUP, s);
-            fill<int64_t>(lv.leaf_nnz, 0, nl, s);
-            leaf_classes_sym(lv.set, P.tau, lv.width, lc, s);
-            partition_u8(lc, nl, LEAF_NBINS, lv.items_sym, nullptr, bins, sc, s);
+        tl.sc = ws.alloc<int64_t>(partition_scratch_elems(nl, LEAF_NBINS));
+        tl.bins = ws.alloc<int64_t>(LEAF_NBINS + 1);
+        tl.lc = ws.alloc<uint8_t>(nl);
+        Timed t(p, GMAGNUS_K_SETUP, s);
+        fill<int64_t>(lv.leaf_nnz, 0, nl, s);
+        leaf_classes_sym(lv.set, P.tau, lv.width, tl.lc, s);
+        partition_u8(tl.lc, nl, LEAF_NBINS, lv.items_sym, nullptr, tl.bins, tl.sc, s);
+    }
+    {
+        HostReads r(s);
+        for (size_t i = 0; i < p->leaves.size(); ++i) {
+            LeafLevel &lv = p->leaves[i];
+            if (lv.set.hi - lv.set.lo <= 0) continue;
+            if (!r.room(LEAF_NBINS + 3, 3)) r.wait();
+            r.add(tmp[i].bins, LEAF_NBINS + 1, lv.bins_sym);
+            r.add(lv.set.ptr + lv.set.lo, 1, &tmp[i].e0);
+            r.add(lv.set.ptr + lv.set.hi, 1, &tmp[i].e1);
         }
-        int64_t e0 = 0, e1 = 0;
-        {
-            HostReads r(s);
-            r.add(bins, LEAF_NBINS + 1, lv.bins_sym);
-            r.add(lv.set.ptr + lv.set.lo, 1, &e0);
-            r.add(lv.set.ptr + lv.set.hi, 1, &e1);
-            r.wait();
-        }
-        lv.elems = e1 - e0;
+        r.wait();
+    }
+    for (size_t i = 0; i < p->leaves.size(); ++i) {
+        LeafLevel &lv = p->leaves[i];
+        const int64_t nl = lv.set.hi - lv.set.lo;
+        if (nl <= 0) continue;
+        LeafTmp &tl = tmp[i];
+        lv.elems = tl.e1 - tl.e0;
         {
             LeafTask *tasks = ws.alloc<LeafTask>(nl);
             leaf_tasks_sym(lv.set, lv.items_sym, nl, tasks, s);
@@ -1245,7 +1334,7 @@ void heavy_symbolic(gmagnus_plan_s *p) {
                 if (b == LEAF_DENSE_BIG) continue;  // launched together with LEAF_DENSE, first
                 const int64_t b0 = b == LEAF_DENSE ? lv.bins_sym[LEAF_DENSE_BIG] : lv.bins_sym[b];
                 const int64_t cnt = lv.bins_sym[b + 1] - b0;
-                leaf_symbolic(lv.set, b, tasks + b0, cnt, lv.width, e1, lv.leaf_nnz, p->slot, s);
+                leaf_symbolic(lv.set, b, tasks + b0, cnt, lv.width, tl.e1, lv.leaf_nnz, p->slot, s);
                 if (cnt) p->info.kernel_launches[GMAGNUS_K_CHUNK_SYM] += 1;
                 if (b == LEAF_DENSE) p->info.n_leaves_dense += cnt;
                 else if (b == LEAF_RANK || b == LEAF_RANK_L || b == LEAF_RANK_XL || b == LEAF_RANK_T)
@@ -1256,15 +1345,24 @@ void heavy_symbolic(gmagnus_plan_s *p) {
             ws.free(tasks);
         }
         // numeric bins now, so the numeric phase needs no host round trip
-        {
-            Timed t(p, GMAGNUS_K_SETUP, s);
-            leaf_classes_num(lv.set, lv.leaf_nnz, P.tau, lv.width, lc, s);
-            partition_u8(lc, nl, LEAF_NBINS, lv.items_num, nullptr, bins, sc, s);
-            read_bins(bins, LEAF_NBINS, lv.bins_num, s);
+        Timed t(p, GMAGNUS_K_SETUP, s);
+        leaf_classes_num(lv.set, lv.leaf_nnz, P.tau, lv.width, tl.lc, s);
+        partition_u8(tl.lc, nl, LEAF_NBINS, lv.items_num, nullptr, tl.bins, tl.sc, s);
+    }
+    {
+        HostReads r(s);
+        for (size_t i = 0; i < p->leaves.size(); ++i) {
+            LeafLevel &lv = p->leaves[i];
+            if (lv.set.hi - lv.set.lo <= 0) continue;
+            if (!r.room(LEAF_NBINS + 1, 1)) r.wait();
+            r.add(tmp[i].bins, LEAF_NBINS + 1, lv.bins_num);
         }
-        ws.free(sc);
-        ws.free(bins);
-        ws.free(lc);
+        r.wait();
+    }
+    for (LeafTmp &tl : tmp) {
+        ws.free(tl.sc);
+        ws.free(tl.bins);
+        ws.free(tl.lc);
     }
     {
         Timed t(p, GMAGNUS_K_ROWPTR, s);
@@ -1334,39 +1432,42 @@ void do_symbolic(gmagnus_plan_s *p, int64_t *c_row_ptr, int64_t *c_nnz) {
     GM_HIP(hipStreamWaitEvent(p->stream, jl, 0));
     GM_HIP(hipStreamWaitEvent(p->stream, jh, 0));
     ws.free(light_keep);
+    // C's row pointers, then the light rows' numeric bins; nnz(C) and the
+    // bins come back in one host round trip
+    int64_t *hs = nullptr, *sc = nullptr;
     {
         Timed t(p, GMAGNUS_K_ROWPTR, p->stream);
-        int64_t *sc = ws.alloc<int64_t>(scan_scratch_elems(n));
+        sc = ws.alloc<int64_t>(scan_scratch_elems(n));
         scan_i64(p->row_nnz, n, c_row_ptr, sc, p->stream);
-        int64_t *hs = nullptr;
-        HostReads r(p->stream);
-        r.add(c_row_ptr + n, 1, &p->c_nnz);
         if (p->n_heavy > 0) {
             hs = ws.alloc<int64_t>(p->n_heavy + 1);
             scan_gather_i64(p->row_nnz, p->heavy_rows, p->n_heavy, hs, sc, p->stream);  // sc: after the first scan
-            r.add(hs + p->n_heavy, 1, &p->info.c_nnz_heavy);
         }
-        r.wait();
-        ws.free(hs);
-        ws.free(sc);
         add_bytes(p, GMAGNUS_K_ROWPTR, 16.0 * n);
     }
-    // numeric bins of the light rows
+    uint8_t *cls = ws.alloc<uint8_t>(n);
+    int64_t *bins = ws.alloc<int64_t>(LIGHT_NBINS + 1);
+    int64_t *psc = ws.alloc<int64_t>(partition_scratch_elems(n, LIGHT_NBINS));
     {
         Timed t(p, GMAGNUS_K_SETUP, p->stream);
         const bool window = (p->opts.flags & GMAGNUS_FLAG_NO_WINDOW) == 0;
-        uint8_t *cls = ws.alloc<uint8_t>(n);
-        int64_t *bins = ws.alloc<int64_t>(LIGHT_NBINS + 1);
-        int64_t *sc = ws.alloc<int64_t>(partition_scratch_elems(n, LIGHT_NBINS));
         p->perm_num = ws.alloc<int64_t>(n);
         light_classes_num(p->ip, p->row_nnz, p->minc, p->maxc, p->B.ci64, n, p->info.row_tau, window, cls,
                           p->stream);
-        partition_u8(cls, n, LIGHT_NBINS, p->perm_num, nullptr, bins, sc, p->stream);
-        read_bins(bins, LIGHT_NBINS, p->bins_num, p->stream);
-        ws.free(cls);
-        ws.free(bins);
-        ws.free(sc);
+        partition_u8(cls, n, LIGHT_NBINS, p->perm_num, nullptr, bins, psc, p->stream);
     }
+    {
+        HostReads r(p->stream);
+        r.add(c_row_ptr + n, 1, &p->c_nnz);
+        if (hs) r.add(hs + p->n_heavy, 1, &p->info.c_nnz_heavy);
+        r.add(bins, LIGHT_NBINS + 1, p->bins_num);
+        r.wait();
+    }
+    ws.free(hs);
+    ws.free(sc);
+    ws.free(cls);
+    ws.free(bins);
+    ws.free(psc);
     *c_nnz = p->c_nnz;
     p->info.c_nnz = p->c_nnz;
     p->symbolic_done = true;
@@ -1686,8 +1787,8 @@ gmagnus_status_t gmagnus_split_panels_typed(const gmagnus_matrix_t *A, const gma
             // matrix is one panel and the row products need not be formed
             int64_t *mx = ws.alloc<int64_t>(1);
             fill<int64_t>(mx, 0, 1, s);
-            hipLaunchKernelGGL(k_max_row_len, dim3(grid_for(B->n_rows, 256, 4096)), dim3(256), 0, s, B->row_ptr,
-                               B->n_rows, (unsigned long long *)mx);
+            hipLaunchKernelGGL(k_max_row_len, dim3(grid_for(B->n_rows, MAXLEN_BLOCK, MAXLEN_GRID)), dim3(MAXLEN_BLOCK),
+                               0, s, B->row_ptr, B->n_rows, (unsigned long long *)mx);
             GM_CHECK_LAUNCH();
             const int64_t maxlen = read_scalar(mx, s);
             if (maxlen == 0 || A->nnz <= max_products / maxlen) {
