@@ -517,15 +517,16 @@ __global__ __launch_bounds__(256) void k_fine_bounds(CsrV<CI, NoV> B, const int3
 // F[h * nf + f] += fine chunk f's products of heavy row h: each work group
 // takes FC_ENTRIES consecutive row-ordered entries, thread t owns the fine
 // chunks t, t + FC_BLOCK, ... for entries with long B rows (sizes from the
-// fine boundaries), the waves take turns to histogram the columns of short B
-// rows in LDS, and a row's counts are flushed with one atomic per nonzero
-// counter when the row changes.
-constexpr int FC_BLOCK = 256, FC_ENTRIES = 256, FC_MAXF = 1024;
+// fine boundaries, loaded for FC_U entries at a time so that their loads are
+// in flight together), the waves take turns to histogram the columns of
+// short B rows in LDS, and a row's counts are flushed with one atomic per
+// nonzero counter when the row changes.
+constexpr int FC_BLOCK = 256, FC_ENTRIES = 256, FC_MAXF = 1024, FC_U = 8;
 
-template <typename CI>
+template <typename CI, int FPT>  // FPT: fine chunks per thread, nf <= FPT * FC_BLOCK
 __global__ __launch_bounds__(FC_BLOCK) void k_fine_counts(CsrV<CI, NoV> B, RowEntries ent, int64_t n_ent,
                                                           const int32_t *bndf, int nf, int fshift, int64_t *F) {
-    constexpr int FPT = FC_MAXF / FC_BLOCK;
+    static_assert(FPT * FC_BLOCK <= FC_MAXF, "the short rows' counters hold every fine chunk");
     __shared__ int32_t es[FC_ENTRIES], eh[FC_ENTRIES], el[FC_ENTRIES];
     __shared__ int64_t eb[FC_ENTRIES];
     __shared__ int32_t sh[FC_MAXF];  // the current row's counts from short B rows
@@ -550,47 +551,70 @@ __global__ __launch_bounds__(FC_BLOCK) void k_fine_counts(CsrV<CI, NoV> B, RowEn
     int64_t acc[FPT];
 #pragma unroll
     for (int j = 0; j < FPT; ++j) acc[j] = 0;
-    int32_t cur = eh[0];
-    for (int i = 0; i <= ne; ++i) {
-        const int32_t h = i < ne ? eh[i] : -1;
-        if (h != cur) {  // uniform: flush the row's counts
-            __syncthreads();
+    // adds row h's counts to F and clears them (all threads)
+    auto flush = [&](int32_t h) {
+        __syncthreads();
 #pragma unroll
-            for (int j = 0; j < FPT; ++j) {
-                const int f = tid + j * FC_BLOCK;
-                if (f < nf) {
-                    const int64_t v = acc[j] + sh[f];
-                    if (v) atomicAdd((unsigned long long *)&F[(int64_t)cur * nf + f], (unsigned long long)v);
-                    sh[f] = 0;
-                }
-                acc[j] = 0;
+        for (int j = 0; j < FPT; ++j) {
+            const int f = tid + j * FC_BLOCK;
+            if (f < nf) {
+                const int64_t v = acc[j] + sh[f];
+                if (v) atomicAdd((unsigned long long *)&F[(int64_t)h * nf + f], (unsigned long long)v);
+                sh[f] = 0;
             }
-            __syncthreads();
-            cur = h;
+            acc[j] = 0;
         }
-        if (i == ne) break;
-        const int32_t sl = es[i], len = el[i];
-        if (sl < 0 || len == 0) continue;
-        if (len > FB_SHORT) {
-            const int32_t *bq = bndf + (int64_t)sl * (nf + 1);
+        __syncthreads();
+    };
+    int32_t cur = eh[0];
+    for (int i0 = 0; i0 < ne; i0 += FC_U) {
+        // the fine boundaries of the long B rows among the next FC_U entries,
+        // loaded with no branch between the loads (a slot with nothing to
+        // read loads bndf[0] and is dropped), so that they are in flight together
+        int32_t lo[FC_U][FPT], hi[FC_U][FPT];
+#pragma unroll
+        for (int u = 0; u < FC_U; ++u) {
+            const int i = i0 + u < ne ? i0 + u : ne - 1;
+            const bool lng = es[i] >= 0 && el[i] > FB_SHORT;
+            const int32_t *bq = bndf + (int64_t)(lng ? es[i] : 0) * (nf + 1);
 #pragma unroll
             for (int j = 0; j < FPT; ++j) {
                 const int f = tid + j * FC_BLOCK;
-                if (f < nf) acc[j] += bq[f + 1] - bq[f];
+                const bool ok = lng && f < nf;
+                lo[u][j] = *(ok ? bq + f : bndf);
+                hi[u][j] = *(ok ? bq + f + 1 : bndf);
             }
-        } else if (tid / GM_WAVE == (i & (FC_BLOCK / GM_WAVE - 1))) {
-            // short B rows go to the waves in turn; one lane per element, a
-            // run of equal chunks adds its length once
-            const int f = lane < len ? (int)(B.ci[eb[i] + lane] >> fshift) : -1;
-            const int fp = prev_lane(f, -2);
-            const uint64_t starts = ballot(f >= 0 && f != fp);
-            if (f >= 0 && ((starts >> lane) & 1)) {
-                const uint64_t above = starts & ~((lanemask_lt() << 1) | 1ull);
-                const int end = above ? __ffsll((long long)above) - 1 : (len < GM_WAVE ? len : GM_WAVE);
-                atomicAdd(&sh[f], end - lane);
+        }
+#pragma unroll
+        for (int u = 0; u < FC_U; ++u) {
+            const int i = i0 + u;
+            if (i >= ne) break;  // uniform
+            const int32_t h = eh[i];
+            if (h != cur) {  // uniform: flush the row's counts
+                flush(cur);
+                cur = h;
+            }
+            const int32_t sl = es[i], len = el[i];
+            if (sl < 0 || len == 0) continue;
+            if (len > FB_SHORT) {
+#pragma unroll
+                for (int j = 0; j < FPT; ++j)
+                    if (tid + j * FC_BLOCK < nf) acc[j] += hi[u][j] - lo[u][j];
+            } else if (tid / GM_WAVE == (i & (FC_BLOCK / GM_WAVE - 1))) {
+                // short B rows go to the waves in turn; one lane per element, a
+                // run of equal chunks adds its length once
+                const int f = lane < len ? (int)(B.ci[eb[i] + lane] >> fshift) : -1;
+                const int fp = prev_lane(f, -2);
+                const uint64_t starts = ballot(f >= 0 && f != fp);
+                if (f >= 0 && ((starts >> lane) & 1)) {
+                    const uint64_t above = starts & ~((lanemask_lt() << 1) | 1ull);
+                    const int end = above ? __ffsll((long long)above) - 1 : (len < GM_WAVE ? len : GM_WAVE);
+                    atomicAdd(&sh[f], end - lane);
+                }
             }
         }
     }
+    flush(cur);
 }
 
 // counts1[r * nc1 + c1] = F[h * nf + c * nc1 + c1] for the heavy regions r of
@@ -974,8 +998,12 @@ void fine_counts(const Csr &B, const RowEntries &ent, int64_t n_ent, const int32
     GM_REQUIRE(blocks < (int64_t)1 << 31, GMAGNUS_ERROR_UNSUPPORTED, "fine counts: too many entries");
     with_index_type(B.ci64, [&](auto ci) {
         using CI = decltype(ci);
-        hipLaunchKernelGGL(k_fine_counts<CI>, dim3((unsigned)blocks), dim3(FC_BLOCK), 0, s, typed<CI, NoV>(B), ent,
-                           n_ent, bndf, nf, fshift, F);
+        if (nf <= 2 * FC_BLOCK)
+            hipLaunchKernelGGL((k_fine_counts<CI, 2>), dim3((unsigned)blocks), dim3(FC_BLOCK), 0, s,
+                               typed<CI, NoV>(B), ent, n_ent, bndf, nf, fshift, F);
+        else
+            hipLaunchKernelGGL((k_fine_counts<CI, FC_MAXF / FC_BLOCK>), dim3((unsigned)blocks), dim3(FC_BLOCK), 0, s,
+                               typed<CI, NoV>(B), ent, n_ent, bndf, nf, fshift, F);
         GM_CHECK_LAUNCH();
     });
 }
