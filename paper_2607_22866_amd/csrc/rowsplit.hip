@@ -822,7 +822,10 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows2(Rs2Args<CI, V> a) {
                 for (int u = 0; u < RS2_E; ++u) {
                     const int k = key[u];
                     const int kprev = prev_lane(k, k);
-                    const uint64_t starts = ballot(lane == 0 || k != kprev);
+                    // lane 0 always starts a run: its bit is set after the ballot
+                    // (the whole wave is active here), which keeps the ballot
+                    // a single comparison
+                    const uint64_t starts = ballot(k != kprev) | 1ull;
                     const int first = 63 - __clzll((long long)(starts & le_mask));
                     const uint64_t above = starts & ~le_mask;
                     const int rl = (above ? __ffsll((long long)above) - 1 : GM_WAVE) - first;
