@@ -71,6 +71,10 @@ def test_rmat12_every_depth(g, opts, levels):
     assert info.n_heavy_rows == int((ip > info.row_tau).sum())
     assert info.products_total == int(ip.sum())
     assert info.products_heavy == int(ip[ip > info.row_tau].sum())
+    # nnz(C) and the heavy rows' share of it, from the oracle's row counts
+    cnt = oracle.row_counts(A, A)
+    assert info.c_nnz == int(cnt.sum())
+    assert info.c_nnz_heavy == int(cnt[ip > info.row_tau].sum())
     if levels:
         assert info.levels_run >= 1
 
