@@ -459,11 +459,21 @@ __global__ __launch_bounds__(RS_BLOCK) void k_expand_rows(RsArgs<CI, V> a) {
 // other). Each search starts from its first-level chunk's part of the row
 // (the slice's coarse bounds), about five steps shorter than the whole row.
 constexpr int FB_SHORT = 64;
+// Rows of at most FB_STREAM elements are read once instead: their columns
+// (FB_ILP loads per lane in flight) are counted per fine chunk in the wave's
+// LDS histogram, one add per run of equal chunks (the row is sorted), and the
+// boundaries are the histogram's exclusive scan, written in one coalesced
+// pass: about len / (64 * FB_ILP) rounds of loads instead of a dozen
+// dependent search steps.
+constexpr int FB_STREAM = 4096, FB_ILP = 8, FB_MAXF = 1024, FB_WAVES = 4;
 
 template <int PER, typename CI>
-__global__ __launch_bounds__(256) void k_fine_bounds(CsrV<CI, NoV> B, const int32_t *slice_k, int64_t n_slices, int nf,
-                                                     int fshift, const int32_t *sbnd, int nc, int32_t *bndf) {
+__global__ __launch_bounds__(FB_WAVES * GM_WAVE) void k_fine_bounds(CsrV<CI, NoV> B, const int32_t *slice_k,
+                                                                    int64_t n_slices, int nf, int fshift,
+                                                                    const int32_t *sbnd, int nc, int32_t *bndf) {
+    __shared__ int32_t hist_all[FB_WAVES][FB_MAXF];
     const int lane = threadIdx.x & (GM_WAVE - 1);
+    int32_t *hist = hist_all[threadIdx.x / GM_WAVE];
     const int nc1 = nf / nc;
     const int64_t nwaves = (int64_t)gridDim.x * (blockDim.x / GM_WAVE);
     for (int64_t s = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / GM_WAVE; s < n_slices; s += nwaves) {
@@ -473,6 +483,48 @@ __global__ __launch_bounds__(256) void k_fine_bounds(CsrV<CI, NoV> B, const int3
         int32_t *out = bndf + s * (nf + 1);
         const int32_t *cb = sbnd + s * (nc + 1);  // the row's first-level chunk bounds
         const CI *row = B.ci + b0;
+        if (len <= FB_STREAM) {  // uniform over the wave
+            for (int f = lane; f < nf; f += GM_WAVE) hist[f] = 0;
+            wave_lds_fence();
+            for (int p0 = 0; p0 < (int)len; p0 += GM_WAVE * FB_ILP) {
+                int fc[FB_ILP];
+#pragma unroll
+                for (int u = 0; u < FB_ILP; ++u) {
+                    const int p = p0 + u * GM_WAVE + lane;
+                    const int64_t f = p < (int)len ? ((int64_t)row[p] >> fshift) : -1;
+                    fc[u] = f < nf ? (int)f : nf - 1;  // (a column past C's width would be invalid input)
+                }
+#pragma unroll
+                for (int u = 0; u < FB_ILP; ++u) {
+                    const int fp = prev_lane(fc[u], -2);
+                    const uint64_t starts = ballot(fc[u] >= 0 && fc[u] != fp);
+                    if (fc[u] >= 0 && ((starts >> lane) & 1)) {
+                        const uint64_t above = starts & ~((lanemask_lt() << 1) | 1ull);
+                        const int left = (int)len - (p0 + u * GM_WAVE);  // elements of this batch in the row
+                        const int end = above ? __ffsll((long long)above) - 1 : (left < GM_WAVE ? left : GM_WAVE);
+                        atomicAdd(&hist[fc[u]], end - lane);
+                    }
+                }
+            }
+            wave_lds_fence();
+            // boundary f = elements in fine chunks below f: lane l scans the
+            // counters [l * per, l * per + per), then adds the lanes before it
+            const int per = (nf + 1 + GM_WAVE - 1) / GM_WAVE;
+            const int f0 = lane * per;
+            int32_t tot = 0;
+            for (int j = 0; j < per; ++j) {
+                const int f = f0 + j;
+                if (f < nf) tot += hist[f];
+            }
+            int32_t run = wave_incl_scan<int32_t>(tot) - tot;
+            for (int j = 0; j < per; ++j) {
+                const int f = f0 + j;
+                if (f <= nf) out[f] = run;
+                if (f < nf) run += hist[f];
+            }
+            wave_lds_fence();  // the counters are read before the next slice clears them
+            continue;
+        }
         for (int f0 = 0; f0 <= nf; f0 += PER * GM_WAVE) {  // PER boundaries per lane at a time
             int32_t lo[PER], hi[PER];
 #pragma unroll
@@ -980,14 +1032,14 @@ int64_t fine_bounds_words(int64_t n_slices, int nf) { return n_slices * (nf + 1)
 void fine_bounds(const Csr &B, const int32_t *slice_k, int64_t n_slices, int nf, int fshift, const int32_t *sbnd,
                  int nc, int32_t *bndf, hipStream_t s) {
     if (n_slices <= 0) return;
-    GM_REQUIRE(nf >= 1 && nf <= FC_MAXF && (int64_t)B.nnz < ((int64_t)1 << 31), GMAGNUS_ERROR_UNSUPPORTED,
-               "fine boundaries: too many fine chunks or B too large");
+    GM_REQUIRE(nf >= 1 && nf <= FC_MAXF && nf <= FB_MAXF && (int64_t)B.nnz < ((int64_t)1 << 31),
+               GMAGNUS_ERROR_UNSUPPORTED, "fine boundaries: too many fine chunks or B too large");
     GM_REQUIRE(nc >= 1 && nf % nc == 0, GMAGNUS_ERROR_UNSUPPORTED, "fine boundaries: fine chunks must refine the first level");
     // 9 boundaries per lane cover nf = 512 (R-MAT 22's 32 x 16 chunks) in one round
     with_index_type(B.ci64, [&](auto ci) {
         using CI = decltype(ci);
-        hipLaunchKernelGGL((k_fine_bounds<9, CI>), dim3(grid_for(n_slices, 4, 65536)), dim3(256), 0, s,
-                           typed<CI, NoV>(B), slice_k, n_slices, nf, fshift, sbnd, nc, bndf);
+        hipLaunchKernelGGL((k_fine_bounds<9, CI>), dim3(grid_for(n_slices, FB_WAVES, 65536)), dim3(FB_WAVES * GM_WAVE),
+                           0, s, typed<CI, NoV>(B), slice_k, n_slices, nf, fshift, sbnd, nc, bndf);
         GM_CHECK_LAUNCH();
     });
 }
