@@ -223,7 +223,9 @@ __global__ void k_slice_lengths(Csr B, const int32_t *slice_k, int64_t n, int64_
 // Level-0 chunk boundaries of every slice's B row: bnd[s * (nc + 1) + c] =
 // offset in B[k,:] of the row's first column >= c << shift (c = 0..nc). The
 // row is sorted, so lane c of a wave finds it by binary search; chunk c of
-// the row is [bnd[c], bnd[c + 1]).
+// the row is [bnd[c], bnd[c + 1]). A row of at most 64 elements (most of
+// them) is loaded once, one element per lane, and searched across the lanes
+// with shuffles instead of a chain of dependent global loads.
 template <typename CI>
 __global__ __launch_bounds__(256) void k_slice_chunk_bounds(CsrV<CI, NoV> B, const int32_t *slice_k, int64_t n_slices,
                                                             int nc, int shift, int32_t *bnd) {
@@ -232,6 +234,25 @@ __global__ __launch_bounds__(256) void k_slice_chunk_bounds(CsrV<CI, NoV> B, con
     for (int64_t s = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / GM_WAVE; s < n_slices; s += nwaves) {
         const int32_t k = slice_k[s];
         const int64_t b0 = B.rp[k], b1 = B.rp[k + 1];
+        if (b1 - b0 <= GM_WAVE) {  // uniform over the wave
+            const int len = (int)(b1 - b0);
+            // chunk of each element (lanes past the row: past every chunk)
+            const int ch = lane < len ? (int)((int64_t)B.ci[b0 + lane] >> shift) : INT32_MAX;
+            int lo = 0, hi = len;  // lane c: first element whose chunk is >= c
+#pragma unroll
+            for (int st = 0; st < 7; ++st) {  // 2^7 > 64: every search closes
+                const int mid = (lo + hi) >> 1;
+                const int v = __shfl(ch, mid < GM_WAVE ? mid : GM_WAVE - 1, GM_WAVE);
+                if (lo < hi) {
+                    if (v < lane)
+                        lo = mid + 1;
+                    else
+                        hi = mid;
+                }
+            }
+            if (lane <= nc) bnd[s * (nc + 1) + lane] = lo;
+            continue;
+        }
         int64_t lo = b0, hi = b1;
         if (lane <= nc) {
             const int64_t bound = (int64_t)lane << shift;
