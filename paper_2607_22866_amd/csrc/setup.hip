@@ -274,7 +274,7 @@ __global__ __launch_bounds__(256) void k_slice_chunk_bounds(CsrV<CI, NoV> B, con
 // chunk sizes (differences of the boundaries above). Each wave walks
 // SH_ENTRIES consecutive A~ entries in row-major order, lane c accumulating
 // chunk c, and flushes at row ends.
-constexpr int SH_ENTRIES = 256;
+constexpr int SH_ENTRIES = 256, SH_U = 8;
 
 template <typename CI>
 __global__ __launch_bounds__(256) void k_struct_hist(CsrV<CI, NoV> A, const int64_t *heavy_rows, int64_t n_heavy, int64_t r0,
@@ -303,20 +303,35 @@ __global__ __launch_bounds__(256) void k_struct_hist(CsrV<CI, NoV> A, const int6
             s = k_to_slice[(int64_t)A.ci[a_base + e]];
         }
         const int cnt = (int)(e1 - eb < GM_WAVE ? e1 - eb : GM_WAVE);
-        for (int q = 0; q < cnt; ++q) {
-            const int64_t hq = __shfl(h, q, GM_WAVE);
-            const int32_t sq = __shfl(s, q, GM_WAVE);
-            if (hq != cur) {
-                if (lane < nc && acc) {
-                    const int64_t ix = cmajor_rows ? lane * cmajor_rows + cur : cur * nc + lane;
-                    atomicAdd((unsigned long long *)&counts[ix], (unsigned long long)acc);
-                }
-                acc = 0;
-                cur = hq;
+        for (int q0 = 0; q0 < cnt; q0 += SH_U) {
+            // the chunk bounds of SH_U entries, loaded with no branch between
+            // the loads so that they are in flight together (a slot with
+            // nothing to read loads bnd[0] and is dropped)
+            int32_t lo[SH_U], hi[SH_U];
+            int64_t hq[SH_U];
+            bool ok[SH_U];
+#pragma unroll
+            for (int u = 0; u < SH_U; ++u) {
+                const int q = q0 + u < cnt ? q0 + u : cnt - 1;
+                hq[u] = __shfl(h, q, GM_WAVE);
+                const int32_t sq = __shfl(s, q, GM_WAVE);
+                ok[u] = q0 + u < cnt && sq >= 0 && lane < nc;
+                const int32_t *bq = bnd + (int64_t)(sq >= 0 ? sq : 0) * (nc + 1);
+                lo[u] = *(ok[u] ? bq + lane : bnd);
+                hi[u] = *(ok[u] ? bq + lane + 1 : bnd);
             }
-            if (sq >= 0 && lane < nc) {
-                const int32_t *bq = bnd + (int64_t)sq * (nc + 1);
-                acc += bq[lane + 1] - bq[lane];
+#pragma unroll
+            for (int u = 0; u < SH_U; ++u) {
+                if (q0 + u >= cnt) break;  // uniform
+                if (hq[u] != cur) {
+                    if (lane < nc && acc) {
+                        const int64_t ix = cmajor_rows ? lane * cmajor_rows + cur : cur * nc + lane;
+                        atomicAdd((unsigned long long *)&counts[ix], (unsigned long long)acc);
+                    }
+                    acc = 0;
+                    cur = hq[u];
+                }
+                if (ok[u]) acc += hi[u] - lo[u];
             }
         }
         // lanes past the last entry may have stopped walking; realign for the next group
