@@ -1177,9 +1177,13 @@ __global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(8))) void
 constexpr int RANK_BLOCK = 512;
 constexpr int RANK_EPT = 16;  // RANK_BLOCK * RANK_EPT >= tau_limit()
 constexpr int RANK_WBLOCK = 256, RANK_WEPT = 4;  // the small wide shape
-constexpr int RANK_LBLOCK = 256, RANK_LWEPT = 27;  // wide numeric, at most RANK_SMALL columns: 4 waves and
-                                                   // under 32 KB of LDS, so five work groups share a CU
-static_assert(RANK_LBLOCK * RANK_LWEPT >= SORT_CAP[2] && RANK_BLOCK * RANK_EPT >= SORT_CAP[2],
+constexpr int RANK_L2BLOCK = 512, RANK_L2EPT = 14;  // the same in 8 waves: twice the waves per CU when the
+                                                   // LDS caps the work groups (R-MAT 23's 2^18 columns:
+                                                   // 193 -> 150 ms per step for these kernels)
+constexpr int RANK_LBLOCK = 256, RANK_LWEPT = 27;  // wide symbolic at 2^17 columns: 4 waves and 16 KB of
+                                                   // LDS, so eight work groups share a CU
+static_assert(RANK_LBLOCK * RANK_LWEPT >= SORT_CAP[2] && RANK_BLOCK * RANK_EPT >= SORT_CAP[2] &&
+                  RANK_L2BLOCK * RANK_L2EPT >= SORT_CAP[2],
               "the wide shapes hold a light chunk of up to the largest tau");
 static_assert(RANK_WBLOCK * RANK_WEPT >= RANK_WIDE_SMALL, "the small wide shape holds its chunks");
 constexpr int RANK_SBLOCK = 256, RANK_SWORDS = 256, RANK_SCAP = 512, RANK_SEPT = 2, RANK_LEPT = 8;
@@ -1715,9 +1719,9 @@ void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *items, int64_t n, 
         else if (width <= (1 << 17))  // 4 waves per work group: 8 of them (chunks) per CU
             launch_items(k_leaf_rank_sym<RANK_LBLOCK, W17, RANK_LWEPT>, RANK_LBLOCK, n, s, L, items, width, leaf_nnz,
                          slot_cnt);
-        else
-            launch_items(k_leaf_rank_sym<RANK_LBLOCK, W18, RANK_LWEPT, 1>, RANK_LBLOCK, n, s, L, items, width, leaf_nnz,
-                         slot_cnt);
+        else  // the 32 KB bitmap leaves four work groups per CU: 8 waves each
+            launch_items(k_leaf_rank_sym<RANK_L2BLOCK, W18, RANK_L2EPT, 1>, RANK_L2BLOCK, n, s, L, items, width,
+                         leaf_nnz, slot_cnt);
         break;
     }
     default: break;
@@ -1780,10 +1784,10 @@ void leaf_numeric_typed(const LeafSet &L, int bin, const LeafTask *items, int64_
             launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_MID, RANK_EPT, 1, CI, V>, RANK_BLOCK, n, s, L, items,
                          width, o);
         else if (bin != LEAF_RANK_XL && narrow)  // at most RANK_SMALL distinct columns
-            launch_items(k_leaf_rank_num<RANK_LBLOCK, W17, RANK_SMALL, RANK_LWEPT, 1, CI, V>, RANK_LBLOCK, n, s, L,
+            launch_items(k_leaf_rank_num<RANK_L2BLOCK, W17, RANK_SMALL, RANK_L2EPT, 1, CI, V>, RANK_L2BLOCK, n, s, L,
                          items, width, o);
         else if (bin != LEAF_RANK_XL)
-            launch_items(k_leaf_rank_num<RANK_LBLOCK, W18, RANK_SMALL, RANK_LWEPT, 1, CI, V>, RANK_LBLOCK, n, s, L,
+            launch_items(k_leaf_rank_num<RANK_L2BLOCK, W18, RANK_SMALL, RANK_L2EPT, 1, CI, V>, RANK_L2BLOCK, n, s, L,
                          items, width, o);
         else if (narrow)
             launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_NNZ_MAX, RANK_EPT, 1, CI, V>, RANK_BLOCK, n, s, L, items,
