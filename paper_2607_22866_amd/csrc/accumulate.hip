@@ -1180,10 +1180,11 @@ constexpr int RANK_WBLOCK = 256, RANK_WEPT = 4;  // the small wide shape
 constexpr int RANK_L2BLOCK = 512, RANK_L2EPT = 14;  // the same in 8 waves: twice the waves per CU when the
                                                    // LDS caps the work groups (R-MAT 23's 2^18 columns:
                                                    // 193 -> 150 ms per step for these kernels)
+constexpr int RANK_X2BLOCK = 1024, RANK_X2EPT = 8;  // 16 waves for the shapes whose LDS allows two groups per CU
 constexpr int RANK_LBLOCK = 256, RANK_LWEPT = 27;  // wide symbolic at 2^17 columns: 4 waves and 16 KB of
                                                    // LDS, so eight work groups share a CU
 static_assert(RANK_LBLOCK * RANK_LWEPT >= SORT_CAP[2] && RANK_BLOCK * RANK_EPT >= SORT_CAP[2] &&
-                  RANK_L2BLOCK * RANK_L2EPT >= SORT_CAP[2],
+                  RANK_L2BLOCK * RANK_L2EPT >= SORT_CAP[2] && RANK_X2BLOCK * RANK_X2EPT >= SORT_CAP[2],
               "the wide shapes hold a light chunk of up to the largest tau");
 static_assert(RANK_WBLOCK * RANK_WEPT >= RANK_WIDE_SMALL, "the small wide shape holds its chunks");
 constexpr int RANK_SBLOCK = 256, RANK_SWORDS = 256, RANK_SCAP = 512, RANK_SEPT = 2, RANK_LEPT = 8;
@@ -1713,9 +1714,9 @@ void leaf_symbolic(const LeafSet &L, int bin, const LeafTask *items, int64_t n, 
         else if (width <= (1 << 17) && bin == LEAF_RANK)
             launch_items(k_leaf_rank_sym<RANK_WBLOCK, W17, RANK_WEPT>, RANK_WBLOCK, n, s, L, items, width, leaf_nnz,
                          slot_cnt);
-        else if (bin == LEAF_RANK)
-            launch_items(k_leaf_rank_sym<RANK_WBLOCK, W18, RANK_WEPT, 1>, RANK_WBLOCK, n, s, L, items, width, leaf_nnz,
-                         slot_cnt);
+        else if (bin == LEAF_RANK)  // 32 KB bitmap: four groups per CU, 8 waves each
+            launch_items(k_leaf_rank_sym<2 * RANK_WBLOCK, W18, RANK_WEPT / 2, 1>, 2 * RANK_WBLOCK, n, s, L, items, width,
+                         leaf_nnz, slot_cnt);
         else if (width <= (1 << 17))  // 4 waves per work group: 8 of them (chunks) per CU
             launch_items(k_leaf_rank_sym<RANK_LBLOCK, W17, RANK_LWEPT>, RANK_LBLOCK, n, s, L, items, width, leaf_nnz,
                          slot_cnt);
@@ -1780,21 +1781,21 @@ void leaf_numeric_typed(const LeafSet &L, int bin, const LeafTask *items, int64_
         else if (bin == LEAF_RANK && narrow)  // wide, at most RANK_MID distinct columns
             launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_MID, RANK_EPT, 1, CI, V>, RANK_BLOCK, n, s, L, items,
                          width, o);
-        else if (bin == LEAF_RANK)
-            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_MID, RANK_EPT, 1, CI, V>, RANK_BLOCK, n, s, L, items,
-                         width, o);
+        else if (bin == LEAF_RANK)  // 64 KB of LDS: two groups per CU, so 16 waves each
+            launch_items(k_leaf_rank_num<RANK_X2BLOCK, W18, RANK_MID, RANK_X2EPT, 1, CI, V>, RANK_X2BLOCK, n, s, L,
+                         items, width, o);
         else if (bin != LEAF_RANK_XL && narrow)  // at most RANK_SMALL distinct columns
             launch_items(k_leaf_rank_num<RANK_L2BLOCK, W17, RANK_SMALL, RANK_L2EPT, 1, CI, V>, RANK_L2BLOCK, n, s, L,
                          items, width, o);
         else if (bin != LEAF_RANK_XL)
             launch_items(k_leaf_rank_num<RANK_L2BLOCK, W18, RANK_SMALL, RANK_L2EPT, 1, CI, V>, RANK_L2BLOCK, n, s, L,
                          items, width, o);
-        else if (narrow)
+        else if (narrow)  // (16 waves were no faster here)
             launch_items(k_leaf_rank_num<RANK_BLOCK, W17, RANK_NNZ_MAX, RANK_EPT, 1, CI, V>, RANK_BLOCK, n, s, L, items,
                          width, o);
-        else
-            launch_items(k_leaf_rank_num<RANK_BLOCK, W18, RANK_NNZ_MAX, RANK_EPT, 2, CI, V>, RANK_BLOCK, n, s, L, items,
-                         width, o);
+        else  // 73 KB of LDS: two groups per CU, 16 waves each
+            launch_items(k_leaf_rank_num<RANK_X2BLOCK, W18, RANK_NNZ_MAX, RANK_X2EPT, 2, CI, V>, RANK_X2BLOCK, n, s, L,
+                         items, width, o);
         break;
     }
     default: break;
